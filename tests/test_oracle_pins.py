@@ -1,0 +1,358 @@
+"""Pins of the fp64 oracle against facts fixed outside the oracle's own code.
+
+Each test checks the oracle against brute force, a closed form, an invariant, or a
+library routine that the operator reduces to in a special case (CPU only):
+  - landmarks: exact mean of exactly representable keys; the mean-of-logits identity
+    q . Kbar_c = mean_s q . k_s (App. A, mean-pooled relevance);
+  - selection: brute force over all chunk subsets; ties to the lower chunk index;
+    invariance of the selected set to positive query scaling;
+  - weights: sum to 1, equal 1 for k = 1, padded slots;
+  - forward: S=1, h=1, k>=L reduces to causal attention without the diagonal (torch
+    SDPA); S=1 with small k to top-k token attention (torch.topk); k=1 to attention over
+    the single best chunk (torch SDPA); all-past selection to a dense two-level softmax;
+    per-chunk key shifts leave the output unchanged when the weights are held fixed;
+  - backward: central finite differences of sum(dO*O) (selection fixed, weights moving
+    with the scores) and torch float64 autograd of a gather+softmax formulation;
+  - decode: equals the forward's row at the same position.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import hsa_synth
+import oracle
+
+pytestmark = pytest.mark.filterwarnings("ignore::UserWarning")
+
+
+def rnd(seed, *shape, std=1.0):
+    return hsa_synth.philox(seed, 99, *shape).standard_normal(shape) * std
+
+
+def small_problem(seed, L=24, h=2, d=4, S=3, k=3, mu=1.0, G=1, B=1):
+    Q = rnd(seed, B, L, G * h, d)
+    K = rnd(seed + 1, B, L, G, d)
+    C_all = -(-L // S)
+    K += np.repeat(rnd(seed + 2, B, C_all, G, d, std=mu), S, axis=1)[:, :L]
+    V = rnd(seed + 3, B, L, G, d)
+    dO = rnd(seed + 4, B, L, G * h, d)
+    return Q, K, V, dO
+
+
+# ------------------------------------------------------------------ landmarks ----
+
+def test_landmarks_exact_mean_of_representable_keys():
+    g = hsa_synth.philox(11, 1)
+    K = g.integers(-64, 64, size=(2, 256, 3, 8)).astype(np.float64) / 16.0
+    Kb = oracle.landmarks(K, 64)
+    ref = K.reshape(2, 4, 64, 3, 8).mean(axis=2)
+    assert np.array_equal(Kb, ref)
+
+
+def test_landmarks_ragged_tail_ignored():
+    K = rnd(3, 1, 70, 1, 5)
+    Kb = oracle.landmarks(K, 16)
+    assert Kb.shape == (1, 4, 1, 5)
+    np.testing.assert_allclose(Kb[0, 3, 0], K[0, 48:64, 0].mean(0), rtol=0, atol=1e-14)
+
+
+def test_mean_of_logits_identity():
+    """App. A: q . Kbar_c equals the mean over the chunk of the token logits q . k_s."""
+    K = rnd(5, 1, 128, 1, 16)
+    q = rnd(6, 16)
+    Kb = oracle.landmarks(K, 32)[0, :, 0]
+    logits = K[0, :, 0] @ q
+    np.testing.assert_allclose(Kb @ q, logits.reshape(4, 32).mean(1), rtol=1e-13, atol=1e-13)
+
+
+# ------------------------------------------------------------------ selection ----
+
+def brute_force_select(scores, ncand, k):
+    """All subsets of size min(k, ncand): maximal score sum, ties -> lexicographically
+    smallest ascending index tuple; returned in descending chunk order."""
+    n = min(k, ncand)
+    if n == 0:
+        return []
+    best, best_sum = None, -np.inf
+    for sub in itertools.combinations(range(ncand), n):
+        ssum = float(sum(scores[c] for c in sub))
+        if ssum > best_sum + 1e-12:
+            best, best_sum = sub, ssum
+    return sorted(best, reverse=True)
+
+
+@pytest.mark.parametrize("seed,k", [(21, 1), (22, 3), (23, 5)])
+def test_select_brute_force(seed, k):
+    L, h, d, S = 40, 3, 5, 4
+    Q, K, _, _ = small_problem(seed, L=L, h=h, d=d, S=S, k=k)
+    Kb = oracle.landmarks(K, S)
+    idx, w, gap, ss = oracle.select(Q, Kb, 1, S, k)
+    alpha = 1.0 / math.sqrt(h * d)
+    for t in range(L):
+        ncand = t // S
+        scores = alpha * (Q[0, t].sum(0) @ Kb[0, :, 0].T)
+        want = brute_force_select(scores, ncand, k)
+        got = [int(c) for c in idx[0, t, 0] if c >= 0]
+        assert got == want, (t, got, want)
+        assert all(c == -1 for c in idx[0, t, 0, len(want):])
+        if want:
+            ref_w = torch.softmax(torch.tensor(scores[want]), 0).numpy()
+            np.testing.assert_allclose(w[0, t, 0, :len(want)], ref_w, rtol=1e-12, atol=1e-14)
+        assert np.all(w[0, t, 0, len(want):] == 0)
+
+
+def test_select_ties_go_to_lower_index():
+    # d = 1, h = 1, q = 1: scores are alpha * Kbar, with exact ties at the top-2 boundary
+    S = 1
+    vals = np.array([3., 5., 5., 2., 5., 1.])
+    K = vals.reshape(1, 6, 1, 1)
+    L = 7
+    Kfull = np.zeros((1, L, 1, 1))
+    Kfull[0, :6] = K[0]
+    Q = np.ones((1, L, 1, 1))
+    idx, w, gap, _ = oracle.select(Q, oracle.landmarks(Kfull, S), 1, S, 2)
+    # token 6 sees chunks 0..5; the top-2 among {1, 2, 4} (all 5.0) are 1 and 2
+    assert list(idx[0, 6, 0]) == [2, 1]
+    assert gap[0, 6, 0] == 0.0
+    np.testing.assert_allclose(w[0, 6, 0], [0.5, 0.5])
+
+
+def test_select_positive_query_scaling_keeps_indices():
+    Q, K, _, _ = small_problem(31, L=48, h=2, d=6, S=4, k=3)
+    Kb = oracle.landmarks(K, 4)
+    i1, w1, _, _ = oracle.select(Q, Kb, 1, 4, 3)
+    i2, w2, _, _ = oracle.select(Q * 3.7, Kb, 1, 4, 3)
+    assert np.array_equal(i1, i2)
+    assert not np.allclose(w1[0, 40:], w2[0, 40:])
+
+
+def test_select_k_at_least_all_candidates_is_noop():
+    Q, K, _, _ = small_problem(33, L=32, h=2, d=4, S=4, k=8)
+    Kb = oracle.landmarks(K, 4)
+    idx, w, gap, _ = oracle.select(Q, Kb, 1, 4, 8)
+    for t in range(32):
+        n = t // 4
+        assert list(idx[0, t, 0, :n]) == list(range(n - 1, -1, -1))
+        assert np.isinf(gap[0, t, 0])
+
+
+def test_weights_sum_to_one_and_k1():
+    Q, K, _, _ = small_problem(35, L=64, h=2, d=4, S=4, k=4)
+    Kb = oracle.landmarks(K, 4)
+    _, w, _, _ = oracle.select(Q, Kb, 1, 4, 4)
+    s = w[0, 4:, 0].sum(-1)
+    np.testing.assert_allclose(s, 1.0, rtol=0, atol=1e-14)
+    assert np.all(w[0, :4] == 0)
+    _, w1, _, _ = oracle.select(Q, Kb, 1, 4, 1)
+    assert np.all(w1[0, 4:, 0, 0] == 1.0)
+
+
+# ------------------------------------------------------------------- forward ----
+
+def sdpa(q, k, v, scale, mask=None):
+    return torch.nn.functional.scaled_dot_product_attention(
+        torch.tensor(q), torch.tensor(k), torch.tensor(v), attn_mask=mask, scale=scale).numpy()
+
+
+def test_S1_full_k_is_causal_attention_without_diagonal():
+    L, d = 33, 8
+    Q = rnd(41, 1, L, 1, d)
+    K = rnd(42, 1, L, 1, d)
+    V = rnd(43, 1, L, 1, d)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, 1), 1, 1, L)
+    O = oracle.forward(Q, K, V, idx, w, 1)
+    mask = torch.tril(torch.ones(L, L, dtype=torch.bool), diagonal=-1)
+    ref = sdpa(Q[0, 1:, 0], K[0, :, 0], V[0, :, 0], 1.0 / math.sqrt(d), mask[1:])
+    np.testing.assert_allclose(O[0, 1:, 0], ref, rtol=1e-11, atol=1e-12)
+    assert np.all(O[0, 0] == 0)
+
+
+def test_S1_small_k_is_topk_token_attention():
+    L, d, k = 40, 6, 5
+    Q = rnd(45, 1, L, 1, d)
+    K = rnd(46, 1, L, 1, d)
+    V = rnd(47, 1, L, 1, d)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, 1), 1, 1, k)
+    O = oracle.forward(Q, K, V, idx, w, 1)
+    q, kk, v = (torch.tensor(x[0, :, 0]) for x in (Q, K, V))
+    logits = (q @ kk.T) / math.sqrt(d)
+    for t in range(1, L):
+        n = min(k, t)
+        top = torch.topk(logits[t, :t], n)
+        ref = torch.softmax(top.values, 0) @ v[top.indices]
+        np.testing.assert_allclose(O[0, t, 0], ref.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_k1_is_attention_over_the_best_chunk():
+    L, h, d, S = 64, 3, 8, 8
+    Q, K, V, _ = small_problem(51, L=L, h=h, d=d, S=S, k=1)
+    Kb = oracle.landmarks(K, S)
+    idx, w, _, _ = oracle.select(Q, Kb, 1, S, 1)
+    O = oracle.forward(Q, K, V, idx, w, S)
+    for t in range(S, L):
+        scores = Q[0, t].sum(0) @ Kb[0, :t // S, 0].T
+        c = int(np.argmax(scores))
+        assert idx[0, t, 0, 0] == c
+        ref = sdpa(Q[0, t], K[0, c * S:(c + 1) * S, 0], V[0, c * S:(c + 1) * S, 0],
+                   1.0 / math.sqrt(d))
+        np.testing.assert_allclose(O[0, t], ref, rtol=1e-11, atol=1e-12)
+
+
+def test_all_past_selection_is_dense_two_level_softmax():
+    L, h, d, S = 48, 2, 5, 6
+    C = L // S
+    Q, K, V, _ = small_problem(55, L=L, h=h, d=d, S=S, k=C)
+    Kb = oracle.landmarks(K, S)
+    idx, w, _, _ = oracle.select(Q, Kb, 1, S, C)
+    O = oracle.forward(Q, K, V, idx, w, S)
+    Kt = torch.tensor(K[0, :, 0]).reshape(C, S, d)
+    Vt = torch.tensor(V[0, :, 0]).reshape(C, S, d)
+    alpha = 1.0 / math.sqrt(h * d)
+    for t in range(L):
+        n = t // S
+        if n == 0:
+            assert np.all(O[0, t] == 0)
+            continue
+        q = torch.tensor(Q[0, t])
+        wts = torch.softmax(alpha * (Kt[:n].mean(1) @ q.sum(0)), 0)
+        per_chunk = torch.nn.functional.scaled_dot_product_attention(
+            q[None].expand(n, h, d), Kt[:n], Vt[:n], scale=1.0 / math.sqrt(d))
+        ref = (wts[:, None, None] * per_chunk).sum(0)
+        np.testing.assert_allclose(O[0, t], ref.numpy(), rtol=1e-11, atol=1e-12)
+
+
+def test_per_chunk_key_shift_leaves_output_unchanged():
+    L, h, d, S = 64, 2, 6, 8
+    Q, K, V, _ = small_problem(57, L=L, h=h, d=d, S=S, k=3)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), 1, S, 3)
+    O1 = oracle.forward(Q, K, V, idx, w, S)
+    K2 = K.copy()
+    K2[0, 2 * S:3 * S, 0] += rnd(58, d)
+    O2 = oracle.forward(Q, K2, V, idx, w, S)
+    np.testing.assert_allclose(O1, O2, rtol=1e-12, atol=1e-13)
+
+
+# ------------------------------------------------------------------ backward ----
+
+def _loss(Q, K, V, dO, S, k, idx_ref):
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), K.shape[2], S, k)
+    assert np.array_equal(idx, idx_ref), "selection moved under the perturbation"
+    return float((oracle.forward(Q, K, V, idx, w, S) * dO).sum())
+
+
+@pytest.mark.parametrize("G", [1, 2])
+def test_backward_finite_differences(G):
+    L, h, d, S, k = 12, 2, 3, 2, 2
+    Q, K, V, dO = small_problem(61 + G, L=L, h=h, d=d, S=S, k=k, mu=2.0, G=G)
+    idx, w, gap, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k)
+    assert gap[np.isfinite(gap)].min() > 1e-4
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S)
+    eps = 1e-6
+    for name, X, grad in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
+        num = np.zeros_like(X)
+        it = np.nditer(X, flags=["multi_index"])
+        for _ in it:
+            i = it.multi_index
+            Xp, Xm = X.copy(), X.copy()
+            Xp[i] += eps
+            Xm[i] -= eps
+            args = {"Q": Q, "K": K, "V": V}
+            args[name] = Xp
+            fp = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx)
+            args[name] = Xm
+            fm = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx)
+            num[i] = (fp - fm) / (2 * eps)
+        np.testing.assert_allclose(grad, num, rtol=1e-5, atol=1e-7, err_msg=name)
+
+
+def torch_hsa_forward(Q, K, V, idx, S, alpha, beta):
+    """Gather + softmax formulation (fixed idx; weights from the scores) in autograd."""
+    B, L, H, d = Q.shape
+    G = K.shape[2]
+    h = H // G
+    k = idx.shape[-1]
+    C = L // S
+    O = torch.zeros_like(Q)
+    Kc = K[:, :C * S].reshape(B, C, S, G, d)
+    Vc = V[:, :C * S].reshape(B, C, S, G, d)
+    Kbar = Kc.mean(2)                                            # [B, C, G, d]
+    for b in range(B):
+        for g in range(G):
+            for t in range(L):
+                sel = [int(c) for c in idx[b, t, g] if c >= 0]
+                if not sel:
+                    continue
+                q = Q[b, t, g * h:(g + 1) * h]                   # [h, d]
+                s = alpha * (Kbar[b, sel, g] @ q.sum(0))         # [n]
+                wts = torch.softmax(s, 0)
+                kk = Kc[b, sel, :, g]                             # [n, S, d]
+                vv = Vc[b, sel, :, g]
+                p = torch.softmax(beta * torch.einsum("jd,nsd->njs", q, kk), -1)
+                o = torch.einsum("njs,nsd->njd", p, vv)
+                O[b, t, g * h:(g + 1) * h] = (wts[:, None, None] * o).sum(0)
+    return O
+
+
+def test_backward_matches_torch_autograd():
+    L, h, d, S, k, G = 40, 2, 4, 4, 3, 2
+    Q, K, V, dO = small_problem(71, L=L, h=h, d=d, S=S, k=k, G=G)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S)
+    Qt, Kt, Vt = (torch.tensor(x, requires_grad=True) for x in (Q, K, V))
+    O = torch_hsa_forward(Qt, Kt, Vt, idx, S, 1 / math.sqrt(h * d), 1 / math.sqrt(d))
+    np.testing.assert_allclose(O.detach().numpy(), oracle.forward(Q, K, V, idx, w, S),
+                               rtol=1e-12, atol=1e-13)
+    (O * torch.tensor(dO)).sum().backward()
+    np.testing.assert_allclose(dQ, Qt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dK, Kt.grad.numpy(), rtol=1e-10, atol=1e-12)
+    np.testing.assert_allclose(dV, Vt.grad.numpy(), rtol=1e-10, atol=1e-12)
+
+
+def test_backward_row_and_chunk_subsets_match_full():
+    L, h, d, S, k = 48, 2, 4, 4, 3
+    Q, K, V, dO = small_problem(73, L=L, h=h, d=d, S=S, k=k)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), 1, S, k)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S)
+    dm = oracle.dims(L, h, d, S, k)
+    Qs, dOs = Q[0, :, :h], dO[0, :, :h]
+    Kb = oracle.landmarks_slice(dm, K[0, :, 0])
+    rows = np.array([47, 5, 30])
+    dq, ds_rows = oracle.backward_q_slice(dm, Qs, K[0, :, 0], V[0, :, 0], Kb, idx[0, :, 0],
+                                          w[0, :, 0], dOs, rows=rows)
+    np.testing.assert_allclose(dq, dQ[0, rows], rtol=0, atol=1e-15)
+    _, ds = oracle.backward_q_slice(dm, Qs, K[0, :, 0], V[0, :, 0], Kb, idx[0, :, 0],
+                                    w[0, :, 0], dOs)
+    ch = np.array([7, 0, 3])
+    dk, dv = oracle.backward_kv_slice(dm, Qs, K[0, :, 0], V[0, :, 0], idx[0, :, 0],
+                                      w[0, :, 0], dOs, ds, chunks=ch)
+    for i, c in enumerate(ch):
+        np.testing.assert_allclose(dk[i], dK[0, c * S:(c + 1) * S, 0], rtol=0, atol=1e-15)
+        np.testing.assert_allclose(dv[i], dV[0, c * S:(c + 1) * S, 0], rtol=0, atol=1e-15)
+
+
+# -------------------------------------------------------------------- decode ----
+
+@pytest.mark.parametrize("t", [64, 67, 100, 31])
+def test_decode_equals_forward_row(t):
+    L, h, d, S, k, G = 128, 2, 8, 8, 3, 2
+    Q, K, V, _ = small_problem(81, L=L, h=h, d=d, S=S, k=k, G=G)
+    Kb = oracle.landmarks(K, S)
+    idx, w, _, _ = oracle.select(Q, Kb, G, S, k)
+    O = oracle.forward(Q, K, V, idx, w, S)
+    o, di, dw, _ = oracle.decode(Q[:, t], K, V, Kb, [t], S, k)
+    assert np.array_equal(di[0], idx[0, t])
+    np.testing.assert_allclose(dw[0], w[0, t], rtol=1e-13, atol=1e-15)
+    np.testing.assert_allclose(o[0], O[0, t], rtol=1e-12, atol=1e-14)
+
+
+def test_decode_planted_chunk_is_selected():
+    shape = hsa_synth.HsaShape(2, 8192, 16, 2, 128, 64, 8, "bf16")
+    inp = hsa_synth.make_decode_inputs(shape, 4)
+    Kb = oracle.landmarks(inp["Kc"], 64)
+    o, idx, w, gap = oracle.decode(inp["q"], inp["Kc"], inp["Vc"], Kb, [8192, 8192], 64, 8)
+    for b in range(2):
+        for g in range(2):
+            assert inp["planted"][b, g].item() in set(idx[b, g].tolist())
