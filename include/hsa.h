@@ -1,0 +1,154 @@
+/*
+ * Hierarchical Sparse Attention (HSA, arXiv 2504.16795) for AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of libhsa_mi355x.so.  Plain C, no HIP or torch types: device buffers are passed
+ * as pointers and the HIP stream as an opaque handle.
+ *
+ * Notation (Sec. 3.1 "Notations"): B batch, L sequence length, H query heads, G KV heads
+ * (groups), h = H/G query heads per group, d head dimension, S chunk size, k top-k,
+ * C = floor(L/S) complete chunks.  Query head j of group g is head g*h + j.
+ *
+ * Layouts (row-major, contiguous, last index fastest):
+ *     Q, O, dO, dQ        [B, L, H, d]           element type params.dtype
+ *     K, V, dK, dV        [B, L, G, d]           element type params.dtype
+ *     Kbar                [B, C, G, d]           float32 (training), f32 or bf16 (decode cache)
+ *     idx                 [B, L, G, k]  int32    selected chunks, descending chunk order, -1 pad
+ *     w                   [B, L, G, k]  float32  chunk weights, 0 pad
+ *
+ * Semantics fixed by this library (readings of the paper):
+ *   - a token t may select only chunks c < floor(t/S) (chunks strictly before its own);
+ *   - group score s_c = alpha * (sum_j q_j) . Kbar_c  (the group query of dimension h*d
+ *     against the landmark tiled over the h heads), alpha = 1/sqrt(h*d) by default;
+ *   - top-k by score, ties to the lower chunk index, slots ordered by descending chunk
+ *     index (the sort of Sec. 3.1.1), n = min(k, floor(t/S)) valid slots;
+ *   - chunk weights are a softmax over the n selected scores;
+ *   - intra-chunk attention is a standard softmax over the S keys, scale beta = 1/sqrt(d);
+ *   - O_t = sum_i w_i O_{t,i}; O_t = 0 when the token has no candidate chunk;
+ *   - gradients treat the selected index set as constant and flow through the intra-chunk
+ *     attention and through w -> s -> (q, Kbar -> K).
+ *
+ * Ownership and behaviour (all entry points):
+ *   - every pointer is device memory owned by the caller; the library never allocates,
+ *     frees or synchronises, and enqueues its kernels on `stream` (a hipStream_t; NULL is
+ *     the default stream) before returning;
+ *   - inputs are read-only; outputs are fully overwritten (padding included);
+ *   - scratch memory comes from `ws` (size from hsa_attn_workspace_size), which may hold
+ *     anything on entry; calls sharing one workspace must be ordered on one stream;
+ *   - arguments are validated before any launch: on error nothing is enqueued and the
+ *     call returns HSA_ATTN_ERR_INVALID_ARGUMENT / _UNSUPPORTED / _WORKSPACE_TOO_SMALL;
+ *     a failed launch returns HSA_ATTN_ERR_HIP.  hsa_attn_last_error() gives the detail
+ *     (thread-local).
+ *   - Supported by the kernels: 1 <= h <= 16, d in {64, 128}, S in {16, 32, 64, 128},
+ *     1 <= k <= 32, S * d <= 8192 for F32, L >= 0 (L need not be a multiple of S; a
+ *     trailing partial chunk is never a candidate), pointers 16-byte aligned.  Inputs
+ *     must be finite.  idx entries outside [0, floor(t/S)) are treated as empty slots.
+ */
+#ifndef HSA_MI355X_H
+#define HSA_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    HSA_ATTN_OK = 0,
+    HSA_ATTN_ERR_INVALID_ARGUMENT = 1,
+    HSA_ATTN_ERR_UNSUPPORTED = 2,
+    HSA_ATTN_ERR_WORKSPACE_TOO_SMALL = 3,
+    HSA_ATTN_ERR_HIP = 4
+} hsa_attn_status_t;
+
+typedef enum { HSA_DTYPE_F32 = 0, HSA_DTYPE_BF16 = 1 } hsa_dtype_t;
+
+typedef enum {
+    HSA_OP_LANDMARKS = 0,
+    HSA_OP_SELECT = 1,
+    HSA_OP_FORWARD = 2,
+    HSA_OP_BACKWARD = 3,
+    HSA_OP_DECODE = 4
+} hsa_op_t;
+
+typedef struct {
+    int32_t batch;       /* B                                                         */
+    int32_t seqlen;      /* L (for hsa_decode: the cache capacity N_cap)              */
+    int32_t n_qheads;    /* H                                                         */
+    int32_t n_kvheads;   /* G, H % G == 0                                             */
+    int32_t head_dim;    /* d                                                         */
+    int32_t chunk;       /* S                                                         */
+    int32_t topk;        /* k                                                         */
+    hsa_dtype_t dtype;   /* element type of Q, K, V, O, dO, dQ, dK, dV                */
+    float sm_scale;      /* beta; <= 0 selects 1/sqrt(d)                              */
+    float sel_scale;     /* alpha; <= 0 selects 1/sqrt(h*d)                           */
+    uint32_t flags;      /* reserved, must be 0                                       */
+} hsa_attn_params_t;
+
+/* Landmarks (Fig. 1; Sec. 3.1 "Chunk Selection": mean-pooled chunk representation):
+ * Kbar[b, c, g, :] = (1/S) sum_{s<S} K[b, c*S + s, g, :] for chunks c in
+ * [chunk_begin, chunk_end) (0 <= begin <= end <= C), accumulated in fp32 and stored as
+ * kbar_dtype (F32, or BF16 rounded to nearest even for a compact decode cache).  Other
+ * chunks of Kbar are left untouched, so a decode cache can be extended incrementally. */
+hsa_attn_status_t hsa_landmarks(const hsa_attn_params_t* p, const void* K, void* Kbar,
+                                hsa_dtype_t kbar_dtype, int32_t chunk_begin,
+                                int32_t chunk_end, void* stream);
+
+/* Chunk selection + chunk weights (Sec. 3.1 chunk-selection equation; softmax weights of
+ * the paper's ablation without stick-breaking).  Q: [B,L,H,d] params.dtype; Kbar:
+ * [B,C,G,d] float32 (from hsa_landmarks).  Writes idx and w ([B,L,G,k]).  Scores are
+ * accumulated in fp32.  Needs no workspace (ws may be NULL). */
+hsa_attn_status_t hsa_select_topk(const hsa_attn_params_t* p, const void* Q,
+                                  const float* Kbar, int32_t* idx, float* w, void* ws,
+                                  size_t ws_bytes, void* stream);
+
+/* Forward (Sec. 3.1.1 "Hierarchical Attention"; kernel design of Sec. 3.1.2): for every
+ * (b, t, g) and valid slot i, O_{t,j,i} = softmax(beta q_j K_c^T) V_c over the S keys of
+ * chunk c = idx[i]; O_{t,j} = sum_i w_i O_{t,j,i}.  idx, w are inputs (normally from
+ * hsa_select_topk), so one selection may serve several attention layers.  Entries of idx
+ * must be -1 or satisfy 0 <= c < floor(t/S), without repeats. */
+hsa_attn_status_t hsa_forward(const hsa_attn_params_t* p, const void* Q, const void* K,
+                              const void* V, const int32_t* idx, const float* w, void* O,
+                              void* ws, size_t ws_bytes, void* stream);
+
+/* Backward (Sec. 3.1.2, two-phase backward: queries and weights first, then keys and
+ * values): gradients of sum(dO * O) w.r.t. Q, K, V with the selection fixed and
+ * w = softmax of the selected scores s = alpha (sum_j q_j) . Kbar_c.  dQ includes the
+ * score term alpha sum_i ds_i Kbar_{c_i}; dK includes the landmark term dKbar_c / S.
+ * Kbar must be the float32 landmarks of K.  dK, dV are written for all L rows
+ * (zero for chunks no token selected, and for a trailing partial chunk).  Needs
+ * hsa_attn_workspace_size(p, HSA_OP_BACKWARD) bytes of workspace.  The key/value pass
+ * is chunk-major and accumulates without atomics, in a fixed order: results are bitwise
+ * reproducible run to run. */
+hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const void* K,
+                               const void* V, const float* Kbar, const int32_t* idx,
+                               const float* w, const void* dO, void* dQ, void* dK, void* dV,
+                               void* ws, size_t ws_bytes, void* stream);
+
+/* Single-token decode (Sec. 3.2 "Inference": only the landmark cache is scanned, and the
+ * selected chunks' keys and values are read).  p->seqlen is the cache capacity N_cap;
+ * q, o: [B, H, d] params.dtype; Kcache, Vcache: [B, N_cap, G, d] params.dtype;
+ * Kbar_cache: [B, floor(N_cap/S), G, d] of kbar_dtype (F32 or BF16), valid for every
+ * complete cached chunk; cache_len: device int32 [B] with 0 <= cache_len[b] <= N_cap, or
+ * NULL for all N_cap.  The query of sequence b sits at position cache_len[b] and sees the
+ * chunks c < floor(cache_len[b]/S).  Writes o, idx [B,G,k], w [B,G,k].  Needs
+ * hsa_attn_workspace_size(p, HSA_OP_DECODE) bytes of workspace. */
+hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const void* Kcache,
+                             const void* Vcache, const void* Kbar_cache,
+                             hsa_dtype_t kbar_dtype, const int32_t* cache_len, void* o,
+                             int32_t* idx, float* w, void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes needed by `op` (an hsa_op_t) for these params; 0 if none.  Returns 0
+ * for invalid params as well (the entry point then reports the error). */
+size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op);
+
+/* Static description of a status code. */
+const char* hsa_attn_status_string(hsa_attn_status_t s);
+
+/* Detail of the last error on the calling thread ("" if none). */
+const char* hsa_attn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HSA_MI355X_H */

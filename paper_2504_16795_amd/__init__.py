@@ -1,0 +1,14 @@
+"""Hierarchical Sparse Attention (arXiv 2504.16795) for AMD Instinct MI355X (gfx950).
+
+The operator lives in the HIP library libhsa_mi355x.so (C ABI in include/hsa.h); this
+package is its thin Python binding.  Importing the package does not load the library;
+`load()` (or the first call) does, and raises if it has not been built.
+"""
+from .binding import (HsaError, HsaParams, hsa_backward, hsa_decode, hsa_forward,
+                      hsa_landmarks, hsa_select_topk, load, make_params, workspace_size,
+                      HSA_DTYPE_BF16, HSA_DTYPE_F32, HSA_OP_BACKWARD, HSA_OP_DECODE,
+                      HSA_OP_FORWARD, HSA_OP_LANDMARKS, HSA_OP_SELECT, EXPORTED, LIB_PATH)
+
+__all__ = ["HsaError", "HsaParams", "hsa_backward", "hsa_decode", "hsa_forward",
+           "hsa_landmarks", "hsa_select_topk", "load", "make_params", "workspace_size",
+           "EXPORTED", "LIB_PATH"]

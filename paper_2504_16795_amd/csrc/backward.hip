@@ -1,0 +1,390 @@
+// Backward of hierarchical sparse attention (Sec. 3.1.2, two-phase backward).
+//
+// Phase 1 (query-major, one workgroup per (b, t, g)): recompute P and O for every slot,
+// D_j = dO_j . O_{j,i}, dw_i = sum_j D_j, dz = w_i P (dP - D_j), dq_j += beta dz K; then
+// the softmax-weight Jacobian ds_i = w_i (dw_i - sum_m w_m dw_m) and the score term
+// dq_j += alpha sum_i ds_i Kbar_{c_i}.  ds is kept in the workspace for phase 2.
+//
+// Selection matrix: the paper's M[t, c] ("token t selected chunk c") is built as a bitmap
+// per (b, g, chunk) over tokens with bitwise-OR atomics (order-independent, exact).
+//
+// Phase 2 (chunk-major, one workgroup per (b, g, chunk)): walks the chunk's bitmap row in
+// increasing token order, recomputes P, dP, D for the selecting tokens and accumulates
+// dV = sum w P^T dO, dK = beta sum dz^T q and dKbar = alpha sum ds q~ in registers, then
+// writes dK = dK + dKbar / S and dV.  No float atomics: every dK/dV row is owned by one
+// workgroup and summed in a fixed order, so results are bitwise reproducible.
+//
+// The MFMA path for the main bf16 shapes lives in backward_mfma.hip.
+#include "common.h"
+
+namespace hsa {
+
+bool backward_mfma_supported(const Dims& dm, bool in_bf16);
+size_t backward_mfma_workspace(const Dims& dm);
+hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
+                                const float* Kbar, const int32_t* idx, const float* w,
+                                const void* dO, void* dQ, void* dK, void* dV, void* ws,
+                                hipStream_t st);
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int SMAX = 128;
+constexpr int HMAX = 16;
+constexpr int KMAX = 32;
+
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void bwd_q_generic(
+    Dims dm, const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const float* __restrict__ Kbar, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const T* __restrict__ dO, T* __restrict__ dQ, float* __restrict__ ds_out) {
+    constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
+    constexpr int NACC = HMAX * D / kThreads;
+    __shared__ T Ks[SMAX * KP];
+    __shared__ T Vs[SMAX * KP];
+    __shared__ float qf[HMAX * D];
+    __shared__ float gf[HMAX * D];
+    __shared__ float dz[HMAX * SMAX];
+    __shared__ float Dl[HMAX];
+    __shared__ float dwl[KMAX];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const int h = dm.h, S = dm.S, k = dm.k;
+    const int ncand = t / S;
+    const size_t qoff = (((size_t)b * dm.L + t) * dm.H + (size_t)g * h) * D;
+    const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
+
+    for (int i = tid; i < h * D; i += kThreads) {
+        qf[i] = to_f32(Q[qoff + i]);
+        gf[i] = to_f32(dO[qoff + i]);
+    }
+    if (tid < KMAX) dwl[tid] = 0.f;
+    float acc[NACC];
+#pragma unroll
+    for (int r = 0; r < NACC; ++r) acc[r] = 0.f;
+
+    for (int slot = 0; slot < k; ++slot) {
+        const int c = idx[sel + slot];
+        if (c < 0 || c >= ncand) continue;
+        const float wi = w[sel + slot];
+        __syncthreads();
+        for (int i = tid; i < S * D; i += kThreads) {
+            const int s = i / D, e = i % D;
+            const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+            Ks[s * KP + e] = K[gi];
+            Vs[s * KP + e] = V[gi];
+        }
+        __syncthreads();
+        for (int j = wave; j < h; j += kThreads / 64) {
+            float z[2], dp[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int s = lane + 64 * u;
+                float a = 0.f, bb = 0.f;
+                if (s < S) {
+                    for (int e = 0; e < D; ++e) {
+                        a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
+                        bb = fmaf(gf[j * D + e], to_f32(Vs[s * KP + e]), bb);
+                    }
+                    z[u] = dm.beta * a;
+                } else {
+                    z[u] = -INFINITY;
+                }
+                dp[u] = bb;
+            }
+            const float m = wave_max(fmaxf(z[0], z[1]));
+            float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
+            const float inv = 1.f / wave_sum(p0 + p1);
+            p0 *= inv;
+            p1 *= inv;
+            const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
+            if (lane < S) dz[j * SMAX + lane] = wi * p0 * (dp[0] - Dj);
+            if (lane + 64 < S) dz[j * SMAX + lane + 64] = wi * p1 * (dp[1] - Dj);
+            if (lane == 0) Dl[j] = Dj;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            float s = 0.f;
+            for (int j = 0; j < h; ++j) s += Dl[j];
+            dwl[slot] = s;
+        }
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+            const int i = tid + r * kThreads;
+            if (i < h * D) {
+                const int j = i / D, e = i % D;
+                float a = 0.f;
+                for (int s = 0; s < S; ++s) a = fmaf(dz[j * SMAX + s], to_f32(Ks[s * KP + e]), a);
+                acc[r] = fmaf(dm.beta, a, acc[r]);
+            }
+        }
+    }
+    __syncthreads();
+    // softmax-weight Jacobian and the score term
+    float wdw = 0.f;
+    for (int i = 0; i < k; ++i) {
+        const int c = idx[sel + i];
+        if (c >= 0 && c < ncand) wdw += w[sel + i] * dwl[i];
+    }
+    for (int i = 0; i < k; ++i) {
+        const int c = idx[sel + i];
+        const bool ok = (c >= 0 && c < ncand);
+        const float dsi = ok ? w[sel + i] * (dwl[i] - wdw) : 0.f;
+        if (tid == 0) ds_out[sel + i] = dsi;
+        if (!ok) continue;
+        const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+            const int ii = tid + r * kThreads;
+            if (ii < h * D) acc[r] = fmaf(dm.alpha * dsi, kb[ii % D], acc[r]);
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < NACC; ++r) {
+        const int i = tid + r * kThreads;
+        if (i < h * D) dQ[qoff + i] = from_f32<T>(acc[r]);
+    }
+}
+
+__global__ void fill_zero_u32(uint32_t* __restrict__ p, size_t n) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+__global__ void bitmap_build(Dims dm, const int32_t* __restrict__ idx, uint32_t* __restrict__ bm,
+                             int nwords) {
+    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const size_t total = (size_t)dm.B * dm.L * dm.G * dm.k;
+    if (i >= total) return;
+    const int c = idx[i];
+    size_t r = i / dm.k;
+    const int g = (int)(r % dm.G);
+    r /= dm.G;
+    const int t = (int)(r % dm.L);
+    const int b = (int)(r / dm.L);
+    if (c < 0 || c >= t / dm.S) return;     // only valid entries; others are ignored
+    atomicOr(&bm[(((size_t)b * dm.G + g) * dm.C + c) * nwords + (t >> 5)], 1u << (t & 31));
+}
+
+template <typename T, int D, int CS>
+__global__ __launch_bounds__(kThreads) void bwd_kv_generic(
+    Dims dm, const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
+    const int32_t* __restrict__ idx, const float* __restrict__ w, const T* __restrict__ dO,
+    const float* __restrict__ ds, const uint32_t* __restrict__ bm, int nwords,
+    T* __restrict__ dK, T* __restrict__ dV) {
+    constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
+    constexpr int NE = CS * D / kThreads;
+    __shared__ T Ks[CS * KP];
+    __shared__ T Vs[CS * KP];
+    __shared__ float qf[HMAX * D];
+    __shared__ float gf[HMAX * D];
+    __shared__ float pw[HMAX * CS];
+    __shared__ float dz[HMAX * CS];
+    __shared__ float dkb[D];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int c = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const int h = dm.h, k = dm.k;
+    const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;   // row cS
+
+    if (c >= dm.C) {   // trailing partial chunk: never selected, zero gradient
+        const int rows = dm.L - c * CS;
+        for (int i = tid; i < rows * D; i += kThreads) {
+            const size_t gi = (rowbase + (size_t)(i / D) * dm.G) * D + i % D;
+            dK[gi] = from_f32<T>(0.f);
+            dV[gi] = from_f32<T>(0.f);
+        }
+        return;
+    }
+    for (int i = tid; i < CS * D; i += kThreads) {
+        const int s = i / D, e = i % D;
+        const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
+        Ks[s * KP + e] = K[gi];
+        Vs[s * KP + e] = V[gi];
+    }
+    float aK[NE], aV[NE];
+#pragma unroll
+    for (int r = 0; r < NE; ++r) aK[r] = aV[r] = 0.f;
+    float dkbar = 0.f;   // thread tid < D owns element tid of dKbar
+
+    const uint32_t* row = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
+    for (int wi = ((c + 1) * CS) >> 5; wi < nwords; ++wi) {
+        uint32_t word = row[wi];
+        while (word) {
+            const int t = wi * 32 + (__ffs(word) - 1);
+            word &= word - 1;
+            const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
+            int slot = 0;
+            for (int i = 0; i < k; ++i)
+                if (idx[sel + i] == c) slot = i;
+            const float wt = w[sel + slot];
+            const float dst = ds[sel + slot];
+            const size_t qoff = (((size_t)b * dm.L + t) * dm.H + (size_t)g * h) * D;
+            __syncthreads();
+            for (int i = tid; i < h * D; i += kThreads) {
+                qf[i] = to_f32(Q[qoff + i]);
+                gf[i] = to_f32(dO[qoff + i]);
+            }
+            __syncthreads();
+            for (int j = wave; j < h; j += kThreads / 64) {
+                float z[2], dp[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int s = lane + 64 * u;
+                    float a = 0.f, bb = 0.f;
+                    if (s < CS) {
+                        for (int e = 0; e < D; ++e) {
+                            a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
+                            bb = fmaf(gf[j * D + e], to_f32(Vs[s * KP + e]), bb);
+                        }
+                        z[u] = dm.beta * a;
+                    } else {
+                        z[u] = -INFINITY;
+                    }
+                    dp[u] = bb;
+                }
+                const float m = wave_max(fmaxf(z[0], z[1]));
+                float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
+                const float inv = 1.f / wave_sum(p0 + p1);
+                p0 *= inv;
+                p1 *= inv;
+                const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
+                if (lane < CS) {
+                    pw[j * CS + lane] = wt * p0;
+                    dz[j * CS + lane] = wt * p0 * (dp[0] - Dj);
+                }
+                if (lane + 64 < CS) {
+                    pw[j * CS + lane + 64] = wt * p1;
+                    dz[j * CS + lane + 64] = wt * p1 * (dp[1] - Dj);
+                }
+            }
+            if (tid < D) {
+                float qs = 0.f;
+                for (int j = 0; j < h; ++j) qs += qf[j * D + tid];
+                dkbar = fmaf(dm.alpha * dst, qs, dkbar);
+            }
+            __syncthreads();
+#pragma unroll
+            for (int r = 0; r < NE; ++r) {
+                const int i = tid + r * kThreads;
+                const int s = i / D, e = i % D;
+                float av = 0.f, ak = 0.f;
+                for (int j = 0; j < h; ++j) {
+                    av = fmaf(pw[j * CS + s], gf[j * D + e], av);
+                    ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
+                }
+                aV[r] += av;
+                aK[r] = fmaf(dm.beta, ak, aK[r]);
+            }
+        }
+    }
+    __syncthreads();
+    if (tid < D) dkb[tid] = dkbar;
+    __syncthreads();
+    const float invS = 1.f / (float)CS;
+#pragma unroll
+    for (int r = 0; r < NE; ++r) {
+        const int i = tid + r * kThreads;
+        const int s = i / D, e = i % D;
+        const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
+        dK[gi] = from_f32<T>(aK[r] + dkb[e] * invS);
+        dV[gi] = from_f32<T>(aV[r]);
+    }
+}
+
+template <typename T, int D, int CS>
+void launch_kv(const Dims& dm, const void* Q, const void* K, const void* V, const int32_t* idx,
+               const float* w, const void* dO, const float* ds, const uint32_t* bm, int nwords,
+               void* dK, void* dV, hipStream_t st) {
+    dim3 grid(dm.Call, dm.B * dm.G);
+    hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), grid, dim3(kThreads), 0, st, dm, (const T*)Q,
+                       (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm, nwords, (T*)dK,
+                       (T*)dV);
+}
+
+template <typename T, int D>
+void launch_kv_s(const Dims& dm, const void* Q, const void* K, const void* V,
+                 const int32_t* idx, const float* w, const void* dO, const float* ds,
+                 const uint32_t* bm, int nwords, void* dK, void* dV, hipStream_t st) {
+    switch (dm.S) {
+        case 16: launch_kv<T, D, 16>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
+        case 32: launch_kv<T, D, 32>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
+        case 64: launch_kv<T, D, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
+        default:
+            // fp32 with S = 128 and d = 128 exceeds the LDS of one workgroup; rejected by the
+            // argument checks, so it is not instantiated.
+            if constexpr (!(sizeof(T) == 4 && D == 128))
+                launch_kv<T, D, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+            break;
+    }
+}
+
+template <typename T>
+hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
+                    const float* Kbar, const int32_t* idx, const float* w, const void* dO,
+                    void* dQ, void* dK, void* dV, void* ws, hipStream_t st) {
+    const int nwords = cdiv(dm.L, 32);
+    float* ds = (float*)ws;
+    uint32_t* bm = (uint32_t*)((char*)ws + align256((size_t)dm.B * dm.L * dm.G * dm.k * 4));
+    const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
+
+    dim3 g1(dm.L, dm.B * dm.G);
+    if (dm.d == 128)
+        hipLaunchKernelGGL((bwd_q_generic<T, 128>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
+                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
+    else
+        hipLaunchKernelGGL((bwd_q_generic<T, 64>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
+                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
+    if (nbm) {
+        hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)cdiv((int)((nbm + 255) / 256), 1)),
+                           dim3(256), 0, st, bm, nbm);
+        const size_t ne = (size_t)dm.B * dm.L * dm.G * dm.k;
+        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st,
+                           dm, idx, bm, nwords);
+    }
+    if (dm.d == 128)
+        launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+    else
+        launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+size_t backward_generic_workspace(const Dims& dm) {
+    const size_t nwords = (size_t)cdiv(dm.L, 32);
+    return align256((size_t)dm.B * dm.L * dm.G * dm.k * 4) +
+           align256((size_t)dm.B * dm.G * dm.C * nwords * 4);
+}
+
+size_t backward_workspace(const Dims& dm) {
+    const size_t a = backward_generic_workspace(dm);
+    const size_t b = backward_mfma_workspace(dm);
+    return a > b ? a : b;
+}
+
+hipError_t launch_backward_generic(const Dims& dm, bool in_bf16, const void* Q, const void* K,
+                                   const void* V, const float* Kbar, const int32_t* idx,
+                                   const float* w, const void* dO, void* dQ, void* dK, void* dV,
+                                   void* ws, hipStream_t st) {
+    if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    return in_bf16 ? launch_t<bf16>(dm, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st)
+                   : launch_t<float>(dm, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);
+}
+
+hipError_t launch_backward(const Dims& dm, bool in_bf16, const void* Q, const void* K,
+                           const void* V, const float* Kbar, const int32_t* idx, const float* w,
+                           const void* dO, void* dQ, void* dK, void* dV, void* ws,
+                           hipStream_t st) {
+    if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    if (backward_mfma_supported(dm, in_bf16))
+        return launch_backward_mfma(dm, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);
+    return launch_backward_generic(dm, in_bf16, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);
+}
+
+}  // namespace hsa

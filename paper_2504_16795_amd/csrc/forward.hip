@@ -1,0 +1,135 @@
+// Forward of hierarchical sparse attention (Sec. 3.1.1 "Hierarchical Attention").
+//
+// Generic path (any supported h, d, S; fp32 or bf16): one workgroup per (b, t, g), as in
+// the paper's per-token program: the group's h query rows live in LDS, each selected chunk
+// is staged in LDS, each wave takes a head, lanes take keys, the softmax over the S keys
+// is a wave reduction, and the weighted chunk output is accumulated in registers.
+// Without an online softmax: every chunk is normalised on its own and scaled by w_i.
+//
+// The bf16 MFMA path for the main shapes lives in forward_mfma.hip and is selected by
+// launch_forward when it applies.
+#include "common.h"
+
+namespace hsa {
+
+bool forward_mfma_supported(const Dims& dm, bool in_bf16);
+hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
+                               const int32_t* idx, const float* w, void* O, void* ws,
+                               hipStream_t st);
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int SMAX = 128;
+constexpr int HMAX = 16;
+
+template <typename T, int D>
+__global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __restrict__ Q,
+                                                            const T* __restrict__ K,
+                                                            const T* __restrict__ V,
+                                                            const int32_t* __restrict__ idx,
+                                                            const float* __restrict__ w,
+                                                            T* __restrict__ O) {
+    constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
+    constexpr int NACC = HMAX * D / kThreads;
+    __shared__ T Ks[SMAX * KP];
+    __shared__ T Vs[SMAX * D];
+    __shared__ float qf[HMAX * D];
+    __shared__ float p[HMAX * SMAX];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int t = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const int h = dm.h, S = dm.S, k = dm.k;
+    const size_t qoff = (((size_t)b * dm.L + t) * dm.H + (size_t)g * h) * D;
+
+    for (int i = tid; i < h * D; i += kThreads) qf[i] = to_f32(Q[qoff + i]);
+    float acc[NACC];
+#pragma unroll
+    for (int r = 0; r < NACC; ++r) acc[r] = 0.f;
+
+    const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
+    for (int slot = 0; slot < k; ++slot) {
+        const int c = idx[sel + slot];
+        if (c < 0 || c >= t / S) continue;   // empty (or out-of-range) slot
+        const float wi = w[sel + slot];
+        __syncthreads();
+        for (int i = tid; i < S * D; i += kThreads) {
+            const int s = i / D, e = i % D;
+            const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+            Ks[s * KP + e] = K[gi];
+            Vs[s * D + e] = V[gi];
+        }
+        __syncthreads();
+        for (int j = wave; j < h; j += kThreads / 64) {
+            float z[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int s = lane + 64 * u;
+                float a = 0.f;
+                if (s < S) {
+                    for (int e = 0; e < D; ++e) a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
+                    z[u] = dm.beta * a;
+                } else {
+                    z[u] = -INFINITY;
+                }
+            }
+            const float m = wave_max(fmaxf(z[0], z[1]));
+            const float e0 = expf(z[0] - m), e1 = expf(z[1] - m);
+            const float scale = wi / wave_sum(e0 + e1);
+            if (lane < S) p[j * SMAX + lane] = e0 * scale;
+            if (lane + 64 < S) p[j * SMAX + lane + 64] = e1 * scale;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+            const int i = tid + r * kThreads;
+            if (i < h * D) {
+                const int j = i / D, e = i % D;
+                float a = 0.f;
+                for (int s = 0; s < S; ++s) a = fmaf(p[j * SMAX + s], to_f32(Vs[s * D + e]), a);
+                acc[r] += a;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < NACC; ++r) {
+        const int i = tid + r * kThreads;
+        if (i < h * D) O[qoff + i] = from_f32<T>(acc[r]);
+    }
+}
+
+template <typename T>
+hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
+                    const int32_t* idx, const float* w, void* O, hipStream_t st) {
+    dim3 grid(dm.L, dm.B * dm.G);
+    if (dm.d == 128)
+        hipLaunchKernelGGL((forward_generic<T, 128>), grid, dim3(kThreads), 0, st, dm,
+                           (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
+    else
+        hipLaunchKernelGGL((forward_generic<T, 64>), grid, dim3(kThreads), 0, st, dm,
+                           (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_forward(const Dims& dm, bool in_bf16, const void* Q, const void* K,
+                          const void* V, const int32_t* idx, const float* w, void* O, void* ws,
+                          hipStream_t st) {
+    if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    if (forward_mfma_supported(dm, in_bf16))
+        return launch_forward_mfma(dm, Q, K, V, idx, w, O, ws, st);
+    return in_bf16 ? launch_t<bf16>(dm, Q, K, V, idx, w, O, st)
+                   : launch_t<float>(dm, Q, K, V, idx, w, O, st);
+}
+
+hipError_t launch_forward_generic(const Dims& dm, bool in_bf16, const void* Q, const void* K,
+                                  const void* V, const int32_t* idx, const float* w, void* O,
+                                  hipStream_t st) {
+    if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    return in_bf16 ? launch_t<bf16>(dm, Q, K, V, idx, w, O, st)
+                   : launch_t<float>(dm, Q, K, V, idx, w, O, st);
+}
+
+}  // namespace hsa

@@ -1,0 +1,240 @@
+// C ABI of the HSA library (declarations and contract in include/hsa.h): argument
+// validation, default scales, workspace sizes and dispatch to the kernel launchers.
+// Nothing is enqueued unless every check passes.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "common.h"
+#include "hsa.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+hsa_attn_status_t fail(hsa_attn_status_t s, const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+hsa_attn_status_t ok() {
+    g_err[0] = '\0';
+    return HSA_ATTN_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define CHECK_PTR(ptr, name)                                                              \
+    do {                                                                                  \
+        if ((ptr) == nullptr)                                                             \
+            return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "%s is NULL", name);              \
+        if (!aligned16(ptr))                                                              \
+            return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);\
+    } while (0)
+
+// Shape checks shared by every op; fills the kernel-side description.
+hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
+    if (p == nullptr) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "params is NULL");
+    if (p->batch < 0 || p->seqlen < 0)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "batch and seqlen must be >= 0");
+    if (p->n_qheads < 1 || p->n_kvheads < 1 || p->n_qheads % p->n_kvheads != 0)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT,
+                    "n_qheads (%d) must be a positive multiple of n_kvheads (%d)", p->n_qheads,
+                    p->n_kvheads);
+    if (p->dtype != HSA_DTYPE_F32 && p->dtype != HSA_DTYPE_BF16)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown dtype %d", (int)p->dtype);
+    if (p->topk < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "topk must be >= 1");
+    if (p->chunk < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "chunk must be >= 1");
+    if (p->head_dim < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "head_dim must be >= 1");
+    if (p->flags != 0) return fail(HSA_ATTN_ERR_UNSUPPORTED, "flags must be 0");
+    const int h = p->n_qheads / p->n_kvheads;
+    if (h > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "at most 16 query heads per KV head");
+    if (p->head_dim != 64 && p->head_dim != 128)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", p->head_dim);
+    if (p->chunk != 16 && p->chunk != 32 && p->chunk != 64 && p->chunk != 128)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED, "chunk %d not in {16, 32, 64, 128}", p->chunk);
+    if (p->topk > 32) return fail(HSA_ATTN_ERR_UNSUPPORTED, "topk %d > 32", p->topk);
+    if (p->dtype == HSA_DTYPE_F32 && p->chunk * p->head_dim > 8192)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED, "float32 needs chunk * head_dim <= 8192");
+    if ((long long)p->batch * p->n_kvheads > 65535)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED, "batch * n_kvheads > 65535");
+    dm->B = p->batch;
+    dm->L = p->seqlen;
+    dm->H = p->n_qheads;
+    dm->G = p->n_kvheads;
+    dm->h = h;
+    dm->d = p->head_dim;
+    dm->S = p->chunk;
+    dm->k = p->topk;
+    dm->C = p->seqlen / p->chunk;
+    dm->Call = (p->seqlen + p->chunk - 1) / p->chunk;
+    dm->beta = p->sm_scale > 0.f ? p->sm_scale : (float)(1.0 / sqrt((double)p->head_dim));
+    dm->alpha = p->sel_scale > 0.f ? p->sel_scale : (float)(1.0 / sqrt((double)h * p->head_dim));
+    return HSA_ATTN_OK;
+}
+
+hsa_attn_status_t launched(hipError_t e, const char* what) {
+    if (e != hipSuccess)
+        return fail(HSA_ATTN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+size_t op_workspace(const hsa::Dims& dm, int op) {
+    switch (op) {
+        case HSA_OP_BACKWARD: return hsa::backward_workspace(dm);
+        case HSA_OP_DECODE: return hsa::decode_workspace(dm);
+        default: return 0;
+    }
+}
+
+hsa_attn_status_t check_ws(const hsa::Dims& dm, int op, const void* ws, size_t ws_bytes) {
+    const size_t need = op_workspace(dm, op);
+    if (need == 0) return HSA_ATTN_OK;
+    if (ws_bytes < need)
+        return fail(HSA_ATTN_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed",
+                    ws_bytes, need);
+    CHECK_PTR(ws, "ws");
+    return HSA_ATTN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+hsa_attn_status_t hsa_landmarks(const hsa_attn_params_t* p, const void* K, void* Kbar,
+                                hsa_dtype_t kbar_dtype, int32_t chunk_begin, int32_t chunk_end,
+                                void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (kbar_dtype != HSA_DTYPE_F32 && kbar_dtype != HSA_DTYPE_BF16)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown kbar_dtype %d", (int)kbar_dtype);
+    if (chunk_begin < 0 || chunk_end < chunk_begin || chunk_end > dm.C)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "chunk range [%d, %d) outside [0, %d]",
+                    chunk_begin, chunk_end, dm.C);
+    if (dm.B == 0 || chunk_end == chunk_begin) return ok();
+    CHECK_PTR(K, "K");
+    CHECK_PTR(Kbar, "Kbar");
+    return launched(hsa::launch_landmarks(dm, p->dtype == HSA_DTYPE_BF16, K, Kbar,
+                                          kbar_dtype == HSA_DTYPE_BF16, chunk_begin, chunk_end,
+                                          (hipStream_t)stream),
+                    "hsa_landmarks");
+}
+
+hsa_attn_status_t hsa_select_topk(const hsa_attn_params_t* p, const void* Q, const float* Kbar,
+                                  int32_t* idx, float* w, void* ws, size_t ws_bytes,
+                                  void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    (void)ws;
+    (void)ws_bytes;
+    if (dm.B == 0 || dm.L == 0) return ok();
+    CHECK_PTR(Q, "Q");
+    if (dm.C > 0) CHECK_PTR(Kbar, "Kbar");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    return launched(hsa::launch_select(dm, p->dtype == HSA_DTYPE_BF16, Q, Kbar, idx, w,
+                                       (hipStream_t)stream),
+                    "hsa_select_topk");
+}
+
+hsa_attn_status_t hsa_forward(const hsa_attn_params_t* p, const void* Q, const void* K,
+                              const void* V, const int32_t* idx, const float* w, void* O,
+                              void* ws, size_t ws_bytes, void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (dm.B == 0 || dm.L == 0) return ok();
+    s = check_ws(dm, HSA_OP_FORWARD, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(Q, "Q");
+    CHECK_PTR(K, "K");
+    CHECK_PTR(V, "V");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    CHECK_PTR(O, "O");
+    return launched(hsa::launch_forward(dm, p->dtype == HSA_DTYPE_BF16, Q, K, V, idx, w, O, ws,
+                                        (hipStream_t)stream),
+                    "hsa_forward");
+}
+
+hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const void* K,
+                               const void* V, const float* Kbar, const int32_t* idx,
+                               const float* w, const void* dO, void* dQ, void* dK, void* dV,
+                               void* ws, size_t ws_bytes, void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (dm.B == 0 || dm.L == 0) return ok();
+    s = check_ws(dm, HSA_OP_BACKWARD, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(Q, "Q");
+    CHECK_PTR(K, "K");
+    CHECK_PTR(V, "V");
+    if (dm.C > 0) CHECK_PTR(Kbar, "Kbar");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    CHECK_PTR(dO, "dO");
+    CHECK_PTR(dQ, "dQ");
+    CHECK_PTR(dK, "dK");
+    CHECK_PTR(dV, "dV");
+    return launched(hsa::launch_backward(dm, p->dtype == HSA_DTYPE_BF16, Q, K, V, Kbar, idx, w,
+                                         dO, dQ, dK, dV, ws, (hipStream_t)stream),
+                    "hsa_backward");
+}
+
+hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const void* Kcache,
+                             const void* Vcache, const void* Kbar_cache, hsa_dtype_t kbar_dtype,
+                             const int32_t* cache_len, void* o, int32_t* idx, float* w, void* ws,
+                             size_t ws_bytes, void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (kbar_dtype != HSA_DTYPE_F32 && kbar_dtype != HSA_DTYPE_BF16)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown kbar_dtype %d", (int)kbar_dtype);
+    if (dm.G > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "decode supports at most 16 KV heads");
+    if (dm.B == 0) return ok();
+    s = check_ws(dm, HSA_OP_DECODE, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(q, "q");
+    CHECK_PTR(o, "o");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    if (dm.C > 0) {
+        CHECK_PTR(Kcache, "Kcache");
+        CHECK_PTR(Vcache, "Vcache");
+        CHECK_PTR(Kbar_cache, "Kbar_cache");
+    }
+    if (cache_len != nullptr && ((uintptr_t)cache_len & 3u))
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "cache_len is not 4-byte aligned");
+    return launched(hsa::launch_decode(dm, p->dtype == HSA_DTYPE_BF16, q, Kcache, Vcache,
+                                       Kbar_cache, kbar_dtype == HSA_DTYPE_BF16, cache_len, o,
+                                       idx, w, ws, (hipStream_t)stream),
+                    "hsa_decode");
+}
+
+size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op) {
+    hsa::Dims dm;
+    if (make_dims(p, &dm) != HSA_ATTN_OK) return 0;
+    return op_workspace(dm, op);
+}
+
+const char* hsa_attn_status_string(hsa_attn_status_t s) {
+    switch (s) {
+        case HSA_ATTN_OK: return "success";
+        case HSA_ATTN_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case HSA_ATTN_ERR_UNSUPPORTED: return "unsupported configuration";
+        case HSA_ATTN_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+        case HSA_ATTN_ERR_HIP: return "HIP error";
+    }
+    return "unknown status";
+}
+
+const char* hsa_attn_last_error(void) { return g_err; }
+
+}  // extern "C"

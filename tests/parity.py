@@ -1,0 +1,96 @@
+"""Shared helpers of the GPU parity tests: seeded inputs, the oracle reference and the
+tolerances (written here, used by every GPU test).
+
+Tolerances (fixed in advance, independent of the measured error):
+  - fp32 mode: max-abs error <= 1e-4 for outputs and gradients;
+  - bf16 mode: |got - ref| <= 2e-2 * RMS(ref) + 2^-8 * |ref| element-wise: the operator's
+    bound relative to the output RMS plus half an ulp of the bf16 output format at the
+    reference value (the final rounding to bf16, which no implementation avoids);
+  - selected chunk indices: bit-exact for every token whose oracle top-k score gap is
+    >= 1e-3 (gap-enforced inputs make that every token);
+  - chunk weights: max-abs <= 1e-5 (fp32 softmax of fp32 scores whose error is ~1e-7);
+  - landmarks: max-abs <= 1e-6 * max|Kbar| + 1e-7 (fp32 mean of S values).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+import torch
+
+import hsa_synth
+import oracle
+from oracle.gapfix import enforce_gap
+
+MIN_GAP = 1e-3
+F32_ATOL = 1e-4
+BF16_RMS_FRAC = 2e-2
+W_ATOL = 1e-5
+
+
+def torch_dtype(shape):
+    return torch.bfloat16 if shape.dtype == "bf16" else torch.float32
+
+
+def to_dev(x: np.ndarray, shape) -> torch.Tensor:
+    return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(torch_dtype(shape))
+
+
+def make_case(shape, seed, kind="iid", mu_std=0.5, gap=True):
+    inp = hsa_synth.make_training_inputs(shape, seed, kind=kind, mu_std=mu_std)
+    stats = enforce_gap(inp, shape, seed, MIN_GAP) if gap else None
+    return inp, stats
+
+
+def oracle_reference(inp, shape, backward=True):
+    S, k, G = shape.S, shape.k, shape.G
+    ref = {"Kbar": oracle.landmarks(inp["K"], S)}
+    idx, w, gap, _ = oracle.select(inp["Q"], ref["Kbar"], G, S, k)
+    ref.update(idx=idx, w=w, gap=gap)
+    ref["O"] = oracle.forward(inp["Q"], inp["K"], inp["V"], idx, w, S)
+    if backward:
+        ref["dQ"], ref["dK"], ref["dV"] = oracle.backward(inp["Q"], inp["K"], inp["V"], idx, w,
+                                                           inp["dO"], S)
+    return ref
+
+
+BF16_HALF_ULP = 2.0 ** -8
+
+
+def tol(shape, ref: np.ndarray, ulps: float = 1.0):
+    """Element-wise tolerance array (see the module docstring)."""
+    if shape.dtype == "f32":
+        return np.full(ref.shape, F32_ATOL)
+    rms = float(np.sqrt(np.mean(np.square(ref)))) if ref.size else 0.0
+    return BF16_RMS_FRAC * rms + ulps * BF16_HALF_ULP * np.abs(ref)
+
+
+def assert_close(name, shape, got: torch.Tensor, ref: np.ndarray, ulps: float = 1.0):
+    g = got.detach().float().cpu().numpy().astype(np.float64)
+    assert g.shape == ref.shape, (name, g.shape, ref.shape)
+    assert np.all(np.isfinite(g)), name + " has non-finite values"
+    if not ref.size:
+        return 0.0
+    err = np.abs(g - ref)
+    t = tol(shape, ref, ulps)
+    worst = int(np.argmax(err - t))
+    assert np.all(err <= t), "%s: error %.3e > tolerance %.3e at flat index %d (max-abs %.3e)" % (
+        name, err.flat[worst], t.flat[worst], worst, err.max())
+    return float(err.max())
+
+
+def assert_indices(idx_gpu: torch.Tensor, ref_idx: np.ndarray, gap: np.ndarray, S: int):
+    """Bit-exact where the oracle gap is >= MIN_GAP; elsewhere only validity is checked
+    (distinct, descending, in range, the right count)."""
+    got = idx_gpu.cpu().numpy()
+    sure = gap >= MIN_GAP                                    # [B, L, G]
+    bad = np.nonzero((got != ref_idx).any(-1) & sure)
+    assert bad[0].size == 0, "index mismatch at %s" % (list(zip(*bad))[:5],)
+    k = got.shape[-1]
+    for b, t, g in zip(*np.nonzero(~sure)):
+        row = got[b, t, g]
+        valid = row[row >= 0]
+        assert len(valid) == min(k, t // S)
+        assert np.all(row[len(valid):] == -1)
+        assert np.all(np.diff(valid) < 0) and np.all(valid < t // S)
+    return int(sure.sum()), int((~sure).sum())

@@ -1,0 +1,104 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function declared in
+include/hsa.h, and rejects bad arguments before any launch with the documented codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2504_16795_amd as hsa
+from paper_2504_16795_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+OK, INVALID, UNSUPPORTED, WS_SMALL = 0, 1, 2, 3
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "hsa.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(hsa_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return hsa.load()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def P(**kw):
+    base = dict(B=2, L=256, H=16, G=2, d=128, S=64, k=8, dtype=hsa.HSA_DTYPE_BF16)
+    base.update(kw)
+    return hsa.make_params(**base)
+
+
+FAKE = ctypes.c_void_p(0x10000)          # aligned, never dereferenced (rejected earlier)
+
+
+def fwd(lib, p, Q=FAKE, ws=None, nb=0):
+    return lib.hsa_forward(ctypes.byref(p), Q, FAKE, FAKE, FAKE, FAKE, FAKE, ws, nb, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(H=15), INVALID), (dict(G=0), INVALID), (dict(k=0), INVALID), (dict(S=0), INVALID),
+    (dict(d=96), UNSUPPORTED), (dict(S=48), UNSUPPORTED), (dict(k=33), UNSUPPORTED),
+    (dict(H=34, G=2), UNSUPPORTED), (dict(dtype=7), INVALID), (dict(B=-1), INVALID),
+    (dict(dtype=hsa.HSA_DTYPE_F32, S=128, d=128), UNSUPPORTED),
+])
+def test_forward_rejects_bad_shapes(lib, kw, code):
+    assert fwd(lib, P(**kw)) == code
+    assert lib.hsa_attn_last_error().decode() != ""
+
+
+def test_flags_reserved(lib):
+    p = P()
+    p.flags = 1
+    assert fwd(lib, p) == UNSUPPORTED
+
+
+def test_null_and_misaligned_pointers(lib):
+    assert fwd(lib, P(), Q=None) == INVALID
+    assert "Q" in lib.hsa_attn_last_error().decode()
+    assert fwd(lib, P(), Q=ctypes.c_void_p(0x10004)) == INVALID
+    assert "aligned" in lib.hsa_attn_last_error().decode()
+
+
+def test_workspace_checks(lib):
+    p = P()
+    need = lib.hsa_attn_workspace_size(ctypes.byref(p), hsa.HSA_OP_BACKWARD)
+    assert need > 0
+    st = lib.hsa_backward(ctypes.byref(p), *([FAKE] * 10), FAKE, need - 1, None)
+    assert st == WS_SMALL
+    assert lib.hsa_attn_workspace_size(ctypes.byref(P(H=15)), hsa.HSA_OP_BACKWARD) == 0
+    assert lib.hsa_attn_workspace_size(ctypes.byref(p), hsa.HSA_OP_DECODE) > 0
+    assert lib.hsa_attn_workspace_size(ctypes.byref(p), hsa.HSA_OP_SELECT) == 0
+
+
+def test_landmark_range_checks(lib):
+    p = P()
+    assert lib.hsa_landmarks(ctypes.byref(p), FAKE, FAKE, 0, 2, 1, None) == INVALID
+    assert lib.hsa_landmarks(ctypes.byref(p), FAKE, FAKE, 0, 0, 5, None) == INVALID
+    assert lib.hsa_landmarks(ctypes.byref(p), FAKE, FAKE, 3, 0, 4, None) == INVALID
+    # empty range and empty batch are no-ops that launch nothing
+    assert lib.hsa_landmarks(ctypes.byref(p), FAKE, FAKE, 0, 2, 2, None) == OK
+    assert lib.hsa_landmarks(ctypes.byref(P(B=0)), None, None, 0, 0, 4, None) == OK
+
+
+def test_decode_checks(lib):
+    p = P(G=32, H=32)
+    assert lib.hsa_decode(ctypes.byref(p), *([FAKE] * 4), 1, None, FAKE, FAKE, FAKE, FAKE,
+                          1 << 20, None) == UNSUPPORTED
+    p = P()
+    assert lib.hsa_decode(ctypes.byref(p), *([FAKE] * 4), 5, None, FAKE, FAKE, FAKE, FAKE,
+                          1 << 20, None) == INVALID
+
+
+def test_status_strings(lib):
+    for s in range(5):
+        assert lib.hsa_attn_status_string(s)
+    assert lib.hsa_attn_status_string(99) == b"unknown status"

@@ -1,0 +1,217 @@
+"""GPU parity: every entry point of the HIP library against the fp64 oracle.
+
+Sizes are small enough for the oracle to finish in seconds, yet span several query tiles,
+several landmark blocks and ragged tails.  Every case prints its name before the GPU work.
+"""
+import numpy as np
+import pytest
+import torch
+
+import hsa_synth
+import oracle
+from parity import (W_ATOL, assert_close, assert_indices, make_case,
+                    oracle_reference, to_dev, torch_dtype)
+
+pytestmark = pytest.mark.gpu
+
+Shape = hsa_synth.HsaShape
+
+CASES = {
+    # name: (shape, seed, kind)
+    "tiny_f32": (Shape(1, 1024, 4, 1, 64, 64, 4, "f32"), 1, "iid"),
+    "L4K_like_bf16": (Shape(2, 1024, 16, 2, 128, 64, 8, "bf16"), 2, "iid"),
+    "long_like_bf16": (Shape(1, 2048, 16, 2, 128, 64, 8, "bf16"), 3, "long"),
+    "wide_like_bf16": (Shape(1, 1024, 32, 4, 128, 128, 4, "bf16"), 5, "lowrank"),
+    "ragged_f32": (Shape(2, 1000, 8, 2, 64, 32, 5, "f32"), 11, "iid"),
+    "ragged_bf16": (Shape(1, 777, 6, 2, 64, 16, 7, "bf16"), 12, "iid"),
+    "h1_S128_bf16": (Shape(1, 1100, 3, 3, 128, 128, 3, "bf16"), 13, "iid"),
+    "k_exceeds_chunks_f32": (Shape(1, 300, 4, 2, 64, 64, 8, "f32"), 14, "iid"),
+    "no_candidates_bf16": (Shape(2, 50, 8, 1, 128, 64, 4, "bf16"), 15, "iid"),
+}
+
+_cache = {}
+
+
+def case(name):
+    if name not in _cache:
+        shape, seed, kind = CASES[name]
+        inp, stats = make_case(shape, seed, kind=kind, mu_std=0.0 if kind == "lowrank" else 0.5)
+        ref = oracle_reference(inp, shape)
+        dev = {n: to_dev(v, shape) for n, v in inp.items()}
+        _cache[name] = (shape, inp, ref, dev)
+    return _cache[name]
+
+
+def banner(name, what):
+    print("\n[gpu] %s: %s" % (name, what), flush=True)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_landmarks(hsa_gpu, name):
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_landmarks")
+    Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
+    torch.cuda.synchronize()
+    got = Kbar.cpu().numpy().astype(np.float64)
+    want = ref["Kbar"]
+    assert got.shape == want.shape
+    if want.size:
+        err = np.max(np.abs(got - want))
+        assert err <= 1e-6 * np.max(np.abs(want)) + 1e-7, err
+
+
+def test_landmarks_exact_and_bf16_cache(hsa_gpu):
+    banner("exact", "hsa_landmarks on exactly representable keys; bf16 output")
+    g = hsa_synth.philox(7, 1)
+    K = (g.integers(-64, 64, size=(2, 512, 2, 128)) / 16.0).astype(np.float32)
+    Kd = torch.from_numpy(K).cuda().to(torch.bfloat16)
+    want = oracle.landmarks(K, 64)
+    got = hsa_gpu.hsa_landmarks(Kd, 64).cpu().numpy()
+    assert np.array_equal(got.astype(np.float64), want)
+    got16 = hsa_gpu.hsa_landmarks(Kd, 64, kbar_dtype=torch.bfloat16)
+    want16 = hsa_synth.round_bf16(want.astype(np.float32))
+    assert np.array_equal(got16.float().cpu().numpy(), want16)
+    # partial range leaves the other chunks untouched
+    out = torch.full((2, 8, 2, 128), 7.0, device="cuda")
+    hsa_gpu.hsa_landmarks(Kd, 64, chunk_begin=2, chunk_end=5, out=out)
+    o = out.cpu().numpy()
+    assert np.all(o[:, :2] == 7.0) and np.all(o[:, 5:] == 7.0)
+    assert np.array_equal(o[:, 2:5].astype(np.float64), want[:, 2:5])
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_select(hsa_gpu, name):
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_select_topk")
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k)
+    torch.cuda.synchronize()
+    sure, loose = assert_indices(idx, ref["idx"], ref["gap"], shape.S)
+    assert loose == 0
+    err = np.max(np.abs(w.cpu().numpy() - ref["w"])) if w.numel() else 0.0
+    assert err <= W_ATOL, err
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_forward(hsa_gpu, name):
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_forward (oracle selection)")
+    idx = torch.from_numpy(ref["idx"]).cuda()
+    w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    torch.cuda.synchronize()
+    assert_close("O", shape, O, ref["O"])
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_backward(hsa_gpu, name):
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_backward (oracle selection)")
+    idx = torch.from_numpy(ref["idx"]).cuda()
+    w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    dQ, dK, dV = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"],
+                                      shape.S)
+    torch.cuda.synchronize()
+    assert_close("dQ", shape, dQ, ref["dQ"])
+    assert_close("dK", shape, dK, ref["dK"])
+    assert_close("dV", shape, dV, ref["dV"])
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "L4K_like_bf16", "ragged_bf16", "wide_like_bf16"])
+def test_end_to_end_pipeline(hsa_gpu, name):
+    """landmarks -> select -> forward -> backward, all on the GPU."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "pipeline")
+    Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
+    idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k)
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    dQ, dK, dV = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"],
+                                      shape.S)
+    torch.cuda.synchronize()
+    assert_indices(idx, ref["idx"], ref["gap"], shape.S)
+    for n, t in (("O", O), ("dQ", dQ), ("dK", dK), ("dV", dV)):
+        assert_close(n, shape, t, ref[n])
+
+
+def test_backward_is_bitwise_deterministic(hsa_gpu):
+    shape, inp, ref, dev = case("L4K_like_bf16")
+    banner("L4K_like_bf16", "backward determinism")
+    Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
+    idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k)
+    r1 = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"], shape.S)
+    r2 = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"], shape.S)
+    torch.cuda.synchronize()
+    for a, b in zip(r1, r2):
+        assert torch.equal(a, b)
+
+
+def test_outputs_fully_overwritten(hsa_gpu):
+    shape, inp, ref, dev = case("ragged_bf16")
+    banner("ragged_bf16", "overwrite semantics")
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    idx = torch.full((shape.B, shape.L, shape.G, shape.k), 12345, dtype=torch.int32,
+                     device="cuda")
+    w = torch.full_like(idx, 0, dtype=torch.float32).fill_(float("nan"))
+    hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k, idx=idx, w=w)
+    O = torch.full_like(dev["Q"], float("nan"))
+    hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S, out=O)
+    outs = tuple(torch.full_like(x, float("nan")) for x in (dev["Q"], dev["K"], dev["V"]))
+    hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"], shape.S,
+                         out=outs)
+    torch.cuda.synchronize()
+    assert np.array_equal(idx.cpu().numpy(), ref["idx"])
+    for t in (w, O) + outs:
+        assert torch.isfinite(t.float()).all()
+
+
+@pytest.mark.parametrize("kbar_dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode(hsa_gpu, dtype, kbar_dtype):
+    shape = Shape(3, 4096 + 64, 16, 2, 128 if dtype == "bf16" else 64, 64, 8, dtype)
+    banner("decode_%s_kbar_%s" % (dtype, kbar_dtype), "hsa_decode")
+    inp = hsa_synth.make_decode_inputs(shape, 21, device="cuda")
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
+    lens = [4096, 4096 + 40, 1000]            # full chunks, a partial tail, a short cache
+    cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    kb_ref = oracle.landmarks(Kc, 64)
+    Kbar = torch.from_numpy(kb_ref.astype(np.float32)).cuda().to(kbar_dtype)
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, 8, cache_len=cache_len)
+    torch.cuda.synchronize()
+    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar.float(), lens, 64, 8)
+    assert np.array_equal(idx.cpu().numpy()[rgap >= 1e-3], ridx[rgap >= 1e-3])
+    assert np.max(np.abs(w.cpu().numpy() - rw)) <= W_ATOL
+    assert_close("o", shape, o, ro)
+    for b in range(3):
+        for g in range(2):
+            p = inp["planted"][b, g].item()
+            if p < lens[b] // 64:          # the planted chunk is a candidate: it must win
+                assert p in idx[b, g].tolist()
+
+
+def test_decode_matches_forward_row(hsa_gpu):
+    """Decode at position t equals row t of the forward (same K, V, landmarks)."""
+    shape, inp, ref, dev = case("L4K_like_bf16")
+    banner("L4K_like_bf16", "decode vs forward row")
+    t = 777
+    Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
+    idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k)
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    q = dev["Q"][:, t].contiguous()
+    cl = torch.full((shape.B,), t, dtype=torch.int32, device="cuda")
+    o, di, dw = hsa_gpu.hsa_decode(q, dev["K"], dev["V"], Kbar, shape.S, shape.k, cache_len=cl)
+    torch.cuda.synchronize()
+    assert torch.equal(di, idx[:, t])
+    assert torch.allclose(dw, w[:, t], rtol=0, atol=1e-6)
+    # both sides are rounded to bf16: allow the RMS bound plus one full ulp
+    assert_close("o", shape, o, O[:, t].double().cpu().numpy(), ulps=2.0)
+
+
+def test_empty_batch_is_noop(hsa_gpu):
+    banner("empty", "B = 0")
+    Q = torch.empty((0, 128, 8, 64), device="cuda", dtype=torch.bfloat16)
+    K = torch.empty((0, 128, 2, 64), device="cuda", dtype=torch.bfloat16)
+    Kbar = hsa_gpu.hsa_landmarks(K, 64)
+    idx, w = hsa_gpu.hsa_select_topk(Q, Kbar, 2, 64, 4)
+    O = hsa_gpu.hsa_forward(Q, K, K, idx, w, 64)
+    assert O.shape == Q.shape
