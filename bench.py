@@ -1,0 +1,285 @@
+#!/usr/bin/env python
+"""Benchmark of the HSA operator on one MI355X.
+
+A step is one pass of the whole hot path over one batch of synthetic input:
+landmarks -> score + top-k -> forward -> backward (fwd+bwd workloads), or one decode step.
+Inputs are resident in HBM before the timed region.  The main line is the 4K-context
+fwd+bwd workload (B 8, L 4096, H 16 / G 2, d 128, S 64, k 8, bf16); the 64K-context
+fwd+bwd and the 1M-token decode step are reported under "also".
+
+Kernel durations come from HIP events recorded by the library around each of its launches
+on the launch stream (hsa_attn_timing_enable), inside the timed region.  The fp64 oracle
+is timed on the host cores on a bounded sample (cpu_baseline).
+
+Prints one JSON line.  `--gpus N` with N > 1 exits: this operator runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "HSA fwd+bwd tokens/s at L=4K and 64K; decode µs/token at 1M-token ctx"
+
+# MI355X published peaks
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_VALU_TFLOPS = 157.3
+
+# per-kernel algorithmic work: ("flops" per valid (token, group, slot) pair in units of
+# h*S*d, bound) or ("bytes", ...).  A valid pair is a selected chunk of a token.
+# forward: Q K^T and P V (2 matmuls = 4 h S d flops); backward: 5 matmuls in total
+# (recomputed Q K^T, dO V^T, dz K in the query pass; P^T dO, dz^T Q in the chunk pass).
+MATMULS = {"forward_generic": 2, "forward_mfma": 2, "bwd_q_generic": 3, "bwd_q_mfma": 3,
+           "bwd_kv_generic": 2, "bwd_kv_mfma": 2}
+MFMA_KERNELS = {"forward_mfma", "bwd_q_mfma", "bwd_kv_mfma"}
+
+
+def valid_pairs(B, L, G, S, k):
+    """Number of (b, t, g, slot) with a selected chunk: sum_t min(k, floor(t/S))."""
+    n = 0
+    for c in range(-(-L // S)):
+        rows = min(S, L - c * S)
+        n += rows * min(k, c)
+    return B * G * n
+
+
+def kernel_work(name, sh, pairs):
+    """(amount, unit, bound, peak) of the algorithmic work of one launch."""
+    B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
+    h = H // G
+    es = 2 if sh.dtype == "bf16" else 4
+    if name in MATMULS:
+        fl = MATMULS[name] * 2.0 * h * S * d * pairs
+        if name in MFMA_KERNELS:
+            return fl, "TFLOP/s", "mfma", PEAK_BF16_TFLOPS
+        return fl, "TFLOP/s", "alu", PEAK_FP32_VALU_TFLOPS
+    C = L // S
+    if name == "landmarks_kernel":
+        return B * C * S * G * d * es + B * C * G * d * 4, "GB/s", "hbm", PEAK_HBM_GBS
+    if name.startswith("select"):
+        return (B * L * H * d * es + B * C * G * d * 4 + B * L * G * k * 8,
+                "GB/s", "hbm", PEAK_HBM_GBS)
+    return None
+
+
+def make_training(name, torch):
+    import hsa_synth
+    wl = hsa_synth.WORKLOADS[name]
+    sh = wl["shape"]
+    t0 = time.time()
+    inp = hsa_synth.make_training_inputs(name)
+    dt = torch.bfloat16 if sh.dtype == "bf16" else torch.float32
+    dev = {n: torch.from_numpy(v).to("cuda").to(dt) for n, v in inp.items()}
+    return sh, inp, dev, time.time() - t0
+
+
+def time_training(sh, dev, steps, warmup, torch, hsa):
+    B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
+    Q, K, V, dO = dev["Q"], dev["K"], dev["V"], dev["dO"]
+    Kbar = torch.empty((B, L // S, G, d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((B, L, G, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((B, L, G, k), dtype=torch.float32, device="cuda")
+    O = torch.empty_like(Q)
+    grads = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
+    p = hsa.make_params(B, L, H, G, d, S, k, Q.dtype)
+    ws_f = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_FORWARD)), dtype=torch.uint8,
+                       device="cuda")
+    ws_b = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_BACKWARD)), dtype=torch.uint8,
+                       device="cuda")
+
+    def step():
+        hsa.hsa_landmarks(K, S, out=Kbar)
+        hsa.hsa_select_topk(Q, Kbar, G, S, k, idx=idx, w=w)
+        hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f)
+        hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    hsa.timing_collect()                       # drop anything recorded before
+    hsa.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    hsa.timing_enable(False)
+    kern = hsa.timing_collect()
+    ms = e0.elapsed_time(e1) / steps
+    return ms, kern
+
+
+def roofline_of(kern, sh, pairs):
+    """Roofline entry of the kernel with the largest total time in the timed region."""
+    name, (cnt, tot) = max(kern.items(), key=lambda kv: kv[1][1])
+    work = kernel_work(name, sh, pairs)
+    avg_ms = tot / cnt
+    if work is None:
+        return {"kernel": name, "avg_ms": avg_ms, "bound": None}
+    amount, unit, bound, peak = work
+    if unit == "TFLOP/s":
+        achieved = amount / (avg_ms * 1e-3) / 1e12
+    else:
+        achieved = amount / (avg_ms * 1e-3) / 1e9
+    return {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 5), "traffic": None,
+            "avg_ms": round(avg_ms, 5), "launches": cnt,
+            "work_per_launch": amount,
+            "work_unit": "flop" if unit == "TFLOP/s" else "byte"}
+
+
+def bench_decode(steps, warmup, torch, hsa):
+    import hsa_synth
+    wl = hsa_synth.WORKLOADS["decode_1M_bf16"]
+    sh = wl["shape"]
+    inp = hsa_synth.make_decode_inputs(sh, wl["seed"], device="cuda")
+    q, Kc, Vc = inp["q"], inp["Kc"], inp["Vc"]
+    kbar = hsa.hsa_landmarks(Kc, sh.S, kbar_dtype=torch.bfloat16)
+    p = hsa.make_params(sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k, q.dtype)
+    ws = torch.empty(hsa.workspace_size(p, hsa.HSA_OP_DECODE), dtype=torch.uint8, device="cuda")
+    o = torch.empty_like(q)
+    idx = torch.empty((sh.B, sh.G, sh.k), dtype=torch.int32, device="cuda")
+    w = torch.empty((sh.B, sh.G, sh.k), dtype=torch.float32, device="cuda")
+    for _ in range(warmup):
+        hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
+    torch.cuda.synchronize()
+    hsa.timing_collect()
+    hsa.timing_enable(True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    hsa.timing_enable(False)
+    kern = hsa.timing_collect()
+    us = e0.elapsed_time(e1) / steps * 1e3
+    planted_ok = all(int(inp["planted"][b, g]) in idx[b, g].tolist()
+                     for b in range(sh.B) for g in range(sh.G))
+    C = sh.L // sh.S
+    stream_bytes = sh.B * C * sh.G * sh.d * 2                     # bf16 landmark cache
+    gather_bytes = sh.B * sh.G * sh.k * sh.S * sh.d * 2 * 2       # selected K and V chunks
+    scan = kern.get("decode_scan")
+    out = {"workload": "decode 1M ctx: B8, 1 token/seq, cache 2^20 tokens (16384 chunks of 64),"
+                       " H16/G2 d128 k8, bf16 landmark cache",
+           "us_per_step": round(us, 3), "us_per_sequence_token": round(us / sh.B, 3),
+           "tokens_per_s": round(sh.B / (us * 1e-6), 1), "planted_chunk_selected": planted_ok,
+           "kernels_avg_us": {n: round(t / c * 1e3, 3) for n, (c, t) in kern.items()}}
+    if scan:
+        avg = scan[1] / scan[0]
+        gbs = stream_bytes / (avg * 1e-3) / 1e9
+        out["scan_roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                                "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                                "bytes_per_launch": stream_bytes}
+    out["algorithmic_bytes_per_step"] = stream_bytes + gather_bytes
+    return out
+
+
+def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
+    """Oracle fwd+bwd on whole (b, g) slices of the workload until the budget is used."""
+    import numpy as np
+    import hsa_synth
+    import oracle
+    sh = hsa_synth.WORKLOADS[name]["shape"]
+    L, G, h, d, S, k = sh.L, sh.G, sh.H // sh.G, sh.d, sh.S, sh.k
+    oracle.build(force=False)
+    done, t0 = 0, time.time()
+    for b in range(sh.B):
+        for g in range(G):
+            dm = oracle.dims(L, h, d, S, k)
+            Qs = np.ascontiguousarray(inp["Q"][b, :, g * h:(g + 1) * h], dtype=np.float64)
+            dOs = np.ascontiguousarray(inp["dO"][b, :, g * h:(g + 1) * h], dtype=np.float64)
+            Ks = np.ascontiguousarray(inp["K"][b, :, g], dtype=np.float64)
+            Vs = np.ascontiguousarray(inp["V"][b, :, g], dtype=np.float64)
+            Kb = oracle.landmarks_slice(dm, Ks)
+            idx, w, _, _ = oracle.select_slice(dm, Qs, Kb)
+            oracle.forward_slice(dm, Qs, Ks, Vs, idx, w)
+            _, ds = oracle.backward_q_slice(dm, Qs, Ks, Vs, Kb, idx, w, dOs)
+            oracle.backward_kv_slice(dm, Qs, Ks, Vs, idx, w, dOs, ds)
+            done += 1
+            if time.time() - t0 >= budget_s or done >= max_slices:
+                break
+        if time.time() - t0 >= budget_s or done >= max_slices:
+            break
+    el = time.time() - t0
+    tokens = done * L / G            # each (b, g) slice is 1/G of a sequence's work
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return {"value": round(tokens / el, 2), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "%d of %d (batch, group) slices of the %s workload, fwd+bwd "
+                      "(landmarks, select, forward, backward), fp64, %.1f s" % (
+                          done, sh.B * G, name, el)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the 64K fwd+bwd and 1M decode lines")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: the HSA operator here is a single-GPU build; run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2504_16795_amd as hsa
+    hsa.load()
+    torch.cuda.init()
+
+    name = "L4K_bf16"
+    sh, inp, dev, gen_s = make_training(name, torch)
+    print("[bench] %s inputs ready (%.1f s)" % (name, gen_s), file=sys.stderr, flush=True)
+    ms, kern = time_training(sh, dev, args.steps, args.warmup, torch, hsa)
+    pairs = valid_pairs(sh.B, sh.L, sh.G, sh.S, sh.k)
+    tokens = sh.B * sh.L
+    res = {
+        "metric": METRIC, "value": round(tokens / (ms * 1e-3), 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "HSA fwd+bwd at 4K context: B8 L4096 H16/G2 d128 S64 k8, bf16",
+                   "batch": sh.B, "seq_len": sh.L, "q_heads": sh.H, "kv_heads": sh.G,
+                   "head_dim": sh.d, "chunk": sh.S, "topk": sh.k},
+        "roofline": roofline_of(kern, sh, pairs),
+        "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern.items()},
+    }
+    print("[bench] %s: %.3f ms/step" % (name, ms), file=sys.stderr, flush=True)
+    if not args.no_extra:
+        del dev
+        torch.cuda.empty_cache()
+        name3 = "L64K_bf16"
+        sh3, _, dev3, _ = make_training(name3, torch)
+        ms3, kern3 = time_training(sh3, dev3, max(2, args.steps // 2), 1, torch, hsa)
+        pairs3 = valid_pairs(sh3.B, sh3.L, sh3.G, sh3.S, sh3.k)
+        res["also"] = {"L64K_bf16": {
+            "workload": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
+            "tokens_per_s": round(sh3.B * sh3.L / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 4),
+            "roofline": roofline_of(kern3, sh3, pairs3),
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern3.items()}}}
+        print("[bench] %s: %.3f ms/step" % (name3, ms3), file=sys.stderr, flush=True)
+        del dev3
+        torch.cuda.empty_cache()
+        res["also"]["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 5, torch, hsa)
+        print("[bench] decode: %.2f us/step" % res["also"]["decode_1M_bf16"]["us_per_step"],
+              file=sys.stderr, flush=True)
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(name, inp)
+        print("[bench] cpu baseline done", file=sys.stderr, flush=True)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -138,6 +138,17 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
                              hsa_dtype_t kbar_dtype, const int32_t* cache_len, void* o,
                              int32_t* idx, float* w, void* ws, size_t ws_bytes, void* stream);
 
+/* Optional kernel timing: while enabled (on != 0), every kernel launched by this library is
+ * bracketed by two HIP events recorded on its stream.  Off by default. */
+hsa_attn_status_t hsa_attn_timing_enable(int on);
+
+/* Waits for the recorded events and accumulates, per kernel name, the launches and total
+ * milliseconds since the last delivery.  If len is at least the returned length, writes
+ * one line per kernel, "name launches total_ms\n", NUL-terminated, into buf and starts a
+ * new accumulation; otherwise keeps the totals (buf, if given, receives "").  Returns the
+ * length needed including the NUL. */
+int hsa_attn_timing_collect(char* buf, size_t len);
+
 /* Workspace bytes needed by `op` (an hsa_op_t) for these params; 0 if none.  Returns 0
  * for invalid params as well (the entry point then reports the error). */
 size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op);

@@ -39,7 +39,8 @@ class HsaError(RuntimeError):
 
 
 EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
-            "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error")
+            "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
+            "hsa_attn_timing_enable", "hsa_attn_timing_collect")
 
 
 def load(path: Optional[str] = None) -> ctypes.CDLL:
@@ -66,6 +67,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_attn_status_string.restype = ctypes.c_char_p
     lib.hsa_attn_last_error.argtypes = []
     lib.hsa_attn_last_error.restype = ctypes.c_char_p
+    lib.hsa_attn_timing_enable.argtypes = [ctypes.c_int]
+    lib.hsa_attn_timing_enable.restype = I32
+    lib.hsa_attn_timing_collect.argtypes = [ctypes.c_char_p, SZ]
+    lib.hsa_attn_timing_collect.restype = ctypes.c_int
     if path is None:
         _lib = lib
     return lib
@@ -228,3 +233,22 @@ def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
                              _ptr(o), _ptr(idx), _ptr(w), _ptr(ws), nb, _stream(q.device)),
            "hsa_decode")
     return o, idx, w
+
+
+def timing_enable(on: bool = True) -> None:
+    """Bracket every kernel launch of the library with HIP events on its stream."""
+    load().hsa_attn_timing_enable(1 if on else 0)
+
+
+def timing_collect() -> dict:
+    """{kernel name: (launches, total ms)} for the launches recorded since the last call."""
+    lib = load()
+    n = lib.hsa_attn_timing_collect(None, 0)
+    buf = ctypes.create_string_buffer(n + 4096)
+    while lib.hsa_attn_timing_collect(buf, len(buf)) > len(buf):
+        buf = ctypes.create_string_buffer(2 * len(buf))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        out[name] = (int(cnt), float(ms))
+    return out

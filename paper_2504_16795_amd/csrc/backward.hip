@@ -302,9 +302,12 @@ void launch_kv(const Dims& dm, const void* Q, const void* K, const void* V, cons
                const float* w, const void* dO, const float* ds, const uint32_t* bm, int nwords,
                void* dK, void* dV, hipStream_t st) {
     dim3 grid(dm.Call, dm.B * dm.G);
-    hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), grid, dim3(kThreads), 0, st, dm, (const T*)Q,
-                       (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm, nwords, (T*)dK,
-                       (T*)dV);
+    {
+        HSA_TIMED("bwd_kv_generic", st);
+        hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), grid, dim3(kThreads), 0, st, dm, (const T*)Q,
+                           (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm, nwords, (T*)dK,
+                           (T*)dV);
+    }
 }
 
 template <typename T, int D>
@@ -324,37 +327,73 @@ void launch_kv_s(const Dims& dm, const void* Q, const void* K, const void* V,
     }
 }
 
+// selection bitmap, then the chunk-major key/value pass (ds already in the workspace)
 template <typename T>
-hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
-                    const float* Kbar, const int32_t* idx, const float* w, const void* dO,
-                    void* dQ, void* dK, void* dV, void* ws, hipStream_t st) {
+void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
+                    const int32_t* idx, const float* w, const void* dO, void* dK, void* dV,
+                    void* ws, hipStream_t st) {
     const int nwords = cdiv(dm.L, 32);
-    float* ds = (float*)ws;
+    const float* ds = (const float*)ws;
     uint32_t* bm = (uint32_t*)((char*)ws + align256((size_t)dm.B * dm.L * dm.G * dm.k * 4));
     const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
-
-    dim3 g1(dm.L, dm.B * dm.G);
-    if (dm.d == 128)
-        hipLaunchKernelGGL((bwd_q_generic<T, 128>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
-                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
-    else
-        hipLaunchKernelGGL((bwd_q_generic<T, 64>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
-                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
     if (nbm) {
-        hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)cdiv((int)((nbm + 255) / 256), 1)),
-                           dim3(256), 0, st, bm, nbm);
+        {
+            HSA_TIMED("fill_zero_u32", st);
+            hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0,
+                               st, bm, nbm);
+        }
         const size_t ne = (size_t)dm.B * dm.L * dm.G * dm.k;
-        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st,
-                           dm, idx, bm, nwords);
+        {
+            HSA_TIMED("bitmap_build", st);
+            hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st,
+                               dm, idx, bm, nwords);
+        }
     }
     if (dm.d == 128)
         launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
     else
         launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+}
+
+template <typename T>
+hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
+                    const float* Kbar, const int32_t* idx, const float* w, const void* dO,
+                    void* dQ, void* dK, void* dV, void* ws, hipStream_t st) {
+    float* ds = (float*)ws;
+    dim3 g1(dm.L, dm.B * dm.G);
+    if (dm.d == 128) {
+        HSA_TIMED("bwd_q_generic", st);
+        hipLaunchKernelGGL((bwd_q_generic<T, 128>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
+                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
+    } else {
+        HSA_TIMED("bwd_q_generic", st);
+        hipLaunchKernelGGL((bwd_q_generic<T, 64>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
+                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
+    }
+    launch_kv_pass<T>(dm, Q, K, V, idx, w, dO, dK, dV, ws, st);
     return hipGetLastError();
 }
 
 }  // namespace
+
+hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm,
+                                   hipStream_t st) {
+    const int nwords = cdiv(dm.L, 32);
+    const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
+    if (!nbm) return hipSuccess;
+    {
+        HSA_TIMED("fill_zero_u32", st);
+        hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0, st,
+                           bm, nbm);
+    }
+    const size_t ne = (size_t)dm.B * dm.L * dm.G * dm.k;
+    {
+        HSA_TIMED("bitmap_build", st);
+        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st, dm,
+                           idx, bm, nwords);
+    }
+    return hipGetLastError();
+}
 
 size_t backward_generic_workspace(const Dims& dm) {
     const size_t nwords = (size_t)cdiv(dm.L, 32);

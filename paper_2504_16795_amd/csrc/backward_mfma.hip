@@ -1,15 +1,632 @@
-// bf16 MFMA backward for the main shapes (placeholder until the MFMA kernels land).
-#include "common.h"
+// bf16 MFMA backward of hierarchical sparse attention (Sec. 3.1.2, two-phase backward),
+// for h = 8 query heads per KV head, d = 128, S in {64, 128}.
+//
+// Query pass (bwd_q_mfma): same tiling as the forward (32-token tile inside one query
+// chunk, union of the tile's chunks staged once in LDS, wave = two row blocks of 16 rows).
+// Per active row block and chunk:
+//     Z^T  = K_c Q^T,  dP^T = V_c dO^T                     (keys x rows, MFMA)
+//     P    = softmax over keys;  D_row = sum_keys P dP      (= dO_row . O_{row,c})
+//     dZ^T = w P (dP - D)
+//     dQ^T += K_c^T dZ^T                                    (MFMA, K^T staged in LDS;
+//                                                             dZ as a bf16 hi/lo pair)
+//     dw_{t,c} = sum over the token's 8 heads of D_row
+// then ds_i = w_i (dw_i - sum_m w_m dw_m) and dQ = beta dQ + alpha sum_i ds_i Kbar_{c_i}.
+// For the key pass it stores, per (token, slot, head), the log-sum-exp of the scaled logits
+// and D, plus ds per (token, slot).
+//
+// Key pass: chunk-major, reading those statistics (see bwd_kv_mfma below).
+#include <cstdlib>
+
+#include "mfma_common.h"
 
 namespace hsa {
 
-bool backward_mfma_supported(const Dims&, bool) { return false; }
-size_t backward_mfma_workspace(const Dims&) { return 0; }
+size_t backward_generic_workspace(const Dims& dm);
+hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm,
+                                   hipStream_t st);
 
-hipError_t launch_backward_mfma(const Dims&, const void*, const void*, const void*,
-                                const float*, const int32_t*, const float*, const void*, void*,
-                                void*, void*, void*, hipStream_t) {
-    return hipErrorNotSupported;
+namespace {
+
+constexpr int D = 128;
+constexpr int HG = 8;
+constexpr int NW = 8;
+constexpr int kThreads = NW * 64;
+constexpr int TQ = 32;
+constexpr int KMAX = 32;
+constexpr int KP = D + 8;
+
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// workspace layout shared by both passes (ds and the bitmap first, as in the generic path)
+struct WsLayout {
+    size_t ds, bitmap, lse, dd, end;
+};
+__host__ __device__ inline WsLayout ws_layout(const Dims& dm) {
+    WsLayout l;
+    const size_t nsel = (size_t)dm.B * dm.L * dm.G * dm.k;
+    const size_t nwords = (size_t)((dm.L + 31) / 32);
+    l.ds = 0;
+    l.bitmap = align256(nsel * 4);
+    l.lse = l.bitmap + align256((size_t)dm.B * dm.G * dm.C * nwords * 4);
+    l.dd = l.lse + align256(nsel * dm.h * 4);
+    l.end = l.dd + align256(nsel * dm.h * 4);
+    return l;
+}
+
+template <int S>
+struct SmemQ {
+    static constexpr int VP = S + 8;
+    __bf16 Ks[S * KP];
+    __bf16 Vs[S * KP];
+    __bf16 Kt[D * VP];
+    int32_t sidx[TQ * KMAX];
+    float sw[TQ * KMAX];
+    float dw[TQ * KMAX];
+    int32_t ulist[TQ * KMAX];
+    uint8_t flag[TQ * KMAX];
+    int nu;
+};
+
+template <int S>
+__global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
+    Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
+    const __bf16* __restrict__ V, const float* __restrict__ Kbar,
+    const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const __bf16* __restrict__ dO, __bf16* __restrict__ dQ, float* __restrict__ ds_out,
+    float* __restrict__ lse_out, float* __restrict__ d_out, int ntiles) {
+    constexpr int VP = SmemQ<S>::VP;
+    constexpr int MB = S / 16;
+    constexpr int KS2 = S / 32;
+    constexpr int NPF = S * D / 8 / kThreads;
+    __shared__ SmemQ<S> sm;
+
+    const int lid = xcd_logical_id(ntiles * dm.B * dm.G);
+    if (lid < 0) return;
+    const int tile = lid % ntiles, bg = lid / ntiles;
+    const int b = bg / dm.G, g = bg % dm.G;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int k = dm.k;
+    const int t0 = tile * TQ;
+    const int ncand = t0 / S;
+    const int row = lane & 15, grp = lane >> 4;
+
+    // ---- selections of the tile and their union -------------------------------------
+    const int ne = TQ * k;
+    for (int e = tid; e < ne; e += kThreads) {
+        const int tau = e / k, t = t0 + tau;
+        int c = -1;
+        float wt = 0.f;
+        if (t < dm.L) {
+            const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k + e % k;
+            c = idx[o];
+            wt = w[o];
+            if (c < 0 || c >= ncand) {
+                c = -1;
+                wt = 0.f;
+            }
+        }
+        sm.sidx[e] = c;
+        sm.sw[e] = wt;
+        sm.dw[e] = 0.f;
+    }
+    __syncthreads();
+    for (int e = tid; e < ne; e += kThreads) {
+        const int c = sm.sidx[e];
+        bool first = c >= 0;
+        for (int e2 = 0; e2 < e && first; ++e2) first = sm.sidx[e2] != c;
+        sm.flag[e] = first ? 1 : 0;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const int per = (ne + 63) / 64;
+        const int e0 = lane * per, e1 = min(ne, e0 + per);
+        int cnt = 0;
+        for (int e = e0; e < e1; ++e) cnt += sm.flag[e];
+        int incl = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += v;
+        }
+        int pos = incl - cnt;
+        for (int e = e0; e < e1; ++e)
+            if (sm.flag[e]) sm.ulist[pos++] = sm.sidx[e];
+        if (lane == 63) sm.nu = incl;
+    }
+
+    // ---- Q^T and dO^T operands of the wave's row blocks -------------------------------
+    bf16x8_t qB[2][4], gB[2][4];
+    f32x4_t acc[2][8];
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        const int t = t0 + wave * 4 + rb * 2 + (row >> 3);
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            if (t < dm.L) {
+                const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D +
+                                 32 * ks + 8 * grp;
+                qB[rb][ks] = ld_bf16x8(Q + o);
+                gB[rb][ks] = ld_bf16x8(dO + o);
+            } else {
+                qB[rb][ks] = bf16x8_t{};
+                gB[rb][ks] = bf16x8_t{};
+            }
+        }
+#pragma unroll
+        for (int db = 0; db < 8; ++db) acc[rb][db] = zero4();
+    }
+    __syncthreads();
+    const int nu = sm.nu;
+
+    const size_t rowstride = (size_t)dm.G * D;
+    // staging: thread covers keys 2 (p / 16), 2 (p / 16) + 1 of column block p % 16 (vector
+    // pairs); K and V go to LDS row-major, K also transposed (key pairs packed).
+    u32x4_t kreg[NPF], vreg[NPF];
+    auto load_chunk = [&](int c) __attribute__((always_inline)) {
+        const size_t base = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
+#pragma unroll
+        for (int i = 0; i < NPF; ++i) {
+            const int p = tid + (i >> 1) * kThreads;
+            const int r = (p >> 4) * 2 + (i & 1), col = (p & 15) * 8;
+            kreg[i] = *reinterpret_cast<const u32x4_t*>(K + base + (size_t)r * rowstride + col);
+            vreg[i] = *reinterpret_cast<const u32x4_t*>(V + base + (size_t)r * rowstride + col);
+        }
+    };
+    auto store_chunk = [&]() __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < NPF; ++i) {
+            const int p = tid + (i >> 1) * kThreads;
+            const int r = (p >> 4) * 2 + (i & 1), col = (p & 15) * 8;
+            *reinterpret_cast<u32x4_t*>(&sm.Ks[r * KP + col]) = kreg[i];
+            *reinterpret_cast<u32x4_t*>(&sm.Vs[r * KP + col]) = vreg[i];
+        }
+#pragma unroll
+        for (int i = 0; i < NPF; i += 2) {
+            const int p = tid + (i >> 1) * kThreads;
+            const int r = (p >> 4) * 2, col = (p & 15) * 8;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t a = kreg[i][j], c2 = kreg[i + 1][j];
+                *reinterpret_cast<uint32_t*>(&sm.Kt[(col + 2 * j) * VP + r]) =
+                    (a & 0xFFFFu) | (c2 << 16);
+                *reinterpret_cast<uint32_t*>(&sm.Kt[(col + 2 * j + 1) * VP + r]) =
+                    (a >> 16) | (c2 & 0xFFFF0000u);
+            }
+        }
+    };
+
+    const float beta = dm.beta;
+    const float sl2 = beta * 1.44269504088896341f;
+    const float ln2 = 0.69314718055994531f;
+    if (nu > 0) load_chunk(sm.ulist[0]);
+    for (int u = 0; u < nu; ++u) {
+        const int c = sm.ulist[u];
+        __syncthreads();
+        store_chunk();
+        __syncthreads();
+        if (u + 1 < nu) load_chunk(sm.ulist[u + 1]);
+
+#pragma unroll
+        for (int rb = 0; rb < 2; ++rb) {
+            const int tau = wave * 4 + rb * 2 + (row >> 3);
+            float wl = 0.f;
+            int slot = -1;
+            for (int s = 0; s < k; ++s)
+                if (sm.sidx[tau * k + s] == c) {
+                    wl = sm.sw[tau * k + s];
+                    slot = s;
+                }
+            if (__ballot(slot >= 0) == 0) continue;
+
+            f32x4_t z[MB], dp[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                z[mb] = zero4();
+                dp[mb] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8_t ka = ld_bf16x8(&sm.Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
+                    z[mb] = mfma16(ka, qB[rb][ks], z[mb]);
+                    const bf16x8_t va = ld_bf16x8(&sm.Vs[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
+                    dp[mb] = mfma16(va, gB[rb][ks], dp[mb]);
+                }
+            }
+            float m = -INFINITY;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
+            m = fmaxf(m, __shfl_xor(m, 16, 64));
+            m = fmaxf(m, __shfl_xor(m, 32, 64));
+            float ssum = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    z[mb][i] = exp2f((z[mb][i] - m) * sl2);
+                    ssum += z[mb][i];
+                }
+            ssum += __shfl_xor(ssum, 16, 64);
+            ssum += __shfl_xor(ssum, 32, 64);
+            const float inv = 1.f / ssum;
+            float dsum = 0.f;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    z[mb][i] *= inv;                                  // P
+                    dsum = fmaf(z[mb][i], dp[mb][i], dsum);
+                }
+            dsum += __shfl_xor(dsum, 16, 64);
+            dsum += __shfl_xor(dsum, 32, 64);                         // D of this row
+            // dZ = w P (dP - D), fed as the B operand of dQ^T += K^T dZ^T.  sum_s dZ_s = 0,
+            // so dQ is a cancelling sum: dZ enters as a bf16 pair (hi + lo, ~16 mantissa
+            // bits) to keep its rounding from being amplified by the key magnitudes.
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) z[mb][i] = wl * z[mb][i] * (dp[mb][i] - dsum);
+#pragma unroll
+            for (int ks2 = 0; ks2 < KS2; ++ks2) {
+                bf16x8_t zh, zl;
+                split8(z[2 * ks2], z[2 * ks2 + 1], zh, zl);
+#pragma unroll
+                for (int db = 0; db < 8; ++db) {
+                    const __bf16* kr = &sm.Kt[(16 * db + row) * VP + 32 * ks2 + 4 * grp];
+                    const bf16x8_t a = cat(ld_bf16x4(kr), ld_bf16x4(kr + 16));
+                    acc[rb][db] = mfma16(a, zh, acc[rb][db]);
+                    acc[rb][db] = mfma16(a, zl, acc[rb][db]);
+                }
+            }
+            // statistics of this (token, slot, head) and dw of the token
+            float dtok = dsum;
+            dtok += __shfl_xor(dtok, 1, 64);
+            dtok += __shfl_xor(dtok, 2, 64);
+            dtok += __shfl_xor(dtok, 4, 64);
+            if (slot >= 0) {
+                const int t = t0 + tau;
+                const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k + slot;
+                if (grp == 0) {
+                    lse_out[so * HG + (row & 7)] = m * beta + __logf(ssum);
+                    d_out[so * HG + (row & 7)] = dsum;
+                }
+                if (grp == 0 && (row & 7) == 0) sm.dw[tau * k + slot] = dtok;
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- softmax-weight Jacobian, score term, write dQ and ds ----------------------------
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb) {
+        const int tau = wave * 4 + rb * 2 + (row >> 3);
+        const int t = t0 + tau;
+        if (t >= dm.L) continue;
+        float wdw = 0.f;
+        for (int s = 0; s < k; ++s) wdw = fmaf(sm.sw[tau * k + s], sm.dw[tau * k + s], wdw);
+        f32x4_t out[8];
+#pragma unroll
+        for (int db = 0; db < 8; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) out[db][i] = beta * acc[rb][db][i];
+        for (int s = 0; s < k; ++s) {
+            const int c = sm.sidx[tau * k + s];
+            const float dsv = (c >= 0) ? sm.sw[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
+            if (grp == 0 && (row & 7) == 0)
+                ds_out[(((size_t)b * dm.L + t) * dm.G + g) * k + s] = dsv;
+            if (c < 0) continue;
+            const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;
+            const float coef = dm.alpha * dsv;
+#pragma unroll
+            for (int db = 0; db < 8; ++db) {
+                const float4 kv = *reinterpret_cast<const float4*>(kb + 16 * db + 4 * grp);
+                out[db][0] = fmaf(coef, kv.x, out[db][0]);
+                out[db][1] = fmaf(coef, kv.y, out[db][1]);
+                out[db][2] = fmaf(coef, kv.z, out[db][2]);
+                out[db][3] = fmaf(coef, kv.w, out[db][3]);
+            }
+        }
+        __bf16* op = dQ + (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const bf16x4_t o4{f2bf(out[db][0]), f2bf(out[db][1]), f2bf(out[db][2]),
+                              f2bf(out[db][3])};
+            *reinterpret_cast<bf16x4_t*>(op + 16 * db + 4 * grp) = o4;
+        }
+    }
+}
+
+// ----------------------------------------------------------------------------------------
+// Key pass (bwd_kv_mfma): workgroup = (b, g, chunk c); wave w owns keys 16w..16w+15 and
+// keeps K_sub, V_sub as B operands in registers and dK_sub, dV_sub [16 x 128] as fp32
+// accumulators.  The tokens that selected c are read from the selection bitmap in
+// increasing order, four at a time (32 rows = 4 tokens x 8 heads):
+//     Z  [32 x 16] = Q_rows K_sub^T,   dP = dO_rows V_sub^T          (MFMA)
+//     P  = exp(beta Z - lse_row),  dZ = w P (dP - D_row)            (stored by the query pass)
+//     dV_sub += (w P)^T dO_rows,  dK_sub += dZ^T Q_rows              (MFMA, K = 32 rows;
+//                                                 w P and dZ as bf16 hi/lo pairs)
+// The C layout of Z feeds the A operand of the last two products directly (row
+// permutation applied to the transposed Q / dO rows in LDS).  dKbar_c = alpha sum ds q~ is
+// a VALU side sum; dK = beta dK_sub + dKbar_c / S.  No atomics; fixed token order.
+constexpr int RP = 32 + 8;        // padded row count of the transposed Q / dO group tiles
+constexpr int LISTCAP = 64 * 32 + 4;
+
+struct SmemKV {
+    __bf16 Qr[32 * KP];
+    __bf16 Gr[32 * KP];
+    __bf16 Qt[D * RP];
+    __bf16 Gt[D * RP];
+    float lse[32], dd[32];
+    float tw[4], tds[4];
+    int ttok[4];
+    int list[LISTCAP];
+    float dkb[D];
+    int nlist;
+};
+
+template <int S>
+__global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
+    Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
+    const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const __bf16* __restrict__ dO, const float* __restrict__ ds, const float* __restrict__ lse,
+    const float* __restrict__ dd, const uint32_t* __restrict__ bm, int nwords,
+    __bf16* __restrict__ dK, __bf16* __restrict__ dV) {
+    constexpr int NT = S * 4;               // threads: S / 16 waves
+    __shared__ SmemKV sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = lane & 15, grp = lane >> 4;
+    const int c = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const int k = dm.k;
+    const size_t rowstride = (size_t)dm.G * D;
+    const size_t cbase = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
+
+    if (c >= dm.C) {   // trailing partial chunk: never selected
+        const int rows = dm.L - c * S;
+        for (int i = tid; i < rows * D; i += NT) {
+            const size_t o = cbase + (size_t)(i / D) * rowstride + i % D;
+            dK[o] = __bf16(0.f);
+            dV[o] = __bf16(0.f);
+        }
+        return;
+    }
+
+    // B operands of the wave's 16 keys: K_sub^T[d][key], V_sub^T[d][key]
+    bf16x8_t kB[4], vB[4];
+    const int key = 16 * wave + row;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+        vB[ks] = ld_bf16x8(V + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+    }
+    f32x4_t aK[8], aV[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
+    float dkbar = 0.f;                       // thread tid < D owns dKbar[tid]
+    if (tid == 0) sm.nlist = 0;
+    const float beta = dm.beta;
+    const float l2e = 1.44269504088896341f;
+
+    const uint32_t* bmrow = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
+    const int wbeg = ((c + 1) * S) >> 5;
+    bool last_round = wbeg >= nwords;
+    for (int wb = wbeg; ; wb += 64) {
+        __syncthreads();
+        if (!last_round && wave == 0) {
+            const int wi = wb + lane;
+            const uint32_t word = wi < nwords ? bmrow[wi] : 0u;
+            const int cnt = __popc(word);
+            int incl = cnt;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int v = __shfl_up(incl, o, 64);
+                if (lane >= o) incl += v;
+            }
+            const int n0 = sm.nlist;
+            int pos = n0 + incl - cnt;
+            uint32_t x = word;
+            while (x) {
+                sm.list[pos++] = wi * 32 + (__ffs(x) - 1);
+                x &= x - 1;
+            }
+            const int tot = __shfl(incl, 63, 64);
+            if (lane == 0) sm.nlist = n0 + tot;
+        }
+        if (!last_round) last_round = wb + 64 >= nwords;
+        __syncthreads();
+        const int nl = sm.nlist;
+        const int ngroups = last_round ? (nl + 3) / 4 : nl / 4;
+        for (int gi = 0; gi < ngroups; ++gi) {
+            // ---- stage the group: token info, Q / dO rows (row-major and transposed) -----
+            if (tid < 4) {
+                const int li = gi * 4 + tid;
+                int t = -1, slot = 0;
+                if (li < nl) {
+                    t = sm.list[li];
+                    const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
+                    for (int s2 = 0; s2 < k; ++s2)
+                        if (idx[so + s2] == c) slot = s2;
+                    sm.tw[tid] = w[so + slot];
+                    sm.tds[tid] = ds[so + slot];
+                } else {
+                    sm.tw[tid] = 0.f;
+                    sm.tds[tid] = 0.f;
+                }
+                sm.ttok[tid] = t;
+                // per-row statistics of the token's 8 heads
+                for (int j = 0; j < HG; ++j) {
+                    float lv = 0.f, dv = 0.f;
+                    if (t >= 0) {
+                        const size_t so = ((((size_t)b * dm.L + t) * dm.G + g) * k + slot) * HG + j;
+                        lv = lse[so];
+                        dv = dd[so];
+                    }
+                    sm.lse[tid * 8 + j] = lv;
+                    sm.dd[tid * 8 + j] = dv;
+                }
+            }
+            __syncthreads();
+            for (int pv = tid; pv < 256; pv += NT) {
+                const int r = (pv >> 4) * 2, col = (pv & 15) * 8;   // rows r, r+1 (same token)
+                const int t = sm.ttok[r >> 3];
+                u32x4_t q0 = {0, 0, 0, 0}, q1 = q0, g0 = q0, g1 = q0;
+                if (t >= 0) {
+                    const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (r & 7)) * D + col;
+                    q0 = *reinterpret_cast<const u32x4_t*>(Q + o);
+                    q1 = *reinterpret_cast<const u32x4_t*>(Q + o + D);
+                    g0 = *reinterpret_cast<const u32x4_t*>(dO + o);
+                    g1 = *reinterpret_cast<const u32x4_t*>(dO + o + D);
+                }
+                *reinterpret_cast<u32x4_t*>(&sm.Qr[r * KP + col]) = q0;
+                *reinterpret_cast<u32x4_t*>(&sm.Qr[(r + 1) * KP + col]) = q1;
+                *reinterpret_cast<u32x4_t*>(&sm.Gr[r * KP + col]) = g0;
+                *reinterpret_cast<u32x4_t*>(&sm.Gr[(r + 1) * KP + col]) = g1;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int sh = (e & 1) ? 16 : 0;
+                    const uint32_t qa = (q0[e >> 1] >> sh) & 0xFFFFu, qb = (q1[e >> 1] >> sh) & 0xFFFFu;
+                    const uint32_t ga = (g0[e >> 1] >> sh) & 0xFFFFu, gb = (g1[e >> 1] >> sh) & 0xFFFFu;
+                    *reinterpret_cast<uint32_t*>(&sm.Qt[(col + e) * RP + r]) = qa | (qb << 16);
+                    *reinterpret_cast<uint32_t*>(&sm.Gt[(col + e) * RP + r]) = ga | (gb << 16);
+                }
+            }
+            __syncthreads();
+
+            // ---- Z, dP for the wave's 16 keys ---------------------------------------------
+            f32x4_t z[2], dp[2];
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                z[rb] = zero4();
+                dp[rb] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks) {
+                    const bf16x8_t qa = ld_bf16x8(&sm.Qr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
+                    z[rb] = mfma16(qa, kB[ks], z[rb]);
+                    const bf16x8_t ga = ld_bf16x8(&sm.Gr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
+                    dp[rb] = mfma16(ga, vB[ks], dp[rb]);
+                }
+            }
+            // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2)
+            f32x4_t pw[2], dz[2];
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                const float wt = sm.tw[2 * rb + (grp >> 1)];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int r = 16 * rb + 4 * grp + i;
+                    const float p = exp2f((beta * z[rb][i] - sm.lse[r]) * l2e);
+                    pw[rb][i] = wt * p;
+                    dz[rb][i] = wt * p * (dp[rb][i] - sm.dd[r]);
+                }
+            }
+            // both products accumulate over every row that selected the chunk (thousands for
+            // a popular chunk): w P and dZ enter as bf16 hi/lo pairs
+            bf16x8_t pvh, pvl, dzh, dzl;
+            split8(pw[0], pw[1], pvh, pvl);
+            split8(dz[0], dz[1], dzh, dzl);
+#pragma unroll
+            for (int db = 0; db < 8; ++db) {
+                const __bf16* gr = &sm.Gt[(16 * db + row) * RP + 4 * grp];
+                const bf16x8_t gb = cat(ld_bf16x4(gr), ld_bf16x4(gr + 16));
+                aV[db] = mfma16(pvh, gb, aV[db]);
+                aV[db] = mfma16(pvl, gb, aV[db]);
+                const __bf16* qr = &sm.Qt[(16 * db + row) * RP + 4 * grp];
+                const bf16x8_t qb = cat(ld_bf16x4(qr), ld_bf16x4(qr + 16));
+                aK[db] = mfma16(dzh, qb, aK[db]);
+                aK[db] = mfma16(dzl, qb, aK[db]);
+            }
+            // landmark term: dKbar += alpha * ds_tok * sum_j q_{tok, j}
+            if (tid < D) {
+                float a = 0.f;
+#pragma unroll
+                for (int r = 0; r < 32; ++r)
+                    a = fmaf(sm.tds[r >> 3], (float)sm.Qt[tid * RP + r], a);
+                dkbar = fmaf(dm.alpha, a, dkbar);
+            }
+            __syncthreads();
+        }
+        // keep the tokens of an incomplete group for the next batch
+        if (!last_round) {
+            const int rem = nl - ngroups * 4;
+            if (tid < rem) sm.list[tid] = sm.list[ngroups * 4 + tid];
+            __syncthreads();
+            if (tid == 0) sm.nlist = rem;
+        } else {
+            break;
+        }
+    }
+    if (tid < D) sm.dkb[tid] = dkbar;
+    __syncthreads();
+    const float invS = 1.f / (float)S;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+        const int d = 16 * db + row;
+        const float kb = sm.dkb[d] * invS;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const size_t o = cbase + (size_t)(16 * wave + 4 * grp + i) * rowstride + d;
+            dK[o] = f2bf(beta * aK[db][i] + kb);
+            dV[o] = f2bf(aV[db][i]);
+        }
+    }
+}
+
+}  // namespace
+
+bool backward_mfma_supported(const Dims& dm, bool in_bf16) {
+    return in_bf16 && dm.h == HG && dm.d == D && (dm.S == 64 || dm.S == 128) && dm.k <= KMAX &&
+           !getenv("HSA_FORCE_GENERIC");
+}
+
+size_t backward_mfma_workspace(const Dims& dm) {
+    if (dm.h != HG || dm.d != D) return 0;
+    return ws_layout(dm).end;
+}
+
+hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
+                                const float* Kbar, const int32_t* idx, const float* w,
+                                const void* dO, void* dQ, void* dK, void* dV, void* ws,
+                                hipStream_t st) {
+    const WsLayout l = ws_layout(dm);
+    char* wsb = (char*)ws;
+    float* ds = (float*)(wsb + l.ds);
+    float* lse = (float*)(wsb + l.lse);
+    float* dd = (float*)(wsb + l.dd);
+    const int ntiles = cdiv(dm.L, TQ);
+    const int nlog = ntiles * dm.B * dm.G;
+    const int grid = 8 * cdiv(nlog, 8);
+    if (dm.S == 64) {
+        HSA_TIMED("bwd_q_mfma", st);
+        hipLaunchKernelGGL((bwd_q_mfma<64>), dim3(grid), dim3(kThreads), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Kbar, idx, w,
+                           (const __bf16*)dO, (__bf16*)dQ, ds, lse, dd, ntiles);
+    } else {
+        HSA_TIMED("bwd_q_mfma", st);
+        hipLaunchKernelGGL((bwd_q_mfma<128>), dim3(grid), dim3(kThreads), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Kbar, idx, w,
+                           (const __bf16*)dO, (__bf16*)dQ, ds, lse, dd, ntiles);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // selection bitmap (shared with the generic path), then the key pass
+    e = launch_selection_bitmap(dm, idx, (uint32_t*)(wsb + l.bitmap), st);
+    if (e != hipSuccess) return e;
+    const int nwords = cdiv(dm.L, 32);
+    dim3 g2(dm.Call, dm.B * dm.G);
+    if (dm.S == 64) {
+        HSA_TIMED("bwd_kv_mfma", st);
+        hipLaunchKernelGGL((bwd_kv_mfma<64>), g2, dim3(256), 0, st, dm, (const __bf16*)Q,
+                           (const __bf16*)K, (const __bf16*)V, idx, w, (const __bf16*)dO, ds,
+                           lse, dd, (const uint32_t*)(wsb + l.bitmap), nwords, (__bf16*)dK,
+                           (__bf16*)dV);
+    } else {
+        HSA_TIMED("bwd_kv_mfma", st);
+        hipLaunchKernelGGL((bwd_kv_mfma<128>), g2, dim3(512), 0, st, dm, (const __bf16*)Q,
+                           (const __bf16*)K, (const __bf16*)V, idx, w, (const __bf16*)dO, ds,
+                           lse, dd, (const uint32_t*)(wsb + l.bitmap), nwords, (__bf16*)dK,
+                           (__bf16*)dV);
+    }
+    return hipGetLastError();
 }
 
 }  // namespace hsa

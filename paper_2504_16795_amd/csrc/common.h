@@ -49,6 +49,22 @@ __device__ __forceinline__ float wave_max(float v) {
 
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// RAII bracket of one kernel launch for the optional per-kernel timing (timing.hip).
+class KernelTimer {
+  public:
+    KernelTimer(const char* name, hipStream_t st);
+    ~KernelTimer();
+    KernelTimer(const KernelTimer&) = delete;
+    KernelTimer& operator=(const KernelTimer&) = delete;
+
+  private:
+    const char* name_;
+    hipStream_t st_;
+    hipEvent_t a_ = nullptr, b_ = nullptr;
+};
+
+#define HSA_TIMED(name, st) ::hsa::KernelTimer hsa_kernel_timer_(name, st)
+
 }  // namespace hsa
 
 // Host launchers implemented in the kernel translation units (called by hsa_api.hip).

@@ -299,17 +299,29 @@ void launch_tk(const Dims& dm, const void* q, const void* Kc, const void* Vc, co
     int32_t* cc = (int32_t*)((char*)ws + (((size_t)dm.B * dm.G * nslices * dm.k * 4 + 255) & ~(size_t)255));
     dim3 g1(nslices, dm.B);
     if (dm.d == 128) {
-        hipLaunchKernelGGL((decode_scan<T, Tk, 128>), g1, dim3(kScanThreads), 0, st, dm,
-                           (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
-        hipLaunchKernelGGL((decode_finish<T, 128>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
-                           dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                           nslices, (T*)o, idx, w);
+        {
+            HSA_TIMED("decode_scan", st);
+            hipLaunchKernelGGL((decode_scan<T, Tk, 128>), g1, dim3(kScanThreads), 0, st, dm,
+                               (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
+        }
+        {
+            HSA_TIMED("decode_finish", st);
+            hipLaunchKernelGGL((decode_finish<T, 128>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
+                               dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
+                               nslices, (T*)o, idx, w);
+        }
     } else {
-        hipLaunchKernelGGL((decode_scan<T, Tk, 64>), g1, dim3(kScanThreads), 0, st, dm,
-                           (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
-        hipLaunchKernelGGL((decode_finish<T, 64>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
-                           dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                           nslices, (T*)o, idx, w);
+        {
+            HSA_TIMED("decode_scan", st);
+            hipLaunchKernelGGL((decode_scan<T, Tk, 64>), g1, dim3(kScanThreads), 0, st, dm,
+                               (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
+        }
+        {
+            HSA_TIMED("decode_finish", st);
+            hipLaunchKernelGGL((decode_finish<T, 64>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
+                               dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
+                               nslices, (T*)o, idx, w);
+        }
     }
 }
 

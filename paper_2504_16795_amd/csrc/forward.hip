@@ -103,12 +103,15 @@ template <typename T>
 hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
                     const int32_t* idx, const float* w, void* O, hipStream_t st) {
     dim3 grid(dm.L, dm.B * dm.G);
-    if (dm.d == 128)
+    if (dm.d == 128) {
+        HSA_TIMED("forward_generic", st);
         hipLaunchKernelGGL((forward_generic<T, 128>), grid, dim3(kThreads), 0, st, dm,
                            (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
-    else
+    } else {
+        HSA_TIMED("forward_generic", st);
         hipLaunchKernelGGL((forward_generic<T, 64>), grid, dim3(kThreads), 0, st, dm,
                            (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
+    }
     return hipGetLastError();
 }
 

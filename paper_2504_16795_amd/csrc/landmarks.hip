@@ -80,12 +80,15 @@ template <typename Tin>
 hipError_t launch_t(const Dims& dm, const void* K, void* Kbar, bool out_bf16, int c0, int c1,
                     hipStream_t st) {
     dim3 grid(c1 - c0, dm.B);
-    if (out_bf16)
+    if (out_bf16) {
+        HSA_TIMED("landmarks_kernel", st);
         hipLaunchKernelGGL((landmarks_kernel<Tin, bf16>), grid, dim3(kThreads), 0, st, dm,
                            (const Tin*)K, (bf16*)Kbar, c0);
-    else
+    } else {
+        HSA_TIMED("landmarks_kernel", st);
         hipLaunchKernelGGL((landmarks_kernel<Tin, float>), grid, dim3(kThreads), 0, st, dm,
                            (const Tin*)K, (float*)Kbar, c0);
+    }
     return hipGetLastError();
 }
 

@@ -1,0 +1,67 @@
+// MFMA building blocks for the bf16 attention kernels (gfx950, wave64).
+//
+// v_mfma_f32_16x16x32_bf16 operand layouts (lane l, i the element within the lane):
+//   A (16 x 32, row-major M x K):  A[m = l % 16][k = 8 (l / 16) + i],  i < 8
+//   B (32 x 16, K x N):            B[k = 8 (l / 16) + i][n = l % 16],  i < 8
+//   C (16 x 16, fp32):             C[m = 4 (l / 16) + i][n = l % 16],  i < 4
+// Every operand is K-contiguous within a lane, so a product over keys needs its key-side
+// operand stored key-contiguous (V^T in LDS).  The C layout of a 32-key pair of M-blocks
+// (keys 4g..4g+3 and 16+4g..16+4g+3 in lane group g = l / 16) is used directly as a
+// K-operand with the matching key permutation on the other operand.
+#pragma once
+
+#include "common.h"
+
+namespace hsa {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));   // 16 raw bytes
+
+__device__ __forceinline__ f32x4_t mfma16(const bf16x8_t& a, const bf16x8_t& b, const f32x4_t& c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4_t zero4() { return f32x4_t{0.f, 0.f, 0.f, 0.f}; }
+
+// round-to-nearest-even fp32 -> bf16 (finite inputs)
+__device__ __forceinline__ __bf16 f2bf(float x) { return (__bf16)x; }
+
+__device__ __forceinline__ bf16x8_t ld_bf16x8(const void* p) {
+    return *reinterpret_cast<const bf16x8_t*>(p);
+}
+__device__ __forceinline__ bf16x4_t ld_bf16x4(const void* p) {
+    return *reinterpret_cast<const bf16x4_t*>(p);
+}
+__device__ __forceinline__ bf16x8_t cat(const bf16x4_t& a, const bf16x4_t& b) {
+    return bf16x8_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+}
+__device__ __forceinline__ bf16x8_t pack8(const f32x4_t& a, const f32x4_t& b, float s) {
+    return bf16x8_t{f2bf(a[0] * s), f2bf(a[1] * s), f2bf(a[2] * s), f2bf(a[3] * s),
+                    f2bf(b[0] * s), f2bf(b[1] * s), f2bf(b[2] * s), f2bf(b[3] * s)};
+}
+
+// A value pair (a, b) of the C layout as a bf16 hi/lo operand pair: hi + lo carries ~16
+// mantissa bits, for products whose fp32 result cancels or accumulates many terms.
+__device__ __forceinline__ void split8(const f32x4_t& a, const f32x4_t& b, bf16x8_t& hi,
+                                       bf16x8_t& lo) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float v = (i < 4) ? a[i] : b[i - 4];
+        hi[i] = f2bf(v);
+        lo[i] = f2bf(v - (float)hi[i]);
+    }
+}
+
+// Logical workgroup id with an XCD-aware order: hardware dispatches consecutive ids to the
+// 8 XCDs round-robin, so consecutive logical ids (same (b, g), neighbouring tiles, sharing
+// chunks through L2) are mapped to the same XCD.  Returns -1 for padding ids.
+__device__ __forceinline__ int xcd_logical_id(int nlogical) {
+    const int id = blockIdx.x;
+    const int per = (nlogical + 7) >> 3;
+    const int lid = (id & 7) * per + (id >> 3);
+    return lid < nlogical ? lid : -1;
+}
+
+}  // namespace hsa

@@ -158,12 +158,15 @@ hipError_t launch_t(const Dims& dm, const void* Q, const float* Kbar, int32_t* i
                     hipStream_t st) {
     const int tq = dm.S < TQ ? dm.S : TQ;
     dim3 grid(cdiv(dm.L, tq), dm.B * dm.G);
-    if (dm.d == 128)
+    if (dm.d == 128) {
+        HSA_TIMED("select_kernel", st);
         hipLaunchKernelGGL((select_kernel<T, 128>), grid, dim3(kThreads), 0, st, dm,
                            (const T*)Q, Kbar, idx, w, tq);
-    else
+    } else {
+        HSA_TIMED("select_kernel", st);
         hipLaunchKernelGGL((select_kernel<T, 64>), grid, dim3(kThreads), 0, st, dm,
                            (const T*)Q, Kbar, idx, w, tq);
+    }
     return hipGetLastError();
 }
 

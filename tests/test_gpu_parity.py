@@ -27,6 +27,8 @@ CASES = {
     "h1_S128_bf16": (Shape(1, 1100, 3, 3, 128, 128, 3, "bf16"), 13, "iid"),
     "k_exceeds_chunks_f32": (Shape(1, 300, 4, 2, 64, 64, 8, "f32"), 14, "iid"),
     "no_candidates_bf16": (Shape(2, 50, 8, 1, 128, 64, 4, "bf16"), 15, "iid"),
+    "ragged_mfma_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 16, "iid"),
+    "wide_k16_bf16": (Shape(1, 2304, 32, 4, 128, 128, 16, "bf16"), 17, "lowrank"),
 }
 
 _cache = {}
