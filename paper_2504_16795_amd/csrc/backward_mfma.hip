@@ -187,9 +187,10 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const uint32_t a = kreg[i][j], c2 = kreg[i + 1][j];
-                *reinterpret_cast<uint32_t*>(&sm.Kt[(col + 2 * j) * VP + r]) =
+                const int d0 = col + 2 * j, d1 = d0 + 1;
+                *reinterpret_cast<uint32_t*>(&sm.Kt[d0 * VP + tpos(d0, r, S)]) =
                     (a & 0xFFFFu) | (c2 << 16);
-                *reinterpret_cast<uint32_t*>(&sm.Kt[(col + 2 * j + 1) * VP + r]) =
+                *reinterpret_cast<uint32_t*>(&sm.Kt[d1 * VP + tpos(d1, r, S)]) =
                     (a >> 16) | (c2 & 0xFFFF0000u);
             }
         }
@@ -220,34 +221,31 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
 
             f32x4_t z[MB], dp[MB];
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                z[mb] = zero4();
-                dp[mb] = zero4();
+            for (int mb = 0; mb < MB; ++mb) z[mb] = dp[mb] = zero4();
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
                     const bf16x8_t ka = ld_bf16x8(&sm.Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
                     z[mb] = mfma16(ka, qB[rb][ks], z[mb]);
                     const bf16x8_t va = ld_bf16x8(&sm.Vs[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
                     dp[mb] = mfma16(va, gB[rb][ks], dp[mb]);
                 }
-            }
             float m = -INFINITY;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-            m = fmaxf(m, __shfl_xor(m, 16, 64));
-            m = fmaxf(m, __shfl_xor(m, 32, 64));
+            m = col_max(m);
             float ssum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    z[mb][i] = exp2f((z[mb][i] - m) * sl2);
+                    z[mb][i] = fast_exp2((z[mb][i] - m) * sl2);
                     ssum += z[mb][i];
                 }
-            ssum += __shfl_xor(ssum, 16, 64);
-            ssum += __shfl_xor(ssum, 32, 64);
+            ssum = col_sum(ssum);
             const float inv = 1.f / ssum;
             float dsum = 0.f;
 #pragma unroll
@@ -257,8 +255,7 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
                     z[mb][i] *= inv;                                  // P
                     dsum = fmaf(z[mb][i], dp[mb][i], dsum);
                 }
-            dsum += __shfl_xor(dsum, 16, 64);
-            dsum += __shfl_xor(dsum, 32, 64);                         // D of this row
+            dsum = col_sum(dsum);                                     // D of this row
             // dZ = w P (dP - D), fed as the B operand of dQ^T += K^T dZ^T.  sum_s dZ_s = 0,
             // so dQ is a cancelling sum: dZ enters as a bf16 pair (hi + lo, ~16 mantissa
             // bits) to keep its rounding from being amplified by the key magnitudes.
@@ -272,8 +269,10 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
                 split8(z[2 * ks2], z[2 * ks2 + 1], zh, zl);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
-                    const __bf16* kr = &sm.Kt[(16 * db + row) * VP + 32 * ks2 + 4 * grp];
-                    const bf16x8_t a = cat(ld_bf16x4(kr), ld_bf16x4(kr + 16));
+                    const int d = 16 * db + row;
+                    const __bf16* kr = &sm.Kt[d * VP];
+                    const bf16x8_t a = cat(ld_bf16x4(kr + tpos(d, 32 * ks2 + 4 * grp, S)),
+                                           ld_bf16x4(kr + tpos(d, 32 * ks2 + 16 + 4 * grp, S)));
                     acc[rb][db] = mfma16(a, zh, acc[rb][db]);
                     acc[rb][db] = mfma16(a, zl, acc[rb][db]);
                 }
@@ -346,8 +345,8 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
 //     dV_sub += (w P)^T dO_rows,  dK_sub += dZ^T Q_rows              (MFMA, K = 32 rows;
 //                                                 w P and dZ as bf16 hi/lo pairs)
 // The C layout of Z feeds the A operand of the last two products directly (row
-// permutation applied to the transposed Q / dO rows in LDS).  dKbar_c = alpha sum ds q~ is
-// a VALU side sum; dK = beta dK_sub + dKbar_c / S.  No atomics; fixed token order.
+// permutation applied to the transposed Q / dO rows in LDS).  The landmark term
+// dKbar_c / S = (alpha / S) sum ds q~ is folded into dZ.  No atomics; fixed token order.
 constexpr int RP = 32 + 8;        // padded row count of the transposed Q / dO group tiles
 constexpr int LISTCAP = 64 * 32 + 4;
 
@@ -358,10 +357,17 @@ struct SmemKV {
     __bf16 Gt[D * RP];
     float lse[32], dd[32];
     float tw[4], tds[4];
-    int ttok[4];
     int list[LISTCAP];
-    float dkb[D];
+    float lw[LISTCAP], lds[LISTCAP];
+    uint8_t lslot[LISTCAP];
     int nlist;
+};
+
+// Registers of one staged group: two rows (same token) of one 8-column block of Q and dO,
+// plus the two rows' statistics (held by the thread that stages column block 0).
+struct GroupRegs {
+    u32x4_t q0, q1, g0, g1;
+    float l0, l1, d0, d1;
 };
 
 template <int S>
@@ -402,10 +408,61 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
     f32x4_t aK[8], aV[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
-    float dkbar = 0.f;                       // thread tid < D owns dKbar[tid]
     if (tid == 0) sm.nlist = 0;
     const float beta = dm.beta;
     const float l2e = 1.44269504088896341f;
+    const float lmk = dm.alpha / (beta * (float)S);
+
+    // staging unit of thread tid < 256: rows sr, sr + 1 (one token), columns scol..scol+7
+    const int sr = (tid >> 4) * 2, scol = (tid & 15) * 8;
+    auto prefetch = [&](int gi, int nl, GroupRegs& R) __attribute__((always_inline)) {
+        R.q0 = R.q1 = R.g0 = R.g1 = u32x4_t{0, 0, 0, 0};
+        R.l0 = R.l1 = R.d0 = R.d1 = 0.f;
+        if (tid >= 256) return;
+        const int li = gi * 4 + (sr >> 3);
+        if (li >= nl) return;
+        const int t = sm.list[li];
+        const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (sr & 7)) * D + scol;
+        R.q0 = *reinterpret_cast<const u32x4_t*>(Q + o);
+        R.q1 = *reinterpret_cast<const u32x4_t*>(Q + o + D);
+        R.g0 = *reinterpret_cast<const u32x4_t*>(dO + o);
+        R.g1 = *reinterpret_cast<const u32x4_t*>(dO + o + D);
+        if (scol == 0) {
+            const size_t so =
+                ((((size_t)b * dm.L + t) * dm.G + g) * k + sm.lslot[li]) * HG + (sr & 7);
+            R.l0 = lse[so];
+            R.l1 = lse[so + 1];
+            R.d0 = dd[so];
+            R.d1 = dd[so + 1];
+        }
+    };
+    auto stage = [&](int gi, int nl, const GroupRegs& R) __attribute__((always_inline)) {
+        if (tid < 4) {
+            const int li = gi * 4 + tid;
+            sm.tw[tid] = li < nl ? sm.lw[li] : 0.f;
+            sm.tds[tid] = li < nl ? sm.lds[li] : 0.f;
+        }
+        if (tid >= 256) return;
+        *reinterpret_cast<u32x4_t*>(&sm.Qr[sr * KP + scol]) = R.q0;
+        *reinterpret_cast<u32x4_t*>(&sm.Qr[(sr + 1) * KP + scol]) = R.q1;
+        *reinterpret_cast<u32x4_t*>(&sm.Gr[sr * KP + scol]) = R.g0;
+        *reinterpret_cast<u32x4_t*>(&sm.Gr[(sr + 1) * KP + scol]) = R.g1;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int sh = (e & 1) ? 16 : 0;
+            const uint32_t qa = (R.q0[e >> 1] >> sh) & 0xFFFFu, qb = (R.q1[e >> 1] >> sh) & 0xFFFFu;
+            const uint32_t ga = (R.g0[e >> 1] >> sh) & 0xFFFFu, gb = (R.g1[e >> 1] >> sh) & 0xFFFFu;
+            const int dd2 = scol + e, pos = tpos(dd2, sr, 32);
+            *reinterpret_cast<uint32_t*>(&sm.Qt[dd2 * RP + pos]) = qa | (qb << 16);
+            *reinterpret_cast<uint32_t*>(&sm.Gt[dd2 * RP + pos]) = ga | (gb << 16);
+        }
+        if (scol == 0) {
+            sm.lse[sr] = R.l0;
+            sm.lse[sr + 1] = R.l1;
+            sm.dd[sr] = R.d0;
+            sm.dd[sr + 1] = R.d1;
+        }
+    };
 
     const uint32_t* bmrow = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
     const int wbeg = ((c + 1) * S) >> 5;
@@ -435,88 +492,54 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
         if (!last_round) last_round = wb + 64 >= nwords;
         __syncthreads();
         const int nl = sm.nlist;
+        // per-token slot, weight and ds of the batch, resolved in parallel
+        for (int li = tid; li < nl; li += NT) {
+            const int t = sm.list[li];
+            const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
+            int slot = 0;
+            for (int s2 = 0; s2 < k; ++s2)
+                if (idx[so + s2] == c) slot = s2;
+            sm.lslot[li] = (uint8_t)slot;
+            sm.lw[li] = w[so + slot];
+            sm.lds[li] = ds[so + slot];
+        }
+        __syncthreads();
         const int ngroups = last_round ? (nl + 3) / 4 : nl / 4;
+        GroupRegs R;
+        if (ngroups > 0) prefetch(0, nl, R);
         for (int gi = 0; gi < ngroups; ++gi) {
-            // ---- stage the group: token info, Q / dO rows (row-major and transposed) -----
-            if (tid < 4) {
-                const int li = gi * 4 + tid;
-                int t = -1, slot = 0;
-                if (li < nl) {
-                    t = sm.list[li];
-                    const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
-                    for (int s2 = 0; s2 < k; ++s2)
-                        if (idx[so + s2] == c) slot = s2;
-                    sm.tw[tid] = w[so + slot];
-                    sm.tds[tid] = ds[so + slot];
-                } else {
-                    sm.tw[tid] = 0.f;
-                    sm.tds[tid] = 0.f;
-                }
-                sm.ttok[tid] = t;
-                // per-row statistics of the token's 8 heads
-                for (int j = 0; j < HG; ++j) {
-                    float lv = 0.f, dv = 0.f;
-                    if (t >= 0) {
-                        const size_t so = ((((size_t)b * dm.L + t) * dm.G + g) * k + slot) * HG + j;
-                        lv = lse[so];
-                        dv = dd[so];
-                    }
-                    sm.lse[tid * 8 + j] = lv;
-                    sm.dd[tid * 8 + j] = dv;
-                }
-            }
+            stage(gi, nl, R);
             __syncthreads();
-            for (int pv = tid; pv < 256; pv += NT) {
-                const int r = (pv >> 4) * 2, col = (pv & 15) * 8;   // rows r, r+1 (same token)
-                const int t = sm.ttok[r >> 3];
-                u32x4_t q0 = {0, 0, 0, 0}, q1 = q0, g0 = q0, g1 = q0;
-                if (t >= 0) {
-                    const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (r & 7)) * D + col;
-                    q0 = *reinterpret_cast<const u32x4_t*>(Q + o);
-                    q1 = *reinterpret_cast<const u32x4_t*>(Q + o + D);
-                    g0 = *reinterpret_cast<const u32x4_t*>(dO + o);
-                    g1 = *reinterpret_cast<const u32x4_t*>(dO + o + D);
-                }
-                *reinterpret_cast<u32x4_t*>(&sm.Qr[r * KP + col]) = q0;
-                *reinterpret_cast<u32x4_t*>(&sm.Qr[(r + 1) * KP + col]) = q1;
-                *reinterpret_cast<u32x4_t*>(&sm.Gr[r * KP + col]) = g0;
-                *reinterpret_cast<u32x4_t*>(&sm.Gr[(r + 1) * KP + col]) = g1;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const int sh = (e & 1) ? 16 : 0;
-                    const uint32_t qa = (q0[e >> 1] >> sh) & 0xFFFFu, qb = (q1[e >> 1] >> sh) & 0xFFFFu;
-                    const uint32_t ga = (g0[e >> 1] >> sh) & 0xFFFFu, gb = (g1[e >> 1] >> sh) & 0xFFFFu;
-                    *reinterpret_cast<uint32_t*>(&sm.Qt[(col + e) * RP + r]) = qa | (qb << 16);
-                    *reinterpret_cast<uint32_t*>(&sm.Gt[(col + e) * RP + r]) = ga | (gb << 16);
-                }
-            }
-            __syncthreads();
+            if (gi + 1 < ngroups) prefetch(gi + 1, nl, R);
 
             // ---- Z, dP for the wave's 16 keys ---------------------------------------------
             f32x4_t z[2], dp[2];
+            z[0] = z[1] = dp[0] = dp[1] = zero4();
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                z[rb] = zero4();
-                dp[rb] = zero4();
+            for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
+                for (int rb = 0; rb < 2; ++rb) {
                     const bf16x8_t qa = ld_bf16x8(&sm.Qr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
                     z[rb] = mfma16(qa, kB[ks], z[rb]);
                     const bf16x8_t ga = ld_bf16x8(&sm.Gr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
                     dp[rb] = mfma16(ga, vB[ks], dp[rb]);
                 }
-            }
-            // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2)
+            // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2).  The landmark term
+            // dKbar_c / S = (alpha / S) sum_rows ds_tok q_row reaches every key of the chunk, so
+            // it is folded into dZ as alpha ds_tok / (beta S) before the dZ^T Q product.
             f32x4_t pw[2], dz[2];
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
-                const float wt = sm.tw[2 * rb + (grp >> 1)];
+                const int tk = 2 * rb + (grp >> 1);
+                const float wt = sm.tw[tk];
+                const float lm = sm.tds[tk] * lmk;
+                const f32x4_t lv = *reinterpret_cast<const f32x4_t*>(&sm.lse[16 * rb + 4 * grp]);
+                const f32x4_t dv = *reinterpret_cast<const f32x4_t*>(&sm.dd[16 * rb + 4 * grp]);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int r = 16 * rb + 4 * grp + i;
-                    const float p = exp2f((beta * z[rb][i] - sm.lse[r]) * l2e);
+                    const float p = fast_exp2((beta * z[rb][i] - lv[i]) * l2e);
                     pw[rb][i] = wt * p;
-                    dz[rb][i] = wt * p * (dp[rb][i] - sm.dd[r]);
+                    dz[rb][i] = wt * p * (dp[rb][i] - dv[i]) + lm;
                 }
             }
             // both products accumulate over every row that selected the chunk (thousands for
@@ -526,22 +549,16 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             split8(dz[0], dz[1], dzh, dzl);
 #pragma unroll
             for (int db = 0; db < 8; ++db) {
-                const __bf16* gr = &sm.Gt[(16 * db + row) * RP + 4 * grp];
-                const bf16x8_t gb = cat(ld_bf16x4(gr), ld_bf16x4(gr + 16));
+                const int d = 16 * db + row;
+                const int p0 = tpos(d, 4 * grp, 32), p1 = tpos(d, 16 + 4 * grp, 32);
+                const __bf16* gr = &sm.Gt[d * RP];
+                const bf16x8_t gb = cat(ld_bf16x4(gr + p0), ld_bf16x4(gr + p1));
                 aV[db] = mfma16(pvh, gb, aV[db]);
                 aV[db] = mfma16(pvl, gb, aV[db]);
-                const __bf16* qr = &sm.Qt[(16 * db + row) * RP + 4 * grp];
-                const bf16x8_t qb = cat(ld_bf16x4(qr), ld_bf16x4(qr + 16));
+                const __bf16* qr = &sm.Qt[d * RP];
+                const bf16x8_t qb = cat(ld_bf16x4(qr + p0), ld_bf16x4(qr + p1));
                 aK[db] = mfma16(dzh, qb, aK[db]);
                 aK[db] = mfma16(dzl, qb, aK[db]);
-            }
-            // landmark term: dKbar += alpha * ds_tok * sum_j q_{tok, j}
-            if (tid < D) {
-                float a = 0.f;
-#pragma unroll
-                for (int r = 0; r < 32; ++r)
-                    a = fmaf(sm.tds[r >> 3], (float)sm.Qt[tid * RP + r], a);
-                dkbar = fmaf(dm.alpha, a, dkbar);
             }
             __syncthreads();
         }
@@ -555,17 +572,13 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             break;
         }
     }
-    if (tid < D) sm.dkb[tid] = dkbar;
-    __syncthreads();
-    const float invS = 1.f / (float)S;
 #pragma unroll
     for (int db = 0; db < 8; ++db) {
         const int d = 16 * db + row;
-        const float kb = sm.dkb[d] * invS;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const size_t o = cbase + (size_t)(16 * wave + 4 * grp + i) * rowstride + d;
-            dK[o] = f2bf(beta * aK[db][i] + kb);
+            dK[o] = f2bf(beta * aK[db][i]);
             dV[o] = f2bf(aV[db][i]);
         }
     }

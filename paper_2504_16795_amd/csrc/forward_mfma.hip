@@ -32,8 +32,8 @@ constexpr int KP = D + 8;        // padded K row (bf16 elements)
 template <int S>
 struct Smem {
     static constexpr int VP = S + 8;                  // padded V^T row (keys)
-    __bf16 Ks[S * KP];
-    __bf16 Vt[D * VP];
+    __bf16 Ks[2][S * KP];             // double-buffered chunk stage
+    __bf16 Vt[2][D * VP];
     int32_t sidx[TQ * KMAX];
     float sw[TQ * KMAX];
     int32_t ulist[TQ * KMAX];
@@ -85,15 +85,15 @@ __device__ __forceinline__ void store_chunk(const u32x4_t (&kreg)[S * D / 8 / kT
         const int p = tid + i * kThreads;
         const int r = (p >> 4) * 2, col = (p & 15) * 8;
         const u32x4_t a = vreg[2 * i], c2 = vreg[2 * i + 1];
-        // columns col + 2j (low halves) and col + 2j + 1 (high halves)
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 0) * VP + r]) = (a.x & 0xFFFFu) | (c2.x << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 1) * VP + r]) = (a.x >> 16) | (c2.x & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 2) * VP + r]) = (a.y & 0xFFFFu) | (c2.y << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 3) * VP + r]) = (a.y >> 16) | (c2.y & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 4) * VP + r]) = (a.z & 0xFFFFu) | (c2.z << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 5) * VP + r]) = (a.z >> 16) | (c2.z & 0xFFFF0000u);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 6) * VP + r]) = (a.w & 0xFFFFu) | (c2.w << 16);
-        *reinterpret_cast<uint32_t*>(&Vt[(col + 7) * VP + r]) = (a.w >> 16) | (c2.w & 0xFFFF0000u);
+        // column col + 2j from the low halves, col + 2j + 1 from the high halves
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int d0 = col + 2 * j, d1 = d0 + 1;
+            *reinterpret_cast<uint32_t*>(&Vt[d0 * VP + tpos(d0, r, S)]) =
+                (a[j] & 0xFFFFu) | (c2[j] << 16);
+            *reinterpret_cast<uint32_t*>(&Vt[d1 * VP + tpos(d1, r, S)]) =
+                (a[j] >> 16) | (c2[j] & 0xFFFF0000u);
+        }
     }
 }
 
@@ -193,16 +193,19 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
     u32x4_t kreg[NPF], vreg[NPF];
 
     const float sl2 = dm.beta * 1.44269504088896341f;   // beta * log2(e)
-    if (nu > 0) load_chunk<S>(kreg, vreg, K, V, bgbase + (size_t)sm.ulist[0] * S * rowstride, rowstride, tid);
+    // Pipeline: chunk u is computed from stage u % 2 while chunk u + 1 (already in registers)
+    // is written to the other stage and chunk u + 2 is being fetched; one barrier per chunk.
+    auto chunk_base = [&](int u) { return bgbase + (size_t)sm.ulist[u] * S * rowstride; };
+    if (nu > 0) {
+        load_chunk<S>(kreg, vreg, K, V, chunk_base(0), rowstride, tid);
+        store_chunk<S>(kreg, vreg, sm.Ks[0], sm.Vt[0], tid);
+    }
+    if (nu > 1) load_chunk<S>(kreg, vreg, K, V, chunk_base(1), rowstride, tid);
+    __syncthreads();
     for (int u = 0; u < nu; ++u) {
         const int c = sm.ulist[u];
-        __syncthreads();                 // every wave is done with the previous chunk
-        store_chunk<S>(kreg, vreg, sm.Ks, sm.Vt, tid);
-        __syncthreads();
-        if (u + 1 < nu)
-            load_chunk<S>(kreg, vreg, K, V, bgbase + (size_t)sm.ulist[u + 1] * S * rowstride,
-                          rowstride, tid);
-
+        const __bf16* Ks = sm.Ks[u & 1];
+        const __bf16* Vt = sm.Vt[u & 1];
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
             const int tau = wave * 4 + rb * 2 + (row >> 3);
@@ -214,32 +217,30 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
             // Z^T = K_c Q^T
             f32x4_t z[MB];
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                z[mb] = zero4();
+            for (int mb = 0; mb < MB; ++mb) z[mb] = zero4();
 #pragma unroll
-                for (int ks = 0; ks < 4; ++ks) {
-                    const bf16x8_t a = ld_bf16x8(&sm.Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    const bf16x8_t a = ld_bf16x8(&Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
                     z[mb] = mfma16(a, qB[rb][ks], z[mb]);
                 }
-            }
             // softmax over the S keys of each row (column `row` of Z^T)
             float m = -INFINITY;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-            m = fmaxf(m, __shfl_xor(m, 16, 64));
-            m = fmaxf(m, __shfl_xor(m, 32, 64));
+            m = col_max(m);
             float ssum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    z[mb][i] = exp2f((z[mb][i] - m) * sl2);
+                    z[mb][i] = fast_exp2((z[mb][i] - m) * sl2);
                     ssum += z[mb][i];
                 }
-            ssum += __shfl_xor(ssum, 16, 64);
-            ssum += __shfl_xor(ssum, 32, 64);
+            ssum = col_sum(ssum);
             const float scale = wl / ssum;
             // O^T += V^T P^T
 #pragma unroll
@@ -247,12 +248,17 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
                 const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
-                    const __bf16* vr = &sm.Vt[(16 * db + row) * VP + 32 * ks2 + 4 * grp];
-                    const bf16x8_t a = cat(ld_bf16x4(vr), ld_bf16x4(vr + 16));
+                    const int d = 16 * db + row;
+                    const __bf16* vr = &Vt[d * VP];
+                    const bf16x8_t a = cat(ld_bf16x4(vr + tpos(d, 32 * ks2 + 4 * grp, S)),
+                                           ld_bf16x4(vr + tpos(d, 32 * ks2 + 16 + 4 * grp, S)));
                     acc[rb][db] = mfma16(a, pb, acc[rb][db]);
                 }
             }
         }
+        if (u + 1 < nu) store_chunk<S>(kreg, vreg, sm.Ks[(u + 1) & 1], sm.Vt[(u + 1) & 1], tid);
+        __syncthreads();
+        if (u + 2 < nu) load_chunk<S>(kreg, vreg, K, V, chunk_base(u + 2), rowstride, tid);
     }
 
     // ---- output: O^T C layout -> O[b, t, g*8 + j, d] ----------------------------------

@@ -42,6 +42,38 @@ __device__ __forceinline__ bf16x8_t pack8(const f32x4_t& a, const f32x4_t& b, fl
                     f2bf(b[0] * s), f2bf(b[1] * s), f2bf(b[2] * s), f2bf(b[3] * s)};
 }
 
+// Reductions over the four lanes l, l^16, l^32, l^48 that hold one column of a C layout,
+// with the gfx950 lane-swap instructions (no LDS traffic): a swap of v with itself returns
+// (v[l], v[partner]) in some order, so the pair sum / max is order-free.
+__device__ __forceinline__ float pair16_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair32_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair16_max(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair32_max(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float col_sum(float v) { return pair32_sum(pair16_sum(v)); }
+__device__ __forceinline__ float col_max(float v) { return pair32_max(pair16_max(v)); }
+
+// 2^x on the hardware exponential (inputs here are <= 0; results below 2^-126 flush to 0,
+// which is exact enough for softmax probabilities)
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Transposed LDS tiles T[d][n] (n keys or rows per d-row, n a power of two >= 32) store
+// entry (d, s) at position tpos(d, s, n): a rotation by 8 (d / 16).  Staging threads that
+// cover 16 consecutive column blocks of a few rows then write 64 distinct banks, and every
+// 4-aligned group of 4 entries stays contiguous (8-byte reads), rotated as a unit.
+__device__ __forceinline__ int tpos(int d, int s, int n) { return (s + 8 * (d >> 4)) & (n - 1); }
+
 // A value pair (a, b) of the C layout as a bf16 hi/lo operand pair: hi + lo carries ~16
 // mantissa bits, for products whose fp32 result cancels or accumulates many terms.
 __device__ __forceinline__ void split8(const f32x4_t& a, const f32x4_t& b, bf16x8_t& hi,
