@@ -41,7 +41,8 @@
  *   - Supported by the kernels: 1 <= h <= 16, d in {64, 128}, S in {16, 32, 64, 128},
  *     1 <= k <= 32, S * d <= 8192 for F32, L >= 0 (L need not be a multiple of S; a
  *     trailing partial chunk is never a candidate), pointers 16-byte aligned.  Inputs
- *     must be finite.  idx entries outside [0, floor(t/S)) are treated as empty slots.
+ *     must be finite.  idx entries outside [0, floor(t/S)) are treated as empty slots;
+ *     the valid entries of one token must be distinct (hsa_select_topk's are).
  */
 #ifndef HSA_MI355X_H
 #define HSA_MI355X_H

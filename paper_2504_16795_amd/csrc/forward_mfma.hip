@@ -1,14 +1,16 @@
 // bf16 MFMA forward of hierarchical sparse attention (Sec. 3.1.1), for h = 8 query heads
 // per KV head, d = 128, S in {64, 128}.
 //
-// Workgroup = (b, g, tile of 32 tokens inside one query chunk), 8 waves; wave w owns tokens
-// 4w..4w+3 as two row blocks of 16 rows (2 tokens x 8 heads).
-//  1. The tile's selections are deduplicated into a union list of chunks.
-//  2. Each union chunk is staged once in LDS: K row-major [S][d], V transposed [d][S]
-//     (the next chunk's global loads are in flight while the current one is computed).
-//  3. Per row block whose tokens selected the chunk (a wave-uniform test), the wave runs
+// Workgroup = (b, g, tile of 32 tokens inside one query chunk), 16 waves; wave w owns
+// tokens 2w, 2w+1 as one row block of 16 rows (2 tokens x 8 heads).
+//  1. Each token's valid selections are sorted by descending chunk; the tile's union is
+//     marked in an LDS bitmap over the candidates and listed in descending chunk order, so
+//     every lane follows its token's slot list with a register pointer.
+//  2. Each union chunk is staged once in LDS (double-buffered): K row-major [S][d], V
+//     transposed [d][S]; the next chunk's global loads are in flight meanwhile.
+//  3. A wave whose tokens selected the chunk (wave-uniform test) runs
 //        Z^T [S x 16] = K_c [S x d] . Q^T [d x 16]        (S/16 * 4 MFMAs)
-//        P^T = softmax over keys, scaled by w_{t,c} (0 for rows that did not select c)
+//        P^T = softmax over keys, scaled by w_{t,c} (0 for the row block's other token)
 //        O^T [d x 16] += V_c^T [d x S] . P^T [S x 16]     (8 * S/32 MFMAs)
 //     The C layout of Z^T feeds P^T straight into the B operand of the second product with
 //     a key permutation applied to the V^T reads.  Q^T lives in registers for the whole
@@ -23,76 +25,81 @@ namespace {
 
 constexpr int D = 128;
 constexpr int HG = 8;            // query heads per KV head
-constexpr int NW = 8;            // waves per workgroup
+constexpr int NW = 16;           // waves per workgroup
 constexpr int kThreads = NW * 64;
-constexpr int TQ = 32;           // tokens per tile
+constexpr int TQ = 32;           // tokens per tile (2 per wave)
 constexpr int KMAX = 32;
 constexpr int KP = D + 8;        // padded K row (bf16 elements)
+constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
 template <int S>
 struct Smem {
-    static constexpr int VP = S + 8;                  // padded V^T row (keys)
-    __bf16 Ks[2][S * KP];             // double-buffered chunk stage
+    static constexpr int VP = S + 8;              // padded V^T row (keys)
+    __bf16 Ks[2][S * KP];                         // double-buffered chunk stage
     __bf16 Vt[2][D * VP];
-    int32_t sidx[TQ * KMAX];
+    int32_t sidx[TQ * KMAX];                      // per token: valid chunks, descending, -1 pad
     float sw[TQ * KMAX];
-    int32_t ulist[TQ * KMAX];
-    uint8_t flag[TQ * KMAX];
+    uint32_t ubits[UWORDS];
+    int32_t ulist[TQ * KMAX];                     // union, descending chunk order
+    int wsum[NW];
     int nu;
 };
 
-// Staging of one chunk: global -> registers (load_chunk) and registers -> LDS (store_chunk).
-// K: vector v (16 bytes) = key v / 16, columns 8 (v % 16) .. +7, stored row-major.
-// V: vector pair p = keys 2 (p / 16) and 2 (p / 16) + 1, columns 8 (p % 16) .. +7, stored
-//    transposed as 8 packed key pairs.
+// Staging of one chunk: K vectors (key v / 16, columns 8 (v % 16) .. +7) go row-major to
+// LDS; V vector pairs (keys 2 (p / 16), 2 (p / 16) + 1, same columns) go transposed as
+// packed key pairs.
 template <int S>
-__device__ __forceinline__ void load_chunk(u32x4_t (&kreg)[S * D / 8 / kThreads],
-                                           u32x4_t (&vreg)[S * D / 8 / kThreads],
-                                           const __bf16* __restrict__ K,
+struct Stage {
+    static constexpr int NK = S * D / 8 / kThreads;                      // K vectors / thread
+    static constexpr int NV = (S * D / 16 + kThreads - 1) / kThreads;    // V pairs / thread
+    u32x4_t k[NK];
+    u32x4_t v[2 * NV];
+};
+
+template <int S>
+__device__ __forceinline__ void load_chunk(Stage<S>& st, const __bf16* __restrict__ K,
                                            const __bf16* __restrict__ V, size_t base,
                                            size_t rowstride, int tid) {
-    constexpr int NPF = S * D / 8 / kThreads;
 #pragma unroll
-    for (int i = 0; i < NPF; ++i) {
+    for (int i = 0; i < Stage<S>::NK; ++i) {
         const int v = tid + i * kThreads;
-        const int r = v >> 4, col = (v & 15) * 8;
-        kreg[i] = *reinterpret_cast<const u32x4_t*>(K + base + (size_t)r * rowstride + col);
+        st.k[i] = *reinterpret_cast<const u32x4_t*>(K + base + (size_t)(v >> 4) * rowstride +
+                                                    (v & 15) * 8);
     }
 #pragma unroll
-    for (int i = 0; i < NPF / 2; ++i) {
+    for (int i = 0; i < Stage<S>::NV; ++i) {
         const int p = tid + i * kThreads;
-        const int r = (p >> 4) * 2, col = (p & 15) * 8;
-        vreg[2 * i] = *reinterpret_cast<const u32x4_t*>(V + base + (size_t)r * rowstride + col);
-        vreg[2 * i + 1] =
-            *reinterpret_cast<const u32x4_t*>(V + base + (size_t)(r + 1) * rowstride + col);
+        if (p < S * 8) {
+            const size_t o = base + (size_t)((p >> 4) * 2) * rowstride + (p & 15) * 8;
+            st.v[2 * i] = *reinterpret_cast<const u32x4_t*>(V + o);
+            st.v[2 * i + 1] = *reinterpret_cast<const u32x4_t*>(V + o + rowstride);
+        }
     }
 }
 
 template <int S>
-__device__ __forceinline__ void store_chunk(const u32x4_t (&kreg)[S * D / 8 / kThreads],
-                                            const u32x4_t (&vreg)[S * D / 8 / kThreads],
-                                            __bf16* Ks, __bf16* Vt, int tid) {
-    constexpr int NPF = S * D / 8 / kThreads;
+__device__ __forceinline__ void store_chunk(const Stage<S>& st, __bf16* Ks, __bf16* Vt,
+                                            int tid) {
     constexpr int VP = S + 8;
 #pragma unroll
-    for (int i = 0; i < NPF; ++i) {
+    for (int i = 0; i < Stage<S>::NK; ++i) {
         const int v = tid + i * kThreads;
-        const int r = v >> 4, col = (v & 15) * 8;
-        *reinterpret_cast<u32x4_t*>(&Ks[r * KP + col]) = kreg[i];
+        *reinterpret_cast<u32x4_t*>(&Ks[(v >> 4) * KP + (v & 15) * 8]) = st.k[i];
     }
 #pragma unroll
-    for (int i = 0; i < NPF / 2; ++i) {
+    for (int i = 0; i < Stage<S>::NV; ++i) {
         const int p = tid + i * kThreads;
-        const int r = (p >> 4) * 2, col = (p & 15) * 8;
-        const u32x4_t a = vreg[2 * i], c2 = vreg[2 * i + 1];
-        // column col + 2j from the low halves, col + 2j + 1 from the high halves
+        if (p < S * 8) {
+            const int r = (p >> 4) * 2, col = (p & 15) * 8;
+            const u32x4_t a = st.v[2 * i], c2 = st.v[2 * i + 1];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d0 = col + 2 * j, d1 = d0 + 1;
-            *reinterpret_cast<uint32_t*>(&Vt[d0 * VP + tpos(d0, r, S)]) =
-                (a[j] & 0xFFFFu) | (c2[j] << 16);
-            *reinterpret_cast<uint32_t*>(&Vt[d1 * VP + tpos(d1, r, S)]) =
-                (a[j] >> 16) | (c2[j] & 0xFFFF0000u);
+            for (int j = 0; j < 4; ++j) {
+                const int d0 = col + 2 * j, d1 = d0 + 1;
+                *reinterpret_cast<uint32_t*>(&Vt[d0 * VP + tpos(d0, r, S)]) =
+                    (a[j] & 0xFFFFu) | (c2[j] << 16);
+                *reinterpret_cast<uint32_t*>(&Vt[d1 * VP + tpos(d1, r, S)]) =
+                    (a[j] >> 16) | (c2[j] & 0xFFFF0000u);
+            }
         }
     }
 }
@@ -105,7 +112,6 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
     constexpr int VP = Smem<S>::VP;
     constexpr int MB = S / 16;            // key blocks of Z^T
     constexpr int KS2 = S / 32;           // key steps of P V
-    constexpr int NPF = S * D / 8 / kThreads;   // 16-byte K vectors per thread per chunk
     __shared__ Smem<S> sm;
 
     const int lid = xcd_logical_id(ntiles * dm.B * dm.G);
@@ -117,103 +123,121 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
     const int t0 = tile * TQ;
     const int ncand = t0 / S;
     const int row = lane & 15, grp = lane >> 4;
+    const int nwd = (ncand + 31) >> 5;
 
-    // ---- selections of the tile and their union -------------------------------------
-    const int ne = TQ * k;
-    for (int e = tid; e < ne; e += kThreads) {
-        const int tau = e / k, t = t0 + tau;
-        int c = -1;
-        float wt = 0.f;
+    // ---- selections: valid entries of each token, descending chunk order -----------------
+    if (tid < TQ) {
+        const int t = t0 + tid;
+        int* cs = &sm.sidx[tid * k];
+        float* ws = &sm.sw[tid * k];
+        int n = 0;
         if (t < dm.L) {
-            const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k + e % k;
-            c = idx[o];
-            wt = w[o];
-            if (c < 0 || c >= ncand) {
-                c = -1;
-                wt = 0.f;
+            const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
+            for (int s = 0; s < k; ++s) {
+                const int c = idx[o + s];
+                if (c < 0 || c >= ncand) continue;
+                const float wv = w[o + s];
+                int e = 0;
+                while (e < n && cs[e] != c) ++e;
+                if (e < n) {                          // repeated chunk: weights add
+                    ws[e] += wv;
+                    continue;
+                }
+                int j = n++;
+                while (j > 0 && cs[j - 1] < c) {      // insertion: descending chunk index
+                    cs[j] = cs[j - 1];
+                    ws[j] = ws[j - 1];
+                    --j;
+                }
+                cs[j] = c;
+                ws[j] = wv;
             }
         }
-        sm.sidx[e] = c;
-        sm.sw[e] = wt;
+        for (int s = n; s < k; ++s) {
+            cs[s] = -1;
+            ws[s] = 0.f;
+        }
     }
+    for (int i = tid; i < nwd; i += kThreads) sm.ubits[i] = 0u;
     __syncthreads();
-    for (int e = tid; e < ne; e += kThreads) {
+    for (int e = tid; e < TQ * k; e += kThreads) {
         const int c = sm.sidx[e];
-        bool first = c >= 0;
-        for (int e2 = 0; e2 < e && first; ++e2) first = sm.sidx[e2] != c;
-        sm.flag[e] = first ? 1 : 0;
+        if (c >= 0) atomicOr(&sm.ubits[c >> 5], 1u << (c & 31));
     }
     __syncthreads();
-    if (wave == 0) {
-        const int per = (ne + 63) / 64;
-        const int e0 = lane * per, e1 = min(ne, e0 + per);
-        int cnt = 0;
-        for (int e = e0; e < e1; ++e) cnt += sm.flag[e];
+    // union in descending chunk order: thread i takes word nwd - 1 - i
+    {
+        const int wi = nwd - 1 - tid;
+        const uint32_t word = (tid < nwd) ? sm.ubits[wi] : 0u;
+        const int cnt = __popc(word);
         int incl = cnt;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
             const int v = __shfl_up(incl, o, 64);
             if (lane >= o) incl += v;
         }
-        int pos = incl - cnt;
-        for (int e = e0; e < e1; ++e)
-            if (sm.flag[e]) sm.ulist[pos++] = sm.sidx[e];
-        if (lane == 63) sm.nu = incl;
+        if (lane == 63) sm.wsum[wave] = incl;
+        __syncthreads();
+        int base = 0;
+        for (int i = 0; i < wave; ++i) base += sm.wsum[i];
+        int pos = base + incl - cnt;
+        uint32_t x = word;
+        while (x) {
+            const int bit = 31 - __clz(x);
+            sm.ulist[pos++] = wi * 32 + bit;
+            x &= ~(1u << bit);
+        }
+        if (tid == kThreads - 1) {
+            int tot = 0;
+            for (int i = 0; i < NW; ++i) tot += sm.wsum[i];
+            sm.nu = tot;
+        }
     }
 
-    // ---- Q^T operands of the wave's two row blocks (registers, whole kernel) ------------
-    bf16x8_t qB[2][4];
-    f32x4_t acc[2][8];
+    // ---- Q^T operand of the wave's row block (registers, whole kernel) -------------------
+    const int tau = wave * 2 + (row >> 3);
+    const int t_row = t0 + tau;
+    bf16x8_t qB[4];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        const int tau = wave * 4 + rb * 2 + (row >> 3);
-        const int t = t0 + tau;
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if (t < dm.L) {
-                const size_t qo = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D +
-                                  32 * ks + 8 * grp;
-                qB[rb][ks] = ld_bf16x8(Q + qo);
-            } else {
-                qB[rb][ks] = bf16x8_t{};
-            }
+    for (int ks = 0; ks < 4; ++ks) {
+        if (t_row < dm.L) {
+            const size_t qo = (((size_t)b * dm.L + t_row) * dm.H + (size_t)g * HG + (row & 7)) * D +
+                              32 * ks + 8 * grp;
+            qB[ks] = ld_bf16x8(Q + qo);
+        } else {
+            qB[ks] = bf16x8_t{};
         }
-#pragma unroll
-        for (int db = 0; db < 8; ++db) acc[rb][db] = zero4();
     }
+    f32x4_t acc[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) acc[db] = zero4();
     __syncthreads();
     const int nu = sm.nu;
+    // this lane's token: next selected chunk and its weight
+    int sp = 0;
+    int cur_c = sm.sidx[tau * k];
+    float cur_w = sm.sw[tau * k];
 
-    // ---- staging of one chunk: global -> registers -> LDS -----------------------------
-    // K: vector v (16 bytes) = row v / 16, columns 8 (v % 16) .. +7.
-    // V: vector pair p = (keys 2 (p / 16), 2 (p / 16) + 1; columns 8 (p % 16) .. +7),
-    //    written to V^T as 8 packed key pairs.
-    const size_t rowstride = (size_t)dm.G * D;          // elements between token rows
+    const size_t rowstride = (size_t)dm.G * D;
     const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
-    u32x4_t kreg[NPF], vreg[NPF];
-
-    const float sl2 = dm.beta * 1.44269504088896341f;   // beta * log2(e)
+    Stage<S> st;
     // Pipeline: chunk u is computed from stage u % 2 while chunk u + 1 (already in registers)
     // is written to the other stage and chunk u + 2 is being fetched; one barrier per chunk.
-    auto chunk_base = [&](int u) { return bgbase + (size_t)sm.ulist[u] * S * rowstride; };
     if (nu > 0) {
-        load_chunk<S>(kreg, vreg, K, V, chunk_base(0), rowstride, tid);
-        store_chunk<S>(kreg, vreg, sm.Ks[0], sm.Vt[0], tid);
+        load_chunk<S>(st, K, V, bgbase + (size_t)sm.ulist[0] * S * rowstride, rowstride, tid);
+        store_chunk<S>(st, sm.Ks[0], sm.Vt[0], tid);
     }
-    if (nu > 1) load_chunk<S>(kreg, vreg, K, V, chunk_base(1), rowstride, tid);
+    if (nu > 1)
+        load_chunk<S>(st, K, V, bgbase + (size_t)sm.ulist[1] * S * rowstride, rowstride, tid);
     __syncthreads();
+    const float sl2 = dm.beta * 1.44269504088896341f;   // beta * log2(e)
     for (int u = 0; u < nu; ++u) {
         const int c = sm.ulist[u];
-        const __bf16* Ks = sm.Ks[u & 1];
-        const __bf16* Vt = sm.Vt[u & 1];
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            const int tau = wave * 4 + rb * 2 + (row >> 3);
-            float wl = 0.f;
-            for (int s = 0; s < k; ++s)
-                if (sm.sidx[tau * k + s] == c) wl = sm.sw[tau * k + s];
-            if (__ballot(wl != 0.f) == 0) continue;
-
+        const bool mine = (cur_c == c);
+        if (__ballot(mine) != 0) {
+            const __bf16* Ks = sm.Ks[u & 1];
+            const __bf16* Vt = sm.Vt[u & 1];
+            const float wl = mine ? cur_w : 0.f;
             // Z^T = K_c Q^T
             f32x4_t z[MB];
 #pragma unroll
@@ -223,7 +247,7 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
                     const bf16x8_t a = ld_bf16x8(&Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
-                    z[mb] = mfma16(a, qB[rb][ks], z[mb]);
+                    z[mb] = mfma16(a, qB[ks], z[mb]);
                 }
             // softmax over the S keys of each row (column `row` of Z^T)
             float m = -INFINITY;
@@ -252,26 +276,29 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
                     const __bf16* vr = &Vt[d * VP];
                     const bf16x8_t a = cat(ld_bf16x4(vr + tpos(d, 32 * ks2 + 4 * grp, S)),
                                            ld_bf16x4(vr + tpos(d, 32 * ks2 + 16 + 4 * grp, S)));
-                    acc[rb][db] = mfma16(a, pb, acc[rb][db]);
+                    acc[db] = mfma16(a, pb, acc[db]);
                 }
             }
+            if (mine) {
+                ++sp;
+                cur_c = sp < k ? sm.sidx[tau * k + sp] : -1;
+                cur_w = sp < k ? sm.sw[tau * k + sp] : 0.f;
+            }
         }
-        if (u + 1 < nu) store_chunk<S>(kreg, vreg, sm.Ks[(u + 1) & 1], sm.Vt[(u + 1) & 1], tid);
+        if (u + 1 < nu) store_chunk<S>(st, sm.Ks[(u + 1) & 1], sm.Vt[(u + 1) & 1], tid);
         __syncthreads();
-        if (u + 2 < nu) load_chunk<S>(kreg, vreg, K, V, chunk_base(u + 2), rowstride, tid);
+        if (u + 2 < nu)
+            load_chunk<S>(st, K, V, bgbase + (size_t)sm.ulist[u + 2] * S * rowstride, rowstride,
+                          tid);
     }
 
     // ---- output: O^T C layout -> O[b, t, g*8 + j, d] ----------------------------------
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        const int tau = wave * 4 + rb * 2 + (row >> 3);
-        const int t = t0 + tau;
-        if (t >= dm.L) continue;
-        __bf16* op = O + (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D;
+    if (t_row < dm.L) {
+        __bf16* op = O + (((size_t)b * dm.L + t_row) * dm.H + (size_t)g * HG + (row & 7)) * D;
 #pragma unroll
         for (int db = 0; db < 8; ++db) {
-            const bf16x4_t o4{f2bf(acc[rb][db][0]), f2bf(acc[rb][db][1]), f2bf(acc[rb][db][2]),
-                              f2bf(acc[rb][db][3])};
+            const bf16x4_t o4{f2bf(acc[db][0]), f2bf(acc[db][1]), f2bf(acc[db][2]),
+                              f2bf(acc[db][3])};
             *reinterpret_cast<bf16x4_t*>(op + 16 * db + 4 * grp) = o4;
         }
     }
@@ -281,7 +308,7 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
 
 bool forward_mfma_supported(const Dims& dm, bool in_bf16) {
     return in_bf16 && dm.h == HG && dm.d == D && (dm.S == 64 || dm.S == 128) && dm.k <= KMAX &&
-           !getenv("HSA_FORCE_GENERIC");
+           dm.C <= UWORDS * 32 && !getenv("HSA_FORCE_GENERIC");
 }
 
 hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
