@@ -1,9 +1,10 @@
 // bf16 MFMA backward of hierarchical sparse attention (Sec. 3.1.2, two-phase backward),
 // for h = 8 query heads per KV head, d = 128, S in {64, 128}.
 //
-// Query pass (bwd_q_mfma): same tiling as the forward (32-token tile inside one query
-// chunk, union of the tile's chunks staged once in LDS, wave = two row blocks of 16 rows).
-// Per active row block and chunk:
+// Query pass (bwd_q_mfma): the forward's tiling (a tile of 2 NW tokens inside one query
+// chunk, wave w owning tokens 2w, 2w+1 as one row block of 16 rows; the tile's union of
+// chunks listed in descending order and staged once in LDS, each lane following its
+// token's descending slot list with a pointer).  Per chunk selected by the row block:
 //     Z^T  = K_c Q^T,  dP^T = V_c dO^T                     (keys x rows, MFMA)
 //     P    = softmax over keys;  D_row = sum_keys P dP      (= dO_row . O_{row,c})
 //     dZ^T = w P (dP - D)
@@ -29,11 +30,9 @@ namespace {
 
 constexpr int D = 128;
 constexpr int HG = 8;
-constexpr int NW = 8;
-constexpr int kThreads = NW * 64;
-constexpr int TQ = 32;
 constexpr int KMAX = 32;
 constexpr int KP = D + 8;
+constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -53,32 +52,110 @@ __host__ __device__ inline WsLayout ws_layout(const Dims& dm) {
     return l;
 }
 
+// Query-pass shape: S = 64 runs 16 waves with two chunk stages in LDS; S = 128 (twice the
+// stage and twice the Z / dP registers per row block) runs 8 waves with one stage.
 template <int S>
-struct SmemQ {
-    static constexpr int VP = S + 8;
-    __bf16 Ks[S * KP];
-    __bf16 Vs[S * KP];
-    __bf16 Kt[D * VP];
-    int32_t sidx[TQ * KMAX];
-    float sw[TQ * KMAX];
-    float dw[TQ * KMAX];
-    int32_t ulist[TQ * KMAX];
-    uint8_t flag[TQ * KMAX];
-    int nu;
+struct QCfg;
+template <>
+struct QCfg<64> {
+    static constexpr int NW = 8, NBUF = 2;
+};
+template <>
+struct QCfg<128> {
+    static constexpr int NW = 8, NBUF = 1;
 };
 
 template <int S>
-__global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
+struct SmemQ {
+    static constexpr int NW = QCfg<S>::NW, NBUF = QCfg<S>::NBUF, TQ = 2 * NW;
+    static constexpr int VP = S + 8;
+    __bf16 Ks[NBUF][S * KP];
+    __bf16 Vs[NBUF][S * KP];
+    __bf16 Kt[NBUF][D * VP];
+    int32_t sidx[TQ * KMAX];      // per token: valid chunks in descending order, -1 pad
+    uint8_t sslot[TQ * KMAX];     // ... and their slot numbers
+    int32_t oidx[TQ * KMAX];      // per token and slot: the chunk, -1 if not a valid entry
+    float ow[TQ * KMAX];
+    float dw[TQ * KMAX];
+    uint32_t ubits[UWORDS];
+    int32_t ulist[TQ * KMAX];     // union, descending chunk order
+    int wsum[NW];
+    int nu;
+};
+
+// Staging of one chunk by NT threads in units of vector pairs (rows 2 (p / 16), +1,
+// columns 8 (p % 16)..+7): units [0, 8S) are K pairs, [8S, 16S) V pairs.  K and V go to
+// LDS row-major, K pairs also transposed (key pairs packed) into K^T.
+template <int S>
+struct StageQ {
+    static constexpr int NT = QCfg<S>::NW * 64;
+    static constexpr int NP = S * 8;
+    static constexpr int NU = (2 * NP + NT - 1) / NT;
+    u32x4_t r[2 * NU];
+};
+
+template <int S>
+__device__ __forceinline__ void q_load(StageQ<S>& st, const __bf16* __restrict__ K,
+                                       const __bf16* __restrict__ V, size_t base,
+                                       size_t rowstride, int tid) {
+    using T = StageQ<S>;
+#pragma unroll
+    for (int i = 0; i < T::NU; ++i) {
+        const int u = tid + i * T::NT;
+        if (u < 2 * T::NP) {
+            const bool isk = u < T::NP;
+            const int p = isk ? u : u - T::NP;
+            const __bf16* src = (isk ? K : V) + base + (size_t)((p >> 4) * 2) * rowstride +
+                                (p & 15) * 8;
+            st.r[2 * i] = *reinterpret_cast<const u32x4_t*>(src);
+            st.r[2 * i + 1] = *reinterpret_cast<const u32x4_t*>(src + rowstride);
+        }
+    }
+}
+
+template <int S>
+__device__ __forceinline__ void q_store(const StageQ<S>& st, __bf16* Ks, __bf16* Vs,
+                                        __bf16* Kt, int tid) {
+    using T = StageQ<S>;
+    constexpr int VP = S + 8;
+#pragma unroll
+    for (int i = 0; i < T::NU; ++i) {
+        const int u = tid + i * T::NT;
+        if (u < 2 * T::NP) {
+            const bool isk = u < T::NP;
+            const int p = isk ? u : u - T::NP;
+            const int r = (p >> 4) * 2, col = (p & 15) * 8;
+            __bf16* dst = isk ? Ks : Vs;
+            *reinterpret_cast<u32x4_t*>(&dst[r * KP + col]) = st.r[2 * i];
+            *reinterpret_cast<u32x4_t*>(&dst[(r + 1) * KP + col]) = st.r[2 * i + 1];
+            if (isk) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t a = st.r[2 * i][j], c2 = st.r[2 * i + 1][j];
+                    const int d0 = col + 2 * j, d1 = d0 + 1;
+                    *reinterpret_cast<uint32_t*>(&Kt[d0 * VP + tpos(d0, r, S)]) =
+                        (a & 0xFFFFu) | (c2 << 16);
+                    *reinterpret_cast<uint32_t*>(&Kt[d1 * VP + tpos(d1, r, S)]) =
+                        (a >> 16) | (c2 & 0xFFFF0000u);
+                }
+            }
+        }
+    }
+}
+
+template <int S>
+__global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const float* __restrict__ Kbar,
     const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, __bf16* __restrict__ dQ, float* __restrict__ ds_out,
     float* __restrict__ lse_out, float* __restrict__ d_out, int ntiles) {
-    constexpr int VP = SmemQ<S>::VP;
+    using SM = SmemQ<S>;
+    constexpr int NW = SM::NW, NT = NW * 64, TQ = SM::TQ, NBUF = SM::NBUF;
+    constexpr int VP = SM::VP;
     constexpr int MB = S / 16;
     constexpr int KS2 = S / 32;
-    constexpr int NPF = S * D / 8 / kThreads;
-    __shared__ SmemQ<S> sm;
+    __shared__ SM sm;
 
     const int lid = xcd_logical_id(ntiles * dm.B * dm.G);
     if (lid < 0) return;
@@ -89,136 +166,141 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
     const int t0 = tile * TQ;
     const int ncand = t0 / S;
     const int row = lane & 15, grp = lane >> 4;
+    const int nwd = (ncand + 31) >> 5;
 
-    // ---- selections of the tile and their union -------------------------------------
-    const int ne = TQ * k;
-    for (int e = tid; e < ne; e += kThreads) {
-        const int tau = e / k, t = t0 + tau;
-        int c = -1;
-        float wt = 0.f;
-        if (t < dm.L) {
-            const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k + e % k;
-            c = idx[o];
-            wt = w[o];
-            if (c < 0 || c >= ncand) {
-                c = -1;
-                wt = 0.f;
+    // ---- selections: per slot as given, and the valid ones sorted by descending chunk ----
+    if (tid < TQ) {
+        const int t = t0 + tid;
+        int* cs = &sm.sidx[tid * k];
+        uint8_t* sl = &sm.sslot[tid * k];
+        int n = 0;
+        for (int s = 0; s < k; ++s) {
+            int c = -1;
+            float wv = 0.f;
+            if (t < dm.L) {
+                const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k + s;
+                c = idx[o];
+                wv = w[o];
+                if (c < 0 || c >= ncand) {
+                    c = -1;
+                    wv = 0.f;
+                }
             }
+            sm.oidx[tid * k + s] = c;
+            sm.ow[tid * k + s] = wv;
+            sm.dw[tid * k + s] = 0.f;
+            if (c < 0) continue;
+            int j = n++;
+            while (j > 0 && cs[j - 1] < c) {
+                cs[j] = cs[j - 1];
+                sl[j] = sl[j - 1];
+                --j;
+            }
+            cs[j] = c;
+            sl[j] = (uint8_t)s;
         }
-        sm.sidx[e] = c;
-        sm.sw[e] = wt;
-        sm.dw[e] = 0.f;
+        for (int s = n; s < k; ++s) {
+            cs[s] = -1;
+            sl[s] = 0;
+        }
     }
+    for (int i = tid; i < nwd; i += NT) sm.ubits[i] = 0u;
     __syncthreads();
-    for (int e = tid; e < ne; e += kThreads) {
+    for (int e = tid; e < TQ * k; e += NT) {
         const int c = sm.sidx[e];
-        bool first = c >= 0;
-        for (int e2 = 0; e2 < e && first; ++e2) first = sm.sidx[e2] != c;
-        sm.flag[e] = first ? 1 : 0;
+        if (c >= 0) atomicOr(&sm.ubits[c >> 5], 1u << (c & 31));
     }
     __syncthreads();
-    if (wave == 0) {
-        const int per = (ne + 63) / 64;
-        const int e0 = lane * per, e1 = min(ne, e0 + per);
-        int cnt = 0;
-        for (int e = e0; e < e1; ++e) cnt += sm.flag[e];
+    // union in descending chunk order: thread i takes word nwd - 1 - i
+    for (int w0 = 0; w0 < nwd; w0 += NT) {
+        const int wi = nwd - 1 - (w0 + tid);
+        const uint32_t word = (wi >= 0) ? sm.ubits[wi] : 0u;
+        const int cnt = __popc(word);
         int incl = cnt;
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
             const int v = __shfl_up(incl, o, 64);
             if (lane >= o) incl += v;
         }
-        int pos = incl - cnt;
-        for (int e = e0; e < e1; ++e)
-            if (sm.flag[e]) sm.ulist[pos++] = sm.sidx[e];
-        if (lane == 63) sm.nu = incl;
-    }
-
-    // ---- Q^T and dO^T operands of the wave's row blocks -------------------------------
-    bf16x8_t qB[2][4], gB[2][4];
-    f32x4_t acc[2][8];
-#pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        const int t = t0 + wave * 4 + rb * 2 + (row >> 3);
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            if (t < dm.L) {
-                const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D +
-                                 32 * ks + 8 * grp;
-                qB[rb][ks] = ld_bf16x8(Q + o);
-                gB[rb][ks] = ld_bf16x8(dO + o);
-            } else {
-                qB[rb][ks] = bf16x8_t{};
-                gB[rb][ks] = bf16x8_t{};
-            }
+        if (lane == 63) sm.wsum[wave] = incl;
+        __syncthreads();
+        int base = w0 == 0 ? 0 : sm.nu;
+        for (int i = 0; i < wave; ++i) base += sm.wsum[i];
+        int pos = base + incl - cnt;
+        uint32_t x = word;
+        while (x) {
+            const int bit = 31 - __clz(x);
+            sm.ulist[pos++] = wi * 32 + bit;
+            x &= ~(1u << bit);
         }
-#pragma unroll
-        for (int db = 0; db < 8; ++db) acc[rb][db] = zero4();
+        __syncthreads();
+        if (tid == 0) {
+            int tot = w0 == 0 ? 0 : sm.nu;
+            for (int i = 0; i < NW; ++i) tot += sm.wsum[i];
+            sm.nu = tot;
+        }
+        __syncthreads();
     }
+    if (nwd == 0 && tid == 0) sm.nu = 0;
+
+    // ---- Q^T and dO^T operands of the wave's row block ---------------------------------
+    const int tau = wave * 2 + (row >> 3);
+    const int t_row = t0 + tau;
+    bf16x8_t qB[4], gB[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+        if (t_row < dm.L) {
+            const size_t o = (((size_t)b * dm.L + t_row) * dm.H + (size_t)g * HG + (row & 7)) * D +
+                             32 * ks + 8 * grp;
+            qB[ks] = ld_bf16x8(Q + o);
+            gB[ks] = ld_bf16x8(dO + o);
+        } else {
+            qB[ks] = bf16x8_t{};
+            gB[ks] = bf16x8_t{};
+        }
+    }
+    f32x4_t acc[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) acc[db] = zero4();
     __syncthreads();
     const int nu = sm.nu;
+    // this lane's token: next selected chunk, its slot and weight
+    int sp = 0;
+    int cur_c = sm.sidx[tau * k];
+    int cur_s = sm.sslot[tau * k];
 
     const size_t rowstride = (size_t)dm.G * D;
-    // staging: thread covers keys 2 (p / 16), 2 (p / 16) + 1 of column block p % 16 (vector
-    // pairs); K and V go to LDS row-major, K also transposed (key pairs packed).
-    u32x4_t kreg[NPF], vreg[NPF];
-    auto load_chunk = [&](int c) __attribute__((always_inline)) {
-        const size_t base = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
-#pragma unroll
-        for (int i = 0; i < NPF; ++i) {
-            const int p = tid + (i >> 1) * kThreads;
-            const int r = (p >> 4) * 2 + (i & 1), col = (p & 15) * 8;
-            kreg[i] = *reinterpret_cast<const u32x4_t*>(K + base + (size_t)r * rowstride + col);
-            vreg[i] = *reinterpret_cast<const u32x4_t*>(V + base + (size_t)r * rowstride + col);
-        }
-    };
-    auto store_chunk = [&]() __attribute__((always_inline)) {
-#pragma unroll
-        for (int i = 0; i < NPF; ++i) {
-            const int p = tid + (i >> 1) * kThreads;
-            const int r = (p >> 4) * 2 + (i & 1), col = (p & 15) * 8;
-            *reinterpret_cast<u32x4_t*>(&sm.Ks[r * KP + col]) = kreg[i];
-            *reinterpret_cast<u32x4_t*>(&sm.Vs[r * KP + col]) = vreg[i];
-        }
-#pragma unroll
-        for (int i = 0; i < NPF; i += 2) {
-            const int p = tid + (i >> 1) * kThreads;
-            const int r = (p >> 4) * 2, col = (p & 15) * 8;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const uint32_t a = kreg[i][j], c2 = kreg[i + 1][j];
-                const int d0 = col + 2 * j, d1 = d0 + 1;
-                *reinterpret_cast<uint32_t*>(&sm.Kt[d0 * VP + tpos(d0, r, S)]) =
-                    (a & 0xFFFFu) | (c2 << 16);
-                *reinterpret_cast<uint32_t*>(&sm.Kt[d1 * VP + tpos(d1, r, S)]) =
-                    (a >> 16) | (c2 & 0xFFFF0000u);
-            }
-        }
-    };
-
+    const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
     const float beta = dm.beta;
     const float sl2 = beta * 1.44269504088896341f;
-    const float ln2 = 0.69314718055994531f;
-    if (nu > 0) load_chunk(sm.ulist[0]);
+    StageQ<S> st;
+    // S = 64: chunk u is computed from stage u % 2 while chunk u + 1 (in registers) is
+    // written to the other stage and chunk u + 2 is fetched; one barrier per chunk.
+    // S = 128: one stage, written between two barriers, chunk u + 1 fetched meanwhile.
+    if (nu > 0) q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[0] * S * rowstride, rowstride, tid);
+    if constexpr (NBUF == 2) {
+        if (nu > 0) q_store<S>(st, sm.Ks[0], sm.Vs[0], sm.Kt[0], tid);
+        if (nu > 1)
+            q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[1] * S * rowstride, rowstride, tid);
+        __syncthreads();
+    }
     for (int u = 0; u < nu; ++u) {
         const int c = sm.ulist[u];
-        __syncthreads();
-        store_chunk();
-        __syncthreads();
-        if (u + 1 < nu) load_chunk(sm.ulist[u + 1]);
-
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            const int tau = wave * 4 + rb * 2 + (row >> 3);
-            float wl = 0.f;
-            int slot = -1;
-            for (int s = 0; s < k; ++s)
-                if (sm.sidx[tau * k + s] == c) {
-                    wl = sm.sw[tau * k + s];
-                    slot = s;
-                }
-            if (__ballot(slot >= 0) == 0) continue;
-
+        if constexpr (NBUF == 1) {
+            __syncthreads();
+            q_store<S>(st, sm.Ks[0], sm.Vs[0], sm.Kt[0], tid);
+            __syncthreads();
+            if (u + 1 < nu)
+                q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[u + 1] * S * rowstride,
+                          rowstride, tid);
+        }
+        const int bi = (NBUF == 2) ? (u & 1) : 0;
+        const bool mine = (cur_c == c);
+        if (__ballot(mine) != 0) {
+            const __bf16* Ks = sm.Ks[bi];
+            const __bf16* Vs = sm.Vs[bi];
+            const __bf16* Kt = sm.Kt[bi];
+            const float wl = mine ? sm.ow[tau * k + cur_s] : 0.f;
             f32x4_t z[MB], dp[MB];
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) z[mb] = dp[mb] = zero4();
@@ -226,10 +308,10 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    const bf16x8_t ka = ld_bf16x8(&sm.Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
-                    z[mb] = mfma16(ka, qB[rb][ks], z[mb]);
-                    const bf16x8_t va = ld_bf16x8(&sm.Vs[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
-                    dp[mb] = mfma16(va, gB[rb][ks], dp[mb]);
+                    const bf16x8_t ka = ld_bf16x8(&Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
+                    z[mb] = mfma16(ka, qB[ks], z[mb]);
+                    const bf16x8_t va = ld_bf16x8(&Vs[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
+                    dp[mb] = mfma16(va, gB[ks], dp[mb]);
                 }
             float m = -INFINITY;
 #pragma unroll
@@ -270,11 +352,11 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
                     const int d = 16 * db + row;
-                    const __bf16* kr = &sm.Kt[d * VP];
+                    const __bf16* kr = &Kt[d * VP];
                     const bf16x8_t a = cat(ld_bf16x4(kr + tpos(d, 32 * ks2 + 4 * grp, S)),
                                            ld_bf16x4(kr + tpos(d, 32 * ks2 + 16 + 4 * grp, S)));
-                    acc[rb][db] = mfma16(a, zh, acc[rb][db]);
-                    acc[rb][db] = mfma16(a, zl, acc[rb][db]);
+                    acc[db] = mfma16(a, zh, acc[db]);
+                    acc[db] = mfma16(a, zl, acc[db]);
                 }
             }
             // statistics of this (token, slot, head) and dw of the token
@@ -282,56 +364,61 @@ __global__ __launch_bounds__(kThreads, 1) void bwd_q_mfma(
             dtok += __shfl_xor(dtok, 1, 64);
             dtok += __shfl_xor(dtok, 2, 64);
             dtok += __shfl_xor(dtok, 4, 64);
-            if (slot >= 0) {
-                const int t = t0 + tau;
-                const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k + slot;
+            if (mine) {
+                const size_t so = (((size_t)b * dm.L + t_row) * dm.G + g) * k + cur_s;
                 if (grp == 0) {
                     lse_out[so * HG + (row & 7)] = m * beta + __logf(ssum);
                     d_out[so * HG + (row & 7)] = dsum;
                 }
-                if (grp == 0 && (row & 7) == 0) sm.dw[tau * k + slot] = dtok;
+                if (grp == 0 && (row & 7) == 0) sm.dw[tau * k + cur_s] = dtok;
+                ++sp;
+                cur_c = sp < k ? sm.sidx[tau * k + sp] : -1;
+                cur_s = sp < k ? sm.sslot[tau * k + sp] : 0;
             }
+        }
+        if constexpr (NBUF == 2) {
+            if (u + 1 < nu)
+                q_store<S>(st, sm.Ks[(u + 1) & 1], sm.Vs[(u + 1) & 1], sm.Kt[(u + 1) & 1], tid);
+            __syncthreads();
+            if (u + 2 < nu)
+                q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[u + 2] * S * rowstride,
+                          rowstride, tid);
         }
     }
     __syncthreads();
 
     // ---- softmax-weight Jacobian, score term, write dQ and ds ----------------------------
+    if (t_row >= dm.L) return;
+    float wdw = 0.f;
+    for (int s = 0; s < k; ++s) wdw = fmaf(sm.ow[tau * k + s], sm.dw[tau * k + s], wdw);
+    f32x4_t out[8];
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-        const int tau = wave * 4 + rb * 2 + (row >> 3);
-        const int t = t0 + tau;
-        if (t >= dm.L) continue;
-        float wdw = 0.f;
-        for (int s = 0; s < k; ++s) wdw = fmaf(sm.sw[tau * k + s], sm.dw[tau * k + s], wdw);
-        f32x4_t out[8];
+    for (int db = 0; db < 8; ++db)
 #pragma unroll
-        for (int db = 0; db < 8; ++db)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) out[db][i] = beta * acc[rb][db][i];
-        for (int s = 0; s < k; ++s) {
-            const int c = sm.sidx[tau * k + s];
-            const float dsv = (c >= 0) ? sm.sw[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
-            if (grp == 0 && (row & 7) == 0)
-                ds_out[(((size_t)b * dm.L + t) * dm.G + g) * k + s] = dsv;
-            if (c < 0) continue;
-            const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;
-            const float coef = dm.alpha * dsv;
-#pragma unroll
-            for (int db = 0; db < 8; ++db) {
-                const float4 kv = *reinterpret_cast<const float4*>(kb + 16 * db + 4 * grp);
-                out[db][0] = fmaf(coef, kv.x, out[db][0]);
-                out[db][1] = fmaf(coef, kv.y, out[db][1]);
-                out[db][2] = fmaf(coef, kv.z, out[db][2]);
-                out[db][3] = fmaf(coef, kv.w, out[db][3]);
-            }
-        }
-        __bf16* op = dQ + (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (row & 7)) * D;
+        for (int i = 0; i < 4; ++i) out[db][i] = beta * acc[db][i];
+    for (int s = 0; s < k; ++s) {
+        const int c = sm.oidx[tau * k + s];
+        const float dsv = (c >= 0) ? sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
+        if (grp == 0 && (row & 7) == 0)
+            ds_out[(((size_t)b * dm.L + t_row) * dm.G + g) * k + s] = dsv;
+        if (c < 0) continue;
+        const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;
+        const float coef = dm.alpha * dsv;
 #pragma unroll
         for (int db = 0; db < 8; ++db) {
-            const bf16x4_t o4{f2bf(out[db][0]), f2bf(out[db][1]), f2bf(out[db][2]),
-                              f2bf(out[db][3])};
-            *reinterpret_cast<bf16x4_t*>(op + 16 * db + 4 * grp) = o4;
+            const float4 kv = *reinterpret_cast<const float4*>(kb + 16 * db + 4 * grp);
+            out[db][0] = fmaf(coef, kv.x, out[db][0]);
+            out[db][1] = fmaf(coef, kv.y, out[db][1]);
+            out[db][2] = fmaf(coef, kv.z, out[db][2]);
+            out[db][3] = fmaf(coef, kv.w, out[db][3]);
         }
+    }
+    __bf16* op = dQ + (((size_t)b * dm.L + t_row) * dm.H + (size_t)g * HG + (row & 7)) * D;
+#pragma unroll
+    for (int db = 0; db < 8; ++db) {
+        const bf16x4_t o4{f2bf(out[db][0]), f2bf(out[db][1]), f2bf(out[db][2]),
+                          f2bf(out[db][3])};
+        *reinterpret_cast<bf16x4_t*>(op + 16 * db + 4 * grp) = o4;
     }
 }
 
@@ -588,7 +675,7 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
 
 bool backward_mfma_supported(const Dims& dm, bool in_bf16) {
     return in_bf16 && dm.h == HG && dm.d == D && (dm.S == 64 || dm.S == 128) && dm.k <= KMAX &&
-           !getenv("HSA_FORCE_GENERIC");
+           dm.C <= UWORDS * 32 && !getenv("HSA_FORCE_GENERIC");
 }
 
 size_t backward_mfma_workspace(const Dims& dm) {
@@ -605,17 +692,20 @@ hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, co
     float* ds = (float*)(wsb + l.ds);
     float* lse = (float*)(wsb + l.lse);
     float* dd = (float*)(wsb + l.dd);
-    const int ntiles = cdiv(dm.L, TQ);
-    const int nlog = ntiles * dm.B * dm.G;
-    const int grid = 8 * cdiv(nlog, 8);
     if (dm.S == 64) {
+        constexpr int NW = QCfg<64>::NW;
+        const int ntiles = cdiv(dm.L, 2 * NW);
+        const int grid = 8 * cdiv(ntiles * dm.B * dm.G, 8);
         HSA_TIMED("bwd_q_mfma", st);
-        hipLaunchKernelGGL((bwd_q_mfma<64>), dim3(grid), dim3(kThreads), 0, st, dm,
+        hipLaunchKernelGGL((bwd_q_mfma<64>), dim3(grid), dim3(NW * 64), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Kbar, idx, w,
                            (const __bf16*)dO, (__bf16*)dQ, ds, lse, dd, ntiles);
     } else {
+        constexpr int NW = QCfg<128>::NW;
+        const int ntiles = cdiv(dm.L, 2 * NW);
+        const int grid = 8 * cdiv(ntiles * dm.B * dm.G, 8);
         HSA_TIMED("bwd_q_mfma", st);
-        hipLaunchKernelGGL((bwd_q_mfma<128>), dim3(grid), dim3(kThreads), 0, st, dm,
+        hipLaunchKernelGGL((bwd_q_mfma<128>), dim3(grid), dim3(NW * 64), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, Kbar, idx, w,
                            (const __bf16*)dO, (__bf16*)dQ, ds, lse, dd, ntiles);
     }
