@@ -468,8 +468,16 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
     __shared__ SmemKV sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
-    const int c = blockIdx.x;
-    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    // With at least 8 (b, g) slices, the chunks of one slice run together on one XCD, so
+    // the Q / dO rows of a token, read once per chunk it selected, are shared through that
+    // XCD's L2.  With fewer slices, whole-slice ranges would leave the XCDs unevenly loaded
+    // (early chunks have more candidate tokens), so chunks stay interleaved over the XCDs.
+    const int nlog = dm.Call * dm.B * dm.G;
+    const int lid = (dm.B * dm.G >= 8) ? xcd_logical_id(nlog)
+                                        : ((int)blockIdx.x < nlog ? (int)blockIdx.x : -1);
+    if (lid < 0) return;
+    const int c = lid % dm.Call;
+    const int bg = lid / dm.Call, b = bg / dm.G, g = bg % dm.G;
     const int k = dm.k;
     const size_t rowstride = (size_t)dm.G * D;
     const size_t cbase = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
@@ -715,7 +723,7 @@ hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, co
     e = launch_selection_bitmap(dm, idx, (uint32_t*)(wsb + l.bitmap), st);
     if (e != hipSuccess) return e;
     const int nwords = cdiv(dm.L, 32);
-    dim3 g2(dm.Call, dm.B * dm.G);
+    const dim3 g2(8 * cdiv(dm.Call * dm.B * dm.G, 8));
     if (dm.S == 64) {
         HSA_TIMED("bwd_kv_mfma", st);
         hipLaunchKernelGGL((bwd_kv_mfma<64>), g2, dim3(256), 0, st, dm, (const __bf16*)Q,

@@ -1,8 +1,9 @@
 // bf16 MFMA forward of hierarchical sparse attention (Sec. 3.1.1), for h = 8 query heads
 // per KV head, d = 128, S in {64, 128}.
 //
-// Workgroup = (b, g, tile of 32 tokens inside one query chunk), 16 waves; wave w owns
-// tokens 2w, 2w+1 as one row block of 16 rows (2 tokens x 8 heads).
+// Workgroup = (b, g, tile of 2 NW tokens inside one query chunk), NW waves (16 for S = 64,
+// 8 for S = 128); wave w owns tokens 2w, 2w+1 as one row block of 16 rows (2 tokens x 8
+// heads).
 //  1. Each token's valid selections are sorted by descending chunk; the tile's union is
 //     marked in an LDS bitmap over the candidates and listed in descending chunk order, so
 //     every lane follows its token's slot list with a register pointer.
@@ -25,21 +26,32 @@ namespace {
 
 constexpr int D = 128;
 constexpr int HG = 8;            // query heads per KV head
-constexpr int NW = 16;           // waves per workgroup
-constexpr int kThreads = NW * 64;
-constexpr int TQ = 32;           // tokens per tile (2 per wave)
 constexpr int KMAX = 32;
 constexpr int KP = D + 8;        // padded K row (bf16 elements)
 constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
+// Waves per workgroup (a tile holds 2 NW tokens, 2 per wave) and the waves per SIMD the
+// register budget is sized for.  At S = 64 the 32-token tile shares each staged chunk
+// among more tokens; S = 128 needs the register room of 8 waves.
+template <int S>
+struct FCfg;
+template <>
+struct FCfg<64> {
+    static constexpr int NW = 16, WPE = 4;
+};
+template <>
+struct FCfg<128> {
+    static constexpr int NW = 8, WPE = 2;
+};
+
 template <int S>
 struct Smem {
+    static constexpr int NW = FCfg<S>::NW, TQ = 2 * NW;
     static constexpr int VP = S + 8;              // padded V^T row (keys)
     __bf16 Ks[2][S * KP];                         // double-buffered chunk stage
     __bf16 Vt[2][D * VP];
     int32_t sidx[TQ * KMAX];                      // per token: valid chunks, descending, -1 pad
     float sw[TQ * KMAX];
-    uint32_t ubits[UWORDS];
     int32_t ulist[TQ * KMAX];                     // union, descending chunk order
     int wsum[NW];
     int nu;
@@ -50,6 +62,7 @@ struct Smem {
 // packed key pairs.
 template <int S>
 struct Stage {
+    static constexpr int kThreads = FCfg<S>::NW * 64;
     static constexpr int NK = S * D / 8 / kThreads;                      // K vectors / thread
     static constexpr int NV = (S * D / 16 + kThreads - 1) / kThreads;    // V pairs / thread
     u32x4_t k[NK];
@@ -62,13 +75,13 @@ __device__ __forceinline__ void load_chunk(Stage<S>& st, const __bf16* __restric
                                            size_t rowstride, int tid) {
 #pragma unroll
     for (int i = 0; i < Stage<S>::NK; ++i) {
-        const int v = tid + i * kThreads;
+        const int v = tid + i * Stage<S>::kThreads;
         st.k[i] = *reinterpret_cast<const u32x4_t*>(K + base + (size_t)(v >> 4) * rowstride +
                                                     (v & 15) * 8);
     }
 #pragma unroll
     for (int i = 0; i < Stage<S>::NV; ++i) {
-        const int p = tid + i * kThreads;
+        const int p = tid + i * Stage<S>::kThreads;
         if (p < S * 8) {
             const size_t o = base + (size_t)((p >> 4) * 2) * rowstride + (p & 15) * 8;
             st.v[2 * i] = *reinterpret_cast<const u32x4_t*>(V + o);
@@ -83,12 +96,12 @@ __device__ __forceinline__ void store_chunk(const Stage<S>& st, __bf16* Ks, __bf
     constexpr int VP = S + 8;
 #pragma unroll
     for (int i = 0; i < Stage<S>::NK; ++i) {
-        const int v = tid + i * kThreads;
+        const int v = tid + i * Stage<S>::kThreads;
         *reinterpret_cast<u32x4_t*>(&Ks[(v >> 4) * KP + (v & 15) * 8]) = st.k[i];
     }
 #pragma unroll
     for (int i = 0; i < Stage<S>::NV; ++i) {
-        const int p = tid + i * kThreads;
+        const int p = tid + i * Stage<S>::kThreads;
         if (p < S * 8) {
             const int r = (p >> 4) * 2, col = (p & 15) * 8;
             const u32x4_t a = st.v[2 * i], c2 = st.v[2 * i + 1];
@@ -105,11 +118,12 @@ __device__ __forceinline__ void store_chunk(const Stage<S>& st, __bf16* Ks, __bf
 }
 
 template <int S>
-__global__ __launch_bounds__(kThreads, 1) void forward_mfma(
+__global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     __bf16* __restrict__ O, int ntiles) {
     constexpr int VP = Smem<S>::VP;
+    constexpr int NW = Smem<S>::NW, TQ = Smem<S>::TQ, kThreads = NW * 64;
     constexpr int MB = S / 16;            // key blocks of Z^T
     constexpr int KS2 = S / 32;           // key steps of P V
     __shared__ Smem<S> sm;
@@ -158,17 +172,20 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
             ws[s] = 0.f;
         }
     }
-    for (int i = tid; i < nwd; i += kThreads) sm.ubits[i] = 0u;
+    // the union bitmap lives in stage 1, which is first written after the union is listed
+    uint32_t* ubits = reinterpret_cast<uint32_t*>(sm.Ks[1]);
+    static_assert(sizeof(sm.Ks[1]) >= UWORDS * 4, "bitmap does not fit the stage");
+    for (int i = tid; i < nwd; i += kThreads) ubits[i] = 0u;
     __syncthreads();
     for (int e = tid; e < TQ * k; e += kThreads) {
         const int c = sm.sidx[e];
-        if (c >= 0) atomicOr(&sm.ubits[c >> 5], 1u << (c & 31));
+        if (c >= 0) atomicOr(&ubits[c >> 5], 1u << (c & 31));
     }
     __syncthreads();
     // union in descending chunk order: thread i takes word nwd - 1 - i
-    {
-        const int wi = nwd - 1 - tid;
-        const uint32_t word = (tid < nwd) ? sm.ubits[wi] : 0u;
+    for (int w0 = 0; w0 < nwd; w0 += kThreads) {
+        const int wi = nwd - 1 - (w0 + tid);
+        const uint32_t word = (wi >= 0) ? ubits[wi] : 0u;
         const int cnt = __popc(word);
         int incl = cnt;
 #pragma unroll
@@ -178,7 +195,7 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
         }
         if (lane == 63) sm.wsum[wave] = incl;
         __syncthreads();
-        int base = 0;
+        int base = w0 == 0 ? 0 : sm.nu;
         for (int i = 0; i < wave; ++i) base += sm.wsum[i];
         int pos = base + incl - cnt;
         uint32_t x = word;
@@ -187,12 +204,15 @@ __global__ __launch_bounds__(kThreads, 1) void forward_mfma(
             sm.ulist[pos++] = wi * 32 + bit;
             x &= ~(1u << bit);
         }
-        if (tid == kThreads - 1) {
-            int tot = 0;
+        __syncthreads();
+        if (tid == 0) {
+            int tot = w0 == 0 ? 0 : sm.nu;
             for (int i = 0; i < NW; ++i) tot += sm.wsum[i];
             sm.nu = tot;
         }
+        __syncthreads();
     }
+    if (nwd == 0 && tid == 0) sm.nu = 0;
 
     // ---- Q^T operand of the wave's row block (registers, whole kernel) -------------------
     const int tau = wave * 2 + (row >> 3);
@@ -314,17 +334,20 @@ bool forward_mfma_supported(const Dims& dm, bool in_bf16) {
 hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
                                const int32_t* idx, const float* w, void* O, void*,
                                hipStream_t st) {
-    const int ntiles = cdiv(dm.L, TQ);
-    const int nlog = ntiles * dm.B * dm.G;
-    const int grid = 8 * cdiv(nlog, 8);
     if (dm.S == 64) {
+        constexpr int NW = FCfg<64>::NW;
+        const int ntiles = cdiv(dm.L, 2 * NW);
+        const int grid = 8 * cdiv(ntiles * dm.B * dm.G, 8);
         HSA_TIMED("forward_mfma", st);
-        hipLaunchKernelGGL((forward_mfma<64>), dim3(grid), dim3(kThreads), 0, st, dm,
+        hipLaunchKernelGGL((forward_mfma<64>), dim3(grid), dim3(NW * 64), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
                            (__bf16*)O, ntiles);
     } else {
+        constexpr int NW = FCfg<128>::NW;
+        const int ntiles = cdiv(dm.L, 2 * NW);
+        const int grid = 8 * cdiv(ntiles * dm.B * dm.G, 8);
         HSA_TIMED("forward_mfma", st);
-        hipLaunchKernelGGL((forward_mfma<128>), dim3(grid), dim3(kThreads), 0, st, dm,
+        hipLaunchKernelGGL((forward_mfma<128>), dim3(grid), dim3(NW * 64), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
                            (__bf16*)O, ntiles);
     }
