@@ -18,7 +18,7 @@
 // Key pass: chunk-major, reading those statistics (see bwd_kv_mfma below).
 #include <cstdlib>
 
-#include "mfma_common.h"
+#include "tile_sel.h"
 
 namespace hsa {
 
@@ -72,15 +72,15 @@ struct SmemQ {
     __bf16 Ks[NBUF][S * KP];
     __bf16 Vs[NBUF][S * KP];
     __bf16 Kt[NBUF][D * VP];
-    int32_t sidx[TQ * KMAX];      // per token: valid chunks in descending order, -1 pad
-    uint8_t sslot[TQ * KMAX];     // ... and their slot numbers
-    int32_t oidx[TQ * KMAX];      // per token and slot: the chunk, -1 if not a valid entry
+    int32_t oidx[TQ * KMAX];      // selection tables (see tile_sel.h)
     float ow[TQ * KMAX];
-    float dw[TQ * KMAX];
+    int32_t sidx[TQ * KMAX];
+    float sw[TQ * KMAX];
+    int32_t ulist[TQ * KMAX];
     uint32_t ubits[UWORDS];
-    int32_t ulist[TQ * KMAX];     // union, descending chunk order
+    float dw[TQ * KMAX];          // per slot: dw of the token
+    uint8_t sslot[TQ * KMAX];
     int wsum[NW];
-    int nu;
 };
 
 // Staging of one chunk by NT threads in units of vector pairs (rows 2 (p / 16), +1,
@@ -166,82 +166,6 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
     const int t0 = tile * TQ;
     const int ncand = t0 / S;
     const int row = lane & 15, grp = lane >> 4;
-    const int nwd = (ncand + 31) >> 5;
-
-    // ---- selections: per slot as given, and the valid ones sorted by descending chunk ----
-    if (tid < TQ) {
-        const int t = t0 + tid;
-        int* cs = &sm.sidx[tid * k];
-        uint8_t* sl = &sm.sslot[tid * k];
-        int n = 0;
-        for (int s = 0; s < k; ++s) {
-            int c = -1;
-            float wv = 0.f;
-            if (t < dm.L) {
-                const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k + s;
-                c = idx[o];
-                wv = w[o];
-                if (c < 0 || c >= ncand) {
-                    c = -1;
-                    wv = 0.f;
-                }
-            }
-            sm.oidx[tid * k + s] = c;
-            sm.ow[tid * k + s] = wv;
-            sm.dw[tid * k + s] = 0.f;
-            if (c < 0) continue;
-            int j = n++;
-            while (j > 0 && cs[j - 1] < c) {
-                cs[j] = cs[j - 1];
-                sl[j] = sl[j - 1];
-                --j;
-            }
-            cs[j] = c;
-            sl[j] = (uint8_t)s;
-        }
-        for (int s = n; s < k; ++s) {
-            cs[s] = -1;
-            sl[s] = 0;
-        }
-    }
-    for (int i = tid; i < nwd; i += NT) sm.ubits[i] = 0u;
-    __syncthreads();
-    for (int e = tid; e < TQ * k; e += NT) {
-        const int c = sm.sidx[e];
-        if (c >= 0) atomicOr(&sm.ubits[c >> 5], 1u << (c & 31));
-    }
-    __syncthreads();
-    // union in descending chunk order: thread i takes word nwd - 1 - i
-    for (int w0 = 0; w0 < nwd; w0 += NT) {
-        const int wi = nwd - 1 - (w0 + tid);
-        const uint32_t word = (wi >= 0) ? sm.ubits[wi] : 0u;
-        const int cnt = __popc(word);
-        int incl = cnt;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int v = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += v;
-        }
-        if (lane == 63) sm.wsum[wave] = incl;
-        __syncthreads();
-        int base = w0 == 0 ? 0 : sm.nu;
-        for (int i = 0; i < wave; ++i) base += sm.wsum[i];
-        int pos = base + incl - cnt;
-        uint32_t x = word;
-        while (x) {
-            const int bit = 31 - __clz(x);
-            sm.ulist[pos++] = wi * 32 + bit;
-            x &= ~(1u << bit);
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int tot = w0 == 0 ? 0 : sm.nu;
-            for (int i = 0; i < NW; ++i) tot += sm.wsum[i];
-            sm.nu = tot;
-        }
-        __syncthreads();
-    }
-    if (nwd == 0 && tid == 0) sm.nu = 0;
 
     // ---- Q^T and dO^T operands of the wave's row block ---------------------------------
     const int tau = wave * 2 + (row >> 3);
@@ -259,15 +183,19 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
             gB[ks] = bf16x8_t{};
         }
     }
+    // ---- selections of the tile, sorted per token, and their union ----------------------
+    const TileSel ts{sm.oidx, sm.ow, sm.sidx, sm.sslot, sm.sw, sm.ubits, sm.ulist, sm.wsum};
+    const int nu = tile_selection<NT, TQ>(ts, idx, w, (((size_t)b * dm.L + t0) * dm.G + g) * k,
+                                          (size_t)dm.G * k, k, min(TQ, dm.L - t0), ncand);
+    for (int e = tid; e < TQ * k; e += NT) sm.dw[e] = 0.f;
     f32x4_t acc[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc[db] = zero4();
-    __syncthreads();
-    const int nu = sm.nu;
-    // this lane's token: next selected chunk, its slot and weight
+    // this lane's token: next selected chunk, its first slot and its weight
     int sp = 0;
     int cur_c = sm.sidx[tau * k];
     int cur_s = sm.sslot[tau * k];
+    float cur_w = sm.sw[tau * k];
 
     const size_t rowstride = (size_t)dm.G * D;
     const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
@@ -300,7 +228,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
             const __bf16* Ks = sm.Ks[bi];
             const __bf16* Vs = sm.Vs[bi];
             const __bf16* Kt = sm.Kt[bi];
-            const float wl = mine ? sm.ow[tau * k + cur_s] : 0.f;
+            const float wl = mine ? cur_w : 0.f;
             f32x4_t z[MB], dp[MB];
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) z[mb] = dp[mb] = zero4();
@@ -374,6 +302,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
                 ++sp;
                 cur_c = sp < k ? sm.sidx[tau * k + sp] : -1;
                 cur_s = sp < k ? sm.sslot[tau * k + sp] : 0;
+                cur_w = sp < k ? sm.sw[tau * k + sp] : 0.f;
             }
         }
         if constexpr (NBUF == 2) {
@@ -396,21 +325,29 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
     for (int db = 0; db < 8; ++db)
 #pragma unroll
         for (int i = 0; i < 4; ++i) out[db][i] = beta * acc[db][i];
+    // score term: empty slots add 0 (their loads use chunk 0, which exists when any slot of
+    // the tile is valid); loads of several slots are in flight at once
     for (int s = 0; s < k; ++s) {
         const int c = sm.oidx[tau * k + s];
         const float dsv = (c >= 0) ? sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
         if (grp == 0 && (row & 7) == 0)
             ds_out[(((size_t)b * dm.L + t_row) * dm.G + g) * k + s] = dsv;
-        if (c < 0) continue;
-        const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;
-        const float coef = dm.alpha * dsv;
+    }
+    if (ncand > 0) {
+#pragma unroll 4
+        for (int s = 0; s < k; ++s) {
+            const int c = sm.oidx[tau * k + s];
+            const float dsv = (c >= 0) ? sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
+            const float* kb = Kbar + (((size_t)b * dm.C + max(c, 0)) * dm.G + g) * D;
+            const float coef = dm.alpha * dsv;
 #pragma unroll
-        for (int db = 0; db < 8; ++db) {
-            const float4 kv = *reinterpret_cast<const float4*>(kb + 16 * db + 4 * grp);
-            out[db][0] = fmaf(coef, kv.x, out[db][0]);
-            out[db][1] = fmaf(coef, kv.y, out[db][1]);
-            out[db][2] = fmaf(coef, kv.z, out[db][2]);
-            out[db][3] = fmaf(coef, kv.w, out[db][3]);
+            for (int db = 0; db < 8; ++db) {
+                const float4 kv = *reinterpret_cast<const float4*>(kb + 16 * db + 4 * grp);
+                out[db][0] = fmaf(coef, kv.x, out[db][0]);
+                out[db][1] = fmaf(coef, kv.y, out[db][1]);
+                out[db][2] = fmaf(coef, kv.z, out[db][2]);
+                out[db][3] = fmaf(coef, kv.w, out[db][3]);
+            }
         }
     }
     __bf16* op = dQ + (((size_t)b * dm.L + t_row) * dm.H + (size_t)g * HG + (row & 7)) * D;

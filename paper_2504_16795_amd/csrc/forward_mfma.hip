@@ -19,7 +19,7 @@
 //     once per tile instead of once per (token, slot), and no online softmax is needed.
 #include <cstdlib>
 
-#include "mfma_common.h"
+#include "tile_sel.h"
 
 namespace hsa {
 namespace {
@@ -50,11 +50,13 @@ struct Smem {
     static constexpr int VP = S + 8;              // padded V^T row (keys)
     __bf16 Ks[2][S * KP];                         // double-buffered chunk stage
     __bf16 Vt[2][D * VP];
-    int32_t sidx[TQ * KMAX];                      // per token: valid chunks, descending, -1 pad
+    int32_t oidx[TQ * KMAX];                      // selection tables (see tile_sel.h)
+    float ow[TQ * KMAX];
+    int32_t sidx[TQ * KMAX];
     float sw[TQ * KMAX];
-    int32_t ulist[TQ * KMAX];                     // union, descending chunk order
+    int32_t ulist[TQ * KMAX];
+    uint8_t sslot[TQ * KMAX];
     int wsum[NW];
-    int nu;
 };
 
 // Staging of one chunk: K vectors (key v / 16, columns 8 (v % 16) .. +7) go row-major to
@@ -137,82 +139,6 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     const int t0 = tile * TQ;
     const int ncand = t0 / S;
     const int row = lane & 15, grp = lane >> 4;
-    const int nwd = (ncand + 31) >> 5;
-
-    // ---- selections: valid entries of each token, descending chunk order -----------------
-    if (tid < TQ) {
-        const int t = t0 + tid;
-        int* cs = &sm.sidx[tid * k];
-        float* ws = &sm.sw[tid * k];
-        int n = 0;
-        if (t < dm.L) {
-            const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
-            for (int s = 0; s < k; ++s) {
-                const int c = idx[o + s];
-                if (c < 0 || c >= ncand) continue;
-                const float wv = w[o + s];
-                int e = 0;
-                while (e < n && cs[e] != c) ++e;
-                if (e < n) {                          // repeated chunk: weights add
-                    ws[e] += wv;
-                    continue;
-                }
-                int j = n++;
-                while (j > 0 && cs[j - 1] < c) {      // insertion: descending chunk index
-                    cs[j] = cs[j - 1];
-                    ws[j] = ws[j - 1];
-                    --j;
-                }
-                cs[j] = c;
-                ws[j] = wv;
-            }
-        }
-        for (int s = n; s < k; ++s) {
-            cs[s] = -1;
-            ws[s] = 0.f;
-        }
-    }
-    // the union bitmap lives in stage 1, which is first written after the union is listed
-    uint32_t* ubits = reinterpret_cast<uint32_t*>(sm.Ks[1]);
-    static_assert(sizeof(sm.Ks[1]) >= UWORDS * 4, "bitmap does not fit the stage");
-    for (int i = tid; i < nwd; i += kThreads) ubits[i] = 0u;
-    __syncthreads();
-    for (int e = tid; e < TQ * k; e += kThreads) {
-        const int c = sm.sidx[e];
-        if (c >= 0) atomicOr(&ubits[c >> 5], 1u << (c & 31));
-    }
-    __syncthreads();
-    // union in descending chunk order: thread i takes word nwd - 1 - i
-    for (int w0 = 0; w0 < nwd; w0 += kThreads) {
-        const int wi = nwd - 1 - (w0 + tid);
-        const uint32_t word = (wi >= 0) ? ubits[wi] : 0u;
-        const int cnt = __popc(word);
-        int incl = cnt;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int v = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += v;
-        }
-        if (lane == 63) sm.wsum[wave] = incl;
-        __syncthreads();
-        int base = w0 == 0 ? 0 : sm.nu;
-        for (int i = 0; i < wave; ++i) base += sm.wsum[i];
-        int pos = base + incl - cnt;
-        uint32_t x = word;
-        while (x) {
-            const int bit = 31 - __clz(x);
-            sm.ulist[pos++] = wi * 32 + bit;
-            x &= ~(1u << bit);
-        }
-        __syncthreads();
-        if (tid == 0) {
-            int tot = w0 == 0 ? 0 : sm.nu;
-            for (int i = 0; i < NW; ++i) tot += sm.wsum[i];
-            sm.nu = tot;
-        }
-        __syncthreads();
-    }
-    if (nwd == 0 && tid == 0) sm.nu = 0;
 
     // ---- Q^T operand of the wave's row block (registers, whole kernel) -------------------
     const int tau = wave * 2 + (row >> 3);
@@ -228,11 +154,17 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
             qB[ks] = bf16x8_t{};
         }
     }
+    // ---- selections of the tile, sorted per token, and their union ----------------------
+    // (the union bitmap lives in stage 1, which is first written after the union is listed)
+    static_assert(sizeof(sm.Ks[1]) >= UWORDS * 4, "bitmap does not fit the stage");
+    const TileSel ts{sm.oidx, sm.ow, sm.sidx, sm.sslot, sm.sw,
+                     reinterpret_cast<uint32_t*>(sm.Ks[1]), sm.ulist, sm.wsum};
+    const int nu = tile_selection<kThreads, TQ>(
+        ts, idx, w, (((size_t)b * dm.L + t0) * dm.G + g) * k, (size_t)dm.G * k, k,
+        min(TQ, dm.L - t0), ncand);
     f32x4_t acc[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc[db] = zero4();
-    __syncthreads();
-    const int nu = sm.nu;
     // this lane's token: next selected chunk and its weight
     int sp = 0;
     int cur_c = sm.sidx[tau * k];

@@ -9,7 +9,7 @@ import torch
 
 import hsa_synth
 import oracle
-from parity import (W_ATOL, assert_close, assert_indices, make_case,
+from parity import (W_ATOL, assert_close, assert_indices, attention_abs, make_case,
                     oracle_reference, to_dev, torch_dtype)
 
 pytestmark = pytest.mark.gpu
@@ -102,7 +102,7 @@ def test_forward(hsa_gpu, name):
     w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
     O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
     torch.cuda.synchronize()
-    assert_close("O", shape, O, ref["O"])
+    assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
 
 
 @pytest.mark.parametrize("name", list(CASES))
@@ -132,7 +132,8 @@ def test_end_to_end_pipeline(hsa_gpu, name):
                                       shape.S)
     torch.cuda.synchronize()
     assert_indices(idx, ref["idx"], ref["gap"], shape.S)
-    for n, t in (("O", O), ("dQ", dQ), ("dK", dK), ("dV", dV)):
+    assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
+    for n, t in (("dQ", dQ), ("dK", dK), ("dV", dV)):
         assert_close(n, shape, t, ref[n])
 
 
@@ -181,9 +182,10 @@ def test_decode(hsa_gpu, dtype, kbar_dtype):
     o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, 8, cache_len=cache_len)
     torch.cuda.synchronize()
     ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar.float(), lens, 64, 8)
+    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar.float(), lens, 64, 8)[0]
     assert np.array_equal(idx.cpu().numpy()[rgap >= 1e-3], ridx[rgap >= 1e-3])
     assert np.max(np.abs(w.cpu().numpy() - rw)) <= W_ATOL
-    assert_close("o", shape, o, ro)
+    assert_close("o", shape, o, ro, o_abs=ro_abs)
     for b in range(3):
         for g in range(2):
             p = inp["planted"][b, g].item()
@@ -217,3 +219,53 @@ def test_empty_batch_is_noop(hsa_gpu):
     idx, w = hsa_gpu.hsa_select_topk(Q, Kbar, 2, 64, 4)
     O = hsa_gpu.hsa_forward(Q, K, K, idx, w, 64)
     assert O.shape == Q.shape
+
+
+def _scrambled_selection(ref, shape, seed, repeats):
+    """The oracle's selection with empty slots mixed in: -1, the token's own chunk or a
+    later one, and an index far past the end; with `repeats`, some slots also repeat the
+    token's slot-0 chunk.  Returns (idx, w) as given to the library and the idx the
+    oracle sees, where every entry outside [0, floor(t / S)) is -1 (an empty slot)."""
+    rng = np.random.default_rng(seed)
+    idx = ref["idx"].copy()
+    w = rng.uniform(0.05, 1.0, idx.shape).astype(np.float32)
+    ncand = (np.arange(shape.L) // shape.S)[None, :, None, None]
+    u = rng.random(idx.shape)
+    idx = np.where(u < 0.08, -1, idx)
+    idx = np.where((u >= 0.08) & (u < 0.16), ncand + rng.integers(0, 3, idx.shape), idx)
+    idx = np.where((u >= 0.16) & (u < 0.18), 1 << 30, idx)
+    if repeats:
+        rep = (rng.random(idx.shape) < 0.15) & (np.arange(shape.k) > 0)
+        idx = np.where(rep, idx[..., :1], idx)
+    idx = idx.astype(np.int32)
+    idx_oracle = np.where((idx < 0) | (idx >= ncand), -1, idx).astype(np.int32)
+    return idx, w, idx_oracle
+
+
+@pytest.mark.parametrize("name", ["ragged_mfma_bf16", "wide_like_bf16", "ragged_f32"])
+def test_forward_empty_and_repeated_slots(hsa_gpu, name):
+    """Empty slots add nothing; a chunk given in several slots adds each slot's weight."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_forward, empty and repeated slots")
+    idx, w, idx_o = _scrambled_selection(ref, shape, 31, repeats=True)
+    want = oracle.forward(inp["Q"], inp["K"], inp["V"], idx_o, w, shape.S)
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], torch.from_numpy(idx).cuda(),
+                            torch.from_numpy(w).cuda(), shape.S)
+    torch.cuda.synchronize()
+    assert_close("O", shape, O, want, o_abs=attention_abs(inp, idx_o, w, shape.S))
+
+
+@pytest.mark.parametrize("name", ["ragged_mfma_bf16", "wide_like_bf16", "ragged_f32"])
+def test_backward_empty_slots(hsa_gpu, name):
+    """Empty slots (outside the token's candidates) carry no weight and no gradient."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_backward, empty slots")
+    idx, w, idx_o = _scrambled_selection(ref, shape, 32, repeats=False)
+    # the valid entries left are a subset of the oracle's selection, so they stay distinct
+    want = oracle.backward(inp["Q"], inp["K"], inp["V"], idx_o, w, inp["dO"], shape.S)
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, torch.from_numpy(idx).cuda(),
+                               torch.from_numpy(w).cuda(), dev["dO"], shape.S)
+    torch.cuda.synchronize()
+    for n, g_, r in zip(("dQ", "dK", "dV"), got, want):
+        assert_close(n, shape, g_, r)
