@@ -188,6 +188,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
     const int nu = tile_selection<NT, TQ>(ts, idx, w, (((size_t)b * dm.L + t0) * dm.G + g) * k,
                                           (size_t)dm.G * k, k, min(TQ, dm.L - t0), ncand);
     for (int e = tid; e < TQ * k; e += NT) sm.dw[e] = 0.f;
+    wait_global_loads();
     f32x4_t acc[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc[db] = zero4();
@@ -437,6 +438,7 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
         kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
         vB[ks] = ld_bf16x8(V + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
     }
+    wait_global_loads();
     f32x4_t aK[8], aV[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();

@@ -162,6 +162,7 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     const int nu = tile_selection<kThreads, TQ>(
         ts, idx, w, (((size_t)b * dm.L + t0) * dm.G + g) * k, (size_t)dm.G * k, k,
         min(TQ, dm.L - t0), ncand);
+    wait_global_loads();
     f32x4_t acc[8];
 #pragma unroll
     for (int db = 0; db < 8; ++db) acc[db] = zero4();

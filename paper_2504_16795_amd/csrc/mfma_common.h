@@ -86,6 +86,13 @@ __device__ __forceinline__ void split8(const f32x4_t& a, const f32x4_t& b, bf16x
     }
 }
 
+// Waits until every global load of this wave has landed.  Called once after the loads of
+// operands that stay in registers for a whole loop (Q^T, K / V blocks): the compiler cannot
+// tell at the loop header that those loads are complete, and otherwise makes the loop's
+// MFMAs wait for the in-order load counter to drain, i.e. for the next chunk's prefetch.
+// (s_waitcnt immediate: vmcnt 0, expcnt and lgkmcnt at their no-wait maxima.)
+__device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 // Logical workgroup id with an XCD-aware order: hardware dispatches consecutive ids to the
 // 8 XCDs round-robin, so consecutive logical ids (same (b, g), neighbouring tiles, sharing
 // chunks through L2) are mapped to the same XCD.  Returns -1 for padding ids.
