@@ -3,13 +3,15 @@
 //
 // Query pass (bwd_q_mfma): the forward's tiling (a tile of 2 NW tokens inside one query
 // chunk, wave w owning tokens 2w, 2w+1 as one row block of 16 rows; the tile's union of
-// chunks listed in descending order and staged once in LDS, each lane following its
-// token's descending slot list with a pointer).  Per chunk selected by the row block:
+// chunks listed in descending order and copied once into a ring of LDS stages, each lane
+// following its token's descending slot list with a pointer).  Per chunk selected by the
+// row block:
 //     Z^T  = K_c Q^T,  dP^T = V_c dO^T                     (keys x rows, MFMA)
 //     P    = softmax over keys;  D_row = sum_keys P dP      (= dO_row . O_{row,c})
 //     dZ^T = w P (dP - D)
-//     dQ^T += K_c^T dZ^T                                    (MFMA, K^T staged in LDS;
-//                                                             dZ as a bf16 hi/lo pair)
+//     dQ^T += K_c^T dZ^T                                    (MFMA, K^T fragments from
+//                                                             transposed reads of the K
+//                                                             tile; dZ as a bf16 hi/lo pair)
 //     dw_{t,c} = sum over the token's 8 heads of D_row
 // then ds_i = w_i (dw_i - sum_m w_m dw_m) and dQ = beta dQ + alpha sum_i ds_i Kbar_{c_i}.
 // For the key pass it stores, per (token, slot, head), the log-sum-exp of the scaled logits
@@ -18,6 +20,7 @@
 // Key pass: chunk-major, reading those statistics (see bwd_kv_mfma below).
 #include <cstdlib>
 
+#include "chunk_lds.h"
 #include "tile_sel.h"
 
 namespace hsa {
@@ -52,26 +55,23 @@ __host__ __device__ inline WsLayout ws_layout(const Dims& dm) {
     return l;
 }
 
-// Query-pass shape: S = 64 runs 16 waves with two chunk stages in LDS; S = 128 (twice the
-// stage and twice the Z / dP registers per row block) runs 8 waves with one stage.
+// Query-pass shape: waves per workgroup (one row block each) and chunk stages in LDS.
 template <int S>
 struct QCfg;
 template <>
 struct QCfg<64> {
-    static constexpr int NW = 8, NBUF = 2;
+    static constexpr int NW = 8, NST = 3;
 };
 template <>
 struct QCfg<128> {
-    static constexpr int NW = 8, NBUF = 1;
+    static constexpr int NW = 8, NST = 2;
 };
 
 template <int S>
 struct SmemQ {
-    static constexpr int NW = QCfg<S>::NW, NBUF = QCfg<S>::NBUF, TQ = 2 * NW;
-    static constexpr int VP = S + 8;
-    __bf16 Ks[NBUF][S * KP];
-    __bf16 Vs[NBUF][S * KP];
-    __bf16 Kt[NBUF][D * VP];
+    static constexpr int NW = QCfg<S>::NW, NST = QCfg<S>::NST, TQ = 2 * NW;
+    __bf16 Ks[NST][S * D];        // K, row-major, swizzled (chunk_lds.h)
+    __bf16 Vs[NST][S * D];        // V, row-major, swizzled
     int32_t oidx[TQ * KMAX];      // selection tables (see tile_sel.h)
     float ow[TQ * KMAX];
     int32_t sidx[TQ * KMAX];
@@ -83,78 +83,18 @@ struct SmemQ {
     int wsum[NW];
 };
 
-// Staging of one chunk by NT threads in units of vector pairs (rows 2 (p / 16), +1,
-// columns 8 (p % 16)..+7): units [0, 8S) are K pairs, [8S, 16S) V pairs.  K and V go to
-// LDS row-major, K pairs also transposed (key pairs packed) into K^T.
 template <int S>
-struct StageQ {
-    static constexpr int NT = QCfg<S>::NW * 64;
-    static constexpr int NP = S * 8;
-    static constexpr int NU = (2 * NP + NT - 1) / NT;
-    u32x4_t r[2 * NU];
-};
-
-template <int S>
-__device__ __forceinline__ void q_load(StageQ<S>& st, const __bf16* __restrict__ K,
-                                       const __bf16* __restrict__ V, size_t base,
-                                       size_t rowstride, int tid) {
-    using T = StageQ<S>;
-#pragma unroll
-    for (int i = 0; i < T::NU; ++i) {
-        const int u = tid + i * T::NT;
-        if (u < 2 * T::NP) {
-            const bool isk = u < T::NP;
-            const int p = isk ? u : u - T::NP;
-            const __bf16* src = (isk ? K : V) + base + (size_t)((p >> 4) * 2) * rowstride +
-                                (p & 15) * 8;
-            st.r[2 * i] = *reinterpret_cast<const u32x4_t*>(src);
-            st.r[2 * i + 1] = *reinterpret_cast<const u32x4_t*>(src + rowstride);
-        }
-    }
-}
-
-template <int S>
-__device__ __forceinline__ void q_store(const StageQ<S>& st, __bf16* Ks, __bf16* Vs,
-                                        __bf16* Kt, int tid) {
-    using T = StageQ<S>;
-    constexpr int VP = S + 8;
-#pragma unroll
-    for (int i = 0; i < T::NU; ++i) {
-        const int u = tid + i * T::NT;
-        if (u < 2 * T::NP) {
-            const bool isk = u < T::NP;
-            const int p = isk ? u : u - T::NP;
-            const int r = (p >> 4) * 2, col = (p & 15) * 8;
-            __bf16* dst = isk ? Ks : Vs;
-            *reinterpret_cast<u32x4_t*>(&dst[r * KP + col]) = st.r[2 * i];
-            *reinterpret_cast<u32x4_t*>(&dst[(r + 1) * KP + col]) = st.r[2 * i + 1];
-            if (isk) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t a = st.r[2 * i][j], c2 = st.r[2 * i + 1][j];
-                    const int d0 = col + 2 * j, d1 = d0 + 1;
-                    *reinterpret_cast<uint32_t*>(&Kt[d0 * VP + tpos(d0, r, S)]) =
-                        (a & 0xFFFFu) | (c2 << 16);
-                    *reinterpret_cast<uint32_t*>(&Kt[d1 * VP + tpos(d1, r, S)]) =
-                        (a >> 16) | (c2 & 0xFFFF0000u);
-                }
-            }
-        }
-    }
-}
-
-template <int S>
-__global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
+__global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const float* __restrict__ Kbar,
     const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, __bf16* __restrict__ dQ, float* __restrict__ ds_out,
     float* __restrict__ lse_out, float* __restrict__ d_out, int ntiles) {
     using SM = SmemQ<S>;
-    constexpr int NW = SM::NW, NT = NW * 64, TQ = SM::TQ, NBUF = SM::NBUF;
-    constexpr int VP = SM::VP;
+    constexpr int NW = SM::NW, NT = NW * 64, TQ = SM::TQ, NST = SM::NST;
     constexpr int MB = S / 16;
     constexpr int KS2 = S / 32;
+    constexpr int IPC = 2 * (S / 4) / NW; // copy instructions per chunk and wave
     __shared__ SM sm;
 
     const int lid = xcd_logical_id(ntiles * dm.B * dm.G);
@@ -202,33 +142,34 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
     const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
     const float beta = dm.beta;
     const float sl2 = beta * 1.44269504088896341f;
-    StageQ<S> st;
-    // S = 64: chunk u is computed from stage u % 2 while chunk u + 1 (in registers) is
-    // written to the other stage and chunk u + 2 is fetched; one barrier per chunk.
-    // S = 128: one stage, written between two barriers, chunk u + 1 fetched meanwhile.
-    if (nu > 0) q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[0] * S * rowstride, rowstride, tid);
-    if constexpr (NBUF == 2) {
-        if (nu > 0) q_store<S>(st, sm.Ks[0], sm.Vs[0], sm.Kt[0], tid);
-        if (nu > 1)
-            q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[1] * S * rowstride, rowstride, tid);
-        __syncthreads();
-    }
+    auto issue = [&](int u) __attribute__((always_inline)) {
+        const size_t base = bgbase + (size_t)sm.ulist[u] * S * rowstride;
+        chunk_to_lds<S, NW>(K + base, rowstride, sm.Ks[u % NST], wave, lane);
+        chunk_to_lds<S, NW>(V + base, rowstride, sm.Vs[u % NST], wave, lane);
+    };
+    int koff[4], toff[8];
+    row_read_offsets(lane, koff);
+    tr_read_offsets(lane, toff);
+
+    // ring of NST stages: NST - 1 chunks in flight while one is computed
+#pragma unroll
+    for (int u = 0; u < NST - 1; ++u)
+        if (u < nu) issue(u);
     for (int u = 0; u < nu; ++u) {
-        const int c = sm.ulist[u];
-        if constexpr (NBUF == 1) {
-            __syncthreads();
-            q_store<S>(st, sm.Ks[0], sm.Vs[0], sm.Kt[0], tid);
-            __syncthreads();
-            if (u + 1 < nu)
-                q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[u + 1] * S * rowstride,
-                          rowstride, tid);
+        if constexpr (NST == 3) {
+            if (u + 1 < nu) wait_loads_le<IPC>();
+            else wait_loads_le<0>();
+        } else {
+            wait_loads_le<0>();
         }
-        const int bi = (NBUF == 2) ? (u & 1) : 0;
+        barrier_keep_copies();    // chunk u landed for every wave; stage (u - 1) % NST free
+        if (u + NST - 1 < nu) issue(u + NST - 1);
+
+        const int c = sm.ulist[u];
         const bool mine = (cur_c == c);
         if (__ballot(mine) != 0) {
-            const __bf16* Ks = sm.Ks[bi];
-            const __bf16* Vs = sm.Vs[bi];
-            const __bf16* Kt = sm.Kt[bi];
+            const __bf16* Ks = sm.Ks[u % NST];
+            const __bf16* Vs = sm.Vs[u % NST];
             const float wl = mine ? cur_w : 0.f;
             f32x4_t z[MB], dp[MB];
 #pragma unroll
@@ -237,10 +178,8 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    const bf16x8_t ka = ld_bf16x8(&Ks[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
-                    z[mb] = mfma16(ka, qB[ks], z[mb]);
-                    const bf16x8_t va = ld_bf16x8(&Vs[(16 * mb + row) * KP + 32 * ks + 8 * grp]);
-                    dp[mb] = mfma16(va, gB[ks], dp[mb]);
+                    z[mb] = mfma16(ld_bf16x8(Ks + koff[ks] + mb * 2048), qB[ks], z[mb]);
+                    dp[mb] = mfma16(ld_bf16x8(Vs + koff[ks] + mb * 2048), gB[ks], dp[mb]);
                 }
             float m = -INFINITY;
 #pragma unroll
@@ -257,7 +196,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
                     ssum += z[mb][i];
                 }
             ssum = col_sum(ssum);
-            const float inv = 1.f / ssum;
+            const float inv = __builtin_amdgcn_rcpf(ssum);
             float dsum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
@@ -280,10 +219,8 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
                 split8(z[2 * ks2], z[2 * ks2 + 1], zh, zl);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
-                    const int d = 16 * db + row;
-                    const __bf16* kr = &Kt[d * VP];
-                    const bf16x8_t a = cat(ld_bf16x4(kr + tpos(d, 32 * ks2 + 4 * grp, S)),
-                                           ld_bf16x4(kr + tpos(d, 32 * ks2 + 16 + 4 * grp, S)));
+                    const __bf16* kp = Ks + toff[db] + 32 * ks2 * D;
+                    const bf16x8_t a = cat(ld_tr16(kp), ld_tr16(kp + 16 * D));
                     acc[db] = mfma16(a, zh, acc[db]);
                     acc[db] = mfma16(a, zl, acc[db]);
                 }
@@ -305,14 +242,6 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 1) void bwd_q_mfma(
                 cur_s = sp < k ? sm.sslot[tau * k + sp] : 0;
                 cur_w = sp < k ? sm.sw[tau * k + sp] : 0.f;
             }
-        }
-        if constexpr (NBUF == 2) {
-            if (u + 1 < nu)
-                q_store<S>(st, sm.Ks[(u + 1) & 1], sm.Vs[(u + 1) & 1], sm.Kt[(u + 1) & 1], tid);
-            __syncthreads();
-            if (u + 2 < nu)
-                q_load<S>(st, K, V, bgbase + (size_t)sm.ulist[u + 2] * S * rowstride,
-                          rowstride, tid);
         }
     }
     __syncthreads();
