@@ -1,173 +1,169 @@
-// Chunk selection + chunk weights (Sec. 3.1 chunk-selection equation; softmax weights).
+// Chunk selection + chunk weights (Sec. 3.1: the top-k chunks by the landmark score
+// s_c = alpha * (sum_j q_j) . Kbar_c over the chunks before the token's own, and their
+// softmax weights).
 //
-// Workgroup = (b, g, tile of TQ <= 64 tokens inside one query chunk): all tokens of a
-// tile share the candidate set c < floor(t0 / S).  The tile's group queries
-// q~ = sum_j q_j are kept in LDS (fp32); landmarks stream through LDS in blocks of 64;
-// a 4x4 register tile per thread computes 64x64 fp32 scores per block.  Each wave then
-// merges the 64 new scores of its tokens into a running top-k list with a wave-wide
-// partial sort: only lanes above the current k-th score (ballot) are inserted, each
-// insertion is a ballot-rank plus a one-lane shift of the sorted list.  Candidates arrive
-// in increasing chunk order, so "ties to the lower index" is "strictly greater wins".
-// The final list gets softmax weights and is written in descending chunk order.
+// One wave per tile of 64 consecutive tokens of one (b, g); lane = token.  Each lane keeps
+// its group query q~ = sum_j q_j (fp32, d registers) and a running top-KC list (scores and
+// chunk indices, registers, descending).  Candidates are visited in increasing chunk
+// order; the landmark row Kbar_c is the same for every lane, so it comes through scalar
+// loads.  A candidate enters a list only when its score is strictly greater than the
+// list's last entry and moves up past every entry it beats strictly: on equal scores the
+// lower chunk index stays first.  The k best get softmax weights and are written in
+// descending chunk order, padded with -1 / 0.
 #include "common.h"
 
 namespace hsa {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int TQ = 64;      // tokens per tile (max)
-constexpr int NB = 64;      // landmarks per block
-constexpr int KMAX = 32;
+constexpr int kTile = 64;     // tokens per wave
+
+// q~ = sum over the h heads of the group, for token t (d fp32 values in qb)
+template <int D>
+__device__ __forceinline__ void group_query(const bf16* __restrict__ qp, int h, float (&qb)[D]) {
+#pragma unroll
+    for (int e = 0; e < D; ++e) qb[e] = 0.f;
+    for (int j = 0; j < h; ++j) {
+        const uint4* p = reinterpret_cast<const uint4*>(qp + (size_t)j * D);
+#pragma unroll
+        for (int v = 0; v < D / 8; ++v) {
+            const uint4 u = p[v];
+            const uint32_t wds[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                qb[8 * v + 2 * i] += __uint_as_float(wds[i] << 16);
+                qb[8 * v + 2 * i + 1] += __uint_as_float(wds[i] & 0xFFFF0000u);
+            }
+        }
+    }
+}
+
+template <int D>
+__device__ __forceinline__ void group_query(const float* __restrict__ qp, int h, float (&qb)[D]) {
+#pragma unroll
+    for (int e = 0; e < D; ++e) qb[e] = 0.f;
+    for (int j = 0; j < h; ++j) {
+        const float4* p = reinterpret_cast<const float4*>(qp + (size_t)j * D);
+#pragma unroll
+        for (int v = 0; v < D / 4; ++v) {
+            const float4 u = p[v];
+            qb[4 * v] += u.x;
+            qb[4 * v + 1] += u.y;
+            qb[4 * v + 2] += u.z;
+            qb[4 * v + 3] += u.w;
+        }
+    }
+}
+
+template <typename T, int D, int KC>
+__global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restrict__ Q,
+                                                       const float* __restrict__ Kbar,
+                                                       int32_t* __restrict__ idx,
+                                                       float* __restrict__ w, int ntiles) {
+    const int lane = threadIdx.x;
+    // latest tiles (most candidates) first
+    const int nbg = dm.B * dm.G;
+    const int tile = ntiles - 1 - (int)blockIdx.x / nbg;
+    const int bg = (int)blockIdx.x % nbg, b = bg / dm.G, g = bg % dm.G;
+    const int t0 = tile * kTile;
+    const int t = t0 + lane;
+    const bool valid = t < dm.L;
+    const int ncand = valid ? t / dm.S : 0;
+    const int nwave = (min(t0 + kTile, dm.L) - 1) / dm.S;     // candidates of the last token
+    const int k = dm.k;
+
+    float qb[D];
+    if (valid) {
+        group_query<D>(Q + (((size_t)b * dm.L + t) * dm.H + (size_t)g * dm.h) * D, dm.h, qb);
+    } else {
+#pragma unroll
+        for (int e = 0; e < D; ++e) qb[e] = 0.f;
+    }
+    float ls[KC];
+    int lc[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        ls[j] = -INFINITY;
+        lc[j] = -1;
+    }
+
+    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D;   // row c at kb + c G D
+    const size_t cstride = (size_t)dm.G * D;
+    for (int c = 0; c < nwave; ++c) {
+        const float* kr = kb + (size_t)c * cstride;              // same for every lane
+        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+        for (int e = 0; e < D; e += 4) {
+            a0 = fmaf(qb[e], kr[e], a0);
+            a1 = fmaf(qb[e + 1], kr[e + 1], a1);
+            a2 = fmaf(qb[e + 2], kr[e + 2], a2);
+            a3 = fmaf(qb[e + 3], kr[e + 3], a3);
+        }
+        float s = (c < ncand) ? dm.alpha * ((a0 + a1) + (a2 + a3)) : -INFINITY;
+        if (__ballot(s > ls[KC - 1]) == 0) continue;
+        int ci = c;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) {          // insertion: strictly greater moves up
+            const bool gt = s > ls[j];
+            const float ts = gt ? s : ls[j];
+            const int tc = gt ? ci : lc[j];
+            s = gt ? ls[j] : s;
+            ci = gt ? lc[j] : ci;
+            ls[j] = ts;
+            lc[j] = tc;
+        }
+    }
+    if (!valid) return;
+
+    // softmax over the k best, written in descending chunk order
+    const int n = min(k, ncand);
+    const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
+    float ex[KC];
+    float z = 0.f;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        ex[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
+        z += ex[j];
+    }
+    const float iz = 1.f / z;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        if (j >= k) break;
+        if (j < n) {
+            int rank = 0;
+#pragma unroll
+            for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
+            idx[o + rank] = lc[j];
+            w[o + rank] = ex[j] * iz;
+        } else {
+            idx[o + j] = -1;
+            w[o + j] = 0.f;
+        }
+    }
+}
 
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __restrict__ Q,
-                                                          const float* __restrict__ Kbar,
-                                                          int32_t* __restrict__ idx,
-                                                          float* __restrict__ w, int tq) {
-    constexpr int DP = D + 1;
-    __shared__ float qs[TQ * DP];
-    __shared__ float kb[NB * DP];
-    __shared__ float sc[TQ * (NB + 1)];
-    __shared__ float lst_s[TQ * KMAX];
-    __shared__ int lst_c[TQ * KMAX];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
-    const int t0 = blockIdx.x * tq;
-    const int ntok = min(tq, dm.L - t0);
-    const int ncand = t0 / dm.S;
-    const int k = dm.k, h = dm.h;
-
-    // group queries of the tile
-    for (int i = tid; i < TQ * D; i += kThreads) {
-        const int tau = i / D, e = i % D;
-        float s = 0.f;
-        if (tau < ntok) {
-            const T* qp = Q + (((size_t)b * dm.L + t0 + tau) * dm.H + (size_t)g * h) * D + e;
-            for (int j = 0; j < h; ++j) s += to_f32(qp[(size_t)j * D]);
-        }
-        qs[tau * DP + e] = s;
-    }
-    for (int i = tid; i < TQ * KMAX; i += kThreads) {
-        lst_s[i] = -INFINITY;
-        lst_c[i] = 0x7FFFFFFF;
-    }
-    int count = 0;   // entries in every running list of this tile (identical for all tokens)
-
-    const int ty = tid >> 4, tx = tid & 15;
-    for (int cb = 0; cb < ncand; cb += NB) {
-        const int nb = min(NB, ncand - cb);
-        __syncthreads();
-        for (int i = tid; i < nb * D; i += kThreads) {
-            const int cl = i / D, e = i % D;
-            kb[cl * DP + e] = Kbar[(((size_t)b * dm.C + cb + cl) * dm.G + g) * D + e];
-        }
-        __syncthreads();
-        float acc[4][4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int m = 0; m < 4; ++m) acc[i][m] = 0.f;
-        for (int e = 0; e < D; ++e) {
-            float qv[4], kv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) qv[i] = qs[(ty * 4 + i) * DP + e];
-#pragma unroll
-            for (int m = 0; m < 4; ++m) kv[m] = kb[(tx + 16 * m) * DP + e];
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int m = 0; m < 4; ++m) acc[i][m] = fmaf(qv[i], kv[m], acc[i][m]);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const int cl = tx + 16 * m;
-                sc[(ty * 4 + i) * (NB + 1) + cl] = (cl < nb) ? dm.alpha * acc[i][m] : -INFINITY;
-            }
-        __syncthreads();
-
-        // merge: wave `wave` owns tokens [wave*16, wave*16+16)
-        for (int tt = 0; tt < 16; ++tt) {
-            const int tau = wave * 16 + tt;
-            if (tau >= ntok) break;
-            const float s = sc[tau * (NB + 1) + lane];   // -inf for lanes >= nb
-            float ls = (lane < k) ? lst_s[tau * KMAX + lane] : -INFINITY;
-            int lc = (lane < k) ? lst_c[tau * KMAX + lane] : 0x7FFFFFFF;
-            int cnt = count;
-            float thr = (cnt == k) ? __shfl(ls, k - 1, 64) : -INFINITY;
-            uint64_t mask = __ballot(s > thr);
-            while (mask) {
-                const int src = __ffsll((unsigned long long)mask) - 1;
-                const float sn = __shfl(s, src, 64);
-                const int cn = cb + src;
-                const bool ahead = (lane < k) && (ls > sn || (ls == sn && lc < cn));
-                const int pos = __popcll(__ballot(ahead));
-                const float ls_up = __shfl_up(ls, 1, 64);
-                const int lc_up = __shfl_up(lc, 1, 64);
-                if (lane < k) {
-                    if (lane > pos) {
-                        ls = ls_up;
-                        lc = lc_up;
-                    } else if (lane == pos) {
-                        ls = sn;
-                        lc = cn;
-                    }
-                }
-                cnt = min(cnt + 1, k);
-                thr = (cnt == k) ? __shfl(ls, k - 1, 64) : -INFINITY;
-                mask &= ~(1ull << src);
-                mask &= __ballot(s > thr);
-            }
-            if (lane < k) {
-                lst_s[tau * KMAX + lane] = ls;
-                lst_c[tau * KMAX + lane] = lc;
-            }
-        }
-        count = min(count + nb, k);
-    }
-    __syncthreads();
-
-    // finalize: softmax weights, descending chunk order, padding
-    const int n = min(k, ncand);
-    for (int tt = 0; tt < 16; ++tt) {
-        const int tau = wave * 16 + tt;
-        if (tau >= ntok) break;
-        const int t = t0 + tau;
-        const float ls = (lane < n) ? lst_s[tau * KMAX + lane] : -INFINITY;
-        const int lc = (lane < n) ? lst_c[tau * KMAX + lane] : -1;
-        const float m = __shfl(ls, 0, 64);
-        const float ex = (lane < n) ? expf(ls - m) : 0.f;
-        const float z = wave_sum(ex);
-        int rank = 0;
-        for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
-        const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
-        if (lane < n) {
-            idx[o + rank] = lc;
-            w[o + rank] = ex / z;
-        } else if (lane < k) {
-            idx[o + lane] = -1;
-            w[o + lane] = 0.f;
-        }
-    }
+hipError_t launch_d(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
+                    hipStream_t st) {
+    const int ntiles = cdiv(dm.L, kTile);
+    const dim3 grid(ntiles * dm.B * dm.G);
+    HSA_TIMED("select_kernel", st);
+    if (dm.k <= 8)
+        hipLaunchKernelGGL((select_kernel<T, D, 8>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
+                           Kbar, idx, w, ntiles);
+    else if (dm.k <= 16)
+        hipLaunchKernelGGL((select_kernel<T, D, 16>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
+                           Kbar, idx, w, ntiles);
+    else
+        hipLaunchKernelGGL((select_kernel<T, D, 32>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
+                           Kbar, idx, w, ntiles);
+    return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_t(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
                     hipStream_t st) {
-    const int tq = dm.S < TQ ? dm.S : TQ;
-    dim3 grid(cdiv(dm.L, tq), dm.B * dm.G);
-    if (dm.d == 128) {
-        HSA_TIMED("select_kernel", st);
-        hipLaunchKernelGGL((select_kernel<T, 128>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, Kbar, idx, w, tq);
-    } else {
-        HSA_TIMED("select_kernel", st);
-        hipLaunchKernelGGL((select_kernel<T, 64>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, Kbar, idx, w, tq);
-    }
-    return hipGetLastError();
+    return dm.d == 128 ? launch_d<T, 128>(dm, Q, Kbar, idx, w, st)
+                       : launch_d<T, 64>(dm, Q, Kbar, idx, w, st);
 }
 
 }  // namespace
