@@ -34,7 +34,6 @@ namespace {
 constexpr int D = 128;
 constexpr int HG = 8;
 constexpr int KMAX = 32;
-constexpr int KP = D + 8;
 constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -298,40 +297,38 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
 //     P  = exp(beta Z - lse_row),  dZ = w P (dP - D_row)            (stored by the query pass)
 //     dV_sub += (w P)^T dO_rows,  dK_sub += dZ^T Q_rows              (MFMA, K = 32 rows;
 //                                                 w P and dZ as bf16 hi/lo pairs)
-// The C layout of Z feeds the A operand of the last two products directly (row
-// permutation applied to the transposed Q / dO rows in LDS).  The landmark term
-// dKbar_c / S = (alpha / S) sum ds q~ is folded into dZ.  No atomics; fixed token order.
-constexpr int RP = 32 + 8;        // padded row count of the transposed Q / dO group tiles
+// A group's Q and dO rows (and their lse / D) are copied straight into a ring of LDS stages
+// (chunk_lds.h), two groups in flight while one is computed.  Z and dP read the rows; the
+// last two products read them transposed, in the row order of the C layout of Z, which
+// then serves as their A operand directly.  The landmark term dKbar_c / S =
+// (alpha / S) sum ds q~ is folded into dZ.  No atomics; fixed token order.
 constexpr int LISTCAP = 64 * 32 + 4;
+constexpr int KV_NST = 3;
+
+struct KvStage {
+    __bf16 q[32 * D];             // Q rows of the group (row 8 token + head), swizzled
+    __bf16 g[32 * D];             // dO rows
+    float meta[256];              // [0, 32): lse per row, [32, 64): D per row, rest scratch
+};
 
 struct SmemKV {
-    __bf16 Qr[32 * KP];
-    __bf16 Gr[32 * KP];
-    __bf16 Qt[D * RP];
-    __bf16 Gt[D * RP];
-    float lse[32], dd[32];
-    float tw[4], tds[4];
+    KvStage st[KV_NST];
     int list[LISTCAP];
     float lw[LISTCAP], lds[LISTCAP];
     uint8_t lslot[LISTCAP];
     int nlist;
 };
 
-// Registers of one staged group: two rows (same token) of one 8-column block of Q and dO,
-// plus the two rows' statistics (held by the thread that stages column block 0).
-struct GroupRegs {
-    u32x4_t q0, q1, g0, g1;
-    float l0, l1, d0, d1;
-};
-
 template <int S>
-__global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
+__global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, const float* __restrict__ ds, const float* __restrict__ lse,
     const float* __restrict__ dd, const uint32_t* __restrict__ bm, int nwords,
     __bf16* __restrict__ dK, __bf16* __restrict__ dV) {
-    constexpr int NT = S * 4;               // threads: S / 16 waves
+    constexpr int NW = S / 16;              // waves
+    constexpr int NT = NW * 64;
+    constexpr int BPW = 8 / NW;             // 1 KB row blocks of Q (and of dO) per wave
     __shared__ SmemKV sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
@@ -375,55 +372,37 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
     const float beta = dm.beta;
     const float l2e = 1.44269504088896341f;
     const float lmk = dm.alpha / (beta * (float)S);
+    int koff[4], toff[8];
+    row_read_offsets(lane, koff);
+    tr_read_offsets(lane, toff);
 
-    // staging unit of thread tid < 256: rows sr, sr + 1 (one token), columns scol..scol+7
-    const int sr = (tid >> 4) * 2, scol = (tid & 15) * 8;
-    auto prefetch = [&](int gi, int nl, GroupRegs& R) __attribute__((always_inline)) {
-        R.q0 = R.q1 = R.g0 = R.g1 = u32x4_t{0, 0, 0, 0};
-        R.l0 = R.l1 = R.d0 = R.d1 = 0.f;
-        if (tid >= 256) return;
-        const int li = gi * 4 + (sr >> 3);
-        if (li >= nl) return;
-        const int t = sm.list[li];
-        const size_t o = (((size_t)b * dm.L + t) * dm.H + (size_t)g * HG + (sr & 7)) * D + scol;
-        R.q0 = *reinterpret_cast<const u32x4_t*>(Q + o);
-        R.q1 = *reinterpret_cast<const u32x4_t*>(Q + o + D);
-        R.g0 = *reinterpret_cast<const u32x4_t*>(dO + o);
-        R.g1 = *reinterpret_cast<const u32x4_t*>(dO + o + D);
-        if (scol == 0) {
-            const size_t so =
-                ((((size_t)b * dm.L + t) * dm.G + g) * k + sm.lslot[li]) * HG + (sr & 7);
-            R.l0 = lse[so];
-            R.l1 = lse[so + 1];
-            R.d0 = dd[so];
-            R.d1 = dd[so + 1];
-        }
-    };
-    auto stage = [&](int gi, int nl, const GroupRegs& R) __attribute__((always_inline)) {
-        if (tid < 4) {
-            const int li = gi * 4 + tid;
-            sm.tw[tid] = li < nl ? sm.lw[li] : 0.f;
-            sm.tds[tid] = li < nl ? sm.lds[li] : 0.f;
-        }
-        if (tid >= 256) return;
-        *reinterpret_cast<u32x4_t*>(&sm.Qr[sr * KP + scol]) = R.q0;
-        *reinterpret_cast<u32x4_t*>(&sm.Qr[(sr + 1) * KP + scol]) = R.q1;
-        *reinterpret_cast<u32x4_t*>(&sm.Gr[sr * KP + scol]) = R.g0;
-        *reinterpret_cast<u32x4_t*>(&sm.Gr[(sr + 1) * KP + scol]) = R.g1;
+    // copies of group gi (tokens 4 gi .. 4 gi + 3 of the list; a missing token repeats the
+    // group's first one, with weight and ds 0): wave w copies the Q and dO row blocks
+    // w BPW .. w BPW + BPW - 1 (4 rows = half a token each); the last wave also copies the
+    // lse and D of the 32 rows
+    auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
+        KvStage& st = sm.st[gi % KV_NST];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int sh = (e & 1) ? 16 : 0;
-            const uint32_t qa = (R.q0[e >> 1] >> sh) & 0xFFFFu, qb = (R.q1[e >> 1] >> sh) & 0xFFFFu;
-            const uint32_t ga = (R.g0[e >> 1] >> sh) & 0xFFFFu, gb = (R.g1[e >> 1] >> sh) & 0xFFFFu;
-            const int dd2 = scol + e, pos = tpos(dd2, sr, 32);
-            *reinterpret_cast<uint32_t*>(&sm.Qt[dd2 * RP + pos]) = qa | (qb << 16);
-            *reinterpret_cast<uint32_t*>(&sm.Gt[dd2 * RP + pos]) = ga | (gb << 16);
+        for (int i = 0; i < BPW; ++i) {
+            const int blk = wave * BPW + i;
+            const int r = blk * 4 + (lane >> 4);
+            int li = gi * 4 + (r >> 3);
+            if (li >= nl) li = gi * 4;
+            const size_t o = (((size_t)b * dm.L + sm.list[li]) * dm.H + (size_t)g * HG + (r & 7)) * D +
+                             unit_pos(r, lane & 15) * 8;
+            lds_copy16(Q + o, __builtin_amdgcn_readfirstlane(lds_address(st.q + blk * 512)));
+            lds_copy16(dO + o, __builtin_amdgcn_readfirstlane(lds_address(st.g + blk * 512)));
         }
-        if (scol == 0) {
-            sm.lse[sr] = R.l0;
-            sm.lse[sr + 1] = R.l1;
-            sm.dd[sr] = R.d0;
-            sm.dd[sr + 1] = R.d1;
+        if (wave == NW - 1) {
+            // lanes 16 m + 2 j + h (j < 4 tokens, h halves of the 8 heads): m = 0 lse, m = 1 D,
+            // m >= 2 repeat (scratch)
+            int li = gi * 4 + ((lane & 7) >> 1);
+            if (li >= nl) li = gi * 4;
+            const size_t so =
+                ((((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li]) * HG +
+                4 * (lane & 1);
+            lds_copy16(((lane >> 3) & 1 ? dd : lse) + so,
+                       __builtin_amdgcn_readfirstlane(lds_address(st.meta)));
         }
     };
 
@@ -460,7 +439,7 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             const int t = sm.list[li];
             const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
             int slot = 0;
-            for (int s2 = 0; s2 < k; ++s2)
+            for (int s2 = k - 1; s2 >= 0; --s2)
                 if (idx[so + s2] == c) slot = s2;
             sm.lslot[li] = (uint8_t)slot;
             sm.lw[li] = w[so + slot];
@@ -468,12 +447,20 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
         }
         __syncthreads();
         const int ngroups = last_round ? (nl + 3) / 4 : nl / 4;
-        GroupRegs R;
-        if (ngroups > 0) prefetch(0, nl, R);
+#pragma unroll
+        for (int u = 0; u < KV_NST - 1; ++u)
+            if (u < ngroups) issue(u, nl);
         for (int gi = 0; gi < ngroups; ++gi) {
-            stage(gi, nl, R);
-            __syncthreads();
-            if (gi + 1 < ngroups) prefetch(gi + 1, nl, R);
+            // group gi has landed once at most the next group's copies remain
+            if (gi + 1 < ngroups) {
+                if (wave == NW - 1) wait_loads_le<2 * BPW + 1>();
+                else wait_loads_le<2 * BPW>();
+            } else {
+                wait_loads_le<0>();
+            }
+            barrier_keep_copies();            // ... for every wave; stage (gi - 1) % NST free
+            if (gi + KV_NST - 1 < ngroups) issue(gi + KV_NST - 1, nl);
+            const KvStage& st = sm.st[gi % KV_NST];
 
             // ---- Z, dP for the wave's 16 keys ---------------------------------------------
             f32x4_t z[2], dp[2];
@@ -482,10 +469,8 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) {
-                    const bf16x8_t qa = ld_bf16x8(&sm.Qr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
-                    z[rb] = mfma16(qa, kB[ks], z[rb]);
-                    const bf16x8_t ga = ld_bf16x8(&sm.Gr[(16 * rb + row) * KP + 32 * ks + 8 * grp]);
-                    dp[rb] = mfma16(ga, vB[ks], dp[rb]);
+                    z[rb] = mfma16(ld_bf16x8(st.q + koff[ks] + rb * 2048), kB[ks], z[rb]);
+                    dp[rb] = mfma16(ld_bf16x8(st.g + koff[ks] + rb * 2048), vB[ks], dp[rb]);
                 }
             // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2).  The landmark term
             // dKbar_c / S = (alpha / S) sum_rows ds_tok q_row reaches every key of the chunk, so
@@ -493,11 +478,12 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             f32x4_t pw[2], dz[2];
 #pragma unroll
             for (int rb = 0; rb < 2; ++rb) {
-                const int tk = 2 * rb + (grp >> 1);
-                const float wt = sm.tw[tk];
-                const float lm = sm.tds[tk] * lmk;
-                const f32x4_t lv = *reinterpret_cast<const f32x4_t*>(&sm.lse[16 * rb + 4 * grp]);
-                const f32x4_t dv = *reinterpret_cast<const f32x4_t*>(&sm.dd[16 * rb + 4 * grp]);
+                const int li = gi * 4 + 2 * rb + (grp >> 1);
+                const float wt = li < nl ? sm.lw[li] : 0.f;
+                const float lm = li < nl ? sm.lds[li] * lmk : 0.f;
+                const f32x4_t lv = *reinterpret_cast<const f32x4_t*>(&st.meta[16 * rb + 4 * grp]);
+                const f32x4_t dv =
+                    *reinterpret_cast<const f32x4_t*>(&st.meta[32 + 16 * rb + 4 * grp]);
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const float p = fast_exp2((beta * z[rb][i] - lv[i]) * l2e);
@@ -512,22 +498,18 @@ __global__ __launch_bounds__(S * 4, 1) void bwd_kv_mfma(
             split8(dz[0], dz[1], dzh, dzl);
 #pragma unroll
             for (int db = 0; db < 8; ++db) {
-                const int d = 16 * db + row;
-                const int p0 = tpos(d, 4 * grp, 32), p1 = tpos(d, 16 + 4 * grp, 32);
-                const __bf16* gr = &sm.Gt[d * RP];
-                const bf16x8_t gb = cat(ld_bf16x4(gr + p0), ld_bf16x4(gr + p1));
+                const bf16x8_t gb = cat(ld_tr16(st.g + toff[db]), ld_tr16(st.g + toff[db] + 16 * D));
                 aV[db] = mfma16(pvh, gb, aV[db]);
                 aV[db] = mfma16(pvl, gb, aV[db]);
-                const __bf16* qr = &sm.Qt[d * RP];
-                const bf16x8_t qb = cat(ld_bf16x4(qr + p0), ld_bf16x4(qr + p1));
+                const bf16x8_t qb = cat(ld_tr16(st.q + toff[db]), ld_tr16(st.q + toff[db] + 16 * D));
                 aK[db] = mfma16(dzh, qb, aK[db]);
                 aK[db] = mfma16(dzl, qb, aK[db]);
             }
-            __syncthreads();
         }
         // keep the tokens of an incomplete group for the next batch
         if (!last_round) {
             const int rem = nl - ngroups * 4;
+            __syncthreads();
             if (tid < rem) sm.list[tid] = sm.list[ngroups * 4 + tid];
             __syncthreads();
             if (tid == 0) sm.nlist = rem;
