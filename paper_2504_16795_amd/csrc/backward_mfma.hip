@@ -69,8 +69,7 @@ struct QCfg<128> {
 template <int S>
 struct SmemQ {
     static constexpr int NW = QCfg<S>::NW, NST = QCfg<S>::NST, TQ = 2 * NW;
-    __bf16 Ks[NST][S * D];        // K, row-major, swizzled (chunk_lds.h)
-    __bf16 Vs[NST][S * D];        // V, row-major, swizzled
+    ChunkStage<S> st[NST];        // K, V rows, swizzled (chunk_lds.h)
     int32_t oidx[TQ * KMAX];      // selection tables (see tile_sel.h)
     float ow[TQ * KMAX];
     int32_t sidx[TQ * KMAX];
@@ -143,8 +142,8 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
     const float sl2 = beta * 1.44269504088896341f;
     auto issue = [&](int u) __attribute__((always_inline)) {
         const size_t base = bgbase + (size_t)sm.ulist[u] * S * rowstride;
-        chunk_to_lds<S, NW>(K + base, rowstride, sm.Ks[u % NST], wave, lane);
-        chunk_to_lds<S, NW>(V + base, rowstride, sm.Vs[u % NST], wave, lane);
+        chunk_to_lds<S, NW>(K + base, rowstride, sm.st[u % NST].k, wave, lane);
+        chunk_to_lds<S, NW>(V + base, rowstride, sm.st[u % NST].v, wave, lane);
     };
     int koff[4], toff[8];
     row_read_offsets(lane, koff);
@@ -167,9 +166,10 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
         const int c = sm.ulist[u];
         const bool mine = (cur_c == c);
         if (__ballot(mine) != 0) {
-            const __bf16* Ks = sm.Ks[u % NST];
-            const __bf16* Vs = sm.Vs[u % NST];
+            const ChunkStage<S>& cs = sm.st[u % NST];
             const float wl = mine ? cur_w : 0.f;
+            // K rows at kp[ks] + mb * 2048, V rows at the same offsets in cs.v
+            constexpr int VOFF = S * D;
             f32x4_t z[MB], dp[MB];
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb) z[mb] = dp[mb] = zero4();
@@ -177,8 +177,8 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) {
-                    z[mb] = mfma16(ld_bf16x8(Ks + koff[ks] + mb * 2048), qB[ks], z[mb]);
-                    dp[mb] = mfma16(ld_bf16x8(Vs + koff[ks] + mb * 2048), gB[ks], dp[mb]);
+                    z[mb] = mfma16(ld_bf16x8(cs.k + koff[ks] + mb * 2048), qB[ks], z[mb]);
+                    dp[mb] = mfma16(ld_bf16x8(cs.k + koff[ks] + VOFF + mb * 2048), gB[ks], dp[mb]);
                 }
             float m = -INFINITY;
 #pragma unroll
@@ -186,40 +186,36 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
             m = col_max(m);
-            float ssum = 0.f;
+            const float msl = m * sl2;
+            // unnormalised probabilities Pu = exp(beta (z - m)), their sum and sum Pu dP
+            float ssum = 0.f, dsu = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    z[mb][i] = fast_exp2((z[mb][i] - m) * sl2);
+                    z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
                     ssum += z[mb][i];
+                    dsu = fmaf(z[mb][i], dp[mb][i], dsu);
                 }
             ssum = col_sum(ssum);
             const float inv = __builtin_amdgcn_rcpf(ssum);
-            float dsum = 0.f;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    z[mb][i] *= inv;                                  // P
-                    dsum = fmaf(z[mb][i], dp[mb][i], dsum);
-                }
-            dsum = col_sum(dsum);                                     // D of this row
+            const float dsum = col_sum(dsu) * inv;                    // D of this row
             // dZ = w P (dP - D), fed as the B operand of dQ^T += K^T dZ^T.  sum_s dZ_s = 0,
             // so dQ is a cancelling sum: dZ enters as a bf16 pair (hi + lo, ~16 mantissa
             // bits) to keep its rounding from being amplified by the key magnitudes.
+            const float wp = wl * inv;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) z[mb][i] = wl * z[mb][i] * (dp[mb][i] - dsum);
+                for (int i = 0; i < 4; ++i) z[mb][i] = (wp * z[mb][i]) * (dp[mb][i] - dsum);
 #pragma unroll
             for (int ks2 = 0; ks2 < KS2; ++ks2) {
                 bf16x8_t zh, zl;
                 split8(z[2 * ks2], z[2 * ks2 + 1], zh, zl);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
-                    const __bf16* kp = Ks + toff[db] + 32 * ks2 * D;
-                    const bf16x8_t a = cat(ld_tr16(kp), ld_tr16(kp + 16 * D));
+                    const __bf16* p = cs.k + toff[db] + 32 * ks2 * D;
+                    const bf16x8_t a = cat(ld_tr16(p), ld_tr16(p + 16 * D));
                     acc[db] = mfma16(a, zh, acc[db]);
                     acc[db] = mfma16(a, zl, acc[db]);
                 }

@@ -32,6 +32,14 @@ constexpr int kChunkD = 128;          // bf16 elements per row
 __device__ __forceinline__ int swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 __device__ __forceinline__ int unit_pos(int r, int j) { return j ^ swz(r); }
 
+// One LDS stage of a chunk: K and V rows, each swizzled.  V sits at a fixed offset from K,
+// so reads of both use one address register per lane and immediate offsets.
+template <int S>
+struct ChunkStage {
+    __bf16 k[S * kChunkD];
+    __bf16 v[S * kChunkD];
+};
+
 // One global_load_lds_dwordx4: lane l copies 16 bytes from gsrc to LDS byte address
 // lds_base + 16 l (lds_base wave-uniform, passed in M0).  Issued as inline assembly: the
 // compiler's wait insertion would otherwise make every later transposed LDS read wait for

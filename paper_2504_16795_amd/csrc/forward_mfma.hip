@@ -48,8 +48,7 @@ struct FCfg<128> {
 template <int S>
 struct Smem {
     static constexpr int NW = FCfg<S>::NW, TQ = 2 * NW, NST = FCfg<S>::NST;
-    __bf16 Ks[NST][S * D];                        // K, row-major, swizzled (chunk_lds.h)
-    __bf16 Vs[NST][S * D];                        // V, row-major, swizzled
+    ChunkStage<S> st[NST];                        // K, V rows, swizzled (chunk_lds.h)
     int32_t oidx[TQ * KMAX];                      // selection tables (see tile_sel.h)
     float ow[TQ * KMAX];
     int32_t sidx[TQ * KMAX];
@@ -99,8 +98,8 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     // ---- selections of the tile, sorted per token, and their union ----------------------
     uint32_t* ubits;
     if constexpr (NST > 2) {
-        static_assert(sizeof(sm.Ks[NST - 1]) >= UWORDS * 4, "bitmap does not fit the stage");
-        ubits = reinterpret_cast<uint32_t*>(sm.Ks[NST - 1]);   // first written in the loop
+        static_assert(sizeof(sm.st[NST - 1]) >= UWORDS * 4, "bitmap does not fit the stage");
+        ubits = reinterpret_cast<uint32_t*>(sm.st[NST - 1].k);   // first written in the loop
     } else {
         ubits = sm.ubits;
     }
@@ -121,8 +120,8 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
     auto issue = [&](int u) __attribute__((always_inline)) {
         const size_t base = bgbase + (size_t)sm.ulist[u] * S * rowstride;
-        chunk_to_lds<S, NW>(K + base, rowstride, sm.Ks[u % NST], wave, lane);
-        chunk_to_lds<S, NW>(V + base, rowstride, sm.Vs[u % NST], wave, lane);
+        chunk_to_lds<S, NW>(K + base, rowstride, sm.st[u % NST].k, wave, lane);
+        chunk_to_lds<S, NW>(V + base, rowstride, sm.st[u % NST].v, wave, lane);
     };
     int koff[4], toff[8];
     row_read_offsets(lane, koff);
@@ -146,8 +145,7 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
         const int c = sm.ulist[u];
         const bool mine = (cur_c == c);
         if (__ballot(mine) != 0) {
-            const __bf16* Ks = sm.Ks[u % NST];
-            const __bf16* Vs = sm.Vs[u % NST];
+            const ChunkStage<S>& cs = sm.st[u % NST];
             const float wl = mine ? cur_w : 0.f;
             // Z^T = K_c Q^T
             f32x4_t z[MB];
@@ -157,20 +155,20 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
             for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb)
-                    z[mb] = mfma16(ld_bf16x8(Ks + koff[ks] + mb * 2048), qB[ks], z[mb]);
+                    z[mb] = mfma16(ld_bf16x8(cs.k + koff[ks] + mb * 2048), qB[ks], z[mb]);
             // softmax over the S keys of each row (column `row` of Z^T)
             float m = -INFINITY;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-            m = col_max(m);
+            const float msl = col_max(m) * sl2;
             float ssum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    z[mb][i] = fast_exp2((z[mb][i] - m) * sl2);
+                    z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
                     ssum += z[mb][i];
                 }
             ssum = col_sum(ssum);
@@ -181,8 +179,8 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
                 const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
-                    const __bf16* vp = Vs + toff[db] + 32 * ks2 * D;
-                    acc[db] = mfma16(cat(ld_tr16(vp), ld_tr16(vp + 16 * D)), pb, acc[db]);
+                    const __bf16* p = cs.v + toff[db] + 32 * ks2 * D;
+                    acc[db] = mfma16(cat(ld_tr16(p), ld_tr16(p + 16 * D)), pb, acc[db]);
                 }
             }
             if (mine) {
