@@ -54,12 +54,14 @@ __host__ __device__ inline WsLayout ws_layout(const Dims& dm) {
     return l;
 }
 
-// Query-pass shape: waves per workgroup (one row block each) and chunk stages in LDS.
+// Query-pass shape: waves per workgroup (one row block each) and chunk stages in LDS.  At
+// S = 64 two workgroups of 4 waves share a CU (76 KB of LDS each), so one computes while
+// the other waits at its per-chunk barrier.
 template <int S>
 struct QCfg;
 template <>
 struct QCfg<64> {
-    static constexpr int NW = 8, NST = 3;
+    static constexpr int NW = 4, NST = 2;
 };
 template <>
 struct QCfg<128> {

@@ -1,9 +1,8 @@
 // bf16 MFMA forward of hierarchical sparse attention (Sec. 3.1.1), for h = 8 query heads
 // per KV head, d = 128, S in {64, 128}.
 //
-// Workgroup = (b, g, tile of 2 NW tokens inside one query chunk), NW waves (16 for S = 64,
-// 8 for S = 128); wave w owns tokens 2w, 2w+1 as one row block of 16 rows (2 tokens x 8
-// heads).
+// Workgroup = (b, g, tile of 2 NW tokens inside one query chunk), NW = 8 waves; wave w
+// owns tokens 2w, 2w+1 as one row block of 16 rows (2 tokens x 8 heads).
 //  1. Each token's valid selections are sorted by descending chunk and the tile's union is
 //     listed in the same order (tile_sel.h), so every lane follows its token's slot list
 //     with a register pointer.
@@ -33,12 +32,14 @@ constexpr int KMAX = 32;
 constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
 // Waves per workgroup (a tile holds 2 NW tokens, 2 per wave), the waves per SIMD the
-// register budget is sized for, and the chunk stages in LDS.
+// register budget is sized for, and the chunk stages in LDS.  At S = 64 two workgroups of
+// 8 waves share a CU (80 KB of LDS and 128 registers each): while one waits at its
+// per-chunk barrier or for a copy, the other computes.
 template <int S>
 struct FCfg;
 template <>
 struct FCfg<64> {
-    static constexpr int NW = 16, WPE = 4, NST = 3;
+    static constexpr int NW = 8, WPE = 4, NST = 2;
 };
 template <>
 struct FCfg<128> {
