@@ -118,7 +118,35 @@ def time_training(sh, dev, steps, warmup, torch, hsa):
     return ms, kern
 
 
-def roofline_of(kern, sh, pairs):
+def source_digest():
+    """sha256 over the HIP sources and headers of the library (traffic figures measured on
+    other sources are stale)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2504_16795_amd", "csrc")
+    for f in sorted(glob.glob(os.path.join(csrc, "*.hip")) + glob.glob(os.path.join(csrc, "*.h"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def traffic_of(name, workload):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated) of `name` on `workload`
+    from profiles/traffic_<workload>.json, or None if absent or taken on other sources."""
+    path = os.path.join(ROOT, "profiles", "traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    if rec.get("source_sha256") != source_digest():
+        return None
+    k = rec.get("kernels", {}).get(name)
+    return None if k is None else k["hbm_bytes_per_launch"]
+
+
+def roofline_of(kern, sh, pairs, workload):
     """Roofline entry of the kernel with the largest total time in the timed region."""
     name, (cnt, tot) = max(kern.items(), key=lambda kv: kv[1][1])
     work = kernel_work(name, sh, pairs)
@@ -131,7 +159,8 @@ def roofline_of(kern, sh, pairs):
     else:
         achieved = amount / (avg_ms * 1e-3) / 1e9
     return {"kernel": name, "bound": bound, "achieved": round(achieved, 3), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 5), "traffic": None,
+            "unit": unit, "frac": round(achieved / peak, 5),
+            "traffic": traffic_of(name, workload),
             "avg_ms": round(avg_ms, 5), "launches": cnt,
             "work_per_launch": amount,
             "work_unit": "flop" if unit == "TFLOP/s" else "byte"}
@@ -220,6 +249,64 @@ def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
                           done, sh.B * G, name, el)}
 
 
+CALIB_BYTES = 256 << 20
+
+
+def pmc_run(workload, steps, torch, hsa):
+    """Workload for counter collection under rocprofv3 --pmc: a device copy of CALIB_BYTES
+    (the calibration of FETCH_SIZE / WRITE_SIZE) three times, then `steps` steps."""
+    x = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    sh, _, dev, _ = make_training(workload, torch)
+    time_training(sh, dev, steps, 0, torch, hsa)
+    torch.cuda.synchronize()
+
+
+def pmc_summarize(workload, fetch_csv, write_csv, out_path):
+    """Per-kernel HBM traffic from the two counter passes, calibrated on the copy kernel:
+    factor = bytes the copy moves / bytes the counter reports for it."""
+    import csv
+    from collections import defaultdict
+
+    def read(path, counter):
+        per = defaultdict(list)
+        for r in csv.DictReader(open(path)):
+            if r["Counter_Name"].startswith(counter):
+                per[r["Kernel_Name"]].append(float(r["Counter_Value"]) * 1024.0)   # KiB
+        return per
+
+    fetch, write = read(fetch_csv, "FETCH_SIZE"), read(write_csv, "WRITE_SIZE")
+    # the runtime's device-to-device copy kernel (torch's same-dtype copy_ goes through it)
+    copy = [n for n in fetch if "copybuffer" in n.lower()]
+    if not copy:
+        raise SystemExit("no copy kernel in %s" % fetch_csv)
+    cname = max(copy, key=lambda n: max(fetch[n]))
+    f_fac = CALIB_BYTES / max(fetch[cname])
+    w_fac = CALIB_BYTES / max(write[cname])
+    names = {"landmarks_kernel", "select_kernel", "forward_mfma", "bwd_q_mfma", "bwd_kv_mfma",
+             "bitmap_build", "fill_zero_u32", "forward_generic", "bwd_q_generic",
+             "bwd_kv_generic"}
+    kernels = {}
+    for full in fetch:
+        short = next((n for n in names if n in full), None)
+        if short is None or full not in write:
+            continue
+        fb = sum(fetch[full]) / len(fetch[full]) * f_fac
+        wb = sum(write[full]) / len(write[full]) * w_fac
+        kernels[short] = {"fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
+                          "hbm_bytes_per_launch": round(fb + wb), "dispatches": len(fetch[full])}
+    rec = {"workload": workload, "source_sha256": source_digest(),
+           "calibration": {"kernel": cname, "bytes": CALIB_BYTES,
+                           "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4)},
+           "kernels": kernels}
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+    print(json.dumps(rec))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,7 +315,15 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the 64K fwd+bwd and 1M decode lines")
+    ap.add_argument("--pmc-run", metavar="WORKLOAD",
+                    help="calibration copy + a few steps of WORKLOAD, for rocprofv3 --pmc")
+    ap.add_argument("--pmc-summarize", nargs=4,
+                    metavar=("WORKLOAD", "FETCH_CSV", "WRITE_CSV", "OUT_JSON"),
+                    help="turn the two counter passes into profiles/traffic_<workload>.json")
     args = ap.parse_args()
+    if args.pmc_summarize:
+        pmc_summarize(*args.pmc_summarize)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py: the HSA operator here is a single-GPU build; run with --gpus 1",
               file=sys.stderr)
@@ -238,6 +333,9 @@ def main():
     import paper_2504_16795_amd as hsa
     hsa.load()
     torch.cuda.init()
+    if args.pmc_run:
+        pmc_run(args.pmc_run, 3, torch, hsa)
+        return
 
     name = "L4K_bf16"
     sh, inp, dev, gen_s = make_training(name, torch)
@@ -253,7 +351,7 @@ def main():
         "config": {"workload": "HSA fwd+bwd at 4K context: B8 L4096 H16/G2 d128 S64 k8, bf16",
                    "batch": sh.B, "seq_len": sh.L, "q_heads": sh.H, "kv_heads": sh.G,
                    "head_dim": sh.d, "chunk": sh.S, "topk": sh.k},
-        "roofline": roofline_of(kern, sh, pairs),
+        "roofline": roofline_of(kern, sh, pairs, name),
         "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern.items()},
     }
     print("[bench] %s: %.3f ms/step" % (name, ms), file=sys.stderr, flush=True)
@@ -267,7 +365,7 @@ def main():
         res["also"] = {"L64K_bf16": {
             "workload": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
             "tokens_per_s": round(sh3.B * sh3.L / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 4),
-            "roofline": roofline_of(kern3, sh3, pairs3),
+            "roofline": roofline_of(kern3, sh3, pairs3, name3),
             "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern3.items()}}}
         print("[bench] %s: %.3f ms/step" % (name3, ms3), file=sys.stderr, flush=True)
         del dev3
