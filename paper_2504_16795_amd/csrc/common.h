@@ -47,6 +47,97 @@ __device__ __forceinline__ float wave_max(float v) {
     return v;
 }
 
+// Cross-lane reductions without LDS traffic: DPP moves inside 16-lane rows (quad
+// permutations, half-row and row mirrors), then the gfx950 lane swaps across rows.  After
+// each step every lane of a group holds the group's value, and each combine takes the
+// same two operands in both lanes of a pair, so all lanes end with the same result.
+constexpr int kDppXor1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141;   // lane i <- lane 7 - i within each 8 lanes
+constexpr int kDppMirror = 0x140;       // lane i <- lane 15 - i within each 16 lanes
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_mov(int v) {
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+    return __int_as_float(dpp_mov<CTRL>(__float_as_int(v)));
+}
+// (own, partner) across 16-lane rows (l <-> l ^ 16) and across halves (l <-> l ^ 32)
+template <bool HALVES>
+__device__ __forceinline__ void lane_swap(float& a, float& b, float v) {
+    const auto r = HALVES ? __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false)
+                          : __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+}
+template <bool HALVES>
+__device__ __forceinline__ void lane_swap(int& a, int& b, int v) {
+    const auto r = HALVES ? __builtin_amdgcn_permlane32_swap((uint32_t)v, (uint32_t)v, false, false)
+                          : __builtin_amdgcn_permlane16_swap((uint32_t)v, (uint32_t)v, false, false);
+    a = (int)r[0];
+    b = (int)r[1];
+}
+
+// sum over aligned groups of N consecutive lanes (N in {8, 16, 32, 64})
+template <int N>
+__device__ __forceinline__ float group_sum(float v) {
+    v += dpp_mov<kDppXor1>(v);
+    v += dpp_mov<kDppXor2>(v);
+    v += dpp_mov<kDppHalfMirror>(v);
+    if constexpr (N >= 16) v += dpp_mov<kDppMirror>(v);
+    if constexpr (N >= 32) {
+        float a, b;
+        lane_swap<false>(a, b, v);
+        v = a + b;
+    }
+    if constexpr (N >= 64) {
+        float a, b;
+        lane_swap<true>(a, b, v);
+        v = a + b;
+    }
+    return v;
+}
+
+__device__ __forceinline__ float wave_max_dpp(float v) {
+    v = fmaxf(v, dpp_mov<kDppXor1>(v));
+    v = fmaxf(v, dpp_mov<kDppXor2>(v));
+    v = fmaxf(v, dpp_mov<kDppHalfMirror>(v));
+    v = fmaxf(v, dpp_mov<kDppMirror>(v));
+    float a, b;
+    lane_swap<false>(a, b, v);
+    v = fmaxf(a, b);
+    lane_swap<true>(a, b, v);
+    return fmaxf(a, b);
+}
+
+// wave-wide best (s, c) pair: larger s, ties to the smaller c
+__device__ __forceinline__ void pick_better(float& s, int& c, float s2, int c2) {
+    if (s2 > s || (s2 == s && c2 < c)) {
+        s = s2;
+        c = c2;
+    }
+}
+__device__ __forceinline__ void wave_argmax_dpp(float& s, int& c) {
+    pick_better(s, c, dpp_mov<kDppXor1>(s), dpp_mov<kDppXor1>(c));
+    pick_better(s, c, dpp_mov<kDppXor2>(s), dpp_mov<kDppXor2>(c));
+    pick_better(s, c, dpp_mov<kDppHalfMirror>(s), dpp_mov<kDppHalfMirror>(c));
+    pick_better(s, c, dpp_mov<kDppMirror>(s), dpp_mov<kDppMirror>(c));
+    float s0, s1;
+    int c0, c1;
+    lane_swap<false>(s0, s1, s);
+    lane_swap<false>(c0, c1, c);
+    s = s0;
+    c = c0;
+    pick_better(s, c, s1, c1);
+    lane_swap<true>(s0, s1, s);
+    lane_swap<true>(c0, c1, c);
+    s = s0;
+    c = c0;
+    pick_better(s, c, s1, c1);
+}
+
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // RAII bracket of one kernel launch for the optional per-kernel timing (timing.hip).

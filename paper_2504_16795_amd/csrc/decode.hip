@@ -6,10 +6,8 @@
 // D/VN consecutive lanes share a row and reduce their partial dot products with
 // shuffles.  Each wave then extracts the slice's top-k of one group by k rounds of a
 // wave-wide arg-max (ties to the lower chunk index) and writes k (score, chunk) candidates.
-// Stage 2 (finish): workgroup = (b, g).  Wave 0 merges the slice candidates into the final
-// top-k, computes the softmax chunk weights and the descending-chunk slot order; then the
-// 8 waves take one slot each, compute the intra-chunk softmax for all h heads and the
-// weighted P V, and the per-wave partial outputs are summed in a fixed order.
+// Stage 2 (finish): workgroup = (slot, b, g): the k selected chunks are attended in
+// parallel and their weighted partial outputs summed in slot order (see decode_finish).
 #include "common.h"
 
 namespace hsa {
@@ -18,10 +16,11 @@ namespace {
 constexpr int kScanThreads = 256;
 constexpr int SL = 256;            // chunks per scan slice
 constexpr int GMAX = 16;
-constexpr int kFinThreads = 512;
+constexpr int kFinThreads = 256;
 constexpr int NW = kFinThreads / 64;
 constexpr int HMAX = 16;
 constexpr int KMAX = 32;
+constexpr int NCMAX = 4096;        // slice candidates merged from LDS (else from global memory)
 
 template <typename T> struct V16;
 template <> struct V16<float> { static constexpr int n = 4; };
@@ -45,19 +44,6 @@ __device__ __forceinline__ bool better(float s1, int c1, float s2, int c2) {
     return s1 > s2 || (s1 == s2 && c1 < c2);
 }
 
-// wave-wide arg-max of (s, c) pairs; ties to the lower c
-__device__ __forceinline__ void wave_argmax(float& s, int& c) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-        const float so = __shfl_xor(s, o, 64);
-        const int co = __shfl_xor(c, o, 64);
-        if (better(so, co, s, c)) {
-            s = so;
-            c = co;
-        }
-    }
-}
-
 __device__ __forceinline__ int cache_tokens(const int32_t* cache_len, int b, int ncap) {
     int n = cache_len ? cache_len[b] : ncap;
     return n < 0 ? 0 : (n > ncap ? ncap : n);
@@ -67,7 +53,7 @@ template <typename Tq, typename Tk, int D>
 __global__ __launch_bounds__(kScanThreads) void decode_scan(
     Dims dm, const Tq* __restrict__ q, const Tk* __restrict__ Kbar,
     const int32_t* __restrict__ cache_len, float* __restrict__ cand_s,
-    int32_t* __restrict__ cand_c, int nslices) {
+    int32_t* __restrict__ cand_c, uint32_t* __restrict__ counter, int nslices) {
     constexpr int VN = V16<Tk>::n;
     constexpr int LPR = D / VN;       // lanes per landmark row
     __shared__ float qs[GMAX * D];
@@ -78,6 +64,7 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
     const int ncand = cache_tokens(cache_len, b, dm.L) / dm.S;
     const int c0 = slice * SL;
     const int nch = max(0, min(SL, ncand - c0));
+    if (slice == 0 && tid < G) counter[b * G + tid] = 0u;   // completion counters of stage 2
 
     for (int i = tid; i < G * D; i += kScanThreads) {
         const int g = i / D, e = i % D;
@@ -88,22 +75,31 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
     __syncthreads();
     const Tk* base = Kbar + ((size_t)b * dm.C + c0) * G * D;
     const int nvec = nch * G * LPR;
-    const int nit = cdiv(nvec, kScanThreads);
-    for (int it = 0; it < nit; ++it) {
-        const int v = it * kScanThreads + tid;
-        const bool valid = v < nvec;
-        const int row = v / LPR, part = v % LPR;
-        float dot = 0.f;
-        if (valid) {
-            float x[VN];
-            unpack16(base + (size_t)row * D + part * VN, x);
-            const float* qg = qs + (row % G) * D + part * VN;
+    // U vectors per thread per pass, loads first; a row's LPR lanes reduce with DPP moves
+    constexpr int U = 8;
+    for (int v0 = 0; v0 < nvec; v0 += kScanThreads * U) {
+        float x[U][VN];
 #pragma unroll
-            for (int i = 0; i < VN; ++i) dot = fmaf(qg[i], x[i], dot);
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * kScanThreads + tid;
+            if (v < nvec) {
+                unpack16(base + (size_t)(v / LPR) * D + (v % LPR) * VN, x[u]);
+            } else {
+#pragma unroll
+                for (int i = 0; i < VN; ++i) x[u][i] = 0.f;
+            }
         }
 #pragma unroll
-        for (int o = LPR / 2; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
-        if (valid && part == 0) sc[row] = dm.alpha * dot;
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * kScanThreads + tid;
+            const int row = v / LPR, part = v % LPR;
+            const float* qg = qs + (row % G) * D + part * VN;
+            float dot = 0.f;
+#pragma unroll
+            for (int i = 0; i < VN; ++i) dot = fmaf(qg[i], x[u][i], dot);
+            dot = group_sum<LPR>(dot);
+            if (v < nvec && part == 0) sc[row] = dm.alpha * dot;
+        }
     }
     __syncthreads();
     for (int g = wave; g < G; g += kScanThreads / 64) {
@@ -119,14 +115,8 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
             float bs = -INFINITY;
             int bc = 0x7FFFFFFF;
 #pragma unroll
-            for (int m = 0; m < SL / 64; ++m) {
-                const int cl = lane + 64 * m;
-                if (better(s[m], cl, bs, bc)) {
-                    bs = s[m];
-                    bc = cl;
-                }
-            }
-            wave_argmax(bs, bc);
+            for (int m = 0; m < SL / 64; ++m) pick_better(bs, bc, s[m], lane + 64 * m);
+            wave_argmax_dpp(bs, bc);
             const bool found = bs > -INFINITY;
             if (lane == 0) {
                 os[i] = bs;
@@ -143,26 +133,42 @@ template <typename T, int D>
 __global__ __launch_bounds__(kFinThreads) void decode_finish(
     Dims dm, const T* __restrict__ q, const T* __restrict__ Kc, const T* __restrict__ Vc,
     const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
-    const int32_t* __restrict__ cand_c, int nslices, T* __restrict__ o,
-    int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
-    constexpr int VN = V16<T>::n;
-    constexpr int EPL = D / 64;       // output elements per lane in P V
-    __shared__ float qf[HMAX * D];
+    const int32_t* __restrict__ cand_c, int nslices, float* __restrict__ part,
+    uint32_t* __restrict__ counter, T* __restrict__ o, int32_t* __restrict__ idx_out,
+    float* __restrict__ w_out) {
+    constexpr int DP = D + 1;
+    constexpr int SMAX = 128;
+    constexpr int NE = sizeof(T) == 4 ? 8192 : SMAX * D;   // S * d <= 8192 for fp32 inputs
+    __shared__ T ks[NE];
+    __shared__ T vs[NE];
+    __shared__ float qf[HMAX * DP];
+    __shared__ float pz[HMAX * SMAX];
     __shared__ int sel_c[KMAX];
     __shared__ float sel_w[KMAX];
-    __shared__ float ow[NW][HMAX * D];
+    __shared__ float lcs[NCMAX];
+    __shared__ int lcc[NCMAX];
+    __shared__ int last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bg = blockIdx.x, b = bg / dm.G, g = bg % dm.G;
+    const int slot = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
     const int h = dm.h, S = dm.S, k = dm.k;
     const int ncand = cache_tokens(cache_len, b, dm.L) / S;
     const int n = min(k, ncand);
 
     for (int i = tid; i < h * D; i += kFinThreads)
-        qf[i] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
+        qf[(i / D) * DP + i % D] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
+    const int nc = nslices * k;
+    const bool in_lds = nc <= NCMAX;
+    if (in_lds) {
+        for (int x = tid; x < nc; x += kFinThreads) {
+            lcs[x] = cand_s[(size_t)bg * nc + x];
+            lcc[x] = cand_c[(size_t)bg * nc + x];
+        }
+    }
+    __syncthreads();
     if (wave == 0) {
-        const int nc = nslices * k;
-        const float* cs = cand_s + (size_t)bg * nc;
-        const int32_t* cc = cand_c + (size_t)bg * nc;
+        const float* cs = in_lds ? lcs : cand_s + (size_t)bg * nc;
+        const int32_t* cc = in_lds ? lcc : cand_c + (size_t)bg * nc;
         float ls = -INFINITY;      // lane i < n receives the i-th best candidate
         int lc = -1;
         // Candidates carry distinct chunk ids, so (score desc, chunk asc) is a strict total
@@ -184,7 +190,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
                     }
                 }
             }
-            wave_argmax(bs, bc);
+            wave_argmax_dpp(bs, bc);
             if (lane == i) {
                 ls = bs;
                 lc = bc;
@@ -200,93 +206,122 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         if (lane < n) {
             sel_c[rank] = lc;
             sel_w[rank] = ex / z;
-            idx_out[(size_t)bg * k + rank] = lc;
-            w_out[(size_t)bg * k + rank] = ex / z;
         } else if (lane < k) {
             sel_c[lane] = -1;
             sel_w[lane] = 0.f;
-            idx_out[(size_t)bg * k + lane] = -1;
-            w_out[(size_t)bg * k + lane] = 0.f;
         }
     }
     __syncthreads();
+    if (slot == 0 && tid < k) {
+        idx_out[(size_t)bg * k + tid] = sel_c[tid];
+        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    }
 
-    float acc[HMAX][EPL];
-#pragma unroll
-    for (int j = 0; j < HMAX; ++j)
-#pragma unroll
-        for (int u = 0; u < EPL; ++u) acc[j][u] = 0.f;
-    for (int slot = wave; slot < n; slot += NW) {
+    if (slot < n) {
         const int c = sel_c[slot];
         const float wi = sel_w[slot];
-        // logits: lane = key (two keys per lane for S = 128)
-        float z[2][HMAX];
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int j = 0; j < HMAX; ++j) z[u][j] = 0.f;
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            const int s = lane + 64 * u;
-            if (s < S) {
-                const T* kr = Kc + (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D;
-                for (int e0 = 0; e0 < D; e0 += VN) {
-                    float x[VN];
-                    unpack16(kr + e0, x);
-#pragma unroll
-                    for (int j = 0; j < HMAX; ++j) {
-                        if (j < h) {
-#pragma unroll
-                            for (int i = 0; i < VN; ++i) z[u][j] = fmaf(qf[j * D + e0 + i], x[i], z[u][j]);
-                        }
-                    }
-                }
-            }
+        // the chunk's S rows of K and V for group g
+        constexpr int VN = V16<T>::n;
+        for (int v = tid; v < S * D / VN; v += kFinThreads) {
+            const int s = v / (D / VN), e = (v % (D / VN)) * VN;
+            const size_t src = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+            *reinterpret_cast<uint4*>(&ks[s * D + e]) = *reinterpret_cast<const uint4*>(Kc + src);
+            *reinterpret_cast<uint4*>(&vs[s * D + e]) = *reinterpret_cast<const uint4*>(Vc + src);
         }
-        float pz[2][HMAX];
-#pragma unroll
-        for (int j = 0; j < HMAX; ++j) {
-            pz[0][j] = pz[1][j] = 0.f;
-            if (j < h) {
-                const float z0 = (lane < S) ? dm.beta * z[0][j] : -INFINITY;
-                const float z1 = (lane + 64 < S) ? dm.beta * z[1][j] : -INFINITY;
-                const float m = wave_max(fmaxf(z0, z1));
-                const float e0 = expf(z0 - m), e1 = expf(z1 - m);
-                const float scale = wi / wave_sum(e0 + e1);
-                pz[0][j] = e0 * scale;
-                pz[1][j] = e1 * scale;
+        __syncthreads();
+        // logits z[j][s] = beta q_j . k_s
+        for (int x = tid; x < S * h; x += kFinThreads) {
+            const int s = x / h, j = x % h;
+            float a0 = 0.f, a1 = 0.f;
+#pragma unroll 8
+            for (int e = 0; e < D; e += 2) {
+                a0 = fmaf(qf[j * DP + e], to_f32(ks[s * D + e]), a0);
+                a1 = fmaf(qf[j * DP + e + 1], to_f32(ks[s * D + e + 1]), a1);
             }
+            pz[j * SMAX + s] = dm.beta * (a0 + a1);
         }
-        // P V: lanes own output columns; the probability of key s is broadcast from lane s%64
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-            for (int sl = 0; sl < 64 && u * 64 + sl < S; ++sl) {
-                const int s = u * 64 + sl;
-                const T* vr = Vc + (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D;
-                float v[EPL];
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) v[e] = to_f32(vr[lane + 64 * e]);
-#pragma unroll
-                for (int j = 0; j < HMAX; ++j) {
-                    if (j < h) {
-                        const float p = __shfl(pz[u][j], sl, 64);
-#pragma unroll
-                        for (int e = 0; e < EPL; ++e) acc[j][e] = fmaf(p, v[e], acc[j][e]);
-                    }
-                }
+        __syncthreads();
+        // intra-chunk softmax of each head, scaled by the chunk weight
+        for (int j = wave; j < h; j += NW) {
+            const float z0 = lane < S ? pz[j * SMAX + lane] : -INFINITY;
+            const float z1 = lane + 64 < S ? pz[j * SMAX + lane + 64] : -INFINITY;
+            const float m = wave_max(fmaxf(z0, z1));
+            const float e0 = lane < S ? expf(z0 - m) : 0.f;
+            const float e1 = lane + 64 < S ? expf(z1 - m) : 0.f;
+            const float scale = wi / wave_sum(e0 + e1);
+            if (lane < S) pz[j * SMAX + lane] = e0 * scale;
+            if (lane + 64 < S) pz[j * SMAX + lane + 64] = e1 * scale;
+        }
+        __syncthreads();
+        // w_i P V for the h heads
+        float* pp = part + (((size_t)bg * k + slot) * h) * D;
+        for (int x = tid; x < h * D; x += kFinThreads) {
+            const int j = x / D, d = x % D;
+            float a0 = 0.f, a1 = 0.f;
+            for (int s = 0; s < S; s += 2) {
+                a0 = fmaf(pz[j * SMAX + s], to_f32(vs[s * D + d]), a0);
+                a1 = fmaf(pz[j * SMAX + s + 1], to_f32(vs[(s + 1) * D + d]), a1);
             }
+            pp[x] = a0 + a1;
         }
     }
-#pragma unroll
-    for (int j = 0; j < HMAX; ++j)
-        if (j < h)
-#pragma unroll
-            for (int u = 0; u < EPL; ++u) ow[wave][j * D + lane + 64 * u] = acc[j][u];
+
+    // the last workgroup of (b, g) sums the partials in slot order
+    __threadfence();
     __syncthreads();
-    for (int i = tid; i < h * D; i += kFinThreads) {
+    if (tid == 0) {
+        const uint32_t prev = __hip_atomic_fetch_add(counter + bg, 1u, __ATOMIC_ACQ_REL,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        last = (prev == (uint32_t)(k - 1));
+    }
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    for (int x = tid; x < h * D; x += kFinThreads) {
         float s = 0.f;
-        for (int wv = 0; wv < NW; ++wv) s += ow[wv][i];
-        o[((size_t)b * dm.H + (size_t)g * h) * D + i] = from_f32<T>(s);
+        for (int i = 0; i < n; ++i) s += part[(((size_t)bg * k + i) * h) * D + x];
+        o[((size_t)b * dm.H + (size_t)g * h) * D + x] = from_f32<T>(s);
+    }
+    if (tid == 0) __hip_atomic_store(counter + bg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+struct DecodeWs {
+    size_t cs, cc, part, counter, end;
+};
+DecodeWs decode_ws(const Dims& dm) {
+    const size_t nslices = (size_t)cdiv(dm.C > 0 ? dm.C : 1, SL);
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    DecodeWs l;
+    l.cs = 0;
+    l.cc = al(l.cs + (size_t)dm.B * dm.G * nslices * dm.k * 4);
+    l.part = al(l.cc + (size_t)dm.B * dm.G * nslices * dm.k * 4);
+    l.counter = al(l.part + (size_t)dm.B * dm.G * dm.k * dm.h * dm.d * 4);
+    l.end = al(l.counter + (size_t)dm.B * dm.G * 4);
+    return l;
+}
+
+template <typename T, typename Tk, int D>
+void launch_tkd(const Dims& dm, const void* q, const void* Kc, const void* Vc, const void* Kbar,
+                const int32_t* cache_len, void* o, int32_t* idx, float* w, void* ws,
+                hipStream_t st) {
+    const int nslices = cdiv(dm.C > 0 ? dm.C : 1, SL);
+    const DecodeWs l = decode_ws(dm);
+    char* wb = (char*)ws;
+    float* cs = (float*)(wb + l.cs);
+    int32_t* cc = (int32_t*)(wb + l.cc);
+    float* part = (float*)(wb + l.part);
+    uint32_t* counter = (uint32_t*)(wb + l.counter);
+    {
+        HSA_TIMED("decode_scan", st);
+        hipLaunchKernelGGL((decode_scan<T, Tk, D>), dim3(nslices, dm.B), dim3(kScanThreads), 0,
+                           st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, counter,
+                           nslices);
+    }
+    {
+        HSA_TIMED("decode_finish", st);
+        hipLaunchKernelGGL((decode_finish<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
+                           st, dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
+                           nslices, part, counter, (T*)o, idx, w);
     }
 }
 
@@ -294,44 +329,13 @@ template <typename T, typename Tk>
 void launch_tk(const Dims& dm, const void* q, const void* Kc, const void* Vc, const void* Kbar,
                const int32_t* cache_len, void* o, int32_t* idx, float* w, void* ws,
                hipStream_t st) {
-    const int nslices = cdiv(dm.C > 0 ? dm.C : 1, SL);
-    float* cs = (float*)ws;
-    int32_t* cc = (int32_t*)((char*)ws + (((size_t)dm.B * dm.G * nslices * dm.k * 4 + 255) & ~(size_t)255));
-    dim3 g1(nslices, dm.B);
-    if (dm.d == 128) {
-        {
-            HSA_TIMED("decode_scan", st);
-            hipLaunchKernelGGL((decode_scan<T, Tk, 128>), g1, dim3(kScanThreads), 0, st, dm,
-                               (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
-        }
-        {
-            HSA_TIMED("decode_finish", st);
-            hipLaunchKernelGGL((decode_finish<T, 128>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
-                               dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                               nslices, (T*)o, idx, w);
-        }
-    } else {
-        {
-            HSA_TIMED("decode_scan", st);
-            hipLaunchKernelGGL((decode_scan<T, Tk, 64>), g1, dim3(kScanThreads), 0, st, dm,
-                               (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, nslices);
-        }
-        {
-            HSA_TIMED("decode_finish", st);
-            hipLaunchKernelGGL((decode_finish<T, 64>), dim3(dm.B * dm.G), dim3(kFinThreads), 0, st,
-                               dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                               nslices, (T*)o, idx, w);
-        }
-    }
+    if (dm.d == 128) launch_tkd<T, Tk, 128>(dm, q, Kc, Vc, Kbar, cache_len, o, idx, w, ws, st);
+    else launch_tkd<T, Tk, 64>(dm, q, Kc, Vc, Kbar, cache_len, o, idx, w, ws, st);
 }
 
 }  // namespace
 
-size_t decode_workspace(const Dims& dm) {
-    const size_t nslices = (size_t)cdiv(dm.C > 0 ? dm.C : 1, SL);
-    const size_t one = ((size_t)dm.B * dm.G * nslices * dm.k * 4 + 255) & ~(size_t)255;
-    return 2 * one;
-}
+size_t decode_workspace(const Dims& dm) { return decode_ws(dm).end; }
 
 hipError_t launch_decode(const Dims& dm, bool in_bf16, const void* q, const void* Kc,
                          const void* Vc, const void* Kbar, bool kbar_bf16,

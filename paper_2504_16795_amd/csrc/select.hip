@@ -5,8 +5,7 @@
 // One wave per tile of 64 consecutive tokens of one (b, g); lane = token.  Each lane keeps
 // its group query q~ = sum_j q_j (fp32, d registers) and a running top-KC list (scores and
 // chunk indices, registers, descending).  Candidates are visited in increasing chunk
-// order; the landmark row Kbar_c is the same for every lane, so it comes through scalar
-// loads.  A candidate enters a list only when its score is strictly greater than the
+// order; the landmark row Kbar_c is read at the same address by every lane.  A candidate enters a list only when its score is strictly greater than the
 // list's last entry and moves up past every entry it beats strictly: on equal scores the
 // lower chunk index stays first.  The k best get softmax weights and are written in
 // descending chunk order, padded with -1 / 0.
@@ -44,12 +43,16 @@ __device__ __forceinline__ void group_query(const float* __restrict__ qp, int h,
     for (int j = 0; j < h; ++j) {
         const float4* p = reinterpret_cast<const float4*>(qp + (size_t)j * D);
 #pragma unroll
-        for (int v = 0; v < D / 4; ++v) {
-            const float4 u = p[v];
-            qb[4 * v] += u.x;
-            qb[4 * v + 1] += u.y;
-            qb[4 * v + 2] += u.z;
-            qb[4 * v + 3] += u.w;
+        for (int v = 0; v < D / 8; ++v) {
+            const float4 u0 = p[2 * v], u1 = p[2 * v + 1];
+            qb[8 * v] += u0.x;
+            qb[8 * v + 1] += u0.y;
+            qb[8 * v + 2] += u0.z;
+            qb[8 * v + 3] += u0.w;
+            qb[8 * v + 4] += u1.x;
+            qb[8 * v + 5] += u1.y;
+            qb[8 * v + 6] += u1.z;
+            qb[8 * v + 7] += u1.w;
         }
     }
 }
@@ -127,14 +130,13 @@ __global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restr
     const float iz = 1.f / z;
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
-        if (j >= k) break;
         if (j < n) {
             int rank = 0;
 #pragma unroll
             for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
             idx[o + rank] = lc[j];
             w[o + rank] = ex[j] * iz;
-        } else {
+        } else if (j < k) {
             idx[o + j] = -1;
             w[o + j] = 0.f;
         }
