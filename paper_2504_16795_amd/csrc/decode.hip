@@ -2,12 +2,14 @@
 // the selected chunks' keys and values are read.
 //
 // Stage 1 (scan): workgroup = (b, slice of 256 chunks).  The slice's landmark rows for all
-// G groups are one contiguous block of the [B, C, G, d] cache, streamed with 16-byte loads;
-// D/VN consecutive lanes share a row and reduce their partial dot products with
-// shuffles.  Each wave then extracts the slice's top-k of one group by k rounds of a
-// wave-wide arg-max (ties to the lower chunk index) and writes k (score, chunk) candidates.
+// G groups are one contiguous block of the [B, C, G, d] cache, streamed with 16-byte loads
+// (all of a thread's loads issued first); D/VN consecutive lanes share a row and reduce
+// their partial dot products with DPP moves.  Each wave then extracts the slice's top-k of
+// one group by k rounds of a wave-wide arg-max (ties to the lower chunk index) and writes
+// k (score, chunk) candidates.
 // Stage 2 (finish): workgroup = (slot, b, g): the k selected chunks are attended in
-// parallel and their weighted partial outputs summed in slot order (see decode_finish).
+// parallel.  Stage 3 (combine): workgroup = (b, g), sums their weighted partial outputs in
+// slot order.
 #include "common.h"
 
 namespace hsa {
@@ -53,7 +55,7 @@ template <typename Tq, typename Tk, int D>
 __global__ __launch_bounds__(kScanThreads) void decode_scan(
     Dims dm, const Tq* __restrict__ q, const Tk* __restrict__ Kbar,
     const int32_t* __restrict__ cache_len, float* __restrict__ cand_s,
-    int32_t* __restrict__ cand_c, uint32_t* __restrict__ counter, int nslices) {
+    int32_t* __restrict__ cand_c, int nslices) {
     constexpr int VN = V16<Tk>::n;
     constexpr int LPR = D / VN;       // lanes per landmark row
     __shared__ float qs[GMAX * D];
@@ -64,7 +66,6 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
     const int ncand = cache_tokens(cache_len, b, dm.L) / dm.S;
     const int c0 = slice * SL;
     const int nch = max(0, min(SL, ncand - c0));
-    if (slice == 0 && tid < G) counter[b * G + tid] = 0u;   // completion counters of stage 2
 
     for (int i = tid; i < G * D; i += kScanThreads) {
         const int g = i / D, e = i % D;
@@ -76,27 +77,26 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
     const Tk* base = Kbar + ((size_t)b * dm.C + c0) * G * D;
     const int nvec = nch * G * LPR;
     // U vectors per thread per pass, loads first; a row's LPR lanes reduce with DPP moves
-    constexpr int U = 8;
+    constexpr int U = 32;
     for (int v0 = 0; v0 < nvec; v0 += kScanThreads * U) {
-        float x[U][VN];
+        uint4 raw[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int v = v0 + u * kScanThreads + tid;
-            if (v < nvec) {
-                unpack16(base + (size_t)(v / LPR) * D + (v % LPR) * VN, x[u]);
-            } else {
-#pragma unroll
-                for (int i = 0; i < VN; ++i) x[u][i] = 0.f;
-            }
+            raw[u] = v < nvec ? *reinterpret_cast<const uint4*>(base + (size_t)(v / LPR) * D +
+                                                                (v % LPR) * VN)
+                              : uint4{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int v = v0 + u * kScanThreads + tid;
             const int row = v / LPR, part = v % LPR;
             const float* qg = qs + (row % G) * D + part * VN;
+            float xu[VN];
+            unpack16(reinterpret_cast<const Tk*>(&raw[u]), xu);
             float dot = 0.f;
 #pragma unroll
-            for (int i = 0; i < VN; ++i) dot = fmaf(qg[i], x[u][i], dot);
+            for (int i = 0; i < VN; ++i) dot = fmaf(qg[i], xu[i], dot);
             dot = group_sum<LPR>(dot);
             if (v < nvec && part == 0) sc[row] = dm.alpha * dot;
         }
@@ -129,13 +129,18 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
     }
 }
 
+// Stage 2 (finish): workgroup = (slot, b, g), so the k selected chunks of a sequence are
+// attended in parallel.  Wave 0 of every workgroup merges the slice candidates into the
+// final top-k (the same deterministic merge in each), computes the softmax chunk weights and
+// the descending-chunk slot order.  The workgroup of slot i stages its chunk's K and V in
+// LDS, computes the intra-chunk softmax of the h heads and w_i P V, and stores that partial
+// output.  Stage 3 (combine) sums the partials of a (b, g) in slot order.
 template <typename T, int D>
 __global__ __launch_bounds__(kFinThreads) void decode_finish(
     Dims dm, const T* __restrict__ q, const T* __restrict__ Kc, const T* __restrict__ Vc,
     const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
     const int32_t* __restrict__ cand_c, int nslices, float* __restrict__ part,
-    uint32_t* __restrict__ counter, T* __restrict__ o, int32_t* __restrict__ idx_out,
-    float* __restrict__ w_out) {
+    int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
     constexpr int DP = D + 1;
     constexpr int SMAX = 128;
     constexpr int NE = sizeof(T) == 4 ? 8192 : SMAX * D;   // S * d <= 8192 for fp32 inputs
@@ -147,7 +152,6 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     __shared__ float sel_w[KMAX];
     __shared__ float lcs[NCMAX];
     __shared__ int lcc[NCMAX];
-    __shared__ int last;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int slot = blockIdx.x;
     const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
@@ -266,27 +270,25 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         }
     }
 
-    // the last workgroup of (b, g) sums the partials in slot order
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) {
-        const uint32_t prev = __hip_atomic_fetch_add(counter + bg, 1u, __ATOMIC_ACQ_REL,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
-        last = (prev == (uint32_t)(k - 1));
-    }
-    __syncthreads();
-    if (!last) return;
-    __threadfence();
-    for (int x = tid; x < h * D; x += kFinThreads) {
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(256) void decode_combine(Dims dm,
+                                                      const int32_t* __restrict__ cache_len,
+                                                      const float* __restrict__ part,
+                                                      T* __restrict__ o) {
+    const int bg = blockIdx.x, b = bg / dm.G, g = bg % dm.G;
+    const int h = dm.h, k = dm.k;
+    const int n = min(k, cache_tokens(cache_len, b, dm.L) / dm.S);
+    for (int x = threadIdx.x; x < h * D; x += 256) {
         float s = 0.f;
         for (int i = 0; i < n; ++i) s += part[(((size_t)bg * k + i) * h) * D + x];
         o[((size_t)b * dm.H + (size_t)g * h) * D + x] = from_f32<T>(s);
     }
-    if (tid == 0) __hip_atomic_store(counter + bg, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 struct DecodeWs {
-    size_t cs, cc, part, counter, end;
+    size_t cs, cc, part, end;
 };
 DecodeWs decode_ws(const Dims& dm) {
     const size_t nslices = (size_t)cdiv(dm.C > 0 ? dm.C : 1, SL);
@@ -295,8 +297,7 @@ DecodeWs decode_ws(const Dims& dm) {
     l.cs = 0;
     l.cc = al(l.cs + (size_t)dm.B * dm.G * nslices * dm.k * 4);
     l.part = al(l.cc + (size_t)dm.B * dm.G * nslices * dm.k * 4);
-    l.counter = al(l.part + (size_t)dm.B * dm.G * dm.k * dm.h * dm.d * 4);
-    l.end = al(l.counter + (size_t)dm.B * dm.G * 4);
+    l.end = al(l.part + (size_t)dm.B * dm.G * dm.k * dm.h * dm.d * 4);
     return l;
 }
 
@@ -310,18 +311,22 @@ void launch_tkd(const Dims& dm, const void* q, const void* Kc, const void* Vc, c
     float* cs = (float*)(wb + l.cs);
     int32_t* cc = (int32_t*)(wb + l.cc);
     float* part = (float*)(wb + l.part);
-    uint32_t* counter = (uint32_t*)(wb + l.counter);
     {
         HSA_TIMED("decode_scan", st);
         hipLaunchKernelGGL((decode_scan<T, Tk, D>), dim3(nslices, dm.B), dim3(kScanThreads), 0,
-                           st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc, counter,
+                           st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc,
                            nslices);
     }
     {
         HSA_TIMED("decode_finish", st);
         hipLaunchKernelGGL((decode_finish<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
                            st, dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                           nslices, part, counter, (T*)o, idx, w);
+                           nslices, part, idx, w);
+    }
+    {
+        HSA_TIMED("decode_combine", st);
+        hipLaunchKernelGGL((decode_combine<T, D>), dim3(dm.B * dm.G), dim3(256), 0, st, dm,
+                           cache_len, part, (T*)o);
     }
 }
 
