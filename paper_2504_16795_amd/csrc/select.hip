@@ -2,10 +2,11 @@
 // s_c = alpha * (sum_j q_j) . Kbar_c over the chunks before the token's own, and their
 // softmax weights).
 //
-// One wave per tile of 64 consecutive tokens of one (b, g); lane = token.  Each lane keeps
-// its group query q~ = sum_j q_j (fp32, d registers) and a running top-KC list (scores and
-// chunk indices, registers, descending).  Candidates are visited in increasing chunk
-// order; the landmark row Kbar_c is read at the same address by every lane.  A candidate enters a list only when its score is strictly greater than the
+// Workgroup = 4 waves on 256 consecutive tokens of one (b, g); lane = token.  Each lane
+// keeps its group query q~ = sum_j q_j (fp32, d registers) and a running top-KC list
+// (scores and chunk indices, registers, descending).  The candidates' landmark rows are
+// copied into LDS in blocks of 64 (two blocks in flight), shared by the four waves, and
+// read with broadcast LDS loads; candidates are visited in increasing chunk order.  A candidate enters a list only when its score is strictly greater than the
 // list's last entry and moves up past every entry it beats strictly: on equal scores the
 // lower chunk index stays first.  The k best get softmax weights and are written in
 // descending chunk order, padded with -1 / 0.
@@ -15,6 +16,29 @@ namespace hsa {
 namespace {
 
 constexpr int kTile = 64;     // tokens per wave
+constexpr int NW = 4;         // waves per workgroup: 4 consecutive tiles of one (b, g)
+constexpr int kThreads = NW * kTile;
+constexpr int NB = 64;        // candidate rows per LDS block
+constexpr int NST = 2;        // LDS blocks
+
+// One global_load_lds_dwordx4 (lane l copies 16 bytes to lds_base + 16 l; lds_base
+// wave-uniform in M0), as inline assembly so that the compiler's waits do not make the
+// LDS reads wait for copies of the other block.  Completion is awaited with vmcnt(0);
+// no compiler-visible global load is in flight across the copies.
+__device__ __forceinline__ void sel_copy16(const void* gsrc, uint32_t lds_base) {
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gsrc), "{m0}"(lds_base)
+                 : "memory");
+}
+__device__ __forceinline__ uint32_t sel_lds_address(const void* p) {
+    return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+__device__ __forceinline__ void sel_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void wait_global_loads_sel() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ void sel_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 
 // q~ = sum over the h heads of the group, for token t (d fp32 values in qb)
 template <int D>
@@ -58,20 +82,23 @@ __device__ __forceinline__ void group_query(const float* __restrict__ qp, int h,
 }
 
 template <typename T, int D, int KC>
-__global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restrict__ Q,
-                                                       const float* __restrict__ Kbar,
-                                                       int32_t* __restrict__ idx,
-                                                       float* __restrict__ w, int ntiles) {
-    const int lane = threadIdx.x;
-    // latest tiles (most candidates) first
+__global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __restrict__ Q,
+                                                          const float* __restrict__ Kbar,
+                                                          int32_t* __restrict__ idx,
+                                                          float* __restrict__ w, int ngroups) {
+    __shared__ float kb_s[NST][NB * D];         // landmark rows of the staged candidate blocks
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // latest token groups (most candidates) first
     const int nbg = dm.B * dm.G;
-    const int tile = ntiles - 1 - (int)blockIdx.x / nbg;
+    const int grp = ngroups - 1 - (int)blockIdx.x / nbg;
     const int bg = (int)blockIdx.x % nbg, b = bg / dm.G, g = bg % dm.G;
-    const int t0 = tile * kTile;
+    const int t0 = grp * kThreads + wave * kTile;        // this wave's 64 tokens
     const int t = t0 + lane;
     const bool valid = t < dm.L;
     const int ncand = valid ? t / dm.S : 0;
-    const int nwave = (min(t0 + kTile, dm.L) - 1) / dm.S;     // candidates of the last token
+    const int nwave = t0 < dm.L ? (min(t0 + kTile, dm.L) - 1) / dm.S : 0;
+    const int tlast = min(grp * kThreads + kThreads, dm.L) - 1;
+    const int nwg = (tlast >= grp * kThreads) ? tlast / dm.S : 0;   // candidates of the group
     const int k = dm.k;
 
     float qb[D];
@@ -81,6 +108,7 @@ __global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restr
 #pragma unroll
         for (int e = 0; e < D; ++e) qb[e] = 0.f;
     }
+    wait_global_loads_sel();
     float ls[KC];
     int lc[KC];
 #pragma unroll
@@ -89,30 +117,54 @@ __global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restr
         lc[j] = -1;
     }
 
-    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D;   // row c at kb + c G D
+    // candidate blocks of NB rows (row c of group g: D fp32 at Kbar + ((b C + c) G + g) D),
+    // copied into LDS by the NW waves: 2 rows per 1 KB copy instruction
+    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D;
     const size_t cstride = (size_t)dm.G * D;
-    for (int c = 0; c < nwave; ++c) {
-        const float* kr = kb + (size_t)c * cstride;              // same for every lane
-        float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+    const int nblk = cdiv(nwg, NB);
+    auto issue = [&](int blk) __attribute__((always_inline)) {
+        float* dst = kb_s[blk % NST];
+        constexpr int RPI = 1024 / (D * 4);                // rows per copy instruction
 #pragma unroll
-        for (int e = 0; e < D; e += 4) {
-            a0 = fmaf(qb[e], kr[e], a0);
-            a1 = fmaf(qb[e + 1], kr[e + 1], a1);
-            a2 = fmaf(qb[e + 2], kr[e + 2], a2);
-            a3 = fmaf(qb[e + 3], kr[e + 3], a3);
+        for (int i = 0; i < NB / RPI / NW; ++i) {
+            const int ci = (wave + i * NW);                // copy instruction of the block
+            const int r = ci * RPI + lane / (64 / RPI);    // row within the block
+            const int c = min(blk * NB + r, nwg - 1);      // past the end: repeat a valid row
+            sel_copy16(kb + (size_t)c * cstride + (lane % (64 / RPI)) * 4,
+                       __builtin_amdgcn_readfirstlane(sel_lds_address(dst + ci * 256)));
         }
-        float s = (c < ncand) ? dm.alpha * ((a0 + a1) + (a2 + a3)) : -INFINITY;
-        if (__ballot(s > ls[KC - 1]) == 0) continue;
-        int ci = c;
+    };
+    if (nblk > 0) issue(0);
+    for (int blk = 0; blk < nblk; ++blk) {
+        sel_wait_all();
+        sel_barrier();                                     // block landed; other stage free
+        if (blk + 1 < nblk) issue(blk + 1);
+        const float* rows = kb_s[blk % NST];
+        const int cend = min(nwave, blk * NB + NB);
+        for (int c = blk * NB; c < cend; ++c) {
+            const float4* kr = reinterpret_cast<const float4*>(rows + (c - blk * NB) * D);
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
-        for (int j = 0; j < KC; ++j) {          // insertion: strictly greater moves up
-            const bool gt = s > ls[j];
-            const float ts = gt ? s : ls[j];
-            const int tc = gt ? ci : lc[j];
-            s = gt ? ls[j] : s;
-            ci = gt ? lc[j] : ci;
-            ls[j] = ts;
-            lc[j] = tc;
+            for (int e = 0; e < D / 4; ++e) {
+                const float4 kv = kr[e];
+                a0 = fmaf(qb[4 * e], kv.x, a0);
+                a1 = fmaf(qb[4 * e + 1], kv.y, a1);
+                a2 = fmaf(qb[4 * e + 2], kv.z, a2);
+                a3 = fmaf(qb[4 * e + 3], kv.w, a3);
+            }
+            float s = (c < ncand) ? dm.alpha * ((a0 + a1) + (a2 + a3)) : -INFINITY;
+            if (__ballot(s > ls[KC - 1]) == 0) continue;
+            int ci = c;
+#pragma unroll
+            for (int j = 0; j < KC; ++j) {      // insertion: strictly greater moves up
+                const bool gt = s > ls[j];
+                const float ts = gt ? s : ls[j];
+                const int tc = gt ? ci : lc[j];
+                s = gt ? ls[j] : s;
+                ci = gt ? lc[j] : ci;
+                ls[j] = ts;
+                lc[j] = tc;
+            }
         }
     }
     if (!valid) return;
@@ -146,18 +198,18 @@ __global__ __launch_bounds__(kTile) void select_kernel(Dims dm, const T* __restr
 template <typename T, int D>
 hipError_t launch_d(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
                     hipStream_t st) {
-    const int ntiles = cdiv(dm.L, kTile);
-    const dim3 grid(ntiles * dm.B * dm.G);
+    const int ngroups = cdiv(dm.L, kThreads);
+    const dim3 grid(ngroups * dm.B * dm.G);
     HSA_TIMED("select_kernel", st);
     if (dm.k <= 8)
-        hipLaunchKernelGGL((select_kernel<T, D, 8>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
-                           Kbar, idx, w, ntiles);
+        hipLaunchKernelGGL((select_kernel<T, D, 8>), grid, dim3(kThreads), 0, st, dm,
+                           (const T*)Q, Kbar, idx, w, ngroups);
     else if (dm.k <= 16)
-        hipLaunchKernelGGL((select_kernel<T, D, 16>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
-                           Kbar, idx, w, ntiles);
+        hipLaunchKernelGGL((select_kernel<T, D, 16>), grid, dim3(kThreads), 0, st, dm,
+                           (const T*)Q, Kbar, idx, w, ngroups);
     else
-        hipLaunchKernelGGL((select_kernel<T, D, 32>), grid, dim3(kTile), 0, st, dm, (const T*)Q,
-                           Kbar, idx, w, ntiles);
+        hipLaunchKernelGGL((select_kernel<T, D, 32>), grid, dim3(kThreads), 0, st, dm,
+                           (const T*)Q, Kbar, idx, w, ngroups);
     return hipGetLastError();
 }
 
