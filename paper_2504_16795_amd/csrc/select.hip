@@ -2,24 +2,31 @@
 // s_c = alpha * (sum_j q_j) . Kbar_c over the chunks before the token's own, and their
 // softmax weights).
 //
-// Workgroup = 4 waves on 256 consecutive tokens of one (b, g); lane = token.  Each lane
-// keeps its group query q~ = sum_j q_j (fp32, d registers) and a running top-KC list
-// (scores and chunk indices, registers, descending).  The candidates' landmark rows are
-// copied into LDS in blocks of 64 (two blocks in flight), shared by the four waves, and
-// read with broadcast LDS loads; candidates are visited in increasing chunk order.  A candidate enters a list only when its score is strictly greater than the
-// list's last entry and moves up past every entry it beats strictly: on equal scores the
-// lower chunk index stays first.  The k best get softmax weights and are written in
-// descending chunk order, padded with -1 / 0.
+// Lane = token; each lane keeps its group query q~ = sum_j q_j (fp32, d registers) and a
+// running top-KC list (scores and chunk indices, registers, descending).  The landmark rows
+// of the candidates are copied into LDS (direct copies, the next block in flight) and read
+// with broadcast LDS loads, in increasing chunk order.  Two schedules of the 4 waves of a
+// workgroup:
+//   - few candidates (short sequences): the waves hold 4 consecutive 64-token tiles and
+//     share blocks of 64 landmark rows;
+//   - many candidates: the waves hold the same tile and split its candidates (wave w takes
+//     the 16-row blocks w, w + 4, ...); the four lists are merged at the end.
+// A candidate enters a list only when its score is strictly greater than the list's last
+// entry and moves up past every entry it beats strictly: on equal scores the lower chunk
+// index stays first (the merge compares (score, chunk) the same way).  The k best get
+// softmax weights and are written in descending chunk order, padded with -1 / 0.
 #include "common.h"
 
 namespace hsa {
 namespace {
 
 constexpr int kTile = 64;     // tokens per wave
-constexpr int NW = 4;         // waves per workgroup: 4 consecutive tiles of one (b, g)
+constexpr int NW = 4;         // waves per workgroup, all on the same 64 tokens
 constexpr int kThreads = NW * kTile;
-constexpr int NB = 64;        // candidate rows per LDS block
-constexpr int NST = 2;        // LDS blocks
+constexpr int NB = 16;        // candidate rows per LDS block
+constexpr int NST = 2;        // LDS blocks per wave
+constexpr int TNB = 64;       // candidate rows per LDS block when the 4 waves share blocks
+constexpr int kSplitFrom = 256;   // more complete chunks than this: split the candidates
 
 // One global_load_lds_dwordx4 (lane l copies 16 bytes to lds_base + 16 l; lds_base
 // wave-uniform in M0), as inline assembly so that the compiler's waits do not make the
@@ -82,11 +89,11 @@ __device__ __forceinline__ void group_query(const float* __restrict__ qp, int h,
 }
 
 template <typename T, int D, int KC>
-__global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __restrict__ Q,
+__global__ __launch_bounds__(kThreads) void select_tiles_kernel(Dims dm, const T* __restrict__ Q,
                                                           const float* __restrict__ Kbar,
                                                           int32_t* __restrict__ idx,
                                                           float* __restrict__ w, int ngroups) {
-    __shared__ float kb_s[NST][NB * D];         // landmark rows of the staged candidate blocks
+    __shared__ float kb_s[NST][TNB * D];        // landmark rows of the staged candidate blocks
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // latest token groups (most candidates) first
     const int nbg = dm.B * dm.G;
@@ -117,19 +124,19 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __re
         lc[j] = -1;
     }
 
-    // candidate blocks of NB rows (row c of group g: D fp32 at Kbar + ((b C + c) G + g) D),
+    // candidate blocks of TNB rows (row c of group g: D fp32 at Kbar + ((b C + c) G + g) D),
     // copied into LDS by the NW waves: 2 rows per 1 KB copy instruction
     const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D;
     const size_t cstride = (size_t)dm.G * D;
-    const int nblk = cdiv(nwg, NB);
+    const int nblk = cdiv(nwg, TNB);
     auto issue = [&](int blk) __attribute__((always_inline)) {
         float* dst = kb_s[blk % NST];
         constexpr int RPI = 1024 / (D * 4);                // rows per copy instruction
 #pragma unroll
-        for (int i = 0; i < NB / RPI / NW; ++i) {
+        for (int i = 0; i < TNB / RPI / NW; ++i) {
             const int ci = (wave + i * NW);                // copy instruction of the block
             const int r = ci * RPI + lane / (64 / RPI);    // row within the block
-            const int c = min(blk * NB + r, nwg - 1);      // past the end: repeat a valid row
+            const int c = min(blk * TNB + r, nwg - 1);      // past the end: repeat a valid row
             sel_copy16(kb + (size_t)c * cstride + (lane % (64 / RPI)) * 4,
                        __builtin_amdgcn_readfirstlane(sel_lds_address(dst + ci * 256)));
         }
@@ -140,9 +147,9 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __re
         sel_barrier();                                     // block landed; other stage free
         if (blk + 1 < nblk) issue(blk + 1);
         const float* rows = kb_s[blk % NST];
-        const int cend = min(nwave, blk * NB + NB);
-        for (int c = blk * NB; c < cend; ++c) {
-            const float4* kr = reinterpret_cast<const float4*>(rows + (c - blk * NB) * D);
+        const int cend = min(nwave, blk * TNB + TNB);
+        for (int c = blk * TNB; c < cend; ++c) {
+            const float4* kr = reinterpret_cast<const float4*>(rows + (c - blk * TNB) * D);
             float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
             for (int e = 0; e < D / 4; ++e) {
@@ -195,21 +202,173 @@ __global__ __launch_bounds__(kThreads) void select_kernel(Dims dm, const T* __re
     }
 }
 
+template <typename T, int D, int KC>
+__global__ __launch_bounds__(kThreads) void select_split_kernel(Dims dm, const T* __restrict__ Q,
+                                                          const float* __restrict__ Kbar,
+                                                          int32_t* __restrict__ idx,
+                                                          float* __restrict__ w, int ntiles) {
+    // per wave: NST blocks of NB landmark rows; reused for the list merge at the end
+    constexpr int KBF = NW * NST * NB * D, MERGEF = 2 * NW * KC * 64;
+    __shared__ float lds_f[KBF > MERGEF ? KBF : MERGEF];
+    auto kb_s = reinterpret_cast<float (*)[NST][NB * D]>(lds_f);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    // latest tiles (most candidates) first
+    const int nbg = dm.B * dm.G;
+    const int tile = ntiles - 1 - (int)blockIdx.x / nbg;
+    const int bg = (int)blockIdx.x % nbg, b = bg / dm.G, g = bg % dm.G;
+    const int t0 = tile * kTile;
+    const int t = t0 + lane;
+    const bool valid = t < dm.L;
+    const int ncand = valid ? t / dm.S : 0;
+    const int ntile = (min(t0 + kTile, dm.L) - 1) / dm.S;   // candidates of the last token
+    const int k = dm.k;
+
+    float qb[D];
+    if (valid) {
+        group_query<D>(Q + (((size_t)b * dm.L + t) * dm.H + (size_t)g * dm.h) * D, dm.h, qb);
+    } else {
+#pragma unroll
+        for (int e = 0; e < D; ++e) qb[e] = 0.f;
+    }
+    wait_global_loads_sel();
+    float ls[KC];
+    int lc[KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        ls[j] = -INFINITY;
+        lc[j] = -1;
+    }
+
+    // wave w takes the candidate blocks w, w + NW, ... (NB rows each; row c of group g is
+    // D fp32 at Kbar + ((b C + c) G + g) D), copied into its own LDS blocks
+    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D;
+    const size_t cstride = (size_t)dm.G * D;
+    const int nblk = cdiv(ntile, NB);
+    auto issue = [&](int blk) __attribute__((always_inline)) {
+        float* dst = kb_s[wave][(blk / NW) % NST];
+        constexpr int RPI = 1024 / (D * 4);                // rows per copy instruction
+#pragma unroll
+        for (int ci = 0; ci < NB / RPI; ++ci) {
+            const int r = ci * RPI + lane / (64 / RPI);
+            const int c = min(blk * NB + r, ntile - 1);   // past the end: repeat a valid row
+            sel_copy16(kb + (size_t)c * cstride + (lane % (64 / RPI)) * 4,
+                       __builtin_amdgcn_readfirstlane(sel_lds_address(dst + ci * 256)));
+        }
+    };
+    if (wave < nblk) issue(wave);
+    for (int blk = wave; blk < nblk; blk += NW) {
+        sel_wait_all();                                    // this wave's block has landed
+        if (blk + NW < nblk) issue(blk + NW);
+        const float* rows = kb_s[wave][(blk / NW) % NST];
+        const int cend = min(ntile, blk * NB + NB);
+        for (int c = blk * NB; c < cend; ++c) {
+            const float4* kr = reinterpret_cast<const float4*>(rows + (c - blk * NB) * D);
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+            for (int e = 0; e < D / 4; ++e) {
+                const float4 kv = kr[e];
+                a0 = fmaf(qb[4 * e], kv.x, a0);
+                a1 = fmaf(qb[4 * e + 1], kv.y, a1);
+                a2 = fmaf(qb[4 * e + 2], kv.z, a2);
+                a3 = fmaf(qb[4 * e + 3], kv.w, a3);
+            }
+            float s = (c < ncand) ? dm.alpha * ((a0 + a1) + (a2 + a3)) : -INFINITY;
+            if (__ballot(s > ls[KC - 1]) == 0) continue;
+            int ci = c;
+#pragma unroll
+            for (int j = 0; j < KC; ++j) {      // insertion: strictly greater moves up
+                const bool gt = s > ls[j];
+                const float ts = gt ? s : ls[j];
+                const int tc = gt ? ci : lc[j];
+                s = gt ? ls[j] : s;
+                ci = gt ? lc[j] : ci;
+                ls[j] = ts;
+                lc[j] = tc;
+            }
+        }
+    }
+    // merge the waves' lists into wave 0's: each list is ordered by (score desc, chunk asc);
+    // the merge compares the same way, so ties keep the lower chunk first
+    __syncthreads();
+    float* ms = lds_f;                                      // [NW][KC][64] scores, then chunks
+    int* mc = reinterpret_cast<int*>(ms + NW * KC * 64);
+    if (wave > 0) {
+#pragma unroll
+        for (int j = 0; j < KC; ++j) {
+            ms[(wave * KC + j) * 64 + lane] = ls[j];
+            mc[(wave * KC + j) * 64 + lane] = lc[j];
+        }
+    }
+    __syncthreads();
+    if (wave != 0 || !valid) return;
+    for (int ow = 1; ow < NW; ++ow) {
+        for (int jj = 0; jj < KC; ++jj) {
+            float s = ms[(ow * KC + jj) * 64 + lane];
+            int ci = mc[(ow * KC + jj) * 64 + lane];
+            if (__ballot(s > ls[KC - 1] || (s == ls[KC - 1] && ci < lc[KC - 1] && s > -INFINITY)) == 0)
+                break;                                     // the rest of this list is no better
+#pragma unroll
+            for (int j = 0; j < KC; ++j) {
+                const bool gt = s > ls[j] || (s == ls[j] && ci < lc[j] && s > -INFINITY);
+                const float ts = gt ? s : ls[j];
+                const int tc = gt ? ci : lc[j];
+                s = gt ? ls[j] : s;
+                ci = gt ? lc[j] : ci;
+                ls[j] = ts;
+                lc[j] = tc;
+            }
+        }
+    }
+
+    // softmax over the k best, written in descending chunk order
+    const int n = min(k, ncand);
+    const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
+    float ex[KC];
+    float z = 0.f;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        ex[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
+        z += ex[j];
+    }
+    const float iz = 1.f / z;
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        if (j < n) {
+            int rank = 0;
+#pragma unroll
+            for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
+            idx[o + rank] = lc[j];
+            w[o + rank] = ex[j] * iz;
+        } else if (j < k) {
+            idx[o + j] = -1;
+            w[o + j] = 0.f;
+        }
+    }
+}
+
+template <typename T, int D, int KC>
+void launch_kc(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
+               hipStream_t st) {
+    if (dm.C <= kSplitFrom) {
+        // few candidates: four consecutive tiles share each landmark block
+        const int ngroups = cdiv(dm.L, kThreads);
+        hipLaunchKernelGGL((select_tiles_kernel<T, D, KC>), dim3(ngroups * dm.B * dm.G),
+                           dim3(kThreads), 0, st, dm, (const T*)Q, Kbar, idx, w, ngroups);
+    } else {
+        // many candidates: the four waves of a tile split them
+        const int ntiles = cdiv(dm.L, kTile);
+        hipLaunchKernelGGL((select_split_kernel<T, D, KC>), dim3(ntiles * dm.B * dm.G),
+                           dim3(kThreads), 0, st, dm, (const T*)Q, Kbar, idx, w, ntiles);
+    }
+}
+
 template <typename T, int D>
 hipError_t launch_d(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
                     hipStream_t st) {
-    const int ngroups = cdiv(dm.L, kThreads);
-    const dim3 grid(ngroups * dm.B * dm.G);
     HSA_TIMED("select_kernel", st);
-    if (dm.k <= 8)
-        hipLaunchKernelGGL((select_kernel<T, D, 8>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, Kbar, idx, w, ngroups);
-    else if (dm.k <= 16)
-        hipLaunchKernelGGL((select_kernel<T, D, 16>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, Kbar, idx, w, ngroups);
-    else
-        hipLaunchKernelGGL((select_kernel<T, D, 32>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, Kbar, idx, w, ngroups);
+    if (dm.k <= 8) launch_kc<T, D, 8>(dm, Q, Kbar, idx, w, st);
+    else if (dm.k <= 16) launch_kc<T, D, 16>(dm, Q, Kbar, idx, w, st);
+    else launch_kc<T, D, 32>(dm, Q, Kbar, idx, w, st);
     return hipGetLastError();
 }
 

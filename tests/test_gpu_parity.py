@@ -29,6 +29,8 @@ CASES = {
     "no_candidates_bf16": (Shape(2, 50, 8, 1, 128, 64, 4, "bf16"), 15, "iid"),
     "ragged_mfma_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 16, "iid"),
     "wide_k16_bf16": (Shape(1, 2304, 32, 4, 128, 128, 16, "bf16"), 17, "lowrank"),
+    "k24_bf16": (Shape(1, 2048, 16, 2, 128, 32, 24, "bf16"), 18, "iid"),
+    "k20_d64_f32": (Shape(1, 1500, 4, 2, 64, 32, 20, "f32"), 19, "iid"),
 }
 
 _cache = {}
@@ -269,3 +271,22 @@ def test_backward_empty_slots(hsa_gpu, name):
     torch.cuda.synchronize()
     for n, g_, r in zip(("dQ", "dK", "dV"), got, want):
         assert_close(n, shape, g_, r)
+
+
+@pytest.mark.parametrize("shape", [Shape(1, 20480, 16, 2, 128, 64, 8, "bf16"),
+                                   Shape(1, 8192, 4, 1, 64, 16, 20, "f32")],
+                         ids=["C320_bf16", "C512_d64_k20_f32"])
+def test_select_many_candidates(hsa_gpu, shape):
+    """Sequences with more than 256 complete chunks: the selection splits each tile's
+    candidates over its waves and merges their lists."""
+    banner("select_%dx%d" % (shape.L, shape.S), "hsa_select_topk, many candidates")
+    inp, _ = make_case(shape, 41, kind="iid")
+    Kbar_ref = oracle.landmarks(inp["K"], shape.S)
+    idx_ref, w_ref, gap, _ = oracle.select(inp["Q"], Kbar_ref, shape.G, shape.S, shape.k)
+    Q = to_dev(inp["Q"], shape)
+    Kbar = torch.from_numpy(Kbar_ref.astype(np.float32)).cuda()
+    idx, w = hsa_gpu.hsa_select_topk(Q, Kbar, shape.G, shape.S, shape.k)
+    torch.cuda.synchronize()
+    sure, loose = assert_indices(idx, idx_ref, gap, shape.S)
+    assert loose == 0
+    assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= W_ATOL
