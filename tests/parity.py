@@ -95,9 +95,11 @@ def assert_close(name, shape, got: torch.Tensor, ref: np.ndarray, ulps: float = 
     return float(err.max())
 
 
-def assert_indices(idx_gpu: torch.Tensor, ref_idx: np.ndarray, gap: np.ndarray, S: int):
+def assert_indices(idx_gpu: torch.Tensor, ref_idx: np.ndarray, gap: np.ndarray, S: int,
+                   tokens=None):
     """Bit-exact where the oracle gap is >= MIN_GAP; elsewhere only validity is checked
-    (distinct, descending, in range, the right count)."""
+    (distinct, descending, in range, the right count).  tokens[i] is the sequence position
+    of row i along axis 1 (default: row i is token i)."""
     got = idx_gpu.cpu().numpy()
     sure = gap >= MIN_GAP                                    # [B, L, G]
     bad = np.nonzero((got != ref_idx).any(-1) & sure)
@@ -106,7 +108,8 @@ def assert_indices(idx_gpu: torch.Tensor, ref_idx: np.ndarray, gap: np.ndarray, 
     for b, t, g in zip(*np.nonzero(~sure)):
         row = got[b, t, g]
         valid = row[row >= 0]
-        assert len(valid) == min(k, t // S)
+        pos = int(tokens[t]) if tokens is not None else int(t)
+        assert len(valid) == min(k, pos // S)
         assert np.all(row[len(valid):] == -1)
-        assert np.all(np.diff(valid) < 0) and np.all(valid < t // S)
+        assert np.all(np.diff(valid) < 0) and np.all(valid < pos // S)
     return int(sure.sum()), int((~sure).sum())
