@@ -138,6 +138,46 @@ __device__ __forceinline__ void wave_argmax_dpp(float& s, int& c) {
     pick_better(s, c, s1, c1);
 }
 
+// (score, chunk) as one unsigned 64-bit key ordered like (score desc, chunk asc): the float
+// bits mapped to an order-preserving unsigned value above the complemented chunk id.  Key 0
+// is below every key of a real candidate (even one scoring -inf).
+__device__ __forceinline__ uint64_t order_key(float s, int c) {
+    const uint32_t u = __float_as_uint(s + 0.0f);     // -0 and +0 rank alike
+
+    const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+    return ((uint64_t)o << 32) | (uint32_t)(~(uint32_t)c);
+}
+__device__ __forceinline__ int key_chunk(uint64_t key) { return (int)~(uint32_t)key; }
+__device__ __forceinline__ float key_score(uint64_t key) {
+    const uint32_t o = (uint32_t)(key >> 32);
+    return __uint_as_float((o & 0x80000000u) ? (o & 0x7FFFFFFFu) : ~o);
+}
+__device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return b > a ? b : a; }
+
+// Wave-wide maximum of a 64-bit key, branch-free (DPP moves inside rows, then the lane
+// swaps across rows); every lane ends with the maximum.
+__device__ __forceinline__ uint64_t wave_max_key(uint64_t x) {
+    auto step = [&](auto mov) __attribute__((always_inline)) {
+        const uint32_t lo = (uint32_t)mov((int)(uint32_t)x);
+        const uint32_t hi = (uint32_t)mov((int)(uint32_t)(x >> 32));
+        x = max_u64(x, ((uint64_t)hi << 32) | lo);
+    };
+    step([](int v) { return dpp_mov<kDppXor1>(v); });
+    step([](int v) { return dpp_mov<kDppXor2>(v); });
+    step([](int v) { return dpp_mov<kDppHalfMirror>(v); });
+    step([](int v) { return dpp_mov<kDppMirror>(v); });
+    int a0, a1, b0, b1;
+    lane_swap<false>(a0, a1, (int)(uint32_t)x);
+    lane_swap<false>(b0, b1, (int)(uint32_t)(x >> 32));
+    x = max_u64(((uint64_t)(uint32_t)b0 << 32) | (uint32_t)a0,
+                ((uint64_t)(uint32_t)b1 << 32) | (uint32_t)a1);
+    lane_swap<true>(a0, a1, (int)(uint32_t)x);
+    lane_swap<true>(b0, b1, (int)(uint32_t)(x >> 32));
+    x = max_u64(((uint64_t)(uint32_t)b0 << 32) | (uint32_t)a0,
+                ((uint64_t)(uint32_t)b1 << 32) | (uint32_t)a1);
+    return x;
+}
+
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // RAII bracket of one kernel launch for the optional per-kernel timing (timing.hip).

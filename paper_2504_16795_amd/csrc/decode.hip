@@ -7,10 +7,17 @@
 // their partial dot products with DPP moves.  Each wave then extracts the slice's top-k of
 // one group by k rounds of a wave-wide arg-max (ties to the lower chunk index) and writes
 // k (score, chunk) candidates.
-// Stage 2 (finish): workgroup = (slot, b, g): the k selected chunks are attended in
-// parallel.  Stage 3 (combine): workgroup = (b, g), sums their weighted partial outputs in
-// slot order.
-#include "common.h"
+// Stages 2 and 3, MFMA path (bf16, d = 128, h = 8, S = 64): workgroup = (b, g) with 8
+// waves.  Wave 0 merges the slice candidates into the top-k; wave w then attends the
+// selected chunks w, w + 8, ... with matrix cores (K fragments straight from global memory
+// into registers, V rows copied into the wave's own LDS stage and read transposed, as in
+// the forward), and the waves' weighted partial outputs are summed in LDS in wave order.
+// Other shapes: stage 2 (finish), workgroup = (slot, b, g), attends the k selected chunks
+// in parallel; stage 3 (combine), workgroup = (b, g), sums their weighted partial outputs
+// in slot order.
+#include <cstdlib>
+
+#include "chunk_lds.h"
 
 namespace hsa {
 namespace {
@@ -22,7 +29,7 @@ constexpr int kFinThreads = 256;
 constexpr int NW = kFinThreads / 64;
 constexpr int HMAX = 16;
 constexpr int KMAX = 32;
-constexpr int NCMAX = 4096;        // slice candidates merged from LDS (else from global memory)
+constexpr int NCMAX = 4096;        // slice candidates merged in registers (else sequentially)
 
 template <typename T> struct V16;
 template <> struct V16<float> { static constexpr int n = 4; };
@@ -51,35 +58,48 @@ __device__ __forceinline__ int cache_tokens(const int32_t* cache_len, int b, int
     return n < 0 ? 0 : (n > ncap ? ncap : n);
 }
 
-template <typename Tq, typename Tk, int D>
-__global__ __launch_bounds__(kScanThreads) void decode_scan(
-    Dims dm, const Tq* __restrict__ q, const Tk* __restrict__ Kbar,
-    const int32_t* __restrict__ cache_len, float* __restrict__ cand_s,
-    int32_t* __restrict__ cand_c, int nslices) {
-    constexpr int VN = V16<Tk>::n;
-    constexpr int LPR = D / VN;       // lanes per landmark row
-    __shared__ float qs[GMAX * D];
-    __shared__ float sc[SL * GMAX];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int b = blockIdx.y, slice = blockIdx.x;
-    const int G = dm.G, h = dm.h, k = dm.k;
-    const int ncand = cache_tokens(cache_len, b, dm.L) / dm.S;
-    const int c0 = slice * SL;
-    const int nch = max(0, min(SL, ncand - c0));
-
-    for (int i = tid; i < G * D; i += kScanThreads) {
-        const int g = i / D, e = i % D;
+// Query of group g summed over its h heads, qs[g D + e] (fp32).  Called by every thread of
+// the scan workgroup; `issue` is run right after the loads of the first kScanThreads
+// elements are issued and before their values are used, so loads it issues overlap them
+// (vector-memory loads complete in order: the query's, issued first, land first; further
+// elements, G d > kScanThreads, are loaded after it).  The loads are branch-free (indices
+// clamped to valid elements, unused values dropped) so that they issue back to back.
+template <typename Tq, int D, typename Issue>
+__device__ __forceinline__ void scan_query(const Dims& dm, const Tq* __restrict__ q, int b,
+                                           float* qs, Issue issue) {
+    const int tid = threadIdx.x;
+    const int G = dm.G, h = dm.h;
+    for (int i00 = 0; i00 < G * D; i00 += kScanThreads) {
+        const int i = i00 + tid;
+        const int i0 = i < G * D ? i : 0;
+        const int g = i0 / D, e = i0 % D;
+        float qv[HMAX];
+#pragma unroll
+        for (int j = 0; j < HMAX; ++j)
+            qv[j] = to_f32(q[((size_t)b * dm.H + g * h + min(j, h - 1)) * D + e]);
+        if (i00 == 0) issue();
         float s = 0.f;
-        for (int j = 0; j < h; ++j) s += to_f32(q[((size_t)b * dm.H + g * h + j) * D + e]);
-        qs[i] = s;
+#pragma unroll
+        for (int j = 0; j < HMAX; ++j) s += (j < h) ? qv[j] : 0.f;
+        if (i < G * D) qs[i] = s;
     }
-    __syncthreads();
+}
+
+// Scores with vector ALU dot products: U 16-byte vectors per thread per pass, loads first;
+// D / VN consecutive lanes share a landmark row and reduce with DPP moves.
+template <typename Tq, typename Tk, int D>
+__device__ __forceinline__ void scan_scores_valu(const Dims& dm, const Tq* __restrict__ q,
+                                                 const Tk* __restrict__ Kbar, int b, int c0,
+                                                 int nch, float* qs, float* sc) {
+    constexpr int VN = V16<Tk>::n;
+    constexpr int LPR = D / VN;
+    constexpr int U = 32;
+    const int tid = threadIdx.x;
+    const int G = dm.G;
     const Tk* base = Kbar + ((size_t)b * dm.C + c0) * G * D;
     const int nvec = nch * G * LPR;
-    // U vectors per thread per pass, loads first; a row's LPR lanes reduce with DPP moves
-    constexpr int U = 32;
-    for (int v0 = 0; v0 < nvec; v0 += kScanThreads * U) {
-        uint4 raw[U];
+    uint4 raw[U];
+    auto load_pass = [&](int v0) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int v = v0 + u * kScanThreads + tid;
@@ -87,6 +107,11 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
                                                                 (v % LPR) * VN)
                               : uint4{0u, 0u, 0u, 0u};
         }
+    };
+    scan_query<Tq, D>(dm, q, b, qs, [&]() __attribute__((always_inline)) { load_pass(0); });
+    __syncthreads();
+    for (int v0 = 0; v0 < nvec; v0 += kScanThreads * U) {
+        if (v0 > 0) load_pass(v0);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int v = v0 + u * kScanThreads + tid;
@@ -101,32 +126,261 @@ __global__ __launch_bounds__(kScanThreads) void decode_scan(
             if (v < nvec && part == 0) sc[row] = dm.alpha * dot;
         }
     }
+}
+
+// Scores of bf16 landmarks with packed dot products: the same contiguous loads as
+// scan_scores_valu (a 16-byte vector per lane, D / 8 lanes per row), each vector reduced by
+// four bf16 pair dot products (fp32 accumulation) against the summed query split into a
+// bf16 pair hi + lo (16 mantissa bits together), then across the row's lanes.  A thread's
+// slice of d and its group are the same for all its vectors when G divides the rows a
+// pass covers per thread step (kScanThreads / (D / 8)), so its query fragments are loaded
+// once.  Vectors are reduced as they land (loads complete in order).
+template <typename Tq, int D>
+__device__ __forceinline__ void scan_scores_dot2(const Dims& dm, const Tq* __restrict__ q,
+                                                 const bf16* __restrict__ Kb, int b, int c0,
+                                                 int nch, float* qs, float* sc) {
+    constexpr int LPR = D / 8;
+    constexpr int U = 32;
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const int tid = threadIdx.x;
+    const int G = dm.G;
+    const bf16* base = Kb + ((size_t)b * dm.C + c0) * G * D;
+    const int nvec = nch * G * LPR;
+    uint4 raw[U];
+    auto load_pass = [&](int v0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * kScanThreads + tid;
+            raw[u] = v < nvec ? *reinterpret_cast<const uint4*>(base + (size_t)(v / LPR) * D +
+                                                                (v % LPR) * 8)
+                              : uint4{0u, 0u, 0u, 0u};
+        }
+    };
+    scan_query<Tq, D>(dm, q, b, qs, [&]() __attribute__((always_inline)) { load_pass(0); });
     __syncthreads();
+    const int part = tid % LPR, g = (tid / LPR) % G;
+    bf16x2_t qh[4], ql[4];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float v = qs[g * D + part * 8 + i];
+        const __bf16 hi = f2bf(v);
+        qh[i >> 1][i & 1] = hi;
+        ql[i >> 1][i & 1] = f2bf(v - (float)hi);
+    }
+    for (int v0 = 0; v0 < nvec; v0 += kScanThreads * U) {
+        if (v0 > 0) load_pass(v0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = v0 + u * kScanThreads + tid;
+            const uint32_t w[4] = {raw[u].x, raw[u].y, raw[u].z, raw[u].w};
+            float dot = 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bf16x2_t x = __builtin_bit_cast(bf16x2_t, w[i]);
+                dot = __builtin_amdgcn_fdot2_f32_bf16(x, qh[i], dot, false);
+                dot = __builtin_amdgcn_fdot2_f32_bf16(x, ql[i], dot, false);
+            }
+            dot = group_sum<LPR>(dot);
+            if (v < nvec && part == 0) sc[v / LPR] = dm.alpha * dot;
+        }
+    }
+}
+
+template <typename Tk, int D>
+constexpr bool kDot2Scan = sizeof(Tk) == 2 && (D == 128 || D == 64);
+
+template <typename Tq, typename Tk, int D>
+__global__ __launch_bounds__(kScanThreads, 2) void decode_scan(
+    Dims dm, const Tq* __restrict__ q, const Tk* __restrict__ Kbar,
+    const int32_t* __restrict__ cache_len, float* __restrict__ cand_s,
+    int32_t* __restrict__ cand_c, int nslices) {
+    __shared__ float qs[GMAX * D];
+    __shared__ float sc[SL * GMAX];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int b = blockIdx.y, slice = blockIdx.x;
+    const int G = dm.G, k = dm.k;
+    const int ncand = cache_tokens(cache_len, b, dm.L) / dm.S;
+    const int c0 = slice * SL;
+    const int nch = max(0, min(SL, ncand - c0));
+
+    // Scores sc[cl G + g] = alpha qbar_g . Kbar[c0 + cl, g] of the slice's rows.
+    if constexpr (kDot2Scan<Tk, D>) {
+        if ((kScanThreads / (D / 8)) % G == 0)
+            scan_scores_dot2<Tq, D>(dm, q, reinterpret_cast<const bf16*>(Kbar), b, c0, nch, qs,
+                                    sc);
+        else scan_scores_valu<Tq, Tk, D>(dm, q, Kbar, b, c0, nch, qs, sc);
+    } else {
+        scan_scores_valu<Tq, Tk, D>(dm, q, Kbar, b, c0, nch, qs, sc);
+    }
+    __syncthreads();
+    // top-k of the slice for each group: k rounds of a wave-wide maximum of order keys
     for (int g = wave; g < G; g += kScanThreads / 64) {
-        float s[SL / 64];
+        uint64_t key[SL / 64];
 #pragma unroll
         for (int m = 0; m < SL / 64; ++m) {
             const int cl = lane + 64 * m;
-            s[m] = (cl < nch) ? sc[cl * G + g] : -INFINITY;
+            key[m] = (cl < nch) ? order_key(sc[cl * G + g], c0 + cl) : 0;
         }
         float* os = cand_s + (((size_t)b * G + g) * nslices + slice) * k;
         int32_t* oc = cand_c + (((size_t)b * G + g) * nslices + slice) * k;
         for (int i = 0; i < k; ++i) {
-            float bs = -INFINITY;
-            int bc = 0x7FFFFFFF;
+            uint64_t best = 0;
 #pragma unroll
-            for (int m = 0; m < SL / 64; ++m) pick_better(bs, bc, s[m], lane + 64 * m);
-            wave_argmax_dpp(bs, bc);
-            const bool found = bs > -INFINITY;
+            for (int m = 0; m < SL / 64; ++m) best = max_u64(best, key[m]);
+            best = wave_max_key(best);
             if (lane == 0) {
-                os[i] = bs;
-                oc[i] = found ? c0 + bc : -1;
+                os[i] = best ? key_score(best) : -INFINITY;
+                oc[i] = best ? key_chunk(best) : -1;
             }
 #pragma unroll
             for (int m = 0; m < SL / 64; ++m)
-                if (found && bc == lane + 64 * m) s[m] = -INFINITY;
+                if (key[m] == best) key[m] = 0;
         }
     }
+}
+
+// Final top-k of (b, g) from the slice candidates, by wave 0 (lane i < n receives the
+// i-th best; candidates carry distinct chunk ids, so (score desc, chunk asc) is a strict
+// total order and round i takes the best candidate ranked below the winner of round
+// i - 1), then the softmax chunk weights and the descending-chunk slot order into sel_c /
+// sel_w (slots n .. k - 1 empty).
+__device__ __forceinline__ void merge_candidates(const float* cs, const int32_t* cc, int nc,
+                                                 int n, int k, int lane, int* sel_c,
+                                                 float* sel_w) {
+    float ls = -INFINITY;
+    int lc = -1;
+    float ps = INFINITY;
+    int pc = -1;
+    const int niter = cdiv(nc, 64);
+    for (int i = 0; i < n; ++i) {
+        float bs = -INFINITY;
+        int bc = 0x7FFFFFFF;
+        for (int it = 0; it < niter; ++it) {
+            const int x = it * 64 + lane;
+            if (x < nc) {
+                const int c = cc[x];
+                const float s = cs[x];
+                if (c >= 0 && better(ps, pc, s, c) && better(s, c, bs, bc)) {
+                    bs = s;
+                    bc = c;
+                }
+            }
+        }
+        wave_argmax_dpp(bs, bc);
+        if (lane == i) {
+            ls = bs;
+            lc = bc;
+        }
+        ps = bs;
+        pc = bc;
+    }
+    const float m = __shfl(ls, 0, 64);
+    const float ex = (lane < n) ? expf(ls - m) : 0.f;
+    const float z = wave_sum(ex);
+    int rank = 0;
+    for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
+    if (lane < n) {
+        sel_c[rank] = lc;
+        sel_w[rank] = ex / z;
+    } else if (lane < k) {
+        sel_c[lane] = -1;
+        sel_w[lane] = 0.f;
+    }
+}
+
+// The same top-k by a two-level tournament over the whole workgroup (NWV waves), on order
+// keys (score desc, chunk asc as one 64-bit integer, so every comparison is branch-free):
+// each thread holds the keys of its candidates x = tid + j NT (j < NPL), each wave
+// extracts the top n of its threads' keys by n rounds of a wave-wide maximum (the winner
+// is knocked out of its lane) into tmp, and wave 0 extracts the top n of the NWV n
+// survivors (NP2 per lane), then finishes as merge_candidates.  The top n of a union is the
+// top n of the parts' top n, and the order is strict, so the result equals
+// merge_candidates'.  Needs nc <= NPL NT and NWV n <= 64 NP2; every thread calls it; ends
+// with a barrier.
+template <int NWV, int NPL, int NP2>
+__device__ __forceinline__ void merge_tournament(const float* __restrict__ cs,
+                                                 const int32_t* __restrict__ cc, int nc, int n,
+                                                 int k, uint64_t* tmp, int* sel_c,
+                                                 float* sel_w) {
+    constexpr int NT = NWV * 64;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float s[NPL];
+    int c[NPL];
+    // all loads first (neither depends on the other's value), keys afterwards
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) {
+        const int x = tid + j * NT;
+        c[j] = x < nc ? cc[x] : -1;
+        s[j] = x < nc ? cs[x] : -INFINITY;
+    }
+    uint64_t key[NPL];
+#pragma unroll
+    for (int j = 0; j < NPL; ++j) key[j] = c[j] >= 0 ? order_key(s[j], c[j]) : 0;
+    for (int r = 0; r < n; ++r) {
+        uint64_t best = 0;
+#pragma unroll
+        for (int j = 0; j < NPL; ++j) best = max_u64(best, key[j]);
+        best = wave_max_key(best);
+#pragma unroll
+        for (int j = 0; j < NPL; ++j)
+            if (key[j] == best) key[j] = 0;
+        if (lane == 0) tmp[wave * n + r] = best;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        uint64_t key2[NP2];
+#pragma unroll
+        for (int j = 0; j < NP2; ++j) {
+            const int x = lane + 64 * j;
+            key2[j] = x < NWV * n ? tmp[x] : 0;
+        }
+        uint64_t mine = 0;               // lane r receives the r-th best
+        for (int r = 0; r < n; ++r) {
+            uint64_t best = 0;
+#pragma unroll
+            for (int j = 0; j < NP2; ++j) best = max_u64(best, key2[j]);
+            best = wave_max_key(best);
+#pragma unroll
+            for (int j = 0; j < NP2; ++j)
+                if (key2[j] == best) key2[j] = 0;
+            if (lane == r) mine = best;
+        }
+        const float ls = mine ? key_score(mine) : -INFINITY;
+        const int lc = mine ? key_chunk(mine) : -1;
+        const float m = __shfl(ls, 0, 64);
+        const float ex = (lane < n && lc >= 0) ? expf(ls - m) : 0.f;
+        const float z = wave_sum(ex);
+        int rank = 0;
+        for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
+        if (lane < n) {
+            sel_c[rank] = lc;
+            sel_w[rank] = ex / z;
+        } else if (lane < k) {
+            sel_c[lane] = -1;
+            sel_w[lane] = 0.f;
+        }
+    }
+    __syncthreads();
+}
+
+// merge_tournament with the fewest registers that hold nc candidates and the survivors;
+// false (nothing done) when nc exceeds NPLMAX per thread.
+template <int NWV, int NPLMAX>
+__device__ __forceinline__ bool merge_top(const float* __restrict__ cs,
+                                          const int32_t* __restrict__ cc, int nc, int n, int k,
+                                          uint64_t* tmp, int* sel_c, float* sel_w) {
+    constexpr int NT = NWV * 64;
+    const bool s1 = NWV * n <= 64;
+    if (nc <= NT) {
+        if (s1) merge_tournament<NWV, 1, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+        else merge_tournament<NWV, 1, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+    } else if (nc <= NPLMAX * NT) {
+        if (s1) merge_tournament<NWV, NPLMAX, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+        else merge_tournament<NWV, NPLMAX, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+    } else {
+        return false;
+    }
+    return true;
 }
 
 // Stage 2 (finish): workgroup = (slot, b, g), so the k selected chunks of a sequence are
@@ -150,8 +404,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     __shared__ float pz[HMAX * SMAX];
     __shared__ int sel_c[KMAX];
     __shared__ float sel_w[KMAX];
-    __shared__ float lcs[NCMAX];
-    __shared__ int lcc[NCMAX];
+    __shared__ uint64_t mtmp[NW * KMAX];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int slot = blockIdx.x;
     const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
@@ -162,60 +415,14 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     for (int i = tid; i < h * D; i += kFinThreads)
         qf[(i / D) * DP + i % D] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
     const int nc = nslices * k;
-    const bool in_lds = nc <= NCMAX;
-    if (in_lds) {
-        for (int x = tid; x < nc; x += kFinThreads) {
-            lcs[x] = cand_s[(size_t)bg * nc + x];
-            lcc[x] = cand_c[(size_t)bg * nc + x];
-        }
+    if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                             nc, n, k, mtmp, sel_c, sel_w)) {
+        __syncthreads();
+        if (wave == 0)
+            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
+                             sel_c, sel_w);
+        __syncthreads();
     }
-    __syncthreads();
-    if (wave == 0) {
-        const float* cs = in_lds ? lcs : cand_s + (size_t)bg * nc;
-        const int32_t* cc = in_lds ? lcc : cand_c + (size_t)bg * nc;
-        float ls = -INFINITY;      // lane i < n receives the i-th best candidate
-        int lc = -1;
-        // Candidates carry distinct chunk ids, so (score desc, chunk asc) is a strict total
-        // order: round i takes the best candidate ranked below the winner of round i-1.
-        float ps = INFINITY;
-        int pc = -1;
-        const int niter = cdiv(nc, 64);
-        for (int i = 0; i < n; ++i) {
-            float bs = -INFINITY;
-            int bc = 0x7FFFFFFF;
-            for (int it = 0; it < niter; ++it) {
-                const int x = it * 64 + lane;
-                if (x < nc) {
-                    const int c = cc[x];
-                    const float s = cs[x];
-                    if (c >= 0 && better(ps, pc, s, c) && better(s, c, bs, bc)) {
-                        bs = s;
-                        bc = c;
-                    }
-                }
-            }
-            wave_argmax_dpp(bs, bc);
-            if (lane == i) {
-                ls = bs;
-                lc = bc;
-            }
-            ps = bs;
-            pc = bc;
-        }
-        const float m = __shfl(ls, 0, 64);
-        const float ex = (lane < n) ? expf(ls - m) : 0.f;
-        const float z = wave_sum(ex);
-        int rank = 0;
-        for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
-        if (lane < n) {
-            sel_c[rank] = lc;
-            sel_w[rank] = ex / z;
-        } else if (lane < k) {
-            sel_c[lane] = -1;
-            sel_w[lane] = 0.f;
-        }
-    }
-    __syncthreads();
     if (slot == 0 && tid < k) {
         idx_out[(size_t)bg * k + tid] = sel_c[tid];
         w_out[(size_t)bg * k + tid] = sel_w[tid];
@@ -272,6 +479,131 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
 
 }
 
+constexpr int kAttWaves = 8;
+constexpr int kAttS = 64;
+constexpr int kAttD = 128;
+constexpr int kAttH = 8;
+
+__global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
+    Dims dm, const __bf16* __restrict__ q, const __bf16* __restrict__ Kc,
+    const __bf16* __restrict__ Vc, const int32_t* __restrict__ cache_len,
+    const float* __restrict__ cand_s, const int32_t* __restrict__ cand_c, int nslices,
+    __bf16* __restrict__ o, int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
+    constexpr int S = kAttS, DD = kAttD, NWV = kAttWaves, MB = S / 16, KS2 = S / 32;
+    constexpr int NT = NWV * 64;
+    // Per-wave V stages.  Before the first copy they hold the merge's survivors; after the
+    // last product, the waves' partial outputs.
+    __shared__ __bf16 vst[NWV][S * DD];
+    __shared__ int sel_c[KMAX];
+    __shared__ float sel_w[KMAX];
+    static_assert(NWV * KMAX * sizeof(uint64_t) <= sizeof(vst), "survivors must fit the stages");
+    static_assert(NWV * kAttH * DD * 4 <= sizeof(vst), "partial outputs must fit the stages");
+    uint64_t* mtmp = reinterpret_cast<uint64_t*>(&vst[0][0]);
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = lane & 15, grp = lane >> 4;
+    const int bg = blockIdx.x, b = bg / dm.G, g = bg % dm.G;
+    const int k = dm.k;
+    const int n = min(k, cache_tokens(cache_len, b, dm.L) / S);
+
+    // Q^T operand: columns 0-7 are the group's heads, 8-15 zero
+    bf16x8_t qB[4];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)     // branch-free loads (rows 8-15 repeat 0-7), then zeroed
+        qB[ks] = ld_bf16x8(q + ((size_t)b * dm.H + (size_t)g * kAttH + (row & 7)) * DD + 32 * ks +
+                           8 * grp);
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+        if (row >= kAttH) qB[ks] = bf16x8_t{};
+    const int nc = nslices * k;
+    if (!merge_top<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n,
+                                     k, mtmp, sel_c, sel_w)) {
+        if (wave == 0)
+            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
+                             sel_c, sel_w);
+        __syncthreads();
+    }
+    if (tid < k) {
+        idx_out[(size_t)bg * k + tid] = sel_c[tid];
+        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    }
+
+    f32x4_t acc[8];
+#pragma unroll
+    for (int db = 0; db < 8; ++db) acc[db] = zero4();
+    int toff[8];
+    tr_read_offsets(lane, toff);
+    const float sl2 = dm.beta * 1.44269504088896341f;
+    const size_t rowstride = (size_t)dm.G * DD;
+    __bf16* stage = vst[wave];
+    for (int slot = wave; slot < n; slot += NWV) {
+        const int c = sel_c[slot];
+        const float wi = sel_w[slot];
+        const size_t key0 = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * DD;
+        // V rows into the stage (copies, issued first: older than the K loads below, so
+        // the compiler's waits for those stay exact), K fragments into registers
+        chunk_to_lds<S, 1>(Vc + key0, rowstride, stage, 0, lane);
+        bf16x8_t kf[4][MB];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+                kf[ks][mb] = ld_bf16x8(Kc + key0 + (size_t)(16 * mb + row) * rowstride + 32 * ks +
+                                       8 * grp);
+        // Z^T = K_c Q^T and the softmax over the chunk's keys, scaled by the chunk weight
+        f32x4_t z[MB];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) z[mb] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) z[mb] = mfma16(kf[ks][mb], qB[ks], z[mb]);
+        float m = -INFINITY;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
+        const float msl = col_max(m) * sl2;
+        float ssum = 0.f;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
+                ssum += z[mb][i];
+            }
+        const float scale = wi * __builtin_amdgcn_rcpf(col_sum(ssum));
+        // O^T += V^T P^T, once the copies have landed
+        wait_loads_le<0>();
+#pragma unroll
+        for (int ks2 = 0; ks2 < KS2; ++ks2) {
+            const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
+#pragma unroll
+            for (int db = 0; db < 8; ++db) {
+                const __bf16* pv = stage + toff[db] + 32 * ks2 * DD;
+                acc[db] = mfma16(cat(ld_tr16(pv), ld_tr16(pv + 16 * DD)), pb, acc[db]);
+            }
+        }
+        // the stage is refilled by the next slot's copies: its reads must have returned
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
+    __syncthreads();
+    float* red = reinterpret_cast<float*>(&vst[0][0]);
+    if (row < kAttH) {
+#pragma unroll
+        for (int db = 0; db < 8; ++db)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                red[(wave * kAttH + row) * DD + 16 * db + 4 * grp + i] = acc[db][i];
+    }
+    __syncthreads();
+    for (int x = tid; x < kAttH * DD; x += NT) {
+        float sum = 0.f;
+#pragma unroll
+        for (int w2 = 0; w2 < NWV; ++w2) sum += red[w2 * kAttH * DD + x];
+        o[((size_t)b * dm.H + (size_t)g * kAttH) * DD + x] = f2bf(sum);
+    }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void decode_combine(Dims dm,
                                                       const int32_t* __restrict__ cache_len,
@@ -285,6 +617,14 @@ __global__ __launch_bounds__(256) void decode_combine(Dims dm,
         for (int i = 0; i < n; ++i) s += part[(((size_t)bg * k + i) * h) * D + x];
         o[((size_t)b * dm.H + (size_t)g * h) * D + x] = from_f32<T>(s);
     }
+}
+
+// The MFMA path of stages 2 and 3 applies to bf16 inputs with d = 128, 8 heads per group
+// and chunks of 64 keys.
+template <typename T, int D>
+bool decode_mfma_shape(const Dims& dm) {
+    return sizeof(T) == 2 && D == kAttD && dm.h == kAttH && dm.S == kAttS && dm.k <= KMAX &&
+           !getenv("HSA_FORCE_GENERIC");
 }
 
 struct DecodeWs {
@@ -316,6 +656,13 @@ void launch_tkd(const Dims& dm, const void* q, const void* Kc, const void* Vc, c
         hipLaunchKernelGGL((decode_scan<T, Tk, D>), dim3(nslices, dm.B), dim3(kScanThreads), 0,
                            st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc,
                            nslices);
+    }
+    if (decode_mfma_shape<T, D>(dm)) {
+        HSA_TIMED("decode_attend_mfma", st);
+        hipLaunchKernelGGL(decode_attend_mfma, dim3(dm.B * dm.G), dim3(kAttWaves * 64), 0, st,
+                           dm, (const __bf16*)q, (const __bf16*)Kc, (const __bf16*)Vc,
+                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w);
+        return;
     }
     {
         HSA_TIMED("decode_finish", st);

@@ -17,7 +17,8 @@ pytestmark = pytest.mark.gpu
 Shape = hsa_synth.HsaShape
 
 CASES = {
-    # name: (shape, seed, kind)
+    # name: (shape, seed, kind[, per-chunk key offset scale mu_std; default 0.5, 0 for
+    # "lowrank"])
     "tiny_f32": (Shape(1, 1024, 4, 1, 64, 64, 4, "f32"), 1, "iid"),
     "L4K_like_bf16": (Shape(2, 1024, 16, 2, 128, 64, 8, "bf16"), 2, "iid"),
     "long_like_bf16": (Shape(1, 2048, 16, 2, 128, 64, 8, "bf16"), 3, "long"),
@@ -31,6 +32,9 @@ CASES = {
     "wide_k16_bf16": (Shape(1, 2304, 32, 4, 128, 128, 16, "bf16"), 17, "lowrank"),
     "k24_bf16": (Shape(1, 2048, 16, 2, 128, 32, 24, "bf16"), 18, "iid"),
     "k20_d64_f32": (Shape(1, 1500, 4, 2, 64, 32, 20, "f32"), 19, "iid"),
+    # keys dominated by their chunk's offset (about 23 times the per-key spread): dQ is a
+    # strongly cancelling sum over each chunk's keys
+    "key_offset_bf16": (Shape(1, 1024, 16, 2, 128, 64, 8, "bf16"), 21, "iid", 2.0),
 }
 
 _cache = {}
@@ -38,8 +42,9 @@ _cache = {}
 
 def case(name):
     if name not in _cache:
-        shape, seed, kind = CASES[name]
-        inp, stats = make_case(shape, seed, kind=kind, mu_std=0.0 if kind == "lowrank" else 0.5)
+        shape, seed, kind, *rest = CASES[name]
+        mu_std = rest[0] if rest else (0.0 if kind == "lowrank" else 0.5)
+        inp, stats = make_case(shape, seed, kind=kind, mu_std=mu_std)
         ref = oracle_reference(inp, shape)
         dev = {n: to_dev(v, shape) for n, v in inp.items()}
         _cache[name] = (shape, inp, ref, dev)
@@ -193,6 +198,28 @@ def test_decode(hsa_gpu, dtype, kbar_dtype):
             p = inp["planted"][b, g].item()
             if p < lens[b] // 64:          # the planted chunk is a candidate: it must win
                 assert p in idx[b, g].tolist()
+
+
+@pytest.mark.parametrize("k", [3, 20])
+def test_decode_many_slots(hsa_gpu, k):
+    """k above the 8 waves of the attention stage (a wave attends several chunks in turn)
+    and caches with fewer complete chunks than k."""
+    shape = Shape(2, 4096, 16, 2, 128, 64, k, "bf16")
+    banner("decode_k%d" % k, "hsa_decode")
+    inp = hsa_synth.make_decode_inputs(shape, 23, device="cuda")
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
+    lens = [64 * 5 + 7, 4096]
+    cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    Kbar = torch.from_numpy(oracle.landmarks(Kc, 64).astype(np.float32)).cuda()
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, k, cache_len=cache_len)
+    torch.cuda.synchronize()
+    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, 64, k)
+    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar, lens, 64, k)[0]
+    gi = idx.cpu().numpy()
+    assert np.array_equal(gi[rgap >= 1e-3], ridx[rgap >= 1e-3])
+    assert np.all(gi[0, :, 5:] == -1)                # 5 complete chunks in sequence 0
+    assert np.max(np.abs(w.cpu().numpy() - rw)) <= W_ATOL
+    assert_close("o", shape, o, ro, o_abs=ro_abs)
 
 
 def test_decode_matches_forward_row(hsa_gpu):
