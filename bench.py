@@ -7,9 +7,13 @@ Inputs are resident in HBM before the timed region.  The main line is the 4K-con
 fwd+bwd workload (B 8, L 4096, H 16 / G 2, d 128, S 64, k 8, bf16); the 64K-context
 fwd+bwd and the 1M-token decode step are reported under "also".
 
-Kernel durations come from HIP events recorded by the library around each of its launches
-on the launch stream (hsa_attn_timing_enable), inside the timed region.  The fp64 oracle
-is timed on the host cores on a bounded sample (cpu_baseline).
+Kernel durations come from HIP events recorded by the library around its launches on the
+launch stream (hsa_attn_timing_enable / hsa_attn_timing_select).  The last warm-up step
+brackets every kernel, which gives the per-kernel breakdown and the dominant kernel; the
+timed steps bracket only that kernel (its roofline entry), so the other launches stay back
+to back and the step time carries the cost of one event pair per step.  The decode step is
+timed with no events; its per-kernel figures come from its warm-up.  The fp64 oracle is
+timed on the host cores on a bounded sample (cpu_baseline).
 
 Prints one JSON line.  `--gpus N` with N > 1 exits: this operator runs on one GPU.
 """
@@ -100,10 +104,22 @@ def time_training(sh, dev, steps, warmup, torch, hsa):
         hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f)
         hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b)
 
-    for _ in range(warmup):
+    # Untimed warm-up; its last step brackets every kernel (the per-kernel breakdown and
+    # the dominant kernel).  The timed steps bracket only the dominant kernel: an event pair
+    # costs queue time between launches, which would otherwise count in the step time.
+    hsa.timing_enable(False)
+    hsa.timing_select(None)
+    for i in range(warmup):
+        if i == warmup - 1:
+            torch.cuda.synchronize()
+            hsa.timing_collect()               # drop anything recorded before
+            hsa.timing_enable(True)
         step()
     torch.cuda.synchronize()
-    hsa.timing_collect()                       # drop anything recorded before
+    hsa.timing_enable(False)
+    breakdown = hsa.timing_collect() if warmup else {}
+    dominant = max(breakdown.items(), key=lambda kv: kv[1][1])[0] if breakdown else None
+    hsa.timing_select(dominant)                # None: every kernel
     hsa.timing_enable(True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -113,9 +129,10 @@ def time_training(sh, dev, steps, warmup, torch, hsa):
     e1.record()
     torch.cuda.synchronize()
     hsa.timing_enable(False)
+    hsa.timing_select(None)
     kern = hsa.timing_collect()
     ms = e0.elapsed_time(e1) / steps
-    return ms, kern
+    return ms, kern, breakdown or kern
 
 
 def source_digest():
@@ -178,19 +195,24 @@ def bench_decode(steps, warmup, torch, hsa):
     o = torch.empty_like(q)
     idx = torch.empty((sh.B, sh.G, sh.k), dtype=torch.int32, device="cuda")
     w = torch.empty((sh.B, sh.G, sh.k), dtype=torch.float32, device="cuda")
-    for _ in range(warmup):
+    # warm-up (its second half with every kernel bracketed: the per-kernel figures), then
+    # timed steps with no events between the launches
+    hsa.timing_select(None)
+    for i in range(warmup):
+        if i == warmup // 2:
+            torch.cuda.synchronize()
+            hsa.timing_collect()
+            hsa.timing_enable(True)
         hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
     torch.cuda.synchronize()
-    hsa.timing_collect()
-    hsa.timing_enable(True)
+    hsa.timing_enable(False)
+    kern = hsa.timing_collect()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(steps):
         hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
     e1.record()
     torch.cuda.synchronize()
-    hsa.timing_enable(False)
-    kern = hsa.timing_collect()
     us = e0.elapsed_time(e1) / steps * 1e3
     planted_ok = all(int(inp["planted"][b, g]) in idx[b, g].tolist()
                      for b in range(sh.B) for g in range(sh.G))
@@ -202,7 +224,8 @@ def bench_decode(steps, warmup, torch, hsa):
                        " H16/G2 d128 k8, bf16 landmark cache",
            "us_per_step": round(us, 3), "us_per_sequence_token": round(us / sh.B, 3),
            "tokens_per_s": round(sh.B / (us * 1e-6), 1), "planted_chunk_selected": planted_ok,
-           "kernels_avg_us": {n: round(t / c * 1e3, 3) for n, (c, t) in kern.items()}}
+           "kernels_avg_us": {n: round(t / c * 1e3, 3) for n, (c, t) in kern.items()},
+           "kernels_timed_in": "second half of the warm-up (event pairs around each launch)"}
     if scan:
         avg = scan[1] / scan[0]
         gbs = stream_bytes / (avg * 1e-3) / 1e9
@@ -340,7 +363,7 @@ def main():
     name = "L4K_bf16"
     sh, inp, dev, gen_s = make_training(name, torch)
     print("[bench] %s inputs ready (%.1f s)" % (name, gen_s), file=sys.stderr, flush=True)
-    ms, kern = time_training(sh, dev, args.steps, args.warmup, torch, hsa)
+    ms, kern, brk = time_training(sh, dev, args.steps, args.warmup, torch, hsa)
     pairs = valid_pairs(sh.B, sh.L, sh.G, sh.S, sh.k)
     tokens = sh.B * sh.L
     res = {
@@ -352,7 +375,9 @@ def main():
                    "batch": sh.B, "seq_len": sh.L, "q_heads": sh.H, "kv_heads": sh.G,
                    "head_dim": sh.d, "chunk": sh.S, "topk": sh.k},
         "roofline": roofline_of(kern, sh, pairs, name),
-        "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern.items()},
+        "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk.items()},
+        "kernels_timed_in": ("last warm-up step (event pairs around each launch); the timed "
+                             "steps bracket only the roofline kernel"),
     }
     print("[bench] %s: %.3f ms/step" % (name, ms), file=sys.stderr, flush=True)
     if not args.no_extra:
@@ -360,17 +385,17 @@ def main():
         torch.cuda.empty_cache()
         name3 = "L64K_bf16"
         sh3, _, dev3, _ = make_training(name3, torch)
-        ms3, kern3 = time_training(sh3, dev3, max(2, args.steps // 2), 1, torch, hsa)
+        ms3, kern3, brk3 = time_training(sh3, dev3, max(2, args.steps // 2), 2, torch, hsa)
         pairs3 = valid_pairs(sh3.B, sh3.L, sh3.G, sh3.S, sh3.k)
         res["also"] = {"L64K_bf16": {
             "workload": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
             "tokens_per_s": round(sh3.B * sh3.L / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 4),
             "roofline": roofline_of(kern3, sh3, pairs3, name3),
-            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in kern3.items()}}}
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk3.items()}}}
         print("[bench] %s: %.3f ms/step" % (name3, ms3), file=sys.stderr, flush=True)
         del dev3
         torch.cuda.empty_cache()
-        res["also"]["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 5, torch, hsa)
+        res["also"]["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 10, torch, hsa)
         print("[bench] decode: %.2f us/step" % res["also"]["decode_1M_bf16"]["us_per_step"],
               file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:

@@ -143,6 +143,12 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
  * bracketed by two HIP events recorded on its stream.  Off by default. */
 hsa_attn_status_t hsa_attn_timing_enable(int on);
 
+/* Restricts the timing to the kernels named `name` (the names hsa_attn_timing_collect
+ * reports); NULL or "" times every kernel again.  The string is copied.  Event pairs cost
+ * some microseconds of queue time between launches, so timing one kernel keeps the others'
+ * launches back to back. */
+hsa_attn_status_t hsa_attn_timing_select(const char* name);
+
 /* Waits for the recorded events and accumulates, per kernel name, the launches and total
  * milliseconds since the last delivery.  If len is at least the returned length, writes
  * one line per kernel, "name launches total_ms\n", NUL-terminated, into buf and starts a

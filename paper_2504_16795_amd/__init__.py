@@ -6,11 +6,11 @@ package is its thin Python binding.  Importing the package does not load the lib
 """
 from .binding import (HsaError, HsaParams, hsa_backward, hsa_decode, hsa_forward,
                       hsa_landmarks, hsa_select_topk, load, make_params, workspace_size,
-                      timing_enable, timing_collect,
+                      timing_enable, timing_select, timing_collect,
                       HSA_DTYPE_BF16, HSA_DTYPE_F32, HSA_OP_BACKWARD, HSA_OP_DECODE,
                       HSA_OP_FORWARD, HSA_OP_LANDMARKS, HSA_OP_SELECT, EXPORTED, LIB_PATH)
 
 __all__ = ["HsaError", "HsaParams", "hsa_backward", "hsa_decode", "hsa_forward",
            "hsa_landmarks", "hsa_select_topk", "load", "make_params", "workspace_size",
-           "timing_enable", "timing_collect",
+           "timing_enable", "timing_select", "timing_collect",
            "EXPORTED", "LIB_PATH"]

@@ -40,7 +40,7 @@ class HsaError(RuntimeError):
 
 EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
             "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
-            "hsa_attn_timing_enable", "hsa_attn_timing_collect")
+            "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect")
 
 
 def load(path: Optional[str] = None) -> ctypes.CDLL:
@@ -69,6 +69,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_attn_last_error.restype = ctypes.c_char_p
     lib.hsa_attn_timing_enable.argtypes = [ctypes.c_int]
     lib.hsa_attn_timing_enable.restype = I32
+    lib.hsa_attn_timing_select.argtypes = [ctypes.c_char_p]
+    lib.hsa_attn_timing_select.restype = I32
     lib.hsa_attn_timing_collect.argtypes = [ctypes.c_char_p, SZ]
     lib.hsa_attn_timing_collect.restype = ctypes.c_int
     if path is None:
@@ -238,6 +240,11 @@ def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
 def timing_enable(on: bool = True) -> None:
     """Bracket every kernel launch of the library with HIP events on its stream."""
     load().hsa_attn_timing_enable(1 if on else 0)
+
+
+def timing_select(name: Optional[str] = None) -> None:
+    """Time only the kernels called `name` (None: every kernel)."""
+    load().hsa_attn_timing_select(name.encode() if name else None)
 
 
 def timing_collect() -> dict:

@@ -423,6 +423,7 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
             int pos = n0 + incl - cnt;
             uint32_t x = word;
             while (x) {
+                sm.lslot[pos] = 0;
                 sm.list[pos++] = wi * 32 + (__ffs(x) - 1);
                 x &= x - 1;
             }
@@ -432,16 +433,20 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
         if (!last_round) last_round = wb + 64 >= nwords;
         __syncthreads();
         const int nl = sm.nlist;
-        // per-token slot, weight and ds of the batch, resolved in parallel
+        // per-token slot, weight and ds of the batch.  Threads take consecutive (token,
+        // slot) entries, so every idx load is independent of the others and coalesced; the
+        // slot holding c (a token's valid entries are distinct, so one matches) is noted,
+        // then each token's w and ds are loaded.
+        for (int e = tid; e < nl * k; e += NT) {
+            const int li = e / k, s2 = e - li * k;
+            const size_t so = (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k;
+            if (idx[so + s2] == c) sm.lslot[li] = (uint8_t)s2;
+        }
+        __syncthreads();
         for (int li = tid; li < nl; li += NT) {
-            const int t = sm.list[li];
-            const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
-            int slot = 0;
-            for (int s2 = k - 1; s2 >= 0; --s2)
-                if (idx[so + s2] == c) slot = s2;
-            sm.lslot[li] = (uint8_t)slot;
-            sm.lw[li] = w[so + slot];
-            sm.lds[li] = ds[so + slot];
+            const size_t so = (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li];
+            sm.lw[li] = w[so];
+            sm.lds[li] = ds[so];
         }
         __syncthreads();
         const int ngroups = last_round ? (nl + 3) / 4 : nl / 4;

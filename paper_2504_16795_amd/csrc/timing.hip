@@ -1,5 +1,6 @@
-// Optional per-kernel timing: while enabled, every kernel launch of the library is bracketed
-// by a pair of HIP events recorded on the launch stream.  Collecting waits for the recorded
+// Optional per-kernel timing: while enabled, every kernel launch of the library (or only
+// those of one selected kernel) is bracketed by a pair of HIP events recorded on the launch
+// stream.  Collecting waits for the recorded
 // events and accumulates, per kernel name, the launch count and the total milliseconds.
 // Disabled (the default), a launch costs one relaxed atomic load.
 #include <atomic>
@@ -22,7 +23,9 @@ struct Rec {
 };
 
 std::atomic<bool> g_on{false};
+std::atomic<bool> g_filtered{false};
 std::mutex g_mu;
+std::string g_only;                                       // timed kernel when filtered
 std::vector<Rec> g_pending;
 std::vector<hipEvent_t> g_free;
 std::map<std::string, std::pair<long, double>> g_acc;   // name -> (launches, total ms)
@@ -43,6 +46,7 @@ hipEvent_t take_event() {
 KernelTimer::KernelTimer(const char* name, hipStream_t st) : name_(name), st_(st) {
     if (!g_on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_mu);
+    if (g_filtered.load(std::memory_order_relaxed) && g_only != name) return;
     a_ = take_event();
     b_ = take_event();
     if (a_ && b_) (void)hipEventRecord(a_, st_);
@@ -61,6 +65,13 @@ extern "C" {
 
 hsa_attn_status_t hsa_attn_timing_enable(int on) {
     hsa::g_on.store(on != 0);
+    return HSA_ATTN_OK;
+}
+
+hsa_attn_status_t hsa_attn_timing_select(const char* name) {
+    std::lock_guard<std::mutex> lk(hsa::g_mu);
+    hsa::g_only = name ? name : "";
+    hsa::g_filtered.store(!hsa::g_only.empty());
     return HSA_ATTN_OK;
 }
 
