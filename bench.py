@@ -309,12 +309,16 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
     cname = max(copy, key=lambda n: max(fetch[n]))
     f_fac = CALIB_BYTES / max(fetch[cname])
     w_fac = CALIB_BYTES / max(write[cname])
-    names = {"landmarks_kernel", "select_kernel", "forward_mfma", "bwd_q_mfma", "bwd_kv_mfma",
-             "bitmap_build", "fill_zero_u32", "forward_generic", "bwd_q_generic",
-             "bwd_kv_generic"}
+    # function-name fragment -> the name the library's timing reports
+    names = {"landmarks_kernel": "landmarks_kernel", "select_tiles_kernel": "select_kernel",
+             "select_split_kernel": "select_kernel", "select_kernel": "select_kernel",
+             "forward_mfma": "forward_mfma", "bwd_q_mfma": "bwd_q_mfma",
+             "bwd_kv_mfma": "bwd_kv_mfma", "bitmap_build": "bitmap_build",
+             "fill_zero_u32": "fill_zero_u32", "forward_generic": "forward_generic",
+             "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic"}
     kernels = {}
     for full in fetch:
-        short = next((n for n in names if n in full), None)
+        short = next((v for n, v in names.items() if n in full), None)
         if short is None or full not in write:
             continue
         fb = sum(fetch[full]) / len(fetch[full]) * f_fac
