@@ -381,9 +381,14 @@ hipError_t launch_t(const Dims& dm, const void* Q, const float* Kbar, int32_t* i
 
 }  // namespace
 
+bool select_mfma_supported(const Dims& dm, bool in_bf16);
+hipError_t launch_select_mfma(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx,
+                              float* w, hipStream_t st);
+
 hipError_t launch_select(const Dims& dm, bool in_bf16, const void* Q, const float* Kbar,
                          int32_t* idx, float* w, hipStream_t st) {
     if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    if (select_mfma_supported(dm, in_bf16)) return launch_select_mfma(dm, Q, Kbar, idx, w, st);
     return in_bf16 ? launch_t<bf16>(dm, Q, Kbar, idx, w, st)
                    : launch_t<float>(dm, Q, Kbar, idx, w, st);
 }
