@@ -312,6 +312,7 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
     # function-name fragment -> the name the library's timing reports
     names = {"landmarks_kernel": "landmarks_kernel", "select_tiles_kernel": "select_kernel",
              "select_split_kernel": "select_kernel", "select_kernel": "select_kernel",
+             "select_mfma": "select_kernel",
              "forward_mfma": "forward_mfma", "bwd_q_mfma": "bwd_q_mfma",
              "bwd_kv_mfma": "bwd_kv_mfma", "bitmap_build": "bitmap_build",
              "fill_zero_u32": "fill_zero_u32", "forward_generic": "forward_generic",
