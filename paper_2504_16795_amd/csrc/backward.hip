@@ -21,6 +21,12 @@ namespace hsa {
 
 bool backward_mfma_supported(const Dims& dm, bool in_bf16);
 size_t backward_mfma_workspace(const Dims& dm);
+bool backward_fused_supported(const Dims& dm, bool in_bf16);
+size_t backward_fused_workspace(const Dims& dm);
+hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, const void* V,
+                                 const float* Kbar, const int32_t* idx, const float* w,
+                                 const void* dO, void* dQ, void* dK, void* dV, void* ws,
+                                 hipStream_t st);
 hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
                                 const float* Kbar, const int32_t* idx, const float* w,
                                 const void* dO, void* dQ, void* dK, void* dV, void* ws,
@@ -404,7 +410,9 @@ size_t backward_generic_workspace(const Dims& dm) {
 size_t backward_workspace(const Dims& dm) {
     const size_t a = backward_generic_workspace(dm);
     const size_t b = backward_mfma_workspace(dm);
-    return a > b ? a : b;
+    const size_t f = backward_fused_workspace(dm);
+    const size_t ab = a > b ? a : b;
+    return ab > f ? ab : f;
 }
 
 hipError_t launch_backward_generic(const Dims& dm, bool in_bf16, const void* Q, const void* K,
@@ -421,6 +429,8 @@ hipError_t launch_backward(const Dims& dm, bool in_bf16, const void* Q, const vo
                            const void* dO, void* dQ, void* dK, void* dV, void* ws,
                            hipStream_t st) {
     if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    if (backward_fused_supported(dm, in_bf16))
+        return launch_backward_fused(dm, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);
     if (backward_mfma_supported(dm, in_bf16))
         return launch_backward_mfma(dm, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);
     return launch_backward_generic(dm, in_bf16, Q, K, V, Kbar, idx, w, dO, dQ, dK, dV, ws, st);

@@ -1,0 +1,949 @@
+// Backward of hierarchical sparse attention in one chunk-major pass over the selected
+// (token, chunk) pairs (Sec. 3.1.2: gradients of the chunk attention, of the chunk weights
+// and, through them, of the landmark scores), for bf16 inputs with h = 8 query heads per KV
+// head, d = 128 and S = 64.
+//
+// Work is counted in groups of 4 consecutive tokens of a chunk's selecting tokens (32 rows =
+// 4 tokens x 8 heads).  A chunk's tokens come from the selection bitmap in increasing order.
+// The groups of all (b, g, chunk) rows are laid end to end (row-major: slices, then chunks)
+// and split into kStreamWGs equal ranges, one per workgroup, so a popular chunk (selected by
+// thousands of tokens) is shared by several workgroups instead of setting the kernel time.
+// A workgroup writes the key-side results of the chunks it covers entirely; for the first
+// and last chunk of its range, when shared, it writes fp32 partial sums that bwd_finish adds
+// in workgroup order.
+//
+// bwd_fused_mfma: 4 waves; wave w owns keys 16 w .. 16 w + 15 of the current chunk (K_sub,
+// V_sub operands in registers, dK_sub, dV_sub [16 x 128] fp32 accumulators).  Per group:
+//     Z [32 x 16] = Q_rows K_sub^T,  dP = dO_rows V_sub^T                 (MFMA)
+//     each wave reduces its 16 keys per row (max m_w of the scaled logits, sum of
+//     exp(z - m_w), sum of exp(z - m_w) dP); the four waves' values are exchanged through
+//     LDS and combined into P = softmax over the chunk's 64 keys and D = sum_keys P dP
+//     (= dO_row . O_{row,c})
+//     dZ = W P (dP - D), W the token's weight for c (summed over slots repeating c)
+//     dV_sub += (W P)^T dO_rows,  dK_sub += dZ^T Q_rows                   (MFMA, hi/lo)
+//     dZ^T [64 keys x 32 rows] is staged in LDS; wave w forms the partial
+//     dQ^T [d 32 w .. 32 w + 31 x 32 rows] = K_c^T dZ^T                     (MFMA, hi/lo)
+//     and stores it (bf16) at the (token, slot, head) of the token's first slot holding c;
+//     dw_{t,c} = sum over the token's heads of D is stored beside it.
+// The partial dQ of a group is formed at the start of the next group's step, so a group
+// needs two workgroup barriers (its stage landed / the previous dZ^T complete, and the
+// statistics exchange).
+//
+// bwd_dq_reduce (token-major, one wave per (b, t, g)): ds_i = w_i (dw_i - sum_m w_m dw_m),
+// dQ = beta * (sum of the token's partials) + alpha * sum_i ds_i Kbar_{c_i}, and the token's
+// summed query q~ = sum_j q_j for the landmark term of dK.
+//
+// bwd_lmk_stream (same ranges): dKbar_c = alpha * sum_t ds_{t,c} q~_t, per chunk or partial.
+// bwd_finish (per chunk): dK = beta dK_raw + dKbar_c / S (Kbar_c is the mean of the chunk's
+// keys), dV; zeros for the trailing partial chunk.
+//
+// No atomics; every sum runs in a fixed order.
+#include <cstdlib>
+
+#include "chunk_lds.h"
+
+namespace hsa {
+
+hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm,
+                                   hipStream_t st);
+
+namespace {
+
+constexpr int D = 128;
+constexpr int HG = 8;
+constexpr int CS = 64;              // chunk size of this path
+constexpr int NW = 4;               // waves, 16 keys each
+constexpr int NT = NW * 64;
+constexpr int KMAX = 32;
+constexpr int FNST = 3;             // LDS stages of the group ring
+constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied per wave and group
+constexpr int FLIST = 1024;         // tokens listed at once (a multiple of 4)
+constexpr int kStoresPerStep = 5;   // global stores per lane of one dq step (4 partial, 1 dw)
+constexpr int kStreamWGs = 512;     // workgroups of the stream partition: two per CU
+
+// target of the stores of padding rows (a group's missing tokens), so that every wave issues
+// the same number of stores per group: 8 rows of partial dQ, then 64 floats
+constexpr size_t kTrashBytes = HG * D * 2 + 64 * 4;
+
+__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct FusedWs {
+    size_t bitmap, cnt, gstart, plan, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash, end;
+};
+__host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
+    FusedWs l;
+    const size_t nsel = (size_t)dm.B * dm.L * dm.G * dm.k;
+    const size_t nrow = (size_t)dm.B * dm.L * dm.G;
+    const size_t nwords = (size_t)((dm.L + 31) / 32);
+    const size_t R = (size_t)dm.B * dm.G * dm.C;
+    l.bitmap = 0;
+    l.cnt = align256(R * nwords * 4);
+    l.gstart = l.cnt + align256(R * 4);
+    l.plan = l.gstart + align256((R + 1) * 4);
+    l.part = l.plan + 256;
+    l.dkraw = l.part + align256(nsel * HG * D * 2);
+    l.dw = l.dkraw + align256(nrow * D * 4);
+    l.ds = l.dw + align256(nsel * 4);
+    l.qsum = l.ds + align256(nsel * 4);
+    l.pk = l.qsum + align256(nrow * D * 4);
+    l.pv = l.pk + (size_t)kStreamWGs * 2 * CS * D * 4;
+    l.pkb = l.pv + (size_t)kStreamWGs * 2 * CS * D * 4;
+    l.dkbar = l.pkb + (size_t)kStreamWGs * 2 * D * 4;
+    l.trash = l.dkbar + align256(R * D * 4);
+    l.end = l.trash + kTrashBytes;
+    return l;
+}
+
+struct FStage {
+    __bf16 q[32 * D];               // Q rows of a group (row 8 token + head), swizzled
+    __bf16 g[32 * D];               // dO rows
+};
+
+struct SmemF {
+    FStage st[FNST];                // stage 0 holds the chunk's K rows while K^T is read
+    __bf16 dzt[2][CS * 32];         // dZ^T of a group, hi and lo parts: [key][row], see zpos
+    float stat[NW][3][32];          // per wave and row: m_w, sum exp, sum exp * dP
+    float fac[NW][2][32];           // per wave and row: P scale of the wave's keys, D
+    int list[FLIST];                // token; then its first Q / dO row, (b L + t) H + g h
+    int lsel[FLIST];                // (token, first slot holding c): ((b L + t) G + g) k + s
+    float lw[FLIST];                // the token's total weight for c
+    int wtot[NW];
+};
+
+// dZ^T tile: 64 keys x 32 rows of bf16, 64 bytes per key in 8-byte units of 4 rows; unit u
+// of key j sits at position u ^ zsw(j).  Both the C-layout writes (unit 4 rb + lane group of
+// 16 consecutive keys per instruction) and the transposed reads (4 units of 8 consecutive
+// keys per 32-lane pass) then fall on distinct banks.
+__device__ __forceinline__ int zsw(int j) { return (((j >> 2) & 1) << 2) | (((j >> 3) & 1) << 1); }
+__device__ __forceinline__ int zpos(int j, int u) { return j * 32 + 4 * (u ^ zsw(j)); }
+
+// maximum over the 16 lanes of a row, on the order-preserving integer image of the floats
+// (finite inputs): each step is one integer max with a DPP operand
+__device__ __forceinline__ float row16_max(float x) {
+    int v = __float_as_int(x);
+    v ^= (v >> 31) & 0x7fffffff;
+    v = max(v, dpp_mov<kDppXor1>(v));
+    v = max(v, dpp_mov<kDppXor2>(v));
+    v = max(v, dpp_mov<kDppHalfMirror>(v));
+    v = max(v, dpp_mov<kDppMirror>(v));
+    return __int_as_float(v ^ ((v >> 31) & 0x7fffffff));
+}
+
+// LDS writes of this wave complete (before a barrier that publishes them)
+__device__ __forceinline__ void lds_wait() {
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+}
+
+// Tokens at positions [p0, p1) of a chunk's ascending token list (the set bits of bitmap
+// words wbeg .. nwords - 1 of its row) into list[0 .. p1 - p0).  Whole workgroup; the words
+// are counted 256 at a time with a workgroup prefix sum, stopping once p1 is reached.
+__device__ __forceinline__ void collect_tokens(const uint32_t* __restrict__ bmrow, int wbeg,
+                                               int nwords, int p0, int p1, int* list,
+                                               int* wtot, int tid) {
+    const int lane = tid & 63, wave = tid >> 6;
+    int base = 0;
+    for (int wb = wbeg; wb < nwords; wb += NT) {
+        const int wi = wb + tid;
+        const uint32_t word = wi < nwords ? bmrow[wi] : 0u;
+        const int cnt = __popc(word);
+        int incl = cnt;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += v;
+        }
+        if (lane == 63) wtot[wave] = incl;
+        __syncthreads();
+        int before = 0, tot = 0;
+#pragma unroll
+        for (int w2 = 0; w2 < NW; ++w2) {
+            const int v = wtot[w2];
+            before += (w2 < wave) ? v : 0;
+            tot += v;
+        }
+        int pos = base + before + incl - cnt;
+        if (pos < p1 && pos + cnt > p0) {
+            uint32_t x = word;
+            while (x) {
+                if (pos >= p0 && pos < p1) list[pos - p0] = wi * 32 + (__ffs(x) - 1);
+                ++pos;
+                x &= x - 1;
+            }
+        }
+        base += tot;
+        __syncthreads();                // wtot is rewritten by the next block
+        if (base >= p1) break;
+    }
+}
+
+// The row (b, g, chunk) holding global group gpos: the last r with gstart[r] <= gpos
+// (gstart is non-decreasing, gstart[0] = 0 <= gpos < gstart[R]).
+__device__ __forceinline__ int find_row(const int* __restrict__ gstart, int R, int gpos) {
+    int lo = 0, hi = R;                 // gstart[lo] <= gpos < gstart[hi]
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (gstart[mid] <= gpos) lo = mid;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// tokens per bitmap row (one wave per row)
+__global__ __launch_bounds__(256) void bwd_rowcount(const uint32_t* __restrict__ bm, int R,
+                                                    int nwords, int C, int S,
+                                                    int* __restrict__ cnt) {
+    const int lane = threadIdx.x & 63;
+    const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (r >= R) return;
+    const int c = r % C;
+    const uint32_t* row = bm + (size_t)r * nwords;
+    int n = 0;
+    for (int wi = ((c + 1) * S >> 5) + lane; wi < nwords; wi += 64) n += __popc(row[wi]);
+    n = (int)group_sum<64>((float)n);   // exact: counts stay far below 2^24
+    if (lane == 0) cnt[r] = n;
+}
+
+// group prefix over the rows (one workgroup): gstart[r] = sum_{r' < r} ceil(cnt[r'] / 4);
+// plan = {total groups, groups per workgroup}
+__global__ __launch_bounds__(1024) void bwd_plan(const int* __restrict__ cnt, int R, int nwg,
+                                                 int* __restrict__ gstart, int* __restrict__ plan) {
+    __shared__ int wt[16];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int carry = 0;
+    for (int r0 = 0; r0 < R; r0 += 1024) {
+        const int r = r0 + tid;
+        const int ng = r < R ? (cnt[r] + 3) >> 2 : 0;
+        int incl = ng;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int v = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += v;
+        }
+        if (lane == 63) wt[wave] = incl;
+        __syncthreads();
+        int before = 0, tot = 0;
+        for (int w2 = 0; w2 < 16; ++w2) {
+            before += (w2 < wave) ? wt[w2] : 0;
+            tot += wt[w2];
+        }
+        if (r < R) gstart[r] = carry + before + incl - ng;
+        carry += tot;
+        __syncthreads();
+    }
+    if (tid == 0) {
+        gstart[R] = carry;
+        plan[0] = carry;
+        plan[1] = carry > 0 ? (carry + nwg - 1) / nwg : 1;
+    }
+}
+
+__global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
+    Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
+    const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const __bf16* __restrict__ dO, const uint32_t* __restrict__ bm, int nwords,
+    const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
+    __bf16* __restrict__ part, float* __restrict__ dwc, float* __restrict__ dkraw,
+    float* __restrict__ pk, float* __restrict__ pv, char* __restrict__ trash,
+    __bf16* __restrict__ dV) {
+    __shared__ SmemF sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = lane & 15, grp = lane >> 4;
+    // consecutive ranges (the chunks of one slice) run on one XCD, so a token's Q / dO rows,
+    // read once per chunk it selected, are shared through that XCD's L2
+    const int lid = xcd_logical_id(kStreamWGs);
+    if (lid < 0) return;
+    const int R = dm.B * dm.G * dm.C;
+    const int total = plan[0], T = plan[1];
+    const int g0 = lid * T, g1 = min(g0 + T, total);
+    if (g0 >= g1) return;
+    const int k = dm.k;
+    const size_t rowstride = (size_t)dm.G * D;
+    const float beta = dm.beta;
+    const float sl2 = beta * 1.44269504088896341f;
+
+    // LDS offsets of the chunk-swizzled tiles (see chunk_lds.h), from per-lane bases:
+    //   row reads, d step ks:        kb0 + 32 (ks ^ ks_x)       (+ 2048 per 16-row block)
+    //   transposed reads, block db:  tb0 + 16 (db ^ tr_x)       (+ 16 rows: + 16 D)
+    const int swr = swz(row);
+    const int kb0 = row * D + 8 * (grp ^ (swr & 3)), ks_x = swr >> 2;
+    const int trr = 4 * grp + (row >> 2);
+    const int tb0 = trr * D + 8 * (((row & 3) >> 1) ^ ((trr >> 3) & 1)) + 4 * (row & 1);
+    const int tr_x = trr & 7;
+    auto koff = [&](int ks) __attribute__((always_inline)) { return kb0 + 32 * (ks ^ ks_x); };
+    auto toff = [&](int db) __attribute__((always_inline)) { return tb0 + 16 * (db ^ tr_x); };
+    // transposed-read offsets of the dZ^T tile in the key order of the K^T fragments: lane
+    // (grp, p) loads key kb + (p >> 2), rows 16 rt + 4 (p & 3) .. +3, kb = 32 ks2 + 16 hf +
+    // 4 grp, at zpos(kb + (p >> 2), 4 rt + (p & 3)) = zb[rt] + 1024 ks2 + 512 hf (zsw of
+    // those keys depends on grp only)
+    int zb[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
+    __bf16* const tpart = reinterpret_cast<__bf16*>(trash);
+    float* const tdw = reinterpret_cast<float*>(trash + HG * D * 2);
+
+    for (int r = find_row(gstart, R, g0); r < R; ++r) {
+        const int rs = gstart[r], re = gstart[r + 1];
+        if (rs >= g1) break;
+        if (re == rs) continue;
+        const int j0 = max(g0, rs) - rs, j1 = min(g1, re) - rs;
+        const bool whole = (j0 == 0 && j1 == re - rs);
+        const int pslot = (rs <= g0) ? 0 : 1;     // first row of the range, or its last
+        const int c = r % dm.C;
+        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
+        const size_t cbase = ((size_t)b * dm.L + (size_t)c * CS) * rowstride + (size_t)g * D;
+        const int ntok = cntr[r];
+
+        // ---- the chunk's operands: K_sub^T, V_sub^T (B operands of Z, dP) and K^T (A
+        // operand of dQ^T: d = 32 wave + 16 dt + (lane & 15), keys of lane group grp in step
+        // ks2: 32 ks2 + 4 grp + (0..3) and 32 ks2 + 16 + 4 grp + (0..3))
+        __syncthreads();                          // the previous chunk's stages are read
+        bf16x8_t kB[4], vB[4];
+        const int key = 16 * wave + row;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks) {
+            kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+            vB[ks] = ld_bf16x8(V + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+        }
+        chunk_to_lds<CS, NW>(K + cbase, rowstride, sm.st[0].q, wave, lane);
+        wait_loads_le<0>();
+        __syncthreads();
+        bf16x8_t kT[2][2];
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+            for (int ks2 = 0; ks2 < 2; ++ks2) {
+                const __bf16* p = sm.st[0].q + toff(2 * wave + dt) + 32 * ks2 * D;
+                kT[dt][ks2] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
+            }
+        f32x4_t aK[8], aV[8];
+#pragma unroll
+        for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
+
+        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
+            FStage& st = sm.st[gi % FNST];
+#pragma unroll
+            for (int i = 0; i < BPW; ++i) {
+                const int blk = wave * BPW + i;
+                const int rr = blk * 4 + (lane >> 4);
+                int li = gi * 4 + (rr >> 3);
+                if (li >= nl) li = gi * 4;   // a missing token repeats the group's first (W = 0)
+                const size_t o = ((size_t)(uint32_t)(sm.list[li] + (rr & 7)) << 7) +
+                                 unit_pos(rr, lane & 15) * 8;
+                lds_copy16(Q + o, __builtin_amdgcn_readfirstlane(lds_address(st.q + blk * 512)));
+                lds_copy16(dO + o, __builtin_amdgcn_readfirstlane(lds_address(st.g + blk * 512)));
+            }
+        };
+
+        // partial dQ^T of group gj from the staged dZ^T (all waves' keys), stored per (token,
+        // slot, head): rows 16 rt + (lane & 15), d = 32 wave + 16 dt + 4 grp + (0..3); then
+        // the group's dw (wave 0, carried from its combine step).  Exactly kStoresPerStep
+        // stores per lane: rows of missing tokens go to the trash area.
+        auto dq_step = [&](int gj, int nl, float dtok) __attribute__((always_inline)) {
+            f32x4_t qa[2][2];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt) qa[dt][0] = qa[dt][1] = zero4();
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int ks2 = 0; ks2 < 2; ++ks2)
+#pragma unroll
+                    for (int hl = 0; hl < 2; ++hl) {
+                        const __bf16* zp = sm.dzt[hl] + zb[rt] + 1024 * ks2;
+                        const bf16x8_t bz = cat(ld_tr16(zp), ld_tr16(zp + 512));
+#pragma unroll
+                        for (int dt = 0; dt < 2; ++dt)
+                            qa[dt][rt] = mfma16(kT[dt][ks2], bz, qa[dt][rt]);
+                    }
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                const int li = gj * 4 + 2 * rt + (row >> 3);
+                const int so = li < nl ? sm.lsel[li] : -1;
+                __bf16* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
+                              (row & 7) * D + 32 * wave + 4 * grp;
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const bf16x4_t v4{f2bf(qa[dt][rt][0]), f2bf(qa[dt][rt][1]),
+                                      f2bf(qa[dt][rt][2]), f2bf(qa[dt][rt][3])};
+                    *reinterpret_cast<bf16x4_t*>(dst + 16 * dt) = v4;
+                }
+            }
+            {
+                const int li = gj * 4 + ((lane & 31) >> 3);
+                const int so = (wave == 0 && lane < 32 && (lane & 7) == 0 && li < nl)
+                                   ? sm.lsel[li] : -1;
+                float* dst = so >= 0 ? dwc + (uint32_t)so : tdw + lane;
+                *dst = dtok;
+            }
+        };
+
+        const uint32_t* bmrow = bm + (size_t)r * nwords;
+        const int wbeg = ((c + 1) * CS) >> 5;
+        const int tend = min(4 * j1, ntok);
+        for (int p0 = 4 * j0; p0 < tend; p0 += FLIST) {
+            const int p1 = min(p0 + FLIST, tend);
+            const int nl = p1 - p0;
+            __syncthreads();                      // the list of the previous batch is read
+            collect_tokens(bmrow, wbeg, nwords, p0, p1, sm.list, sm.wtot, tid);
+            // per listed token: its first slot holding c (a set bit means there is one) and
+            // its total weight for c.  All idx and w loads of a token are issued before use.
+            for (int li = tid; li < nl; li += NT) {
+                const int t = sm.list[li];
+                const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
+                int first = KMAX;
+                float wsum = 0.f;
+                for (int s0 = 0; s0 < k; s0 += 8) {
+                    int cc[8];
+                    float ww[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const bool in = s0 + j < k;
+                        cc[j] = in ? idx[so + s0 + j] : -1;
+                        ww[j] = in ? w[so + s0 + j] : 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (cc[j] == c) {
+                            first = min(first, s0 + j);
+                            wsum += ww[j];
+                        }
+                }
+                // -1: no slot holding c (not expected: the bitmap bit says there is one)
+                sm.lsel[li] = first < k ? (int)(so + first) : -1;
+                sm.lw[li] = first < k ? wsum : 0.f;
+                sm.list[li] = (int)(((size_t)b * dm.L + t) * dm.H + (size_t)g * HG);
+            }
+            __syncthreads();
+            const int ngroups = (nl + 3) / 4;
+#pragma unroll
+            for (int u = 0; u < FNST - 1; ++u)
+                if (u < ngroups) issue(u, nl);
+            float dtok_pend = 0.f;
+            for (int gi = 0; gi < ngroups; ++gi) {
+                // Group gi has landed once only the memory operations issued after its copies
+                // remain: the previous iteration's dq stores (when it ran one) and the next
+                // group's copies (when there is a next group).  Loads and stores complete in
+                // issue order.
+                const bool more = gi + 1 < ngroups, stored = gi >= 2;
+                if (more && stored) wait_loads_le<2 * BPW + kStoresPerStep>();
+                else if (more) wait_loads_le<2 * BPW>();
+                else if (stored) wait_loads_le<kStoresPerStep>();
+                else wait_loads_le<0>();
+                lds_wait();
+                barrier_keep_copies();   // stage gi landed, dZ^T of gi - 1 complete, stage gi - 1 free
+                if (gi > 0) dq_step(gi - 1, nl, dtok_pend);
+                if (gi + FNST - 1 < ngroups) issue(gi + FNST - 1, nl);
+                const FStage& st = sm.st[gi % FNST];
+
+                // ---- Z, dP for the wave's 16 keys (rows 16 rb + 4 grp + i, key 16 wave + row) --
+                f32x4_t z[2], dp[2];
+                z[0] = z[1] = dp[0] = dp[1] = zero4();
+    #pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+    #pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) {
+                        z[rb] = mfma16(ld_bf16x8(st.q + koff(ks) + rb * 2048), kB[ks], z[rb]);
+                        dp[rb] = mfma16(ld_bf16x8(st.g + koff(ks) + rb * 2048), vB[ks], dp[rb]);
+                    }
+                // ---- the wave's row statistics over its 16 keys, to LDS ------------------------
+                f32x4_t e[2];
+    #pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    f32x4_t sm_m, sm_l, sm_n;
+    #pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float zl = z[rb][i] * sl2;
+                        const float m = row16_max(zl);
+                        const float ev = fast_exp2(zl - m);
+                        e[rb][i] = ev;
+                        sm_m[i] = m;
+                        sm_l[i] = group_sum<16>(ev);
+                        sm_n[i] = group_sum<16>(ev * dp[rb][i]);
+                    }
+                    if (row == 0) {
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][0][16 * rb + 4 * grp]) = sm_m;
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][1][16 * rb + 4 * grp]) = sm_l;
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][2][16 * rb + 4 * grp]) = sm_n;
+                    }
+                }
+                lds_wait();
+                barrier_keep_copies();   // every wave's statistics of group gi written
+                // ---- combine: lane r (and r + 32) handles row r = lane & 31 --------------------
+                const int r32 = lane & 31;
+                float mv[NW], lv[NW], nv[NW];
+    #pragma unroll
+                for (int w2 = 0; w2 < NW; ++w2) {
+                    mv[w2] = sm.stat[w2][0][r32];
+                    lv[w2] = sm.stat[w2][1][r32];
+                    nv[w2] = sm.stat[w2][2][r32];
+                }
+                const float M = fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3]));
+                float lsum = 0.f, nsum = 0.f, aown = 0.f;
+    #pragma unroll
+                for (int w2 = 0; w2 < NW; ++w2) {
+                    const float a = fast_exp2(mv[w2] - M);
+                    lsum = fmaf(a, lv[w2], lsum);
+                    nsum = fmaf(a, nv[w2], nsum);
+                    aown = (w2 == wave) ? a : aown;
+                }
+                const float inv = __builtin_amdgcn_rcpf(lsum);
+                const float Drow = nsum * inv;
+                if (lane < 32) {
+                    sm.fac[wave][0][r32] = aown * inv;
+                    sm.fac[wave][1][r32] = Drow;
+                }
+                // dw of each token of the group: sum of D over its 8 heads (rows 8 tau .. 8 tau + 7),
+                // stored with the group's partial dQ
+                dtok_pend = group_sum<8>(Drow);
+                // back in the C layout (the wave's own LDS writes, read in order)
+                f32x4_t fv[2], dv[2], pw[2], dz[2];
+    #pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    fv[rb] = *reinterpret_cast<const f32x4_t*>(&sm.fac[wave][0][16 * rb + 4 * grp]);
+                    dv[rb] = *reinterpret_cast<const f32x4_t*>(&sm.fac[wave][1][16 * rb + 4 * grp]);
+                }
+    #pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    const int li = gi * 4 + 2 * rb + (grp >> 1);
+                    const float wt = li < nl ? sm.lw[li] : 0.f;
+    #pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float p = e[rb][i] * fv[rb][i];
+                        pw[rb][i] = wt * p;
+                        dz[rb][i] = wt * p * (dp[rb][i] - dv[rb][i]);
+                    }
+                }
+                // every product below accumulates over many rows (dV, dK) or cancels (dQ, since
+                // sum_keys dZ = 0): W P and dZ enter as bf16 hi/lo pairs
+                bf16x8_t pvh, pvl, dzh, dzl;
+                split8(pw[0], pw[1], pvh, pvl);
+                split8(dz[0], dz[1], dzh, dzl);
+                {
+                    // dZ^T to LDS: key 16 wave + row, rows 16 rb + 4 grp .. +3 = unit 4 rb + grp
+                    const int j = 16 * wave + row;
+                    *reinterpret_cast<bf16x4_t*>(sm.dzt[0] + zpos(j, grp)) =
+                        bf16x4_t{dzh[0], dzh[1], dzh[2], dzh[3]};
+                    *reinterpret_cast<bf16x4_t*>(sm.dzt[0] + zpos(j, 4 + grp)) =
+                        bf16x4_t{dzh[4], dzh[5], dzh[6], dzh[7]};
+                    *reinterpret_cast<bf16x4_t*>(sm.dzt[1] + zpos(j, grp)) =
+                        bf16x4_t{dzl[0], dzl[1], dzl[2], dzl[3]};
+                    *reinterpret_cast<bf16x4_t*>(sm.dzt[1] + zpos(j, 4 + grp)) =
+                        bf16x4_t{dzl[4], dzl[5], dzl[6], dzl[7]};
+                }
+    #pragma unroll
+                for (int db = 0; db < 8; ++db) {
+                    const int to = toff(db);
+                    const bf16x8_t gb = cat(ld_tr16(st.g + to), ld_tr16(st.g + to + 16 * D));
+                    aV[db] = mfma16(pvh, gb, aV[db]);
+                    aV[db] = mfma16(pvl, gb, aV[db]);
+                    const bf16x8_t qb = cat(ld_tr16(st.q + to), ld_tr16(st.q + to + 16 * D));
+                    aK[db] = mfma16(dzh, qb, aK[db]);
+                    aK[db] = mfma16(dzl, qb, aK[db]);
+                }
+            }
+            lds_wait();
+            barrier_keep_copies();   // dZ^T of the batch's last group complete
+            dq_step(ngroups - 1, nl, dtok_pend);
+        }
+        // the chunk's key-side sums: final when this workgroup covered all its groups
+        float* ok = whole ? dkraw : pk + ((size_t)lid * 2 + pslot) * CS * D;
+        float* ov = pv + ((size_t)lid * 2 + pslot) * CS * D;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const int d = 16 * db + row;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int kr = 16 * wave + 4 * grp + i;
+                if (whole) {
+                    const size_t o = cbase + (size_t)kr * rowstride + d;
+                    ok[o] = beta * aK[db][i];
+                    dV[o] = f2bf(aV[db][i]);
+                } else {
+                    ok[kr * D + d] = beta * aK[db][i];
+                    ov[kr * D + d] = aV[db][i];
+                }
+            }
+        }
+    }
+}
+
+// Token-major completion of dQ (one wave per (b, t, g); lane: head lane >> 3, columns
+// 16 (lane & 7) .. +15).  A slot counts when 0 <= c < floor(t / S); a slot repeating an
+// earlier slot's chunk shares that slot's partial (already weighted by the sum of their
+// weights) and its dw.
+__global__ __launch_bounds__(256) void bwd_dq_reduce(
+    Dims dm, const __bf16* __restrict__ Q, const float* __restrict__ Kbar,
+    const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const __bf16* __restrict__ part, const float* __restrict__ dwc, __bf16* __restrict__ dQ,
+    float* __restrict__ ds, float* __restrict__ qsum) {
+    const int lane = threadIdx.x & 63;
+    const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
+    if (item >= (size_t)dm.B * dm.L * dm.G) return;
+    const int g = (int)(item % dm.G);
+    const size_t bt = item / dm.G;
+    const int t = (int)(bt % dm.L);
+    const int b = (int)(bt / dm.L);
+    const int k = dm.k;
+    const size_t so = item * k;
+    const int ncand = t / dm.S;
+    const int head = lane >> 3, c0 = 16 * (lane & 7);
+
+    // this lane's view of the token's query rows, for q~ (issued first)
+    const __bf16* qrow = Q + ((bt * dm.H) + (size_t)g * HG + head) * D + c0;
+    const bf16x8_t q0 = ld_bf16x8(qrow), q1 = ld_bf16x8(qrow + 8);
+
+    int cl = -1;
+    float wl = 0.f, dwl = 0.f;
+    if (lane < k) {
+        cl = idx[so + lane];
+        wl = w[so + lane];
+        dwl = dwc[so + lane];
+    }
+    const bool valid = lane < k && cl >= 0 && cl < ncand;
+    int canon = lane;                       // first slot holding the same chunk
+    for (int s = 0; s < k; ++s) {
+        const int cs = __builtin_amdgcn_readlane(cl, s);
+        if (s < canon && cs == cl) canon = s;
+    }
+    const float dws = __shfl(dwl, canon, 64);
+    const float wdw = group_sum<64>(valid ? wl * dws : 0.f);
+    const float dsl = valid ? wl * (dws - wdw) : 0.f;
+    if (lane < k) ds[so + lane] = dsl;
+    const int own = (valid && canon == lane) ? 1 : 0;
+
+    float acc[16], lmk[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = lmk[i] = 0.f;
+    const size_t kbbase = (size_t)b * dm.C * dm.G + g;
+    for (int s0 = 0; s0 < k; s0 += 4) {
+        bf16x8_t pv[4][2];
+        float4 kv[4][4];
+        float coef[4];
+        int use[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int s = s0 + j;
+            const bool in = s < k;
+            const int cs = in ? __builtin_amdgcn_readlane(cl, s) : -1;
+            use[j] = in ? __builtin_amdgcn_readlane(own, s) : 0;
+            coef[j] = in ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s)) : 0.f;
+            if (use[j]) {
+                const __bf16* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = ld_bf16x8(pp);
+                pv[j][1] = ld_bf16x8(pp + 8);
+            } else {
+                pv[j][0] = pv[j][1] = bf16x8_t{};
+            }
+            const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
+            const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) kv[j][v] = (ncand > 0) ? *reinterpret_cast<const float4*>(kb + 4 * v)
+                                                              : float4{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                acc[i] += (float)pv[j][0][i];
+                acc[8 + i] += (float)pv[j][1][i];
+            }
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                lmk[4 * v + 0] = fmaf(coef[j], kv[j][v].x, lmk[4 * v + 0]);
+                lmk[4 * v + 1] = fmaf(coef[j], kv[j][v].y, lmk[4 * v + 1]);
+                lmk[4 * v + 2] = fmaf(coef[j], kv[j][v].z, lmk[4 * v + 2]);
+                lmk[4 * v + 3] = fmaf(coef[j], kv[j][v].w, lmk[4 * v + 3]);
+            }
+        }
+    }
+    bf16x8_t o0, o1;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o0[i] = f2bf(fmaf(dm.beta, acc[i], dm.alpha * lmk[i]));
+        o1[i] = f2bf(fmaf(dm.beta, acc[8 + i], dm.alpha * lmk[8 + i]));
+    }
+    __bf16* op = dQ + ((bt * dm.H) + (size_t)g * HG + head) * D + c0;
+    *reinterpret_cast<bf16x8_t*>(op) = o0;
+    *reinterpret_cast<bf16x8_t*>(op + 8) = o1;
+
+    // q~ = sum over the group's heads (lanes with the same column block): rows of 16 lanes
+    // pair heads 2m, 2m + 1 (lane ^ 8), then across rows (lane ^ 16, lane ^ 32)
+    float qs[16];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        qs[i] = (float)q0[i];
+        qs[8 + i] = (float)q1[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+        float v = qs[i] + dpp_mov<0x128>(qs[i]);      // row_ror:8 = lane ^ 8 within 16
+        v = pair16_sum(v);
+        qs[i] = pair32_sum(v);
+    }
+    if (lane < 8) {
+        float* qd = qsum + item * D + c0;
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+            *reinterpret_cast<float4*>(qd + 4 * v) =
+                float4{qs[4 * v], qs[4 * v + 1], qs[4 * v + 2], qs[4 * v + 3]};
+    }
+}
+
+
+// Landmark term of dK over the same ranges as bwd_fused_mfma: coef_t = sum of ds over the
+// token's slots holding c; dKbar_c = alpha * sum_t coef_t q~_t, in 8 interleaved token
+// streams (lane group j = tid / 32 takes every 8th token, lane 4 columns) summed in a fixed
+// order; per chunk when the range covers all its groups, else as the range's partial.
+__global__ __launch_bounds__(NT) void bwd_lmk_stream(
+    Dims dm, const int32_t* __restrict__ idx, const float* __restrict__ ds,
+    const float* __restrict__ qsum, const uint32_t* __restrict__ bm, int nwords,
+    const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
+    float* __restrict__ dkbar, float* __restrict__ pkb) {
+    __shared__ int list[FLIST];
+    __shared__ float coef[FLIST];
+    __shared__ float4 red[8][32];
+    __shared__ int wtot[NW];
+    const int tid = threadIdx.x;
+    const int lid = xcd_logical_id(kStreamWGs);
+    if (lid < 0) return;
+    const int R = dm.B * dm.G * dm.C;
+    const int total = plan[0], T = plan[1];
+    const int g0 = lid * T, g1 = min(g0 + T, total);
+    if (g0 >= g1) return;
+    const int k = dm.k;
+    const int j8 = tid >> 5, c4 = tid & 31;
+    for (int r = find_row(gstart, R, g0); r < R; ++r) {
+        const int rs = gstart[r], re = gstart[r + 1];
+        if (rs >= g1) break;
+        if (re == rs) continue;
+        const int j0 = max(g0, rs) - rs, j1 = min(g1, re) - rs;
+        const bool whole = (j0 == 0 && j1 == re - rs);
+        const int pslot = (rs <= g0) ? 0 : 1;
+        const int c = r % dm.C;
+        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
+        const uint32_t* bmrow = bm + (size_t)r * nwords;
+        const int wbeg = ((c + 1) * CS) >> 5;
+        const int tend = min(4 * j1, cntr[r]);
+        float4 acc{0.f, 0.f, 0.f, 0.f};
+        for (int p0 = 4 * j0; p0 < tend; p0 += FLIST) {
+            const int p1 = min(p0 + FLIST, tend);
+            const int nl = p1 - p0;
+            __syncthreads();
+            collect_tokens(bmrow, wbeg, nwords, p0, p1, list, wtot, tid);
+            for (int li = tid; li < nl; li += NT) {
+                const size_t so = (((size_t)b * dm.L + list[li]) * dm.G + g) * k;
+                float cf = 0.f;
+                for (int s0 = 0; s0 < k; s0 += 8) {
+                    int cc[8];
+                    float dd[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const bool in = s0 + j < k;
+                        cc[j] = in ? idx[so + s0 + j] : -1;
+                        dd[j] = in ? ds[so + s0 + j] : 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) cf += (cc[j] == c) ? dd[j] : 0.f;
+                }
+                coef[li] = cf;
+            }
+            __syncthreads();
+            const float* qb = qsum + ((size_t)b * dm.L * dm.G + g) * D + 4 * c4;
+            const size_t tstride = (size_t)dm.G * D;
+            int li = j8;
+            for (; li + 24 < nl; li += 32) {          // four independent loads in flight
+                float4 q[4];
+                float cf[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    q[u] = *reinterpret_cast<const float4*>(qb + (size_t)list[li + 8 * u] * tstride);
+                    cf[u] = coef[li + 8 * u];
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    acc.x = fmaf(cf[u], q[u].x, acc.x);
+                    acc.y = fmaf(cf[u], q[u].y, acc.y);
+                    acc.z = fmaf(cf[u], q[u].z, acc.z);
+                    acc.w = fmaf(cf[u], q[u].w, acc.w);
+                }
+            }
+            for (; li < nl; li += 8) {
+                const float4 q = *reinterpret_cast<const float4*>(qb + (size_t)list[li] * tstride);
+                const float cf = coef[li];
+                acc.x = fmaf(cf, q.x, acc.x);
+                acc.y = fmaf(cf, q.y, acc.y);
+                acc.z = fmaf(cf, q.z, acc.z);
+                acc.w = fmaf(cf, q.w, acc.w);
+            }
+        }
+        red[j8][c4] = acc;
+        __syncthreads();
+        if (tid < 32) {
+            float4 s = red[0][tid];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) {
+                s.x += red[j][tid].x;
+                s.y += red[j][tid].y;
+                s.z += red[j][tid].z;
+                s.w += red[j][tid].w;
+            }
+            const float a = dm.alpha;
+            float* out = whole ? dkbar + (size_t)r * D : pkb + ((size_t)lid * 2 + pslot) * D;
+            *reinterpret_cast<float4*>(out + 4 * tid) = float4{s.x * a, s.y * a, s.z * a, s.w * a};
+        }
+        __syncthreads();                          // red is rewritten for the next chunk
+    }
+}
+
+// Per chunk (b, g, c): dV and dK = beta dK_raw + dKbar_c / S from the chunk's own sums (one
+// workgroup covered it) or from the partials of the workgroups that shared it, added in
+// workgroup order; zeros for chunks nobody selected and for the trailing partial chunk.
+__global__ __launch_bounds__(NT) void bwd_finish(
+    Dims dm, const int* __restrict__ gstart, const int* __restrict__ cntr,
+    const int* __restrict__ plan, const float* __restrict__ dkraw, const float* __restrict__ pk,
+    const float* __restrict__ pv, const float* __restrict__ dkbar, const float* __restrict__ pkb,
+    __bf16* __restrict__ dK, __bf16* __restrict__ dV) {
+    __shared__ float4 lm[32];
+    const int tid = threadIdx.x;
+    const int c = blockIdx.x % dm.Call;
+    const int bg = blockIdx.x / dm.Call, b = bg / dm.G, g = bg % dm.G;
+    const size_t rowstride = (size_t)dm.G * D;
+    const size_t cbase = ((size_t)b * dm.L + (size_t)c * CS) * rowstride + (size_t)g * D;
+    const bf16x4_t z4{__bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f)};
+    const int r = bg * dm.C + c;
+    if (c >= dm.C || cntr[r] == 0) {            // trailing partial chunk, or never selected
+        const int rows = min(CS, dm.L - c * CS);
+        for (int e = tid; e < rows * 32; e += NT) {
+            const size_t o = cbase + (size_t)(e >> 5) * rowstride + 4 * (e & 31);
+            *reinterpret_cast<bf16x4_t*>(dK + o) = z4;
+            *reinterpret_cast<bf16x4_t*>(dV + o) = z4;
+        }
+        return;
+    }
+    const int T = plan[1];
+    const int rs = gstart[r], re = gstart[r + 1];
+    const int wf = rs / T, wl = (re - 1) / T;
+    const float invS = 1.f / (float)CS;
+    if (tid < 32) {
+        float4 s{0.f, 0.f, 0.f, 0.f};
+        if (wf == wl) {
+            s = *reinterpret_cast<const float4*>(dkbar + (size_t)r * D + 4 * tid);
+        } else {
+            for (int wg = wf; wg <= wl; ++wg) {
+                const int sl = (wg > wf || rs == wf * T) ? 0 : 1;
+                const float4 v = *reinterpret_cast<const float4*>(pkb + ((size_t)wg * 2 + sl) * D + 4 * tid);
+                s.x += v.x;
+                s.y += v.y;
+                s.z += v.z;
+                s.w += v.w;
+            }
+        }
+        lm[tid] = float4{s.x * invS, s.y * invS, s.z * invS, s.w * invS};
+    }
+    __syncthreads();
+    for (int e = tid; e < CS * 32; e += NT) {
+        const int kr = e >> 5, q4 = e & 31;
+        const size_t o = cbase + (size_t)kr * rowstride + 4 * q4;
+        float4 sk, sv{0.f, 0.f, 0.f, 0.f};
+        if (wf == wl) {
+            sk = *reinterpret_cast<const float4*>(dkraw + o);
+        } else {
+            sk = float4{0.f, 0.f, 0.f, 0.f};
+            for (int wg = wf; wg <= wl; ++wg) {
+                const int sl = (wg > wf || rs == wf * T) ? 0 : 1;
+                const size_t po = ((size_t)wg * 2 + sl) * CS * D + (size_t)kr * D + 4 * q4;
+                const float4 a = *reinterpret_cast<const float4*>(pk + po);
+                const float4 v = *reinterpret_cast<const float4*>(pv + po);
+                sk.x += a.x;
+                sk.y += a.y;
+                sk.z += a.z;
+                sk.w += a.w;
+                sv.x += v.x;
+                sv.y += v.y;
+                sv.z += v.z;
+                sv.w += v.w;
+            }
+            *reinterpret_cast<bf16x4_t*>(dV + o) =
+                bf16x4_t{f2bf(sv.x), f2bf(sv.y), f2bf(sv.z), f2bf(sv.w)};
+        }
+        const float4 l4 = lm[q4];
+        *reinterpret_cast<bf16x4_t*>(dK + o) =
+            bf16x4_t{f2bf(sk.x + l4.x), f2bf(sk.y + l4.y), f2bf(sk.z + l4.z), f2bf(sk.w + l4.w)};
+    }
+}
+
+}  // namespace
+
+bool backward_fused_supported(const Dims& dm, bool in_bf16) {
+    return in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX &&
+           !getenv("HSA_FORCE_GENERIC") && !getenv("HSA_BWD_TWO_PASS");
+}
+
+size_t backward_fused_workspace(const Dims& dm) {
+    if (dm.h != HG || dm.d != D || dm.S != CS) return 0;
+    return fused_ws(dm).end;
+}
+
+hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, const void* V,
+                                 const float* Kbar, const int32_t* idx, const float* w,
+                                 const void* dO, void* dQ, void* dK, void* dV, void* ws,
+                                 hipStream_t st) {
+    const FusedWs l = fused_ws(dm);
+    char* wsb = (char*)ws;
+    uint32_t* bmp = (uint32_t*)(wsb + l.bitmap);
+    int* cnt = (int*)(wsb + l.cnt);
+    int* gstart = (int*)(wsb + l.gstart);
+    int* plan = (int*)(wsb + l.plan);
+    __bf16* part = (__bf16*)(wsb + l.part);
+    float* dkraw = (float*)(wsb + l.dkraw);
+    float* dwc = (float*)(wsb + l.dw);
+    float* dsb = (float*)(wsb + l.ds);
+    float* qs = (float*)(wsb + l.qsum);
+    float* pk = (float*)(wsb + l.pk);
+    float* pv = (float*)(wsb + l.pv);
+    float* pkb = (float*)(wsb + l.pkb);
+    float* dkbar = (float*)(wsb + l.dkbar);
+    const int R = dm.B * dm.G * dm.C;
+    const int nwords = cdiv(dm.L, 32);
+    hipError_t e = launch_selection_bitmap(dm, idx, bmp, st);
+    if (e != hipSuccess) return e;
+    if (R > 0) {
+        {
+            HSA_TIMED("bwd_plan", st);
+            hipLaunchKernelGGL(bwd_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st,
+                               (const uint32_t*)bmp, R, nwords, dm.C, dm.S, cnt);
+            hipLaunchKernelGGL(bwd_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R,
+                               kStreamWGs, gstart, plan);
+        }
+        HSA_TIMED("bwd_fused_mfma", st);
+        hipLaunchKernelGGL(bwd_fused_mfma, dim3(kStreamWGs), dim3(NT), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
+                           (const __bf16*)dO, (const uint32_t*)bmp, nwords, (const int*)gstart,
+                           (const int*)cnt, (const int*)plan, part, dwc, dkraw, pk, pv,
+                           wsb + l.trash, (__bf16*)dV);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        const size_t items = (size_t)dm.B * dm.L * dm.G;
+        HSA_TIMED("bwd_dq_reduce", st);
+        hipLaunchKernelGGL(bwd_dq_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
+                           (const __bf16*)Q, Kbar, idx, w, (const __bf16*)part, (const float*)dwc,
+                           (__bf16*)dQ, dsb, qs);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        HSA_TIMED("bwd_lmk_finish", st);
+        if (R > 0)
+            hipLaunchKernelGGL(bwd_lmk_stream, dim3(kStreamWGs), dim3(NT), 0, st, dm, idx,
+                               (const float*)dsb, (const float*)qs, (const uint32_t*)bmp, nwords,
+                               (const int*)gstart, (const int*)cnt, (const int*)plan, dkbar, pkb);
+        hipLaunchKernelGGL(bwd_finish, dim3(dm.B * dm.G * dm.Call), dim3(NT), 0, st, dm,
+                           (const int*)gstart, (const int*)cnt, (const int*)plan,
+                           (const float*)dkraw, (const float*)pk, (const float*)pv,
+                           (const float*)dkbar, (const float*)pkb, (__bf16*)dK, (__bf16*)dV);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace hsa

@@ -300,6 +300,44 @@ def test_backward_empty_slots(hsa_gpu, name):
         assert_close(n, shape, g_, r)
 
 
+@pytest.mark.parametrize("name", ["ragged_mfma_bf16", "L4K_like_bf16", "key_offset_bf16"])
+def test_backward_repeated_slots(hsa_gpu, name):
+    """Slots that repeat a chunk: the chunk-major backward (bf16, h = 8, d = 128, S = 64)
+    gives the gradient of the forward, which adds each slot's weighted attention, so it
+    matches the oracle's slot-by-slot sums."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_backward, empty and repeated slots")
+    idx, w, idx_o = _scrambled_selection(ref, shape, 33, repeats=True)
+    srt = np.sort(idx_o, axis=-1)
+    assert ((srt[..., 1:] == srt[..., :-1]) & (srt[..., 1:] >= 0)).any()   # repeats present
+    want = oracle.backward(inp["Q"], inp["K"], inp["V"], idx_o, w, inp["dO"], shape.S)
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, torch.from_numpy(idx).cuda(),
+                               torch.from_numpy(w).cuda(), dev["dO"], shape.S)
+    torch.cuda.synchronize()
+    for n, g_, r in zip(("dQ", "dK", "dV"), got, want):
+        assert_close(n, shape, g_, r)
+
+
+@pytest.mark.parametrize("name", ["L4K_like_bf16", "ragged_mfma_bf16", "key_offset_bf16",
+                                  "no_candidates_bf16"])
+def test_backward_two_pass(hsa_gpu, name, monkeypatch):
+    """The two-pass MFMA backward (query pass, then key pass), which serves S = 128 and
+    is kept selectable for S = 64 with HSA_BWD_TWO_PASS=1."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_backward, two-pass path")
+    monkeypatch.setenv("HSA_BWD_TWO_PASS", "1")
+    idx = torch.from_numpy(ref["idx"]).cuda()
+    w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
+    Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()
+    dQ, dK, dV = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"],
+                                      shape.S)
+    torch.cuda.synchronize()
+    assert_close("dQ", shape, dQ, ref["dQ"])
+    assert_close("dK", shape, dK, ref["dK"])
+    assert_close("dV", shape, dV, ref["dV"])
+
+
 @pytest.mark.parametrize("shape", [Shape(1, 20480, 16, 2, 128, 64, 8, "bf16"),
                                    Shape(1, 8192, 4, 1, 64, 16, 20, "f32")],
                          ids=["C320_bf16", "C512_d64_k20_f32"])
