@@ -33,7 +33,8 @@
 // dQ = beta * (sum of the token's partials) + alpha * sum_i ds_i Kbar_{c_i}, and the token's
 // summed query q~ = sum_j q_j for the landmark term of dK.
 //
-// bwd_lmk_stream (same ranges): dKbar_c = alpha * sum_t ds_{t,c} q~_t, per chunk or partial.
+// bwd_lmk_stream (same ranges): dKbar_c = alpha * sum_t ds_{t,c} q~_t, per chunk or partial,
+// from the (token, slot) of each pair recorded by the fused pass.
 // bwd_finish (per chunk): dK = beta dK_raw + dKbar_c / S (Kbar_c is the mean of the chunk's
 // keys), dV; zeros for the trailing partial chunk.
 //
@@ -68,7 +69,8 @@ constexpr size_t kTrashBytes = HG * D * 2 + 64 * 4;
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct FusedWs {
-    size_t bitmap, cnt, gstart, plan, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash, end;
+    size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash,
+        end;
 };
 __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     FusedWs l;
@@ -80,7 +82,10 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     l.cnt = align256(R * nwords * 4);
     l.gstart = l.cnt + align256(R * 4);
     l.plan = l.gstart + align256((R + 1) * 4);
-    l.part = l.plan + 256;
+    // a pair's (token, first slot) index in stream order: 4 per group, at most one group per
+    // 4 selections plus one partial group per row
+    l.pairsel = l.plan + 256;
+    l.part = l.pairsel + align256((nsel + 4 * R) * 4);
     l.dkraw = l.part + align256(nsel * HG * D * 2);
     l.dw = l.dkraw + align256(nrow * D * 4);
     l.ds = l.dw + align256(nsel * 4);
@@ -242,7 +247,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, const uint32_t* __restrict__ bm, int nwords,
     const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
-    __bf16* __restrict__ part, float* __restrict__ dwc, float* __restrict__ dkraw,
+    int* __restrict__ pairsel, __bf16* __restrict__ part, float* __restrict__ dwc,
+    float* __restrict__ dkraw,
     float* __restrict__ pk, float* __restrict__ pv, char* __restrict__ trash,
     __bf16* __restrict__ dV) {
     __shared__ SmemF sm;
@@ -409,6 +415,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 }
                 // -1: no slot holding c (not expected: the bitmap bit says there is one)
                 sm.lsel[li] = first < k ? (int)(so + first) : -1;
+                pairsel[4 * (size_t)rs + p0 + li] = sm.lsel[li];
                 sm.lw[li] = first < k ? wsum : 0.f;
                 sm.list[li] = (int)(((size_t)b * dm.L + t) * dm.H + (size_t)g * HG);
             }
@@ -607,7 +614,16 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     const float dws = __shfl(dwl, canon, 64);
     const float wdw = group_sum<64>(valid ? wl * dws : 0.f);
     const float dsl = valid ? wl * (dws - wdw) : 0.f;
-    if (lane < k) ds[so + lane] = dsl;
+    // ds summed over the slots holding the same chunk, at the first of them (the landmark
+    // term of dK reads it there), in slot order
+    float dsm = 0.f;
+    for (int s = 0; s < k; ++s) {
+        const int cs = __builtin_amdgcn_readlane(canon, s);
+        const int vs = __builtin_amdgcn_readlane((int)valid, s);
+        const float d2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s));
+        if (vs && cs == lane) dsm += d2;
+    }
+    if (lane < k) ds[so + lane] = dsm;
     const int own = (valid && canon == lane) ? 1 : 0;
 
     float acc[16], lmk[16];
@@ -689,19 +705,19 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
 }
 
 
-// Landmark term of dK over the same ranges as bwd_fused_mfma: coef_t = sum of ds over the
-// token's slots holding c; dKbar_c = alpha * sum_t coef_t q~_t, in 8 interleaved token
-// streams (lane group j = tid / 32 takes every 8th token, lane 4 columns) summed in a fixed
-// order; per chunk when the range covers all its groups, else as the range's partial.
+// Landmark term of dK over the same ranges as bwd_fused_mfma: per pair (in stream order, as
+// the fused pass recorded it) the token's ds summed over its slots holding the chunk, times
+// the token's q~; dKbar_c = alpha * sum over pairs, in 8 interleaved pair streams (lane group
+// j = tid / 32 takes every 8th pair, lane 4 columns) summed in a fixed order; per chunk when
+// the range covers all its groups, else as the range's partial.
 __global__ __launch_bounds__(NT) void bwd_lmk_stream(
-    Dims dm, const int32_t* __restrict__ idx, const float* __restrict__ ds,
-    const float* __restrict__ qsum, const uint32_t* __restrict__ bm, int nwords,
-    const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
-    float* __restrict__ dkbar, float* __restrict__ pkb) {
-    __shared__ int list[FLIST];
-    __shared__ float coef[FLIST];
+    Dims dm, const int* __restrict__ pairsel, const float* __restrict__ dsm,
+    const float* __restrict__ qsum, const int* __restrict__ gstart, const int* __restrict__ cntr,
+    const int* __restrict__ plan, float* __restrict__ dkbar, float* __restrict__ pkb) {
+    constexpr int U = 16;                     // pairs per lane group in flight
+    constexpr int SEG = 2048;                 // pair records staged in LDS at once
     __shared__ float4 red[8][32];
-    __shared__ int wtot[NW];
+    __shared__ int sels[SEG];
     const int tid = threadIdx.x;
     const int lid = xcd_logical_id(kStreamWGs);
     if (lid < 0) return;
@@ -718,61 +734,33 @@ __global__ __launch_bounds__(NT) void bwd_lmk_stream(
         const int j0 = max(g0, rs) - rs, j1 = min(g1, re) - rs;
         const bool whole = (j0 == 0 && j1 == re - rs);
         const int pslot = (rs <= g0) ? 0 : 1;
-        const int c = r % dm.C;
-        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
-        const uint32_t* bmrow = bm + (size_t)r * nwords;
-        const int wbeg = ((c + 1) * CS) >> 5;
-        const int tend = min(4 * j1, cntr[r]);
+        const int* ps = pairsel + 4 * (size_t)rs;
+        const int pend = min(4 * j1, cntr[r]);
         float4 acc{0.f, 0.f, 0.f, 0.f};
-        for (int p0 = 4 * j0; p0 < tend; p0 += FLIST) {
-            const int p1 = min(p0 + FLIST, tend);
-            const int nl = p1 - p0;
+        for (int q0 = 4 * j0; q0 < pend; q0 += SEG) {
+            // the segment's pair records, one coalesced load, then U pairs per lane group in
+            // flight; positions past the chunk's last token add 0
+            const int qn = min(SEG, pend - q0);
+            __syncthreads();                      // sels of the previous segment are read
+            for (int i = tid; i < qn; i += NT) sels[i] = ps[q0 + i];
             __syncthreads();
-            collect_tokens(bmrow, wbeg, nwords, p0, p1, list, wtot, tid);
-            for (int li = tid; li < nl; li += NT) {
-                const size_t so = (((size_t)b * dm.L + list[li]) * dm.G + g) * k;
-                float cf = 0.f;
-                for (int s0 = 0; s0 < k; s0 += 8) {
-                    int cc[8];
-                    float dd[8];
+            for (int p = j8; p < qn; p += 8 * U) {
+                float cf[U];
+                float4 q[U];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const bool in = s0 + j < k;
-                        cc[j] = in ? idx[so + s0 + j] : -1;
-                        dd[j] = in ? ds[so + s0 + j] : 0.f;
-                    }
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) cf += (cc[j] == c) ? dd[j] : 0.f;
-                }
-                coef[li] = cf;
-            }
-            __syncthreads();
-            const float* qb = qsum + ((size_t)b * dm.L * dm.G + g) * D + 4 * c4;
-            const size_t tstride = (size_t)dm.G * D;
-            int li = j8;
-            for (; li + 24 < nl; li += 32) {          // four independent loads in flight
-                float4 q[4];
-                float cf[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    q[u] = *reinterpret_cast<const float4*>(qb + (size_t)list[li + 8 * u] * tstride);
-                    cf[u] = coef[li + 8 * u];
+                for (int u = 0; u < U; ++u) {
+                    const int sel = (p + 8 * u < qn) ? sels[p + 8 * u] : -1;
+                    const int sv = max(sel, 0);
+                    cf[u] = sel >= 0 ? dsm[sv] : 0.f;
+                    q[u] = *reinterpret_cast<const float4*>(qsum + (size_t)(sv / k) * D + 4 * c4);
                 }
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
+                for (int u = 0; u < U; ++u) {
                     acc.x = fmaf(cf[u], q[u].x, acc.x);
                     acc.y = fmaf(cf[u], q[u].y, acc.y);
                     acc.z = fmaf(cf[u], q[u].z, acc.z);
                     acc.w = fmaf(cf[u], q[u].w, acc.w);
                 }
-            }
-            for (; li < nl; li += 8) {
-                const float4 q = *reinterpret_cast<const float4*>(qb + (size_t)list[li] * tstride);
-                const float cf = coef[li];
-                acc.x = fmaf(cf, q.x, acc.x);
-                acc.y = fmaf(cf, q.y, acc.y);
-                acc.z = fmaf(cf, q.z, acc.z);
-                acc.w = fmaf(cf, q.w, acc.w);
             }
         }
         red[j8][c4] = acc;
@@ -823,6 +811,16 @@ __global__ __launch_bounds__(NT) void bwd_finish(
     const int rs = gstart[r], re = gstart[r + 1];
     const int wf = rs / T, wl = (re - 1) / T;
     const float invS = 1.f / (float)CS;
+    constexpr int PER = CS * 32 / NT;          // float4 columns per thread
+    float4 sk[PER];
+    if (wf == wl) {                             // one workgroup covered the chunk: its dK_raw
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int e = tid + u * NT;
+            sk[u] = *reinterpret_cast<const float4*>(dkraw + cbase + (size_t)(e >> 5) * rowstride +
+                                                     4 * (e & 31));
+        }
+    }
     if (tid < 32) {
         float4 s{0.f, 0.f, 0.f, 0.f};
         if (wf == wl) {
@@ -840,34 +838,46 @@ __global__ __launch_bounds__(NT) void bwd_finish(
         lm[tid] = float4{s.x * invS, s.y * invS, s.z * invS, s.w * invS};
     }
     __syncthreads();
-    for (int e = tid; e < CS * 32; e += NT) {
-        const int kr = e >> 5, q4 = e & 31;
-        const size_t o = cbase + (size_t)kr * rowstride + 4 * q4;
-        float4 sk, sv{0.f, 0.f, 0.f, 0.f};
-        if (wf == wl) {
-            sk = *reinterpret_cast<const float4*>(dkraw + o);
-        } else {
-            sk = float4{0.f, 0.f, 0.f, 0.f};
-            for (int wg = wf; wg <= wl; ++wg) {
-                const int sl = (wg > wf || rs == wf * T) ? 0 : 1;
-                const size_t po = ((size_t)wg * 2 + sl) * CS * D + (size_t)kr * D + 4 * q4;
-                const float4 a = *reinterpret_cast<const float4*>(pk + po);
-                const float4 v = *reinterpret_cast<const float4*>(pv + po);
-                sk.x += a.x;
-                sk.y += a.y;
-                sk.z += a.z;
-                sk.w += a.w;
-                sv.x += v.x;
-                sv.y += v.y;
-                sv.z += v.z;
-                sv.w += v.w;
-            }
-            *reinterpret_cast<bf16x4_t*>(dV + o) =
-                bf16x4_t{f2bf(sv.x), f2bf(sv.y), f2bf(sv.z), f2bf(sv.w)};
+    if (wf == wl) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int e = tid + u * NT;
+            const float4 l4 = lm[e & 31];
+            *reinterpret_cast<bf16x4_t*>(dK + cbase + (size_t)(e >> 5) * rowstride + 4 * (e & 31)) =
+                bf16x4_t{f2bf(sk[u].x + l4.x), f2bf(sk[u].y + l4.y), f2bf(sk[u].z + l4.z),
+                         f2bf(sk[u].w + l4.w)};
         }
-        const float4 l4 = lm[q4];
+        return;
+    }
+    float4 sv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) sk[u] = sv[u] = float4{0.f, 0.f, 0.f, 0.f};
+    for (int wg = wf; wg <= wl; ++wg) {
+        const int sl = (wg > wf || rs == wf * T) ? 0 : 1;
+        const size_t pb = ((size_t)wg * 2 + sl) * CS * D;
+        float4 a[PER], v[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int e = tid + u * NT;
+            a[u] = *reinterpret_cast<const float4*>(pk + pb + 4 * e);
+            v[u] = *reinterpret_cast<const float4*>(pv + pb + 4 * e);
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            sk[u].x += a[u].x; sk[u].y += a[u].y; sk[u].z += a[u].z; sk[u].w += a[u].w;
+            sv[u].x += v[u].x; sv[u].y += v[u].y; sv[u].z += v[u].z; sv[u].w += v[u].w;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int e = tid + u * NT;
+        const size_t o = cbase + (size_t)(e >> 5) * rowstride + 4 * (e & 31);
+        const float4 l4 = lm[e & 31];
+        *reinterpret_cast<bf16x4_t*>(dV + o) =
+            bf16x4_t{f2bf(sv[u].x), f2bf(sv[u].y), f2bf(sv[u].z), f2bf(sv[u].w)};
         *reinterpret_cast<bf16x4_t*>(dK + o) =
-            bf16x4_t{f2bf(sk.x + l4.x), f2bf(sk.y + l4.y), f2bf(sk.z + l4.z), f2bf(sk.w + l4.w)};
+            bf16x4_t{f2bf(sk[u].x + l4.x), f2bf(sk[u].y + l4.y), f2bf(sk[u].z + l4.z),
+                     f2bf(sk[u].w + l4.w)};
     }
 }
 
@@ -893,6 +903,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     int* cnt = (int*)(wsb + l.cnt);
     int* gstart = (int*)(wsb + l.gstart);
     int* plan = (int*)(wsb + l.plan);
+    int* pairsel = (int*)(wsb + l.pairsel);
     __bf16* part = (__bf16*)(wsb + l.part);
     float* dkraw = (float*)(wsb + l.dkraw);
     float* dwc = (float*)(wsb + l.dw);
@@ -918,7 +929,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
         hipLaunchKernelGGL(bwd_fused_mfma, dim3(kStreamWGs), dim3(NT), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
                            (const __bf16*)dO, (const uint32_t*)bmp, nwords, (const int*)gstart,
-                           (const int*)cnt, (const int*)plan, part, dwc, dkraw, pk, pv,
+                           (const int*)cnt, (const int*)plan, pairsel, part, dwc, dkraw, pk, pv,
                            wsb + l.trash, (__bf16*)dV);
     }
     e = hipGetLastError();
@@ -932,12 +943,16 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
+    if (R > 0) {
+        HSA_TIMED("bwd_lmk_stream", st);
+        hipLaunchKernelGGL(bwd_lmk_stream, dim3(kStreamWGs), dim3(NT), 0, st, dm,
+                           (const int*)pairsel, (const float*)dsb, (const float*)qs,
+                           (const int*)gstart, (const int*)cnt, (const int*)plan, dkbar, pkb);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     {
-        HSA_TIMED("bwd_lmk_finish", st);
-        if (R > 0)
-            hipLaunchKernelGGL(bwd_lmk_stream, dim3(kStreamWGs), dim3(NT), 0, st, dm, idx,
-                               (const float*)dsb, (const float*)qs, (const uint32_t*)bmp, nwords,
-                               (const int*)gstart, (const int*)cnt, (const int*)plan, dkbar, pkb);
+        HSA_TIMED("bwd_finish", st);
         hipLaunchKernelGGL(bwd_finish, dim3(dm.B * dm.G * dm.Call), dim3(NT), 0, st, dm,
                            (const int*)gstart, (const int*)cnt, (const int*)plan,
                            (const float*)dkraw, (const float*)pk, (const float*)pv,
