@@ -106,8 +106,11 @@ hsa_attn_status_t hsa_select_topk(const hsa_attn_params_t* p, const void* Q,
 /* Forward (Sec. 3.1.1 "Hierarchical Attention"; kernel design of Sec. 3.1.2): for every
  * (b, t, g) and valid slot i, O_{t,j,i} = softmax(beta q_j K_c^T) V_c over the S keys of
  * chunk c = idx[i]; O_{t,j} = sum_i w_i O_{t,j,i}.  idx, w are inputs (normally from
- * hsa_select_topk), so one selection may serve several attention layers.  Entries of idx
- * must be -1 or satisfy 0 <= c < floor(t/S), without repeats. */
+ * hsa_select_topk), so one selection may serve several attention layers.  Entries outside
+ * [0, floor(t/S)) are empty slots (no contribution); a chunk given in several slots adds
+ * each slot's weight.  Needs hsa_attn_workspace_size(p, HSA_OP_FORWARD) bytes of workspace:
+ * zero except for bf16, h = 8, d = 128, S = 64 with at least 256 complete chunks, where the
+ * chunk-major kernels keep a 2 KB partial output per (token, slot). */
 hsa_attn_status_t hsa_forward(const hsa_attn_params_t* p, const void* Q, const void* K,
                               const void* V, const int32_t* idx, const float* w, void* O,
                               void* ws, size_t ws_bytes, void* stream);

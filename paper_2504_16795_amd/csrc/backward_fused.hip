@@ -41,7 +41,7 @@
 // No atomics; every sum runs in a fixed order.
 #include <cstdlib>
 
-#include "chunk_lds.h"
+#include "chunk_stream.h"
 
 namespace hsa {
 
@@ -52,21 +52,14 @@ namespace {
 
 constexpr int D = 128;
 constexpr int HG = 8;
-constexpr int CS = 64;              // chunk size of this path
-constexpr int NW = 4;               // waves, 16 keys each
-constexpr int NT = NW * 64;
 constexpr int KMAX = 32;
 constexpr int FNST = 3;             // LDS stages of the group ring
 constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied per wave and group
-constexpr int FLIST = 1024;         // tokens listed at once (a multiple of 4)
 constexpr int kStoresPerStep = 5;   // global stores per lane of one dq step (4 partial, 1 dw)
-constexpr int kStreamWGs = 512;     // workgroups of the stream partition: two per CU
 
 // target of the stores of padding rows (a group's missing tokens), so that every wave issues
 // the same number of stores per group: 8 rows of partial dQ, then 64 floats
 constexpr size_t kTrashBytes = HG * D * 2 + 64 * 4;
-
-__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct FusedWs {
     size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash,
@@ -114,133 +107,6 @@ struct SmemF {
     float lw[FLIST];                // the token's total weight for c
     int wtot[NW];
 };
-
-// dZ^T tile: 64 keys x 32 rows of bf16, 64 bytes per key in 8-byte units of 4 rows; unit u
-// of key j sits at position u ^ zsw(j).  Both the C-layout writes (unit 4 rb + lane group of
-// 16 consecutive keys per instruction) and the transposed reads (4 units of 8 consecutive
-// keys per 32-lane pass) then fall on distinct banks.
-__device__ __forceinline__ int zsw(int j) { return (((j >> 2) & 1) << 2) | (((j >> 3) & 1) << 1); }
-__device__ __forceinline__ int zpos(int j, int u) { return j * 32 + 4 * (u ^ zsw(j)); }
-
-// maximum over the 16 lanes of a row, on the order-preserving integer image of the floats
-// (finite inputs): each step is one integer max with a DPP operand
-__device__ __forceinline__ float row16_max(float x) {
-    int v = __float_as_int(x);
-    v ^= (v >> 31) & 0x7fffffff;
-    v = max(v, dpp_mov<kDppXor1>(v));
-    v = max(v, dpp_mov<kDppXor2>(v));
-    v = max(v, dpp_mov<kDppHalfMirror>(v));
-    v = max(v, dpp_mov<kDppMirror>(v));
-    return __int_as_float(v ^ ((v >> 31) & 0x7fffffff));
-}
-
-// LDS writes of this wave complete (before a barrier that publishes them)
-__device__ __forceinline__ void lds_wait() {
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-}
-
-// Tokens at positions [p0, p1) of a chunk's ascending token list (the set bits of bitmap
-// words wbeg .. nwords - 1 of its row) into list[0 .. p1 - p0).  Whole workgroup; the words
-// are counted 256 at a time with a workgroup prefix sum, stopping once p1 is reached.
-__device__ __forceinline__ void collect_tokens(const uint32_t* __restrict__ bmrow, int wbeg,
-                                               int nwords, int p0, int p1, int* list,
-                                               int* wtot, int tid) {
-    const int lane = tid & 63, wave = tid >> 6;
-    int base = 0;
-    for (int wb = wbeg; wb < nwords; wb += NT) {
-        const int wi = wb + tid;
-        const uint32_t word = wi < nwords ? bmrow[wi] : 0u;
-        const int cnt = __popc(word);
-        int incl = cnt;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int v = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += v;
-        }
-        if (lane == 63) wtot[wave] = incl;
-        __syncthreads();
-        int before = 0, tot = 0;
-#pragma unroll
-        for (int w2 = 0; w2 < NW; ++w2) {
-            const int v = wtot[w2];
-            before += (w2 < wave) ? v : 0;
-            tot += v;
-        }
-        int pos = base + before + incl - cnt;
-        if (pos < p1 && pos + cnt > p0) {
-            uint32_t x = word;
-            while (x) {
-                if (pos >= p0 && pos < p1) list[pos - p0] = wi * 32 + (__ffs(x) - 1);
-                ++pos;
-                x &= x - 1;
-            }
-        }
-        base += tot;
-        __syncthreads();                // wtot is rewritten by the next block
-        if (base >= p1) break;
-    }
-}
-
-// The row (b, g, chunk) holding global group gpos: the last r with gstart[r] <= gpos
-// (gstart is non-decreasing, gstart[0] = 0 <= gpos < gstart[R]).
-__device__ __forceinline__ int find_row(const int* __restrict__ gstart, int R, int gpos) {
-    int lo = 0, hi = R;                 // gstart[lo] <= gpos < gstart[hi]
-    while (hi - lo > 1) {
-        const int mid = (lo + hi) >> 1;
-        if (gstart[mid] <= gpos) lo = mid;
-        else hi = mid;
-    }
-    return lo;
-}
-
-// tokens per bitmap row (one wave per row)
-__global__ __launch_bounds__(256) void bwd_rowcount(const uint32_t* __restrict__ bm, int R,
-                                                    int nwords, int C, int S,
-                                                    int* __restrict__ cnt) {
-    const int lane = threadIdx.x & 63;
-    const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (r >= R) return;
-    const int c = r % C;
-    const uint32_t* row = bm + (size_t)r * nwords;
-    int n = 0;
-    for (int wi = ((c + 1) * S >> 5) + lane; wi < nwords; wi += 64) n += __popc(row[wi]);
-    n = (int)group_sum<64>((float)n);   // exact: counts stay far below 2^24
-    if (lane == 0) cnt[r] = n;
-}
-
-// group prefix over the rows (one workgroup): gstart[r] = sum_{r' < r} ceil(cnt[r'] / 4);
-// plan = {total groups, groups per workgroup}
-__global__ __launch_bounds__(1024) void bwd_plan(const int* __restrict__ cnt, int R, int nwg,
-                                                 int* __restrict__ gstart, int* __restrict__ plan) {
-    __shared__ int wt[16];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    int carry = 0;
-    for (int r0 = 0; r0 < R; r0 += 1024) {
-        const int r = r0 + tid;
-        const int ng = r < R ? (cnt[r] + 3) >> 2 : 0;
-        int incl = ng;
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int v = __shfl_up(incl, o, 64);
-            if (lane >= o) incl += v;
-        }
-        if (lane == 63) wt[wave] = incl;
-        __syncthreads();
-        int before = 0, tot = 0;
-        for (int w2 = 0; w2 < 16; ++w2) {
-            before += (w2 < wave) ? wt[w2] : 0;
-            tot += wt[w2];
-        }
-        if (r < R) gstart[r] = carry + before + incl - ng;
-        carry += tot;
-        __syncthreads();
-    }
-    if (tid == 0) {
-        gstart[R] = carry;
-        plan[0] = carry;
-        plan[1] = carry > 0 ? (carry + nwg - 1) / nwg : 1;
-    }
-}
 
 __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
@@ -291,9 +157,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
         const int rs = gstart[r], re = gstart[r + 1];
         if (rs >= g1) break;
         if (re == rs) continue;
-        const int j0 = max(g0, rs) - rs, j1 = min(g1, re) - rs;
-        const bool whole = (j0 == 0 && j1 == re - rs);
-        const int pslot = (rs <= g0) ? 0 : 1;     // first row of the range, or its last
+        const Segment sg = segment_of(rs, re, g0, g1);
+        const int j0 = sg.j0, j1 = sg.j1, pslot = sg.pslot;
+        const bool whole = sg.whole;
         const int c = r % dm.C;
         const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
         const size_t cbase = ((size_t)b * dm.L + (size_t)c * CS) * rowstride + (size_t)g * D;
@@ -731,9 +597,9 @@ __global__ __launch_bounds__(NT) void bwd_lmk_stream(
         const int rs = gstart[r], re = gstart[r + 1];
         if (rs >= g1) break;
         if (re == rs) continue;
-        const int j0 = max(g0, rs) - rs, j1 = min(g1, re) - rs;
-        const bool whole = (j0 == 0 && j1 == re - rs);
-        const int pslot = (rs <= g0) ? 0 : 1;
+        const Segment sg = segment_of(rs, re, g0, g1);
+        const int j0 = sg.j0, j1 = sg.j1, pslot = sg.pslot;
+        const bool whole = sg.whole;
         const int* ps = pairsel + 4 * (size_t)rs;
         const int pend = min(4 * j1, cntr[r]);
         float4 acc{0.f, 0.f, 0.f, 0.f};
@@ -920,9 +786,9 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     if (R > 0) {
         {
             HSA_TIMED("bwd_plan", st);
-            hipLaunchKernelGGL(bwd_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st,
+            hipLaunchKernelGGL(stream_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st,
                                (const uint32_t*)bmp, R, nwords, dm.C, dm.S, cnt);
-            hipLaunchKernelGGL(bwd_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R,
+            hipLaunchKernelGGL(stream_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R,
                                kStreamWGs, gstart, plan);
         }
         HSA_TIMED("bwd_fused_mfma", st);

@@ -207,6 +207,7 @@ hipError_t launch_select(const Dims& dm, bool in_bf16, const void* Q, const floa
 hipError_t launch_forward(const Dims& dm, bool in_bf16, const void* Q, const void* K,
                           const void* V, const int32_t* idx, const float* w, void* O,
                           void* ws, hipStream_t st);
+size_t forward_workspace(const Dims& dm, bool in_bf16);
 size_t backward_workspace(const Dims& dm);
 hipError_t launch_backward(const Dims& dm, bool in_bf16, const void* Q, const void* K,
                            const void* V, const float* Kbar, const int32_t* idx,

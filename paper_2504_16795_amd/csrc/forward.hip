@@ -6,13 +6,19 @@
 // is a wave reduction, and the weighted chunk output is accumulated in registers.
 // Without an online softmax: every chunk is normalised on its own and scaled by w_i.
 //
-// The bf16 MFMA path for the main shapes lives in forward_mfma.hip and is selected by
-// launch_forward when it applies.
+// The bf16 MFMA paths for the main shapes live in forward_mfma.hip (tile-major) and
+// forward_fused.hip (chunk-major, for sequences with many chunks); launch_forward selects
+// them when they apply.
 #include "common.h"
 
 namespace hsa {
 
 bool forward_mfma_supported(const Dims& dm, bool in_bf16);
+bool forward_chunk_used(const Dims& dm, bool in_bf16);
+size_t forward_chunk_workspace(const Dims& dm, bool in_bf16);
+hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, const void* V,
+                                const int32_t* idx, const float* w, void* O, void* ws,
+                                hipStream_t st);
 hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,
                                const int32_t* idx, const float* w, void* O, void* ws,
                                hipStream_t st);
@@ -121,10 +127,16 @@ hipError_t launch_forward(const Dims& dm, bool in_bf16, const void* Q, const voi
                           const void* V, const int32_t* idx, const float* w, void* O, void* ws,
                           hipStream_t st) {
     if (dm.B == 0 || dm.L == 0) return hipSuccess;
+    if (forward_chunk_used(dm, in_bf16))
+        return launch_forward_chunk(dm, Q, K, V, idx, w, O, ws, st);
     if (forward_mfma_supported(dm, in_bf16))
         return launch_forward_mfma(dm, Q, K, V, idx, w, O, ws, st);
     return in_bf16 ? launch_t<bf16>(dm, Q, K, V, idx, w, O, st)
                    : launch_t<float>(dm, Q, K, V, idx, w, O, st);
+}
+
+size_t forward_workspace(const Dims& dm, bool in_bf16) {
+    return forward_chunk_workspace(dm, in_bf16);
 }
 
 hipError_t launch_forward_generic(const Dims& dm, bool in_bf16, const void* Q, const void* K,

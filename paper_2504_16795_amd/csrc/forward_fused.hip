@@ -1,0 +1,427 @@
+// Chunk-major forward of hierarchical sparse attention (Sec. 3.1.1 hierarchical attention
+// equation: O_t = sum_i w_i softmax(beta q K_{c_i}^T) V_{c_i}), for bf16 inputs with h = 8
+// query heads per KV head, d = 128 and S = 64, over the even split of chunk_stream.h.
+//
+// fwd_chunk_mfma: 4 waves; wave w owns keys 16 w .. 16 w + 15 of the current chunk (K_sub
+// in registers) and columns 32 w .. 32 w + 31 of d for the output product (V^T fragments of
+// all 64 keys, read transposed from the chunk staged in LDS).  Per group of 4 tokens (32
+// rows):
+//     Z [32 x 16] = Q_rows K_sub^T                                          (MFMA)
+//     each wave reduces its 16 keys per row (max m_w of the scaled logits, sum of
+//     exp(z - m_w)); the four waves' values are exchanged through LDS and combined into
+//     P = softmax over the chunk's 64 keys
+//     (W P)^T [64 keys x 32 rows] is staged in LDS (bf16), W the token's weight for c
+//     (summed over slots repeating c); wave w forms
+//     O_c^T [d 32 w .. 32 w + 31 x 32 rows] = V_c^T (W P)^T                 (MFMA)
+//     and stores it (bf16) at the (token, slot, head) of the token's first slot holding c.
+// fwd_reduce (token-major, one wave per (b, t, g)): O = sum of the token's partials.
+//
+// Against the tile-major forward (forward_mfma.hip) this reads each chunk's K / V once per
+// range instead of once per query tile, and uses every matrix row, at the cost of a 2 KB
+// partial per (token, slot) written and read back: it pays when tokens of a tile rarely share
+// chunks (long contexts).  No atomics; every sum runs in a fixed order.
+#include <cstdlib>
+
+#include "chunk_stream.h"
+
+namespace hsa {
+
+hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm,
+                                   hipStream_t st);
+
+namespace {
+
+constexpr int D = 128;
+constexpr int HG = 8;
+constexpr int KMAX = 32;
+constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
+constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
+constexpr int kOStores = 4;         // global stores per lane of one output step
+constexpr size_t kOTrashBytes = HG * D * 2;
+constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
+
+struct FwdWs {
+    size_t bitmap, cnt, gstart, plan, part, trash, end;
+};
+__host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
+    FwdWs l;
+    const size_t nsel = (size_t)dm.B * dm.L * dm.G * dm.k;
+    const size_t nwords = (size_t)((dm.L + 31) / 32);
+    const size_t R = (size_t)dm.B * dm.G * dm.C;
+    l.bitmap = 0;
+    l.cnt = align256(R * nwords * 4);
+    l.gstart = l.cnt + align256(R * 4);
+    l.plan = l.gstart + align256((R + 1) * 4);
+    l.part = l.plan + 256;
+    l.trash = l.part + align256(nsel * HG * D * 2);
+    l.end = l.trash + kOTrashBytes;
+    return l;
+}
+
+struct SmemO {
+    __bf16 st[ONST][32 * D];        // Q rows of a group, swizzled; stages 0, 1 hold the
+                                    // chunk's V rows while V^T is read
+    __bf16 pt[CS * 32];             // (W P)^T of a group: [key][row], see zpos
+    float stat[NW][2][32];          // per wave and row: m_w, sum exp
+    float fac[NW][32];              // per wave and row: P scale of the wave's keys
+    int list[FLIST];                // token; then its first Q row, (b L + t) H + g h
+    int lsel[FLIST];                // (token, first slot holding c): ((b L + t) G + g) k + s
+    float lw[FLIST];                // the token's total weight for c
+    int wtot[NW];
+};
+static_assert(ONST * 32 * D >= CS * D, "the V rows of a chunk fit in the first stages");
+
+__global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
+    Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
+    const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
+    const uint32_t* __restrict__ bm, int nwords, const int* __restrict__ gstart,
+    const int* __restrict__ cntr, const int* __restrict__ plan, __bf16* __restrict__ part,
+    char* __restrict__ trash) {
+    __shared__ SmemO sm;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int row = lane & 15, grp = lane >> 4;
+    const int lid = xcd_logical_id(kFwdWGs);
+    if (lid < 0) return;
+    const int R = dm.B * dm.G * dm.C;
+    const int total = plan[0], T = plan[1];
+    const int g0 = lid * T, g1 = min(g0 + T, total);
+    if (g0 >= g1) return;
+    const int k = dm.k;
+    const size_t rowstride = (size_t)dm.G * D;
+    const float sl2 = dm.beta * 1.44269504088896341f;
+
+    // LDS offsets of the chunk-swizzled tiles (chunk_lds.h), from per-lane bases: row reads,
+    // d step ks: kb0 + 32 (ks ^ ks_x) (+ 2048 per 16-row block); transposed reads, block db:
+    // tb0 + 16 (db ^ tr_x) (+ 16 rows: + 16 D)
+    const int swr = swz(row);
+    const int kb0 = row * D + 8 * (grp ^ (swr & 3)), ks_x = swr >> 2;
+    const int trr = 4 * grp + (row >> 2);
+    const int tb0 = trr * D + 8 * (((row & 3) >> 1) ^ ((trr >> 3) & 1)) + 4 * (row & 1);
+    const int tr_x = trr & 7;
+    auto koff = [&](int ks) __attribute__((always_inline)) { return kb0 + 32 * (ks ^ ks_x); };
+    auto toff = [&](int db) __attribute__((always_inline)) { return tb0 + 16 * (db ^ tr_x); };
+    int zb[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
+    __bf16* const tpart = reinterpret_cast<__bf16*>(trash);
+
+    for (int r = find_row(gstart, R, g0); r < R; ++r) {
+        const int rs = gstart[r], re = gstart[r + 1];
+        if (rs >= g1) break;
+        if (re == rs) continue;
+        const Segment sg = segment_of(rs, re, g0, g1);
+        const int c = r % dm.C;
+        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
+        const size_t cbase = ((size_t)b * dm.L + (size_t)c * CS) * rowstride + (size_t)g * D;
+        const int ntok = cntr[r];
+
+        // ---- the chunk's operands: K_sub^T (B operand of Z) and V^T (A operand of O^T:
+        // d = 32 wave + 16 dt + (lane & 15), keys of lane group grp in step ks2:
+        // 32 ks2 + 4 grp + (0..3) and 32 ks2 + 16 + 4 grp + (0..3))
+        __syncthreads();                          // the previous chunk's stages are read
+        bf16x8_t kB[4];
+        const int key = 16 * wave + row;
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+            kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+        chunk_to_lds<CS, NW>(V + cbase, rowstride, sm.st[0], wave, lane);
+        wait_loads_le<0>();
+        __syncthreads();
+        bf16x8_t vT[2][2];
+#pragma unroll
+        for (int dt = 0; dt < 2; ++dt)
+#pragma unroll
+            for (int ks2 = 0; ks2 < 2; ++ks2) {
+                const __bf16* p = sm.st[0] + toff(2 * wave + dt) + 32 * ks2 * D;
+                vT[dt][ks2] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
+            }
+
+        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
+            __bf16* st = sm.st[gi % ONST];
+#pragma unroll
+            for (int i = 0; i < OBPW; ++i) {
+                const int blk = wave * OBPW + i;
+                const int rr = blk * 4 + (lane >> 4);
+                int li = gi * 4 + (rr >> 3);
+                if (li >= nl) li = gi * 4;   // a missing token repeats the group's first (W = 0)
+                const size_t o = ((size_t)(uint32_t)(sm.list[li] + (rr & 7)) << 7) +
+                                 unit_pos(rr, lane & 15) * 8;
+                lds_copy16(Q + o, __builtin_amdgcn_readfirstlane(lds_address(st + blk * 512)));
+            }
+        };
+
+        // output partial of group gj from the staged (W P)^T (all waves' keys): rows
+        // 16 rt + (lane & 15), d = 32 wave + 16 dt + 4 grp + (0..3); exactly kOStores stores
+        // per lane (rows of missing tokens go to the trash area)
+        auto o_step = [&](int gj, int nl) __attribute__((always_inline)) {
+            f32x4_t oa[2][2];
+#pragma unroll
+            for (int dt = 0; dt < 2; ++dt) oa[dt][0] = oa[dt][1] = zero4();
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+                for (int ks2 = 0; ks2 < 2; ++ks2) {
+                    const __bf16* zp = sm.pt + zb[rt] + 1024 * ks2;
+                    const bf16x8_t bp = cat(ld_tr16(zp), ld_tr16(zp + 512));
+#pragma unroll
+                    for (int dt = 0; dt < 2; ++dt) oa[dt][rt] = mfma16(vT[dt][ks2], bp, oa[dt][rt]);
+                }
+#pragma unroll
+            for (int rt = 0; rt < 2; ++rt) {
+                const int li = gj * 4 + 2 * rt + (row >> 3);
+                const int so = li < nl ? sm.lsel[li] : -1;
+                __bf16* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
+                              (row & 7) * D + 32 * wave + 4 * grp;
+#pragma unroll
+                for (int dt = 0; dt < 2; ++dt) {
+                    const bf16x4_t v4{f2bf(oa[dt][rt][0]), f2bf(oa[dt][rt][1]),
+                                      f2bf(oa[dt][rt][2]), f2bf(oa[dt][rt][3])};
+                    *reinterpret_cast<bf16x4_t*>(dst + 16 * dt) = v4;
+                }
+            }
+        };
+
+        const uint32_t* bmrow = bm + (size_t)r * nwords;
+        const int wbeg = ((c + 1) * CS) >> 5;
+        const int tend = min(4 * sg.j1, ntok);
+        for (int p0 = 4 * sg.j0; p0 < tend; p0 += FLIST) {
+            const int p1 = min(p0 + FLIST, tend);
+            const int nl = p1 - p0;
+            __syncthreads();                      // the list of the previous batch is read
+            collect_tokens(bmrow, wbeg, nwords, p0, p1, sm.list, sm.wtot, tid);
+            // per listed token: its first slot holding c (a set bit means there is one) and
+            // its total weight for c.  All idx and w loads of a token are issued before use.
+            for (int li = tid; li < nl; li += NT) {
+                const int t = sm.list[li];
+                const size_t so = (((size_t)b * dm.L + t) * dm.G + g) * k;
+                int first = KMAX;
+                float wsum = 0.f;
+                for (int s0 = 0; s0 < k; s0 += 8) {
+                    int cc[8];
+                    float ww[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const bool in = s0 + j < k;
+                        cc[j] = in ? idx[so + s0 + j] : -1;
+                        ww[j] = in ? w[so + s0 + j] : 0.f;
+                    }
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (cc[j] == c) {
+                            first = min(first, s0 + j);
+                            wsum += ww[j];
+                        }
+                }
+                // -1: no slot holding c (not expected: the bitmap bit says there is one)
+                sm.lsel[li] = first < k ? (int)(so + first) : -1;
+                sm.lw[li] = first < k ? wsum : 0.f;
+                sm.list[li] = (int)(((size_t)b * dm.L + t) * dm.H + (size_t)g * HG);
+            }
+            __syncthreads();
+            const int ngroups = (nl + 3) / 4;
+#pragma unroll
+            for (int u = 0; u < ONST - 1; ++u)
+                if (u < ngroups) issue(u, nl);
+            for (int gi = 0; gi < ngroups; ++gi) {
+                // Group gi has landed once only the memory operations issued after its copies
+                // remain: the previous iteration's output stores (when it ran one) and the
+                // next group's copies (when there is a next group).  Loads and stores complete
+                // in issue order.
+                const bool more = gi + 1 < ngroups, stored = gi >= 2;
+                if (more && stored) wait_loads_le<OBPW + kOStores>();
+                else if (more) wait_loads_le<OBPW>();
+                else if (stored) wait_loads_le<kOStores>();
+                else wait_loads_le<0>();
+                lds_wait();
+                barrier_keep_copies();   // stage gi landed, (W P)^T of gi - 1 complete
+                if (gi > 0) o_step(gi - 1, nl);
+                if (gi + ONST - 1 < ngroups) issue(gi + ONST - 1, nl);
+                const __bf16* st = sm.st[gi % ONST];
+
+                // ---- Z for the wave's 16 keys (rows 16 rb + 4 grp + i, key 16 wave + row) --
+                f32x4_t z[2];
+                z[0] = z[1] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb)
+                        z[rb] = mfma16(ld_bf16x8(st + koff(ks) + rb * 2048), kB[ks], z[rb]);
+                // ---- the wave's row statistics over its 16 keys, to LDS -----------------
+                f32x4_t e[2];
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    f32x4_t sm_m, sm_l;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float zl = z[rb][i] * sl2;
+                        const float m = row16_max(zl);
+                        const float ev = fast_exp2(zl - m);
+                        e[rb][i] = ev;
+                        sm_m[i] = m;
+                        sm_l[i] = group_sum<16>(ev);
+                    }
+                    if (row == 0) {
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][0][16 * rb + 4 * grp]) = sm_m;
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][1][16 * rb + 4 * grp]) = sm_l;
+                    }
+                }
+                lds_wait();
+                barrier_keep_copies();   // every wave's statistics of group gi written
+                // ---- combine: lane r (and r + 32) handles row r = lane & 31 ------------------
+                {
+                    const int r32 = lane & 31;
+                    float mv[NW], lv[NW];
+#pragma unroll
+                    for (int w2 = 0; w2 < NW; ++w2) {
+                        mv[w2] = sm.stat[w2][0][r32];
+                        lv[w2] = sm.stat[w2][1][r32];
+                    }
+                    const float M = fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3]));
+                    float lsum = 0.f, aown = 0.f;
+#pragma unroll
+                    for (int w2 = 0; w2 < NW; ++w2) {
+                        const float a = fast_exp2(mv[w2] - M);
+                        lsum = fmaf(a, lv[w2], lsum);
+                        aown = (w2 == wave) ? a : aown;
+                    }
+                    if (lane < 32) sm.fac[wave][r32] = aown * __builtin_amdgcn_rcpf(lsum);
+                }
+                // back in the C layout (the wave's own LDS writes, read in order); W P to LDS as
+                // (W P)^T: key 16 wave + row, rows 16 rb + 4 grp .. +3 = unit 4 rb + grp
+                const int j = 16 * wave + row;
+#pragma unroll
+                for (int rb = 0; rb < 2; ++rb) {
+                    const f32x4_t fv = *reinterpret_cast<const f32x4_t*>(&sm.fac[wave][16 * rb + 4 * grp]);
+                    const int li = gi * 4 + 2 * rb + (grp >> 1);
+                    const float wt = li < nl ? sm.lw[li] : 0.f;
+                    *reinterpret_cast<bf16x4_t*>(sm.pt + zpos(j, 4 * rb + grp)) =
+                        bf16x4_t{f2bf(wt * e[rb][0] * fv[0]), f2bf(wt * e[rb][1] * fv[1]),
+                                 f2bf(wt * e[rb][2] * fv[2]), f2bf(wt * e[rb][3] * fv[3])};
+                }
+            }
+            lds_wait();
+            barrier_keep_copies();   // (W P)^T of the batch's last group complete
+            o_step(ngroups - 1, nl);
+        }
+    }
+}
+
+// O of one (b, t, g) (one wave; lane: head lane >> 3, columns 16 (lane & 7) .. +15): the sum
+// of the partials at the token's slots that hold a chunk first (0 <= c < floor(t / S); a slot
+// repeating an earlier slot's chunk adds nothing: that partial carries both weights).
+__global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __restrict__ idx,
+                                                  const __bf16* __restrict__ part,
+                                                  __bf16* __restrict__ O) {
+    const int lane = threadIdx.x & 63;
+    const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
+    if (item >= (size_t)dm.B * dm.L * dm.G) return;
+    const int g = (int)(item % dm.G);
+    const size_t bt = item / dm.G;
+    const int t = (int)(bt % dm.L);
+    const int k = dm.k;
+    const size_t so = item * k;
+    const int ncand = t / dm.S;
+    const int head = lane >> 3, c0 = 16 * (lane & 7);
+    const int cl = lane < k ? idx[so + lane] : -1;
+    const bool valid = lane < k && cl >= 0 && cl < ncand;
+    int canon = lane;
+    for (int s = 0; s < k; ++s) {
+        const int cs = __builtin_amdgcn_readlane(cl, s);
+        if (s < canon && cs == cl) canon = s;
+    }
+    const int own = (valid && canon == lane) ? 1 : 0;
+    float acc[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+    for (int s0 = 0; s0 < k; s0 += 4) {
+        bf16x8_t pv[4][2];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int s = s0 + j;
+            const int use = s < k ? __builtin_amdgcn_readlane(own, s) : 0;
+            if (use) {
+                const __bf16* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = ld_bf16x8(pp);
+                pv[j][1] = ld_bf16x8(pp + 8);
+            } else {
+                pv[j][0] = pv[j][1] = bf16x8_t{};
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                acc[i] += (float)pv[j][0][i];
+                acc[8 + i] += (float)pv[j][1][i];
+            }
+    }
+    bf16x8_t o0, o1;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        o0[i] = f2bf(acc[i]);
+        o1[i] = f2bf(acc[8 + i]);
+    }
+    __bf16* op = O + ((bt * dm.H) + (size_t)g * HG + head) * D + c0;
+    *reinterpret_cast<bf16x8_t*>(op) = o0;
+    *reinterpret_cast<bf16x8_t*>(op + 8) = o1;
+}
+
+}  // namespace
+
+// The chunk-major forward serves bf16, h = 8, d = 128, S = 64 when the sequence has many
+// chunks (a query tile's tokens then rarely share chunks, which is where the tile-major
+// forward loses its matrix rows); HSA_FWD_PATH=chunk or =tile forces the choice.
+bool forward_chunk_used(const Dims& dm, bool in_bf16) {
+    if (!(in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX) ||
+        getenv("HSA_FORCE_GENERIC"))
+        return false;
+    const char* f = getenv("HSA_FWD_PATH");
+    if (f && f[0] == 'c') return true;
+    if (f && f[0] == 't') return false;
+    return dm.C >= 256;
+}
+
+size_t forward_chunk_workspace(const Dims& dm, bool in_bf16) {
+    return forward_chunk_used(dm, in_bf16) ? fwd_ws(dm).end : 0;
+}
+
+hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, const void* V,
+                                const int32_t* idx, const float* w, void* O, void* ws,
+                                hipStream_t st) {
+    const FwdWs l = fwd_ws(dm);
+    char* wsb = (char*)ws;
+    uint32_t* bmp = (uint32_t*)(wsb + l.bitmap);
+    int* cnt = (int*)(wsb + l.cnt);
+    int* gstart = (int*)(wsb + l.gstart);
+    int* plan = (int*)(wsb + l.plan);
+    __bf16* part = (__bf16*)(wsb + l.part);
+    const int R = dm.B * dm.G * dm.C;
+    const int nwords = cdiv(dm.L, 32);
+    hipError_t e = launch_selection_bitmap(dm, idx, bmp, st);
+    if (e != hipSuccess) return e;
+    if (R > 0) {
+        {
+            HSA_TIMED("fwd_plan", st);
+            hipLaunchKernelGGL(stream_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st,
+                               (const uint32_t*)bmp, R, nwords, dm.C, dm.S, cnt);
+            hipLaunchKernelGGL(stream_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R,
+                               kFwdWGs, gstart, plan);
+        }
+        HSA_TIMED("fwd_chunk_mfma", st);
+        hipLaunchKernelGGL(fwd_chunk_mfma, dim3(kFwdWGs), dim3(NT), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
+                           (const uint32_t*)bmp, nwords, (const int*)gstart, (const int*)cnt,
+                           (const int*)plan, part, wsb + l.trash);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    {
+        const size_t items = (size_t)dm.B * dm.L * dm.G;
+        HSA_TIMED("fwd_reduce", st);
+        hipLaunchKernelGGL(fwd_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
+                           idx, (const __bf16*)part, (__bf16*)O);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace hsa

@@ -83,16 +83,18 @@ hsa_attn_status_t launched(hipError_t e, const char* what) {
     return ok();
 }
 
-size_t op_workspace(const hsa::Dims& dm, int op) {
+size_t op_workspace(const hsa::Dims& dm, bool in_bf16, int op) {
     switch (op) {
+        case HSA_OP_FORWARD: return hsa::forward_workspace(dm, in_bf16);
         case HSA_OP_BACKWARD: return hsa::backward_workspace(dm);
         case HSA_OP_DECODE: return hsa::decode_workspace(dm);
         default: return 0;
     }
 }
 
-hsa_attn_status_t check_ws(const hsa::Dims& dm, int op, const void* ws, size_t ws_bytes) {
-    const size_t need = op_workspace(dm, op);
+hsa_attn_status_t check_ws(const hsa::Dims& dm, bool in_bf16, int op, const void* ws,
+                           size_t ws_bytes) {
+    const size_t need = op_workspace(dm, in_bf16, op);
     if (need == 0) return HSA_ATTN_OK;
     if (ws_bytes < need)
         return fail(HSA_ATTN_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed",
@@ -150,7 +152,7 @@ hsa_attn_status_t hsa_forward(const hsa_attn_params_t* p, const void* Q, const v
     hsa_attn_status_t s = make_dims(p, &dm);
     if (s != HSA_ATTN_OK) return s;
     if (dm.B == 0 || dm.L == 0) return ok();
-    s = check_ws(dm, HSA_OP_FORWARD, ws, ws_bytes);
+    s = check_ws(dm, p->dtype == HSA_DTYPE_BF16, HSA_OP_FORWARD, ws, ws_bytes);
     if (s != HSA_ATTN_OK) return s;
     CHECK_PTR(Q, "Q");
     CHECK_PTR(K, "K");
@@ -171,7 +173,7 @@ hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const 
     hsa_attn_status_t s = make_dims(p, &dm);
     if (s != HSA_ATTN_OK) return s;
     if (dm.B == 0 || dm.L == 0) return ok();
-    s = check_ws(dm, HSA_OP_BACKWARD, ws, ws_bytes);
+    s = check_ws(dm, p->dtype == HSA_DTYPE_BF16, HSA_OP_BACKWARD, ws, ws_bytes);
     if (s != HSA_ATTN_OK) return s;
     CHECK_PTR(Q, "Q");
     CHECK_PTR(K, "K");
@@ -199,7 +201,7 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
         return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown kbar_dtype %d", (int)kbar_dtype);
     if (dm.G > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "decode supports at most 16 KV heads");
     if (dm.B == 0) return ok();
-    s = check_ws(dm, HSA_OP_DECODE, ws, ws_bytes);
+    s = check_ws(dm, p->dtype == HSA_DTYPE_BF16, HSA_OP_DECODE, ws, ws_bytes);
     if (s != HSA_ATTN_OK) return s;
     CHECK_PTR(q, "q");
     CHECK_PTR(o, "o");
@@ -221,7 +223,7 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
 size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op) {
     hsa::Dims dm;
     if (make_dims(p, &dm) != HSA_ATTN_OK) return 0;
-    return op_workspace(dm, op);
+    return op_workspace(dm, p->dtype == HSA_DTYPE_BF16, op);
 }
 
 const char* hsa_attn_status_string(hsa_attn_status_t s) {

@@ -300,6 +300,36 @@ def test_backward_empty_slots(hsa_gpu, name):
         assert_close(n, shape, g_, r)
 
 
+@pytest.mark.parametrize("name", ["L4K_like_bf16", "long_like_bf16", "ragged_mfma_bf16",
+                                  "key_offset_bf16", "no_candidates_bf16"])
+def test_forward_chunk_major(hsa_gpu, name, monkeypatch):
+    """The chunk-major forward (the default for bf16, h = 8, d = 128, S = 64 sequences of at
+    least 256 chunks), forced on the parity shapes with HSA_FWD_PATH=chunk."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_forward, chunk-major path")
+    monkeypatch.setenv("HSA_FWD_PATH", "chunk")
+    idx = torch.from_numpy(ref["idx"]).cuda()
+    w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    torch.cuda.synchronize()
+    assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
+
+
+def test_forward_chunk_major_repeated_slots(hsa_gpu, monkeypatch):
+    """Empty and repeated slots on the chunk-major forward: a chunk given in several slots
+    adds each slot's weight (one partial carries their sum)."""
+    name = "ragged_mfma_bf16"
+    shape, inp, ref, dev = case(name)
+    banner(name, "hsa_forward, chunk-major path, empty and repeated slots")
+    monkeypatch.setenv("HSA_FWD_PATH", "chunk")
+    idx, w, idx_o = _scrambled_selection(ref, shape, 31, repeats=True)
+    want = oracle.forward(inp["Q"], inp["K"], inp["V"], idx_o, w, shape.S)
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], torch.from_numpy(idx).cuda(),
+                            torch.from_numpy(w).cuda(), shape.S)
+    torch.cuda.synchronize()
+    assert_close("O", shape, O, want, o_abs=attention_abs(inp, idx_o, w, shape.S))
+
+
 @pytest.mark.parametrize("name", ["ragged_mfma_bf16", "L4K_like_bf16", "key_offset_bf16"])
 def test_backward_repeated_slots(hsa_gpu, name):
     """Slots that repeat a chunk: the chunk-major backward (bf16, h = 8, d = 128, S = 64)
