@@ -42,8 +42,8 @@ PEAK_FP32_VALU_TFLOPS = 157.3
 # Q K^T, dO V^T, (wP)^T dO, dz^T Q, dz K), all in the fused chunk pass, or split as
 # Q K^T, dO V^T, dz K in the query pass and P^T dO, dz^T Q in the key pass.
 MATMULS = {"forward_generic": 2, "forward_mfma": 2, "bwd_q_generic": 3, "bwd_q_mfma": 3,
-           "bwd_kv_generic": 2, "bwd_kv_mfma": 2, "bwd_fused_mfma": 5}
-MFMA_KERNELS = {"forward_mfma", "bwd_q_mfma", "bwd_kv_mfma", "bwd_fused_mfma"}
+           "bwd_kv_generic": 2, "bwd_kv_mfma": 2, "bwd_fused_mfma": 5, "fwd_chunk_mfma": 2}
+MFMA_KERNELS = {"forward_mfma", "bwd_q_mfma", "bwd_kv_mfma", "bwd_fused_mfma", "fwd_chunk_mfma"}
 
 
 def valid_pairs(B, L, G, S, k):
@@ -68,6 +68,10 @@ def kernel_work(name, sh, pairs):
     C = L // S
     if name == "landmarks_kernel":
         return B * C * S * G * d * es + B * C * G * d * 4, "GB/s", "hbm", PEAK_HBM_GBS
+    if name == "fwd_reduce":
+        # reads each pair's partial output (h d bf16) and idx; writes O
+        return (pairs * h * d * 2 + B * L * H * d * es + B * L * G * k * 4,
+                "GB/s", "hbm", PEAK_HBM_GBS)
     if name == "bwd_dq_reduce":
         # reads each pair's partial dQ (h d bf16), Q, idx / w / dw; writes dQ, ds, q~
         return (pairs * h * d * 2 + 2 * B * L * H * d * es + B * L * G * k * 16 +
@@ -323,6 +327,8 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
              "bwd_fused_mfma": "bwd_fused_mfma", "bwd_dq_reduce": "bwd_dq_reduce",
              "bwd_lmk_stream": "bwd_lmk_stream", "bwd_finish": "bwd_finish",
              "bwd_rowcount": "bwd_plan", "bwd_plan": "bwd_plan",
+             "fwd_chunk_mfma": "fwd_chunk_mfma", "fwd_reduce": "fwd_reduce",
+             "stream_rowcount": "plan", "stream_plan": "plan",
              "fill_zero_u32": "fill_zero_u32", "forward_generic": "forward_generic",
              "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic"}
     kernels = {}

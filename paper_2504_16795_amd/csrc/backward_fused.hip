@@ -55,7 +55,7 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int FNST = 3;             // LDS stages of the group ring
 constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied per wave and group
-constexpr int kStoresPerStep = 5;   // global stores per lane of one dq step (4 partial, 1 dw)
+constexpr int kStoresPerStep = 3;   // global stores per lane of one dq step (2 partial, 1 dw)
 
 // target of the stores of padding rows (a group's missing tokens), so that every wave issues
 // the same number of stores per group: 8 rows of partial dQ, then 64 floats
@@ -166,8 +166,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
         const int ntok = cntr[r];
 
         // ---- the chunk's operands: K_sub^T, V_sub^T (B operands of Z, dP) and K^T (A
-        // operand of dQ^T: d = 32 wave + 16 dt + (lane & 15), keys of lane group grp in step
-        // ks2: 32 ks2 + 4 grp + (0..3) and 32 ks2 + 16 + 4 grp + (0..3))
+        // operand of dQ^T: row m of tile dt is column 32 wave + 8 (m >> 2) + 4 dt + (m & 3) of
+        // d, so a lane's C values of both tiles are 8 consecutive columns; keys of lane group
+        // grp in step ks2: 32 ks2 + 4 grp + (0..3) and 32 ks2 + 16 + 4 grp + (0..3))
         __syncthreads();                          // the previous chunk's stages are read
         bf16x8_t kB[4], vB[4];
         const int key = 16 * wave + row;
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
         for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
             for (int ks2 = 0; ks2 < 2; ++ks2) {
-                const __bf16* p = sm.st[0].q + toff(2 * wave + dt) + 32 * ks2 * D;
+                const __bf16* p = sm.st[0].q + tr_perm_offset(lane, 32 * wave, dt) + 32 * ks2 * D;
                 kT[dt][ks2] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
             }
         f32x4_t aK[8], aV[8];
@@ -207,7 +208,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
         };
 
         // partial dQ^T of group gj from the staged dZ^T (all waves' keys), stored per (token,
-        // slot, head): rows 16 rt + (lane & 15), d = 32 wave + 16 dt + 4 grp + (0..3); then
+        // slot, head): rows 16 rt + (lane & 15), d = 32 wave + 8 grp + (0..7); then
         // the group's dw (wave 0, carried from its combine step).  Exactly kStoresPerStep
         // stores per lane: rows of missing tokens go to the trash area.
         auto dq_step = [&](int gj, int nl, float dtok) __attribute__((always_inline)) {
@@ -231,13 +232,11 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
                 __bf16* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                              (row & 7) * D + 32 * wave + 4 * grp;
-#pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const bf16x4_t v4{f2bf(qa[dt][rt][0]), f2bf(qa[dt][rt][1]),
-                                      f2bf(qa[dt][rt][2]), f2bf(qa[dt][rt][3])};
-                    *reinterpret_cast<bf16x4_t*>(dst + 16 * dt) = v4;
-                }
+                              (row & 7) * D + 32 * wave + 8 * grp;
+                *reinterpret_cast<bf16x8_t*>(dst) =
+                    bf16x8_t{f2bf(qa[0][rt][0]), f2bf(qa[0][rt][1]), f2bf(qa[0][rt][2]),
+                             f2bf(qa[0][rt][3]), f2bf(qa[1][rt][0]), f2bf(qa[1][rt][1]),
+                             f2bf(qa[1][rt][2]), f2bf(qa[1][rt][3])};
             }
             {
                 const int li = gj * 4 + ((lane & 31) >> 3);

@@ -31,6 +31,41 @@ __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size
 __device__ __forceinline__ int zsw(int j) { return (((j >> 2) & 1) << 2) | (((j >> 3) & 1) << 1); }
 __device__ __forceinline__ int zpos(int j, int u) { return j * 32 + 4 * (u ^ zsw(j)); }
 
+// Reductions of N rows at once over the 16 lanes of each row (the lanes holding one row of a
+// C layout): each step is applied to every row before the next, so no step waits on the
+// one before it.  Maxima on the order-preserving integer image of the floats (finite
+// inputs), one integer max with a DPP operand per step; sums with a DPP operand per step.
+template <int N>
+__device__ __forceinline__ void rows16_max(float (&x)[N]) {
+    int v[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        v[i] = __float_as_int(x[i]);
+        v[i] ^= (v[i] >> 31) & 0x7fffffff;
+    }
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = max(v[i], dpp_mov<kDppXor1>(v[i]));
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = max(v[i], dpp_mov<kDppXor2>(v[i]));
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = max(v[i], dpp_mov<kDppHalfMirror>(v[i]));
+#pragma unroll
+    for (int i = 0; i < N; ++i) v[i] = max(v[i], dpp_mov<kDppMirror>(v[i]));
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = __int_as_float(v[i] ^ ((v[i] >> 31) & 0x7fffffff));
+}
+template <int N>
+__device__ __forceinline__ void rows16_sum(float (&x)[N]) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] += dpp_mov<kDppXor1>(x[i]);
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] += dpp_mov<kDppXor2>(x[i]);
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] += dpp_mov<kDppHalfMirror>(x[i]);
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] += dpp_mov<kDppMirror>(x[i]);
+}
+
 // maximum over the 16 lanes of a row, on the order-preserving integer image of the floats
 // (finite inputs): each step is one integer max with a DPP operand
 __device__ __forceinline__ float row16_max(float x) {
@@ -149,6 +184,17 @@ __global__ __launch_bounds__(1024) void stream_plan(const int* __restrict__ cnt,
         plan[0] = carry;
         plan[1] = carry > 0 ? (carry + nwg - 1) / nwg : 1;
     }
+}
+
+// Offset (in a chunk tile of chunk_lds.h) of the transposed read that hands lane i of each
+// 16-lane group column d0 + 8 (i >> 2) + 4 dt + (i & 3) of rows kb .. kb + 3, kb = 4 (lane >>
+// 4) (the caller adds 16 hf + 32 ks2 rows): lane p loads row kb + (p >> 2) at columns d0 +
+// 8 (p & 3) + 4 dt .. +3.  With these as the A operand of a product whose rows are columns
+// of d, the C layout of tiles dt = 0, 1 gives each lane 8 consecutive columns, stored as one
+// 16-byte write.  Read once per chunk, so its 2-way bank conflicts do not matter.
+__device__ __forceinline__ int tr_perm_offset(int lane, int d0, int dt) {
+    const int p = lane & 15, r = 4 * (lane >> 4) + (p >> 2);
+    return r * kChunkD + unit_pos(r, (d0 >> 3) + (p & 3)) * 8 + 4 * dt;
 }
 
 // The segment of row r covered by groups [g0, g1): groups [j0, j1) of the row; whole when

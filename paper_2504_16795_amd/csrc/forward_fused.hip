@@ -36,7 +36,7 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
 constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
-constexpr int kOStores = 4;         // global stores per lane of one output step
+constexpr int kOStores = 2;         // global stores per lane of one output step
 constexpr size_t kOTrashBytes = HG * D * 2;
 constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
 
@@ -115,8 +115,9 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
         const size_t cbase = ((size_t)b * dm.L + (size_t)c * CS) * rowstride + (size_t)g * D;
         const int ntok = cntr[r];
 
-        // ---- the chunk's operands: K_sub^T (B operand of Z) and V^T (A operand of O^T:
-        // d = 32 wave + 16 dt + (lane & 15), keys of lane group grp in step ks2:
+        // ---- the chunk's operands: K_sub^T (B operand of Z) and V^T (A operand of O^T: row
+        // m of tile dt is column 32 wave + 8 (m >> 2) + 4 dt + (m & 3) of d, so a lane's C values
+        // of both tiles are 8 consecutive columns; keys of lane group grp in step ks2:
         // 32 ks2 + 4 grp + (0..3) and 32 ks2 + 16 + 4 grp + (0..3))
         __syncthreads();                          // the previous chunk's stages are read
         bf16x8_t kB[4];
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
         for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
             for (int ks2 = 0; ks2 < 2; ++ks2) {
-                const __bf16* p = sm.st[0] + toff(2 * wave + dt) + 32 * ks2 * D;
+                const __bf16* p = sm.st[0] + tr_perm_offset(lane, 32 * wave, dt) + 32 * ks2 * D;
                 vT[dt][ks2] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
             }
 
@@ -151,8 +152,8 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
         };
 
         // output partial of group gj from the staged (W P)^T (all waves' keys): rows
-        // 16 rt + (lane & 15), d = 32 wave + 16 dt + 4 grp + (0..3); exactly kOStores stores
-        // per lane (rows of missing tokens go to the trash area)
+        // 16 rt + (lane & 15), d = 32 wave + 8 grp + (0..7) (tile dt holds 4 dt + (0..3));
+        // exactly kOStores stores per lane (rows of missing tokens go to the trash area)
         auto o_step = [&](int gj, int nl) __attribute__((always_inline)) {
             f32x4_t oa[2][2];
 #pragma unroll
@@ -171,13 +172,11 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
                 __bf16* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                              (row & 7) * D + 32 * wave + 4 * grp;
-#pragma unroll
-                for (int dt = 0; dt < 2; ++dt) {
-                    const bf16x4_t v4{f2bf(oa[dt][rt][0]), f2bf(oa[dt][rt][1]),
-                                      f2bf(oa[dt][rt][2]), f2bf(oa[dt][rt][3])};
-                    *reinterpret_cast<bf16x4_t*>(dst + 16 * dt) = v4;
-                }
+                              (row & 7) * D + 32 * wave + 8 * grp;
+                *reinterpret_cast<bf16x8_t*>(dst) =
+                    bf16x8_t{f2bf(oa[0][rt][0]), f2bf(oa[0][rt][1]), f2bf(oa[0][rt][2]),
+                             f2bf(oa[0][rt][3]), f2bf(oa[1][rt][0]), f2bf(oa[1][rt][1]),
+                             f2bf(oa[1][rt][2]), f2bf(oa[1][rt][3])};
             }
         };
 
@@ -247,22 +246,23 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                     for (int rb = 0; rb < 2; ++rb)
                         z[rb] = mfma16(ld_bf16x8(st + koff(ks) + rb * 2048), kB[ks], z[rb]);
                 // ---- the wave's row statistics over its 16 keys, to LDS -----------------
+                // (rows 16 rb + 4 grp + i at index 4 rb + i)
+                float zl[8], mx[8], ls[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) mx[i] = zl[i] = z[i >> 2][i & 3] * sl2;
+                rows16_max(mx);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) ls[i] = zl[i] = fast_exp2(zl[i] - mx[i]);
+                rows16_sum(ls);
                 f32x4_t e[2];
 #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) {
-                    f32x4_t sm_m, sm_l;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const float zl = z[rb][i] * sl2;
-                        const float m = row16_max(zl);
-                        const float ev = fast_exp2(zl - m);
-                        e[rb][i] = ev;
-                        sm_m[i] = m;
-                        sm_l[i] = group_sum<16>(ev);
-                    }
+                    e[rb] = f32x4_t{zl[4 * rb], zl[4 * rb + 1], zl[4 * rb + 2], zl[4 * rb + 3]};
                     if (row == 0) {
-                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][0][16 * rb + 4 * grp]) = sm_m;
-                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][1][16 * rb + 4 * grp]) = sm_l;
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][0][16 * rb + 4 * grp]) =
+                            f32x4_t{mx[4 * rb], mx[4 * rb + 1], mx[4 * rb + 2], mx[4 * rb + 3]};
+                        *reinterpret_cast<f32x4_t*>(&sm.stat[wave][1][16 * rb + 4 * grp]) =
+                            f32x4_t{ls[4 * rb], ls[4 * rb + 1], ls[4 * rb + 2], ls[4 * rb + 3]};
                     }
                 }
                 lds_wait();
