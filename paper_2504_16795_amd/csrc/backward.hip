@@ -161,19 +161,38 @@ __global__ void fill_zero_u32(uint32_t* __restrict__ p, size_t n) {
     if (i < n) p[i] = 0u;
 }
 
-__global__ void bitmap_build(Dims dm, const int32_t* __restrict__ idx, uint32_t* __restrict__ bm,
-                             int nwords) {
-    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    const size_t total = (size_t)dm.B * dm.L * dm.G * dm.k;
-    if (i >= total) return;
-    const int c = idx[i];
-    size_t r = i / dm.k;
+// The selection bitmap (the M matrix of the key-side program as bits): bit t of word
+// (b, g, c, t / 32) is set when a slot of token t holds chunk c, 0 <= c < floor(t / S).  One
+// wave per (b, g, slot, 64 consecutive tokens): the lanes holding the same chunk are gathered
+// with a ballot, and one atomic OR per (chunk, word) sets their bits, so tokens that chose the
+// same chunk do not contend for its word one by one (order-independent, exact).
+__global__ __launch_bounds__(256) void bitmap_build(Dims dm, const int32_t* __restrict__ idx,
+                                                    uint32_t* __restrict__ bm, int nwords) {
+    const int lane = threadIdx.x & 63;
+    const size_t wv = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int nblk = (dm.L + 63) / 64;
+    if (wv >= (size_t)dm.B * dm.G * dm.k * nblk) return;
+    const int blk = (int)(wv % nblk);
+    size_t r = wv / nblk;
+    const int s = (int)(r % dm.k);
+    r /= dm.k;
     const int g = (int)(r % dm.G);
-    r /= dm.G;
-    const int t = (int)(r % dm.L);
-    const int b = (int)(r / dm.L);
-    if (c < 0 || c >= t / dm.S) return;     // only valid entries; others are ignored
-    atomicOr(&bm[(((size_t)b * dm.G + g) * dm.C + c) * nwords + (t >> 5)], 1u << (t & 31));
+    const int b = (int)(r / dm.G);
+    const int t = blk * 64 + lane;
+    const int c = t < dm.L ? idx[(((size_t)b * dm.L + t) * dm.G + g) * dm.k + s] : -1;
+    const bool valid = c >= 0 && c < t / dm.S;   // only valid entries; others are ignored
+    uint64_t active = __ballot(valid);
+    uint32_t* row = bm + ((size_t)b * dm.G + g) * dm.C * nwords + 2 * blk;
+    while (active) {
+        const int c0 = __builtin_amdgcn_readlane(c, __ffsll((unsigned long long)active) - 1);
+        const uint64_t m = __ballot(valid && c == c0);
+        if (lane == 0) {
+            const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+            if (lo) atomicOr(row + (size_t)c0 * nwords, lo);
+            if (hi) atomicOr(row + (size_t)c0 * nwords + 1, hi);
+        }
+        active &= ~m;
+    }
 }
 
 template <typename T, int D, int CS>
@@ -348,10 +367,10 @@ void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
             hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0,
                                st, bm, nbm);
         }
-        const size_t ne = (size_t)dm.B * dm.L * dm.G * dm.k;
+        const size_t nwv = (size_t)dm.B * dm.G * dm.k * cdiv(dm.L, 64);
         {
             HSA_TIMED("bitmap_build", st);
-            hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st,
+            hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((nwv + 3) / 4)), dim3(256), 0, st,
                                dm, idx, bm, nwords);
         }
     }
@@ -392,10 +411,10 @@ hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t*
         hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0, st,
                            bm, nbm);
     }
-    const size_t ne = (size_t)dm.B * dm.L * dm.G * dm.k;
+    const size_t nwv = (size_t)dm.B * dm.G * dm.k * cdiv(dm.L, 64);
     {
         HSA_TIMED("bitmap_build", st);
-        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, st, dm,
+        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((nwv + 3) / 4)), dim3(256), 0, st, dm,
                            idx, bm, nwords);
     }
     return hipGetLastError();

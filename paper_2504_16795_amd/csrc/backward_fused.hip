@@ -31,7 +31,7 @@
 //
 // bwd_dq_reduce (token-major, one wave per (b, t, g)): ds_i = w_i (dw_i - sum_m w_m dw_m),
 // dQ = beta * (sum of the token's partials) + alpha * sum_i ds_i Kbar_{c_i}, and the token's
-// summed query q~ = sum_j q_j for the landmark term of dK.
+// summed query q~ = sum_j q_j (stored as bf16) for the landmark term of dK.
 //
 // bwd_lmk_stream (same ranges): dKbar_c = alpha * sum_t ds_{t,c} q~_t, per chunk or partial,
 // from the (token, slot) of each pair recorded by the fused pass.
@@ -75,15 +75,15 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     l.cnt = align256(R * nwords * 4);
     l.gstart = l.cnt + align256(R * 4);
     l.plan = l.gstart + align256((R + 1) * 4);
-    // a pair's (token, first slot) index in stream order: 4 per group, at most one group per
-    // 4 selections plus one partial group per row
+    // a pair's record in stream order, ((b L + t) G + g) * 32 + first slot holding the chunk:
+    // 4 per group, at most one group per 4 selections plus one partial group per row
     l.pairsel = l.plan + 256;
     l.part = l.pairsel + align256((nsel + 4 * R) * 4);
     l.dkraw = l.part + align256(nsel * HG * D * 2);
     l.dw = l.dkraw + align256(nrow * D * 4);
     l.ds = l.dw + align256(nsel * 4);
     l.qsum = l.ds + align256(nsel * 4);
-    l.pk = l.qsum + align256(nrow * D * 4);
+    l.pk = l.qsum + align256(nrow * D * 2);
     l.pv = l.pk + (size_t)kStreamWGs * 2 * CS * D * 4;
     l.pkb = l.pv + (size_t)kStreamWGs * 2 * CS * D * 4;
     l.dkbar = l.pkb + (size_t)kStreamWGs * 2 * D * 4;
@@ -280,7 +280,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 }
                 // -1: no slot holding c (not expected: the bitmap bit says there is one)
                 sm.lsel[li] = first < k ? (int)(so + first) : -1;
-                pairsel[4 * (size_t)rs + p0 + li] = sm.lsel[li];
+                // the pair's record for the landmark term: its q~ row times 32 plus its slot
+                pairsel[4 * (size_t)rs + p0 + li] =
+                    first < k ? (int)((((size_t)b * dm.L + t) * dm.G + g) * 32 + first) : -1;
                 sm.lw[li] = first < k ? wsum : 0.f;
                 sm.list[li] = (int)(((size_t)b * dm.L + t) * dm.H + (size_t)g * HG);
             }
@@ -446,7 +448,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     Dims dm, const __bf16* __restrict__ Q, const float* __restrict__ Kbar,
     const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ part, const float* __restrict__ dwc, __bf16* __restrict__ dQ,
-    float* __restrict__ ds, float* __restrict__ qsum) {
+    float* __restrict__ ds, __bf16* __restrict__ qsum) {
     const int lane = threadIdx.x & 63;
     const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
     if (item >= (size_t)dm.B * dm.L * dm.G) return;
@@ -560,12 +562,16 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
         v = pair16_sum(v);
         qs[i] = pair32_sum(v);
     }
-    if (lane < 8) {
-        float* qd = qsum + item * D + c0;
+    if (lane < 8) {                               // stored as bf16 (the landmark term's input)
+        __bf16* qd = qsum + item * D + c0;
+        bf16x8_t a, b2;
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-            *reinterpret_cast<float4*>(qd + 4 * v) =
-                float4{qs[4 * v], qs[4 * v + 1], qs[4 * v + 2], qs[4 * v + 3]};
+        for (int i = 0; i < 8; ++i) {
+            a[i] = f2bf(qs[i]);
+            b2[i] = f2bf(qs[8 + i]);
+        }
+        *reinterpret_cast<bf16x8_t*>(qd) = a;
+        *reinterpret_cast<bf16x8_t*>(qd + 8) = b2;
     }
 }
 
@@ -577,7 +583,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
 // the range covers all its groups, else as the range's partial.
 __global__ __launch_bounds__(NT) void bwd_lmk_stream(
     Dims dm, const int* __restrict__ pairsel, const float* __restrict__ dsm,
-    const float* __restrict__ qsum, const int* __restrict__ gstart, const int* __restrict__ cntr,
+    const __bf16* __restrict__ qsum, const int* __restrict__ gstart, const int* __restrict__ cntr,
     const int* __restrict__ plan, float* __restrict__ dkbar, float* __restrict__ pkb) {
     constexpr int U = 16;                     // pairs per lane group in flight
     constexpr int SEG = 2048;                 // pair records staged in LDS at once
@@ -615,9 +621,10 @@ __global__ __launch_bounds__(NT) void bwd_lmk_stream(
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
                     const int sel = (p + 8 * u < qn) ? sels[p + 8 * u] : -1;
-                    const int sv = max(sel, 0);
-                    cf[u] = sel >= 0 ? dsm[sv] : 0.f;
-                    q[u] = *reinterpret_cast<const float4*>(qsum + (size_t)(sv / k) * D + 4 * c4);
+                    const int qr = max(sel, 0) >> 5;             // the token's q~ row
+                    cf[u] = sel >= 0 ? dsm[(size_t)qr * k + (sel & 31)] : 0.f;
+                    const bf16x4_t qv = ld_bf16x4(qsum + (size_t)qr * D + 4 * c4);
+                    q[u] = float4{(float)qv[0], (float)qv[1], (float)qv[2], (float)qv[3]};
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
@@ -748,9 +755,11 @@ __global__ __launch_bounds__(NT) void bwd_finish(
 
 }  // namespace
 
+// Row and (token, slot) indices of this path are 32-bit: B L G < 2^26.
 bool backward_fused_supported(const Dims& dm, bool in_bf16) {
     return in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX &&
-           !getenv("HSA_FORCE_GENERIC") && !getenv("HSA_BWD_TWO_PASS");
+           (size_t)dm.B * dm.L * dm.G < ((size_t)1 << 26) && !getenv("HSA_FORCE_GENERIC") &&
+           !getenv("HSA_BWD_TWO_PASS");
 }
 
 size_t backward_fused_workspace(const Dims& dm) {
@@ -773,7 +782,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     float* dkraw = (float*)(wsb + l.dkraw);
     float* dwc = (float*)(wsb + l.dw);
     float* dsb = (float*)(wsb + l.ds);
-    float* qs = (float*)(wsb + l.qsum);
+    __bf16* qs = (__bf16*)(wsb + l.qsum);
     float* pk = (float*)(wsb + l.pk);
     float* pv = (float*)(wsb + l.pv);
     float* pkb = (float*)(wsb + l.pkb);
@@ -811,7 +820,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     if (R > 0) {
         HSA_TIMED("bwd_lmk_stream", st);
         hipLaunchKernelGGL(bwd_lmk_stream, dim3(kStreamWGs), dim3(NT), 0, st, dm,
-                           (const int*)pairsel, (const float*)dsb, (const float*)qs,
+                           (const int*)pairsel, (const float*)dsb, (const __bf16*)qs,
                            (const int*)gstart, (const int*)cnt, (const int*)plan, dkbar, pkb);
     }
     e = hipGetLastError();

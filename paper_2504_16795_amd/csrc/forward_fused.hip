@@ -90,16 +90,11 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     const size_t rowstride = (size_t)dm.G * D;
     const float sl2 = dm.beta * 1.44269504088896341f;
 
-    // LDS offsets of the chunk-swizzled tiles (chunk_lds.h), from per-lane bases: row reads,
-    // d step ks: kb0 + 32 (ks ^ ks_x) (+ 2048 per 16-row block); transposed reads, block db:
-    // tb0 + 16 (db ^ tr_x) (+ 16 rows: + 16 D)
+    // LDS offsets of the row reads of a chunk-swizzled tile (chunk_lds.h), d step ks:
+    // kb0 + 32 (ks ^ ks_x) (+ 2048 per 16-row block)
     const int swr = swz(row);
     const int kb0 = row * D + 8 * (grp ^ (swr & 3)), ks_x = swr >> 2;
-    const int trr = 4 * grp + (row >> 2);
-    const int tb0 = trr * D + 8 * (((row & 3) >> 1) ^ ((trr >> 3) & 1)) + 4 * (row & 1);
-    const int tr_x = trr & 7;
     auto koff = [&](int ks) __attribute__((always_inline)) { return kb0 + 32 * (ks ^ ks_x); };
-    auto toff = [&](int db) __attribute__((always_inline)) { return tb0 + 16 * (db ^ tr_x); };
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
@@ -373,8 +368,8 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
 // forward loses its matrix rows); HSA_FWD_PATH=chunk or =tile forces the choice.
 bool forward_chunk_used(const Dims& dm, bool in_bf16) {
     if (!(in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX) ||
-        getenv("HSA_FORCE_GENERIC"))
-        return false;
+        (size_t)dm.B * dm.L * dm.G >= ((size_t)1 << 26) || getenv("HSA_FORCE_GENERIC"))
+        return false;                             // (row and (token, slot) indices are 32-bit)
     const char* f = getenv("HSA_FWD_PATH");
     if (f && f[0] == 'c') return true;
     if (f && f[0] == 't') return false;
