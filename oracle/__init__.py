@@ -29,7 +29,7 @@ _lib = None
 class _Dims(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int64), ("h", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("S", ctypes.c_int32), ("k", ctypes.c_int32), ("alpha", ctypes.c_double),
-                ("beta", ctypes.c_double)]
+                ("beta", ctypes.c_double), ("stick", ctypes.c_int32)]
 
 
 def build(force: bool = True) -> str:
@@ -79,10 +79,13 @@ def default_scales(h: int, d: int):
     return 1.0 / math.sqrt(h * d), 1.0 / math.sqrt(d)
 
 
-def dims(L, h, d, S, k, alpha=None, beta=None) -> _Dims:
+def dims(L, h, d, S, k, alpha=None, beta=None, stick=False) -> _Dims:
+    """Slice dimensions; stick selects stick-breaking chunk weights (Sec. 3.1.1) instead of
+    the softmax over the selected scores."""
     a0, b0 = default_scales(h, d)
     return _Dims(int(L), int(h), int(d), int(S), int(k),
-                 float(a0 if alpha is None else alpha), float(b0 if beta is None else beta))
+                 float(a0 if alpha is None else alpha), float(b0 if beta is None else beta),
+                 1 if stick else 0)
 
 
 # ----------------------------------------------------------------------------------
@@ -178,7 +181,7 @@ def landmarks(K, S: int) -> np.ndarray:
     return out
 
 
-def select(Q, Kbar, G: int, S: int, k: int, alpha=None):
+def select(Q, Kbar, G: int, S: int, k: int, alpha=None, stick=False):
     """idx [B,L,G,k] int32, w [B,L,G,k], gap [B,L,G], selected scores [B,L,G,k]."""
     Q, Kbar = _f64(Q), _f64(Kbar)
     B, L, H, d = Q.shape
@@ -189,7 +192,7 @@ def select(Q, Kbar, G: int, S: int, k: int, alpha=None):
     ss = np.empty((B, L, G, k))
     for b in range(B):
         for g in range(G):
-            dm = dims(L, h, d, S, k, alpha)
+            dm = dims(L, h, d, S, k, alpha, None, stick)
             i, ww, gp, s = select_slice(dm, Q[b, :, g * h:(g + 1) * h], Kbar[b, :, g])
             idx[b, :, g], w[b, :, g], gap[b, :, g], ss[b, :, g] = i, ww, gp, s
     return idx, w, gap, ss
@@ -209,8 +212,9 @@ def forward(Q, K, V, idx, w, S: int, beta=None):
     return O
 
 
-def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None):
-    """dQ, dK, dV (fp64) of sum(dO * O) with the selection held fixed."""
+def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False):
+    """dQ, dK, dV (fp64) of sum(dO * O) with the selection held fixed (weights a function of
+    the selected scores: softmax, or stick-breaking with stick)."""
     Q, K, V, w, dO = map(_f64, (Q, K, V, w, dO))
     B, L, H, G, d, h = _shape(Q, K)
     k = idx.shape[-1]
@@ -220,7 +224,7 @@ def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None):
     dV = np.zeros((B, L, G, d))
     for b in range(B):
         for g in range(G):
-            dm = dims(L, h, d, S, k, alpha, beta)
+            dm = dims(L, h, d, S, k, alpha, beta, stick)
             Qs = np.ascontiguousarray(Q[b, :, g * h:(g + 1) * h])
             dOs = np.ascontiguousarray(dO[b, :, g * h:(g + 1) * h])
             Ks, Vs = np.ascontiguousarray(K[b, :, g]), np.ascontiguousarray(V[b, :, g])
@@ -236,7 +240,7 @@ def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None):
 
 
 def decode(q, Kc, Vc, Kbar_cache, cache_len: Sequence[int], S: int, k: int,
-           alpha=None, beta=None):
+           alpha=None, beta=None, stick=False):
     """Single-token decode: q [B,H,d]; Kc, Vc [B,N,G,d]; Kbar_cache [B,Cc,G,d] (given).
 
     Returns o [B,H,d], idx [B,G,k], w [B,G,k], gap [B,G]."""
@@ -253,7 +257,7 @@ def decode(q, Kc, Vc, Kbar_cache, cache_len: Sequence[int], S: int, k: int,
         n = int(cache_len[b])
         nch = n // S
         for g in range(G):
-            dm = dims(n, h, d, S, k, alpha, beta)
+            dm = dims(n, h, d, S, k, alpha, beta, stick)
             qs = np.ascontiguousarray(q[b, g * h:(g + 1) * h])
             # only the candidate chunks are read
             Ks = _f64(Kc[b, :nch * S, g]) if nch else np.zeros((1, d))

@@ -8,7 +8,8 @@
  *   - the group score uses the concatenated group query against the tiled landmark,
  *     i.e. alpha * (sum_j q_j) . Kbar_c;
  *   - chunk weights are a softmax over the selected scores (the paper's ablation
- *     without stick-breaking); intra-chunk attention is the standard softmax;
+ *     without stick-breaking), or the stick-breaking weights of the main variant (a dims
+ *     flag); intra-chunk attention is the standard softmax;
  *   - ties in the top-k go to the lower chunk index; slots are ordered by descending
  *     chunk index;
  *   - gradients treat the selected index set as constant.
@@ -92,14 +93,27 @@ static void select_one(const hsa_oracle_dims* dm, const double* q, const double*
 
     /* slots in descending chunk order */
     qsort(cand, (size_t)n, sizeof(cand_t), cmp_chunk_desc);
-    double m = -INFINITY;
-    for (int64_t i = 0; i < n; ++i) m = cand[i].s > m ? cand[i].s : m;
-    double z = 0.0;
-    for (int64_t i = 0; i < n; ++i) z += exp(cand[i].s - m);
-    for (int64_t i = 0; i < n; ++i) {
-        idx[i] = (int32_t)cand[i].c;
-        w[i] = exp(cand[i].s - m) / z;
-        if (sel_score) sel_score[i] = cand[i].s;
+    if (dm->stick) {
+        /* stick-breaking in slot order: b_i = sigmoid(s_i); slot i takes the share b_i of
+           what the earlier slots left, u_i = prod_{m<i} (1 - b_m) */
+        double u = 1.0;
+        for (int64_t i = 0; i < n; ++i) {
+            const double bi = 1.0 / (1.0 + exp(-cand[i].s));
+            idx[i] = (int32_t)cand[i].c;
+            w[i] = bi * u;
+            u *= 1.0 - bi;
+            if (sel_score) sel_score[i] = cand[i].s;
+        }
+    } else {
+        double m = -INFINITY;
+        for (int64_t i = 0; i < n; ++i) m = cand[i].s > m ? cand[i].s : m;
+        double z = 0.0;
+        for (int64_t i = 0; i < n; ++i) z += exp(cand[i].s - m);
+        for (int64_t i = 0; i < n; ++i) {
+            idx[i] = (int32_t)cand[i].c;
+            w[i] = exp(cand[i].s - m) / z;
+            if (sel_score) sel_score[i] = cand[i].s;
+        }
     }
     free(cand);
     free(qsum);
@@ -183,6 +197,7 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
         double* o = (double*)malloc(sizeof(double) * d);
         double* dw = (double*)malloc(sizeof(double) * k);
         double* dsl = (double*)malloc(sizeof(double) * k);
+        double* bsb = (double*)malloc(sizeof(double) * k);
 #pragma omp for schedule(dynamic, 16)
         for (int64_t r = 0; r < ntok; ++r) {
             const int64_t t = rows ? rows[r] : r;
@@ -218,13 +233,35 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
                     }
                 }
             }
-            /* softmax chunk weights: ds_i = w_i (dw_i - sum_m w_m dw_m) */
-            double wdw = 0.0;
-            for (int i = 0; i < k; ++i) wdw += w[t * k + i] * dw[i];
+            if (dm->stick) {
+                /* stick-breaking weights w_i = b_i u_i, u_i = prod_{m<i} (1 - b_m) over the
+                   valid slots: dw_i reaches s_i through b_i directly and through the (1 - b_i)
+                   factor of every later slot, ds_i = (1 - b_i) w_i dw_i - b_i sum_{m>i} w_m dw_m */
+                double u = 1.0;
+                for (int i = 0; i < k; ++i) {
+                    const int64_t c = idx[t * k + i];
+                    if (c < 0) continue;
+                    bsb[i] = u > 0.0 ? w[t * k + i] / u : 0.0;
+                    u -= w[t * k + i];
+                }
+                double tail = 0.0;
+                for (int i = k - 1; i >= 0; --i) {
+                    const int64_t c = idx[t * k + i];
+                    if (c < 0) continue;
+                    const double wd = w[t * k + i] * dw[i];
+                    dsl[i] = (1.0 - bsb[i]) * wd - bsb[i] * tail;
+                    tail += wd;
+                }
+            } else {
+                /* softmax chunk weights: ds_i = w_i (dw_i - sum_m w_m dw_m) */
+                double wdw = 0.0;
+                for (int i = 0; i < k; ++i) wdw += w[t * k + i] * dw[i];
+                for (int i = 0; i < k; ++i)
+                    if (idx[t * k + i] >= 0) dsl[i] = w[t * k + i] * (dw[i] - wdw);
+            }
             for (int i = 0; i < k; ++i) {
                 const int64_t c = idx[t * k + i];
                 if (c < 0) continue;
-                dsl[i] = w[t * k + i] * (dw[i] - wdw);
                 /* s_i = alpha (sum_j q_j) . Kbar_c: the same term reaches every head */
                 for (int j = 0; j < h; ++j)
                     for (int e = 0; e < d; ++e)
@@ -233,6 +270,7 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
             if (ds)
                 for (int i = 0; i < k; ++i) ds[r * k + i] = dsl[i];
         }
+        free(bsb);
         free(dsl);
         free(dw);
         free(o);

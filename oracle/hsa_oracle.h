@@ -33,6 +33,9 @@ typedef struct {
     int32_t k;      /* top-k chunks per token                                          */
     double alpha;   /* selection-score scale (paper: 1/sqrt(d_g), d_g = h * d)         */
     double beta;    /* intra-chunk attention scale (1/sqrt(d))                         */
+    int32_t stick;  /* chunk weights: 0 softmax over the selected scores; 1 stick-breaking
+                       (Sec. 3.1.1): in slot order, b_i = sigmoid(s_i),
+                       w_i = b_i prod_{m<i} (1 - b_m)                                     */
 } hsa_oracle_dims;
 
 /* Mean-pooled landmark of every complete chunk: Kbar[c] = (1/S) sum_s K[c*S + s]
@@ -46,7 +49,7 @@ void hsa_oracle_landmarks(const hsa_oracle_dims* dm, const double* K, double* Kb
  * Sec. 3.1.1), padded with idx = -1, w = 0.  Weights are a softmax over the selected
  * scores.  gap (optional) receives s_(n) - s_(n+1) of the descending score order, or
  * +inf when every candidate is selected.  sel_score (optional) receives the selected
- * scores in slot order. */
+ * scores in slot order.  With dm->stick the weights are stick-breaking instead. */
 void hsa_oracle_select(const hsa_oracle_dims* dm, const double* Q, const double* Kbar,
                        int64_t ntok, const int64_t* rows, int32_t* idx, double* w,
                        double* gap, double* sel_score);
@@ -61,7 +64,8 @@ void hsa_oracle_forward(const hsa_oracle_dims* dm, const double* Q, const double
 
 /* Backward phase 1 (query side; the paper's two-phase scheme, Sec. 3.1.2): gradient of
  * sum(dO * O) w.r.t. the queries of the listed tokens, with the selection held fixed and
- * w = softmax(selected scores).  Includes the intra-chunk term and the chunk-weight term
+ * w = softmax(selected scores), or with dm->stick the stick-breaking weights (their
+ * b_i recovered from w over the valid slots in slot order: b_i = w_i / (1 - sum_{m<i} w_m)).  Includes the intra-chunk term and the chunk-weight term
  * reaching q through the scores.  dQ: [ntok, h, d]; ds (optional): [ntok, k] gradient
  * w.r.t. the selected scores (0 in padded slots). */
 void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const double* K,

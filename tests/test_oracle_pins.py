@@ -150,6 +150,27 @@ def test_weights_sum_to_one_and_k1():
     assert np.all(w1[0, 4:, 0, 0] == 1.0)
 
 
+def test_stick_breaking_weights_telescope_and_k1():
+    """Stick-breaking weights (Sec. 3.1.1): slot i takes the share sigmoid(s_i) of what the
+    earlier slots left, so the weights sum to 1 - prod(1 - sigmoid(s)) (telescoping), stay
+    below 1, and k = 1 gives sigmoid of the best score; the indices do not depend on the
+    weight rule."""
+    Q, K, _, _ = small_problem(37, L=64, h=2, d=4, S=4, k=4, mu=1.5)
+    Kb = oracle.landmarks(K, 4)
+    idx_s, w, _, ss = oracle.select(Q, Kb, 1, 4, 4, stick=True)
+    idx_m, _, _, _ = oracle.select(Q, Kb, 1, 4, 4)
+    assert np.array_equal(idx_s, idx_m)
+    sig = 1.0 / (1.0 + np.exp(-ss[0, 4:, 0]))
+    valid = idx_s[0, 4:, 0] >= 0
+    left = np.prod(np.where(valid, 1.0 - sig, 1.0), axis=-1)
+    np.testing.assert_allclose(w[0, 4:, 0].sum(-1), 1.0 - left, rtol=1e-14, atol=1e-15)
+    assert np.all(w[0, 4:, 0].sum(-1) < 1.0) and np.all(w >= 0)
+    assert np.all(w[0, :4] == 0)
+    _, w1, _, s1 = oracle.select(Q, Kb, 1, 4, 1, stick=True)
+    np.testing.assert_allclose(w1[0, 4:, 0, 0], 1.0 / (1.0 + np.exp(-s1[0, 4:, 0, 0])),
+                               rtol=1e-15, atol=0)
+
+
 # ------------------------------------------------------------------- forward ----
 
 def sdpa(q, k, v, scale, mask=None):
@@ -237,19 +258,19 @@ def test_per_chunk_key_shift_leaves_output_unchanged():
 
 # ------------------------------------------------------------------ backward ----
 
-def _loss(Q, K, V, dO, S, k, idx_ref):
-    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), K.shape[2], S, k)
+def _loss(Q, K, V, dO, S, k, idx_ref, stick=False):
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), K.shape[2], S, k, stick=stick)
     assert np.array_equal(idx, idx_ref), "selection moved under the perturbation"
     return float((oracle.forward(Q, K, V, idx, w, S) * dO).sum())
 
 
-@pytest.mark.parametrize("G", [1, 2])
-def test_backward_finite_differences(G):
+@pytest.mark.parametrize("G,stick", [(1, False), (2, False), (1, True), (2, True)])
+def test_backward_finite_differences(G, stick):
     L, h, d, S, k = 12, 2, 3, 2, 2
     Q, K, V, dO = small_problem(61 + G, L=L, h=h, d=d, S=S, k=k, mu=2.0, G=G)
-    idx, w, gap, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k)
+    idx, w, gap, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k, stick=stick)
     assert gap[np.isfinite(gap)].min() > 1e-4
-    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick)
     eps = 1e-6
     for name, X, grad in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
         num = np.zeros_like(X)
@@ -261,15 +282,17 @@ def test_backward_finite_differences(G):
             Xm[i] -= eps
             args = {"Q": Q, "K": K, "V": V}
             args[name] = Xp
-            fp = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx)
+            fp = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick)
             args[name] = Xm
-            fm = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx)
+            fm = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick)
             num[i] = (fp - fm) / (2 * eps)
         np.testing.assert_allclose(grad, num, rtol=1e-5, atol=1e-7, err_msg=name)
 
 
-def torch_hsa_forward(Q, K, V, idx, S, alpha, beta):
-    """Gather + softmax formulation (fixed idx; weights from the scores) in autograd."""
+def torch_hsa_forward(Q, K, V, idx, S, alpha, beta, stick=False):
+    """Gather + softmax formulation (fixed idx; weights from the scores) in autograd;
+    stick: weights by stick-breaking over the slots (sigmoid, then a cumulative product of
+    the complements)."""
     B, L, H, d = Q.shape
     G = K.shape[2]
     h = H // G
@@ -287,7 +310,12 @@ def torch_hsa_forward(Q, K, V, idx, S, alpha, beta):
                     continue
                 q = Q[b, t, g * h:(g + 1) * h]                   # [h, d]
                 s = alpha * (Kbar[b, sel, g] @ q.sum(0))         # [n]
-                wts = torch.softmax(s, 0)
+                if stick:
+                    bb = torch.sigmoid(s)
+                    left = torch.cumprod(torch.cat([torch.ones_like(bb[:1]), 1 - bb[:-1]]), 0)
+                    wts = bb * left
+                else:
+                    wts = torch.softmax(s, 0)
                 kk = Kc[b, sel, :, g]                             # [n, S, d]
                 vv = Vc[b, sel, :, g]
                 p = torch.softmax(beta * torch.einsum("jd,nsd->njs", q, kk), -1)
@@ -296,13 +324,14 @@ def torch_hsa_forward(Q, K, V, idx, S, alpha, beta):
     return O
 
 
-def test_backward_matches_torch_autograd():
+@pytest.mark.parametrize("stick", [False, True])
+def test_backward_matches_torch_autograd(stick):
     L, h, d, S, k, G = 40, 2, 4, 4, 3, 2
     Q, K, V, dO = small_problem(71, L=L, h=h, d=d, S=S, k=k, G=G)
-    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k)
-    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k, stick=stick)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick)
     Qt, Kt, Vt = (torch.tensor(x, requires_grad=True) for x in (Q, K, V))
-    O = torch_hsa_forward(Qt, Kt, Vt, idx, S, 1 / math.sqrt(h * d), 1 / math.sqrt(d))
+    O = torch_hsa_forward(Qt, Kt, Vt, idx, S, 1 / math.sqrt(h * d), 1 / math.sqrt(d), stick)
     np.testing.assert_allclose(O.detach().numpy(), oracle.forward(Q, K, V, idx, w, S),
                                rtol=1e-12, atol=1e-13)
     (O * torch.tensor(dO)).sum().backward()
