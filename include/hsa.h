@@ -83,8 +83,17 @@ typedef struct {
     hsa_dtype_t dtype;   /* element type of Q, K, V, O, dO, dQ, dK, dV                */
     float sm_scale;      /* beta; <= 0 selects 1/sqrt(d)                              */
     float sel_scale;     /* alpha; <= 0 selects 1/sqrt(h*d)                           */
-    uint32_t flags;      /* reserved, must be 0                                       */
+    uint32_t flags;      /* 0, or HSA_FLAG_STICK_BREAKING; other bits are unsupported */
 } hsa_attn_params_t;
+
+/* Chunk weights by stick-breaking (Sec. 3.1.1, the paper's main variant) instead of the
+ * softmax over the selected scores: in slot order (descending chunk index), b_i =
+ * sigmoid(s_i) and w_i = b_i prod_{m<i} (1 - b_m) over the valid slots, so the weights sum
+ * to less than 1.  Read by hsa_select_topk and hsa_decode (the weights they write) and by
+ * hsa_backward (the score gradient ds_i = (1 - b_i) w_i dw_i - b_i sum_{m>i} w_m dw_m, with
+ * b_i recovered from the given weights as w_i / (1 - sum_{m<i} w_m)); hsa_forward uses the
+ * weights it is given either way. */
+#define HSA_FLAG_STICK_BREAKING 2u
 
 /* Landmarks (Fig. 1; Sec. 3.1 "Chunk Selection": mean-pooled chunk representation):
  * Kbar[b, c, g, :] = (1/S) sum_{s<S} K[b, c*S + s, g, :] for chunks c in

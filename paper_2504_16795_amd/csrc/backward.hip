@@ -130,16 +130,20 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
         }
     }
     __syncthreads();
-    // softmax-weight Jacobian and the score term
+    // chunk-weight Jacobian (softmax or stick-breaking) and the score term
     float wdw = 0.f;
     for (int i = 0; i < k; ++i) {
         const int c = idx[sel + i];
         if (c >= 0 && c < ncand) wdw += w[sel + i] * dwl[i];
     }
+    auto okf = [&](int i) { const int c2 = idx[sel + i]; return c2 >= 0 && c2 < ncand; };
     for (int i = 0; i < k; ++i) {
         const int c = idx[sel + i];
         const bool ok = (c >= 0 && c < ncand);
-        const float dsi = ok ? w[sel + i] * (dwl[i] - wdw) : 0.f;
+        const float dsi = !ok ? 0.f
+                        : dm.stick ? stick_ds(i, k, [&](int m) { return w[sel + m]; },
+                                              [&](int m) { return dwl[m]; }, okf)
+                                   : w[sel + i] * (dwl[i] - wdw);
         if (tid == 0) ds_out[sel + i] = dsi;
         if (!ok) continue;
         const float* kb = Kbar + (((size_t)b * dm.C + c) * dm.G + g) * D;

@@ -479,8 +479,26 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
         if (s < canon && cs == cl) canon = s;
     }
     const float dws = __shfl(dwl, canon, 64);
-    const float wdw = group_sum<64>(valid ? wl * dws : 0.f);
-    const float dsl = valid ? wl * (dws - wdw) : 0.f;
+    const float wd = valid ? wl * dws : 0.f;
+    float dsl;
+    if (dm.stick) {
+        // stick-breaking: b = w / (1 - weight of the earlier valid slots), and
+        // ds = (1 - b) w dw - b (sum of w dw over the later valid slots)
+        float before = 0.f, tail = 0.f;
+        const float wv = valid ? wl : 0.f;
+        for (int s = 0; s < k; ++s) {
+            const float ws = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wv), s));
+            const float wds = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wd), s));
+            if (s < lane) before += ws;
+            if (s > lane) tail += wds;
+        }
+        const float u = 1.f - before;
+        const float bs = u > 0.f ? wl / u : 0.f;
+        dsl = valid ? (1.f - bs) * wd - bs * tail : 0.f;
+    } else {
+        const float wdw = group_sum<64>(wd);
+        dsl = valid ? wl * (dws - wdw) : 0.f;
+    }
     // ds summed over the slots holding the same chunk, at the first of them (the landmark
     // term of dK reads it there), in slot order
     float dsm = 0.f;

@@ -243,7 +243,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
     }
     __syncthreads();
 
-    // ---- softmax-weight Jacobian, score term, write dQ and ds ----------------------------
+    // ---- chunk-weight Jacobian, score term, write dQ and ds --------------------------------
     if (t_row >= dm.L) return;
     float wdw = 0.f;
     for (int s = 0; s < k; ++s) wdw = fmaf(sm.ow[tau * k + s], sm.dw[tau * k + s], wdw);
@@ -254,9 +254,16 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
         for (int i = 0; i < 4; ++i) out[db][i] = beta * acc[db][i];
     // score term: empty slots add 0 (their loads use chunk 0, which exists when any slot of
     // the tile is valid); loads of several slots are in flight at once
+    const bool stick = dm.stick != 0;
+    auto slot_ds = [&](int s) __attribute__((always_inline)) {
+        if (sm.oidx[tau * k + s] < 0) return 0.f;
+        if (!stick) return sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw);
+        return stick_ds(s, k, [&](int m) { return sm.ow[tau * k + m]; },
+                        [&](int m) { return sm.dw[tau * k + m]; },
+                        [&](int m) { return sm.oidx[tau * k + m] >= 0; });
+    };
     for (int s = 0; s < k; ++s) {
-        const int c = sm.oidx[tau * k + s];
-        const float dsv = (c >= 0) ? sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
+        const float dsv = slot_ds(s);
         if (grp == 0 && (row & 7) == 0)
             ds_out[(((size_t)b * dm.L + t_row) * dm.G + g) * k + s] = dsv;
     }
@@ -264,7 +271,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
 #pragma unroll 4
         for (int s = 0; s < k; ++s) {
             const int c = sm.oidx[tau * k + s];
-            const float dsv = (c >= 0) ? sm.ow[tau * k + s] * (sm.dw[tau * k + s] - wdw) : 0.f;
+            const float dsv = slot_ds(s);
             const float* kb = Kbar + (((size_t)b * dm.C + max(c, 0)) * dm.G + g) * D;
             const float coef = dm.alpha * dsv;
 #pragma unroll

@@ -13,6 +13,7 @@ struct Dims {
     int Call;       // chunks including a trailing partial one, ceil(L / S)
     float alpha;    // selection-score scale
     float beta;     // intra-chunk attention scale
+    int stick;      // chunk weights: 0 softmax of the selected scores, 1 stick-breaking
 };
 
 // bfloat16 storage type of the generic kernels (bit pattern only).
@@ -179,6 +180,85 @@ __device__ __forceinline__ uint64_t wave_max_key(uint64_t x) {
 }
 
 __host__ __device__ __forceinline__ int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Chunk weights of the n best entries of a selection list (scores ls[j] in descending score
+// order, chunks lc[j], j < n) and each entry's slot in descending chunk order (rank[j]).
+// Softmax over the n scores (Sec. 3.1.1, the ablation without stick-breaking), or, with
+// stick, stick-breaking in slot order: b_j = sigmoid(s_j), w_j = b_j times the product of
+// (1 - b_i) over the entries i in earlier slots (higher chunks).
+template <int KC>
+__device__ __forceinline__ void list_weights(const float (&ls)[KC], const int (&lc)[KC], int n,
+                                             bool stick, float (&wt)[KC], int (&rank)[KC]) {
+#pragma unroll
+    for (int j = 0; j < KC; ++j) {
+        int r = 0;
+#pragma unroll
+        for (int i = 0; i < KC; ++i) r += (i < n && lc[i] > lc[j]) ? 1 : 0;
+        rank[j] = r;
+    }
+    if (stick) {
+        float om[KC];                            // 1 - b = sigmoid(-s)
+#pragma unroll
+        for (int j = 0; j < KC; ++j) om[j] = (j < n) ? 1.f / (1.f + expf(ls[j])) : 1.f;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) {
+            float left = 1.f;
+#pragma unroll
+            for (int i = 0; i < KC; ++i) left *= (i < n && lc[i] > lc[j]) ? om[i] : 1.f;
+            wt[j] = (j < n) ? left / (1.f + expf(-ls[j])) : 0.f;
+        }
+    } else {
+        float z = 0.f;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) {
+            wt[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
+            z += wt[j];
+        }
+        const float iz = 1.f / z;
+#pragma unroll
+        for (int j = 0; j < KC; ++j) wt[j] *= iz;
+    }
+}
+
+// Stick-breaking gradient w.r.t. the score of slot s (Sec. 3.1.1 weights, see list_weights)
+// from the slots' weights w(i) and dw(i) = dL/dw_i, over the slots with ok(i): b_s is
+// recovered from the weights as w_s / (1 - sum_{m<s} w_m), and
+// ds_s = (1 - b_s) w_s dw_s - b_s sum_{m>s} w_m dw_m (b_s directly, and through the factor
+// (1 - b_s) of every later slot).
+template <class W, class DW, class OK>
+__device__ __forceinline__ float stick_ds(int s, int k, W w, DW dw, OK ok) {
+    if (!ok(s)) return 0.f;
+    float before = 0.f, tail = 0.f;
+    for (int m = 0; m < k; ++m) {
+        if (!ok(m)) continue;
+        if (m < s) before += w(m);
+        if (m > s) tail = fmaf(w(m), dw(m), tail);
+    }
+    const float u = 1.f - before;
+    const float bs = u > 0.f ? w(s) / u : 0.f;
+    return (1.f - bs) * w(s) * dw(s) - bs * tail;
+}
+
+// The same with one entry per lane (lane r holds the r-th best, (ls, lc), present when has;
+// the first n lanes hold entries): the lane's weight and slot.
+__device__ __forceinline__ void lane_weights(float ls, int lc, bool has, int n, bool stick,
+                                             float& wt, int& rank) {
+    rank = 0;
+    for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
+    if (stick) {
+        const float om = has ? 1.f / (1.f + expf(ls)) : 1.f;
+        float left = 1.f;
+        for (int j = 0; j < n; ++j) {
+            const float oj = __shfl(om, j, 64);
+            left *= (__shfl(lc, j, 64) > lc) ? oj : 1.f;
+        }
+        wt = has ? left / (1.f + expf(-ls)) : 0.f;
+    } else {
+        const float m = __shfl(ls, 0, 64);
+        const float ex = has ? expf(ls - m) : 0.f;
+        wt = ex / wave_sum(ex);
+    }
+}
 
 // RAII bracket of one kernel launch for the optional per-kernel timing (timing.hip).
 class KernelTimer {

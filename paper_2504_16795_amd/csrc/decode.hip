@@ -242,11 +242,11 @@ __global__ __launch_bounds__(kScanThreads, 2) void decode_scan(
 // Final top-k of (b, g) from the slice candidates, by wave 0 (lane i < n receives the
 // i-th best; candidates carry distinct chunk ids, so (score desc, chunk asc) is a strict
 // total order and round i takes the best candidate ranked below the winner of round
-// i - 1), then the softmax chunk weights and the descending-chunk slot order into sel_c /
-// sel_w (slots n .. k - 1 empty).
+// i - 1), then the chunk weights (softmax, or stick-breaking with stick) and the
+// descending-chunk slot order into sel_c / sel_w (slots n .. k - 1 empty).
 __device__ __forceinline__ void merge_candidates(const float* cs, const int32_t* cc, int nc,
                                                  int n, int k, int lane, int* sel_c,
-                                                 float* sel_w) {
+                                                 float* sel_w, bool stick) {
     float ls = -INFINITY;
     int lc = -1;
     float ps = INFINITY;
@@ -274,14 +274,12 @@ __device__ __forceinline__ void merge_candidates(const float* cs, const int32_t*
         ps = bs;
         pc = bc;
     }
-    const float m = __shfl(ls, 0, 64);
-    const float ex = (lane < n) ? expf(ls - m) : 0.f;
-    const float z = wave_sum(ex);
-    int rank = 0;
-    for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
+    float wt;
+    int rank;
+    lane_weights(ls, lc, lane < n, n, stick, wt, rank);
     if (lane < n) {
         sel_c[rank] = lc;
-        sel_w[rank] = ex / z;
+        sel_w[rank] = wt;
     } else if (lane < k) {
         sel_c[lane] = -1;
         sel_w[lane] = 0.f;
@@ -301,7 +299,7 @@ template <int NWV, int NPL, int NP2>
 __device__ __forceinline__ void merge_tournament(const float* __restrict__ cs,
                                                  const int32_t* __restrict__ cc, int nc, int n,
                                                  int k, uint64_t* tmp, int* sel_c,
-                                                 float* sel_w) {
+                                                 float* sel_w, bool stick) {
     constexpr int NT = NWV * 64;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float s[NPL];
@@ -347,14 +345,12 @@ __device__ __forceinline__ void merge_tournament(const float* __restrict__ cs,
         }
         const float ls = mine ? key_score(mine) : -INFINITY;
         const int lc = mine ? key_chunk(mine) : -1;
-        const float m = __shfl(ls, 0, 64);
-        const float ex = (lane < n && lc >= 0) ? expf(ls - m) : 0.f;
-        const float z = wave_sum(ex);
-        int rank = 0;
-        for (int j = 0; j < n; ++j) rank += (__shfl(lc, j, 64) > lc) ? 1 : 0;
+        float wt;
+        int rank;
+        lane_weights(ls, lc, lane < n && lc >= 0, n, stick, wt, rank);
         if (lane < n) {
             sel_c[rank] = lc;
-            sel_w[rank] = ex / z;
+            sel_w[rank] = wt;
         } else if (lane < k) {
             sel_c[lane] = -1;
             sel_w[lane] = 0.f;
@@ -368,15 +364,16 @@ __device__ __forceinline__ void merge_tournament(const float* __restrict__ cs,
 template <int NWV, int NPLMAX>
 __device__ __forceinline__ bool merge_top(const float* __restrict__ cs,
                                           const int32_t* __restrict__ cc, int nc, int n, int k,
-                                          uint64_t* tmp, int* sel_c, float* sel_w) {
+                                          uint64_t* tmp, int* sel_c, float* sel_w, bool stick) {
     constexpr int NT = NWV * 64;
     const bool s1 = NWV * n <= 64;
     if (nc <= NT) {
-        if (s1) merge_tournament<NWV, 1, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
-        else merge_tournament<NWV, 1, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+        if (s1) merge_tournament<NWV, 1, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w, stick);
+        else merge_tournament<NWV, 1, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w, stick);
     } else if (nc <= NPLMAX * NT) {
-        if (s1) merge_tournament<NWV, NPLMAX, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
-        else merge_tournament<NWV, NPLMAX, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w);
+        if (s1) merge_tournament<NWV, NPLMAX, 1>(cs, cc, nc, n, k, tmp, sel_c, sel_w, stick);
+        else merge_tournament<NWV, NPLMAX, NWV * KMAX / 64>(cs, cc, nc, n, k, tmp, sel_c, sel_w,
+                                                             stick);
     } else {
         return false;
     }
@@ -385,7 +382,7 @@ __device__ __forceinline__ bool merge_top(const float* __restrict__ cs,
 
 // Stage 2 (finish): workgroup = (slot, b, g), so the k selected chunks of a sequence are
 // attended in parallel.  Wave 0 of every workgroup merges the slice candidates into the
-// final top-k (the same deterministic merge in each), computes the softmax chunk weights and
+// final top-k (the same deterministic merge in each), computes the chunk weights and
 // the descending-chunk slot order.  The workgroup of slot i stages its chunk's K and V in
 // LDS, computes the intra-chunk softmax of the h heads and w_i P V, and stores that partial
 // output.  Stage 3 (combine) sums the partials of a (b, g) in slot order.
@@ -416,11 +413,11 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         qf[(i / D) * DP + i % D] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
     const int nc = nslices * k;
     if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
-                                             nc, n, k, mtmp, sel_c, sel_w)) {
+                                             nc, n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
         __syncthreads();
         if (wave == 0)
             merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
-                             sel_c, sel_w);
+                             sel_c, sel_w, dm.stick != 0);
         __syncthreads();
     }
     if (slot == 0 && tid < k) {
@@ -516,10 +513,10 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
         if (row >= kAttH) qB[ks] = bf16x8_t{};
     const int nc = nslices * k;
     if (!merge_top<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n,
-                                     k, mtmp, sel_c, sel_w)) {
+                                     k, mtmp, sel_c, sel_w, dm.stick != 0)) {
         if (wave == 0)
             merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
-                             sel_c, sel_w);
+                             sel_c, sel_w, dm.stick != 0);
         __syncthreads();
     }
     if (tid < k) {

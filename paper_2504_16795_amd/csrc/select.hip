@@ -1,6 +1,6 @@
 // Chunk selection + chunk weights (Sec. 3.1: the top-k chunks by the landmark score
 // s_c = alpha * (sum_j q_j) . Kbar_c over the chunks before the token's own, and their
-// softmax weights).
+// softmax or stick-breaking weights).
 //
 // Lane = token; each lane keeps its group query q~ = sum_j q_j (fp32, d registers) and a
 // running top-KC list (scores and chunk indices, registers, descending).  The landmark rows
@@ -176,25 +176,17 @@ __global__ __launch_bounds__(kThreads) void select_tiles_kernel(Dims dm, const T
     }
     if (!valid) return;
 
-    // softmax over the k best, written in descending chunk order
+    // weights of the k best, written in descending chunk order
     const int n = min(k, ncand);
     const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
-    float ex[KC];
-    float z = 0.f;
-#pragma unroll
-    for (int j = 0; j < KC; ++j) {
-        ex[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
-        z += ex[j];
-    }
-    const float iz = 1.f / z;
+    float wt[KC];
+    int rank[KC];
+    list_weights<KC>(ls, lc, n, dm.stick != 0, wt, rank);
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
         if (j < n) {
-            int rank = 0;
-#pragma unroll
-            for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
-            idx[o + rank] = lc[j];
-            w[o + rank] = ex[j] * iz;
+            idx[o + rank[j]] = lc[j];
+            w[o + rank[j]] = wt[j];
         } else if (j < k) {
             idx[o + j] = -1;
             w[o + j] = 0.f;
@@ -320,25 +312,17 @@ __global__ __launch_bounds__(kThreads) void select_split_kernel(Dims dm, const T
         }
     }
 
-    // softmax over the k best, written in descending chunk order
+    // weights of the k best, written in descending chunk order
     const int n = min(k, ncand);
     const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
-    float ex[KC];
-    float z = 0.f;
-#pragma unroll
-    for (int j = 0; j < KC; ++j) {
-        ex[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
-        z += ex[j];
-    }
-    const float iz = 1.f / z;
+    float wt[KC];
+    int rank[KC];
+    list_weights<KC>(ls, lc, n, dm.stick != 0, wt, rank);
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
         if (j < n) {
-            int rank = 0;
-#pragma unroll
-            for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
-            idx[o + rank] = lc[j];
-            w[o + rank] = ex[j] * iz;
+            idx[o + rank[j]] = lc[j];
+            w[o + rank[j]] = wt[j];
         } else if (j < k) {
             idx[o + j] = -1;
             w[o + j] = 0.f;

@@ -18,7 +18,8 @@
 // the entries it beats strictly, and a lane sees its chunks in increasing order, so equal
 // scores keep the lower chunk first).  The 4 lanes of a token merge their lists at the
 // end by a bitonic merge on 64-bit order keys (score desc, chunk asc as one integer).  The
-// k best get softmax weights and are written in descending chunk order, padded -1 / 0.
+// k best get softmax (or stick-breaking) weights and are written in descending chunk order,
+// padded -1 / 0.
 #include <cstdlib>
 
 #include "chunk_lds.h"
@@ -210,7 +211,7 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     }
     if (!valid || grp != 0) return;
 
-    // softmax over the k best, written in descending chunk order
+    // weights of the k best, written in descending chunk order
     const int n = min(k, ncand);
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
@@ -218,22 +219,14 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
         lc[j] = key[j] ? key_chunk(key[j]) : -1;
     }
     const size_t o = (((size_t)b * dm.L + t) * dm.G + g) * k;
-    float ex[KC];
-    float z = 0.f;
-#pragma unroll
-    for (int j = 0; j < KC; ++j) {
-        ex[j] = (j < n) ? expf(ls[j] - ls[0]) : 0.f;
-        z += ex[j];
-    }
-    const float iz = 1.f / z;
+    float wt[KC];
+    int rank[KC];
+    list_weights<KC>(ls, lc, n, dm.stick != 0, wt, rank);
 #pragma unroll
     for (int j = 0; j < KC; ++j) {
         if (j < n) {
-            int rank = 0;
-#pragma unroll
-            for (int i = 0; i < KC; ++i) rank += (i < n && lc[i] > lc[j]) ? 1 : 0;
-            idx[o + rank] = lc[j];
-            w[o + rank] = ex[j] * iz;
+            idx[o + rank[j]] = lc[j];
+            w[o + rank[j]] = wt[j];
         } else if (j < k) {
             idx[o + j] = -1;
             w[o + j] = 0.f;

@@ -48,16 +48,18 @@ def make_case(shape, seed, kind="iid", mu_std=0.5, gap=True):
     return inp, stats
 
 
-def oracle_reference(inp, shape, backward=True):
+def oracle_reference(inp, shape, backward=True, stick=False):
+    """The oracle's landmarks, selection, forward and (optionally) backward of one case,
+    with softmax or (stick) stick-breaking chunk weights."""
     S, k, G = shape.S, shape.k, shape.G
     ref = {"Kbar": oracle.landmarks(inp["K"], S)}
-    idx, w, gap, _ = oracle.select(inp["Q"], ref["Kbar"], G, S, k)
+    idx, w, gap, _ = oracle.select(inp["Q"], ref["Kbar"], G, S, k, stick=stick)
     ref.update(idx=idx, w=w, gap=gap)
     ref["O"] = oracle.forward(inp["Q"], inp["K"], inp["V"], idx, w, S)
     ref["O_abs"] = attention_abs(inp, idx, w, S)
     if backward:
         ref["dQ"], ref["dK"], ref["dV"] = oracle.backward(inp["Q"], inp["K"], inp["V"], idx, w,
-                                                           inp["dO"], S)
+                                                           inp["dO"], S, stick=stick)
     return ref
 
 

@@ -59,6 +59,16 @@ def test_flags_reserved(lib):
     p = P()
     p.flags = 1
     assert fwd(lib, p) == UNSUPPORTED
+    p.flags = binding.HSA_FLAG_STICK_BREAKING | 4
+    assert fwd(lib, p) == UNSUPPORTED
+
+
+def test_stick_breaking_flag_accepted(lib):
+    """The stick-breaking flag passes validation: the call then fails on the NULL Q."""
+    p = P(stick_breaking=True)
+    assert p.flags == binding.HSA_FLAG_STICK_BREAKING
+    assert fwd(lib, p, Q=None) == INVALID
+    assert "Q" in lib.hsa_attn_last_error().decode()
 
 
 def test_null_and_misaligned_pointers(lib):

@@ -171,6 +171,31 @@ def test_stick_breaking_weights_telescope_and_k1():
                                rtol=1e-15, atol=0)
 
 
+def test_stick_breaking_most_recent_chunk_breaks_first():
+    """The stick is broken in descending chunk order (Sec. 3.1.1 sorts the selected chunks
+    before the weights): the most recent selected chunk takes sigmoid of its own score,
+    whatever the others score, and the oldest takes what all the more recent ones left.
+    Scores are recomputed here with numpy from the plain definition."""
+    Q, K, _, _ = small_problem(41, L=96, h=2, d=4, S=4, k=5, mu=1.5)
+    Kb = oracle.landmarks(K, 4)
+    idx, w, _, _ = oracle.select(Q, Kb, 1, 4, 5, stick=True)
+    alpha = 1.0 / np.sqrt(2 * 4)
+    sig = lambda x: 1.0 / (1.0 + np.exp(-x))
+    checked = 0
+    for t in range(96):
+        sel = [int(c) for c in idx[0, t, 0] if c >= 0]
+        if len(sel) < 2:
+            continue
+        s = {c: alpha * Q[0, t].sum(0) @ Kb[0, c, 0] for c in sel}
+        newest, oldest = max(sel), min(sel)
+        wt = dict(zip(sel, w[0, t, 0][:len(sel)]))
+        assert abs(wt[newest] - sig(s[newest])) < 1e-14
+        rest = np.prod([1.0 - sig(s[c]) for c in sel if c != oldest])
+        assert abs(wt[oldest] - sig(s[oldest]) * rest) < 1e-14
+        checked += 1
+    assert checked > 50
+
+
 # ------------------------------------------------------------------- forward ----
 
 def sdpa(q, k, v, scale, mask=None):
