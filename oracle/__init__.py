@@ -29,7 +29,8 @@ _lib = None
 class _Dims(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int64), ("h", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("S", ctypes.c_int32), ("k", ctypes.c_int32), ("alpha", ctypes.c_double),
-                ("beta", ctypes.c_double), ("stick", ctypes.c_int32)]
+                ("beta", ctypes.c_double), ("stick", ctypes.c_int32),
+                ("off_by_one", ctypes.c_int32)]
 
 
 def build(force: bool = True) -> str:
@@ -46,8 +47,10 @@ def build(force: bool = True) -> str:
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB_PATH):
-            build(force=False)
+        srcs = (_SRC, os.path.join(_HERE, "hsa_oracle.h"))
+        if not os.path.exists(_LIB_PATH) or \
+                os.path.getmtime(_LIB_PATH) < max(os.path.getmtime(f) for f in srcs):
+            build(force=True)          # absent, or older than its sources
         lib = ctypes.CDLL(_LIB_PATH)
         P = ctypes.c_void_p
         I64 = ctypes.c_int64
@@ -79,13 +82,14 @@ def default_scales(h: int, d: int):
     return 1.0 / math.sqrt(h * d), 1.0 / math.sqrt(d)
 
 
-def dims(L, h, d, S, k, alpha=None, beta=None, stick=False) -> _Dims:
+def dims(L, h, d, S, k, alpha=None, beta=None, stick=False, off_by_one=False) -> _Dims:
     """Slice dimensions; stick selects stick-breaking chunk weights (Sec. 3.1.1) instead of
-    the softmax over the selected scores."""
+    the softmax over the selected scores; off_by_one the softmax off by one for the
+    attention inside a chunk (the paper's kernels, Sec. 3.1.2) instead of the softmax."""
     a0, b0 = default_scales(h, d)
     return _Dims(int(L), int(h), int(d), int(S), int(k),
                  float(a0 if alpha is None else alpha), float(b0 if beta is None else beta),
-                 1 if stick else 0)
+                 1 if stick else 0, 1 if off_by_one else 0)
 
 
 # ----------------------------------------------------------------------------------
@@ -198,21 +202,22 @@ def select(Q, Kbar, G: int, S: int, k: int, alpha=None, stick=False):
     return idx, w, gap, ss
 
 
-def forward(Q, K, V, idx, w, S: int, beta=None):
+def forward(Q, K, V, idx, w, S: int, beta=None, off_by_one=False):
     Q, K, V, w = map(_f64, (Q, K, V, w))
     B, L, H, G, d, h = _shape(Q, K)
     k = idx.shape[-1]
     O = np.empty((B, L, H, d))
     for b in range(B):
         for g in range(G):
-            dm = dims(L, h, d, S, k, None, beta)
+            dm = dims(L, h, d, S, k, None, beta, off_by_one=off_by_one)
             O[b, :, g * h:(g + 1) * h] = forward_slice(
                 dm, Q[b, :, g * h:(g + 1) * h], K[b, :, g], V[b, :, g],
                 np.ascontiguousarray(idx[b, :, g]), w[b, :, g])
     return O
 
 
-def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False):
+def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False,
+             off_by_one=False):
     """dQ, dK, dV (fp64) of sum(dO * O) with the selection held fixed (weights a function of
     the selected scores: softmax, or stick-breaking with stick)."""
     Q, K, V, w, dO = map(_f64, (Q, K, V, w, dO))
@@ -224,7 +229,7 @@ def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False):
     dV = np.zeros((B, L, G, d))
     for b in range(B):
         for g in range(G):
-            dm = dims(L, h, d, S, k, alpha, beta, stick)
+            dm = dims(L, h, d, S, k, alpha, beta, stick, off_by_one)
             Qs = np.ascontiguousarray(Q[b, :, g * h:(g + 1) * h])
             dOs = np.ascontiguousarray(dO[b, :, g * h:(g + 1) * h])
             Ks, Vs = np.ascontiguousarray(K[b, :, g]), np.ascontiguousarray(V[b, :, g])
@@ -240,7 +245,7 @@ def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False):
 
 
 def decode(q, Kc, Vc, Kbar_cache, cache_len: Sequence[int], S: int, k: int,
-           alpha=None, beta=None, stick=False):
+           alpha=None, beta=None, stick=False, off_by_one=False):
     """Single-token decode: q [B,H,d]; Kc, Vc [B,N,G,d]; Kbar_cache [B,Cc,G,d] (given).
 
     Returns o [B,H,d], idx [B,G,k], w [B,G,k], gap [B,G]."""
@@ -257,7 +262,7 @@ def decode(q, Kc, Vc, Kbar_cache, cache_len: Sequence[int], S: int, k: int,
         n = int(cache_len[b])
         nch = n // S
         for g in range(G):
-            dm = dims(n, h, d, S, k, alpha, beta, stick)
+            dm = dims(n, h, d, S, k, alpha, beta, stick, off_by_one)
             qs = np.ascontiguousarray(q[b, g * h:(g + 1) * h])
             # only the candidate chunks are read
             Ks = _f64(Kc[b, :nch * S, g]) if nch else np.zeros((1, d))

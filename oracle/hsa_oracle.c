@@ -9,7 +9,8 @@
  *     i.e. alpha * (sum_j q_j) . Kbar_c;
  *   - chunk weights are a softmax over the selected scores (the paper's ablation
  *     without stick-breaking), or the stick-breaking weights of the main variant (a dims
- *     flag); intra-chunk attention is the standard softmax;
+ *     flag); intra-chunk attention is the standard softmax, or (a dims flag) the softmax
+ *     off by one of the paper's kernels;
  *   - ties in the top-k go to the lower chunk index; slots are ordered by descending
  *     chunk index;
  *   - gradients treat the selected index set as constant.
@@ -134,17 +135,21 @@ void hsa_oracle_select(const hsa_oracle_dims* dm, const double* Q, const double*
 
 /* Standard softmax attention of one query row q [d] over the S keys of a chunk:
    P [S] receives the probabilities, o [d] the attended value (P V). */
+/* Attention of one query over one chunk's S keys: P = softmax(beta q K_c^T), or with
+ * dm->off_by_one P_s = exp(z_s) / (1 + sum_r exp(z_r)) (the "1" is a logit 0 that carries
+ * no value; both are evaluated after subtracting the largest logit, the 0 included);
+ * o = P V_c. */
 static void chunk_attention(const hsa_oracle_dims* dm, const double* q, const double* Kc,
                             const double* Vc, double* P, double* o) {
     const int d = dm->d, S = dm->S;
-    double m = -INFINITY;
+    double m = dm->off_by_one ? 0.0 : -INFINITY;
     for (int s = 0; s < S; ++s) {
         double acc = 0.0;
         for (int e = 0; e < d; ++e) acc += q[e] * Kc[s * d + e];
         P[s] = dm->beta * acc;
         if (P[s] > m) m = P[s];
     }
-    double z = 0.0;
+    double z = dm->off_by_one ? exp(-m) : 0.0;
     for (int s = 0; s < S; ++s) {
         P[s] = exp(P[s] - m);
         z += P[s];
@@ -217,7 +222,9 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
                     const double* qj = Q + (t * h + j) * d;
                     const double* gj = dO + (t * h + j) * d;
                     chunk_attention(dm, qj, Kc, Vc, P, o);
-                    /* D = dO_j . O_{j,i}  (equivalently sum_s P_s dP_s) */
+                    /* D = dO_j . O_{j,i}  (equivalently sum_s P_s dP_s).  The same holds off
+                       by one: its extra logit carries no value, and dP_s/dz_r is still
+                       P_s (delta_sr - P_r) */
                     double D = 0.0;
                     for (int e = 0; e < d; ++e) D += gj[e] * o[e];
                     dw[i] += D;

@@ -36,6 +36,9 @@ typedef struct {
     int32_t stick;  /* chunk weights: 0 softmax over the selected scores; 1 stick-breaking
                        (Sec. 3.1.1): in slot order, b_i = sigmoid(s_i),
                        w_i = b_i prod_{m<i} (1 - b_m)                                     */
+    int32_t off_by_one; /* intra-chunk attention: 0 softmax; 1 softmax off by one (Sec. 3.1.2
+                       kernel description), P_s = exp(z_s) / (1 + sum_r exp(z_r)), so a
+                       token may give a retrieved chunk almost no attention              */
 } hsa_oracle_dims;
 
 /* Mean-pooled landmark of every complete chunk: Kbar[c] = (1/S) sum_s K[c*S + s]
@@ -55,8 +58,9 @@ void hsa_oracle_select(const hsa_oracle_dims* dm, const double* Q, const double*
                        double* gap, double* sel_score);
 
 /* Forward for the listed tokens (Sec. 3.1.1 "Hierarchical Attention"): for every head j
- * and slot i, O_{j,i} = softmax(beta q_j K_c^T) V_c over the S keys of chunk c = idx[i];
- * O_j = sum_i w_i O_{j,i}; O = 0 for a token with no candidate chunk.
+ * and slot i, O_{j,i} = softmax(beta q_j K_c^T) V_c over the S keys of chunk c = idx[i]
+ * (softmax off by one with dm->off_by_one); O_j = sum_i w_i O_{j,i}; O = 0 for a token
+ * with no candidate chunk.
  * O has shape [ntok, h, d]. */
 void hsa_oracle_forward(const hsa_oracle_dims* dm, const double* Q, const double* K,
                         const double* V, const int32_t* idx, const double* w,

@@ -270,6 +270,47 @@ def test_all_past_selection_is_dense_two_level_softmax():
         np.testing.assert_allclose(O[0, t], ref.numpy(), rtol=1e-11, atol=1e-12)
 
 
+def test_S1_off_by_one_is_sigmoid_gated_token_attention():
+    """S = 1, h = 1, k >= L with the softmax off by one: each chunk is one key, whose
+    attention is exp(z) / (1 + exp(z)) = sigmoid(z), so O_t = sum_{c<t} softmax_c(alpha
+    q.k_c) sigmoid(beta q.k_c) v_c."""
+    L, d = 30, 8
+    Q = rnd(141, 1, L, 1, d)
+    K = rnd(142, 1, L, 1, d)
+    V = rnd(143, 1, L, 1, d)
+    idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, 1), 1, 1, L)
+    O = oracle.forward(Q, K, V, idx, w, 1, off_by_one=True)
+    q, kk, v = (torch.tensor(x[0, :, 0]) for x in (Q, K, V))
+    logits = (q @ kk.T) / math.sqrt(d)
+    assert np.all(O[0, 0] == 0)
+    for t in range(1, L):
+        ref = (torch.softmax(logits[t, :t], 0) * torch.sigmoid(logits[t, :t])) @ v[:t]
+        np.testing.assert_allclose(O[0, t, 0], ref.numpy(), rtol=1e-11, atol=1e-13)
+
+
+@pytest.mark.parametrize("key_scale", [1.0, 40.0])
+def test_k1_off_by_one_is_attention_with_a_null_key(key_scale):
+    """k = 1 with the softmax off by one equals plain attention over the chosen chunk's keys
+    plus one all-zero key (logit exactly 0) whose value is zero; key_scale = 40 puts the
+    logits far beyond exp's range on both sides."""
+    L, h, d, S = 64, 3, 8, 8
+    Q, K, V, _ = small_problem(151, L=L, h=h, d=d, S=S, k=1)
+    K = K * key_scale
+    Kb = oracle.landmarks(K, S)
+    idx, w, _, _ = oracle.select(Q, Kb, 1, S, 1)
+    O = oracle.forward(Q, K, V, idx, w, S, off_by_one=True)
+    zero = np.zeros((1, d))
+    for t in range(S, L):
+        c = int(idx[0, t, 0, 0])
+        ref = sdpa(Q[0, t], np.concatenate([zero, K[0, c * S:(c + 1) * S, 0]]),
+                   np.concatenate([zero, V[0, c * S:(c + 1) * S, 0]]), 1.0 / math.sqrt(d))
+        np.testing.assert_allclose(O[0, t], ref, rtol=1e-11, atol=1e-13)
+    # the normaliser is at least 1: a chunk can take less than its weight, never more
+    O_abs = oracle.forward(Q, K, np.abs(V), idx, w, S, off_by_one=True)
+    O_std = oracle.forward(Q, K, np.abs(V), idx, w, S)
+    assert np.all(O_abs <= O_std * (1 + 1e-12))
+
+
 def test_per_chunk_key_shift_leaves_output_unchanged():
     L, h, d, S = 64, 2, 6, 8
     Q, K, V, _ = small_problem(57, L=L, h=h, d=d, S=S, k=3)
@@ -283,19 +324,21 @@ def test_per_chunk_key_shift_leaves_output_unchanged():
 
 # ------------------------------------------------------------------ backward ----
 
-def _loss(Q, K, V, dO, S, k, idx_ref, stick=False):
+def _loss(Q, K, V, dO, S, k, idx_ref, stick=False, off1=False):
     idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), K.shape[2], S, k, stick=stick)
     assert np.array_equal(idx, idx_ref), "selection moved under the perturbation"
-    return float((oracle.forward(Q, K, V, idx, w, S) * dO).sum())
+    return float((oracle.forward(Q, K, V, idx, w, S, off_by_one=off1) * dO).sum())
 
 
-@pytest.mark.parametrize("G,stick", [(1, False), (2, False), (1, True), (2, True)])
-def test_backward_finite_differences(G, stick):
+@pytest.mark.parametrize("G,stick,off1", [(1, False, False), (2, False, False),
+                                          (1, True, False), (2, True, False),
+                                          (2, False, True), (1, True, True)])
+def test_backward_finite_differences(G, stick, off1):
     L, h, d, S, k = 12, 2, 3, 2, 2
     Q, K, V, dO = small_problem(61 + G, L=L, h=h, d=d, S=S, k=k, mu=2.0, G=G)
     idx, w, gap, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k, stick=stick)
     assert gap[np.isfinite(gap)].min() > 1e-4
-    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick, off_by_one=off1)
     eps = 1e-6
     for name, X, grad in (("Q", Q, dQ), ("K", K, dK), ("V", V, dV)):
         num = np.zeros_like(X)
@@ -307,17 +350,18 @@ def test_backward_finite_differences(G, stick):
             Xm[i] -= eps
             args = {"Q": Q, "K": K, "V": V}
             args[name] = Xp
-            fp = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick)
+            fp = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick, off1)
             args[name] = Xm
-            fm = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick)
+            fm = _loss(args["Q"], args["K"], args["V"], dO, S, k, idx, stick, off1)
             num[i] = (fp - fm) / (2 * eps)
         np.testing.assert_allclose(grad, num, rtol=1e-5, atol=1e-7, err_msg=name)
 
 
-def torch_hsa_forward(Q, K, V, idx, S, alpha, beta, stick=False):
+def torch_hsa_forward(Q, K, V, idx, S, alpha, beta, stick=False, off1=False):
     """Gather + softmax formulation (fixed idx; weights from the scores) in autograd;
     stick: weights by stick-breaking over the slots (sigmoid, then a cumulative product of
-    the complements)."""
+    the complements); off1: the chunk's softmax taken over its logits and one extra 0,
+    whose column is then dropped."""
     B, L, H, d = Q.shape
     G = K.shape[2]
     h = H // G
@@ -343,21 +387,28 @@ def torch_hsa_forward(Q, K, V, idx, S, alpha, beta, stick=False):
                     wts = torch.softmax(s, 0)
                 kk = Kc[b, sel, :, g]                             # [n, S, d]
                 vv = Vc[b, sel, :, g]
-                p = torch.softmax(beta * torch.einsum("jd,nsd->njs", q, kk), -1)
+                z = beta * torch.einsum("jd,nsd->njs", q, kk)
+                if off1:
+                    p = torch.softmax(torch.cat([torch.zeros_like(z[..., :1]), z], -1), -1)[..., 1:]
+                else:
+                    p = torch.softmax(z, -1)
                 o = torch.einsum("njs,nsd->njd", p, vv)
                 O[b, t, g * h:(g + 1) * h] = (wts[:, None, None] * o).sum(0)
     return O
 
 
-@pytest.mark.parametrize("stick", [False, True])
-def test_backward_matches_torch_autograd(stick):
+@pytest.mark.parametrize("stick,off1", [(False, False), (True, False), (False, True),
+                                        (True, True)])
+def test_backward_matches_torch_autograd(stick, off1):
     L, h, d, S, k, G = 40, 2, 4, 4, 3, 2
     Q, K, V, dO = small_problem(71, L=L, h=h, d=d, S=S, k=k, G=G)
     idx, w, _, _ = oracle.select(Q, oracle.landmarks(K, S), G, S, k, stick=stick)
-    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick, off_by_one=off1)
     Qt, Kt, Vt = (torch.tensor(x, requires_grad=True) for x in (Q, K, V))
-    O = torch_hsa_forward(Qt, Kt, Vt, idx, S, 1 / math.sqrt(h * d), 1 / math.sqrt(d), stick)
-    np.testing.assert_allclose(O.detach().numpy(), oracle.forward(Q, K, V, idx, w, S),
+    O = torch_hsa_forward(Qt, Kt, Vt, idx, S, 1 / math.sqrt(h * d), 1 / math.sqrt(d), stick,
+                          off1)
+    np.testing.assert_allclose(O.detach().numpy(),
+                               oracle.forward(Q, K, V, idx, w, S, off_by_one=off1),
                                rtol=1e-12, atol=1e-13)
     (O * torch.tensor(dO)).sum().backward()
     np.testing.assert_allclose(dQ, Qt.grad.numpy(), rtol=1e-10, atol=1e-12)
@@ -389,14 +440,15 @@ def test_backward_row_and_chunk_subsets_match_full():
 
 # -------------------------------------------------------------------- decode ----
 
+@pytest.mark.parametrize("off1", [False, True])
 @pytest.mark.parametrize("t", [64, 67, 100, 31])
-def test_decode_equals_forward_row(t):
+def test_decode_equals_forward_row(t, off1):
     L, h, d, S, k, G = 128, 2, 8, 8, 3, 2
     Q, K, V, _ = small_problem(81, L=L, h=h, d=d, S=S, k=k, G=G)
     Kb = oracle.landmarks(K, S)
     idx, w, _, _ = oracle.select(Q, Kb, G, S, k)
-    O = oracle.forward(Q, K, V, idx, w, S)
-    o, di, dw, _ = oracle.decode(Q[:, t], K, V, Kb, [t], S, k)
+    O = oracle.forward(Q, K, V, idx, w, S, off_by_one=off1)
+    o, di, dw, _ = oracle.decode(Q[:, t], K, V, Kb, [t], S, k, off_by_one=off1)
     assert np.array_equal(di[0], idx[0, t])
     np.testing.assert_allclose(dw[0], w[0, t], rtol=1e-13, atol=1e-15)
     np.testing.assert_allclose(o[0], O[0, t], rtol=1e-12, atol=1e-14)
