@@ -83,7 +83,7 @@ typedef struct {
     hsa_dtype_t dtype;   /* element type of Q, K, V, O, dO, dQ, dK, dV                */
     float sm_scale;      /* beta; <= 0 selects 1/sqrt(d)                              */
     float sel_scale;     /* alpha; <= 0 selects 1/sqrt(h*d)                           */
-    uint32_t flags;      /* 0, or HSA_FLAG_STICK_BREAKING; other bits are unsupported */
+    uint32_t flags;      /* HSA_FLAG_* bits (0: the defaults); other bits unsupported */
 } hsa_attn_params_t;
 
 /* Chunk weights by stick-breaking (Sec. 3.1.1, the paper's main variant) instead of the
@@ -94,6 +94,14 @@ typedef struct {
  * b_i recovered from the given weights as w_i / (1 - sum_{m<i} w_m)); hsa_forward uses the
  * weights it is given either way. */
 #define HSA_FLAG_STICK_BREAKING 2u
+
+/* Attention inside a chunk by the softmax off by one (the normaliser of the paper's
+ * kernels, Sec. 3.1.2) instead of the softmax: P_s = exp(z_s) / (1 + sum_r exp(z_r)), an
+ * extra logit 0 that carries no value, so a token can give a retrieved chunk almost no
+ * attention.  Read by hsa_forward, hsa_backward and hsa_decode (the attention inside
+ * every selected chunk); hsa_select_topk does not depend on it.  The backward keeps its
+ * form (dZ = w P (dP - D), D = dO . O_chunk), with P from this normaliser. */
+#define HSA_FLAG_SOFTMAX_OFF_BY_ONE 4u
 
 /* Landmarks (Fig. 1; Sec. 3.1 "Chunk Selection": mean-pooled chunk representation):
  * Kbar[b, c, g, :] = (1/S) sum_{s<S} K[b, c*S + s, g, :] for chunks c in

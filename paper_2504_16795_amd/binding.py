@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libhsa_mi355x.so")
 HSA_DTYPE_F32, HSA_DTYPE_BF16 = 0, 1
 HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE = range(5)
 HSA_FLAG_STICK_BREAKING = 2
+HSA_FLAG_SOFTMAX_OFF_BY_ONE = 4
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP"}
 
 _lib = None
@@ -88,9 +89,10 @@ def _dtype_code(t: torch.dtype) -> int:
 
 
 def make_params(B, L, H, G, d, S, k, dtype, sm_scale=0.0, sel_scale=0.0,
-                stick_breaking=False) -> HsaParams:
+                stick_breaking=False, off_by_one=False) -> HsaParams:
     code = dtype if isinstance(dtype, int) else _dtype_code(dtype)
-    flags = HSA_FLAG_STICK_BREAKING if stick_breaking else 0
+    flags = (HSA_FLAG_STICK_BREAKING if stick_breaking else 0) | \
+        (HSA_FLAG_SOFTMAX_OFF_BY_ONE if off_by_one else 0)
     return HsaParams(int(B), int(L), int(H), int(G), int(d), int(S), int(k), code,
                      float(sm_scale), float(sel_scale), flags)
 
@@ -176,8 +178,10 @@ def hsa_select_topk(Q: torch.Tensor, Kbar: torch.Tensor, G: int, S: int, k: int,
 def hsa_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch.Tensor,
                 w: torch.Tensor, S: int, sm_scale: float = 0.0,
                 out: Optional[torch.Tensor] = None,
-                workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """O [B, L, H, d] = sum_i w_i softmax(beta q K_c^T) V_c over the selected chunks."""
+                workspace: Optional[torch.Tensor] = None,
+                off_by_one: bool = False) -> torch.Tensor:
+    """O [B, L, H, d] = sum_i w_i softmax(beta q K_c^T) V_c over the selected chunks (the
+    softmax off by one with off_by_one)."""
     B, L, H, d = Q.shape
     G, k = K.shape[2], idx.shape[-1]
     _need(Q, "Q")
@@ -185,7 +189,7 @@ def hsa_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch.Te
     _need(V, "V", (B, L, G, d), Q.dtype, Q.device)
     _need(idx, "idx", (B, L, G, k), torch.int32, Q.device)
     _need(w, "w", (B, L, G, k), torch.float32, Q.device)
-    p = make_params(B, L, H, G, d, S, k, Q.dtype, sm_scale)
+    p = make_params(B, L, H, G, d, S, k, Q.dtype, sm_scale, off_by_one=off_by_one)
     if out is None:
         out = torch.empty_like(Q)
     _need(out, "O", Q.shape, Q.dtype, Q.device)
@@ -197,9 +201,10 @@ def hsa_forward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, idx: torch.Te
 
 def hsa_backward(Q, K, V, Kbar, idx, w, dO, S: int, sm_scale: float = 0.0,
                  sel_scale: float = 0.0, out=None, workspace: Optional[torch.Tensor] = None,
-                 stick_breaking: bool = False):
+                 stick_breaking: bool = False, off_by_one: bool = False):
     """(dQ, dK, dV) of sum(dO * O) with the selection held fixed; stick_breaking states
-    how w was formed from the scores (the score term of the gradient depends on it)."""
+    how w was formed from the scores (the score term of the gradient depends on it),
+    off_by_one which softmax the forward took inside a chunk."""
     B, L, H, d = Q.shape
     G, k = K.shape[2], idx.shape[-1]
     for t, n, shp in ((Q, "Q", None), (K, "K", (B, L, G, d)), (V, "V", (B, L, G, d)),
@@ -208,7 +213,8 @@ def hsa_backward(Q, K, V, Kbar, idx, w, dO, S: int, sm_scale: float = 0.0,
     _need(Kbar, "Kbar", (B, L // S, G, d), torch.float32, Q.device)
     _need(idx, "idx", (B, L, G, k), torch.int32, Q.device)
     _need(w, "w", (B, L, G, k), torch.float32, Q.device)
-    p = make_params(B, L, H, G, d, S, k, Q.dtype, sm_scale, sel_scale, stick_breaking)
+    p = make_params(B, L, H, G, d, S, k, Q.dtype, sm_scale, sel_scale, stick_breaking,
+                    off_by_one)
     if out is None:
         out = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
     dQ, dK, dV = out
@@ -222,7 +228,7 @@ def hsa_backward(Q, K, V, Kbar, idx, w, dO, S: int, sm_scale: float = 0.0,
 def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
                cache_len: Optional[torch.Tensor] = None, sm_scale: float = 0.0,
                sel_scale: float = 0.0, out=None, workspace: Optional[torch.Tensor] = None,
-               stick_breaking: bool = False):
+               stick_breaking: bool = False, off_by_one: bool = False):
     """One query token per sequence at position cache_len[b]: (o [B,H,d], idx, w [B,G,k])."""
     B, H, d = q.shape
     Ncap, G = Kcache.shape[1], Kcache.shape[2]
@@ -232,7 +238,8 @@ def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
     _need(Kbar_cache, "Kbar_cache", (B, Ncap // S, G, d), None, q.device)
     if cache_len is not None:
         _need(cache_len, "cache_len", (B,), torch.int32, q.device)
-    p = make_params(B, Ncap, H, G, d, S, k, q.dtype, sm_scale, sel_scale, stick_breaking)
+    p = make_params(B, Ncap, H, G, d, S, k, q.dtype, sm_scale, sel_scale, stick_breaking,
+                    off_by_one)
     if out is None:
         out = (torch.empty_like(q), torch.empty((B, G, k), dtype=torch.int32, device=q.device),
                torch.empty((B, G, k), dtype=torch.float32, device=q.device))

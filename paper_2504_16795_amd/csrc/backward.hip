@@ -102,9 +102,10 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
                 }
                 dp[u] = bb;
             }
-            const float m = wave_max(fmaxf(z[0], z[1]));
+            float m = wave_max(fmaxf(z[0], z[1]));
+            if (dm.off1) m = fmaxf(m, 0.f);
             float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
-            const float inv = 1.f / wave_sum(p0 + p1);
+            const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
             p0 *= inv;
             p1 *= inv;
             const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
@@ -277,9 +278,10 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
                     }
                     dp[u] = bb;
                 }
-                const float m = wave_max(fmaxf(z[0], z[1]));
+                float m = wave_max(fmaxf(z[0], z[1]));
+                if (dm.off1) m = fmaxf(m, 0.f);
                 float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
-                const float inv = 1.f / wave_sum(p0 + p1);
+                const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
                 p0 *= inv;
                 p1 *= inv;
                 const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);

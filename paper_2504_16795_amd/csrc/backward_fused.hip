@@ -58,8 +58,8 @@ constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied p
 constexpr int kStoresPerStep = 3;   // global stores per lane of one dq step (2 partial, 1 dw)
 
 // target of the stores of padding rows (a group's missing tokens), so that every wave issues
-// the same number of stores per group: 8 rows of partial dQ, then 64 floats
-constexpr size_t kTrashBytes = HG * D * 2 + 64 * 4;
+// the same number of stores per group: 8 rows of partial dQ, then 64 float pairs
+constexpr size_t kTrashBytes = HG * D * 2 + 64 * 8;
 
 struct FusedWs {
     size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash,
@@ -81,7 +81,8 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     l.part = l.pairsel + align256((nsel + 4 * R) * 4);
     l.dkraw = l.part + align256(nsel * HG * D * 2);
     l.dw = l.dkraw + align256(nrow * D * 4);
-    l.ds = l.dw + align256(nsel * 4);
+    // dw per (token, slot); off by one, per (token, slot, head) the pair {dw, sum_keys dZ}
+    l.ds = l.dw + align256(nsel * 4 * (dm.off1 ? 2 * HG : 1));
     l.qsum = l.ds + align256(nsel * 4);
     l.pk = l.qsum + align256(nrow * D * 2);
     l.pv = l.pk + (size_t)kStreamWGs * 2 * CS * D * 4;
@@ -101,7 +102,8 @@ struct SmemF {
     FStage st[FNST];                // stage 0 holds the chunk's K rows while K^T is read
     __bf16 dzt[2][CS * 32];         // dZ^T of a group, hi and lo parts: [key][row], see zpos
     float stat[NW][3][32];          // per wave and row: m_w, sum exp, sum exp * dP
-    float fac[NW][2][32];           // per wave and row: P scale of the wave's keys, D
+    float fac[NW][3][32];           // per wave and row: P scale of the wave's keys, D, and
+                                    // (off by one) the mean over the keys of dZ / W
     int list[FLIST];                // token; then its first Q / dO row, (b L + t) H + g h
     int lsel[FLIST];                // (token, first slot holding c): ((b L + t) G + g) k + s
     float lw[FLIST];                // the token's total weight for c
@@ -132,6 +134,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     const size_t rowstride = (size_t)dm.G * D;
     const float beta = dm.beta;
     const float sl2 = beta * 1.44269504088896341f;
+    const bool off1 = dm.off1 != 0;
+    const float mfloor = off1 ? 0.f : -INFINITY;
 
     // LDS offsets of the chunk-swizzled tiles (see chunk_lds.h), from per-lane bases:
     //   row reads, d step ks:        kb0 + 32 (ks ^ ks_x)       (+ 2048 per 16-row block)
@@ -209,9 +213,10 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
 
         // partial dQ^T of group gj from the staged dZ^T (all waves' keys), stored per (token,
         // slot, head): rows 16 rt + (lane & 15), d = 32 wave + 8 grp + (0..7); then
-        // the group's dw (wave 0, carried from its combine step).  Exactly kStoresPerStep
-        // stores per lane: rows of missing tokens go to the trash area.
-        auto dq_step = [&](int gj, int nl, float dtok) __attribute__((always_inline)) {
+        // the group's dw (wave 0, carried from its combine step), off by one with the row's
+        // sum of dZ over the keys (sig, times W here).  Exactly kStoresPerStep stores per
+        // lane: rows of missing tokens go to the trash area.
+        auto dq_step = [&](int gj, int nl, float dtok, float sig) __attribute__((always_inline)) {
             f32x4_t qa[2][2];
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt) qa[dt][0] = qa[dt][1] = zero4();
@@ -238,7 +243,15 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                              f2bf(qa[0][rt][3]), f2bf(qa[1][rt][0]), f2bf(qa[1][rt][1]),
                              f2bf(qa[1][rt][2]), f2bf(qa[1][rt][3])};
             }
-            {
+            if (off1) {
+                // lane (token, head) of wave 0: {dw, W sum_keys dZ} of that head's row
+                const int li = gj * 4 + ((lane & 31) >> 3);
+                const int so = (wave == 0 && lane < 32 && li < nl) ? sm.lsel[li] : -1;
+                float2* dst = so >= 0 ? reinterpret_cast<float2*>(dwc) + (size_t)(uint32_t)so * HG +
+                                            (lane & 7)
+                                      : reinterpret_cast<float2*>(tdw) + lane;
+                *dst = float2{dtok, so >= 0 ? sm.lw[li] * sig : 0.f};
+            } else {
                 const int li = gj * 4 + ((lane & 31) >> 3);
                 const int so = (wave == 0 && lane < 32 && (lane & 7) == 0 && li < nl)
                                    ? sm.lsel[li] : -1;
@@ -291,7 +304,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
 #pragma unroll
             for (int u = 0; u < FNST - 1; ++u)
                 if (u < ngroups) issue(u, nl);
-            float dtok_pend = 0.f;
+            float dtok_pend = 0.f, sig_pend = 0.f;
             for (int gi = 0; gi < ngroups; ++gi) {
                 // Group gi has landed once only the memory operations issued after its copies
                 // remain: the previous iteration's dq stores (when it ran one) and the next
@@ -304,7 +317,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 else wait_loads_le<0>();
                 lds_wait();
                 barrier_keep_copies();   // stage gi landed, dZ^T of gi - 1 complete, stage gi - 1 free
-                if (gi > 0) dq_step(gi - 1, nl, dtok_pend);
+                if (gi > 0) dq_step(gi - 1, nl, dtok_pend, sig_pend);
                 if (gi + FNST - 1 < ngroups) issue(gi + FNST - 1, nl);
                 const FStage& st = sm.st[gi % FNST];
 
@@ -350,8 +363,10 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                     lv[w2] = sm.stat[w2][1][r32];
                     nv[w2] = sm.stat[w2][2][r32];
                 }
-                const float M = fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3]));
-                float lsum = 0.f, nsum = 0.f, aown = 0.f;
+                // off by one, the extra logit 0 joins the maximum and the sum (its value,
+                // and so its share of D, is zero)
+                const float M = fmaxf(fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3])), mfloor);
+                float lsum = off1 ? fast_exp2(-M) : 0.f, nsum = 0.f, aown = 0.f;
     #pragma unroll
                 for (int w2 = 0; w2 < NW; ++w2) {
                     const float a = fast_exp2(mv[w2] - M);
@@ -361,13 +376,18 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 }
                 const float inv = __builtin_amdgcn_rcpf(lsum);
                 const float Drow = nsum * inv;
+                // off by one, a row's dZ sums over the keys to W D P0 (P0: the extra logit's
+                // probability) instead of 0
+                const float dzsum = off1 ? Drow * fast_exp2(-M) * inv : 0.f;
                 if (lane < 32) {
                     sm.fac[wave][0][r32] = aown * inv;
                     sm.fac[wave][1][r32] = Drow;
+                    sm.fac[wave][2][r32] = dzsum * (1.f / CS);
                 }
                 // dw of each token of the group: sum of D over its 8 heads (rows 8 tau .. 8 tau + 7),
                 // stored with the group's partial dQ
                 dtok_pend = group_sum<8>(Drow);
+                sig_pend = dzsum;
                 // back in the C layout (the wave's own LDS writes, read in order)
                 f32x4_t fv[2], dv[2], pw[2], dz[2];
     #pragma unroll
@@ -387,9 +407,24 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                     }
                 }
                 // every product below accumulates over many rows (dV, dK) or cancels (dQ, since
-                // sum_keys dZ = 0): W P and dZ enter as bf16 hi/lo pairs
+                // sum_keys dZ = 0): W P and dZ enter as bf16 hi/lo pairs.  Off by one, dZ^T for
+                // dQ is centred over the keys (its mean W D P0 / S taken out, so the partial
+                // keeps cancelling; dQ completion adds W D P0 Kbar_c back in fp32), while dK
+                // takes dZ itself.
                 bf16x8_t pvh, pvl, dzh, dzl;
                 split8(pw[0], pw[1], pvh, pvl);
+                auto centre = [&](float sgn) __attribute__((always_inline)) {
+    #pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) {
+                        const int li = gi * 4 + 2 * rb + (grp >> 1);
+                        const float wt = li < nl ? sgn * sm.lw[li] : 0.f;
+                        const f32x4_t cv =
+                            *reinterpret_cast<const f32x4_t*>(&sm.fac[wave][2][16 * rb + 4 * grp]);
+    #pragma unroll
+                        for (int i = 0; i < 4; ++i) dz[rb][i] = fmaf(wt, cv[i], dz[rb][i]);
+                    }
+                };
+                if (off1) centre(-1.f);
                 split8(dz[0], dz[1], dzh, dzl);
                 {
                     // dZ^T to LDS: key 16 wave + row, rows 16 rb + 4 grp .. +3 = unit 4 rb + grp
@@ -402,6 +437,10 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                         bf16x4_t{dzl[0], dzl[1], dzl[2], dzl[3]};
                     *reinterpret_cast<bf16x4_t*>(sm.dzt[1] + zpos(j, 4 + grp)) =
                         bf16x4_t{dzl[4], dzl[5], dzl[6], dzl[7]};
+                }
+                if (off1) {
+                    centre(1.f);
+                    split8(dz[0], dz[1], dzh, dzl);
                 }
     #pragma unroll
                 for (int db = 0; db < 8; ++db) {
@@ -416,7 +455,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
             }
             lds_wait();
             barrier_keep_copies();   // dZ^T of the batch's last group complete
-            dq_step(ngroups - 1, nl, dtok_pend);
+            dq_step(ngroups - 1, nl, dtok_pend, sig_pend);
         }
         // the chunk's key-side sums: final when this workgroup covered all its groups
         float* ok = whole ? dkraw : pk + ((size_t)lid * 2 + pslot) * CS * D;
@@ -470,7 +509,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     if (lane < k) {
         cl = idx[so + lane];
         wl = w[so + lane];
-        dwl = dwc[so + lane];
+        dwl = dm.off1 ? dwc[(so + lane) * (2 * HG)] : dwc[so + lane];
     }
     const bool valid = lane < k && cl >= 0 && cl < ncand;
     int canon = lane;                       // first slot holding the same chunk
@@ -518,7 +557,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     for (int s0 = 0; s0 < k; s0 += 4) {
         bf16x8_t pv[4][2];
         float4 kv[4][4];
-        float coef[4];
+        float coef[4], sg[4];
         int use[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -534,6 +573,8 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
             } else {
                 pv[j][0] = pv[j][1] = bf16x8_t{};
             }
+            // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
+            sg[j] = (use[j] && dm.off1) ? dwc[((so + s) * HG + head) * 2 + 1] : 0.f;
             const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
             const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
 #pragma unroll
@@ -553,6 +594,10 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
                 lmk[4 * v + 1] = fmaf(coef[j], kv[j][v].y, lmk[4 * v + 1]);
                 lmk[4 * v + 2] = fmaf(coef[j], kv[j][v].z, lmk[4 * v + 2]);
                 lmk[4 * v + 3] = fmaf(coef[j], kv[j][v].w, lmk[4 * v + 3]);
+                acc[4 * v + 0] = fmaf(sg[j], kv[j][v].x, acc[4 * v + 0]);
+                acc[4 * v + 1] = fmaf(sg[j], kv[j][v].y, acc[4 * v + 1]);
+                acc[4 * v + 2] = fmaf(sg[j], kv[j][v].z, acc[4 * v + 2]);
+                acc[4 * v + 3] = fmaf(sg[j], kv[j][v].w, acc[4 * v + 3]);
             }
         }
     }

@@ -142,6 +142,8 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
     const size_t bgbase = (size_t)b * dm.L * rowstride + (size_t)g * D;
     const float beta = dm.beta;
     const float sl2 = beta * 1.44269504088896341f;
+    const bool off1 = dm.off1 != 0;
+    const float mfloor = off1 ? 0.f : -INFINITY;
     auto issue = [&](int u) __attribute__((always_inline)) {
         const size_t base = bgbase + (size_t)sm.ulist[u] * S * rowstride;
         chunk_to_lds<S, NW>(K + base, rowstride, sm.st[u % NST].k, wave, lane);
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-            m = col_max(m);
+            m = fmaxf(col_max(m), mfloor);      // off by one: the extra logit 0 included
             const float msl = m * sl2;
             // unnormalised probabilities Pu = exp(beta (z - m)), their sum and sum Pu dP
             float ssum = 0.f, dsu = 0.f;
@@ -199,7 +201,7 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
                     ssum += z[mb][i];
                     dsu = fmaf(z[mb][i], dp[mb][i], dsu);
                 }
-            ssum = col_sum(ssum);
+            ssum = col_sum(ssum) + (off1 ? fast_exp2(-msl) : 0.f);
             const float inv = __builtin_amdgcn_rcpf(ssum);
             const float dsum = col_sum(dsu) * inv;                    // D of this row
             // dZ = w P (dP - D), fed as the B operand of dQ^T += K^T dZ^T.  sum_s dZ_s = 0,

@@ -14,6 +14,9 @@ struct Dims {
     float alpha;    // selection-score scale
     float beta;     // intra-chunk attention scale
     int stick;      // chunk weights: 0 softmax of the selected scores, 1 stick-breaking
+    int off1;       // attention inside a chunk: 0 softmax, 1 softmax off by one (an extra
+                    // logit 0 with no value: the row maximum covers it, and the normaliser
+                    // gains exp(0 - max))
 };
 
 // bfloat16 storage type of the generic kernels (bit pattern only).

@@ -453,10 +453,11 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         for (int j = wave; j < h; j += NW) {
             const float z0 = lane < S ? pz[j * SMAX + lane] : -INFINITY;
             const float z1 = lane + 64 < S ? pz[j * SMAX + lane + 64] : -INFINITY;
-            const float m = wave_max(fmaxf(z0, z1));
+            float m = wave_max(fmaxf(z0, z1));
+            if (dm.off1) m = fmaxf(m, 0.f);
             const float e0 = lane < S ? expf(z0 - m) : 0.f;
             const float e1 = lane + 64 < S ? expf(z1 - m) : 0.f;
-            const float scale = wi / wave_sum(e0 + e1);
+            const float scale = wi / (wave_sum(e0 + e1) + (dm.off1 ? expf(-m) : 0.f));
             if (lane < S) pz[j * SMAX + lane] = e0 * scale;
             if (lane + 64 < S) pz[j * SMAX + lane + 64] = e1 * scale;
         }
@@ -530,6 +531,8 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     int toff[8];
     tr_read_offsets(lane, toff);
     const float sl2 = dm.beta * 1.44269504088896341f;
+    const bool off1 = dm.off1 != 0;                  // softmax off by one
+    const float mfloor = off1 ? 0.f : -INFINITY;
     const size_t rowstride = (size_t)dm.G * DD;
     __bf16* stage = vst[wave];
     for (int slot = wave; slot < n; slot += NWV) {
@@ -559,7 +562,7 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-        const float msl = col_max(m) * sl2;
+        const float msl = fmaxf(col_max(m), mfloor) * sl2;
         float ssum = 0.f;
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
@@ -568,7 +571,8 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
                 z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
                 ssum += z[mb][i];
             }
-        const float scale = wi * __builtin_amdgcn_rcpf(col_sum(ssum));
+        const float scale =
+            wi * __builtin_amdgcn_rcpf(col_sum(ssum) + (off1 ? fast_exp2(-msl) : 0.f));
         // O^T += V^T P^T, once the copies have landed
         wait_loads_le<0>();
 #pragma unroll

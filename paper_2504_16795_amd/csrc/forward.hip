@@ -80,9 +80,10 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
                     z[u] = -INFINITY;
                 }
             }
-            const float m = wave_max(fmaxf(z[0], z[1]));
+            float m = wave_max(fmaxf(z[0], z[1]));
+            if (dm.off1) m = fmaxf(m, 0.f);
             const float e0 = expf(z[0] - m), e1 = expf(z[1] - m);
-            const float scale = wi / wave_sum(e0 + e1);
+            const float scale = wi / (wave_sum(e0 + e1) + (dm.off1 ? expf(-m) : 0.f));
             if (lane < S) p[j * SMAX + lane] = e0 * scale;
             if (lane + 64 < S) p[j * SMAX + lane + 64] = e1 * scale;
         }

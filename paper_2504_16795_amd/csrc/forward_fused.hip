@@ -89,6 +89,8 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     const int k = dm.k;
     const size_t rowstride = (size_t)dm.G * D;
     const float sl2 = dm.beta * 1.44269504088896341f;
+    const bool off1 = dm.off1 != 0;
+    const float mfloor = off1 ? 0.f : -INFINITY;
 
     // LDS offsets of the row reads of a chunk-swizzled tile (chunk_lds.h), d step ks:
     // kb0 + 32 (ks ^ ks_x) (+ 2048 per 16-row block)
@@ -271,8 +273,9 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                         mv[w2] = sm.stat[w2][0][r32];
                         lv[w2] = sm.stat[w2][1][r32];
                     }
-                    const float M = fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3]));
-                    float lsum = 0.f, aown = 0.f;
+                    // off by one, the extra logit 0 joins the maximum and the sum
+                    const float M = fmaxf(fmaxf(fmaxf(mv[0], mv[1]), fmaxf(mv[2], mv[3])), mfloor);
+                    float lsum = off1 ? fast_exp2(-M) : 0.f, aown = 0.f;
 #pragma unroll
                     for (int w2 = 0; w2 < NW; ++w2) {
                         const float a = fast_exp2(mv[w2] - M);

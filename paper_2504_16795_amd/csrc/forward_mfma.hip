@@ -128,6 +128,9 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
     row_read_offsets(lane, koff);
     tr_read_offsets(lane, toff);
     const float sl2 = dm.beta * 1.44269504088896341f;   // beta * log2(e)
+    // softmax off by one: the row maximum also covers the extra logit 0
+    const bool off1 = dm.off1 != 0;
+    const float mfloor = off1 ? 0.f : -INFINITY;
 
 #pragma unroll
     for (int u = 0; u < NST - 1; ++u)
@@ -163,7 +166,7 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
             for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-            const float msl = col_max(m) * sl2;
+            const float msl = fmaxf(col_max(m), mfloor) * sl2;
             float ssum = 0.f;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
@@ -172,7 +175,7 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
                     z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
                     ssum += z[mb][i];
                 }
-            ssum = col_sum(ssum);
+            ssum = col_sum(ssum) + (off1 ? fast_exp2(-msl) : 0.f);
             const float scale = wl * __builtin_amdgcn_rcpf(ssum);
             // O^T += V^T P^T
 #pragma unroll

@@ -50,9 +50,10 @@ hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
     if (p->topk < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "topk must be >= 1");
     if (p->chunk < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "chunk must be >= 1");
     if (p->head_dim < 1) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "head_dim must be >= 1");
-    if ((p->flags & ~HSA_FLAG_STICK_BREAKING) != 0)
-        return fail(HSA_ATTN_ERR_UNSUPPORTED, "flags 0x%x: only HSA_FLAG_STICK_BREAKING is supported",
-                    p->flags);
+    if ((p->flags & ~(HSA_FLAG_STICK_BREAKING | HSA_FLAG_SOFTMAX_OFF_BY_ONE)) != 0)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED,
+                    "flags 0x%x: only HSA_FLAG_STICK_BREAKING and HSA_FLAG_SOFTMAX_OFF_BY_ONE "
+                    "are supported", p->flags);
     const int h = p->n_qheads / p->n_kvheads;
     if (h > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "at most 16 query heads per KV head");
     if (p->head_dim != 64 && p->head_dim != 128)
@@ -77,6 +78,7 @@ hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
     dm->beta = p->sm_scale > 0.f ? p->sm_scale : (float)(1.0 / sqrt((double)p->head_dim));
     dm->alpha = p->sel_scale > 0.f ? p->sel_scale : (float)(1.0 / sqrt((double)h * p->head_dim));
     dm->stick = (p->flags & HSA_FLAG_STICK_BREAKING) ? 1 : 0;
+    dm->off1 = (p->flags & HSA_FLAG_SOFTMAX_OFF_BY_ONE) ? 1 : 0;
     return HSA_ATTN_OK;
 }
 

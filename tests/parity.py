@@ -42,30 +42,52 @@ def to_dev(x: np.ndarray, shape) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(torch_dtype(shape))
 
 
-def make_case(shape, seed, kind="iid", mu_std=0.5, gap=True):
+def logit_shift_coord(shape, shift):
+    """The value a (bf16-exact) whose square over sqrt(d) is about |shift|: coordinate 0 of
+    every key set to sign(shift) a and of every query to a adds sign(shift) a^2 / sqrt(d)
+    to every intra-chunk logit beta q.k (beta = 1/sqrt(d))."""
+    a = math.sqrt(abs(shift) * math.sqrt(shape.d))
+    return float(hsa_synth.round_bf16(np.array([a], np.float32))[0])
+
+
+def make_case(shape, seed, kind="iid", mu_std=0.5, gap=True, logit_shift=0.0):
+    """Seeded inputs of one case, gap-enforced.  logit_shift moves every intra-chunk logit
+    by about that constant (see logit_shift_coord): the softmax does not see it, the
+    softmax off by one does.  Every key then has the same coordinate 0, so a token's
+    selection scores all move by one constant and its selection and gap do not change; the
+    keys are set before the gap enforcement (which may redraw queries) and the queries
+    after it."""
     inp = hsa_synth.make_training_inputs(shape, seed, kind=kind, mu_std=mu_std)
+    if logit_shift:
+        a = logit_shift_coord(shape, logit_shift)
+        inp["K"][..., 0] = math.copysign(a, logit_shift)
     stats = enforce_gap(inp, shape, seed, MIN_GAP) if gap else None
+    if logit_shift:
+        inp["Q"][..., 0] = a
     return inp, stats
 
 
-def oracle_reference(inp, shape, backward=True, stick=False):
+def oracle_reference(inp, shape, backward=True, stick=False, off_by_one=False):
     """The oracle's landmarks, selection, forward and (optionally) backward of one case,
-    with softmax or (stick) stick-breaking chunk weights."""
+    with softmax or (stick) stick-breaking chunk weights, and the softmax or (off_by_one)
+    the softmax off by one inside a chunk."""
     S, k, G = shape.S, shape.k, shape.G
     ref = {"Kbar": oracle.landmarks(inp["K"], S)}
     idx, w, gap, _ = oracle.select(inp["Q"], ref["Kbar"], G, S, k, stick=stick)
     ref.update(idx=idx, w=w, gap=gap)
-    ref["O"] = oracle.forward(inp["Q"], inp["K"], inp["V"], idx, w, S)
-    ref["O_abs"] = attention_abs(inp, idx, w, S)
+    ref["O"] = oracle.forward(inp["Q"], inp["K"], inp["V"], idx, w, S, off_by_one=off_by_one)
+    ref["O_abs"] = attention_abs(inp, idx, w, S, off_by_one)
     if backward:
         ref["dQ"], ref["dK"], ref["dV"] = oracle.backward(inp["Q"], inp["K"], inp["V"], idx, w,
-                                                           inp["dO"], S, stick=stick)
+                                                           inp["dO"], S, stick=stick,
+                                                           off_by_one=off_by_one)
     return ref
 
 
-def attention_abs(inp, idx, w, S):
+def attention_abs(inp, idx, w, S, off_by_one=False):
     """O_abs of the attention bound: the oracle forward on |V| and |w|."""
-    return oracle.forward(inp["Q"], inp["K"], np.abs(inp["V"]), idx, np.abs(w), S)
+    return oracle.forward(inp["Q"], inp["K"], np.abs(inp["V"]), idx, np.abs(w), S,
+                          off_by_one=off_by_one)
 
 
 BF16_HALF_ULP = 2.0 ** -8

@@ -59,14 +59,20 @@ def test_flags_reserved(lib):
     p = P()
     p.flags = 1
     assert fwd(lib, p) == UNSUPPORTED
-    p.flags = binding.HSA_FLAG_STICK_BREAKING | 4
+    p.flags = binding.HSA_FLAG_STICK_BREAKING | binding.HSA_FLAG_SOFTMAX_OFF_BY_ONE | 8
     assert fwd(lib, p) == UNSUPPORTED
 
 
-def test_stick_breaking_flag_accepted(lib):
-    """The stick-breaking flag passes validation: the call then fails on the NULL Q."""
-    p = P(stick_breaking=True)
-    assert p.flags == binding.HSA_FLAG_STICK_BREAKING
+@pytest.mark.parametrize("kw,flags", [
+    (dict(stick_breaking=True), binding.HSA_FLAG_STICK_BREAKING),
+    (dict(off_by_one=True), binding.HSA_FLAG_SOFTMAX_OFF_BY_ONE),
+    (dict(stick_breaking=True, off_by_one=True),
+     binding.HSA_FLAG_STICK_BREAKING | binding.HSA_FLAG_SOFTMAX_OFF_BY_ONE)])
+def test_variant_flags_accepted(lib, kw, flags):
+    """The stick-breaking and off-by-one flags pass validation: the call then fails on the
+    NULL Q."""
+    p = P(**kw)
+    assert p.flags == flags
     assert fwd(lib, p, Q=None) == INVALID
     assert "Q" in lib.hsa_attn_last_error().decode()
 

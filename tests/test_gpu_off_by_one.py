@@ -1,0 +1,155 @@
+"""GPU parity of the softmax off by one inside a chunk (the normaliser of the paper's
+kernels, Sec. 3.1.2): every forward, backward and decode path against the oracle run with
+the same normaliser, and the paper's main variant (stick-breaking weights and the softmax
+off by one) end to end.
+
+The inputs carry a common logit shift (parity.make_case's logit_shift): at -4.5 the
+normaliser's extra 1 is about as large as the sum over a chunk's keys, so results of the
+plain softmax miss these bounds by far; at +90 the logits lie beyond exp's float range,
+which the kernels' maximum subtraction must absorb.
+"""
+import numpy as np
+import pytest
+import torch
+
+import hsa_synth
+import oracle
+from parity import (W_ATOL, assert_close, assert_indices, logit_shift_coord, make_case,
+                    oracle_reference, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+Shape = hsa_synth.HsaShape
+
+CASES = {
+    # name: (shape, seed, kind, logit shift).  bf16 h = 8, d = 128, S = 64 takes the fused
+    # backward and the tile-major forward (the chunk-major one on request); S = 128 the
+    # two-pass backward; f32 the generic kernels
+    "L4K_like_bf16": (Shape(2, 1024, 16, 2, 128, 64, 8, "bf16"), 71, "iid", -4.5),
+    "ragged_mfma_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 72, "iid", -4.5),
+    "k24_bf16": (Shape(1, 2048, 16, 2, 128, 32, 24, "bf16"), 73, "iid", -3.5),
+    "wide_S128_bf16": (Shape(1, 1024, 32, 4, 128, 128, 4, "bf16"), 5, "lowrank", -5.0),
+    "ragged_f32": (Shape(2, 1000, 8, 2, 64, 32, 5, "f32"), 74, "iid", -3.5),
+    "k20_d64_f32": (Shape(1, 1500, 4, 2, 64, 32, 20, "f32"), 75, "iid", -3.5),
+    "hot_logits_bf16": (Shape(1, 1024, 16, 2, 128, 64, 8, "bf16"), 76, "iid", 90.0),
+    "hot_logits_f32": (Shape(1, 700, 8, 2, 64, 32, 6, "f32"), 77, "iid", 90.0),
+}
+
+# The mean logit over a chunk is also the chunk's score (up to alpha / beta), so a shift of
+# the logits shifts the selection scores by sqrt(h) times as much: under stick-breaking,
+# -4.5 would leave weights of ~1e-6.  The main-variant cases take -1.5 (weights 0.05 to
+# 0.2, the null logit still several times the bounds' worth).
+MAIN_VARIANT_SHIFT = -1.5
+
+_cache = {}
+
+
+def case(name, stick=False):
+    key = (name, stick)
+    if key not in _cache:
+        shape, seed, kind, shift = CASES[name]
+        if stick:
+            shift = MAIN_VARIANT_SHIFT
+        inp, _ = make_case(shape, seed, kind=kind, mu_std=0.0 if kind == "lowrank" else 0.5,
+                           logit_shift=shift)
+        ref = oracle_reference(inp, shape, stick=stick, off_by_one=True)
+        dev = {n: to_dev(v, shape) for n, v in inp.items()}
+        _cache[key] = (shape, inp, ref, dev)
+    return _cache[key]
+
+
+def banner(name, what):
+    print("\n[gpu] %s: %s" % (name, what), flush=True)
+
+
+def _dev32(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+FWD_PATHS = ["default", "chunk"]
+
+
+@pytest.mark.parametrize("path", FWD_PATHS)
+@pytest.mark.parametrize("name", list(CASES))
+def test_forward_off_by_one(hsa_gpu, name, path, monkeypatch):
+    shape, inp, ref, dev = case(name)
+    chunk_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
+        and shape.H // shape.G == 8
+    if path == "chunk" and not chunk_shape:
+        pytest.skip("the chunk-major forward serves bf16, h = 8, d = 128, S = 64")
+    banner(name, "hsa_forward, softmax off by one (%s path)" % path)
+    if path == "chunk":
+        monkeypatch.setenv("HSA_FWD_PATH", "chunk")
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], _dev32(ref["idx"]),
+                            _dev32(ref["w"].astype(np.float32)), shape.S, off_by_one=True)
+    torch.cuda.synchronize()
+    assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
+
+
+@pytest.mark.parametrize("two_pass", [False, True])
+@pytest.mark.parametrize("name", list(CASES))
+def test_backward_off_by_one(hsa_gpu, name, two_pass, monkeypatch):
+    shape, inp, ref, dev = case(name)
+    fused_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
+        and shape.H // shape.G == 8
+    if two_pass and not fused_shape:
+        pytest.skip("the two-pass switch only changes the path of the fused shapes")
+    banner(name, "hsa_backward, softmax off by one (%s)" % ("two-pass" if two_pass else "default"))
+    if two_pass:
+        monkeypatch.setenv("HSA_BWD_TWO_PASS", "1")
+    got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], _dev32(ref["Kbar"].astype(np.float32)),
+                               _dev32(ref["idx"]), _dev32(ref["w"].astype(np.float32)), dev["dO"],
+                               shape.S, off_by_one=True)
+    torch.cuda.synchronize()
+    for n, g_ in zip(("dQ", "dK", "dV"), got):
+        assert_close(n, shape, g_, ref[n])
+
+
+@pytest.mark.parametrize("name", ["L4K_like_bf16", "wide_S128_bf16", "ragged_f32"])
+def test_main_variant_pipeline(hsa_gpu, name):
+    """The paper's main variant: stick-breaking weights and the softmax off by one, from
+    landmarks to the backward, all on the GPU."""
+    shape, inp, ref, dev = case(name, stick=True)
+    banner(name, "pipeline, stick-breaking + softmax off by one")
+    Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
+    idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k,
+                                     stick_breaking=True)
+    O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S, off_by_one=True)
+    dQ, dK, dV = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"],
+                                      shape.S, stick_breaking=True, off_by_one=True)
+    torch.cuda.synchronize()
+    sure, loose = assert_indices(idx, ref["idx"], ref["gap"], shape.S)
+    assert loose == 0
+    assert np.max(np.abs(w.cpu().numpy() - ref["w"])) <= W_ATOL
+    assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
+    for n, t in (("dQ", dQ), ("dK", dK), ("dV", dV)):
+        assert_close(n, shape, t, ref[n])
+
+
+@pytest.mark.parametrize("stick", [False, True])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_decode_off_by_one(hsa_gpu, dtype, stick):
+    shape = Shape(3, 4096 + 64, 16, 2, 128 if dtype == "bf16" else 64, 64, 8, dtype)
+    banner("decode_off1_%s_stick%d" % (dtype, stick), "hsa_decode, softmax off by one")
+    inp = hsa_synth.make_decode_inputs(shape, 81, device="cuda")
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
+    a = logit_shift_coord(shape, -4.5)
+    Kc[..., 0] = -a                 # every key: the same coordinate 0 (scores move together)
+    q[..., 0] = a
+    lens = [4096, 4096 + 40, 64 * 5 + 3]
+    cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    Kbar = _dev32(oracle.landmarks(Kc, 64).astype(np.float32))
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, 8, cache_len=cache_len,
+                                   stick_breaking=stick, off_by_one=True)
+    torch.cuda.synchronize()
+    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, 64, 8, stick=stick,
+                                       off_by_one=True)
+    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar, lens, 64, 8, stick=stick, off_by_one=True)[0]
+    # groups whose selection is decided by more than the score rounding (nearly all)
+    sure = rgap >= 1e-3
+    assert sure.sum() >= 5
+    assert np.array_equal(idx.cpu().numpy()[sure], ridx[sure])
+    assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
+    heads = torch.from_numpy(np.repeat(sure, shape.H // shape.G, axis=1)).cuda()
+    hm = heads.cpu().numpy()
+    assert_close("o", shape, o[heads], ro[hm], o_abs=ro_abs[hm])
