@@ -101,7 +101,7 @@ typedef struct {
  * attention.  Read by hsa_forward, hsa_backward and hsa_decode (the attention inside
  * every selected chunk); hsa_select_topk does not depend on it.  The backward keeps its
  * form (dZ = w P (dP - D), D = dO . O_chunk), with P from this normaliser. */
-#define HSA_FLAG_SOFTMAX_OFF_BY_ONE 4u
+#define HSA_FLAG_SOFTMAX_OFF_BY_ONE 1u
 
 /* Landmarks (Fig. 1; Sec. 3.1 "Chunk Selection": mean-pooled chunk representation):
  * Kbar[b, c, g, :] = (1/S) sum_{s<S} K[b, c*S + s, g, :] for chunks c in

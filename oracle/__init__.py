@@ -30,7 +30,7 @@ class _Dims(ctypes.Structure):
     _fields_ = [("L", ctypes.c_int64), ("h", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("S", ctypes.c_int32), ("k", ctypes.c_int32), ("alpha", ctypes.c_double),
                 ("beta", ctypes.c_double), ("stick", ctypes.c_int32),
-                ("off_by_one", ctypes.c_int32)]
+                ("off_by_one", ctypes.c_int32), ("sep", ctypes.c_int32)]
 
 
 def build(force: bool = True) -> str:
@@ -58,10 +58,12 @@ def _load():
         lib.hsa_oracle_landmarks.argtypes = [DP, P, P]
         lib.hsa_oracle_select.argtypes = [DP, P, P, I64, P, P, P, P, P]
         lib.hsa_oracle_forward.argtypes = [DP, P, P, P, P, P, I64, P, P]
-        lib.hsa_oracle_backward_q.argtypes = [DP, P, P, P, P, P, P, P, I64, P, P, P]
+        lib.hsa_oracle_backward_q.argtypes = [DP, P, P, P, P, P, P, P, I64, P, P, P, P]
+        lib.hsa_oracle_select_backward.argtypes = [DP, P, P, P, P, P, P, P, P]
         lib.hsa_oracle_backward_kv.argtypes = [DP, P, P, P, P, P, P, P, I64, P, P, P]
         lib.hsa_oracle_decode.argtypes = [DP, P, P, P, P, I64, P, P, P, P]
-        for f in ("landmarks", "select", "forward", "backward_q", "backward_kv", "decode"):
+        for f in ("landmarks", "select", "forward", "backward_q", "backward_kv", "decode",
+                  "select_backward"):
             getattr(lib, "hsa_oracle_" + f).restype = None
         _lib = lib
     return _lib
@@ -82,14 +84,17 @@ def default_scales(h: int, d: int):
     return 1.0 / math.sqrt(h * d), 1.0 / math.sqrt(d)
 
 
-def dims(L, h, d, S, k, alpha=None, beta=None, stick=False, off_by_one=False) -> _Dims:
+def dims(L, h, d, S, k, alpha=None, beta=None, stick=False, off_by_one=False,
+         sep=False) -> _Dims:
     """Slice dimensions; stick selects stick-breaking chunk weights (Sec. 3.1.1) instead of
     the softmax over the selected scores; off_by_one the softmax off by one for the
-    attention inside a chunk (the paper's kernels, Sec. 3.1.2) instead of the softmax."""
+    attention inside a chunk (the paper's kernels, Sec. 3.1.2) instead of the softmax; sep
+    a selection over inputs of its own (Sec. 3.1), whose score term the attention backward
+    leaves out."""
     a0, b0 = default_scales(h, d)
     return _Dims(int(L), int(h), int(d), int(S), int(k),
                  float(a0 if alpha is None else alpha), float(b0 if beta is None else beta),
-                 1 if stick else 0, 1 if off_by_one else 0)
+                 1 if stick else 0, 1 if off_by_one else 0, 1 if sep else 0)
 
 
 # ----------------------------------------------------------------------------------
@@ -137,16 +142,34 @@ def forward_slice(dm: _Dims, Q, K, V, idx, w, rows=None):
     return O
 
 
-def backward_q_slice(dm: _Dims, Q, K, V, Kbar, idx, w, dO, rows=None):
+def backward_q_slice(dm: _Dims, Q, K, V, Kbar, idx, w, dO, rows=None, with_dw=False):
     Q, K, V, Kbar, w, dO = map(_f64, (Q, K, V, Kbar, w, dO))
     idx = np.ascontiguousarray(idx, dtype=np.int32)
     r, n = _rows(rows, dm.L)
     dQ = np.empty((n, dm.h, dm.d))
     ds = np.empty((n, dm.k))
+    dw = np.empty((n, dm.k))
     if n:
         _load().hsa_oracle_backward_q(ctypes.byref(dm), _p(Q), _p(K), _p(V), _p(Kbar),
-                                      _p(idx), _p(w), _p(dO), n, _p(r), _p(dQ), _p(ds))
-    return dQ, ds
+                                      _p(idx), _p(w), _p(dO), n, _p(r), _p(dQ), _p(ds),
+                                      _p(dw))
+    return (dQ, ds, dw) if with_dw else (dQ, ds)
+
+
+def select_backward_slice(dm: _Dims, Q, Kbar, idx, w, dw):
+    """(dQ [L, h, d], dKbar [C, d], ds [L, k]) of one slice through the selection scores."""
+    Q, Kbar, w, dw = map(_f64, (Q, Kbar, w, dw))
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    C = dm.L // dm.S
+    dQ = np.empty((dm.L, dm.h, dm.d))
+    dKbar = np.zeros((C, dm.d))
+    ds = np.empty((dm.L, dm.k))
+    if dm.L:
+        _load().hsa_oracle_select_backward(ctypes.byref(dm), _p(Q),
+                                           _p(Kbar if C else np.zeros((1, dm.d))), _p(idx),
+                                           _p(w), _p(dw), _p(dQ),
+                                           _p(dKbar if C else np.zeros((1, dm.d))), _p(ds))
+    return dQ, dKbar, ds
 
 
 def backward_kv_slice(dm: _Dims, Q, K, V, idx, w, dO, ds, chunks=None):
@@ -217,9 +240,11 @@ def forward(Q, K, V, idx, w, S: int, beta=None, off_by_one=False):
 
 
 def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False,
-             off_by_one=False):
+             off_by_one=False, separate=False):
     """dQ, dK, dV (fp64) of sum(dO * O) with the selection held fixed (weights a function of
-    the selected scores: softmax, or stick-breaking with stick)."""
+    the selected scores: softmax, or stick-breaking with stick).  separate: the scores come
+    from selection inputs of their own, so no score term reaches Q or K; returns
+    (dQ, dK, dV, dw) with dw [B, L, G, k] = d loss / d w."""
     Q, K, V, w, dO = map(_f64, (Q, K, V, w, dO))
     B, L, H, G, d, h = _shape(Q, K)
     k = idx.shape[-1]
@@ -227,21 +252,49 @@ def backward(Q, K, V, idx, w, dO, S: int, alpha=None, beta=None, stick=False,
     dQ = np.empty((B, L, H, d))
     dK = np.zeros((B, L, G, d))
     dV = np.zeros((B, L, G, d))
+    dW = np.zeros((B, L, G, k))
     for b in range(B):
         for g in range(G):
-            dm = dims(L, h, d, S, k, alpha, beta, stick, off_by_one)
+            dm = dims(L, h, d, S, k, alpha, beta, stick, off_by_one, separate)
             Qs = np.ascontiguousarray(Q[b, :, g * h:(g + 1) * h])
             dOs = np.ascontiguousarray(dO[b, :, g * h:(g + 1) * h])
             Ks, Vs = np.ascontiguousarray(K[b, :, g]), np.ascontiguousarray(V[b, :, g])
             ids, ws = np.ascontiguousarray(idx[b, :, g]), np.ascontiguousarray(w[b, :, g])
             Kb = landmarks_slice(dm, Ks)
-            dq, ds = backward_q_slice(dm, Qs, Ks, Vs, Kb, ids, ws, dOs)
+            dq, ds, dw = backward_q_slice(dm, Qs, Ks, Vs, Kb, ids, ws, dOs, with_dw=True)
             dQ[b, :, g * h:(g + 1) * h] = dq
+            dW[b, :, g] = dw
             if C:
                 dk, dv = backward_kv_slice(dm, Qs, Ks, Vs, ids, ws, dOs, ds)
                 dK[b, :C * S, g] = dk.reshape(C * S, d)
                 dV[b, :C * S, g] = dv.reshape(C * S, d)
-    return dQ, dK, dV
+    return (dQ, dK, dV, dW) if separate else (dQ, dK, dV)
+
+
+def select_backward(Q, Kbar, idx, w, dw, G: int, S: int, alpha=None, stick=False):
+    """Gradient through the selection scores s = alpha (sum_j q_j) . Kbar_c for d loss / d w
+    = dw [B, L, G, k]: (dQ [B, L, H, d], dKbar [B, C, G, d], ds [B, L, G, k]).  For a
+    selection over inputs of its own, Q is [B, L, G, d_sel] (h = 1) and Kbar the chunk
+    representations [B, C, G, d_sel]."""
+    Q, Kbar, w, dw = map(_f64, (Q, Kbar, w, dw))
+    B, L, H, d = Q.shape
+    h = H // G
+    k = idx.shape[-1]
+    C = L // S
+    dQ = np.empty((B, L, H, d))
+    dKbar = np.zeros((B, C, G, d))
+    ds = np.empty((B, L, G, k))
+    for b in range(B):
+        for g in range(G):
+            dm = dims(L, h, d, S, k, alpha, None, stick)
+            dq, dkb, dsl = select_backward_slice(
+                dm, np.ascontiguousarray(Q[b, :, g * h:(g + 1) * h]),
+                np.ascontiguousarray(Kbar[b, :, g]), np.ascontiguousarray(idx[b, :, g]),
+                np.ascontiguousarray(w[b, :, g]), np.ascontiguousarray(dw[b, :, g]))
+            dQ[b, :, g * h:(g + 1) * h] = dq
+            dKbar[b, :, g] = dkb
+            ds[b, :, g] = dsl
+    return dQ, dKbar, ds
 
 
 def decode(q, Kc, Vc, Kbar_cache, cache_len: Sequence[int], S: int, k: int,

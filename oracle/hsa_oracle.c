@@ -190,10 +190,42 @@ void hsa_oracle_forward(const hsa_oracle_dims* dm, const double* Q, const double
     }
 }
 
+/* d loss / d s_i of one token from dw_i = d loss / d w_i, through the weight rule over the
+ * valid slots (idx >= 0).  bsb: scratch of k doubles. */
+static void score_grad(const hsa_oracle_dims* dm, const int32_t* idx_t, const double* w_t,
+                       const double* dw, double* bsb, double* dsl) {
+    const int k = dm->k;
+    for (int i = 0; i < k; ++i) dsl[i] = 0.0;
+    if (dm->stick) {
+        /* stick-breaking weights w_i = b_i u_i, u_i = prod_{m<i} (1 - b_m) over the
+           valid slots: dw_i reaches s_i through b_i directly and through the (1 - b_i)
+           factor of every later slot, ds_i = (1 - b_i) w_i dw_i - b_i sum_{m>i} w_m dw_m */
+        double u = 1.0;
+        for (int i = 0; i < k; ++i) {
+            if (idx_t[i] < 0) continue;
+            bsb[i] = u > 0.0 ? w_t[i] / u : 0.0;
+            u -= w_t[i];
+        }
+        double tail = 0.0;
+        for (int i = k - 1; i >= 0; --i) {
+            if (idx_t[i] < 0) continue;
+            const double wd = w_t[i] * dw[i];
+            dsl[i] = (1.0 - bsb[i]) * wd - bsb[i] * tail;
+            tail += wd;
+        }
+    } else {
+        /* softmax chunk weights: ds_i = w_i (dw_i - sum_m w_m dw_m) */
+        double wdw = 0.0;
+        for (int i = 0; i < k; ++i) wdw += w_t[i] * dw[i];
+        for (int i = 0; i < k; ++i)
+            if (idx_t[i] >= 0) dsl[i] = w_t[i] * (dw[i] - wdw);
+    }
+}
+
 void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const double* K,
                            const double* V, const double* Kbar, const int32_t* idx,
                            const double* w, const double* dO, int64_t ntok,
-                           const int64_t* rows, double* dQ, double* ds) {
+                           const int64_t* rows, double* dQ, double* ds, double* dw_out) {
     const int h = dm->h, d = dm->d, S = dm->S, k = dm->k;
 #pragma omp parallel
     {
@@ -240,32 +272,16 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
                     }
                 }
             }
-            if (dm->stick) {
-                /* stick-breaking weights w_i = b_i u_i, u_i = prod_{m<i} (1 - b_m) over the
-                   valid slots: dw_i reaches s_i through b_i directly and through the (1 - b_i)
-                   factor of every later slot, ds_i = (1 - b_i) w_i dw_i - b_i sum_{m>i} w_m dw_m */
-                double u = 1.0;
-                for (int i = 0; i < k; ++i) {
-                    const int64_t c = idx[t * k + i];
-                    if (c < 0) continue;
-                    bsb[i] = u > 0.0 ? w[t * k + i] / u : 0.0;
-                    u -= w[t * k + i];
-                }
-                double tail = 0.0;
-                for (int i = k - 1; i >= 0; --i) {
-                    const int64_t c = idx[t * k + i];
-                    if (c < 0) continue;
-                    const double wd = w[t * k + i] * dw[i];
-                    dsl[i] = (1.0 - bsb[i]) * wd - bsb[i] * tail;
-                    tail += wd;
-                }
-            } else {
-                /* softmax chunk weights: ds_i = w_i (dw_i - sum_m w_m dw_m) */
-                double wdw = 0.0;
-                for (int i = 0; i < k; ++i) wdw += w[t * k + i] * dw[i];
-                for (int i = 0; i < k; ++i)
-                    if (idx[t * k + i] >= 0) dsl[i] = w[t * k + i] * (dw[i] - wdw);
+            if (dw_out)
+                for (int i = 0; i < k; ++i) dw_out[r * k + i] = dw[i];
+            if (dm->sep) {
+                /* the scores do not depend on Q or K: no score term, and no ds for the
+                   landmark term of dK */
+                if (ds)
+                    for (int i = 0; i < k; ++i) ds[r * k + i] = 0.0;
+                continue;
             }
+            score_grad(dm, idx + t * k, w + t * k, dw, bsb, dsl);
             for (int i = 0; i < k; ++i) {
                 const int64_t c = idx[t * k + i];
                 if (c < 0) continue;
@@ -284,6 +300,42 @@ void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const dou
         free(dP);
         free(P);
     }
+}
+
+void hsa_oracle_select_backward(const hsa_oracle_dims* dm, const double* Q,
+                                const double* Kbar, const int32_t* idx, const double* w,
+                                const double* dw, double* dQ, double* dKbar, double* ds) {
+    const int h = dm->h, d = dm->d, k = dm->k;
+    const int64_t L = dm->L, C = dm->L / dm->S;
+    double* dsl = (double*)malloc(sizeof(double) * k);
+    double* bsb = (double*)malloc(sizeof(double) * k);
+    double* qs = (double*)malloc(sizeof(double) * d);
+    memset(dKbar, 0, sizeof(double) * (size_t)(C > 0 ? C : 0) * d);
+    for (int64_t t = 0; t < L; ++t) {
+        score_grad(dm, idx + t * k, w + t * k, dw + t * k, bsb, dsl);
+        if (ds)
+            for (int i = 0; i < k; ++i) ds[t * k + i] = dsl[i];
+        /* q~ = sum_j q_j, the query the score was formed with */
+        for (int e = 0; e < d; ++e) {
+            double a = 0.0;
+            for (int j = 0; j < h; ++j) a += Q[(t * h + j) * d + e];
+            qs[e] = a;
+        }
+        double* dQt = dQ + t * h * d;
+        memset(dQt, 0, sizeof(double) * h * d);
+        for (int i = 0; i < k; ++i) {
+            const int64_t c = idx[t * k + i];
+            if (c < 0) continue;
+            for (int e = 0; e < d; ++e) {
+                const double g = dm->alpha * dsl[i] * Kbar[c * d + e];
+                for (int j = 0; j < h; ++j) dQt[j * d + e] += g;
+                dKbar[c * d + e] += dm->alpha * dsl[i] * qs[e];
+            }
+        }
+    }
+    free(qs);
+    free(bsb);
+    free(dsl);
 }
 
 void hsa_oracle_backward_kv(const hsa_oracle_dims* dm, const double* Q, const double* K,

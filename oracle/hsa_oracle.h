@@ -39,6 +39,10 @@ typedef struct {
     int32_t off_by_one; /* intra-chunk attention: 0 softmax; 1 softmax off by one (Sec. 3.1.2
                        kernel description), P_s = exp(z_s) / (1 + sum_r exp(z_r)), so a
                        token may give a retrieved chunk almost no attention              */
+    int32_t sep;    /* 1: the selection scores come from inputs of their own (Sec. 3.1: the
+                       selection query and chunk representations), not from Q and K; the
+                       attention backward then leaves out the score term (no gradient
+                       reaches Q or K through the selection) and reports dw instead       */
 } hsa_oracle_dims;
 
 /* Mean-pooled landmark of every complete chunk: Kbar[c] = (1/S) sum_s K[c*S + s]
@@ -75,7 +79,19 @@ void hsa_oracle_forward(const hsa_oracle_dims* dm, const double* Q, const double
 void hsa_oracle_backward_q(const hsa_oracle_dims* dm, const double* Q, const double* K,
                            const double* V, const double* Kbar, const int32_t* idx,
                            const double* w, const double* dO, int64_t ntok,
-                           const int64_t* rows, double* dQ, double* ds);
+                           const int64_t* rows, double* dQ, double* ds, double* dw);
+
+/* Gradient through the selection scores alone, for a selection over its own inputs (or
+ * the score term of the fused form): given dw [L, k] = d loss / d w (summed over every
+ * layer that used the selection), ds_i follows from the weight rule (softmax, or
+ * stick-breaking with dm->stick), and with s_i = alpha (sum_j q_j) . Kbar_{c_i}:
+ *   dQ[t, j, :]  = alpha sum_i ds_i Kbar_{c_i}       (the same for each of the h rows)
+ *   dKbar[c, :]  = alpha sum over (t, i) with c_i = c of ds_i (sum_j q_j)
+ * over all L tokens of the slice (dKbar accumulated in increasing token order).  Q [L, h,
+ * d], Kbar [C, d]; outputs dQ [L, h, d], dKbar [C, d], ds [L, k] (optional). */
+void hsa_oracle_select_backward(const hsa_oracle_dims* dm, const double* Q,
+                                const double* Kbar, const int32_t* idx, const double* w,
+                                const double* dw, double* dQ, double* dKbar, double* ds);
 
 /* Backward phase 2 (key/value side): gradient w.r.t. K and V of the S tokens of each
  * listed chunk (chunks == NULL: all C complete chunks), accumulated over the tokens that

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libhsa_mi355x.so")
 HSA_DTYPE_F32, HSA_DTYPE_BF16 = 0, 1
 HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE = range(5)
 HSA_FLAG_STICK_BREAKING = 2
-HSA_FLAG_SOFTMAX_OFF_BY_ONE = 4
+HSA_FLAG_SOFTMAX_OFF_BY_ONE = 1
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP"}
 
 _lib = None

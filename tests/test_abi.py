@@ -57,8 +57,9 @@ def test_forward_rejects_bad_shapes(lib, kw, code):
 
 def test_flags_reserved(lib):
     p = P()
-    p.flags = 1
-    assert fwd(lib, p) == UNSUPPORTED
+    for bit in (4, 8, 1 << 31):
+        p.flags = bit
+        assert fwd(lib, p) == UNSUPPORTED
     p.flags = binding.HSA_FLAG_STICK_BREAKING | binding.HSA_FLAG_SOFTMAX_OFF_BY_ONE | 8
     assert fwd(lib, p) == UNSUPPORTED
 

@@ -462,3 +462,81 @@ def test_decode_planted_chunk_is_selected():
     for b in range(2):
         for g in range(2):
             assert inp["planted"][b, g].item() in set(idx[b, g].tolist())
+
+
+# ------------------------------------------------- selection over its own inputs ----
+
+def _shared_selection_loss(Qs, Ks, layers, S, k, stick, off1, idx_ref):
+    """Sec. 3.1 / Sec. 4.3: one selection from the selection inputs (Qs [B, L, G, d_sel],
+    Ks [B, C, G, d_sel]) serves every layer; loss = sum over layers of sum(O_l * dO_l)."""
+    G = Ks.shape[2]
+    idx, w, _, _ = oracle.select(Qs, Ks, G, S, k, stick=stick)
+    assert np.array_equal(idx, idx_ref), "selection moved under the perturbation"
+    return sum(float((oracle.forward(Q, K, V, idx, w, S, off_by_one=off1) * dO).sum())
+               for Q, K, V, dO in layers)
+
+
+@pytest.mark.parametrize("stick,off1", [(False, False), (True, True)])
+def test_shared_selection_finite_differences(stick, off1):
+    """Two layers sharing a selection over separate inputs: each layer's backward without
+    the score term, plus the selection backward of the summed dw, is the gradient of the
+    summed loss w.r.t. every input (central differences, step 1e-6)."""
+    L, h, d, S, k, G, dsel = 12, 2, 3, 2, 2, 2, 4
+    C = L // S
+    Qs = rnd(201, 1, L, G, dsel)
+    Ks = rnd(202, 1, C, G, dsel, std=1.5)
+    layers = [small_problem(210 + 10 * l, L=L, h=h, d=d, S=S, k=k, mu=1.0, G=G)
+              for l in range(2)]
+    idx, w, gap, _ = oracle.select(Qs, Ks, G, S, k, stick=stick)
+    assert gap[np.isfinite(gap)].min() > 1e-4
+    grads, dw = [], np.zeros_like(w)
+    for Q, K, V, dO in layers:
+        dQ, dK, dV, dwl = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick,
+                                          off_by_one=off1, separate=True)
+        grads.append((dQ, dK, dV))
+        dw += dwl
+    dQs, dKs, _ = oracle.select_backward(Qs, Ks, idx, w, dw, G, S, stick=stick)
+    eps = 1e-6
+
+    def fd(X, put):
+        num = np.zeros_like(X)
+        it = np.nditer(X, flags=["multi_index"])
+        for _ in it:
+            i = it.multi_index
+            Xp, Xm = X.copy(), X.copy()
+            Xp[i] += eps
+            Xm[i] -= eps
+            num[i] = (put(Xp) - put(Xm)) / (2 * eps)
+        return num
+
+    loss = lambda Qs_, Ks_, ls_: _shared_selection_loss(Qs_, Ks_, ls_, S, k, stick, off1, idx)
+    np.testing.assert_allclose(dQs, fd(Qs, lambda X: loss(X, Ks, layers)), rtol=1e-5,
+                               atol=1e-7, err_msg="Qs")
+    np.testing.assert_allclose(dKs, fd(Ks, lambda X: loss(Qs, X, layers)), rtol=1e-5,
+                               atol=1e-7, err_msg="Ks")
+    for l, (Q, K, V, dO) in enumerate(layers):
+        for pos, name in ((0, "Q"), (1, "K"), (2, "V")):
+            def put(X, pos=pos, l=l):
+                ls_ = [list(t) for t in layers]
+                ls_[l][pos] = X
+                return loss(Qs, Ks, [tuple(t) for t in ls_])
+            np.testing.assert_allclose(grads[l][pos], fd(layers[l][pos], put), rtol=1e-5,
+                                       atol=1e-7, err_msg="layer %d %s" % (l, name))
+
+
+@pytest.mark.parametrize("stick", [False, True])
+def test_fused_score_term_is_the_selection_backward_of_the_head_sum(stick):
+    """The fused form scores with q~ = sum_j q_j and Kbar = mean of the chunk's keys: its
+    gradient is the attention-only gradient plus the selection backward of those inputs,
+    with dKbar reaching every key of the chunk as dKbar / S."""
+    L, h, d, S, k, G = 48, 2, 4, 4, 3, 2
+    Q, K, V, dO = small_problem(231, L=L, h=h, d=d, S=S, k=k, G=G)
+    Kb = oracle.landmarks(K, S)
+    idx, w, _, _ = oracle.select(Q, Kb, G, S, k, stick=stick)
+    dQ, dK, dV = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick)
+    dQa, dKa, dVa, dw = oracle.backward(Q, K, V, idx, w, dO, S, stick=stick, separate=True)
+    dQs, dKb, _ = oracle.select_backward(Q, Kb, idx, w, dw, G, S, stick=stick)
+    np.testing.assert_allclose(dV, dVa, rtol=0, atol=0)
+    np.testing.assert_allclose(dQ, dQa + dQs, rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(dK, dKa + np.repeat(dKb / S, S, axis=1), rtol=1e-12,
+                               atol=1e-14)
