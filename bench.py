@@ -5,7 +5,8 @@ A step is one pass of the whole hot path over one batch of synthetic input:
 landmarks -> score + top-k -> forward -> backward (fwd+bwd workloads), or one decode step.
 Inputs are resident in HBM before the timed region.  The main line is the 4K-context
 fwd+bwd workload (B 8, L 4096, H 16 / G 2, d 128, S 64, k 8, bf16); the 64K-context
-fwd+bwd and the 1M-token decode step are reported under "also".
+fwd+bwd, the 1M-token decode step, and three layers sharing one selection over inputs of
+its own (with, for comparison, a selection per layer) are reported under "also".
 
 Kernel durations come from HIP events recorded by the library around its launches on the
 launch stream (hsa_attn_timing_enable / hsa_attn_timing_select).  The last warm-up step
@@ -113,6 +114,11 @@ def time_training(sh, dev, steps, warmup, torch, hsa):
         hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f)
         hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b)
 
+    return time_steps(step, steps, warmup, torch, hsa)
+
+
+def time_steps(step, steps, warmup, torch, hsa):
+    """(ms per step, roofline-kernel timings of the timed steps, per-kernel breakdown)."""
     # Untimed warm-up; its last step brackets every kernel (the per-kernel breakdown and
     # the dominant kernel).  The timed steps bracket only the dominant kernel: an event pair
     # costs queue time between launches, which would otherwise count in the step time.
@@ -243,6 +249,67 @@ def bench_decode(steps, warmup, torch, hsa):
                                 "bytes_per_launch": stream_bytes}
     out["algorithmic_bytes_per_step"] = stream_bytes + gather_bytes
     return out
+
+
+def bench_shared(steps, warmup, torch, hsa):
+    """Sec. 4.3's setting: three attention layers sharing one selection over inputs of their
+    own (d_sel = h d_h = 1024), forward and backward of all three plus the selection and its
+    backward per step; and the same with a selection (and its backward) per layer."""
+    B, L, H, G, d, S, k = 8, 4096, 16, 2, 128, 64, 8
+    dsel, nl = (H // G) * d, 3
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(2504)
+
+    def rnd(*shape, std=1.0, dt=torch.bfloat16):
+        return (torch.randn(shape, generator=gen, device="cuda") * std).to(dt)
+
+    sc = d ** -0.5
+    layers = [dict(Q=rnd(B, L, H, d, std=sc), K=rnd(B, L, G, d, std=sc),
+                   V=rnd(B, L, G, d, std=sc), dO=rnd(B, L, H, d)) for _ in range(nl)]
+    Qs = rnd(B, L, G, dsel)
+    Ks = rnd(B, L // S, G, dsel, dt=torch.float32)
+    idx = torch.empty((B, L, G, k), dtype=torch.int32, device="cuda")
+    w = torch.empty((B, L, G, k), dtype=torch.float32, device="cuda")
+    dw = torch.empty_like(w)
+    O = torch.empty_like(layers[0]["Q"])
+    grads = (torch.empty_like(layers[0]["Q"]), torch.empty_like(layers[0]["K"]),
+             torch.empty_like(layers[0]["V"]))
+    sel_grads = (torch.empty_like(Qs), torch.empty_like(Ks))
+    p = hsa.make_params(B, L, H, G, d, S, k, torch.bfloat16)
+    ps = hsa.make_params(B, L, G, G, dsel, S, k, torch.bfloat16)
+    ws_f = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_FORWARD)), dtype=torch.uint8,
+                       device="cuda")
+    ws_b = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_BACKWARD)), dtype=torch.uint8,
+                       device="cuda")
+    ws_s = torch.empty(max(1, hsa.workspace_size(ps, hsa.HSA_OP_SELECT_BACKWARD)),
+                       dtype=torch.uint8, device="cuda")
+
+    def shared():
+        hsa.hsa_select_topk(Qs, Ks, G, S, k, idx=idx, w=w)
+        for lay in layers:
+            hsa.hsa_forward(lay["Q"], lay["K"], lay["V"], idx, w, S, out=O, workspace=ws_f)
+        for i, lay in enumerate(layers):
+            hsa.hsa_backward_attn(lay["Q"], lay["K"], lay["V"], idx, w, lay["dO"], S, out=grads,
+                                  dw=dw, accumulate_dw=i > 0, workspace=ws_b)
+        hsa.hsa_select_backward(Qs, Ks, idx, w, dw, G, S, out=sel_grads, workspace=ws_s)
+
+    def per_layer():
+        for lay in layers:
+            hsa.hsa_select_topk(Qs, Ks, G, S, k, idx=idx, w=w)
+            hsa.hsa_forward(lay["Q"], lay["K"], lay["V"], idx, w, S, out=O, workspace=ws_f)
+        for lay in layers:
+            hsa.hsa_backward_attn(lay["Q"], lay["K"], lay["V"], idx, w, lay["dO"], S, out=grads,
+                                  dw=dw, workspace=ws_b)
+            hsa.hsa_select_backward(Qs, Ks, idx, w, dw, G, S, out=sel_grads, workspace=ws_s)
+
+    ms, _, brk = time_steps(shared, steps, warmup, torch, hsa)
+    ms_pl, _, _ = time_steps(per_layer, steps, warmup, torch, hsa)
+    return {"workload": ("3 HSA layers sharing one selection at 4K context: B8 L4096 H16/G2 "
+                         "d128 S64 k8, selection inputs d_sel 1024, bf16; fwd+bwd of the "
+                         "3 layers, the selection and its backward"),
+            "tokens_per_s": round(B * L / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+            "ms_per_step_selection_per_layer": round(ms_pl, 4),
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk.items()}}
 
 
 def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
@@ -417,6 +484,10 @@ def main():
         res["also"]["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 10, torch, hsa)
         print("[bench] decode: %.2f us/step" % res["also"]["decode_1M_bf16"]["us_per_step"],
               file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+        res["also"]["shared_x3_L4K_bf16"] = bench_shared(max(2, args.steps // 2), 2, torch, hsa)
+        print("[bench] shared selection x3: %.3f ms/step"
+              % res["also"]["shared_x3_L4K_bf16"]["ms_per_step"], file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(name, inp)
         print("[bench] cpu baseline done", file=sys.stderr, flush=True)

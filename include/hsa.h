@@ -68,8 +68,9 @@ typedef enum {
     HSA_OP_LANDMARKS = 0,
     HSA_OP_SELECT = 1,
     HSA_OP_FORWARD = 2,
-    HSA_OP_BACKWARD = 3,
-    HSA_OP_DECODE = 4
+    HSA_OP_BACKWARD = 3,             /* also hsa_backward_attn */
+    HSA_OP_DECODE = 4,
+    HSA_OP_SELECT_BACKWARD = 5
 } hsa_op_t;
 
 typedef struct {
@@ -145,6 +146,37 @@ hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const 
                                const void* V, const float* Kbar, const int32_t* idx,
                                const float* w, const void* dO, void* dQ, void* dK, void* dV,
                                void* ws, size_t ws_bytes, void* stream);
+
+/* Backward of the attention alone, for a selection over inputs of its own (Sec. 3.1: the
+ * selection query and chunk representations come from projections of their own, and
+ * Sec. 4.3 shares one selection across the HSA layers).  The same as hsa_backward except
+ * that the scores do not depend on Q or K: dQ and dK carry no score or landmark term, no
+ * Kbar is read, and dw [B, L, G, k] float32 receives d loss / d w per slot (0 in empty
+ * slots; each slot holding a chunk gets the chunk's dw), overwritten, or added to what dw
+ * holds when accumulate_dw != 0 (sum over the layers sharing the selection, then pass the
+ * sum to hsa_select_backward).  Workspace: hsa_attn_workspace_size(p, HSA_OP_BACKWARD). */
+hsa_attn_status_t hsa_backward_attn(const hsa_attn_params_t* p, const void* Q, const void* K,
+                                    const void* V, const int32_t* idx, const float* w,
+                                    const void* dO, void* dQ, void* dK, void* dV, float* dw,
+                                    int32_t accumulate_dw, void* ws, size_t ws_bytes,
+                                    void* stream);
+
+/* Backward of the selection scores alone (Sec. 3.1 scores s_i = alpha q~ . Kbar_{c_i} with
+ * q~ = sum_j q_j over the group's h rows; the weight rule of Sec. 3.1.1): from dw
+ * [B, L, G, k] = d loss / d w and the selection (idx, w), ds follows from the weights
+ * (softmax, or stick-breaking with HSA_FLAG_STICK_BREAKING), and
+ *   dQ[b, t, g h + j, :] = alpha sum_i ds_i Kbar[b, c_i, g, :]          (each j < h)
+ *   dKbar[b, c, g, :]   = alpha sum over (t, i) with c_i = c of ds_i q~_t
+ * For a selection over inputs of its own, Q [B, L, G, d_sel] (n_qheads = n_kvheads) holds
+ * the selection queries and Kbar [B, C, G, d_sel] float32 the chunk representations, with
+ * d_sel = head_dim up to 1024 (bf16 above 128); alpha defaults to 1/sqrt(d_sel).  dQ has Q's
+ * type and layout; dKbar is written for all C chunks (zero where nothing selected it);
+ * the chunk sums run in increasing token order, without atomics.  Workspace:
+ * hsa_attn_workspace_size(p, HSA_OP_SELECT_BACKWARD). */
+hsa_attn_status_t hsa_select_backward(const hsa_attn_params_t* p, const void* Q,
+                                      const float* Kbar, const int32_t* idx, const float* w,
+                                      const float* dw, void* dQ, float* dKbar, void* ws,
+                                      size_t ws_bytes, void* stream);
 
 /* Single-token decode (Sec. 3.2 "Inference": only the landmark cache is scanned, and the
  * selected chunks' keys and values are read).  p->seqlen is the cache capacity N_cap;

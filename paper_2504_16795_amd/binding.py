@@ -17,7 +17,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libhsa_mi355x.so")
 
 HSA_DTYPE_F32, HSA_DTYPE_BF16 = 0, 1
-HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE = range(5)
+(HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE,
+ HSA_OP_SELECT_BACKWARD) = range(6)
 HSA_FLAG_STICK_BREAKING = 2
 HSA_FLAG_SOFTMAX_OFF_BY_ONE = 1
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP"}
@@ -41,6 +42,7 @@ class HsaError(RuntimeError):
 
 
 EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
+            "hsa_backward_attn", "hsa_select_backward",
             "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
             "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect")
 
@@ -61,7 +63,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_forward.argtypes = [PP, P, P, P, P, P, P, P, SZ, P]
     lib.hsa_backward.argtypes = [PP, P, P, P, P, P, P, P, P, P, P, P, SZ, P]
     lib.hsa_decode.argtypes = [PP, P, P, P, P, I32, P, P, P, P, P, SZ, P]
-    for f in ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode"):
+    lib.hsa_backward_attn.argtypes = [PP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P]
+    lib.hsa_select_backward.argtypes = [PP, P, P, P, P, P, P, P, P, SZ, P]
+    for f in ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
+              "hsa_backward_attn", "hsa_select_backward"):
         getattr(lib, f).restype = I32
     lib.hsa_attn_workspace_size.argtypes = [PP, ctypes.c_int]
     lib.hsa_attn_workspace_size.restype = SZ
@@ -223,6 +228,61 @@ def hsa_backward(Q, K, V, Kbar, idx, w, dO, S: int, sm_scale: float = 0.0,
                                _ptr(w), _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(ws), nb,
                                _stream(Q.device)), "hsa_backward")
     return dQ, dK, dV
+
+
+def hsa_backward_attn(Q, K, V, idx, w, dO, S: int, sm_scale: float = 0.0, out=None,
+                      dw: Optional[torch.Tensor] = None, accumulate_dw: bool = False,
+                      workspace: Optional[torch.Tensor] = None, off_by_one: bool = False):
+    """(dQ, dK, dV, dw) of sum(dO * O) for one layer whose selection comes from inputs of
+    its own: no score term reaches Q or K; dw [B, L, G, k] float32 = d loss / d w, written,
+    or added to the given dw with accumulate_dw."""
+    B, L, H, d = Q.shape
+    G, k = K.shape[2], idx.shape[-1]
+    for t, n, shp in ((Q, "Q", None), (K, "K", (B, L, G, d)), (V, "V", (B, L, G, d)),
+                      (dO, "dO", (B, L, H, d))):
+        _need(t, n, shp, Q.dtype, Q.device)
+    _need(idx, "idx", (B, L, G, k), torch.int32, Q.device)
+    _need(w, "w", (B, L, G, k), torch.float32, Q.device)
+    if dw is None:
+        if accumulate_dw:
+            raise ValueError("accumulate_dw needs the dw to add to")
+        dw = torch.empty((B, L, G, k), dtype=torch.float32, device=Q.device)
+    _need(dw, "dw", (B, L, G, k), torch.float32, Q.device)
+    p = make_params(B, L, H, G, d, S, k, Q.dtype, sm_scale, off_by_one=off_by_one)
+    if out is None:
+        out = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
+    dQ, dK, dV = out
+    ws, nb = _workspace(p, HSA_OP_BACKWARD, Q.device, workspace)
+    _check(load().hsa_backward_attn(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), _ptr(idx),
+                                    _ptr(w), _ptr(dO), _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(dw),
+                                    1 if accumulate_dw else 0, _ptr(ws), nb,
+                                    _stream(Q.device)), "hsa_backward_attn")
+    return dQ, dK, dV, dw
+
+
+def hsa_select_backward(Qs, Ks, idx, w, dw, G: int, S: int, sel_scale: float = 0.0,
+                        stick_breaking: bool = False, out=None,
+                        workspace: Optional[torch.Tensor] = None):
+    """(dQs, dKs) through the selection scores s = alpha q~ . Ks_c for d loss / d w = dw:
+    Qs [B, L, G h, d_sel] (h = 1 for selection inputs of their own), Ks [B, C, G, d_sel]
+    float32; dQs like Qs, dKs [B, C, G, d_sel] float32."""
+    B, L, H, d = Qs.shape
+    k = idx.shape[-1]
+    C = L // S
+    _need(Qs, "Qs")
+    _need(Ks, "Ks", (B, C, G, d), torch.float32, Qs.device)
+    for t, n in ((idx, "idx"), (w, "w"), (dw, "dw")):
+        _need(t, n, (B, L, G, k), torch.int32 if n == "idx" else torch.float32, Qs.device)
+    p = make_params(B, L, H, G, d, S, k, Qs.dtype, 0.0, sel_scale, stick_breaking)
+    if out is None:
+        out = (torch.empty_like(Qs), torch.empty((B, C, G, d), dtype=torch.float32,
+                                                 device=Qs.device))
+    dQs, dKs = out
+    ws, nb = _workspace(p, HSA_OP_SELECT_BACKWARD, Qs.device, workspace)
+    _check(load().hsa_select_backward(ctypes.byref(p), _ptr(Qs), _ptr(Ks), _ptr(idx), _ptr(w),
+                                      _ptr(dw), _ptr(dQs), _ptr(dKs), _ptr(ws), nb,
+                                      _stream(Qs.device)), "hsa_select_backward")
+    return dQs, dKs
 
 
 def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,

@@ -131,6 +131,23 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
         }
     }
     __syncthreads();
+    if (dm.dwo != nullptr) {
+        // attention alone: dw per slot (0 in empty slots); ds = 0, so the key pass adds no
+        // landmark term
+        if (tid < k) {
+            const int c = idx[sel + tid];
+            const float v = (c >= 0 && c < ncand) ? dwl[tid] : 0.f;
+            float* o = dm.dwo + sel + tid;
+            *o = dm.dwacc ? *o + v : v;
+            ds_out[sel + tid] = 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < NACC; ++r) {
+            const int i = tid + r * kThreads;
+            if (i < h * D) dQ[qoff + i] = from_f32<T>(acc[r]);
+        }
+        return;
+    }
     // chunk-weight Jacobian (softmax or stick-breaking) and the score term
     float wdw = 0.f;
     for (int i = 0; i < k; ++i) {

@@ -62,8 +62,8 @@ constexpr int kStoresPerStep = 3;   // global stores per lane of one dq step (2 
 constexpr size_t kTrashBytes = HG * D * 2 + 64 * 8;
 
 struct FusedWs {
-    size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, trash,
-        end;
+    size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, kmean,
+        trash, end;
 };
 __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     FusedWs l;
@@ -88,7 +88,10 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     l.pv = l.pk + (size_t)kStreamWGs * 2 * CS * D * 4;
     l.pkb = l.pv + (size_t)kStreamWGs * 2 * CS * D * 4;
     l.dkbar = l.pkb + (size_t)kStreamWGs * 2 * D * 4;
-    l.trash = l.dkbar + align256(R * D * 4);
+    // the layer's own key means, for the off-by-one term of dQ when the backward is of the
+    // attention alone (no landmarks are given then)
+    l.kmean = l.dkbar + align256(R * D * 4);
+    l.trash = l.kmean + align256(R * D * 4);
     l.end = l.trash + kTrashBytes;
     return l;
 }
@@ -519,8 +522,17 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     }
     const float dws = __shfl(dwl, canon, 64);
     const float wd = valid ? wl * dws : 0.f;
+    const bool attn_only = dm.dwo != nullptr;
     float dsl;
-    if (dm.stick) {
+    if (attn_only) {
+        // attention alone: every slot holding a chunk gets the chunk's dw; no score term
+        if (lane < k) {
+            float* o = dm.dwo + so + lane;
+            const float v = valid ? dws : 0.f;
+            *o = dm.dwacc ? *o + v : v;
+        }
+        dsl = 0.f;
+    } else if (dm.stick) {
         // stick-breaking: b = w / (1 - weight of the earlier valid slots), and
         // ds = (1 - b) w dw - b (sum of w dw over the later valid slots)
         float before = 0.f, tail = 0.f;
@@ -575,11 +587,15 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
             }
             // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
             sg[j] = (use[j] && dm.off1) ? dwc[((so + s) * HG + head) * 2 + 1] : 0.f;
+            // Kbar_c: the landmark term, and off by one the mean-key term of the partials
+            // (given the attention alone, the launcher passes the layer's key means)
             const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
-            const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
+            const bool need_kb = ncand > 0 && (!attn_only || dm.off1);
+            const float* kb = need_kb ? Kbar + (kbbase + (size_t)cc * dm.G) * D + c0 : nullptr;
 #pragma unroll
-            for (int v = 0; v < 4; ++v) kv[j][v] = (ncand > 0) ? *reinterpret_cast<const float4*>(kb + 4 * v)
-                                                              : float4{0.f, 0.f, 0.f, 0.f};
+            for (int v = 0; v < 4; ++v)
+                kv[j][v] = need_kb ? *reinterpret_cast<const float4*>(kb + 4 * v)
+                                   : float4{0.f, 0.f, 0.f, 0.f};
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -611,6 +627,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     *reinterpret_cast<bf16x8_t*>(op) = o0;
     *reinterpret_cast<bf16x8_t*>(op + 8) = o1;
 
+    if (attn_only) return;              // q~ only serves the landmark term
     // q~ = sum over the group's heads (lanes with the same column block): rows of 16 lanes
     // pair heads 2m, 2m + 1 (lane ^ 8), then across rows (lane ^ 16, lane ^ 32)
     float qs[16];
@@ -758,7 +775,9 @@ __global__ __launch_bounds__(NT) void bwd_finish(
     }
     if (tid < 32) {
         float4 s{0.f, 0.f, 0.f, 0.f};
-        if (wf == wl) {
+        if (dm.dwo != nullptr) {
+            // attention alone: no landmark term
+        } else if (wf == wl) {
             s = *reinterpret_cast<const float4*>(dkbar + (size_t)r * D + 4 * tid);
         } else {
             for (int wg = wf; wg <= wl; ++wg) {
@@ -854,6 +873,12 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     const int nwords = cdiv(dm.L, 32);
     hipError_t e = launch_selection_bitmap(dm, idx, bmp, st);
     if (e != hipSuccess) return e;
+    if (dm.dwo != nullptr && dm.off1 && dm.C > 0) {
+        float* km = (float*)(wsb + l.kmean);
+        e = launch_landmarks(dm, true, K, km, false, 0, dm.C, st);
+        if (e != hipSuccess) return e;
+        Kbar = km;
+    }
     if (R > 0) {
         {
             HSA_TIMED("bwd_plan", st);
@@ -880,7 +905,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (R > 0) {
+    if (R > 0 && dm.dwo == nullptr) {
         HSA_TIMED("bwd_lmk_stream", st);
         hipLaunchKernelGGL(bwd_lmk_stream, dim3(kStreamWGs), dim3(NT), 0, st, dm,
                            (const int*)pairsel, (const float*)dsb, (const __bf16*)qs,

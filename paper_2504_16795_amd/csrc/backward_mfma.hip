@@ -264,12 +264,22 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
                         [&](int m) { return sm.dw[tau * k + m]; },
                         [&](int m) { return sm.oidx[tau * k + m] >= 0; });
     };
+    const bool attn_only = dm.dwo != nullptr;
     for (int s = 0; s < k; ++s) {
+        const size_t so = (((size_t)b * dm.L + t_row) * dm.G + g) * k + s;
+        if (attn_only) {
+            // attention alone: dw per slot, ds = 0 (no landmark term in the key pass)
+            if (grp == 0 && (row & 7) == 0) {
+                const float v = sm.oidx[tau * k + s] >= 0 ? sm.dw[tau * k + s] : 0.f;
+                dm.dwo[so] = dm.dwacc ? dm.dwo[so] + v : v;
+                ds_out[so] = 0.f;
+            }
+            continue;
+        }
         const float dsv = slot_ds(s);
-        if (grp == 0 && (row & 7) == 0)
-            ds_out[(((size_t)b * dm.L + t_row) * dm.G + g) * k + s] = dsv;
+        if (grp == 0 && (row & 7) == 0) ds_out[so] = dsv;
     }
-    if (ncand > 0) {
+    if (ncand > 0 && !attn_only) {
 #pragma unroll 4
         for (int s = 0; s < k; ++s) {
             const int c = sm.oidx[tau * k + s];

@@ -17,6 +17,11 @@ struct Dims {
     int off1;       // attention inside a chunk: 0 softmax, 1 softmax off by one (an extra
                     // logit 0 with no value: the row maximum covers it, and the normaliser
                     // gains exp(0 - max))
+    // backward of the attention alone (the selection scores come from inputs of their
+    // own): dw = d loss / d w per (b, t, g, slot) goes to dwo (added to it with dwacc),
+    // and no score term reaches Q or K.  nullptr: the full backward.
+    float* dwo;
+    int dwacc;
 };
 
 // bfloat16 storage type of the generic kernels (bit pattern only).
@@ -296,6 +301,12 @@ hipError_t launch_backward(const Dims& dm, bool in_bf16, const void* Q, const vo
                            const void* V, const float* Kbar, const int32_t* idx,
                            const float* w, const void* dO, void* dQ, void* dK, void* dV,
                            void* ws, hipStream_t st);
+size_t select_backward_workspace(const Dims& dm);
+bool select_backward_supported(const Dims& dm);
+hipError_t launch_select_backward(const Dims& dm, bool in_bf16, const void* Q,
+                                  const float* Kbar, const int32_t* idx, const float* w,
+                                  const float* dw, void* dQ, float* dKbar, void* ws,
+                                  hipStream_t st);
 size_t decode_workspace(const Dims& dm);
 hipError_t launch_decode(const Dims& dm, bool in_bf16, const void* q, const void* Kc,
                          const void* Vc, const void* Kbar, bool kbar_bf16,

@@ -37,7 +37,9 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
     } while (0)
 
 // Shape checks shared by every op; fills the kernel-side description.
-hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
+// wide_rows: the call is a selection over inputs of its own, whose rows may be longer than
+// an attention head (h = 1, bf16, 256 / 512 / 1024 columns)
+hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm, bool wide_rows = false) {
     if (p == nullptr) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "params is NULL");
     if (p->batch < 0 || p->seqlen < 0)
         return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "batch and seqlen must be >= 0");
@@ -56,8 +58,13 @@ hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
                     "are supported", p->flags);
     const int h = p->n_qheads / p->n_kvheads;
     if (h > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "at most 16 query heads per KV head");
-    if (p->head_dim != 64 && p->head_dim != 128)
-        return fail(HSA_ATTN_ERR_UNSUPPORTED, "head_dim %d not in {64, 128}", p->head_dim);
+    const bool wide = wide_rows && h == 1 && p->dtype == HSA_DTYPE_BF16 &&
+                      (p->head_dim == 256 || p->head_dim == 512 || p->head_dim == 1024);
+    if (p->head_dim != 64 && p->head_dim != 128 && !wide)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED,
+                    "head_dim %d not in {64, 128} (a selection over its own inputs also takes "
+                    "256, 512 or 1024 with n_qheads == n_kvheads, bf16)",
+                    p->head_dim);
     if (p->chunk != 16 && p->chunk != 32 && p->chunk != 64 && p->chunk != 128)
         return fail(HSA_ATTN_ERR_UNSUPPORTED, "chunk %d not in {16, 32, 64, 128}", p->chunk);
     if (p->topk > 32) return fail(HSA_ATTN_ERR_UNSUPPORTED, "topk %d > 32", p->topk);
@@ -79,6 +86,8 @@ hsa_attn_status_t make_dims(const hsa_attn_params_t* p, hsa::Dims* dm) {
     dm->alpha = p->sel_scale > 0.f ? p->sel_scale : (float)(1.0 / sqrt((double)h * p->head_dim));
     dm->stick = (p->flags & HSA_FLAG_STICK_BREAKING) ? 1 : 0;
     dm->off1 = (p->flags & HSA_FLAG_SOFTMAX_OFF_BY_ONE) ? 1 : 0;
+    dm->dwo = nullptr;
+    dm->dwacc = 0;
     return HSA_ATTN_OK;
 }
 
@@ -93,6 +102,7 @@ size_t op_workspace(const hsa::Dims& dm, bool in_bf16, int op) {
         case HSA_OP_FORWARD: return hsa::forward_workspace(dm, in_bf16);
         case HSA_OP_BACKWARD: return hsa::backward_workspace(dm);
         case HSA_OP_DECODE: return hsa::decode_workspace(dm);
+        case HSA_OP_SELECT_BACKWARD: return hsa::select_backward_workspace(dm);
         default: return 0;
     }
 }
@@ -136,7 +146,7 @@ hsa_attn_status_t hsa_select_topk(const hsa_attn_params_t* p, const void* Q, con
                                   int32_t* idx, float* w, void* ws, size_t ws_bytes,
                                   void* stream) {
     hsa::Dims dm;
-    hsa_attn_status_t s = make_dims(p, &dm);
+    hsa_attn_status_t s = make_dims(p, &dm, true);
     if (s != HSA_ATTN_OK) return s;
     (void)ws;
     (void)ws_bytes;
@@ -195,6 +205,60 @@ hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const 
                     "hsa_backward");
 }
 
+hsa_attn_status_t hsa_backward_attn(const hsa_attn_params_t* p, const void* Q, const void* K,
+                                    const void* V, const int32_t* idx, const float* w,
+                                    const void* dO, void* dQ, void* dK, void* dV, float* dw,
+                                    int32_t accumulate_dw, void* ws, size_t ws_bytes,
+                                    void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (dm.B == 0 || dm.L == 0) return ok();
+    s = check_ws(dm, p->dtype == HSA_DTYPE_BF16, HSA_OP_BACKWARD, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(Q, "Q");
+    CHECK_PTR(K, "K");
+    CHECK_PTR(V, "V");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    CHECK_PTR(dO, "dO");
+    CHECK_PTR(dQ, "dQ");
+    CHECK_PTR(dK, "dK");
+    CHECK_PTR(dV, "dV");
+    CHECK_PTR(dw, "dw");
+    dm.dwo = dw;
+    dm.dwacc = accumulate_dw != 0 ? 1 : 0;
+    return launched(hsa::launch_backward(dm, p->dtype == HSA_DTYPE_BF16, Q, K, V, nullptr, idx,
+                                         w, dO, dQ, dK, dV, ws, (hipStream_t)stream),
+                    "hsa_backward_attn");
+}
+
+hsa_attn_status_t hsa_select_backward(const hsa_attn_params_t* p, const void* Q,
+                                      const float* Kbar, const int32_t* idx, const float* w,
+                                      const float* dw, void* dQ, float* dKbar, void* ws,
+                                      size_t ws_bytes, void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm, true);
+    if (s != HSA_ATTN_OK) return s;
+    if (!hsa::select_backward_supported(dm))
+        return fail(HSA_ATTN_ERR_UNSUPPORTED, "head_dim %d", dm.d);
+    if (dm.B == 0 || dm.L == 0) return ok();
+    s = check_ws(dm, p->dtype == HSA_DTYPE_BF16, HSA_OP_SELECT_BACKWARD, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(Q, "Q");
+    if (dm.C > 0) {
+        CHECK_PTR(Kbar, "Kbar");
+        CHECK_PTR(dKbar, "dKbar");
+    }
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    CHECK_PTR(dw, "dw");
+    CHECK_PTR(dQ, "dQ");
+    return launched(hsa::launch_select_backward(dm, p->dtype == HSA_DTYPE_BF16, Q, Kbar, idx, w,
+                                                dw, dQ, dKbar, ws, (hipStream_t)stream),
+                    "hsa_select_backward");
+}
+
 hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const void* Kcache,
                              const void* Vcache, const void* Kbar_cache, hsa_dtype_t kbar_dtype,
                              const int32_t* cache_len, void* o, int32_t* idx, float* w, void* ws,
@@ -227,7 +291,8 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
 
 size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op) {
     hsa::Dims dm;
-    if (make_dims(p, &dm) != HSA_ATTN_OK) return 0;
+    if (make_dims(p, &dm, op == HSA_OP_SELECT || op == HSA_OP_SELECT_BACKWARD) != HSA_ATTN_OK)
+        return 0;
     return op_workspace(dm, p->dtype == HSA_DTYPE_BF16, op);
 }
 

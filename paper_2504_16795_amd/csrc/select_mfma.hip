@@ -1,6 +1,9 @@
 // Chunk selection + chunk weights on matrix cores (Sec. 3.1: the top-k chunks by the
 // landmark score s_c = alpha * (sum_j q_j) . Kbar_c over the chunks before the token's own,
-// and their softmax weights), for bf16 queries with d = 128.
+// and their softmax weights), for bf16 queries with d = 128, or, for a selection over inputs
+// of its own (one query row per group, h = 1), d = 128 ND up to 1024: the products then run
+// over ND slices of 128 columns of each candidate block, and the query, exact in bf16, has
+// no lo part (two products per slice instead of three).
 //
 // Workgroup = (b, g, tile of 64 consecutive tokens), 4 waves of 16 tokens.  The scores of a
 // block of 64 candidate chunks for the tile are the product
@@ -27,7 +30,7 @@
 namespace hsa {
 namespace {
 
-constexpr int D = 128;
+constexpr int D = 128;            // columns of a staged slice
 constexpr int kMT = 64;            // tokens per workgroup
 constexpr int kNW = 4;             // waves, 16 tokens each
 constexpr int kNT = kNW * 64;
@@ -44,11 +47,15 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
     return ((uint64_t)hi << 32) | lo;
 }
 
-template <int KC>
+// ND: slices of 128 columns (d = 128 ND); QLO: the query is a sum over h > 1 heads (fp32,
+// so it enters as a bf16 hi / lo pair); otherwise it is one bf16 row, exact.
+template <int KC, int ND, bool QLO>
 __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __restrict__ Q,
                                                       const float* __restrict__ Kbar,
                                                       int32_t* __restrict__ idx,
                                                       float* __restrict__ w, int ntiles) {
+    static_assert(ND == 1 || !QLO, "a head sum needs d = 128");
+    constexpr int DD = D * ND;         // the query / landmark row length
     __shared__ SelStage st[2];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
@@ -62,10 +69,16 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     const int ncand = valid ? t / dm.S : 0;
     const int k = dm.k;
 
-    // B operand: q~ of the wave's 16 tokens as bf16 hi / lo; the lane holds d = 32 ks +
-    // 8 grp + i of token `row` (a token past the end reads the last one; unused)
-    bf16x8_t qh[4], ql[4];
-    {
+    // B operand: q~ of the wave's 16 tokens as bf16 hi / lo; the lane holds d = 128 db +
+    // 32 ks + 8 grp + i of token `row` (a token past the end reads the last one; unused)
+    bf16x8_t qh[ND][4], ql[QLO ? 4 : 1];
+    if constexpr (!QLO) {
+        const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + g) * DD + 8 * grp;
+#pragma unroll
+        for (int db = 0; db < ND; ++db)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) qh[db][ks] = ld_bf16x8(qp + D * db + 32 * ks);
+    } else {
         float qs[4][8];
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
@@ -88,21 +101,23 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 const __bf16 h = f2bf(qs[ks][i]);
-                qh[ks][i] = h;
+                qh[0][ks][i] = h;
                 ql[ks][i] = f2bf(qs[ks][i] - (float)h);
             }
     }
 
-    // staging: wave w converts rows 16 w .. 16 w + 15 of a block; lane l covers row
-    // 16 w + 2 i + l / 32 (i < 8), floats 4 (l % 32) .. +3
-    const size_t cstride = (size_t)dm.G * D;
-    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * D + 4 * (lane & 31);
+    // staging of stage si (candidate block si / ND, columns 128 (si % ND) ..): wave w
+    // converts rows 16 w .. 16 w + 15; lane l covers row 16 w + 2 i + l / 32 (i < 8),
+    // floats 4 (l % 32) .. +3 of the slice
+    const size_t cstride = (size_t)dm.G * DD;
+    const float* kb = Kbar + ((size_t)b * dm.C * dm.G + g) * DD + 4 * (lane & 31);
     float4 reg[8];
-    auto load_block = [&](int blk) __attribute__((always_inline)) {
+    auto load_block = [&](int si) __attribute__((always_inline)) {
+        const int blk = si / ND, db = si % ND;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int c = min(blk * kCB + 16 * wave + 2 * i + (lane >> 5), nwg - 1);
-            reg[i] = *reinterpret_cast<const float4*>(kb + (size_t)c * cstride);
+            reg[i] = *reinterpret_cast<const float4*>(kb + (size_t)c * cstride + D * db);
         }
     };
     auto store_block = [&](int s) __attribute__((always_inline)) {
@@ -134,34 +149,42 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     row_read_offsets(lane, koff);
     const float alpha = dm.alpha;
     const int nblk = cdiv(nwg, kCB);
+    const int nst = nblk * ND;         // stages: (candidate block, column slice)
     if (nblk > 0) {
         load_block(0);
         store_block(0);
     }
+    constexpr int MB = kCB / 16;
     for (int blk = 0; blk < nblk; ++blk) {
-        __syncthreads();               // block blk staged; the other stage's readers are done
-        if (blk + 1 < nblk) load_block(blk + 1);
-        const SelStage& sb = st[blk & 1];
-        // the 4 row blocks' products interleaved (independent accumulators), then the
-        // candidates
-        constexpr int MB = kCB / 16;
+        // the 4 row blocks' products interleaved (independent accumulators) over the
+        // block's column slices, then the candidates
         f32x4_t acc[MB];
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) acc[mb] = zero4();
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) {
-            bf16x8_t ah[MB], al[MB];
+        for (int db = 0; db < ND; ++db) {
+            const int si = blk * ND + db;
+            __syncthreads();           // stage si staged; the other stage's readers are done
+            if (si + 1 < nst) load_block(si + 1);
+            const SelStage& sb = st[si & 1];
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                ah[mb] = ld_bf16x8(sb.hi + koff[ks] + mb * 2048);
-                al[mb] = ld_bf16x8(sb.lo + koff[ks] + mb * 2048);
+            for (int ks = 0; ks < 4; ++ks) {
+                bf16x8_t ah[MB], al[MB];
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) {
+                    ah[mb] = ld_bf16x8(sb.hi + koff[ks] + mb * 2048);
+                    al[mb] = ld_bf16x8(sb.lo + koff[ks] + mb * 2048);
+                }
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(ah[mb], qh[db][ks], acc[mb]);
+                if constexpr (QLO) {
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(ah[mb], ql[ks], acc[mb]);
+                }
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(al[mb], qh[db][ks], acc[mb]);
             }
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(ah[mb], qh[ks], acc[mb]);
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(ah[mb], ql[ks], acc[mb]);
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(al[mb], qh[ks], acc[mb]);
+            if (si + 1 < nst) store_block((si + 1) & 1);
         }
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
@@ -183,7 +206,6 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
                 }
             }
         }
-        if (blk + 1 < nblk) store_block((blk + 1) & 1);
     }
 
     // merge the lists of a token's 4 lanes (l, l ^ 16, l ^ 32, l ^ 48): the top KC of two
@@ -234,17 +256,31 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     }
 }
 
+template <int KC, int ND, bool QLO>
+void launch_nd(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
+               hipStream_t st) {
+    const int ntiles = cdiv(dm.L, kMT);
+    hipLaunchKernelGGL((select_mfma<KC, ND, QLO>), dim3(ntiles * dm.B * dm.G), dim3(kNT), 0, st,
+                       dm, (const __bf16*)Q, Kbar, idx, w, ntiles);
+}
+
 template <int KC>
 void launch_kc_mfma(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
                     hipStream_t st) {
-    const int ntiles = cdiv(dm.L, kMT);
-    hipLaunchKernelGGL((select_mfma<KC>), dim3(ntiles * dm.B * dm.G), dim3(kNT), 0, st, dm,
-                       (const __bf16*)Q, Kbar, idx, w, ntiles);
+    switch (dm.d) {
+        case 256: launch_nd<KC, 2, false>(dm, Q, Kbar, idx, w, st); break;
+        case 512: launch_nd<KC, 4, false>(dm, Q, Kbar, idx, w, st); break;
+        case 1024: launch_nd<KC, 8, false>(dm, Q, Kbar, idx, w, st); break;
+        default:
+            if (dm.h > 1) launch_nd<KC, 1, true>(dm, Q, Kbar, idx, w, st);
+            else launch_nd<KC, 1, false>(dm, Q, Kbar, idx, w, st);
+    }
 }
 
 }  // namespace
 
 bool select_mfma_supported(const Dims& dm, bool in_bf16) {
+    if (dm.d > D) return in_bf16 && dm.h == 1 && dm.k <= 32;    // only path for wide rows
     return in_bf16 && dm.d == D && dm.k <= 32 && !getenv("HSA_FORCE_GENERIC");
 }
 

@@ -119,3 +119,37 @@ def test_status_strings(lib):
     for s in range(5):
         assert lib.hsa_attn_status_string(s)
     assert lib.hsa_attn_status_string(99) == b"unknown status"
+
+
+def test_wide_selection_rows_only_for_selection_calls(lib):
+    """Rows of 256 / 512 / 1024 columns are a selection over inputs of its own: accepted by
+    the selection calls (one row per group, bf16), refused by the attention calls."""
+    wide = P(H=2, G=2, d=1024)
+    assert fwd(lib, wide) == UNSUPPORTED
+    assert lib.hsa_attn_workspace_size(ctypes.byref(wide), hsa.HSA_OP_SELECT_BACKWARD) > 0
+    assert lib.hsa_attn_workspace_size(ctypes.byref(wide), hsa.HSA_OP_BACKWARD) == 0
+    # a NULL Q passes the shape checks first: INVALID, not UNSUPPORTED
+    assert lib.hsa_select_topk(ctypes.byref(wide), None, FAKE, FAKE, FAKE, None, 0,
+                               None) == INVALID
+    for bad in (P(H=16, G=2, d=1024), P(H=2, G=2, d=1024, dtype=hsa.HSA_DTYPE_F32),
+                P(H=2, G=2, d=384)):
+        assert lib.hsa_select_topk(ctypes.byref(bad), FAKE, FAKE, FAKE, FAKE, None, 0,
+                                   None) == UNSUPPORTED
+
+
+def test_backward_attn_and_select_backward_check_arguments(lib):
+    p = P()
+    n = lib.hsa_attn_workspace_size(ctypes.byref(p), hsa.HSA_OP_BACKWARD)
+    ws = ctypes.c_void_p(0x20000)
+    args = [FAKE] * 9
+    # dw is required
+    assert lib.hsa_backward_attn(ctypes.byref(p), *args, None, 0, ws, n, None) == INVALID
+    assert "dw" in lib.hsa_attn_last_error().decode()
+    assert lib.hsa_backward_attn(ctypes.byref(p), *args, FAKE, 0, ws, 16, None) == WS_SMALL
+    sp = P(H=2, G=2, d=1024)
+    m = lib.hsa_attn_workspace_size(ctypes.byref(sp), hsa.HSA_OP_SELECT_BACKWARD)
+    assert lib.hsa_select_backward(ctypes.byref(sp), FAKE, FAKE, FAKE, FAKE, None, FAKE, FAKE,
+                                   ws, m, None) == INVALID
+    assert "dw" in lib.hsa_attn_last_error().decode()
+    assert lib.hsa_select_backward(ctypes.byref(sp), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                   ws, m - 1, None) == WS_SMALL
