@@ -248,6 +248,41 @@ def bench_decode(steps, warmup, torch, hsa):
                                 "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                                 "bytes_per_launch": stream_bytes}
     out["algorithmic_bytes_per_step"] = stream_bytes + gather_bytes
+    # the same step with the key / value cache in pinned host memory: only the landmark
+    # cache stays on the GPU, and the selected chunks cross the host link each step
+    Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
+    Vh = torch.empty(Vc.shape, dtype=Vc.dtype, pin_memory=True)
+    Kh.copy_(Kc)
+    Vh.copy_(Vc)
+    wsh = torch.empty(hsa.workspace_size(p, hsa.HSA_OP_DECODE_HOST), dtype=torch.uint8,
+                      device="cuda")
+    oh, idxh, wh = torch.empty_like(o), torch.empty_like(idx), torch.empty_like(w)
+    for i in range(warmup):
+        if i == warmup // 2:
+            torch.cuda.synchronize()
+            hsa.timing_collect()
+            hsa.timing_enable(True)
+        hsa.hsa_decode_host(q, Kh, Vh, kbar, sh.S, sh.k, out=(oh, idxh, wh), workspace=wsh)
+    torch.cuda.synchronize()
+    hsa.timing_enable(False)
+    kern_h = hsa.timing_collect()
+    e0.record()
+    for _ in range(steps):
+        hsa.hsa_decode_host(q, Kh, Vh, kbar, sh.S, sh.k, out=(oh, idxh, wh), workspace=wsh)
+    e1.record()
+    torch.cuda.synchronize()
+    us_h = e0.elapsed_time(e1) / steps * 1e3
+    host = {"us_per_step": round(us_h, 3), "us_per_sequence_token": round(us_h / sh.B, 3),
+            "same_outputs_as_device_cache": bool(torch.equal(oh, o) and torch.equal(idxh, idx)
+                                                 and torch.equal(wh, w)),
+            "kernels_avg_us": {n: round(t / c * 1e3, 3) for n, (c, t) in kern_h.items()},
+            "host_bytes_per_step": gather_bytes,
+            "gpu_resident_bytes": stream_bytes}
+    ga = kern_h.get("decode_gather")
+    if ga:
+        host["gather_GBps"] = round(gather_bytes / (ga[1] / ga[0] * 1e-3) / 1e9, 1)
+    out["host_kv_cache"] = host
+    del Kh, Vh
     return out
 
 

@@ -70,7 +70,8 @@ typedef enum {
     HSA_OP_FORWARD = 2,
     HSA_OP_BACKWARD = 3,             /* also hsa_backward_attn */
     HSA_OP_DECODE = 4,
-    HSA_OP_SELECT_BACKWARD = 5
+    HSA_OP_SELECT_BACKWARD = 5,
+    HSA_OP_DECODE_HOST = 6
 } hsa_op_t;
 
 typedef struct {
@@ -217,6 +218,22 @@ const char* hsa_attn_status_string(hsa_attn_status_t s);
 
 /* Detail of the last error on the calling thread ("" if none). */
 const char* hsa_attn_last_error(void);
+
+/* Single-token decode with the key / value cache in host memory (Sec. 3.2 "Inference" and
+ * the memory offloading of Sec. 4.3: only the landmark cache stays on the GPU, and the
+ * selected chunks' keys and values are fetched from the host each step).  The same as
+ * hsa_decode, with Kcache and Vcache [B, N_cap, G, d] in pinned host memory (hipHostMalloc,
+ * or a pinned torch tensor) that the device can address; the selected chunks are read by a
+ * kernel over the host link into a device stage inside the workspace, with no host round
+ * trip.  q, Kbar_cache, cache_len, o, idx, w are device memory, as for hsa_decode.  Returns
+ * INVALID_ARGUMENT when a cache (its first or last byte) is not pinned host memory.  Same
+ * results as hsa_decode on the same cache contents (the same kernels after the gather).
+ * Workspace: hsa_attn_workspace_size(p, HSA_OP_DECODE_HOST). */
+hsa_attn_status_t hsa_decode_host(const hsa_attn_params_t* p, const void* q,
+                                  const void* Kcache_host, const void* Vcache_host,
+                                  const void* Kbar_cache, hsa_dtype_t kbar_dtype,
+                                  const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                                  void* ws, size_t ws_bytes, void* stream);
 
 #ifdef __cplusplus
 }

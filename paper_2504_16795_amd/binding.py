@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libhsa_mi355x.so")
 
 HSA_DTYPE_F32, HSA_DTYPE_BF16 = 0, 1
 (HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE,
- HSA_OP_SELECT_BACKWARD) = range(6)
+ HSA_OP_SELECT_BACKWARD, HSA_OP_DECODE_HOST) = range(7)
 HSA_FLAG_STICK_BREAKING = 2
 HSA_FLAG_SOFTMAX_OFF_BY_ONE = 1
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP"}
@@ -42,7 +42,7 @@ class HsaError(RuntimeError):
 
 
 EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
-            "hsa_backward_attn", "hsa_select_backward",
+            "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host",
             "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
             "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect")
 
@@ -65,8 +65,9 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_decode.argtypes = [PP, P, P, P, P, I32, P, P, P, P, P, SZ, P]
     lib.hsa_backward_attn.argtypes = [PP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P]
     lib.hsa_select_backward.argtypes = [PP, P, P, P, P, P, P, P, P, SZ, P]
+    lib.hsa_decode_host.argtypes = [PP, P, P, P, P, I32, P, P, P, P, P, SZ, P]
     for f in ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
-              "hsa_backward_attn", "hsa_select_backward"):
+              "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host"):
         getattr(lib, f).restype = I32
     lib.hsa_attn_workspace_size.argtypes = [PP, ctypes.c_int]
     lib.hsa_attn_workspace_size.restype = SZ
@@ -309,6 +310,39 @@ def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
                              _ptr(Kbar_cache), _dtype_code(Kbar_cache.dtype), _ptr(cache_len),
                              _ptr(o), _ptr(idx), _ptr(w), _ptr(ws), nb, _stream(q.device)),
            "hsa_decode")
+    return o, idx, w
+
+
+def hsa_decode_host(q, Kcache_host, Vcache_host, Kbar_cache, S: int, k: int,
+                    cache_len: Optional[torch.Tensor] = None, sm_scale: float = 0.0,
+                    sel_scale: float = 0.0, out=None, workspace: Optional[torch.Tensor] = None,
+                    stick_breaking: bool = False, off_by_one: bool = False):
+    """hsa_decode with the key / value cache [B, N_cap, G, d] in pinned host memory (CPU
+    tensors from pin_memory); q, the landmark cache and the outputs live on the GPU."""
+    B, H, d = q.shape
+    Ncap, G = Kcache_host.shape[1], Kcache_host.shape[2]
+    _need(q, "q")
+    for t, n in ((Kcache_host, "Kcache_host"), (Vcache_host, "Vcache_host")):
+        if not isinstance(t, torch.Tensor) or t.is_cuda or not t.is_pinned():
+            raise ValueError("%s must be a pinned CPU tensor" % n)
+        if not t.is_contiguous() or tuple(t.shape) != (B, Ncap, G, d) or t.dtype != q.dtype:
+            raise ValueError("%s must be a contiguous %s tensor of shape %s"
+                             % (n, q.dtype, (B, Ncap, G, d)))
+    _need(Kbar_cache, "Kbar_cache", (B, Ncap // S, G, d), None, q.device)
+    if cache_len is not None:
+        _need(cache_len, "cache_len", (B,), torch.int32, q.device)
+    p = make_params(B, Ncap, H, G, d, S, k, q.dtype, sm_scale, sel_scale, stick_breaking,
+                    off_by_one)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty((B, G, k), dtype=torch.int32, device=q.device),
+               torch.empty((B, G, k), dtype=torch.float32, device=q.device))
+    o, idx, w = out
+    ws, nb = _workspace(p, HSA_OP_DECODE_HOST, q.device, workspace)
+    _check(load().hsa_decode_host(ctypes.byref(p), _ptr(q), ctypes.c_void_p(Kcache_host.data_ptr()),
+                                  ctypes.c_void_p(Vcache_host.data_ptr()), _ptr(Kbar_cache),
+                                  _dtype_code(Kbar_cache.dtype), _ptr(cache_len), _ptr(o),
+                                  _ptr(idx), _ptr(w), _ptr(ws), nb, _stream(q.device)),
+           "hsa_decode_host")
     return o, idx, w
 
 

@@ -308,6 +308,11 @@ hipError_t launch_select_backward(const Dims& dm, bool in_bf16, const void* Q,
                                   const float* dw, void* dQ, float* dKbar, void* ws,
                                   hipStream_t st);
 size_t decode_workspace(const Dims& dm);
+size_t decode_host_workspace(const Dims& dm, bool in_bf16);
+hipError_t launch_decode_host(const Dims& dm, bool in_bf16, const void* q, const void* Kh,
+                              const void* Vh, const void* Kbar, bool kbar_bf16,
+                              const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                              void* ws, hipStream_t st);
 hipError_t launch_decode(const Dims& dm, bool in_bf16, const void* q, const void* Kc,
                          const void* Vc, const void* Kbar, bool kbar_bf16,
                          const int32_t* cache_len, void* o, int32_t* idx, float* w,

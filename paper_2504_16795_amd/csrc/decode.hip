@@ -15,6 +15,11 @@
 // Other shapes: stage 2 (finish), workgroup = (slot, b, g), attends the k selected chunks
 // in parallel; stage 3 (combine), workgroup = (b, g), sums their weighted partial outputs
 // in slot order.
+// With the key / value cache in host memory (Sec. 3.2: only the landmarks stay on the GPU):
+// after the scan, decode_merge writes the selection, decode_gather copies the selected
+// chunks' rows from the host cache (read by the kernel over the host link) into a compact
+// stage [B, G, k, S, d] in device memory, and the attend kernels run "staged": they take
+// the merged selection and read slot i's rows from the stage.
 #include <cstdlib>
 
 #include "chunk_lds.h"
@@ -391,7 +396,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     Dims dm, const T* __restrict__ q, const T* __restrict__ Kc, const T* __restrict__ Vc,
     const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
     const int32_t* __restrict__ cand_c, int nslices, float* __restrict__ part,
-    int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
+    int32_t* __restrict__ idx_out, float* __restrict__ w_out, int staged) {
     constexpr int DP = D + 1;
     constexpr int SMAX = 128;
     constexpr int NE = sizeof(T) == 4 ? 8192 : SMAX * D;   // S * d <= 8192 for fp32 inputs
@@ -412,17 +417,26 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     for (int i = tid; i < h * D; i += kFinThreads)
         qf[(i / D) * DP + i % D] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
     const int nc = nslices * k;
-    if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
-                                             nc, n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
+    if (staged) {                        // the selection is merged already (decode_merge)
+        if (tid < k) {
+            sel_c[tid] = idx_out[(size_t)bg * k + tid];
+            sel_w[tid] = w_out[(size_t)bg * k + tid];
+        }
         __syncthreads();
-        if (wave == 0)
-            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
-                             sel_c, sel_w, dm.stick != 0);
-        __syncthreads();
-    }
-    if (slot == 0 && tid < k) {
-        idx_out[(size_t)bg * k + tid] = sel_c[tid];
-        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    } else {
+        if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc,
+                                                 cand_c + (size_t)bg * nc, nc, n, k, mtmp,
+                                                 sel_c, sel_w, dm.stick != 0)) {
+            __syncthreads();
+            if (wave == 0)
+                merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k,
+                                 lane, sel_c, sel_w, dm.stick != 0);
+            __syncthreads();
+        }
+        if (slot == 0 && tid < k) {
+            idx_out[(size_t)bg * k + tid] = sel_c[tid];
+            w_out[(size_t)bg * k + tid] = sel_w[tid];
+        }
     }
 
     if (slot < n) {
@@ -432,7 +446,8 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         constexpr int VN = V16<T>::n;
         for (int v = tid; v < S * D / VN; v += kFinThreads) {
             const int s = v / (D / VN), e = (v % (D / VN)) * VN;
-            const size_t src = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+            const size_t src = staged ? (((size_t)bg * k + slot) * S + s) * D + e
+                                      : (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
             *reinterpret_cast<uint4*>(&ks[s * D + e]) = *reinterpret_cast<const uint4*>(Kc + src);
             *reinterpret_cast<uint4*>(&vs[s * D + e]) = *reinterpret_cast<const uint4*>(Vc + src);
         }
@@ -486,7 +501,8 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     Dims dm, const __bf16* __restrict__ q, const __bf16* __restrict__ Kc,
     const __bf16* __restrict__ Vc, const int32_t* __restrict__ cache_len,
     const float* __restrict__ cand_s, const int32_t* __restrict__ cand_c, int nslices,
-    __bf16* __restrict__ o, int32_t* __restrict__ idx_out, float* __restrict__ w_out) {
+    __bf16* __restrict__ o, int32_t* __restrict__ idx_out, float* __restrict__ w_out,
+    int staged) {
     constexpr int S = kAttS, DD = kAttD, NWV = kAttWaves, MB = S / 16, KS2 = S / 32;
     constexpr int NT = NWV * 64;
     // Per-wave V stages.  Before the first copy they hold the merge's survivors; after the
@@ -513,16 +529,24 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     for (int ks = 0; ks < 4; ++ks)
         if (row >= kAttH) qB[ks] = bf16x8_t{};
     const int nc = nslices * k;
-    if (!merge_top<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n,
-                                     k, mtmp, sel_c, sel_w, dm.stick != 0)) {
-        if (wave == 0)
-            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
-                             sel_c, sel_w, dm.stick != 0);
+    if (staged) {                        // the selection is merged already (decode_merge)
+        if (tid < k) {
+            sel_c[tid] = idx_out[(size_t)bg * k + tid];
+            sel_w[tid] = w_out[(size_t)bg * k + tid];
+        }
         __syncthreads();
-    }
-    if (tid < k) {
-        idx_out[(size_t)bg * k + tid] = sel_c[tid];
-        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    } else {
+        if (!merge_top<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc,
+                                         n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
+            if (wave == 0)
+                merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k,
+                                 lane, sel_c, sel_w, dm.stick != 0);
+            __syncthreads();
+        }
+        if (tid < k) {
+            idx_out[(size_t)bg * k + tid] = sel_c[tid];
+            w_out[(size_t)bg * k + tid] = sel_w[tid];
+        }
     }
 
     f32x4_t acc[8];
@@ -533,12 +557,14 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     const float sl2 = dm.beta * 1.44269504088896341f;
     const bool off1 = dm.off1 != 0;                  // softmax off by one
     const float mfloor = off1 ? 0.f : -INFINITY;
-    const size_t rowstride = (size_t)dm.G * DD;
+    // rows of a chunk: the cache [B, N, G, d], or the stage [B, G, k, S, d]
+    const size_t rowstride = staged ? (size_t)DD : (size_t)dm.G * DD;
     __bf16* stage = vst[wave];
     for (int slot = wave; slot < n; slot += NWV) {
         const int c = sel_c[slot];
         const float wi = sel_w[slot];
-        const size_t key0 = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * DD;
+        const size_t key0 = staged ? ((size_t)bg * k + slot) * S * DD
+                                   : ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * DD;
         // V rows into the stage (copies, issued first: older than the K loads below, so
         // the compiler's waits for those stay exact), K fragments into registers
         chunk_to_lds<S, 1>(Vc + key0, rowstride, stage, 0, lane);
@@ -605,6 +631,73 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     }
 }
 
+// The merge of stage 2 on its own, for the host-cache path: writes idx, w [B, G, k].
+__global__ __launch_bounds__(kFinThreads) void decode_merge(
+    Dims dm, const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
+    const int32_t* __restrict__ cand_c, int nslices, int32_t* __restrict__ idx_out,
+    float* __restrict__ w_out) {
+    __shared__ int sel_c[KMAX];
+    __shared__ float sel_w[KMAX];
+    __shared__ uint64_t mtmp[NW * KMAX];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int bg = blockIdx.x, b = bg / dm.G;
+    const int k = dm.k;
+    const int n = min(k, cache_tokens(cache_len, b, dm.L) / dm.S);
+    const int nc = nslices * k;
+    if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                             nc, n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
+        __syncthreads();
+        if (wave == 0)
+            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
+                             sel_c, sel_w, dm.stick != 0);
+        __syncthreads();
+    }
+    if (tid < k) {
+        idx_out[(size_t)bg * k + tid] = sel_c[tid];
+        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    }
+}
+
+// The selected chunks' K and V rows, from the cache in host memory [B, N, G, d] to the
+// stage [B, G, k, S, d]: workgroup = (slot, b, g); every thread issues all of its 16-byte
+// loads (K and V) before its stores, so a workgroup keeps 2 S d elem bytes in flight over
+// the host link.
+template <typename T, int D>
+__global__ __launch_bounds__(kFinThreads) void decode_gather(
+    Dims dm, const T* __restrict__ Kh, const T* __restrict__ Vh,
+    const int32_t* __restrict__ cache_len, const int32_t* __restrict__ idx,
+    T* __restrict__ Ks, T* __restrict__ Vs) {
+    constexpr int VN = V16<T>::n;                 // elements per 16 bytes
+    constexpr int PER = 128 * D / VN / kFinThreads;   // 16-byte vectors per thread, S <= 128
+    const int slot = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const int S = dm.S, k = dm.k;
+    const int n = min(k, cache_tokens(cache_len, b, dm.L) / S);
+    if (slot >= n) return;
+    const int c = idx[(size_t)bg * k + slot];
+    const int nv = S * D / VN;
+    uint4 kr[PER], vr[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int v = threadIdx.x + u * kFinThreads;
+        if (v < nv) {
+            const int s = v / (D / VN), e = (v % (D / VN)) * VN;
+            const size_t src = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+            kr[u] = *reinterpret_cast<const uint4*>(Kh + src);
+            vr[u] = *reinterpret_cast<const uint4*>(Vh + src);
+        }
+    }
+    const size_t dst0 = ((size_t)bg * k + slot) * S * D;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int v = threadIdx.x + u * kFinThreads;
+        if (v < nv) {
+            *reinterpret_cast<uint4*>(Ks + dst0 + (size_t)v * VN) = kr[u];
+            *reinterpret_cast<uint4*>(Vs + dst0 + (size_t)v * VN) = vr[u];
+        }
+    }
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void decode_combine(Dims dm,
                                                       const int32_t* __restrict__ cache_len,
@@ -629,16 +722,20 @@ bool decode_mfma_shape(const Dims& dm) {
 }
 
 struct DecodeWs {
-    size_t cs, cc, part, end;
+    size_t cs, cc, part, kst, vst, end;
 };
-DecodeWs decode_ws(const Dims& dm) {
+// elem: bytes per K / V element, when the stages of the host-cache path are included
+DecodeWs decode_ws(const Dims& dm, int elem = 0) {
     const size_t nslices = (size_t)cdiv(dm.C > 0 ? dm.C : 1, SL);
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     DecodeWs l;
     l.cs = 0;
     l.cc = al(l.cs + (size_t)dm.B * dm.G * nslices * dm.k * 4);
     l.part = al(l.cc + (size_t)dm.B * dm.G * nslices * dm.k * 4);
-    l.end = al(l.part + (size_t)dm.B * dm.G * dm.k * dm.h * dm.d * 4);
+    l.kst = al(l.part + (size_t)dm.B * dm.G * dm.k * dm.h * dm.d * 4);
+    const size_t stage = (size_t)dm.B * dm.G * dm.k * dm.S * dm.d * elem;
+    l.vst = al(l.kst + stage);
+    l.end = al(l.vst + stage);
     return l;
 }
 
@@ -662,14 +759,64 @@ void launch_tkd(const Dims& dm, const void* q, const void* Kc, const void* Vc, c
         HSA_TIMED("decode_attend_mfma", st);
         hipLaunchKernelGGL(decode_attend_mfma, dim3(dm.B * dm.G), dim3(kAttWaves * 64), 0, st,
                            dm, (const __bf16*)q, (const __bf16*)Kc, (const __bf16*)Vc,
-                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w);
+                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w, 0);
         return;
     }
     {
         HSA_TIMED("decode_finish", st);
         hipLaunchKernelGGL((decode_finish<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
                            st, dm, (const T*)q, (const T*)Kc, (const T*)Vc, cache_len, cs, cc,
-                           nslices, part, idx, w);
+                           nslices, part, idx, w, 0);
+    }
+    {
+        HSA_TIMED("decode_combine", st);
+        hipLaunchKernelGGL((decode_combine<T, D>), dim3(dm.B * dm.G), dim3(256), 0, st, dm,
+                           cache_len, part, (T*)o);
+    }
+}
+
+// Host-cache path: scan, merge, gather into the stages, then the attend kernels on them.
+template <typename T, typename Tk, int D>
+void launch_tkd_host(const Dims& dm, const void* q, const void* Kh, const void* Vh,
+                     const void* Kbar, const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                     void* ws, hipStream_t st) {
+    const int nslices = cdiv(dm.C > 0 ? dm.C : 1, SL);
+    const DecodeWs l = decode_ws(dm, (int)sizeof(T));
+    char* wb = (char*)ws;
+    float* cs = (float*)(wb + l.cs);
+    int32_t* cc = (int32_t*)(wb + l.cc);
+    float* part = (float*)(wb + l.part);
+    T* kst = (T*)(wb + l.kst);
+    T* vst = (T*)(wb + l.vst);
+    {
+        HSA_TIMED("decode_scan", st);
+        hipLaunchKernelGGL((decode_scan<T, Tk, D>), dim3(nslices, dm.B), dim3(kScanThreads), 0,
+                           st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc,
+                           nslices);
+    }
+    {
+        HSA_TIMED("decode_merge", st);
+        hipLaunchKernelGGL(decode_merge, dim3(dm.B * dm.G), dim3(kFinThreads), 0, st, dm,
+                           cache_len, cs, cc, nslices, idx, w);
+    }
+    {
+        HSA_TIMED("decode_gather", st);
+        hipLaunchKernelGGL((decode_gather<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
+                           st, dm, (const T*)Kh, (const T*)Vh, cache_len, (const int32_t*)idx,
+                           kst, vst);
+    }
+    if (decode_mfma_shape<T, D>(dm)) {
+        HSA_TIMED("decode_attend_mfma", st);
+        hipLaunchKernelGGL(decode_attend_mfma, dim3(dm.B * dm.G), dim3(kAttWaves * 64), 0, st,
+                           dm, (const __bf16*)q, (const __bf16*)kst, (const __bf16*)vst,
+                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w, 1);
+        return;
+    }
+    {
+        HSA_TIMED("decode_finish", st);
+        hipLaunchKernelGGL((decode_finish<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
+                           st, dm, (const T*)q, (const T*)kst, (const T*)vst, cache_len, cs, cc,
+                           nslices, part, idx, w, 1);
     }
     {
         HSA_TIMED("decode_combine", st);
@@ -689,6 +836,28 @@ void launch_tk(const Dims& dm, const void* q, const void* Kc, const void* Vc, co
 }  // namespace
 
 size_t decode_workspace(const Dims& dm) { return decode_ws(dm).end; }
+size_t decode_host_workspace(const Dims& dm, bool in_bf16) {
+    return decode_ws(dm, in_bf16 ? 2 : 4).end;
+}
+
+hipError_t launch_decode_host(const Dims& dm, bool in_bf16, const void* q, const void* Kh,
+                              const void* Vh, const void* Kbar, bool kbar_bf16,
+                              const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                              void* ws, hipStream_t st) {
+    if (dm.B == 0) return hipSuccess;
+#define HSA_HOST_LAUNCH(T, Tk)                                                                  \
+    (dm.d == 128 ? launch_tkd_host<T, Tk, 128>(dm, q, Kh, Vh, Kbar, cache_len, o, idx, w, ws, st) \
+                 : launch_tkd_host<T, Tk, 64>(dm, q, Kh, Vh, Kbar, cache_len, o, idx, w, ws, st))
+    if (in_bf16) {
+        if (kbar_bf16) HSA_HOST_LAUNCH(bf16, bf16);
+        else HSA_HOST_LAUNCH(bf16, float);
+    } else {
+        if (kbar_bf16) HSA_HOST_LAUNCH(float, bf16);
+        else HSA_HOST_LAUNCH(float, float);
+    }
+#undef HSA_HOST_LAUNCH
+    return hipGetLastError();
+}
 
 hipError_t launch_decode(const Dims& dm, bool in_bf16, const void* q, const void* Kc,
                          const void* Vc, const void* Kbar, bool kbar_bf16,

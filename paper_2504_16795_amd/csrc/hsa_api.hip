@@ -103,6 +103,7 @@ size_t op_workspace(const hsa::Dims& dm, bool in_bf16, int op) {
         case HSA_OP_BACKWARD: return hsa::backward_workspace(dm);
         case HSA_OP_DECODE: return hsa::decode_workspace(dm);
         case HSA_OP_SELECT_BACKWARD: return hsa::select_backward_workspace(dm);
+        case HSA_OP_DECODE_HOST: return hsa::decode_host_workspace(dm, in_bf16);
         default: return 0;
     }
 }
@@ -115,6 +116,30 @@ hsa_attn_status_t check_ws(const hsa::Dims& dm, bool in_bf16, int op, const void
         return fail(HSA_ATTN_ERR_WORKSPACE_TOO_SMALL, "workspace of %zu bytes, %zu needed",
                     ws_bytes, need);
     CHECK_PTR(ws, "ws");
+    return HSA_ATTN_OK;
+}
+
+// A cache in host memory: pinned memory the device can address, from its first to its last
+// byte; *dev receives the device-side address of p.
+hsa_attn_status_t host_cache(const void* p, size_t bytes, const char* name, const void** dev) {
+    if (p == nullptr) return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "%s is NULL", name);
+    if (!aligned16(p))
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "%s is not 16-byte aligned", name);
+    for (const char* x : {(const char*)p, (const char*)p + bytes - 1}) {
+        hipPointerAttribute_t a;
+        if (hipPointerGetAttributes(&a, x) != hipSuccess || a.type != hipMemoryTypeHost) {
+            (void)hipGetLastError();
+            return fail(HSA_ATTN_ERR_INVALID_ARGUMENT,
+                        "%s is not pinned host memory over its %zu bytes (allocate it with "
+                        "hipHostMalloc)", name, bytes);
+        }
+    }
+    void* d = nullptr;
+    if (hipHostGetDevicePointer(&d, const_cast<void*>(p), 0) != hipSuccess || d == nullptr) {
+        (void)hipGetLastError();
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "%s has no device mapping", name);
+    }
+    *dev = d;
     return HSA_ATTN_OK;
 }
 
@@ -287,6 +312,43 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
                                        Kbar_cache, kbar_dtype == HSA_DTYPE_BF16, cache_len, o,
                                        idx, w, ws, (hipStream_t)stream),
                     "hsa_decode");
+}
+
+hsa_attn_status_t hsa_decode_host(const hsa_attn_params_t* p, const void* q,
+                                  const void* Kcache_host, const void* Vcache_host,
+                                  const void* Kbar_cache, hsa_dtype_t kbar_dtype,
+                                  const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                                  void* ws, size_t ws_bytes, void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (kbar_dtype != HSA_DTYPE_F32 && kbar_dtype != HSA_DTYPE_BF16)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown kbar_dtype %d", (int)kbar_dtype);
+    if (dm.G > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "decode supports at most 16 KV heads");
+    if (dm.B == 0) return ok();
+    const bool bf = p->dtype == HSA_DTYPE_BF16;
+    s = check_ws(dm, bf, HSA_OP_DECODE_HOST, ws, ws_bytes);
+    if (s != HSA_ATTN_OK) return s;
+    CHECK_PTR(q, "q");
+    CHECK_PTR(o, "o");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    const void* kd = nullptr;
+    const void* vd = nullptr;
+    if (dm.C > 0) {
+        const size_t bytes = (size_t)dm.B * dm.L * dm.G * dm.d * (bf ? 2 : 4);
+        s = host_cache(Kcache_host, bytes, "Kcache_host", &kd);
+        if (s != HSA_ATTN_OK) return s;
+        s = host_cache(Vcache_host, bytes, "Vcache_host", &vd);
+        if (s != HSA_ATTN_OK) return s;
+        CHECK_PTR(Kbar_cache, "Kbar_cache");
+    }
+    if (cache_len != nullptr && ((uintptr_t)cache_len & 3u))
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "cache_len is not 4-byte aligned");
+    return launched(hsa::launch_decode_host(dm, bf, q, kd, vd, Kbar_cache,
+                                            kbar_dtype == HSA_DTYPE_BF16, cache_len, o, idx, w,
+                                            ws, (hipStream_t)stream),
+                    "hsa_decode_host");
 }
 
 size_t hsa_attn_workspace_size(const hsa_attn_params_t* p, int op) {
