@@ -290,19 +290,11 @@ def bench_shared(steps, warmup, torch, hsa):
     """Sec. 4.3's setting: three attention layers sharing one selection over inputs of their
     own (d_sel = h d_h = 1024), forward and backward of all three plus the selection and its
     backward per step; and the same with a selection (and its backward) per layer."""
-    B, L, H, G, d, S, k = 8, 4096, 16, 2, 128, 64, 8
-    dsel, nl = (H // G) * d, 3
-    gen = torch.Generator(device="cuda")
-    gen.manual_seed(2504)
-
-    def rnd(*shape, std=1.0, dt=torch.bfloat16):
-        return (torch.randn(shape, generator=gen, device="cuda") * std).to(dt)
-
-    sc = d ** -0.5
-    layers = [dict(Q=rnd(B, L, H, d, std=sc), K=rnd(B, L, G, d, std=sc),
-                   V=rnd(B, L, G, d, std=sc), dO=rnd(B, L, H, d)) for _ in range(nl)]
-    Qs = rnd(B, L, G, dsel)
-    Ks = rnd(B, L // S, G, dsel, dt=torch.float32)
+    import hsa_synth
+    sh = hsa_synth.WORKLOADS["shared_x3_L4K_bf16"]["shape"]
+    B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
+    dsel = (H // G) * d
+    layers, Qs, Ks = hsa_synth.make_shared_selection_inputs("shared_x3_L4K_bf16")
     idx = torch.empty((B, L, G, k), dtype=torch.int32, device="cuda")
     w = torch.empty((B, L, G, k), dtype=torch.float32, device="cuda")
     dw = torch.empty_like(w)

@@ -68,6 +68,9 @@ WORKLOADS: Dict[str, dict] = {
                            kind="decode", mu_std=0.5),
     "wide_L16K_bf16": dict(shape=HsaShape(4, 16384, 32, 4, 128, 128, 16, "bf16"), seed=5,
                            kind="lowrank", mu_std=0.0),
+    # three attention layers sharing one selection over inputs of their own (d_sel = h d)
+    "shared_x3_L4K_bf16": dict(shape=HsaShape(8, 4096, 16, 2, 128, 64, 8, "bf16"), seed=2504,
+                               kind="shared", mu_std=0.0, layers=3),
 }
 
 
@@ -239,3 +242,31 @@ def make_decode_inputs(shape: HsaShape, seed: int, n_cache: Optional[int] = None
                 keys = r * (0.9 * ub[None, :] + math.sqrt(0.19) * x)
                 kc[b, p * S:(p + 1) * S, g] = keys.to(tdt)
     return {"q": q, "Kc": kc, "Vc": vc, "planted": planted}
+
+
+def make_shared_selection_inputs(name: str = "shared_x3_L4K_bf16", device: str = "cuda"):
+    """Inputs of several attention layers sharing one selection over inputs of its own
+    (torch tensors, drawn with torch's seeded Philox generator on `device`).
+
+    Per layer: Q, K, V ~ N(0, 1/d), dO ~ N(0, 1) (workload dtype).  Selection queries
+    Qs [B, L, G, h d] ~ N(0, 1) (workload dtype) and chunk representations Ks [B, C, G, h d]
+    ~ N(0, 1) float32, so the scores Qs . Ks / sqrt(h d) are about N(0, 1).
+    Returns (layers: list of dicts, Qs, Ks)."""
+    import torch
+    wl = WORKLOADS[name]
+    sh = wl["shape"]
+    B, L, H, G, d, S = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S
+    dsel = (H // G) * d
+    tdt = torch.bfloat16 if sh.dtype == "bf16" else torch.float32
+    gen = torch.Generator(device=device)
+    gen.manual_seed(wl["seed"])
+
+    def rnd(*shape, std=1.0, dt=tdt):
+        return (torch.randn(shape, generator=gen, device=device) * std).to(dt)
+
+    sc = d ** -0.5
+    layers = [dict(Q=rnd(B, L, H, d, std=sc), K=rnd(B, L, G, d, std=sc),
+                   V=rnd(B, L, G, d, std=sc), dO=rnd(B, L, H, d)) for _ in range(wl["layers"])]
+    Qs = rnd(B, L, G, dsel)
+    Ks = rnd(B, L // S, G, dsel, dt=torch.float32)
+    return layers, Qs, Ks

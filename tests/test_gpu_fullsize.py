@@ -153,3 +153,96 @@ def test_fullsize_decode_1M(hsa_gpu):
         assert_close("o", sh, o[b:b + 1], ro, o_abs=ro_abs)
         for g in range(sh.G):
             assert int(inp["planted"][b, g]) in gi[0, g].tolist()
+
+
+def test_fullsize_decode_1M_host_cache(hsa_gpu):
+    """The bench's decode step with the key / value cache in pinned host memory: bitwise the
+    outputs of the HBM-resident decode, and one sequence against the oracle."""
+    wl = hsa_synth.WORKLOADS["decode_1M_bf16"]
+    sh = wl["shape"]
+    banner("decode_1M_bf16", "full-size decode, cache in host memory")
+    inp = hsa_synth.make_decode_inputs(sh, wl["seed"], device="cuda")
+    q, Kc, Vc = inp["q"], inp["Kc"], inp["Vc"]
+    kbar = hsa_gpu.hsa_landmarks(Kc, sh.S, kbar_dtype=torch.bfloat16)
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k)
+    Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
+    Vh = torch.empty(Vc.shape, dtype=Vc.dtype, pin_memory=True)
+    Kh.copy_(Kc)
+    Vh.copy_(Vc)
+    oh, idxh, wh = hsa_gpu.hsa_decode_host(q, Kh, Vh, kbar, sh.S, sh.k)
+    torch.cuda.synchronize()
+    assert torch.equal(idxh, idx) and torch.equal(wh, w) and torch.equal(oh, o)
+    b = 2
+    banner("decode_1M_bf16", "oracle decode of sequence %d" % b)
+    ro, ridx, rw, rgap = oracle.decode(q[b:b + 1].cpu(), Kh[b:b + 1], Vh[b:b + 1],
+                                       kbar[b:b + 1].float().cpu(), [sh.L], sh.S, sh.k)
+    ro_abs = oracle.decode(q[b:b + 1].cpu(), Kh[b:b + 1], Vh[b:b + 1].abs(),
+                           kbar[b:b + 1].float().cpu(), [sh.L], sh.S, sh.k)[0]
+    sure = rgap >= 1e-3
+    assert np.array_equal(idxh[b:b + 1].cpu().numpy()[sure], ridx[sure])
+    assert_close("o", sh, oh[b:b + 1], ro, o_abs=ro_abs)
+
+
+def test_fullsize_shared_x3_L4K(hsa_gpu):
+    """The bench's step of three layers sharing one selection over inputs of its own
+    (B8 L4096 H16/G2 d128 S64 k8, d_sel = 1024): selection, per-layer forward and
+    attention-only backward (dw accumulated), selection backward; sampled tokens and chunks
+    of two slices against the oracle, given the GPU's selection (checked on its own)."""
+    name = "shared_x3_L4K_bf16"
+    sh = hsa_synth.WORKLOADS[name]["shape"]
+    B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
+    h, C = H // G, L // S
+    dsel = h * d
+    banner(name, "full-size shared-selection step")
+    layers, Qs, Ks = hsa_synth.make_shared_selection_inputs(name)
+    idx, w = hsa_gpu.hsa_select_topk(Qs, Ks, G, S, k)
+    dw = torch.empty((B, L, G, k), dtype=torch.float32, device="cuda")
+    outs = []
+    for i, lay in enumerate(layers):
+        O = hsa_gpu.hsa_forward(lay["Q"], lay["K"], lay["V"], idx, w, S)
+        grads = hsa_gpu.hsa_backward_attn(lay["Q"], lay["K"], lay["V"], idx, w, lay["dO"], S,
+                                          dw=dw, accumulate_dw=i > 0)
+        outs.append((O,) + tuple(grads[:3]))
+    dQs, dKs = hsa_gpu.hsa_select_backward(Qs, Ks, idx, w, dw, G, S)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(17)
+    f64 = lambda t: np.ascontiguousarray(t.float().cpu().numpy(), dtype=np.float64)
+    for b, g in ((0, 0), (7, 1)):
+        banner(name, "oracle samples of slice b=%d g=%d" % (b, g))
+        hs = slice(g * h, (g + 1) * h)
+        gi = np.ascontiguousarray(idx[b, :, g].cpu().numpy())
+        gw = f64(w[b, :, g])
+        rows = np.unique(np.concatenate([[0, S, L - 1], rng.choice(L, N_ROWS, replace=False)]))
+        trows = torch.from_numpy(rows).cuda()
+        # selection on the sampled tokens
+        dms = oracle.dims(L, 1, dsel, S, k)
+        Qss, Kss = f64(Qs[b, :, g]).reshape(L, 1, dsel), f64(Ks[b, :, g])
+        ridx, rw, gap, _ = oracle.select_slice(dms, Qss, Kss, rows)
+        assert_indices(torch.from_numpy(gi[rows][None, :, None]), ridx[None, :, None],
+                       gap[None, :, None], S, tokens=rows)
+        sure = gap >= 1e-3
+        assert np.max(np.abs(gw[rows][sure] - rw[sure]), initial=0.0) <= W_ATOL
+        # each layer: O and dQ of the sampled tokens, dK and dV of sampled chunks
+        dm = oracle.dims(L, h, d, S, k, sep=True)
+        chunks = np.unique(np.concatenate([[0, C - 1], rng.choice(C, N_CHUNKS, replace=False)]))
+        key_rows = torch.from_numpy((chunks[:, None] * S + np.arange(S)[None, :]).reshape(-1)).cuda()
+        dw_ref = np.zeros((rows.size, k))
+        for lay, (O, dQ, dK, dV) in zip(layers, outs):
+            Ql, dOl = f64(lay["Q"][b, :, hs]), f64(lay["dO"][b, :, hs])
+            Kl, Vl = f64(lay["K"][b, :, g]), f64(lay["V"][b, :, g])
+            o_ref = oracle.forward_slice(dm, Ql, Kl, Vl, gi, gw, rows)
+            o_abs = oracle.forward_slice(dm, Ql, Kl, np.abs(Vl), gi, np.abs(gw), rows)
+            assert_close("O", sh, O[b, trows][:, hs], o_ref, o_abs=o_abs)
+            dq_ref, _, dwl = oracle.backward_q_slice(dm, Ql, Kl, Vl, np.zeros((C, d)), gi, gw,
+                                                     dOl, rows, with_dw=True)
+            assert_close("dQ", sh, dQ[b, trows][:, hs], dq_ref)
+            dw_ref += dwl
+            dk_ref, dv_ref = oracle.backward_kv_slice(dm, Ql, Kl, Vl, gi, gw, dOl,
+                                                      np.zeros((L, k)), chunks)
+            assert_close("dK", sh, dK[b, key_rows, g], dk_ref.reshape(-1, d))
+            assert_close("dV", sh, dV[b, key_rows, g], dv_ref.reshape(-1, d))
+        assert_close("dw", sh, dw[b, trows, g], dw_ref)
+        # the selection backward of the slice, given the GPU's summed dw
+        dqs_ref, dks_ref, _ = oracle.select_backward_slice(dms, Qss, Kss, gi, gw, f64(dw[b, :, g]))
+        assert_close("dQs", sh, dQs[b, trows, g], dqs_ref[rows, 0])
+        assert_close("dKs", sh, dKs[b, :, g], dks_ref)
