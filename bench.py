@@ -94,7 +94,7 @@ def make_training(name, torch):
     return sh, inp, dev, time.time() - t0
 
 
-def time_training(sh, dev, steps, warmup, torch, hsa):
+def time_training(sh, dev, steps, warmup, torch, hsa, stick=False, off1=False):
     B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
     Q, K, V, dO = dev["Q"], dev["K"], dev["V"], dev["dO"]
     Kbar = torch.empty((B, L // S, G, d), dtype=torch.float32, device="cuda")
@@ -110,9 +110,10 @@ def time_training(sh, dev, steps, warmup, torch, hsa):
 
     def step():
         hsa.hsa_landmarks(K, S, out=Kbar)
-        hsa.hsa_select_topk(Q, Kbar, G, S, k, idx=idx, w=w)
-        hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f)
-        hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b)
+        hsa.hsa_select_topk(Q, Kbar, G, S, k, idx=idx, w=w, stick_breaking=stick)
+        hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f, off_by_one=off1)
+        hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b,
+                         stick_breaking=stick, off_by_one=off1)
 
     return time_steps(step, steps, warmup, torch, hsa)
 
@@ -494,17 +495,27 @@ def main():
     }
     print("[bench] %s: %.3f ms/step" % (name, ms), file=sys.stderr, flush=True)
     if not args.no_extra:
+        # the paper's main variant on the same workload: stick-breaking chunk weights and
+        # the softmax off by one inside a chunk
+        msv, _, brkv = time_training(sh, dev, max(2, args.steps // 2), 2, torch, hsa,
+                                     stick=True, off1=True)
+        res["also"] = {"L4K_bf16_main_variant": {
+            "workload": ("HSA fwd+bwd at 4K context, stick-breaking weights and softmax off by "
+                         "one: B8 L4096 H16/G2 d128 S64 k8, bf16"),
+            "tokens_per_s": round(tokens / (msv * 1e-3), 1), "ms_per_step": round(msv, 4),
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brkv.items()}}}
+        print("[bench] %s main variant: %.3f ms/step" % (name, msv), file=sys.stderr, flush=True)
         del dev
         torch.cuda.empty_cache()
         name3 = "L64K_bf16"
         sh3, _, dev3, _ = make_training(name3, torch)
         ms3, kern3, brk3 = time_training(sh3, dev3, max(2, args.steps // 2), 2, torch, hsa)
         pairs3 = valid_pairs(sh3.B, sh3.L, sh3.G, sh3.S, sh3.k)
-        res["also"] = {"L64K_bf16": {
+        res["also"]["L64K_bf16"] = {
             "workload": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
             "tokens_per_s": round(sh3.B * sh3.L / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 4),
             "roofline": roofline_of(kern3, sh3, pairs3, name3),
-            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk3.items()}}}
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk3.items()}}
         print("[bench] %s: %.3f ms/step" % (name3, ms3), file=sys.stderr, flush=True)
         del dev3
         torch.cuda.empty_cache()

@@ -385,6 +385,77 @@ __device__ __forceinline__ bool merge_top(const float* __restrict__ cs,
     return true;
 }
 
+// The same top-k from at most 64 slice lists, each sorted by descending order key (the
+// scan extracts them in that order) and padded with empty keys: lane l holds list l's
+// first KC keys in registers; round r takes the wave-wide maximum of the lanes' first keys
+// and the winning lane shifts its list up by one.  One wave, no barrier, no memory traffic
+// inside the rounds; the order is strict, so the result equals merge_candidates'.
+template <int KC>
+__device__ __forceinline__ void merge_lists(const float* __restrict__ cs,
+                                            const int32_t* __restrict__ cc, int nlists, int n,
+                                            int k, int lane, int* sel_c, float* sel_w,
+                                            bool stick) {
+    int c[KC];
+    float s[KC];
+#pragma unroll
+    for (int i = 0; i < KC; ++i) {       // all loads first
+        const bool in = lane < nlists && i < k;
+        c[i] = in ? cc[lane * k + i] : -1;
+        s[i] = in ? cs[lane * k + i] : -INFINITY;
+    }
+    uint64_t key[KC];
+#pragma unroll
+    for (int i = 0; i < KC; ++i) key[i] = c[i] >= 0 ? order_key(s[i], c[i]) : 0;
+    uint64_t mine = 0;                   // lane r receives the r-th best
+    for (int r = 0; r < n; ++r) {
+        const uint64_t best = wave_max_key(key[0]);
+        if (lane == r) mine = best;
+        if (best != 0 && key[0] == best) {
+#pragma unroll
+            for (int i = 0; i + 1 < KC; ++i) key[i] = key[i + 1];
+            key[KC - 1] = 0;
+        }
+    }
+    const float ls = mine ? key_score(mine) : -INFINITY;
+    const int lc = mine ? key_chunk(mine) : -1;
+    float wt;
+    int rank;
+    lane_weights(ls, lc, lane < n && lc >= 0, n, stick, wt, rank);
+    if (lane < n) {
+        sel_c[rank] = lc;
+        sel_w[rank] = wt;
+    } else if (lane < k) {
+        sel_c[lane] = -1;
+        sel_w[lane] = 0.f;
+    }
+}
+
+// Final top-k of (b, g) into sel_c / sel_w (LDS) from the slice candidates, by every thread
+// of the workgroup; ends with a barrier.  Up to 64 slices: merge_lists by wave 0; more:
+// the tournament over the whole workgroup, else wave 0 sequentially.
+template <int NWV, int NPLMAX>
+__device__ __forceinline__ void merge_slices(const float* __restrict__ cs,
+                                             const int32_t* __restrict__ cc, int nslices,
+                                             int n, int k, uint64_t* tmp, int* sel_c,
+                                             float* sel_w, bool stick) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int nc = nslices * k;
+    if (nslices <= 64) {
+        if (wave == 0) {
+            if (k <= 8) merge_lists<8>(cs, cc, nslices, n, k, lane, sel_c, sel_w, stick);
+            else if (k <= 16) merge_lists<16>(cs, cc, nslices, n, k, lane, sel_c, sel_w, stick);
+            else merge_lists<KMAX>(cs, cc, nslices, n, k, lane, sel_c, sel_w, stick);
+        }
+        __syncthreads();
+        return;
+    }
+    if (!merge_top<NWV, NPLMAX>(cs, cc, nc, n, k, tmp, sel_c, sel_w, stick)) {
+        __syncthreads();
+        if (wave == 0) merge_candidates(cs, cc, nc, n, k, lane, sel_c, sel_w, stick);
+        __syncthreads();
+    }
+}
+
 // Stage 2 (finish): workgroup = (slot, b, g), so the k selected chunks of a sequence are
 // attended in parallel.  Wave 0 of every workgroup merges the slice candidates into the
 // final top-k (the same deterministic merge in each), computes the chunk weights and
@@ -424,22 +495,22 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
         }
         __syncthreads();
     } else {
-        if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc,
-                                                 cand_c + (size_t)bg * nc, nc, n, k, mtmp,
-                                                 sel_c, sel_w, dm.stick != 0)) {
-            __syncthreads();
-            if (wave == 0)
-                merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k,
-                                 lane, sel_c, sel_w, dm.stick != 0);
-            __syncthreads();
-        }
+        merge_slices<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                              nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
         if (slot == 0 && tid < k) {
             idx_out[(size_t)bg * k + tid] = sel_c[tid];
             w_out[(size_t)bg * k + tid] = sel_w[tid];
         }
     }
 
-    if (slot < n) {
+    // a chunk id outside the candidates (never produced by the scan) leaves the slot empty
+    // rather than indexing the cache with it
+    const bool live = slot < n && sel_c[slot] >= 0 && sel_c[slot] < ncand;
+    if (slot < n && !live) {
+        float* pp = part + (((size_t)bg * k + slot) * h) * D;
+        for (int x = tid; x < h * D; x += kFinThreads) pp[x] = 0.f;
+    }
+    if (live) {
         const int c = sel_c[slot];
         const float wi = sel_w[slot];
         // the chunk's S rows of K and V for group g
@@ -536,13 +607,8 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
         }
         __syncthreads();
     } else {
-        if (!merge_top<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc,
-                                         n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
-            if (wave == 0)
-                merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k,
-                                 lane, sel_c, sel_w, dm.stick != 0);
-            __syncthreads();
-        }
+        merge_slices<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                      nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
         if (tid < k) {
             idx_out[(size_t)bg * k + tid] = sel_c[tid];
             w_out[(size_t)bg * k + tid] = sel_w[tid];
@@ -560,9 +626,11 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     // rows of a chunk: the cache [B, N, G, d], or the stage [B, G, k, S, d]
     const size_t rowstride = staged ? (size_t)DD : (size_t)dm.G * DD;
     __bf16* stage = vst[wave];
+    const int ncand = cache_tokens(cache_len, b, dm.L) / S;
     for (int slot = wave; slot < n; slot += NWV) {
         const int c = sel_c[slot];
         const float wi = sel_w[slot];
+        if (c < 0 || c >= ncand) continue;    // never produced by the scan: an empty slot
         const size_t key0 = staged ? ((size_t)bg * k + slot) * S * DD
                                    : ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * DD;
         // V rows into the stage (copies, issued first: older than the K loads below, so
@@ -644,14 +712,8 @@ __global__ __launch_bounds__(kFinThreads) void decode_merge(
     const int k = dm.k;
     const int n = min(k, cache_tokens(cache_len, b, dm.L) / dm.S);
     const int nc = nslices * k;
-    if (!merge_top<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
-                                             nc, n, k, mtmp, sel_c, sel_w, dm.stick != 0)) {
-        __syncthreads();
-        if (wave == 0)
-            merge_candidates(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc, nc, n, k, lane,
-                             sel_c, sel_w, dm.stick != 0);
-        __syncthreads();
-    }
+    merge_slices<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                          nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
     if (tid < k) {
         idx_out[(size_t)bg * k + tid] = sel_c[tid];
         w_out[(size_t)bg * k + tid] = sel_w[tid];
@@ -675,6 +737,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_gather(
     const int n = min(k, cache_tokens(cache_len, b, dm.L) / S);
     if (slot >= n) return;
     const int c = idx[(size_t)bg * k + slot];
+    if (c < 0 || c >= cache_tokens(cache_len, b, dm.L) / S) return;   // not a candidate
     const int nv = S * D / VN;
     uint4 kr[PER], vr[PER];
 #pragma unroll

@@ -385,3 +385,29 @@ def test_select_many_candidates(hsa_gpu, shape):
     sure, loose = assert_indices(idx, idx_ref, gap, shape.S)
     assert loose == 0
     assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= W_ATOL
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_decode_more_than_64_slices(hsa_gpu, dtype):
+    """A cache of more than 64 scan slices (S = 16, 16385 chunks): the merge of the slice
+    candidates takes the workgroup tournament instead of the one-wave list merge."""
+    d = 64 if dtype == "f32" else 128
+    S, k = 16, 8
+    N = (64 * 256 + 1) * S
+    shape = Shape(2, N, 16, 2, d, S, k, dtype)
+    banner("decode_%d_slices_%s" % (65, dtype), "hsa_decode, tournament merge")
+    inp = hsa_synth.make_decode_inputs(shape, 29, device="cuda")
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
+    lens = [N, N - 5 * S - 3]
+    cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    Kbar = torch.from_numpy(oracle.landmarks(Kc, S).astype(np.float32)).cuda()
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, S, k, cache_len=cache_len)
+    torch.cuda.synchronize()
+    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, S, k)
+    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar, lens, S, k)[0]
+    sure = rgap >= 1e-3
+    assert sure.any()
+    assert np.array_equal(idx.cpu().numpy()[sure], ridx[sure])
+    assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
+    hm = np.repeat(sure, shape.H // shape.G, axis=1)
+    assert_close("o", shape, o[torch.from_numpy(hm).cuda()], ro[hm], o_abs=ro_abs[hm])
