@@ -32,6 +32,8 @@ CASES = {
     "wide_k16_bf16": (Shape(1, 2304, 32, 4, 128, 128, 16, "bf16"), 17, "lowrank"),
     "k24_bf16": (Shape(1, 2048, 16, 2, 128, 32, 24, "bf16"), 18, "iid"),
     "k20_d64_f32": (Shape(1, 1500, 4, 2, 64, 32, 20, "f32"), 19, "iid"),
+    # float32 with d = 128 (the largest float32 chunk: S d = 8192), generic kernels
+    "f32_d128": (Shape(1, 1024, 8, 2, 128, 64, 4, "f32"), 22, "iid"),
     # keys dominated by their chunk's offset (about 23 times the per-key spread): dQ is a
     # strongly cancelling sum over each chunk's keys
     "key_offset_bf16": (Shape(1, 1024, 16, 2, 128, 64, 8, "bf16"), 21, "iid", 2.0),
