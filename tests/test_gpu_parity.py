@@ -413,3 +413,23 @@ def test_decode_more_than_64_slices(hsa_gpu, dtype):
     assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
     hm = np.repeat(sure, shape.H // shape.G, axis=1)
     assert_close("o", shape, o[torch.from_numpy(hm).cuda()], ro[hm], o_abs=ro_abs[hm])
+
+
+def test_decode_f32_d128(hsa_gpu):
+    """Decode in float32 with d = 128 (the finish + combine kernels at S d = 8192)."""
+    shape = Shape(2, 4096 + 64, 8, 2, 128, 64, 6, "f32")
+    banner("decode_f32_d128", "hsa_decode")
+    inp = hsa_synth.make_decode_inputs(shape, 31, device="cuda")
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
+    lens = [4096 + 64, 64 * 7 + 9]
+    cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    Kbar = torch.from_numpy(oracle.landmarks(Kc, 64).astype(np.float32)).cuda()
+    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, 6, cache_len=cache_len)
+    torch.cuda.synchronize()
+    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, 64, 6)
+    sure = rgap >= 1e-3
+    assert sure.any()
+    assert np.array_equal(idx.cpu().numpy()[sure], ridx[sure])
+    assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
+    hm = np.repeat(sure, shape.H // shape.G, axis=1)
+    assert_close("o", shape, o[torch.from_numpy(hm).cuda()], ro[hm])
