@@ -102,7 +102,8 @@ def time_training(sh, dev, steps, warmup, torch, hsa, stick=False, off1=False):
     w = torch.empty((B, L, G, k), dtype=torch.float32, device="cuda")
     O = torch.empty_like(Q)
     grads = (torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V))
-    p = hsa.make_params(B, L, H, G, d, S, k, Q.dtype)
+    # the workspace depends on the variant (the off-by-one backward keeps more per pair)
+    p = hsa.make_params(B, L, H, G, d, S, k, Q.dtype, stick_breaking=stick, off_by_one=off1)
     ws_f = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_FORWARD)), dtype=torch.uint8,
                        device="cuda")
     ws_b = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_BACKWARD)), dtype=torch.uint8,

@@ -16,7 +16,7 @@
 // in parallel; stage 3 (combine), workgroup = (b, g), sums their weighted partial outputs
 // in slot order.
 // With the key / value cache in host memory (Sec. 3.2: only the landmarks stay on the GPU):
-// after the scan, decode_merge writes the selection, decode_gather copies the selected
+// after the scan, decode_gather merges the selection and copies the selected
 // chunks' rows from the host cache (read by the kernel over the host link) into a compact
 // stage [B, G, k, S, d] in device memory, and the attend kernels run "staged": they take
 // the merged selection and read slot i's rows from the stage.
@@ -488,7 +488,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     for (int i = tid; i < h * D; i += kFinThreads)
         qf[(i / D) * DP + i % D] = to_f32(q[((size_t)b * dm.H + (size_t)g * h) * D + i]);
     const int nc = nslices * k;
-    if (staged) {                        // the selection is merged already (decode_merge)
+    if (staged) {                        // the selection is merged already (decode_gather)
         if (tid < k) {
             sel_c[tid] = idx_out[(size_t)bg * k + tid];
             sel_w[tid] = w_out[(size_t)bg * k + tid];
@@ -600,7 +600,7 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     for (int ks = 0; ks < 4; ++ks)
         if (row >= kAttH) qB[ks] = bf16x8_t{};
     const int nc = nslices * k;
-    if (staged) {                        // the selection is merged already (decode_merge)
+    if (staged) {                        // the selection is merged already (decode_gather)
         if (tid < k) {
             sel_c[tid] = idx_out[(size_t)bg * k + tid];
             sel_w[tid] = w_out[(size_t)bg * k + tid];
@@ -699,45 +699,39 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
     }
 }
 
-// The merge of stage 2 on its own, for the host-cache path: writes idx, w [B, G, k].
-__global__ __launch_bounds__(kFinThreads) void decode_merge(
-    Dims dm, const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
-    const int32_t* __restrict__ cand_c, int nslices, int32_t* __restrict__ idx_out,
-    float* __restrict__ w_out) {
-    __shared__ int sel_c[KMAX];
-    __shared__ float sel_w[KMAX];
-    __shared__ uint64_t mtmp[NW * KMAX];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int bg = blockIdx.x, b = bg / dm.G;
-    const int k = dm.k;
-    const int n = min(k, cache_tokens(cache_len, b, dm.L) / dm.S);
-    const int nc = nslices * k;
-    merge_slices<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
-                                          nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
-    if (tid < k) {
-        idx_out[(size_t)bg * k + tid] = sel_c[tid];
-        w_out[(size_t)bg * k + tid] = sel_w[tid];
-    }
-}
-
-// The selected chunks' K and V rows, from the cache in host memory [B, N, G, d] to the
-// stage [B, G, k, S, d]: workgroup = (slot, b, g); every thread issues all of its 16-byte
-// loads (K and V) before its stores, so a workgroup keeps 2 S d elem bytes in flight over
-// the host link.
+// The host-cache path's merge and gather: workgroup = (slot, b, g).  Every workgroup of a
+// (b, g) merges the slice candidates (the same deterministic merge), the slot-0 one writes
+// idx, w [B, G, k], and the workgroup of slot i copies its chunk's K and V rows from the
+// cache in host memory [B, N, G, d] to the stage [B, G, k, S, d]; every thread issues all
+// of its 16-byte loads (K and V) before its stores, so a workgroup keeps 2 S d elem bytes
+// in flight over the host link.
 template <typename T, int D>
 __global__ __launch_bounds__(kFinThreads) void decode_gather(
     Dims dm, const T* __restrict__ Kh, const T* __restrict__ Vh,
-    const int32_t* __restrict__ cache_len, const int32_t* __restrict__ idx,
-    T* __restrict__ Ks, T* __restrict__ Vs) {
+    const int32_t* __restrict__ cache_len, const float* __restrict__ cand_s,
+    const int32_t* __restrict__ cand_c, int nslices, int32_t* __restrict__ idx_out,
+    float* __restrict__ w_out, T* __restrict__ Ks, T* __restrict__ Vs) {
     constexpr int VN = V16<T>::n;                 // elements per 16 bytes
     constexpr int PER = 128 * D / VN / kFinThreads;   // 16-byte vectors per thread, S <= 128
+    __shared__ int sel_c[KMAX];
+    __shared__ float sel_w[KMAX];
+    __shared__ uint64_t mtmp[NW * KMAX];
+    const int tid = threadIdx.x;
     const int slot = blockIdx.x;
     const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
     const int S = dm.S, k = dm.k;
-    const int n = min(k, cache_tokens(cache_len, b, dm.L) / S);
+    const int ncand = cache_tokens(cache_len, b, dm.L) / S;
+    const int n = min(k, ncand);
+    const int nc = nslices * k;
+    merge_slices<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                          nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
+    if (slot == 0 && tid < k) {
+        idx_out[(size_t)bg * k + tid] = sel_c[tid];
+        w_out[(size_t)bg * k + tid] = sel_w[tid];
+    }
     if (slot >= n) return;
-    const int c = idx[(size_t)bg * k + slot];
-    if (c < 0 || c >= cache_tokens(cache_len, b, dm.L) / S) return;   // not a candidate
+    const int c = sel_c[slot];
+    if (c < 0 || c >= ncand) return;              // never produced by the scan
     const int nv = S * D / VN;
     uint4 kr[PER], vr[PER];
 #pragma unroll
@@ -858,15 +852,10 @@ void launch_tkd_host(const Dims& dm, const void* q, const void* Kh, const void* 
                            nslices);
     }
     {
-        HSA_TIMED("decode_merge", st);
-        hipLaunchKernelGGL(decode_merge, dim3(dm.B * dm.G), dim3(kFinThreads), 0, st, dm,
-                           cache_len, cs, cc, nslices, idx, w);
-    }
-    {
         HSA_TIMED("decode_gather", st);
         hipLaunchKernelGGL((decode_gather<T, D>), dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
-                           st, dm, (const T*)Kh, (const T*)Vh, cache_len, (const int32_t*)idx,
-                           kst, vst);
+                           st, dm, (const T*)Kh, (const T*)Vh, cache_len, cs, cc, nslices, idx,
+                           w, kst, vst);
     }
     if (decode_mfma_shape<T, D>(dm)) {
         HSA_TIMED("decode_attend_mfma", st);

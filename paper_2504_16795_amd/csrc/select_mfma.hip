@@ -69,43 +69,6 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     const int ncand = valid ? t / dm.S : 0;
     const int k = dm.k;
 
-    // B operand: q~ of the wave's 16 tokens as bf16 hi / lo; the lane holds d = 128 db +
-    // 32 ks + 8 grp + i of token `row` (a token past the end reads the last one; unused)
-    bf16x8_t qh[ND][4], ql[QLO ? 4 : 1];
-    if constexpr (!QLO) {
-        const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + g) * DD + 8 * grp;
-#pragma unroll
-        for (int db = 0; db < ND; ++db)
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) qh[db][ks] = ld_bf16x8(qp + D * db + 32 * ks);
-    } else {
-        float qs[4][8];
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) qs[ks][i] = 0.f;
-        const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + (size_t)g * dm.h) * D +
-                           8 * grp;
-#pragma unroll 4
-        for (int j = 0; j < dm.h; ++j) {
-            bf16x8_t v[4];
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks) v[ks] = ld_bf16x8(qp + (size_t)j * D + 32 * ks);
-#pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-                for (int i = 0; i < 8; ++i) qs[ks][i] += (float)v[ks][i];
-        }
-#pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                const __bf16 h = f2bf(qs[ks][i]);
-                qh[0][ks][i] = h;
-                ql[ks][i] = f2bf(qs[ks][i] - (float)h);
-            }
-    }
-
     // staging of stage si (candidate block si / ND, columns 128 (si % ND) ..): wave w
     // converts rows 16 w .. 16 w + 15; lane l covers row 16 w + 2 i + l / 32 (i < 8),
     // floats 4 (l % 32) .. +3 of the slice
@@ -138,6 +101,59 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
         }
     };
 
+    const int nblk = cdiv(nwg, kCB);
+    const int nst = nblk * ND;         // stages: (candidate block, column slice)
+    // the first block's landmark loads go out before the query loads (independent of
+    // them), so both latencies overlap
+    if (nblk > 0) load_block(0);
+
+    // B operand: q~ of the wave's 16 tokens as bf16 hi / lo; the lane holds d = 128 db +
+    // 32 ks + 8 grp + i of token `row` (a token past the end reads the last one; unused)
+    bf16x8_t qh[ND][4], ql[QLO ? 4 : 1];
+    if constexpr (!QLO) {
+        const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + g) * DD + 8 * grp;
+#pragma unroll
+        for (int db = 0; db < ND; ++db)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) qh[db][ks] = ld_bf16x8(qp + D * db + 32 * ks);
+    } else {
+        float qs[4][8];
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) qs[ks][i] = 0.f;
+        const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + (size_t)g * dm.h) * D +
+                           8 * grp;
+        // 8 heads at a time: all 32 loads are issued (head index clamped, branch-free)
+        // before the first sum, so the wave waits for one round trip per 8 heads rather
+        // than one per head
+        for (int j0 = 0; j0 < dm.h; j0 += 8) {
+            bf16x8_t v[8][4];
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj)
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+                    v[jj][ks] = ld_bf16x8(qp + (size_t)min(j0 + jj, dm.h - 1) * D + 32 * ks);
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int jj = 0; jj < 8; ++jj) {
+                const bool use = j0 + jj < dm.h;     // a select, so no load is sunk
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) qs[ks][i] += use ? (float)v[jj][ks][i] : 0.f;
+            }
+        }
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const __bf16 h = f2bf(qs[ks][i]);
+                qh[0][ks][i] = h;
+                ql[ks][i] = f2bf(qs[ks][i] - (float)h);
+            }
+    }
+
     float ls[KC];
     int lc[KC];
 #pragma unroll
@@ -148,12 +164,7 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     int koff[4];
     row_read_offsets(lane, koff);
     const float alpha = dm.alpha;
-    const int nblk = cdiv(nwg, kCB);
-    const int nst = nblk * ND;         // stages: (candidate block, column slice)
-    if (nblk > 0) {
-        load_block(0);
-        store_block(0);
-    }
+    if (nblk > 0) store_block(0);
     constexpr int MB = kCB / 16;
     for (int blk = 0; blk < nblk; ++blk) {
         // the 4 row blocks' products interleaved (independent accumulators) over the
