@@ -248,7 +248,8 @@ def bench_decode(steps, warmup, torch, hsa):
         gbs = stream_bytes / (avg * 1e-3) / 1e9
         out["scan_roofline"] = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
                                 "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                                "bytes_per_launch": stream_bytes}
+                                "bytes_per_launch": stream_bytes,
+                                "traffic": traffic_of("decode_scan", "decode_1M_bf16")}
     out["algorithmic_bytes_per_step"] = stream_bytes + gather_bytes
     # the same step with the key / value cache in pinned host memory: only the landmark
     # cache stays on the GPU, and the selected chunks cross the host link each step
@@ -388,8 +389,13 @@ def pmc_run(workload, steps, torch, hsa):
     for _ in range(3):
         y.copy_(x)
     torch.cuda.synchronize()
-    sh, _, dev, _ = make_training(workload, torch)
-    time_training(sh, dev, steps, 0, torch, hsa)
+    if workload == "decode_1M_bf16":
+        # the cache set-up (one landmark launch over the whole cache), then `steps` decode
+        # steps with the cache in HBM and `steps` with it in host memory
+        bench_decode(steps, 0, torch, hsa)
+    else:
+        sh, _, dev, _ = make_training(workload, torch)
+        time_training(sh, dev, steps, 0, torch, hsa)
     torch.cuda.synchronize()
 
 
@@ -403,17 +409,20 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
         per = defaultdict(list)
         for r in csv.DictReader(open(path)):
             if r["Counter_Name"].startswith(counter):
-                per[r["Kernel_Name"]].append(float(r["Counter_Value"]) * 1024.0)   # KiB
-        return per
+                per[r["Kernel_Name"]].append((int(r["Dispatch_Id"]),
+                                              float(r["Counter_Value"]) * 1024.0))   # KiB
+        return {n: [v for _, v in sorted(x)] for n, x in per.items()}
 
     fetch, write = read(fetch_csv, "FETCH_SIZE"), read(write_csv, "WRITE_SIZE")
     # the runtime's device-to-device copy kernel (torch's same-dtype copy_ goes through it)
     copy = [n for n in fetch if "copybuffer" in n.lower()]
     if not copy:
         raise SystemExit("no copy kernel in %s" % fetch_csv)
-    cname = max(copy, key=lambda n: max(fetch[n]))
-    f_fac = CALIB_BYTES / max(fetch[cname])
-    w_fac = CALIB_BYTES / max(write[cname])
+    # the calibration copies are the first three dispatches of that kernel (a workload may
+    # copy more later, e.g. the decode workload's device-to-host copy of its cache)
+    cname = max(copy, key=lambda n: max(fetch[n][:3]))
+    f_fac = CALIB_BYTES / sorted(fetch[cname][:3])[1]
+    w_fac = CALIB_BYTES / sorted(write[cname][:3])[1]
     # function-name fragment -> the name the library's timing reports
     names = {"landmarks_kernel": "landmarks_kernel", "select_tiles_kernel": "select_kernel",
              "select_split_kernel": "select_kernel", "select_kernel": "select_kernel",
@@ -426,7 +435,10 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
              "fwd_chunk_mfma": "fwd_chunk_mfma", "fwd_reduce": "fwd_reduce",
              "stream_rowcount": "plan", "stream_plan": "plan",
              "fill_zero_u32": "fill_zero_u32", "forward_generic": "forward_generic",
-             "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic"}
+             "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic",
+             "decode_scan": "decode_scan", "decode_attend_mfma": "decode_attend_mfma",
+             "decode_gather": "decode_gather", "decode_finish": "decode_finish",
+             "decode_combine": "decode_combine"}
     kernels = {}
     for full in fetch:
         short = next((v for n, v in names.items() if n in full), None)
