@@ -62,8 +62,10 @@ def _load():
         lib.hsa_oracle_select_backward.argtypes = [DP, P, P, P, P, P, P, P, P]
         lib.hsa_oracle_backward_kv.argtypes = [DP, P, P, P, P, P, P, P, I64, P, P, P]
         lib.hsa_oracle_decode.argtypes = [DP, P, P, P, P, I64, P, P, P, P]
+        lib.hsa_oracle_scores.argtypes = [DP, P, P, I64, I64, P, P]
+        lib.hsa_oracle_slot_weights.argtypes = [DP, P, P, I64, I64, P, P, P]
         for f in ("landmarks", "select", "forward", "backward_q", "backward_kv", "decode",
-                  "select_backward"):
+                  "select_backward", "scores", "slot_weights"):
             getattr(lib, "hsa_oracle_" + f).restype = None
         _lib = lib
     return _lib
@@ -129,6 +131,34 @@ def select_slice(dm: _Dims, Q, Kbar, rows=None):
         _load().hsa_oracle_select(ctypes.byref(dm), _p(Q), _p(Kbar), n, _p(r), _p(idx),
                                   _p(w), _p(gap), _p(ss))
     return idx, w, gap, ss
+
+
+def scores_at(dm: _Dims, q, Kbar, pos):
+    """Group scores [n, C] of n queries q [n, h, d] at sequence positions pos [n] against
+    every landmark row of Kbar [C, d]; NaN where c >= floor(pos / S) (not a candidate)."""
+    q, Kbar = _f64(q), _f64(Kbar)
+    pos = np.ascontiguousarray(pos, dtype=np.int64)
+    n, C = pos.size, Kbar.shape[0]
+    assert q.shape == (n, dm.h, dm.d) and Kbar.shape[1] == dm.d
+    s = np.empty((n, C))
+    if n and C:
+        _load().hsa_oracle_scores(ctypes.byref(dm), _p(q), _p(Kbar), C, n, _p(pos), _p(s))
+    return s
+
+
+def slot_weights_at(dm: _Dims, q, Kbar, pos, idx):
+    """The weight rule (softmax, or stick-breaking with dm.stick) applied to the GIVEN slots
+    idx [n, k] of n queries q [n, h, d] at positions pos [n]: [n, k], 0 in empty slots."""
+    q, Kbar = _f64(q), _f64(Kbar)
+    pos = np.ascontiguousarray(pos, dtype=np.int64)
+    idx = np.ascontiguousarray(idx, dtype=np.int32)
+    n, C = pos.size, Kbar.shape[0]
+    assert q.shape == (n, dm.h, dm.d) and idx.shape == (n, dm.k)
+    w = np.zeros((n, dm.k))
+    if n and C:
+        _load().hsa_oracle_slot_weights(ctypes.byref(dm), _p(q), _p(Kbar), C, n, _p(pos),
+                                        _p(idx), _p(w))
+    return w
 
 
 def forward_slice(dm: _Dims, Q, K, V, idx, w, rows=None):

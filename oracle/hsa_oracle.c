@@ -60,11 +60,49 @@ void hsa_oracle_landmarks(const hsa_oracle_dims* dm, const double* K, double* Kb
     }
 }
 
+/* Chunk weights of n selected scores s[0..n) given in slot order (Sec. 3.1.1):
+ * a softmax over them (the ablation without stick-breaking), or with dm->stick the
+ * stick-breaking weights, b_i = sigmoid(s_i) and slot i takes the share b_i of what the
+ * earlier slots left, u_i = prod_{m<i} (1 - b_m). */
+static void weight_rule(const hsa_oracle_dims* dm, const double* s, int64_t n, double* w) {
+    if (dm->stick) {
+        double u = 1.0;
+        for (int64_t i = 0; i < n; ++i) {
+            const double bi = 1.0 / (1.0 + exp(-s[i]));
+            w[i] = bi * u;
+            u *= 1.0 - bi;
+        }
+    } else {
+        double m = -INFINITY;
+        for (int64_t i = 0; i < n; ++i) m = s[i] > m ? s[i] : m;
+        double z = 0.0;
+        for (int64_t i = 0; i < n; ++i) z += exp(s[i] - m);
+        for (int64_t i = 0; i < n; ++i) w[i] = exp(s[i] - m) / z;
+    }
+}
+
+/* Group score of one candidate: alpha * (sum_j q_j) . Kbar_c, with the head sum qsum
+ * formed first (the same dot product as the concatenated group query against the landmark
+ * tiled over the h heads). */
+static double group_score(const hsa_oracle_dims* dm, const double* qsum, const double* kb) {
+    double acc = 0.0;
+    for (int e = 0; e < dm->d; ++e) acc += qsum[e] * kb[e];
+    return dm->alpha * acc;
+}
+
+static void head_sum(const hsa_oracle_dims* dm, const double* q, double* qsum) {
+    for (int e = 0; e < dm->d; ++e) {
+        double acc = 0.0;
+        for (int j = 0; j < dm->h; ++j) acc += q[j * dm->d + e];
+        qsum[e] = acc;
+    }
+}
+
 /* Selection for one token: q [h, d], candidates c < ncand scored against Kbar. */
 static void select_one(const hsa_oracle_dims* dm, const double* q, const double* Kbar,
                        int64_t ncand, int32_t* idx, double* w, double* gap,
                        double* sel_score) {
-    const int h = dm->h, d = dm->d, k = dm->k;
+    const int d = dm->d, k = dm->k;
     for (int i = 0; i < k; ++i) {
         idx[i] = -1;
         w[i] = 0.0;
@@ -76,16 +114,10 @@ static void select_one(const hsa_oracle_dims* dm, const double* q, const double*
     /* group query: concatenating the h heads and tiling the landmark h times gives the
        same dot product as (sum_j q_j) . Kbar_c */
     double* qsum = (double*)malloc(sizeof(double) * d);
-    for (int e = 0; e < d; ++e) {
-        double acc = 0.0;
-        for (int j = 0; j < h; ++j) acc += q[j * d + e];
-        qsum[e] = acc;
-    }
+    head_sum(dm, q, qsum);
     cand_t* cand = (cand_t*)malloc(sizeof(cand_t) * ncand);
     for (int64_t c = 0; c < ncand; ++c) {
-        double acc = 0.0;
-        for (int e = 0; e < d; ++e) acc += qsum[e] * Kbar[c * d + e];
-        cand[c].s = dm->alpha * acc;
+        cand[c].s = group_score(dm, qsum, Kbar + c * d);
         cand[c].c = c;
     }
     qsort(cand, (size_t)ncand, sizeof(cand_t), cmp_score_desc);
@@ -94,28 +126,14 @@ static void select_one(const hsa_oracle_dims* dm, const double* q, const double*
 
     /* slots in descending chunk order */
     qsort(cand, (size_t)n, sizeof(cand_t), cmp_chunk_desc);
-    if (dm->stick) {
-        /* stick-breaking in slot order: b_i = sigmoid(s_i); slot i takes the share b_i of
-           what the earlier slots left, u_i = prod_{m<i} (1 - b_m) */
-        double u = 1.0;
-        for (int64_t i = 0; i < n; ++i) {
-            const double bi = 1.0 / (1.0 + exp(-cand[i].s));
-            idx[i] = (int32_t)cand[i].c;
-            w[i] = bi * u;
-            u *= 1.0 - bi;
-            if (sel_score) sel_score[i] = cand[i].s;
-        }
-    } else {
-        double m = -INFINITY;
-        for (int64_t i = 0; i < n; ++i) m = cand[i].s > m ? cand[i].s : m;
-        double z = 0.0;
-        for (int64_t i = 0; i < n; ++i) z += exp(cand[i].s - m);
-        for (int64_t i = 0; i < n; ++i) {
-            idx[i] = (int32_t)cand[i].c;
-            w[i] = exp(cand[i].s - m) / z;
-            if (sel_score) sel_score[i] = cand[i].s;
-        }
+    double* ssel = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    for (int64_t i = 0; i < n; ++i) {
+        idx[i] = (int32_t)cand[i].c;
+        ssel[i] = cand[i].s;
+        if (sel_score) sel_score[i] = cand[i].s;
     }
+    weight_rule(dm, ssel, n, w);
+    free(ssel);
     free(cand);
     free(qsum);
 }
@@ -130,6 +148,51 @@ void hsa_oracle_select(const hsa_oracle_dims* dm, const double* Q, const double*
         const int64_t ncand = t / dm->S;
         select_one(dm, Q + t * h * d, Kbar, ncand, idx + r * k, w + r * k,
                    gap ? gap + r : NULL, sel_score ? sel_score + r * k : NULL);
+    }
+}
+
+void hsa_oracle_scores(const hsa_oracle_dims* dm, const double* q, const double* Kbar,
+                       int64_t ncol, int64_t n, const int64_t* pos, double* s) {
+    const int h = dm->h, d = dm->d;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int64_t r = 0; r < n; ++r) {
+        double* qsum = (double*)malloc(sizeof(double) * d);
+        head_sum(dm, q + r * h * d, qsum);
+        int64_t ncand = pos[r] / dm->S;
+        if (ncand > ncol) ncand = ncol;
+        for (int64_t c = 0; c < ncol; ++c)
+            s[r * ncol + c] = c < ncand ? group_score(dm, qsum, Kbar + c * d) : NAN;
+        free(qsum);
+    }
+}
+
+void hsa_oracle_slot_weights(const hsa_oracle_dims* dm, const double* q, const double* Kbar,
+                             int64_t ncol, int64_t n, const int64_t* pos,
+                             const int32_t* idx, double* w) {
+    const int h = dm->h, d = dm->d, k = dm->k;
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t r = 0; r < n; ++r) {
+        double* qsum = (double*)malloc(sizeof(double) * d);
+        double* sv = (double*)malloc(sizeof(double) * k);
+        double* wv = (double*)malloc(sizeof(double) * k);
+        int* slot = (int*)malloc(sizeof(int) * k);
+        head_sum(dm, q + r * h * d, qsum);
+        int64_t ncand = pos[r] / dm->S;
+        if (ncand > ncol) ncand = ncol;
+        int64_t nv = 0;
+        for (int i = 0; i < k; ++i) {
+            const int64_t c = idx[r * k + i];
+            w[r * k + i] = 0.0;
+            if (c < 0 || c >= ncand) continue;
+            sv[nv] = group_score(dm, qsum, Kbar + c * d);
+            slot[nv++] = i;
+        }
+        weight_rule(dm, sv, nv, wv);
+        for (int64_t i = 0; i < nv; ++i) w[r * k + slot[i]] = wv[i];
+        free(slot);
+        free(wv);
+        free(sv);
+        free(qsum);
     }
 }
 

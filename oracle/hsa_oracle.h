@@ -61,6 +61,23 @@ void hsa_oracle_select(const hsa_oracle_dims* dm, const double* Q, const double*
                        int64_t ntok, const int64_t* rows, int32_t* idx, double* w,
                        double* gap, double* sel_score);
 
+/* Group scores of every candidate (Sec. 3.1 chunk-selection equation): for n queries
+ * q [n, h, d] at sequence positions pos[n], s[r, c] = alpha * (sum_j q_j) . Kbar_c for
+ * c < min(floor(pos[r]/S), ncol); the other entries of the row [ncol] are NaN.
+ * Kbar has ncol rows [ncol, d]. */
+void hsa_oracle_scores(const hsa_oracle_dims* dm, const double* q, const double* Kbar,
+                       int64_t ncol, int64_t n, const int64_t* pos, double* s);
+
+/* The chunk-weight rule (Sec. 3.1.1) applied to GIVEN slots: for n queries q [n, h, d]
+ * at positions pos[n] and slots idx [n, k], the valid slots (0 <= idx < min(floor(pos/S),
+ * ncol)) get the softmax over their scores s_c = alpha (sum_j q_j) . Kbar_c, or with
+ * dm->stick the stick-breaking weights in the given slot order; other slots get 0.
+ * With the oracle's own selection this is the oracle's w; with another selection of
+ * the same scores it is the weight that selection must carry. */
+void hsa_oracle_slot_weights(const hsa_oracle_dims* dm, const double* q, const double* Kbar,
+                             int64_t ncol, int64_t n, const int64_t* pos,
+                             const int32_t* idx, double* w);
+
 /* Forward for the listed tokens (Sec. 3.1.1 "Hierarchical Attention"): for every head j
  * and slot i, O_{j,i} = softmax(beta q_j K_c^T) V_c over the S keys of chunk c = idx[i]
  * (softmax off by one with dm->off_by_one); O_j = sum_i w_i O_{j,i}; O = 0 for a token

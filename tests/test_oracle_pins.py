@@ -196,6 +196,103 @@ def test_stick_breaking_most_recent_chunk_breaks_first():
     assert checked > 50
 
 
+@pytest.mark.parametrize("seed,k", [(51, 1), (52, 3), (53, 6)])
+def test_gap_is_the_order_statistic_of_a_brute_force_sort(seed, k):
+    """gap = s_(n) - s_(n+1) of the descending score order (n = min(k, #candidates)), +inf
+    when every candidate is selected; checked against numpy's sort of the scores of the
+    concatenated group query against the landmark tiled over the heads (Sec. 3.1: the
+    group query has dimension h d), a formulation the oracle does not use."""
+    L, h, d, S = 60, 3, 5, 4
+    Q, K, _, _ = small_problem(seed, L=L, h=h, d=d, S=S, k=k)
+    Kb = oracle.landmarks(K, S)
+    _, _, gap, _ = oracle.select(Q, Kb, 1, S, k)
+    alpha = 1.0 / math.sqrt(h * d)
+    tiled = np.tile(Kb[0, :, 0], (1, h))                      # [C, h d]
+    checked = 0
+    for t in range(L):
+        ncand = t // S
+        n = min(k, ncand)
+        if ncand <= n:
+            assert np.isinf(gap[0, t, 0]), t
+            continue
+        s = np.sort(alpha * (tiled[:ncand] @ Q[0, t].reshape(-1)))[::-1]
+        assert abs(gap[0, t, 0] - (s[n - 1] - s[n])) <= 1e-13, (t, gap[0, t, 0], s[n - 1] - s[n])
+        checked += 1
+    assert checked > 20
+
+
+def test_gap_at_exact_ties_and_one_below():
+    """Exact ties give gap 0; moving the (n+1)-th score down by exactly 1/2 gives 1/2 (the
+    n-th and (n+1)-th order statistics, not the (n-1)-th or the (n+2)-th)."""
+    S, L = 1, 8
+    q = np.ones((1, L, 1, 1))
+    for vals, k, want in (([4., 9., 7., 7., 1., 3., 2.], 2, 0.0),     # 9 7 | 7
+                          ([4., 9., 7., 6.5, 1., 3., 2.], 2, 0.5),    # 9 7 | 6.5
+                          ([4., 9., 7., 6.5, 1., 3., 2.], 3, 2.5),    # 9 7 6.5 | 4
+                          ([4., 9., 7., 6.5, 1., 3., 2.], 1, 2.0)):   # 9 | 7
+        K = np.zeros((1, L, 1, 1))
+        K[0, :7, 0, 0] = vals
+        _, _, gap, _ = oracle.select(q, oracle.landmarks(K, S), 1, S, k)
+        assert gap[0, 7, 0] == want, (vals, k)
+
+
+def test_scores_at_match_the_tiled_group_query():
+    """scores_at: alpha (sum_j q_j) . Kbar_c for the candidates, NaN beyond, checked against
+    the concatenated group query against the tiled landmark."""
+    L, h, d, S = 50, 2, 6, 5
+    Q, K, _, _ = small_problem(55, L=L, h=h, d=d, S=S, k=2)
+    Kb = oracle.landmarks(K, S)[0, :, 0]
+    dm = oracle.dims(L, h, d, S, 2)
+    pos = np.array([0, 4, 5, 23, 49])
+    s = oracle.scores_at(dm, Q[0, pos], Kb, pos)
+    tiled = np.tile(Kb, (1, h))
+    for r, t in enumerate(pos):
+        nc = t // S
+        want = (tiled[:nc] @ Q[0, t].reshape(-1)) / math.sqrt(h * d)
+        np.testing.assert_allclose(s[r, :nc], want, rtol=1e-13, atol=1e-15)
+        assert np.all(np.isnan(s[r, nc:]))
+
+
+@pytest.mark.parametrize("stick", [False, True])
+def test_slot_weights_at(stick):
+    """The weight rule on given slots: on the oracle's own selection it is the oracle's w;
+    on another selection it is torch.softmax of the scores of its valid slots (or the
+    stick-breaking product in the given slot order), with empty slots at 0."""
+    L, h, d, S, k = 80, 2, 4, 4, 4
+    Q, K, _, _ = small_problem(57, L=L, h=h, d=d, S=S, k=k, mu=1.5)
+    Kb = oracle.landmarks(K, S)[0, :, 0]
+    dm = oracle.dims(L, h, d, S, k, stick=stick)
+    rows = np.arange(L)
+    idx, w, _, _ = oracle.select_slice(dm, Q[0], Kb)
+    np.testing.assert_allclose(oracle.slot_weights_at(dm, Q[0], Kb, rows, idx), w,
+                               rtol=0, atol=1e-15)
+    # another selection: arbitrary candidate chunks in arbitrary slot order, some empty
+    rng = np.random.default_rng(3)
+    other = np.full((L, k), -1, np.int32)
+    for t in range(L):
+        nc = t // S
+        if nc:
+            m = rng.integers(1, min(k, nc) + 1)
+            other[t, :m] = rng.choice(nc, m, replace=False)
+    other[5::7, 0] = 10 ** 6                       # past the candidates: empty
+    got = oracle.slot_weights_at(dm, Q[0], Kb, rows, other)
+    alpha = 1.0 / math.sqrt(h * d)
+    for t in range(L):
+        valid = [(i, int(c)) for i, c in enumerate(other[t]) if 0 <= c < t // S]
+        want = np.zeros(k)
+        if valid:
+            sc = torch.tensor([alpha * Q[0, t].sum(0) @ Kb[c] for _, c in valid])
+            if stick:
+                b = torch.sigmoid(sc)
+                left = torch.cumprod(torch.cat([torch.ones(1, dtype=b.dtype), 1 - b[:-1]]), 0)
+                ww = (b * left).numpy()
+            else:
+                ww = torch.softmax(sc, 0).numpy()
+            for (i, _), x in zip(valid, ww):
+                want[i] = x
+        np.testing.assert_allclose(got[t], want, rtol=1e-13, atol=1e-15)
+
+
 # ------------------------------------------------------------------- forward ----
 
 def sdpa(q, k, v, scale, mask=None):
