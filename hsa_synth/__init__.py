@@ -24,7 +24,7 @@ import numpy as np
 
 __all__ = [
     "HsaShape", "WORKLOADS", "philox", "round_bf16", "make_training_inputs",
-    "make_decode_inputs", "redraw_query_rows",
+    "make_decode_inputs", "redraw_query_rows", "redraw_decode_query",
 ]
 
 # tensor ids of the Philox key; one stream per tensor
@@ -187,7 +187,8 @@ def make_decode_inputs(shape: HsaShape, seed: int, n_cache: Optional[int] = None
     r (0.9 u + sqrt(0.19) v_s) with v_s random unit vectors orthogonal to u and
     r = mu_std*sqrt(d) (the typical norm of a chunk's mean key), so its keys have
     cosine 0.9 with the shared query direction: a passkey-like chunk that must be selected.
-    Returns q [B,H,d], Kc, Vc [B,N,G,d] in the workload dtype and planted [B,G] (int64).
+    Returns q [B,H,d], Kc, Vc [B,N,G,d] in the workload dtype, planted [B,G] (int64) and
+    the query directions u [B,G,d] (float64).
     """
     import torch
     B, H, G, d, S = shape.B, shape.H, shape.G, shape.d, shape.S
@@ -241,7 +242,20 @@ def make_decode_inputs(shape: HsaShape, seed: int, n_cache: Optional[int] = None
                 x /= x.norm(dim=-1, keepdim=True)
                 keys = r * (0.9 * ub[None, :] + math.sqrt(0.19) * x)
                 kc[b, p * S:(p + 1) * S, g] = keys.to(tdt)
-    return {"q": q, "Kc": kc, "Vc": vc, "planted": planted}
+    return {"q": q, "Kc": kc, "Vc": vc, "planted": planted, "u": u, "seed": seed}
+
+
+def redraw_decode_query(q, u, seed: int, b: int, g: int, attempt: int) -> None:
+    """Replace the h query heads of group g of sequence b (q [B, H, d], a torch tensor) by
+    0.5 u[b, g] + a fresh N(0, 1/d) draw (sub-seeded by (b, g, attempt)): the same
+    distribution as make_decode_inputs, so the planted chunk stays aligned with the group."""
+    import torch
+    B, H, d = q.shape
+    G = u.shape[1]
+    h = H // G
+    x = philox(seed, _TID["redraw"], b, g, attempt, 1).standard_normal((h, d))
+    row = 0.5 * u[b, g].double().cpu()[None, :] + torch.from_numpy(x) / math.sqrt(d)
+    q[b, g * h:(g + 1) * h] = row.to(q.dtype).to(q.device)
 
 
 def make_shared_selection_inputs(name: str = "shared_x3_L4K_bf16", device: str = "cuda"):

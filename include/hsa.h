@@ -192,6 +192,33 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
                              hsa_dtype_t kbar_dtype, const int32_t* cache_len, void* o,
                              int32_t* idx, float* w, void* ws, size_t ws_bytes, void* stream);
 
+/* Kernel families an op can be served by (hsa_attn_set_path). */
+typedef enum {
+    HSA_PATH_AUTO = 0,         /* chosen by shape: the fastest family that serves it       */
+    HSA_PATH_GENERIC = 1,      /* the fp32 vector-ALU kernels, which serve every supported
+                                  shape (all ops)                                          */
+    HSA_PATH_TWO_PASS = 2,     /* HSA_OP_BACKWARD: a query pass then a key pass, each
+                                  recomputing the attention (bf16, h = 8, d = 128)         */
+    HSA_PATH_CHUNK_MAJOR = 3,  /* HSA_OP_FORWARD: chunk-major (bf16, h = 8, d = 128, S = 64) */
+    HSA_PATH_TILE_MAJOR = 4,   /* HSA_OP_FORWARD: tile-major (bf16, h = 8, d = 128)         */
+    HSA_PATH_FUSED = 5         /* HSA_OP_BACKWARD: one chunk-major pass with per-(token,
+                                  slot) partial dQ (bf16, h = 8, d = 128, S = 64)          */
+} hsa_path_t;
+
+/* Test and measurement hook, not needed in normal use: serve `op` (HSA_OP_SELECT,
+ * HSA_OP_FORWARD, HSA_OP_BACKWARD, which also covers hsa_backward_attn, or HSA_OP_DECODE,
+ * which also covers hsa_decode_host; -1: all four) with the kernel family `path` from now
+ * on, process-wide and for every thread, until set again (HSA_PATH_AUTO restores the
+ * default).  A family that does not serve a call's shape leaves that call on its default
+ * family.  Results agree across families up to rounding; hsa_attn_workspace_size follows
+ * the setting, so size workspaces after setting it.  Returns INVALID_ARGUMENT for a path
+ * that no kernel of `op` has. */
+hsa_attn_status_t hsa_attn_set_path(int op, int path);
+
+/* The family set for `op` (HSA_PATH_AUTO unless hsa_attn_set_path set another); -1 for an
+ * unknown op. */
+int hsa_attn_get_path(int op);
+
 /* Optional kernel timing: while enabled (on != 0), every kernel launched by this library is
  * bracketed by two HIP events recorded on its stream.  Off by default. */
 hsa_attn_status_t hsa_attn_timing_enable(int on);

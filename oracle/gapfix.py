@@ -14,7 +14,7 @@ import math
 import numpy as np
 
 import hsa_synth
-from . import dims, landmarks_slice, select_slice
+from . import dims, landmarks_slice, scores_at, select_slice
 
 
 def enforce_gap(inp: dict, shape: "hsa_synth.HsaShape", seed: int, min_gap: float = 1e-3,
@@ -46,3 +46,44 @@ def enforce_gap(inp: dict, shape: "hsa_synth.HsaShape", seed: int, min_gap: floa
                 bad = bad[gap2 < min_gap]
                 attempt += 1
     return {"redrawn": int(redrawn), "rows": int(B * L * G)}
+
+
+def decode_gap(q, Kbar, lens, S: int, k: int, alpha=None):
+    """Top-k score gap [B, G] of the decode queries q [B, H, d] (torch or numpy) at positions
+    lens[b] against the landmark cache Kbar [B, C, G, d]: s_(k) - s_(k+1), +inf with at most
+    k candidates."""
+    q = np.asarray(q.detach().double().cpu()) if hasattr(q, "detach") else np.asarray(q, np.float64)
+    B, H, d = q.shape
+    G = Kbar.shape[2]
+    h = H // G
+    gap = np.full((B, G), np.inf)
+    for b in range(B):
+        nc = int(lens[b]) // S
+        if nc <= k:
+            continue
+        kb = Kbar[b, :nc, :].float() if hasattr(Kbar, "float") else Kbar[b, :nc]
+        for g in range(G):
+            dm = dims(int(lens[b]), h, d, S, k, alpha)
+            s = scores_at(dm, q[b, g * h:(g + 1) * h][None], kb[:, g], [int(lens[b])])[0]
+            srt = np.sort(s)[::-1]
+            gap[b, g] = srt[k - 1] - srt[k]
+    return gap
+
+
+def enforce_decode_gap(inp: dict, Kbar, lens, S: int, k: int, min_gap: float = 1e-3,
+                       max_attempts: int = 64, alpha=None) -> int:
+    """Redraw the decode query of every (b, g) whose top-k gap is < min_gap (in place, with
+    hsa_synth.redraw_decode_query, which keeps the planted chunk aligned with the group);
+    returns the number of groups redrawn."""
+    q, u, seed = inp["q"], inp["u"], inp["seed"]
+    gap = decode_gap(q, Kbar, lens, S, k, alpha)
+    bad = list(zip(*np.nonzero(gap < min_gap)))
+    for b, g in bad:
+        for attempt in range(max_attempts + 1):
+            if attempt == max_attempts:
+                raise RuntimeError("decode gap enforcement failed for (%d, %d)" % (b, g))
+            hsa_synth.redraw_decode_query(q, u, seed, int(b), int(g), attempt)
+            one = decode_gap(q[b:b + 1], Kbar[b:b + 1], [lens[b]], S, k, alpha)
+            if one[0, g] >= min_gap:
+                break
+    return len(bad)

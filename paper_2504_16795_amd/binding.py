@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_HERE, "libhsa_mi355x.so")
 HSA_DTYPE_F32, HSA_DTYPE_BF16 = 0, 1
 (HSA_OP_LANDMARKS, HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE,
  HSA_OP_SELECT_BACKWARD, HSA_OP_DECODE_HOST) = range(7)
+(HSA_PATH_AUTO, HSA_PATH_GENERIC, HSA_PATH_TWO_PASS, HSA_PATH_CHUNK_MAJOR,
+ HSA_PATH_TILE_MAJOR, HSA_PATH_FUSED) = range(6)
 HSA_FLAG_STICK_BREAKING = 2
 HSA_FLAG_SOFTMAX_OFF_BY_ONE = 1
 STATUS = {0: "OK", 1: "INVALID_ARGUMENT", 2: "UNSUPPORTED", 3: "WORKSPACE_TOO_SMALL", 4: "HIP"}
@@ -44,7 +46,8 @@ class HsaError(RuntimeError):
 EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
             "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host",
             "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
-            "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect")
+            "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect",
+            "hsa_attn_set_path", "hsa_attn_get_path")
 
 
 def load(path: Optional[str] = None) -> ctypes.CDLL:
@@ -81,9 +84,23 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_attn_timing_select.restype = I32
     lib.hsa_attn_timing_collect.argtypes = [ctypes.c_char_p, SZ]
     lib.hsa_attn_timing_collect.restype = ctypes.c_int
+    lib.hsa_attn_set_path.argtypes = [ctypes.c_int, ctypes.c_int]
+    lib.hsa_attn_set_path.restype = I32
+    lib.hsa_attn_get_path.argtypes = [ctypes.c_int]
+    lib.hsa_attn_get_path.restype = ctypes.c_int
     if path is None:
         _lib = lib
     return lib
+
+
+def set_path(op: int, path: int) -> None:
+    """Serve `op` with the kernel family `path` (hsa_attn_set_path; HSA_PATH_AUTO restores
+    the default); process-wide."""
+    _check(load().hsa_attn_set_path(int(op), int(path)), "hsa_attn_set_path")
+
+
+def get_path(op: int) -> int:
+    return int(load().hsa_attn_get_path(int(op)))
 
 
 def _dtype_code(t: torch.dtype) -> int:

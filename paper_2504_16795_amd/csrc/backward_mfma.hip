@@ -18,8 +18,6 @@
 // and D, plus ds per (token, slot).
 //
 // Key pass: chunk-major, reading those statistics (see bwd_kv_mfma below).
-#include <cstdlib>
-
 #include "chunk_lds.h"
 #include "tile_sel.h"
 
@@ -555,7 +553,7 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
 
 bool backward_mfma_supported(const Dims& dm, bool in_bf16) {
     return in_bf16 && dm.h == HG && dm.d == D && (dm.S == 64 || dm.S == 128) && dm.k <= KMAX &&
-           dm.C <= UWORDS * 32 && !getenv("HSA_FORCE_GENERIC");
+           dm.C <= UWORDS * 32 && path_override(HSA_OP_BACKWARD) != HSA_PATH_GENERIC;
 }
 
 size_t backward_mfma_workspace(const Dims& dm) {

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "hsa.h"
+
 namespace hsa {
 
 // Problem description passed by value to every kernel.
@@ -23,6 +25,10 @@ struct Dims {
     float* dwo;
     int dwacc;
 };
+
+// Kernel-family override of an op (hsa_attn_set_path; HSA_PATH_AUTO unless a caller set
+// one): one relaxed atomic load, so a launcher may read it on every call.
+int path_override(int op);
 
 // bfloat16 storage type of the generic kernels (bit pattern only).
 struct bf16 {

@@ -20,8 +20,6 @@
 // chunks' rows from the host cache (read by the kernel over the host link) into a compact
 // stage [B, G, k, S, d] in device memory, and the attend kernels run "staged": they take
 // the merged selection and read slot i's rows from the stage.
-#include <cstdlib>
-
 #include "chunk_lds.h"
 
 namespace hsa {
@@ -775,7 +773,7 @@ __global__ __launch_bounds__(256) void decode_combine(Dims dm,
 template <typename T, int D>
 bool decode_mfma_shape(const Dims& dm) {
     return sizeof(T) == 2 && D == kAttD && dm.h == kAttH && dm.S == kAttS && dm.k <= KMAX &&
-           !getenv("HSA_FORCE_GENERIC");
+           path_override(HSA_OP_DECODE) != HSA_PATH_GENERIC;
 }
 
 struct DecodeWs {

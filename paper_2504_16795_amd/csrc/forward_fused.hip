@@ -20,8 +20,6 @@
 // range instead of once per query tile, and uses every matrix row, at the cost of a 2 KB
 // partial per (token, slot) written and read back: it pays when tokens of a tile rarely share
 // chunks (long contexts).  No atomics; every sum runs in a fixed order.
-#include <cstdlib>
-
 #include "chunk_stream.h"
 
 namespace hsa {
@@ -36,8 +34,8 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
 constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
-constexpr int kOStores = 2;         // global stores per lane of one output step
-constexpr size_t kOTrashBytes = HG * D * 2;
+constexpr int kOStores = 4;         // global stores per lane of one output step (16 B each)
+constexpr size_t kOTrashBytes = HG * D * 4;
 constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
 
 struct FwdWs {
@@ -53,7 +51,7 @@ __host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
     l.gstart = l.cnt + align256(R * 4);
     l.plan = l.gstart + align256((R + 1) * 4);
     l.part = l.plan + 256;
-    l.trash = l.part + align256(nsel * HG * D * 2);
+    l.trash = l.part + align256(nsel * HG * D * 4);
     l.end = l.trash + kOTrashBytes;
     return l;
 }
@@ -75,7 +73,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const uint32_t* __restrict__ bm, int nwords, const int* __restrict__ gstart,
-    const int* __restrict__ cntr, const int* __restrict__ plan, __bf16* __restrict__ part,
+    const int* __restrict__ cntr, const int* __restrict__ plan, float* __restrict__ part,
     char* __restrict__ trash) {
     __shared__ SmemO sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -100,7 +98,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
-    __bf16* const tpart = reinterpret_cast<__bf16*>(trash);
+    float* const tpart = reinterpret_cast<float*>(trash);
 
     for (int r = find_row(gstart, R, g0); r < R; ++r) {
         const int rs = gstart[r], re = gstart[r + 1];
@@ -168,12 +166,10 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
-                __bf16* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                              (row & 7) * D + 32 * wave + 8 * grp;
-                *reinterpret_cast<bf16x8_t*>(dst) =
-                    bf16x8_t{f2bf(oa[0][rt][0]), f2bf(oa[0][rt][1]), f2bf(oa[0][rt][2]),
-                             f2bf(oa[0][rt][3]), f2bf(oa[1][rt][0]), f2bf(oa[1][rt][1]),
-                             f2bf(oa[1][rt][2]), f2bf(oa[1][rt][3])};
+                float* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
+                             (row & 7) * D + 32 * wave + 8 * grp;
+                *reinterpret_cast<f32x4_t*>(dst) = oa[0][rt];
+                *reinterpret_cast<f32x4_t*>(dst + 4) = oa[1][rt];
             }
         };
 
@@ -308,7 +304,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
 // of the partials at the token's slots that hold a chunk first (0 <= c < floor(t / S); a slot
 // repeating an earlier slot's chunk adds nothing: that partial carries both weights).
 __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __restrict__ idx,
-                                                  const __bf16* __restrict__ part,
+                                                  const float* __restrict__ part,
                                                   __bf16* __restrict__ O) {
     const int lane = threadIdx.x & 63;
     const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
@@ -332,26 +328,20 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
     for (int s0 = 0; s0 < k; s0 += 4) {
-        bf16x8_t pv[4][2];
+        f32x4_t pv[4][4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
             const int use = s < k ? __builtin_amdgcn_readlane(own, s) : 0;
-            if (use) {
-                const __bf16* pp = part + ((so + s) * HG + head) * D + c0;
-                pv[j][0] = ld_bf16x8(pp);
-                pv[j][1] = ld_bf16x8(pp + 8);
-            } else {
-                pv[j][0] = pv[j][1] = bf16x8_t{};
-            }
+            const float* pp = part + ((so + s) * HG + head) * D + c0;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                pv[j][v] = use ? *reinterpret_cast<const f32x4_t*>(pp + 4 * v) : zero4();
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                acc[i] += (float)pv[j][0][i];
-                acc[8 + i] += (float)pv[j][1][i];
-            }
+            for (int i = 0; i < 16; ++i) acc[i] += pv[j][i >> 2][i & 3];
     }
     bf16x8_t o0, o1;
 #pragma unroll
@@ -366,17 +356,16 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
 
 }  // namespace
 
-// The chunk-major forward serves bf16, h = 8, d = 128, S = 64 when the sequence has many
-// chunks (a query tile's tokens then rarely share chunks, which is where the tile-major
-// forward loses its matrix rows); HSA_FWD_PATH=chunk or =tile forces the choice.
+// The chunk-major forward serves bf16, h = 8, d = 128, S = 64 on request
+// (HSA_PATH_CHUNK_MAJOR).
 bool forward_chunk_used(const Dims& dm, bool in_bf16) {
+    const int path = path_override(HSA_OP_FORWARD);
     if (!(in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX) ||
-        (size_t)dm.B * dm.L * dm.G >= ((size_t)1 << 26) || getenv("HSA_FORCE_GENERIC"))
+        (size_t)dm.B * dm.L * dm.G >= ((size_t)1 << 26) || path == HSA_PATH_GENERIC)
         return false;                             // (row and (token, slot) indices are 32-bit)
-    const char* f = getenv("HSA_FWD_PATH");
-    if (f && f[0] == 'c') return true;
-    if (f && f[0] == 't') return false;
-    return dm.C >= 256;
+    // with fp32 partials (bf16 ones round past the bf16 error bound) the tile-major kernel
+    // is the faster one at 4K and 64K tokens: chunk-major on request only
+    return path == HSA_PATH_CHUNK_MAJOR;
 }
 
 size_t forward_chunk_workspace(const Dims& dm, bool in_bf16) {
@@ -392,7 +381,7 @@ hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, co
     int* cnt = (int*)(wsb + l.cnt);
     int* gstart = (int*)(wsb + l.gstart);
     int* plan = (int*)(wsb + l.plan);
-    __bf16* part = (__bf16*)(wsb + l.part);
+    float* part = (float*)(wsb + l.part);
     const int R = dm.B * dm.G * dm.C;
     const int nwords = cdiv(dm.L, 32);
     hipError_t e = launch_selection_bitmap(dm, idx, bmp, st);
@@ -417,7 +406,7 @@ hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, co
         const size_t items = (size_t)dm.B * dm.L * dm.G;
         HSA_TIMED("fwd_reduce", st);
         hipLaunchKernelGGL(fwd_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
-                           idx, (const __bf16*)part, (__bf16*)O);
+                           idx, (const float*)part, (__bf16*)O);
     }
     return hipGetLastError();
 }

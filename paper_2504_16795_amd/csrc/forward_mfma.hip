@@ -18,8 +18,6 @@
 //     reads of the row-major V tile.  Q^T lives in registers for the whole kernel and O^T
 //     accumulates in registers (fp32), so each chunk is read from L2/HBM once per tile
 //     instead of once per (token, slot), and no online softmax is needed.
-#include <cstdlib>
-
 #include "chunk_lds.h"
 #include "tile_sel.h"
 
@@ -211,7 +209,7 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
 
 bool forward_mfma_supported(const Dims& dm, bool in_bf16) {
     return in_bf16 && dm.h == HG && dm.d == D && (dm.S == 64 || dm.S == 128) && dm.k <= KMAX &&
-           dm.C <= UWORDS * 32 && !getenv("HSA_FORCE_GENERIC");
+           dm.C <= UWORDS * 32 && path_override(HSA_OP_FORWARD) != HSA_PATH_GENERIC;
 }
 
 hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, const void* V,

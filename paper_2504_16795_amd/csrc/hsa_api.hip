@@ -2,6 +2,8 @@
 // validation, default scales, workspace sizes and dispatch to the kernel launchers.
 // Nothing is enqueued unless every check passes.
 #include <math.h>
+
+#include <atomic>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -12,6 +14,9 @@
 namespace {
 
 thread_local char g_err[512] = "";
+
+// Kernel-family overrides per op (hsa_attn_set_path), indexed by hsa_op_t.
+std::atomic<int> g_path[8];
 
 hsa_attn_status_t fail(hsa_attn_status_t s, const char* fmt, ...) {
     va_list ap;
@@ -372,3 +377,44 @@ const char* hsa_attn_status_string(hsa_attn_status_t s) {
 const char* hsa_attn_last_error(void) { return g_err; }
 
 }  // extern "C"
+
+namespace hsa {
+int path_override(int op) {
+    return (op >= 0 && op < 8) ? g_path[op].load(std::memory_order_relaxed) : HSA_PATH_AUTO;
+}
+}  // namespace hsa
+
+extern "C" hsa_attn_status_t hsa_attn_set_path(int op, int path) {
+    auto valid_for = [](int o, int pth) {
+        switch (pth) {
+            case HSA_PATH_AUTO:
+            case HSA_PATH_GENERIC: return true;
+            case HSA_PATH_TWO_PASS:
+            case HSA_PATH_FUSED: return o == HSA_OP_BACKWARD;
+            case HSA_PATH_CHUNK_MAJOR:
+            case HSA_PATH_TILE_MAJOR: return o == HSA_OP_FORWARD;
+            default: return false;
+        }
+    };
+    const int ops[4] = {HSA_OP_SELECT, HSA_OP_FORWARD, HSA_OP_BACKWARD, HSA_OP_DECODE};
+    if (op == -1) {
+        if (path != HSA_PATH_AUTO && path != HSA_PATH_GENERIC)
+            return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "path %d does not apply to every op", path);
+        for (int o : ops) g_path[o].store(path, std::memory_order_relaxed);
+        return ok();
+    }
+    if (op != HSA_OP_SELECT && op != HSA_OP_FORWARD && op != HSA_OP_BACKWARD &&
+        op != HSA_OP_DECODE)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "op %d has no kernel families", op);
+    if (!valid_for(op, path))
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "path %d does not apply to op %d", path, op);
+    g_path[op].store(path, std::memory_order_relaxed);
+    return ok();
+}
+
+extern "C" int hsa_attn_get_path(int op) {
+    if (op != HSA_OP_SELECT && op != HSA_OP_FORWARD && op != HSA_OP_BACKWARD &&
+        op != HSA_OP_DECODE)
+        return -1;
+    return g_path[op].load(std::memory_order_relaxed);
+}

@@ -23,8 +23,6 @@
 // end by a bitonic merge on 64-bit order keys (score desc, chunk asc as one integer).  The
 // k best get softmax (or stick-breaking) weights and are written in descending chunk order,
 // padded -1 / 0.
-#include <cstdlib>
-
 #include "chunk_lds.h"
 
 namespace hsa {
@@ -292,7 +290,7 @@ void launch_kc_mfma(const Dims& dm, const void* Q, const float* Kbar, int32_t* i
 
 bool select_mfma_supported(const Dims& dm, bool in_bf16) {
     if (dm.d > D) return in_bf16 && dm.h == 1 && dm.k <= 32;    // only path for wide rows
-    return in_bf16 && dm.d == D && dm.k <= 32 && !getenv("HSA_FORCE_GENERIC");
+    return in_bf16 && dm.d == D && dm.k <= 32 && path_override(HSA_OP_SELECT) != HSA_PATH_GENERIC;
 }
 
 hipError_t launch_select_mfma(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx,

@@ -153,3 +153,29 @@ def test_backward_attn_and_select_backward_check_arguments(lib):
     assert "dw" in lib.hsa_attn_last_error().decode()
     assert lib.hsa_select_backward(ctypes.byref(sp), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                    ws, m - 1, None) == WS_SMALL
+
+
+def test_kernel_path_hook(lib):
+    """hsa_attn_set_path: per-op kernel-family override, validated, read back, restored."""
+    from paper_2504_16795_amd import binding as B
+    assert lib.hsa_attn_get_path(B.HSA_OP_FORWARD) == B.HSA_PATH_AUTO
+    assert lib.hsa_attn_set_path(B.HSA_OP_FORWARD, B.HSA_PATH_CHUNK_MAJOR) == 0
+    assert lib.hsa_attn_get_path(B.HSA_OP_FORWARD) == B.HSA_PATH_CHUNK_MAJOR
+    assert lib.hsa_attn_get_path(B.HSA_OP_BACKWARD) == B.HSA_PATH_AUTO
+    # a family the op has no kernel of, an op without families, an unknown path
+    assert lib.hsa_attn_set_path(B.HSA_OP_BACKWARD, B.HSA_PATH_CHUNK_MAJOR) == 1
+    assert lib.hsa_attn_set_path(B.HSA_OP_FORWARD, B.HSA_PATH_TWO_PASS) == 1
+    assert lib.hsa_attn_set_path(B.HSA_OP_FORWARD, B.HSA_PATH_FUSED) == 1
+    assert lib.hsa_attn_set_path(B.HSA_OP_BACKWARD, B.HSA_PATH_FUSED) == 0
+    assert lib.hsa_attn_get_path(B.HSA_OP_BACKWARD) == B.HSA_PATH_FUSED
+    assert lib.hsa_attn_set_path(B.HSA_OP_LANDMARKS, B.HSA_PATH_GENERIC) == 1
+    assert lib.hsa_attn_set_path(B.HSA_OP_SELECT, 99) == 1
+    assert lib.hsa_attn_set_path(-1, B.HSA_PATH_TWO_PASS) == 1
+    assert lib.hsa_attn_get_path(B.HSA_OP_LANDMARKS) == -1
+    assert lib.hsa_attn_set_path(-1, B.HSA_PATH_GENERIC) == 0
+    for op in (B.HSA_OP_SELECT, B.HSA_OP_FORWARD, B.HSA_OP_BACKWARD, B.HSA_OP_DECODE):
+        assert lib.hsa_attn_get_path(op) == B.HSA_PATH_GENERIC
+    assert lib.hsa_attn_set_path(-1, B.HSA_PATH_AUTO) == 0
+    for op in (B.HSA_OP_SELECT, B.HSA_OP_FORWARD, B.HSA_OP_BACKWARD, B.HSA_OP_DECODE):
+        assert lib.hsa_attn_get_path(op) == B.HSA_PATH_AUTO
+

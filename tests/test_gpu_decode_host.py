@@ -1,5 +1,5 @@
 """GPU parity of the decode step with the key / value cache in host memory (Sec. 3.2 and the
-offloading of Sec. 4.3: only the landmark cache stays on the GPU; the selected chunks are
+offloading of Sec. 4.4: only the landmark cache stays on the GPU; the selected chunks are
 fetched from pinned host memory every step).
 
 The host path runs the same scan, merge and attend kernels as the device-resident decode,
@@ -14,7 +14,7 @@ import torch
 
 import hsa_synth
 import oracle
-from parity import W_ATOL, assert_close
+from parity import check_decode, decode_case
 
 pytestmark = pytest.mark.gpu
 
@@ -40,11 +40,10 @@ def test_decode_host_matches_device_decode_and_oracle(hsa_gpu, dtype, d, k, kbar
                                                       off1):
     shape = Shape(3, 4096 + 64, 16, 2, d, 64, k, dtype)
     banner("decode_host_%s_k%d_stick%d_off%d" % (dtype, k, stick, off1), "hsa_decode_host")
-    inp = hsa_synth.make_decode_inputs(shape, 71, device="cuda")
-    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
     lens = [4096, 4096 + 40, 64 * 5 + 3]
+    inp, Kbar = decode_case(shape, 71, lens, kbar_dtype)
+    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
     cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
-    Kbar = torch.from_numpy(oracle.landmarks(Kc, 64).astype(np.float32)).cuda().to(kbar_dtype)
     Kh, Vh = Kc.cpu().pin_memory(), Vc.cpu().pin_memory()
     o, idx, w = hsa_gpu.hsa_decode_host(q, Kh, Vh, Kbar, 64, k, cache_len=cache_len,
                                         stick_breaking=stick, off_by_one=off1)
@@ -54,16 +53,7 @@ def test_decode_host_matches_device_decode_and_oracle(hsa_gpu, dtype, d, k, kbar
     assert torch.equal(idx, idxd)
     assert torch.equal(w, wd)
     assert torch.equal(o, od)
-    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar.float(), lens, 64, k, stick=stick,
-                                       off_by_one=off1)
-    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar.float(), lens, 64, k, stick=stick,
-                           off_by_one=off1)[0]
-    sure = rgap >= 1e-3             # groups whose selection the score rounding cannot flip
-    assert sure.any()
-    assert np.array_equal(idx.cpu().numpy()[sure], ridx[sure])
-    assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
-    hm = np.repeat(sure, shape.H // shape.G, axis=1)
-    assert_close("o", shape, o[torch.from_numpy(hm).cuda()], ro[hm], o_abs=ro_abs[hm])
+    check_decode(shape, inp, Kbar, lens, o, idx, w, stick=stick, off_by_one=off1)
 
 
 def test_decode_host_refuses_memory_that_is_not_pinned_host_memory(hsa_gpu):

@@ -14,8 +14,8 @@ import torch
 
 import hsa_synth
 import oracle
-from parity import (W_ATOL, assert_close, assert_indices, logit_shift_coord, make_case,
-                    oracle_reference, to_dev)
+from parity import (W_ATOL, assert_close, assert_indices, check_decode, decode_case,
+                    logit_shift_coord, make_case, oracle_reference, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -71,7 +71,7 @@ FWD_PATHS = ["default", "chunk"]
 
 @pytest.mark.parametrize("path", FWD_PATHS)
 @pytest.mark.parametrize("name", list(CASES))
-def test_forward_off_by_one(hsa_gpu, name, path, monkeypatch):
+def test_forward_off_by_one(hsa_gpu, name, path, kernel_path):
     shape, inp, ref, dev = case(name)
     chunk_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
         and shape.H // shape.G == 8
@@ -79,24 +79,24 @@ def test_forward_off_by_one(hsa_gpu, name, path, monkeypatch):
         pytest.skip("the chunk-major forward serves bf16, h = 8, d = 128, S = 64")
     banner(name, "hsa_forward, softmax off by one (%s path)" % path)
     if path == "chunk":
-        monkeypatch.setenv("HSA_FWD_PATH", "chunk")
+        kernel_path(hsa_gpu.HSA_OP_FORWARD, hsa_gpu.HSA_PATH_CHUNK_MAJOR)
     O = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], _dev32(ref["idx"]),
                             _dev32(ref["w"].astype(np.float32)), shape.S, off_by_one=True)
     torch.cuda.synchronize()
     assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
 
 
-@pytest.mark.parametrize("two_pass", [False, True])
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", list(CASES))
-def test_backward_off_by_one(hsa_gpu, name, two_pass, monkeypatch):
+def test_backward_off_by_one(hsa_gpu, name, fused, kernel_path):
     shape, inp, ref, dev = case(name)
     fused_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
         and shape.H // shape.G == 8
-    if two_pass and not fused_shape:
+    if fused and not fused_shape:
         pytest.skip("the two-pass switch only changes the path of the fused shapes")
-    banner(name, "hsa_backward, softmax off by one (%s)" % ("two-pass" if two_pass else "default"))
-    if two_pass:
-        monkeypatch.setenv("HSA_BWD_TWO_PASS", "1")
+    banner(name, "hsa_backward, softmax off by one (%s)" % ("fused" if fused else "default"))
+    if fused:
+        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_FUSED)
     got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], _dev32(ref["Kbar"].astype(np.float32)),
                                _dev32(ref["idx"]), _dev32(ref["w"].astype(np.float32)), dev["dO"],
                                shape.S, off_by_one=True)
@@ -131,25 +131,14 @@ def test_main_variant_pipeline(hsa_gpu, name):
 def test_decode_off_by_one(hsa_gpu, dtype, stick):
     shape = Shape(3, 4096 + 64, 16, 2, 128 if dtype == "bf16" else 64, 64, 8, dtype)
     banner("decode_off1_%s_stick%d" % (dtype, stick), "hsa_decode, softmax off by one")
-    inp = hsa_synth.make_decode_inputs(shape, 81, device="cuda")
-    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
     a = logit_shift_coord(shape, -4.5)
-    Kc[..., 0] = -a                 # every key: the same coordinate 0 (scores move together)
-    q[..., 0] = a
     lens = [4096, 4096 + 40, 64 * 5 + 3]
+    # every key: the same coordinate 0, so all chunk scores move together and the gaps the
+    # query redraws enforce stay; the queries' coordinate 0 is set afterwards
+    inp, Kbar = decode_case(shape, 81, lens, key_coord0=-a)
+    inp["q"][..., 0] = a
     cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
-    Kbar = _dev32(oracle.landmarks(Kc, 64).astype(np.float32))
-    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, 8, cache_len=cache_len,
-                                   stick_breaking=stick, off_by_one=True)
+    o, idx, w = hsa_gpu.hsa_decode(inp["q"], inp["Kc"], inp["Vc"], Kbar, 64, 8,
+                                   cache_len=cache_len, stick_breaking=stick, off_by_one=True)
     torch.cuda.synchronize()
-    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, 64, 8, stick=stick,
-                                       off_by_one=True)
-    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar, lens, 64, 8, stick=stick, off_by_one=True)[0]
-    # groups whose selection is decided by more than the score rounding (nearly all)
-    sure = rgap >= 1e-3
-    assert sure.sum() >= 5
-    assert np.array_equal(idx.cpu().numpy()[sure], ridx[sure])
-    assert np.max(np.abs(w.cpu().numpy()[sure] - rw[sure])) <= W_ATOL
-    heads = torch.from_numpy(np.repeat(sure, shape.H // shape.G, axis=1)).cuda()
-    hm = heads.cpu().numpy()
-    assert_close("o", shape, o[heads], ro[hm], o_abs=ro_abs[hm])
+    check_decode(shape, inp, Kbar, lens, o, idx, w, stick=stick, off_by_one=True)

@@ -10,8 +10,8 @@ import torch
 
 import hsa_synth
 import oracle
-from parity import (W_ATOL, assert_close, assert_indices, make_case, oracle_reference,
-                    to_dev)
+from parity import (W_ATOL, assert_close, assert_indices, check_decode, decode_case,
+                    make_case, oracle_reference, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -65,17 +65,17 @@ def test_select_stick(hsa_gpu, name):
     assert np.all(got.sum(-1) <= 1 + 1e-6)         # the leftover mass goes to no chunk
 
 
-@pytest.mark.parametrize("two_pass", [False, True])
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", list(CASES))
-def test_backward_stick(hsa_gpu, name, two_pass, monkeypatch):
+def test_backward_stick(hsa_gpu, name, fused, kernel_path):
     shape, inp, ref, dev = case(name)
     fused_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
         and shape.H // shape.G == 8
-    if two_pass and not fused_shape:
+    if fused and not fused_shape:
         pytest.skip("the two-pass switch only changes the path of the fused shapes")
-    banner(name, "hsa_backward, stick-breaking (%s)" % ("two-pass" if two_pass else "default"))
-    if two_pass:
-        monkeypatch.setenv("HSA_BWD_TWO_PASS", "1")
+    banner(name, "hsa_backward, stick-breaking (%s)" % ("fused" if fused else "default"))
+    if fused:
+        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_FUSED)
     got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], _dev32(ref["Kbar"].astype(np.float32)),
                                _dev32(ref["idx"]), _dev32(ref["w"].astype(np.float32)), dev["dO"],
                                shape.S, stick_breaking=True)
@@ -131,16 +131,10 @@ def test_pipeline_stick(hsa_gpu, name):
 def test_decode_stick(hsa_gpu, dtype, k):
     shape = Shape(3, 4096 + 64, 16, 2, 128 if dtype == "bf16" else 64, 64, k, dtype)
     banner("decode_stick_%s_k%d" % (dtype, k), "hsa_decode, stick-breaking")
-    inp = hsa_synth.make_decode_inputs(shape, 61, device="cuda")
-    Kc, Vc, q = inp["Kc"], inp["Vc"], inp["q"]
     lens = [4096, 4096 + 40, 64 * 5 + 3]
+    inp, Kbar = decode_case(shape, 61, lens)
     cache_len = torch.tensor(lens, dtype=torch.int32, device="cuda")
-    Kbar = _dev32(oracle.landmarks(Kc, 64).astype(np.float32))
-    o, idx, w = hsa_gpu.hsa_decode(q, Kc, Vc, Kbar, 64, k, cache_len=cache_len,
-                                   stick_breaking=True)
+    o, idx, w = hsa_gpu.hsa_decode(inp["q"], inp["Kc"], inp["Vc"], Kbar, 64, k,
+                                   cache_len=cache_len, stick_breaking=True)
     torch.cuda.synchronize()
-    ro, ridx, rw, rgap = oracle.decode(q, Kc, Vc, Kbar, lens, 64, k, stick=True)
-    ro_abs = oracle.decode(q, Kc, Vc.abs(), Kbar, lens, 64, k, stick=True)[0]
-    assert np.array_equal(idx.cpu().numpy()[rgap >= 1e-3], ridx[rgap >= 1e-3])
-    assert np.max(np.abs(w.cpu().numpy() - rw)) <= W_ATOL
-    assert_close("o", shape, o, ro, o_abs=ro_abs)
+    check_decode(shape, inp, Kbar, lens, o, idx, w, stick=True)
