@@ -262,6 +262,26 @@ hsa_attn_status_t hsa_decode_host(const hsa_attn_params_t* p, const void* q,
                                   const int32_t* cache_len, void* o, int32_t* idx, float* w,
                                   void* ws, size_t ws_bytes, void* stream);
 
+/* Bytes of the device scratch array behind hsa_decode_noalloc (per GPU). */
+#define HSA_DECODE_NOALLOC_SCRATCH_BYTES (8u << 20)
+
+/* hsa_decode for callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that may not call hipMalloc, harnesses that forbid it): the same arguments
+ * and results as hsa_decode, without the workspace arguments.  Its scratch memory (slice
+ * candidates and, off the bf16 h = 8 path, per-slot partial outputs) is a file-scope device
+ * array of HSA_DECODE_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends; the call
+ * allocates and frees nothing.  Shapes whose hsa_attn_workspace_size(p, HSA_OP_DECODE)
+ * exceeds that size return HSA_ATTN_ERR_UNSUPPORTED before any launch (the 1M-token cache of
+ * 8 sequences with 16 query / 2 KV heads needs 0.6 MB).  Every call on a GPU uses that GPU's
+ * one array: calls that overlap on one GPU (on different streams, or from several threads
+ * without ordering) race and give undefined results.  Nothing in the array needs clearing
+ * between calls (every value read was written by the same call). */
+hsa_attn_status_t hsa_decode_noalloc(const hsa_attn_params_t* p, const void* q,
+                                     const void* Kcache, const void* Vcache,
+                                     const void* Kbar_cache, hsa_dtype_t kbar_dtype,
+                                     const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                                     void* stream);
+
 #ifdef __cplusplus
 }
 #endif

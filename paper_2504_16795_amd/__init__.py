@@ -5,7 +5,7 @@ package is its thin Python binding.  Importing the package does not load the lib
 `load()` (or the first call) does, and raises if it has not been built.
 """
 from .binding import (HsaError, HsaParams, hsa_backward, hsa_backward_attn, hsa_decode,
-                      hsa_decode_host,
+                      hsa_decode_host, hsa_decode_noalloc,
                       hsa_forward, hsa_landmarks, hsa_select_backward, hsa_select_topk,
                       load, make_params, workspace_size, set_path, get_path,
                       timing_enable, timing_select, timing_collect,
@@ -18,7 +18,7 @@ from .binding import (HsaError, HsaParams, hsa_backward, hsa_backward_attn, hsa_
                       LIB_PATH)
 
 __all__ = ["HsaError", "HsaParams", "hsa_backward", "hsa_backward_attn", "hsa_decode",
-           "hsa_decode_host",
+           "hsa_decode_host", "hsa_decode_noalloc",
            "hsa_forward", "hsa_landmarks", "hsa_select_backward", "hsa_select_topk", "load",
            "make_params", "workspace_size", "set_path", "get_path",
            "timing_enable", "timing_select", "timing_collect",

@@ -47,7 +47,7 @@ EXPORTED = ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "
             "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host",
             "hsa_attn_workspace_size", "hsa_attn_status_string", "hsa_attn_last_error",
             "hsa_attn_timing_enable", "hsa_attn_timing_select", "hsa_attn_timing_collect",
-            "hsa_attn_set_path", "hsa_attn_get_path")
+            "hsa_attn_set_path", "hsa_attn_get_path", "hsa_decode_noalloc")
 
 
 def load(path: Optional[str] = None) -> ctypes.CDLL:
@@ -69,8 +69,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.hsa_backward_attn.argtypes = [PP, P, P, P, P, P, P, P, P, P, P, I32, P, SZ, P]
     lib.hsa_select_backward.argtypes = [PP, P, P, P, P, P, P, P, P, SZ, P]
     lib.hsa_decode_host.argtypes = [PP, P, P, P, P, I32, P, P, P, P, P, SZ, P]
+    lib.hsa_decode_noalloc.argtypes = [PP, P, P, P, P, I32, P, P, P, P, P]
     for f in ("hsa_landmarks", "hsa_select_topk", "hsa_forward", "hsa_backward", "hsa_decode",
-              "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host"):
+              "hsa_backward_attn", "hsa_select_backward", "hsa_decode_host",
+              "hsa_decode_noalloc"):
         getattr(lib, f).restype = I32
     lib.hsa_attn_workspace_size.argtypes = [PP, ctypes.c_int]
     lib.hsa_attn_workspace_size.restype = SZ
@@ -327,6 +329,34 @@ def hsa_decode(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
                              _ptr(Kbar_cache), _dtype_code(Kbar_cache.dtype), _ptr(cache_len),
                              _ptr(o), _ptr(idx), _ptr(w), _ptr(ws), nb, _stream(q.device)),
            "hsa_decode")
+    return o, idx, w
+
+
+def hsa_decode_noalloc(q, Kcache, Vcache, Kbar_cache, S: int, k: int,
+                       cache_len: Optional[torch.Tensor] = None, sm_scale: float = 0.0,
+                       sel_scale: float = 0.0, out=None, stick_breaking: bool = False,
+                       off_by_one: bool = False):
+    """hsa_decode without a workspace: the library's per-GPU scratch array serves instead
+    (calls overlapping on one GPU race).  Pass `out` to allocate nothing at all."""
+    B, H, d = q.shape
+    Ncap, G = Kcache.shape[1], Kcache.shape[2]
+    _need(q, "q")
+    _need(Kcache, "Kcache", (B, Ncap, G, d), q.dtype, q.device)
+    _need(Vcache, "Vcache", (B, Ncap, G, d), q.dtype, q.device)
+    _need(Kbar_cache, "Kbar_cache", (B, Ncap // S, G, d), None, q.device)
+    if cache_len is not None:
+        _need(cache_len, "cache_len", (B,), torch.int32, q.device)
+    p = make_params(B, Ncap, H, G, d, S, k, q.dtype, sm_scale, sel_scale, stick_breaking,
+                    off_by_one)
+    if out is None:
+        out = (torch.empty_like(q), torch.empty((B, G, k), dtype=torch.int32, device=q.device),
+               torch.empty((B, G, k), dtype=torch.float32, device=q.device))
+    o, idx, w = out
+    _check(load().hsa_decode_noalloc(ctypes.byref(p), _ptr(q), _ptr(Kcache), _ptr(Vcache),
+                                     _ptr(Kbar_cache), _dtype_code(Kbar_cache.dtype),
+                                     _ptr(cache_len), _ptr(o), _ptr(idx), _ptr(w),
+                                     _stream(q.device)),
+           "hsa_decode_noalloc")
     return o, idx, w
 
 

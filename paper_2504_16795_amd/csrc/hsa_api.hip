@@ -4,6 +4,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <mutex>
 #include <stdarg.h>
 #include <stdio.h>
 #include <string.h>
@@ -317,6 +318,86 @@ hsa_attn_status_t hsa_decode(const hsa_attn_params_t* p, const void* q, const vo
                                        Kbar_cache, kbar_dtype == HSA_DTYPE_BF16, cache_len, o,
                                        idx, w, ws, (hipStream_t)stream),
                     "hsa_decode");
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch memory of hsa_decode_noalloc: one array per GPU, held until the process ends.  In
+// host code `scratch` is only a stand-in for the symbol; the device address of each GPU's
+// copy comes from hipGetSymbolAddress and is kept per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)HSA_DECODE_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The calling thread's current device's copy of `scratch` (resolved once per device, with
+// that device current); nullptr with the detail in g_err on failure.
+void* device_scratch() {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        fail(HSA_ATTN_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+        return nullptr;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        fail(HSA_ATTN_ERR_UNSUPPORTED, "device %d beyond the %d supported", dev, kMaxDevices);
+        return nullptr;
+    }
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || ptr == nullptr) {
+            fail(HSA_ATTN_ERR_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+            return nullptr;
+        }
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+hsa_attn_status_t hsa_decode_noalloc(const hsa_attn_params_t* p, const void* q,
+                                     const void* Kcache, const void* Vcache,
+                                     const void* Kbar_cache, hsa_dtype_t kbar_dtype,
+                                     const int32_t* cache_len, void* o, int32_t* idx, float* w,
+                                     void* stream) {
+    hsa::Dims dm;
+    hsa_attn_status_t s = make_dims(p, &dm);
+    if (s != HSA_ATTN_OK) return s;
+    if (kbar_dtype != HSA_DTYPE_F32 && kbar_dtype != HSA_DTYPE_BF16)
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "unknown kbar_dtype %d", (int)kbar_dtype);
+    if (dm.G > 16) return fail(HSA_ATTN_ERR_UNSUPPORTED, "decode supports at most 16 KV heads");
+    if (dm.B == 0) return ok();
+    const size_t need = hsa::decode_workspace(dm);
+    if (need > kNoAllocScratchBytes)
+        return fail(HSA_ATTN_ERR_UNSUPPORTED,
+                    "hsa_decode_noalloc: these shapes need %zu bytes of scratch, more than its "
+                    "%zu (use hsa_decode with a workspace)", need, kNoAllocScratchBytes);
+    CHECK_PTR(q, "q");
+    CHECK_PTR(o, "o");
+    CHECK_PTR(idx, "idx");
+    CHECK_PTR(w, "w");
+    if (dm.C > 0) {
+        CHECK_PTR(Kcache, "Kcache");
+        CHECK_PTR(Vcache, "Vcache");
+        CHECK_PTR(Kbar_cache, "Kbar_cache");
+    }
+    if (cache_len != nullptr && ((uintptr_t)cache_len & 3u))
+        return fail(HSA_ATTN_ERR_INVALID_ARGUMENT, "cache_len is not 4-byte aligned");
+    void* ws = device_scratch();
+    if (ws == nullptr) return HSA_ATTN_ERR_HIP;
+    return launched(hsa::launch_decode(dm, p->dtype == HSA_DTYPE_BF16, q, Kcache, Vcache,
+                                       Kbar_cache, kbar_dtype == HSA_DTYPE_BF16, cache_len, o,
+                                       idx, w, ws, (hipStream_t)stream),
+                    "hsa_decode_noalloc");
 }
 
 hsa_attn_status_t hsa_decode_host(const hsa_attn_params_t* p, const void* q,

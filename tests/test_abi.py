@@ -179,3 +179,22 @@ def test_kernel_path_hook(lib):
     for op in (B.HSA_OP_SELECT, B.HSA_OP_FORWARD, B.HSA_OP_BACKWARD, B.HSA_OP_DECODE):
         assert lib.hsa_attn_get_path(op) == B.HSA_PATH_AUTO
 
+
+def test_decode_noalloc_checks(lib):
+    """hsa_decode_noalloc refuses shapes whose scratch exceeds its per-GPU array, before any
+    launch, and accepts an empty batch."""
+    from paper_2504_16795_amd import binding as B
+    p = B.make_params(4096, 1 << 20, 16, 2, 128, 64, 8, 1)
+    need = lib.hsa_attn_workspace_size(ctypes.byref(p), B.HSA_OP_DECODE)
+    assert need > (8 << 20)
+    fake = ctypes.c_void_p(1 << 20)
+    r = lib.hsa_decode_noalloc(ctypes.byref(p), fake, fake, fake, fake, 0, None, fake, fake,
+                               fake, None)
+    assert r == UNSUPPORTED
+    assert "scratch" in lib.hsa_attn_last_error().decode()
+    p0 = B.make_params(0, 1 << 20, 16, 2, 128, 64, 8, 1)
+    assert lib.hsa_decode_noalloc(ctypes.byref(p0), None, None, None, None, 0, None, None,
+                                  None, None, None) == OK
+    # the 1M-token decode workload fits
+    p1 = B.make_params(8, 1 << 20, 16, 2, 128, 64, 8, 1)
+    assert lib.hsa_attn_workspace_size(ctypes.byref(p1), B.HSA_OP_DECODE) <= (8 << 20)
