@@ -53,11 +53,11 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int FNST = 3;             // LDS stages of the group ring
 constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied per wave and group
-constexpr int kStoresPerStep = 5;   // global stores per lane of one dq step (4 partial, 1 dw)
+constexpr int kStoresPerStep = 3;   // global stores per lane of one dq step (2 partial, 1 dw)
 
 // target of the stores of padding rows (a group's missing tokens), so that every wave issues
 // the same number of stores per group: 8 rows of partial dQ, then 64 float pairs
-constexpr size_t kTrashBytes = HG * D * 4 + 64 * 8;
+constexpr size_t kTrashBytes = HG * D * 2 + 64 * 8;
 
 struct FusedWs {
     size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, kmean,
@@ -77,7 +77,7 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     // 4 per group, at most one group per 4 selections plus one partial group per row
     l.pairsel = l.plan + 256;
     l.part = l.pairsel + align256((nsel + 4 * R) * 4);
-    l.dkraw = l.part + align256(nsel * HG * D * 4);
+    l.dkraw = l.part + align256(nsel * HG * D * 2);
     l.dw = l.dkraw + align256(nrow * D * 4);
     // dw per (token, slot); off by one, per (token, slot, head) the pair {dw, sum_keys dZ}
     l.ds = l.dw + align256(nsel * 4 * (dm.off1 ? 2 * HG : 1));
@@ -116,7 +116,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, const uint32_t* __restrict__ bm, int nwords,
     const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
-    int* __restrict__ pairsel, float* __restrict__ part, float* __restrict__ dwc,
+    int* __restrict__ pairsel, uint16_t* __restrict__ part, float* __restrict__ dwc,
     float* __restrict__ dkraw,
     float* __restrict__ pk, float* __restrict__ pv, char* __restrict__ trash,
     __bf16* __restrict__ dV) {
@@ -155,8 +155,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
-    float* const tpart = reinterpret_cast<float*>(trash);
-    float* const tdw = reinterpret_cast<float*>(trash + HG * D * 4);
+    uint16_t* const tpart = reinterpret_cast<uint16_t*>(trash);
+    float* const tdw = reinterpret_cast<float*>(trash + HG * D * 2);
 
     for (int r = find_row(gstart, R, g0); r < R; ++r) {
         const int rs = gstart[r], re = gstart[r + 1];
@@ -237,10 +237,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
-                float* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                             (row & 7) * D + 32 * wave + 8 * grp;
-                *reinterpret_cast<f32x4_t*>(dst) = qa[0][rt];
-                *reinterpret_cast<f32x4_t*>(dst + 4) = qa[1][rt];
+                uint16_t* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
+                                (row & 7) * D + 32 * wave + 8 * grp;
+                *reinterpret_cast<u32x4_t*>(dst) = bfp_pack8(qa[0][rt], qa[1][rt]);
             }
             if (off1) {
                 // lane (token, head) of wave 0: {dw, W sum_keys dZ} of that head's row
@@ -485,7 +484,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
 __global__ __launch_bounds__(256) void bwd_dq_reduce(
     Dims dm, const __bf16* __restrict__ Q, const float* __restrict__ Kbar,
     const int32_t* __restrict__ idx, const float* __restrict__ w,
-    const float* __restrict__ part, const float* __restrict__ dwc, __bf16* __restrict__ dQ,
+    const uint16_t* __restrict__ part, const float* __restrict__ dwc, __bf16* __restrict__ dQ,
     float* __restrict__ ds, __bf16* __restrict__ qsum) {
     const int lane = threadIdx.x & 63;
     const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
@@ -563,7 +562,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     for (int i = 0; i < 16; ++i) acc[i] = lmk[i] = 0.f;
     const size_t kbbase = (size_t)b * dm.C * dm.G + g;
     for (int s0 = 0; s0 < k; s0 += 4) {
-        f32x4_t pv[4][4];
+        u32x4_t pv[4][2];
         float4 kv[4][4];
         float coef[4], sg[4];
         int use[4];
@@ -574,10 +573,11 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
             const int cs = in ? __builtin_amdgcn_readlane(cl, s) : -1;
             use[j] = in ? __builtin_amdgcn_readlane(own, s) : 0;
             coef[j] = in ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s)) : 0.f;
-            const float* pp = part + ((so + s) * HG + head) * D + c0;
+            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-                pv[j][v] = use[j] ? *reinterpret_cast<const f32x4_t*>(pp + 4 * v) : zero4();
+            for (int v = 0; v < 2; ++v)
+                pv[j][v] = use[j] ? *reinterpret_cast<const u32x4_t*>(pp + 8 * v)
+                                  : u32x4_t{0u, 0u, 0u, 0u};
             // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
             sg[j] = (use[j] && dm.off1) ? dwc[((so + s) * HG + head) * 2 + 1] : 0.f;
             // Kbar_c: the landmark term, and off by one the mean-key term of the partials
@@ -593,7 +593,12 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
 #pragma unroll
-            for (int i = 0; i < 16; ++i) acc[i] += pv[j][i >> 2][i & 3];
+            for (int v = 0; v < 2; ++v) {
+                float x[8];
+                bfp_unpack8(pv[j][v], x);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[8 * v + i] += x[i];
+            }
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 lmk[4 * v + 0] = fmaf(coef[j], kv[j][v].x, lmk[4 * v + 0]);
@@ -827,15 +832,14 @@ __global__ __launch_bounds__(NT) void bwd_finish(
 
 }  // namespace
 
-// Row and (token, slot) indices of this path are 32-bit: B L G < 2^26.  By default it serves
-// sequences of at least 256 chunks (64K tokens: 4.3 ms against 5.6 for the two-pass kernels;
-// at 4K tokens the two-pass kernels are faster, 1.69 against 1.76 ms); HSA_PATH_FUSED forces
-// it.
+// Row and (token, slot) indices of this path are 32-bit: B L G < 2^26.  The default for its
+// shapes (4K tokens: 1.52 ms against 1.68 for the two-pass kernels; 64K: 3.62 against 5.62);
+// HSA_PATH_TWO_PASS selects the two-pass kernels instead.
 bool backward_fused_supported(const Dims& dm, bool in_bf16) {
     const int path = path_override(HSA_OP_BACKWARD);
     return in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX &&
            (size_t)dm.B * dm.L * dm.G < ((size_t)1 << 26) &&
-           (path == HSA_PATH_FUSED || (path == HSA_PATH_AUTO && dm.C >= 256));
+           (path == HSA_PATH_FUSED || path == HSA_PATH_AUTO);
 }
 
 size_t backward_fused_workspace(const Dims& dm) {
@@ -854,7 +858,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     int* gstart = (int*)(wsb + l.gstart);
     int* plan = (int*)(wsb + l.plan);
     int* pairsel = (int*)(wsb + l.pairsel);
-    float* part = (float*)(wsb + l.part);
+    uint16_t* part = (uint16_t*)(wsb + l.part);
     float* dkraw = (float*)(wsb + l.dkraw);
     float* dwc = (float*)(wsb + l.dw);
     float* dsb = (float*)(wsb + l.ds);
@@ -894,7 +898,7 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
         const size_t items = (size_t)dm.B * dm.L * dm.G;
         HSA_TIMED("bwd_dq_reduce", st);
         hipLaunchKernelGGL(bwd_dq_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
-                           (const __bf16*)Q, Kbar, idx, w, (const float*)part, (const float*)dwc,
+                           (const __bf16*)Q, Kbar, idx, w, (const uint16_t*)part, (const float*)dwc,
                            (__bf16*)dQ, dsb, qs);
     }
     e = hipGetLastError();

@@ -34,8 +34,8 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
 constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
-constexpr int kOStores = 4;         // global stores per lane of one output step (16 B each)
-constexpr size_t kOTrashBytes = HG * D * 4;
+constexpr int kOStores = 2;         // global stores per lane of one output step (16 B each)
+constexpr size_t kOTrashBytes = HG * D * 2;
 constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
 
 struct FwdWs {
@@ -51,7 +51,7 @@ __host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
     l.gstart = l.cnt + align256(R * 4);
     l.plan = l.gstart + align256((R + 1) * 4);
     l.part = l.plan + 256;
-    l.trash = l.part + align256(nsel * HG * D * 4);
+    l.trash = l.part + align256(nsel * HG * D * 2);
     l.end = l.trash + kOTrashBytes;
     return l;
 }
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const uint32_t* __restrict__ bm, int nwords, const int* __restrict__ gstart,
-    const int* __restrict__ cntr, const int* __restrict__ plan, float* __restrict__ part,
+    const int* __restrict__ cntr, const int* __restrict__ plan, uint16_t* __restrict__ part,
     char* __restrict__ trash) {
     __shared__ SmemO sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
-    float* const tpart = reinterpret_cast<float*>(trash);
+    uint16_t* const tpart = reinterpret_cast<uint16_t*>(trash);
 
     for (int r = find_row(gstart, R, g0); r < R; ++r) {
         const int rs = gstart[r], re = gstart[r + 1];
@@ -166,10 +166,9 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
-                float* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                             (row & 7) * D + 32 * wave + 8 * grp;
-                *reinterpret_cast<f32x4_t*>(dst) = oa[0][rt];
-                *reinterpret_cast<f32x4_t*>(dst + 4) = oa[1][rt];
+                uint16_t* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
+                                (row & 7) * D + 32 * wave + 8 * grp;
+                *reinterpret_cast<u32x4_t*>(dst) = bfp_pack8(oa[0][rt], oa[1][rt]);
             }
         };
 
@@ -304,7 +303,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
 // of the partials at the token's slots that hold a chunk first (0 <= c < floor(t / S); a slot
 // repeating an earlier slot's chunk adds nothing: that partial carries both weights).
 __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __restrict__ idx,
-                                                  const float* __restrict__ part,
+                                                  const uint16_t* __restrict__ part,
                                                   __bf16* __restrict__ O) {
     const int lane = threadIdx.x & 63;
     const size_t item = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);    // ((b L) + t) G + g
@@ -328,20 +327,25 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
     for (int s0 = 0; s0 < k; s0 += 4) {
-        f32x4_t pv[4][4];
+        u32x4_t pv[4][2];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
             const int use = s < k ? __builtin_amdgcn_readlane(own, s) : 0;
-            const float* pp = part + ((so + s) * HG + head) * D + c0;
+            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
 #pragma unroll
-            for (int v = 0; v < 4; ++v)
-                pv[j][v] = use ? *reinterpret_cast<const f32x4_t*>(pp + 4 * v) : zero4();
+            for (int v = 0; v < 2; ++v)
+                pv[j][v] = use ? *reinterpret_cast<const u32x4_t*>(pp + 8 * v) : u32x4_t{0u, 0u, 0u, 0u};
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) acc[i] += pv[j][i >> 2][i & 3];
+            for (int v = 0; v < 2; ++v) {
+                float x[8];
+                bfp_unpack8(pv[j][v], x);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[8 * v + i] += x[i];
+            }
     }
     bf16x8_t o0, o1;
 #pragma unroll
@@ -356,16 +360,18 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
 
 }  // namespace
 
-// The chunk-major forward serves bf16, h = 8, d = 128, S = 64 on request
-// (HSA_PATH_CHUNK_MAJOR).
+// The chunk-major forward serves bf16, h = 8, d = 128, S = 64 by default from 256 chunks on
+// (64K tokens: 1.75 ms against 2.51 for the tile-major kernel, whose tiles then rarely share
+// a chunk; at 4K tokens 0.81 against 0.54); HSA_PATH_CHUNK_MAJOR or HSA_PATH_TILE_MAJOR
+// forces the choice.
 bool forward_chunk_used(const Dims& dm, bool in_bf16) {
     const int path = path_override(HSA_OP_FORWARD);
     if (!(in_bf16 && dm.h == HG && dm.d == D && dm.S == CS && dm.k <= KMAX) ||
         (size_t)dm.B * dm.L * dm.G >= ((size_t)1 << 26) || path == HSA_PATH_GENERIC)
         return false;                             // (row and (token, slot) indices are 32-bit)
-    // with fp32 partials (bf16 ones round past the bf16 error bound) the tile-major kernel
-    // is the faster one at 4K and 64K tokens: chunk-major on request only
-    return path == HSA_PATH_CHUNK_MAJOR;
+    if (path == HSA_PATH_CHUNK_MAJOR) return true;
+    if (path == HSA_PATH_TILE_MAJOR) return false;
+    return dm.C >= 256;
 }
 
 size_t forward_chunk_workspace(const Dims& dm, bool in_bf16) {
@@ -381,7 +387,7 @@ hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, co
     int* cnt = (int*)(wsb + l.cnt);
     int* gstart = (int*)(wsb + l.gstart);
     int* plan = (int*)(wsb + l.plan);
-    float* part = (float*)(wsb + l.part);
+    uint16_t* part = (uint16_t*)(wsb + l.part);
     const int R = dm.B * dm.G * dm.C;
     const int nwords = cdiv(dm.L, 32);
     hipError_t e = launch_selection_bitmap(dm, idx, bmp, st);
@@ -406,7 +412,7 @@ hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, co
         const size_t items = (size_t)dm.B * dm.L * dm.G;
         HSA_TIMED("fwd_reduce", st);
         hipLaunchKernelGGL(fwd_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
-                           idx, (const float*)part, (__bf16*)O);
+                           idx, (const uint16_t*)part, (__bf16*)O);
     }
     return hipGetLastError();
 }

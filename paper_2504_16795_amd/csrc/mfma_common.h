@@ -86,6 +86,42 @@ __device__ __forceinline__ void split8(const f32x4_t& a, const f32x4_t& b, bf16x
     }
 }
 
+// Per-(token, slot) partial outputs are stored as blocks of 8 values in 16 bytes (block
+// floating point): one power-of-two scale per block and a 13-bit signed integer per value.
+// With E the biased exponent of the block's largest magnitude (at least 14), the value x
+// is stored as q = round(x 2^(139 - E)), |q| < 2^13, in the 16-bit field (q << 1) | bit i of
+// E (field i carries bit i of E).  The error is at most 2^-13 of the block's largest
+// magnitude (bf16 storage: up to 2^-8 of each value's own), in the bytes of bf16.
+__device__ __forceinline__ u32x4_t bfp_pack8(const f32x4_t& a, const f32x4_t& b) {
+    const float m = fmaxf(fmaxf(fmaxf(fabsf(a[0]), fabsf(a[1])), fmaxf(fabsf(a[2]), fabsf(a[3]))),
+                          fmaxf(fmaxf(fabsf(b[0]), fabsf(b[1])), fmaxf(fabsf(b[2]), fabsf(b[3]))));
+    const uint32_t e = max((__float_as_uint(m) >> 23) & 0xFFu, 14u);
+    const float sc = __uint_as_float((266u - e) << 23);        // 2^(139 - e)
+    uint32_t f[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const float x = i < 4 ? a[i] : b[i - 4];
+        // round to the nearest integer: |x sc| < 2^13, so x sc + 1.5 2^23 keeps it in the
+        // low mantissa bits
+        const int q = __float_as_int(fmaf(x, sc, 12582912.f)) - 0x4B400000;
+        f[i] = (((uint32_t)q << 1) | ((e >> i) & 1u)) & 0xFFFFu;
+    }
+    return u32x4_t{f[0] | (f[1] << 16), f[2] | (f[3] << 16), f[4] | (f[5] << 16),
+                   f[6] | (f[7] << 16)};
+}
+
+__device__ __forceinline__ void bfp_unpack8(const u32x4_t& v, float x[8]) {
+    uint32_t e = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) e |= ((v[j] & 1u) << (2 * j)) | (((v[j] >> 16) & 1u) << (2 * j + 1));
+    const float inv = __uint_as_float((e - 12u) << 23);         // 2^(e - 139)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        x[2 * j] = (float)(((int32_t)(v[j] << 16)) >> 17) * inv;
+        x[2 * j + 1] = (float)(((int32_t)v[j]) >> 17) * inv;
+    }
+}
+
 // Waits until every global load of this wave has landed.  Called once after the loads of
 // operands that stay in registers for a whole loop (Q^T, K / V blocks): the compiler cannot
 // tell at the loop header that those loads are complete, and otherwise makes the loop's

@@ -86,17 +86,17 @@ def test_forward_off_by_one(hsa_gpu, name, path, kernel_path):
     assert_close("O", shape, O, ref["O"], o_abs=ref["O_abs"])
 
 
-@pytest.mark.parametrize("fused", [False, True])
+@pytest.mark.parametrize("two_pass", [False, True])
 @pytest.mark.parametrize("name", list(CASES))
-def test_backward_off_by_one(hsa_gpu, name, fused, kernel_path):
+def test_backward_off_by_one(hsa_gpu, name, two_pass, kernel_path):
     shape, inp, ref, dev = case(name)
     fused_shape = shape.dtype == "bf16" and shape.d == 128 and shape.S == 64 \
         and shape.H // shape.G == 8
-    if fused and not fused_shape:
+    if two_pass and not fused_shape:
         pytest.skip("the two-pass switch only changes the path of the fused shapes")
-    banner(name, "hsa_backward, softmax off by one (%s)" % ("fused" if fused else "default"))
-    if fused:
-        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_FUSED)
+    banner(name, "hsa_backward, softmax off by one (%s)" % ("two-pass" if two_pass else "default"))
+    if two_pass:
+        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_TWO_PASS)
     got = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], _dev32(ref["Kbar"].astype(np.float32)),
                                _dev32(ref["idx"]), _dev32(ref["w"].astype(np.float32)), dev["dO"],
                                shape.S, off_by_one=True)

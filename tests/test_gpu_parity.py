@@ -368,13 +368,12 @@ def test_backward_repeated_slots(hsa_gpu, name, kernel_path):
 
 @pytest.mark.parametrize("name", ["L4K_like_bf16", "ragged_mfma_bf16", "key_offset_bf16",
                                   "no_candidates_bf16"])
-def test_backward_fused(hsa_gpu, name, kernel_path):
-    """The fused chunk-major backward (one pass over the selected pairs, per-(token, slot)
-    partial dQ), the default for sequences of at least 256 chunks, forced with
-    HSA_PATH_FUSED on the parity shapes (where the two-pass kernels are the default)."""
+def test_backward_two_pass(hsa_gpu, name, kernel_path):
+    """The two-pass MFMA backward (query pass, then key pass), which serves S = 128 and
+    is selectable for S = 64 with HSA_PATH_TWO_PASS."""
     shape, inp, ref, dev = case(name)
-    banner(name, "hsa_backward, fused path")
-    kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_FUSED)
+    banner(name, "hsa_backward, two-pass path")
+    kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_TWO_PASS)
     idx = torch.from_numpy(ref["idx"]).cuda()
     w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
     Kbar = torch.from_numpy(ref["Kbar"].astype(np.float32)).cuda()

@@ -67,8 +67,8 @@ def test_select_on_selection_inputs(hsa_gpu, dsel, k, stick):
 ATTN_CASES = {
     # name: (shape, seed, options): the fused chunk-major path, the two-pass path (forced, and
     # at S = 128) and the generic kernels
-    "fused_bf16": (Shape(2, 1024, 16, 2, 128, 64, 8, "bf16"), 401, {"fused": True}),
-    "two_pass_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 402, {}),
+    "fused_bf16": (Shape(2, 1024, 16, 2, 128, 64, 8, "bf16"), 401, {}),
+    "two_pass_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 402, {"two_pass": True}),
     "S128_bf16": (Shape(1, 1024, 32, 4, 128, 128, 4, "bf16"), 403, {}),
     "generic_f32": (Shape(2, 1000, 8, 2, 64, 32, 5, "f32"), 404, {}),
 }
@@ -79,8 +79,8 @@ ATTN_CASES = {
 def test_backward_attn(hsa_gpu, name, off1, kernel_path):
     shape, seed, env = ATTN_CASES[name]
     banner(name, "hsa_backward_attn (off by one %d)" % off1)
-    if env.get("fused"):
-        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_FUSED)
+    if env.get("two_pass"):
+        kernel_path(hsa_gpu.HSA_OP_BACKWARD, hsa_gpu.HSA_PATH_TWO_PASS)
     inp, _ = make_case(shape, seed, logit_shift=-4.5 if off1 else 0.0)
     ref = oracle_reference(inp, shape, backward=False)
     dQ_r, dK_r, dV_r, dw_r = oracle.backward(inp["Q"], inp["K"], inp["V"], ref["idx"],
