@@ -439,19 +439,30 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
              "decode_scan": "decode_scan", "decode_attend_mfma": "decode_attend_mfma",
              "decode_gather": "decode_gather", "decode_finish": "decode_finish",
              "decode_combine": "decode_combine"}
-    kernels = {}
+    # per timing name: the bytes of every kernel that maps to it (the two plan kernels, say,
+    # each launched once per step) summed, per launch of the stage (the largest dispatch
+    # count among them); per full kernel name as well
+    totals, by_kernel = {}, {}
     for full in fetch:
         short = next((v for n, v in names.items() if n in full), None)
         if short is None or full not in write:
             continue
-        fb = sum(fetch[full]) / len(fetch[full]) * f_fac
-        wb = sum(write[full]) / len(write[full]) * w_fac
+        ft, wt, nd = sum(fetch[full]) * f_fac, sum(write[full]) * w_fac, len(fetch[full])
+        by_kernel[full] = {"short": short, "fetch_bytes_per_launch": round(ft / nd),
+                           "write_bytes_per_launch": round(wt / nd), "dispatches": nd}
+        t = totals.setdefault(short, [0.0, 0.0, 0])
+        t[0] += ft
+        t[1] += wt
+        t[2] = max(t[2], nd)
+    kernels = {}
+    for short, (ft, wt, nd) in totals.items():
+        fb, wb = ft / nd, wt / nd
         kernels[short] = {"fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
-                          "hbm_bytes_per_launch": round(fb + wb), "dispatches": len(fetch[full])}
+                          "hbm_bytes_per_launch": round(fb + wb), "dispatches": nd}
     rec = {"workload": workload, "source_sha256": source_digest(),
            "calibration": {"kernel": cname, "bytes": CALIB_BYTES,
                            "fetch_factor": round(f_fac, 4), "write_factor": round(w_fac, 4)},
-           "kernels": kernels}
+           "kernels": kernels, "by_kernel": by_kernel}
     with open(out_path, "w") as fh:
         json.dump(rec, fh, indent=1)
     print(json.dumps(rec))

@@ -50,3 +50,28 @@ def test_traffic_summary_calibrates_on_the_first_three_copies(tmp_path):
     assert k["write_bytes_per_launch"] == round(20.0 * 1024)
     assert k["hbm_bytes_per_launch"] == k["fetch_bytes_per_launch"] + k["write_bytes_per_launch"]
     assert rec["source_sha256"] == b.source_digest()
+
+
+def test_traffic_summary_adds_kernels_that_share_a_name(tmp_path):
+    """stream_rowcount and stream_plan both report as 'plan': their bytes add up per launch of
+    the stage instead of the later one replacing the earlier."""
+    b = _bench()
+    copy = "__amd_rocclr_copyBuffer"
+    rc = "void hsa::(anonymous namespace)::stream_rowcount(...)"
+    pl = "void hsa::(anonymous namespace)::stream_plan(...)"
+    calib_kib = b.CALIB_BYTES / 1024.0
+    fetch = [(1, copy, calib_kib / 2), (2, copy, calib_kib / 2), (3, copy, calib_kib / 2),
+             (4, rc, 100.0), (5, pl, 3.0), (6, rc, 100.0), (7, pl, 5.0)]
+    write = [(1, copy, calib_kib), (2, copy, calib_kib), (3, copy, calib_kib),
+             (4, rc, 1.0), (5, pl, 2.0), (6, rc, 1.0), (7, pl, 2.0)]
+    _write(tmp_path / "f.csv", "FETCH_SIZE", fetch)
+    _write(tmp_path / "w.csv", "WRITE_SIZE", write)
+    out = tmp_path / "t.json"
+    b.pmc_summarize("L4K_bf16", str(tmp_path / "f.csv"), str(tmp_path / "w.csv"), str(out))
+    rec = json.loads(out.read_text())
+    k = rec["kernels"]["plan"]
+    assert k["dispatches"] == 2
+    assert k["fetch_bytes_per_launch"] == round((100.0 + 4.0) * 1024 * 2.0)
+    assert k["write_bytes_per_launch"] == round(3.0 * 1024)
+    assert rec["by_kernel"][pl]["fetch_bytes_per_launch"] == round(4.0 * 1024 * 2.0)
+    assert rec["by_kernel"][rc]["short"] == "plan"
