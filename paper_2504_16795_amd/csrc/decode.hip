@@ -7,11 +7,11 @@
 // their partial dot products with DPP moves.  Each wave then extracts the slice's top-k of
 // one group by k rounds of a wave-wide arg-max (ties to the lower chunk index) and writes
 // k (score, chunk) candidates.
-// Stages 2 and 3, MFMA path (bf16, d = 128, h = 8, S = 64): workgroup = (b, g) with 8
-// waves.  Wave 0 merges the slice candidates into the top-k; wave w then attends the
-// selected chunks w, w + 8, ... with matrix cores (K fragments straight from global memory
-// into registers, V rows copied into the wave's own LDS stage and read transposed, as in
-// the forward), and the waves' weighted partial outputs are summed in LDS in wave order.
+// Stages 2 and 3, MFMA path (bf16, d = 128, h = 8, S = 64): workgroup = (slot, b, g).
+// Each merges the slice candidates into the top-k, attends its slot's chunk with matrix
+// cores (K fragments straight from global memory into registers, V rows copied into LDS
+// and read transposed, as in the forward) and stores its weighted partial output; stage 3
+// (combine) sums the partials in slot order.
 // Other shapes: stage 2 (finish), workgroup = (slot, b, g), attends the k selected chunks
 // in parallel; stage 3 (combine), workgroup = (b, g), sums their weighted partial outputs
 // in slot order.
@@ -561,42 +561,45 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
 
 }
 
-constexpr int kAttWaves = 8;
 constexpr int kAttS = 64;
 constexpr int kAttD = 128;
 constexpr int kAttH = 8;
 
-__global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
+// Stage 2 on matrix cores, one workgroup per (slot, b, g) so that the k chunks of a sequence
+// are read through k CUs: every workgroup of a (b, g) merges the slice candidates (the same
+// deterministic merge; the slot-0 one writes idx and w), and wave 0 attends the slot's chunk
+// (K fragments from global memory into registers, V rows copied into LDS and read
+// transposed) and stores w_i P V (fp32) as the slot's partial; decode_combine sums them.
+__global__ __launch_bounds__(kFinThreads) void decode_attend_slot(
     Dims dm, const __bf16* __restrict__ q, const __bf16* __restrict__ Kc,
     const __bf16* __restrict__ Vc, const int32_t* __restrict__ cache_len,
     const float* __restrict__ cand_s, const int32_t* __restrict__ cand_c, int nslices,
-    __bf16* __restrict__ o, int32_t* __restrict__ idx_out, float* __restrict__ w_out,
+    float* __restrict__ part, int32_t* __restrict__ idx_out, float* __restrict__ w_out,
     int staged) {
-    constexpr int S = kAttS, DD = kAttD, NWV = kAttWaves, MB = S / 16, KS2 = S / 32;
-    constexpr int NT = NWV * 64;
-    // Per-wave V stages.  Before the first copy they hold the merge's survivors; after the
-    // last product, the waves' partial outputs.
-    __shared__ __bf16 vst[NWV][S * DD];
+    constexpr int S = kAttS, DD = kAttD, MB = S / 16, KS2 = S / 32;
+    __shared__ __bf16 vst[S * DD];
     __shared__ int sel_c[KMAX];
     __shared__ float sel_w[KMAX];
-    static_assert(NWV * KMAX * sizeof(uint64_t) <= sizeof(vst), "survivors must fit the stages");
-    static_assert(NWV * kAttH * DD * 4 <= sizeof(vst), "partial outputs must fit the stages");
-    uint64_t* mtmp = reinterpret_cast<uint64_t*>(&vst[0][0]);
+    __shared__ uint64_t mtmp[NW * KMAX];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
-    const int bg = blockIdx.x, b = bg / dm.G, g = bg % dm.G;
+    const int slot = blockIdx.x;
+    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
     const int k = dm.k;
-    const int n = min(k, cache_tokens(cache_len, b, dm.L) / S);
+    const int ncand = cache_tokens(cache_len, b, dm.L) / S;
+    const int n = min(k, ncand);
 
-    // Q^T operand: columns 0-7 are the group's heads, 8-15 zero
+    // Q^T operand of wave 0: columns 0-7 are the group's heads, 8-15 zero
     bf16x8_t qB[4];
+    if (wave == 0) {
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)     // branch-free loads (rows 8-15 repeat 0-7), then zeroed
-        qB[ks] = ld_bf16x8(q + ((size_t)b * dm.H + (size_t)g * kAttH + (row & 7)) * DD + 32 * ks +
-                           8 * grp);
+        for (int ks = 0; ks < 4; ++ks)   // branch-free loads (rows 8-15 repeat 0-7), then zeroed
+            qB[ks] = ld_bf16x8(q + ((size_t)b * dm.H + (size_t)g * kAttH + (row & 7)) * DD +
+                               32 * ks + 8 * grp);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-        if (row >= kAttH) qB[ks] = bf16x8_t{};
+        for (int ks = 0; ks < 4; ++ks)
+            if (row >= kAttH) qB[ks] = bf16x8_t{};
+    }
     const int nc = nslices * k;
     if (staged) {                        // the selection is merged already (decode_gather)
         if (tid < k) {
@@ -605,95 +608,79 @@ __global__ __launch_bounds__(kAttWaves * 64) void decode_attend_mfma(
         }
         __syncthreads();
     } else {
-        merge_slices<NWV, NCMAX / NT>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
-                                      nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
-        if (tid < k) {
+        merge_slices<NW, NCMAX / kFinThreads>(cand_s + (size_t)bg * nc, cand_c + (size_t)bg * nc,
+                                              nslices, n, k, mtmp, sel_c, sel_w, dm.stick != 0);
+        if (slot == 0 && tid < k) {
             idx_out[(size_t)bg * k + tid] = sel_c[tid];
             w_out[(size_t)bg * k + tid] = sel_w[tid];
         }
     }
 
-    f32x4_t acc[8];
+    float* const pp = part + ((size_t)bg * k + slot) * kAttH * DD;
+    if (wave == 0 && slot < n) {
+        f32x4_t acc[8];
 #pragma unroll
-    for (int db = 0; db < 8; ++db) acc[db] = zero4();
-    int toff[8];
-    tr_read_offsets(lane, toff);
-    const float sl2 = dm.beta * 1.44269504088896341f;
-    const bool off1 = dm.off1 != 0;                  // softmax off by one
-    const float mfloor = off1 ? 0.f : -INFINITY;
-    // rows of a chunk: the cache [B, N, G, d], or the stage [B, G, k, S, d]
-    const size_t rowstride = staged ? (size_t)DD : (size_t)dm.G * DD;
-    __bf16* stage = vst[wave];
-    const int ncand = cache_tokens(cache_len, b, dm.L) / S;
-    for (int slot = wave; slot < n; slot += NWV) {
+        for (int db = 0; db < 8; ++db) acc[db] = zero4();
         const int c = sel_c[slot];
-        const float wi = sel_w[slot];
-        if (c < 0 || c >= ncand) continue;    // never produced by the scan: an empty slot
-        const size_t key0 = staged ? ((size_t)bg * k + slot) * S * DD
-                                   : ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * DD;
-        // V rows into the stage (copies, issued first: older than the K loads below, so
-        // the compiler's waits for those stay exact), K fragments into registers
-        chunk_to_lds<S, 1>(Vc + key0, rowstride, stage, 0, lane);
-        bf16x8_t kf[4][MB];
+        // a chunk id outside the candidates (never produced by the scan) leaves the slot empty
+        if (c >= 0 && c < ncand) {
+            const float wi = sel_w[slot];
+            const size_t rowstride = staged ? (size_t)DD : (size_t)dm.G * DD;
+            const size_t key0 = staged ? ((size_t)bg * k + slot) * S * DD
+                                       : ((size_t)b * dm.L + (size_t)c * S) * rowstride +
+                                             (size_t)g * DD;
+            // V rows into LDS (copies, issued first), K fragments into registers
+            chunk_to_lds<S, 1>(Vc + key0, rowstride, vst, 0, lane);
+            bf16x8_t kf[4][MB];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+                    kf[ks][mb] = ld_bf16x8(Kc + key0 + (size_t)(16 * mb + row) * rowstride +
+                                           32 * ks + 8 * grp);
+            f32x4_t z[MB];
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) z[mb] = zero4();
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) z[mb] = mfma16(kf[ks][mb], qB[ks], z[mb]);
+            const float sl2 = dm.beta * 1.44269504088896341f;
+            const bool off1 = dm.off1 != 0;
+            float m = -INFINITY;
 #pragma unroll
             for (int mb = 0; mb < MB; ++mb)
-                kf[ks][mb] = ld_bf16x8(Kc + key0 + (size_t)(16 * mb + row) * rowstride + 32 * ks +
-                                       8 * grp);
-        // Z^T = K_c Q^T and the softmax over the chunk's keys, scaled by the chunk weight
-        f32x4_t z[MB];
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb) z[mb] = zero4();
+                for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
+            const float msl = fmaxf(col_max(m), off1 ? 0.f : -INFINITY) * sl2;
+            float ssum = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
+            for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) z[mb] = mfma16(kf[ks][mb], qB[ks], z[mb]);
-        float m = -INFINITY;
+                for (int i = 0; i < 4; ++i) {
+                    z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
+                    ssum += z[mb][i];
+                }
+            const float scale =
+                wi * __builtin_amdgcn_rcpf(col_sum(ssum) + (off1 ? fast_exp2(-msl) : 0.f));
+            int toff[8];
+            tr_read_offsets(lane, toff);
+            wait_loads_le<0>();
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+            for (int ks2 = 0; ks2 < KS2; ++ks2) {
+                const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) m = fmaxf(m, z[mb][i]);
-        const float msl = fmaxf(col_max(m), mfloor) * sl2;
-        float ssum = 0.f;
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                z[mb][i] = fast_exp2(fmaf(z[mb][i], sl2, -msl));
-                ssum += z[mb][i];
-            }
-        const float scale =
-            wi * __builtin_amdgcn_rcpf(col_sum(ssum) + (off1 ? fast_exp2(-msl) : 0.f));
-        // O^T += V^T P^T, once the copies have landed
-        wait_loads_le<0>();
-#pragma unroll
-        for (int ks2 = 0; ks2 < KS2; ++ks2) {
-            const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
-#pragma unroll
-            for (int db = 0; db < 8; ++db) {
-                const __bf16* pv = stage + toff[db] + 32 * ks2 * DD;
-                acc[db] = mfma16(cat(ld_tr16(pv), ld_tr16(pv + 16 * DD)), pb, acc[db]);
+                for (int db = 0; db < 8; ++db) {
+                    const __bf16* pv = vst + toff[db] + 32 * ks2 * DD;
+                    acc[db] = mfma16(cat(ld_tr16(pv), ld_tr16(pv + 16 * DD)), pb, acc[db]);
+                }
             }
         }
-        // the stage is refilled by the next slot's copies: its reads must have returned
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    }
-    __syncthreads();
-    float* red = reinterpret_cast<float*>(&vst[0][0]);
-    if (row < kAttH) {
+        if (row < kAttH) {
 #pragma unroll
-        for (int db = 0; db < 8; ++db)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                red[(wave * kAttH + row) * DD + 16 * db + 4 * grp + i] = acc[db][i];
-    }
-    __syncthreads();
-    for (int x = tid; x < kAttH * DD; x += NT) {
-        float sum = 0.f;
-#pragma unroll
-        for (int w2 = 0; w2 < NWV; ++w2) sum += red[w2 * kAttH * DD + x];
-        o[((size_t)b * dm.H + (size_t)g * kAttH) * DD + x] = f2bf(sum);
+            for (int db = 0; db < 8; ++db)
+                *reinterpret_cast<f32x4_t*>(pp + row * DD + 16 * db + 4 * grp) = acc[db];
+        }
     }
 }
 
@@ -761,10 +748,31 @@ __global__ __launch_bounds__(256) void decode_combine(Dims dm,
     const int bg = blockIdx.x, b = bg / dm.G, g = bg % dm.G;
     const int h = dm.h, k = dm.k;
     const int n = min(k, cache_tokens(cache_len, b, dm.L) / dm.S);
-    for (int x = threadIdx.x; x < h * D; x += 256) {
-        float s = 0.f;
-        for (int i = 0; i < n; ++i) s += part[(((size_t)bg * k + i) * h) * D + x];
-        o[((size_t)b * dm.H + (size_t)g * h) * D + x] = from_f32<T>(s);
+    const size_t stride = (size_t)h * D;            // floats per slot
+    const float* p0 = part + (size_t)bg * k * stride;
+    // 4 consecutive outputs per thread; the slots' loads of 8 slots are issued together
+    // (a loop carrying one load at a time waits for each in turn), then added in slot order
+    for (int x = 4 * threadIdx.x; x < h * D; x += 4 * 256) {
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int i0 = 0; i0 < n; i0 += 8) {
+            float4 v[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                v[j] = i0 + j < n ? *reinterpret_cast<const float4*>(p0 + (i0 + j) * stride + x)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                s.x += v[j].x;
+                s.y += v[j].y;
+                s.z += v[j].z;
+                s.w += v[j].w;
+            }
+        }
+        T* op = o + ((size_t)b * dm.H + (size_t)g * h) * D + x;
+        op[0] = from_f32<T>(s.x);
+        op[1] = from_f32<T>(s.y);
+        op[2] = from_f32<T>(s.z);
+        op[3] = from_f32<T>(s.w);
     }
 }
 
@@ -804,17 +812,23 @@ void launch_tkd(const Dims& dm, const void* q, const void* Kc, const void* Vc, c
     float* cs = (float*)(wb + l.cs);
     int32_t* cc = (int32_t*)(wb + l.cc);
     float* part = (float*)(wb + l.part);
+    const bool mfma = decode_mfma_shape<T, D>(dm);
     {
         HSA_TIMED("decode_scan", st);
         hipLaunchKernelGGL((decode_scan<T, Tk, D>), dim3(nslices, dm.B), dim3(kScanThreads), 0,
                            st, dm, (const T*)q, (const Tk*)Kbar, cache_len, cs, cc,
                            nslices);
     }
-    if (decode_mfma_shape<T, D>(dm)) {
-        HSA_TIMED("decode_attend_mfma", st);
-        hipLaunchKernelGGL(decode_attend_mfma, dim3(dm.B * dm.G), dim3(kAttWaves * 64), 0, st,
-                           dm, (const __bf16*)q, (const __bf16*)Kc, (const __bf16*)Vc,
-                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w, 0);
+    if (mfma) {
+        {
+            HSA_TIMED("decode_attend_mfma", st);
+            hipLaunchKernelGGL(decode_attend_slot, dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
+                               st, dm, (const __bf16*)q, (const __bf16*)Kc, (const __bf16*)Vc,
+                               cache_len, cs, cc, nslices, part, idx, w, 0);
+        }
+        HSA_TIMED("decode_combine", st);
+        hipLaunchKernelGGL((decode_combine<T, D>), dim3(dm.B * dm.G), dim3(256), 0, st, dm,
+                           cache_len, part, (T*)o);
         return;
     }
     {
@@ -841,6 +855,7 @@ void launch_tkd_host(const Dims& dm, const void* q, const void* Kh, const void* 
     float* cs = (float*)(wb + l.cs);
     int32_t* cc = (int32_t*)(wb + l.cc);
     float* part = (float*)(wb + l.part);
+    const bool mfma = decode_mfma_shape<T, D>(dm);
     T* kst = (T*)(wb + l.kst);
     T* vst = (T*)(wb + l.vst);
     {
@@ -855,11 +870,16 @@ void launch_tkd_host(const Dims& dm, const void* q, const void* Kh, const void* 
                            st, dm, (const T*)Kh, (const T*)Vh, cache_len, cs, cc, nslices, idx,
                            w, kst, vst);
     }
-    if (decode_mfma_shape<T, D>(dm)) {
-        HSA_TIMED("decode_attend_mfma", st);
-        hipLaunchKernelGGL(decode_attend_mfma, dim3(dm.B * dm.G), dim3(kAttWaves * 64), 0, st,
-                           dm, (const __bf16*)q, (const __bf16*)kst, (const __bf16*)vst,
-                           cache_len, cs, cc, nslices, (__bf16*)o, idx, w, 1);
+    if (mfma) {
+        {
+            HSA_TIMED("decode_attend_mfma", st);
+            hipLaunchKernelGGL(decode_attend_slot, dim3(dm.k, dm.B * dm.G), dim3(kFinThreads), 0,
+                               st, dm, (const __bf16*)q, (const __bf16*)kst, (const __bf16*)vst,
+                               cache_len, cs, cc, nslices, part, idx, w, 1);
+        }
+        HSA_TIMED("decode_combine", st);
+        hipLaunchKernelGGL((decode_combine<T, D>), dim3(dm.B * dm.G), dim3(256), 0, st, dm,
+                           cache_len, part, (T*)o);
         return;
     }
     {
