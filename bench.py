@@ -4,9 +4,14 @@
 A step is one pass of the whole hot path over one batch of synthetic input:
 landmarks -> score + top-k -> forward -> backward (fwd+bwd workloads), or one decode step.
 Inputs are resident in HBM before the timed region.  The main line is the 4K-context
-fwd+bwd workload (B 8, L 4096, H 16 / G 2, d 128, S 64, k 8, bf16); the 64K-context
-fwd+bwd, the 1M-token decode step, and three layers sharing one selection over inputs of
-its own (with, for comparison, a selection per layer) are reported under "also".
+fwd+bwd workload (B 8, L 4096, H 16 / G 2, d 128, S 64, k 8, bf16); under "also": the same
+with the paper's main variant (stick-breaking weights, softmax off by one), the 64K-context
+fwd+bwd, the wide-selection 16K workload (B 4, H 32 / G 4, S 128, k 16), the tiny fp32
+workload (latency), the 1M-token decode step, and three layers sharing one selection over
+inputs of its own (with, for comparison, a selection per layer).  Every fwd+bwd line
+carries per-stage rates: landmarks and selection against HBM, forward and backward against
+the bf16 matrix-core peak (fp32: the vector peak), from a pass with events between the four
+calls; the decode line carries the scan against HBM and the attend stage.
 
 Kernel durations come from HIP events recorded by the library around its launches on the
 launch stream (hsa_attn_timing_enable / hsa_attn_timing_select).  The last warm-up step
@@ -31,6 +36,14 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "HSA fwd+bwd tokens/s at L=4K and 64K; decode µs/token at 1M-token ctx"
+
+LABELS = {
+    "L4K_bf16": "HSA fwd+bwd at 4K context: B8 L4096 H16/G2 d128 S64 k8, bf16",
+    "L64K_bf16": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
+    "wide_L16K_bf16": ("wide-selection HSA fwd+bwd: B4 L16384 H32/G4 d128 S128 k16, bf16; Q and "
+                       "K of rank 16 plus N(0, 0.1) noise (many queries pick the same chunks)"),
+    "tiny_f32": "tiny HSA fwd+bwd, fp32 (latency): B1 L1024 H4/G1 d64 S64 k4",
+}
 
 # MI355X published peaks
 PEAK_HBM_GBS = 8000.0
@@ -109,14 +122,95 @@ def time_training(sh, dev, steps, warmup, torch, hsa, stick=False, off1=False):
     ws_b = torch.empty(max(1, hsa.workspace_size(p, hsa.HSA_OP_BACKWARD)), dtype=torch.uint8,
                        device="cuda")
 
-    def step():
-        hsa.hsa_landmarks(K, S, out=Kbar)
-        hsa.hsa_select_topk(Q, Kbar, G, S, k, idx=idx, w=w, stick_breaking=stick)
-        hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f, off_by_one=off1)
-        hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads, workspace=ws_b,
-                         stick_breaking=stick, off_by_one=off1)
+    stages = (
+        ("landmarks", lambda: hsa.hsa_landmarks(K, S, out=Kbar)),
+        ("select", lambda: hsa.hsa_select_topk(Q, Kbar, G, S, k, idx=idx, w=w,
+                                               stick_breaking=stick)),
+        ("forward", lambda: hsa.hsa_forward(Q, K, V, idx, w, S, out=O, workspace=ws_f,
+                                            off_by_one=off1)),
+        ("backward", lambda: hsa.hsa_backward(Q, K, V, Kbar, idx, w, dO, S, out=grads,
+                                              workspace=ws_b, stick_breaking=stick,
+                                              off_by_one=off1)))
 
-    return time_steps(step, steps, warmup, torch, hsa)
+    def step():
+        for _, fn in stages:
+            fn()
+
+    ms, kern, brk = time_steps(step, steps, warmup, torch, hsa)
+    return ms, kern, brk, stage_times(stages, max(2, min(steps, 5)), torch)
+
+
+def stage_times(stages, reps, torch):
+    """Mean ms of each stage of a step, from events recorded between the stage calls on the
+    current stream (a pass of its own, after the timed steps)."""
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
+    tot = [0.0] * len(stages)
+    for _ in range(reps):
+        ev[0].record()
+        for i, (_, fn) in enumerate(stages):
+            fn()
+            ev[i + 1].record()
+        torch.cuda.synchronize()
+        for i in range(len(stages)):
+            tot[i] += ev[i].elapsed_time(ev[i + 1])
+    return {name: tot[i] / reps for i, (name, _) in enumerate(stages)}
+
+
+def candidate_scores(B, L, G, S):
+    """Group scores a selection computes: sum over tokens of the candidate count."""
+    n = 0
+    for c in range(-(-L // S)):
+        n += min(S, L - c * S) * c
+    return B * G * n
+
+
+def stage_fractions(sh, pairs, st):
+    """Per stage: achieved rate of its algorithmic work and the fraction of the bound it
+    meets (landmarks and selection against HBM, the attention stages against the matrix
+    cores for bf16, the fp32 vector peak for fp32)."""
+    B, L, H, G, d, S, k = sh.B, sh.L, sh.H, sh.G, sh.d, sh.S, sh.k
+    h, C = H // G, L // S
+    es = 2 if sh.dtype == "bf16" else 4
+    mpeak, munit = ((PEAK_BF16_TFLOPS, "mfma") if sh.dtype == "bf16"
+                    else (PEAK_FP32_VALU_TFLOPS, "alu"))
+    work = {
+        "landmarks": (B * C * S * G * d * es + B * C * G * d * 4, "hbm"),
+        "select": (B * L * H * d * es + B * C * G * d * 4 + B * L * G * k * 8, "hbm"),
+        "forward": (4.0 * h * S * d * pairs, munit),
+        "backward": (10.0 * h * S * d * pairs, munit),
+    }
+    out = {}
+    for name, ms in st.items():
+        amount, bound = work[name]
+        if bound == "hbm":
+            rate = amount / (ms * 1e-3) / 1e9
+            out[name] = {"ms": round(ms, 5), "bound": "hbm", "achieved": round(rate, 1),
+                         "unit": "GB/s", "frac": round(rate / PEAK_HBM_GBS, 4),
+                         "work": amount, "work_unit": "byte"}
+        else:
+            rate = amount / (ms * 1e-3) / 1e12
+            peak = mpeak
+            out[name] = {"ms": round(ms, 5), "bound": bound, "achieved": round(rate, 2),
+                         "unit": "TFLOP/s", "frac": round(rate / peak, 4),
+                         "work": amount, "work_unit": "flop"}
+    out["select"]["score_flops"] = 2.0 * h * d * candidate_scores(B, L, G, S)
+    return out
+
+
+def bench_training(name, steps, warmup, torch, hsa, stick=False, off1=False, label=None):
+    """One fwd+bwd workload: tokens/s, ms per step, per-kernel times, the roofline of the
+    dominant kernel and the per-stage rates."""
+    import hsa_synth
+    sh, _, dev, _ = make_training(name, torch)
+    ms, kern, brk, st = time_training(sh, dev, steps, warmup, torch, hsa, stick, off1)
+    pairs = valid_pairs(sh.B, sh.L, sh.G, sh.S, sh.k)
+    del dev
+    torch.cuda.empty_cache()
+    return {"workload": label or hsa_synth.WORKLOADS[name].get("label", name),
+            "tokens_per_s": round(sh.B * sh.L / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+            "roofline": roofline_of(kern, sh, pairs, name),
+            "stages": stage_fractions(sh, pairs, st),
+            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk.items()}}
 
 
 def time_steps(step, steps, warmup, torch, hsa):
@@ -251,6 +345,19 @@ def bench_decode(steps, warmup, torch, hsa):
                                 "bytes_per_launch": stream_bytes,
                                 "traffic": traffic_of("decode_scan", "decode_1M_bf16")}
     out["algorithmic_bytes_per_step"] = stream_bytes + gather_bytes
+    # per stage: the scan streams the landmark cache (HBM-bound); the attend stage (merge,
+    # attention, combine) reads the selected chunks' keys and values
+    att = [kern[n] for n in ("decode_attend_mfma", "decode_combine", "decode_finish") if n in kern]
+    stages = {}
+    if scan:
+        stages["scan"] = dict(out["scan_roofline"], us=round(scan[1] / scan[0] * 1e3, 3))
+    if att:
+        us_att = sum(t / c for c, t in att) * 1e3
+        gbs = gather_bytes / (us_att * 1e-6) / 1e9
+        stages["attend"] = {"us": round(us_att, 3), "bound": "hbm", "achieved": round(gbs, 1),
+                            "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                            "bytes_per_step": gather_bytes}
+    out["stages"] = stages
     # the same step with the key / value cache in pinned host memory: only the landmark
     # cache stays on the GPU, and the selected chunks cross the host link each step
     Kh = torch.empty(Kc.shape, dtype=Kc.dtype, pin_memory=True)
@@ -342,8 +449,20 @@ def bench_shared(steps, warmup, torch, hsa):
             "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk.items()}}
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
-    """Oracle fwd+bwd on whole (b, g) slices of the workload until the budget is used."""
+    """Oracle fwd+bwd on whole (b, g) slices of the workload until the budget is used, each
+    stage timed on its own."""
     import numpy as np
     import hsa_synth
     import oracle
@@ -351,6 +470,14 @@ def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
     L, G, h, d, S, k = sh.L, sh.G, sh.H // sh.G, sh.d, sh.S, sh.k
     oracle.build(force=False)
     done, t0 = 0, time.time()
+    st = {"landmarks": 0.0, "select": 0.0, "forward": 0.0, "backward": 0.0}
+
+    def timed(stage, fn, *a):
+        t = time.time()
+        r = fn(*a)
+        st[stage] += time.time() - t
+        return r
+
     for b in range(sh.B):
         for g in range(G):
             dm = oracle.dims(L, h, d, S, k)
@@ -358,11 +485,11 @@ def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
             dOs = np.ascontiguousarray(inp["dO"][b, :, g * h:(g + 1) * h], dtype=np.float64)
             Ks = np.ascontiguousarray(inp["K"][b, :, g], dtype=np.float64)
             Vs = np.ascontiguousarray(inp["V"][b, :, g], dtype=np.float64)
-            Kb = oracle.landmarks_slice(dm, Ks)
-            idx, w, _, _ = oracle.select_slice(dm, Qs, Kb)
-            oracle.forward_slice(dm, Qs, Ks, Vs, idx, w)
-            _, ds = oracle.backward_q_slice(dm, Qs, Ks, Vs, Kb, idx, w, dOs)
-            oracle.backward_kv_slice(dm, Qs, Ks, Vs, idx, w, dOs, ds)
+            Kb = timed("landmarks", oracle.landmarks_slice, dm, Ks)
+            idx, w, _, _ = timed("select", oracle.select_slice, dm, Qs, Kb)
+            timed("forward", oracle.forward_slice, dm, Qs, Ks, Vs, idx, w)
+            _, ds = timed("backward", oracle.backward_q_slice, dm, Qs, Ks, Vs, Kb, idx, w, dOs)
+            timed("backward", oracle.backward_kv_slice, dm, Qs, Ks, Vs, idx, w, dOs, ds)
             done += 1
             if time.time() - t0 >= budget_s or done >= max_slices:
                 break
@@ -372,10 +499,12 @@ def cpu_baseline(name, inp, budget_s=12.0, max_slices=16):
     tokens = done * L / G            # each (b, g) slice is 1/G of a sequence's work
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     return {"value": round(tokens / el, 2), "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu_model(),
+            "stage_seconds": {n: round(v, 3) for n, v in st.items()},
+            "stage_tokens_per_s": {n: round(tokens / v, 1) for n, v in st.items() if v > 0},
             "sample": "%d of %d (batch, group) slices of the %s workload, fwd+bwd "
-                      "(landmarks, select, forward, backward), fp64, %.1f s" % (
-                          done, sh.B * G, name, el)}
+                      "(landmarks, select, forward, backward), fp64 on %d OpenMP threads, "
+                      "%.1f s" % (done, sh.B * G, name, threads, el)}
 
 
 CALIB_BYTES = 256 << 20
@@ -395,7 +524,7 @@ def pmc_run(workload, steps, torch, hsa):
         bench_decode(steps, 0, torch, hsa)
     else:
         sh, _, dev, _ = make_training(workload, torch)
-        time_training(sh, dev, steps, 0, torch, hsa)
+        time_training(sh, dev, steps, 1, torch, hsa)
     torch.cuda.synchronize()
 
 
@@ -501,7 +630,7 @@ def main():
     name = "L4K_bf16"
     sh, inp, dev, gen_s = make_training(name, torch)
     print("[bench] %s inputs ready (%.1f s)" % (name, gen_s), file=sys.stderr, flush=True)
-    ms, kern, brk = time_training(sh, dev, args.steps, args.warmup, torch, hsa)
+    ms, kern, brk, st = time_training(sh, dev, args.steps, args.warmup, torch, hsa)
     pairs = valid_pairs(sh.B, sh.L, sh.G, sh.S, sh.k)
     tokens = sh.B * sh.L
     res = {
@@ -509,47 +638,40 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "HSA fwd+bwd at 4K context: B8 L4096 H16/G2 d128 S64 k8, bf16",
+        "config": {"workload": LABELS[name],
                    "batch": sh.B, "seq_len": sh.L, "q_heads": sh.H, "kv_heads": sh.G,
                    "head_dim": sh.d, "chunk": sh.S, "topk": sh.k},
         "roofline": roofline_of(kern, sh, pairs, name),
+        "stages": stage_fractions(sh, pairs, st),
         "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk.items()},
         "kernels_timed_in": ("last warm-up step (event pairs around each launch); the timed "
-                             "steps bracket only the roofline kernel"),
+                             "steps bracket only the roofline kernel; stages from a pass of "
+                             "their own with events between the four calls"),
     }
     print("[bench] %s: %.3f ms/step" % (name, ms), file=sys.stderr, flush=True)
+    del dev
+    torch.cuda.empty_cache()
     if not args.no_extra:
+        also = res["also"] = {}
         # the paper's main variant on the same workload: stick-breaking chunk weights and
         # the softmax off by one inside a chunk
-        msv, _, brkv = time_training(sh, dev, max(2, args.steps // 2), 2, torch, hsa,
-                                     stick=True, off1=True)
-        res["also"] = {"L4K_bf16_main_variant": {
-            "workload": ("HSA fwd+bwd at 4K context, stick-breaking weights and softmax off by "
-                         "one: B8 L4096 H16/G2 d128 S64 k8, bf16"),
-            "tokens_per_s": round(tokens / (msv * 1e-3), 1), "ms_per_step": round(msv, 4),
-            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brkv.items()}}}
-        print("[bench] %s main variant: %.3f ms/step" % (name, msv), file=sys.stderr, flush=True)
-        del dev
-        torch.cuda.empty_cache()
-        name3 = "L64K_bf16"
-        sh3, _, dev3, _ = make_training(name3, torch)
-        ms3, kern3, brk3 = time_training(sh3, dev3, max(2, args.steps // 2), 2, torch, hsa)
-        pairs3 = valid_pairs(sh3.B, sh3.L, sh3.G, sh3.S, sh3.k)
-        res["also"]["L64K_bf16"] = {
-            "workload": "HSA fwd+bwd at 64K context: B1 L65536 H16/G2 d128 S64 k8, bf16",
-            "tokens_per_s": round(sh3.B * sh3.L / (ms3 * 1e-3), 1), "ms_per_step": round(ms3, 4),
-            "roofline": roofline_of(kern3, sh3, pairs3, name3),
-            "kernels_avg_ms": {n: round(t / c, 5) for n, (c, t) in brk3.items()}}
-        print("[bench] %s: %.3f ms/step" % (name3, ms3), file=sys.stderr, flush=True)
-        del dev3
-        torch.cuda.empty_cache()
-        res["also"]["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 10, torch, hsa)
-        print("[bench] decode: %.2f us/step" % res["also"]["decode_1M_bf16"]["us_per_step"],
+        also["L4K_bf16_main_variant"] = bench_training(
+            name, max(2, args.steps // 2), 2, torch, hsa, stick=True, off1=True,
+            label=LABELS[name] + "; stick-breaking weights and softmax off by one")
+        print("[bench] %s main variant: %.3f ms/step"
+              % (name, also["L4K_bf16_main_variant"]["ms_per_step"]), file=sys.stderr, flush=True)
+        for extra in ("L64K_bf16", "wide_L16K_bf16", "tiny_f32"):
+            also[extra] = bench_training(extra, max(2, args.steps // 2), 2, torch, hsa,
+                                         label=LABELS[extra])
+            print("[bench] %s: %.3f ms/step" % (extra, also[extra]["ms_per_step"]),
+                  file=sys.stderr, flush=True)
+        also["decode_1M_bf16"] = bench_decode(max(20, args.steps * 5), 10, torch, hsa)
+        print("[bench] decode: %.2f us/step" % also["decode_1M_bf16"]["us_per_step"],
               file=sys.stderr, flush=True)
         torch.cuda.empty_cache()
-        res["also"]["shared_x3_L4K_bf16"] = bench_shared(max(2, args.steps // 2), 2, torch, hsa)
+        also["shared_x3_L4K_bf16"] = bench_shared(max(2, args.steps // 2), 2, torch, hsa)
         print("[bench] shared selection x3: %.3f ms/step"
-              % res["also"]["shared_x3_L4K_bf16"]["ms_per_step"], file=sys.stderr, flush=True)
+              % also["shared_x3_L4K_bf16"]["ms_per_step"], file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(name, inp)
         print("[bench] cpu baseline done", file=sys.stderr, flush=True)
