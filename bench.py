@@ -397,7 +397,7 @@ def bench_decode(steps, warmup, torch, hsa):
 
 
 def bench_shared(steps, warmup, torch, hsa):
-    """Sec. 4.3's setting: three attention layers sharing one selection over inputs of their
+    """Sec. 4.4's setting: three attention layers sharing one selection over inputs of their
     own (d_sel = h d_h = 1024), forward and backward of all three plus the selection and its
     backward per step; and the same with a selection (and its backward) per layer."""
     import hsa_synth

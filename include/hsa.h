@@ -150,7 +150,7 @@ hsa_attn_status_t hsa_backward(const hsa_attn_params_t* p, const void* Q, const 
 
 /* Backward of the attention alone, for a selection over inputs of its own (Sec. 3.1: the
  * selection query and chunk representations come from projections of their own, and
- * Sec. 4.3 shares one selection across the HSA layers).  The same as hsa_backward except
+ * Sec. 4.4 shares one selection across the HSA layers).  The same as hsa_backward except
  * that the scores do not depend on Q or K: dQ and dK carry no score or landmark term, no
  * Kbar is read, and dw [B, L, G, k] float32 receives d loss / d w per slot (0 in empty
  * slots; each slot holding a chunk gets the chunk's dw), overwritten, or added to what dw
@@ -247,7 +247,7 @@ const char* hsa_attn_status_string(hsa_attn_status_t s);
 const char* hsa_attn_last_error(void);
 
 /* Single-token decode with the key / value cache in host memory (Sec. 3.2 "Inference" and
- * the memory offloading of Sec. 4.3: only the landmark cache stays on the GPU, and the
+ * the memory offloading of Sec. 4.4: only the landmark cache stays on the GPU, and the
  * selected chunks' keys and values are fetched from the host each step).  The same as
  * hsa_decode, with Kcache and Vcache [B, N_cap, G, d] in pinned host memory (hipHostMalloc,
  * or a pinned torch tensor) that the device can address; the selected chunks are read by a

@@ -1,6 +1,6 @@
 // Gradient through the selection scores alone (Sec. 3.1: s_i = alpha q~ . Kbar_{c_i}; the
 // weights of Sec. 3.1.1), for a selection over inputs of its own whose dw was summed over
-// every layer that used it (Sec. 4.3 shares one selection across the HSA layers):
+// every layer that used it (Sec. 4.4 shares one selection across the HSA layers):
 //   ds_i          from dw and w by the weight rule (softmax, or stick-breaking)
 //   dQ[t, j, :]   = alpha sum_i ds_i Kbar_{c_i}               (each of the group's h rows)
 //   dKbar[c, :]   = alpha sum over (t, i) with c_i = c of ds_i q~_t,  q~ = sum_j q_j

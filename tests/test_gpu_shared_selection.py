@@ -1,6 +1,6 @@
 """GPU parity of a selection over inputs of its own shared by several layers (Sec. 3.1: the
 selection query and chunk representations come from projections of their own, of the
-group dimension d_g = h d_h; Sec. 4.3: one selection serves every HSA layer):
+group dimension d_g = h d_h; Sec. 4.4: one selection serves every HSA layer):
 hsa_select_topk on the selection inputs (rows up to 1024 long), hsa_backward_attn per
 layer (no score term, dw out or accumulated), hsa_select_backward of the summed dw.
 """
@@ -127,7 +127,7 @@ def test_select_backward(hsa_gpu, dsel, dtype, stick):
 
 @pytest.mark.parametrize("stick,off1", [(False, False), (True, True)])
 def test_three_layers_share_one_selection(hsa_gpu, stick, off1):
-    """Sec. 4.3's setting: one selection over inputs of their own (d_sel = h d_h = 1024)
+    """Sec. 4.4's setting: one selection over inputs of their own (d_sel = h d_h = 1024)
     serves three attention layers; forward per layer, backward per layer with dw
     accumulated, then the selection backward, all on the GPU, against the oracle."""
     shape = Shape(1, 2048, 16, 2, 128, 64, 8, "bf16")

@@ -564,7 +564,7 @@ def test_decode_planted_chunk_is_selected():
 # ------------------------------------------------- selection over its own inputs ----
 
 def _shared_selection_loss(Qs, Ks, layers, S, k, stick, off1, idx_ref):
-    """Sec. 3.1 / Sec. 4.3: one selection from the selection inputs (Qs [B, L, G, d_sel],
+    """Sec. 3.1 / Sec. 4.4: one selection from the selection inputs (Qs [B, L, G, d_sel],
     Ks [B, C, G, d_sel]) serves every layer; loss = sum over layers of sum(O_l * dO_l)."""
     G = Ks.shape[2]
     idx, w, _, _ = oracle.select(Qs, Ks, G, S, k, stick=stick)
