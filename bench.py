@@ -140,12 +140,34 @@ def time_training(sh, dev, steps, warmup, torch, hsa, stick=False, off1=False):
     return ms, kern, brk, stage_times(stages, max(2, min(steps, 5)), torch)
 
 
+def gpu_backlog(torch, ms=2.0):
+    """Queue about `ms` of device time ahead of the host (a spin kernel), so that launches
+    enqueued next run back to back instead of waiting for the host; the spin is calibrated
+    once per process."""
+    global _SPIN_PER_MS
+    if _SPIN_PER_MS is None:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1000)                 # first launch of the spin kernel
+        torch.cuda.synchronize()
+        e0.record()
+        torch.cuda._sleep(1000000)
+        e1.record()
+        torch.cuda.synchronize()
+        _SPIN_PER_MS = 1000000 / max(e0.elapsed_time(e1), 1e-3)
+    torch.cuda._sleep(int(ms * _SPIN_PER_MS))
+
+
+_SPIN_PER_MS = None
+
+
 def stage_times(stages, reps, torch):
     """Mean ms of each stage of a step, from events recorded between the stage calls on the
-    current stream (a pass of its own, after the timed steps)."""
+    current stream (a pass of its own, after the timed steps).  Each pass starts behind a
+    queued spin kernel, so the events time the stages' kernels, not the host's calls."""
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(stages) + 1)]
     tot = [0.0] * len(stages)
     for _ in range(reps):
+        gpu_backlog(torch)
         ev[0].record()
         for i, (_, fn) in enumerate(stages):
             fn()
@@ -224,6 +246,7 @@ def time_steps(step, steps, warmup, torch, hsa):
         if i == warmup - 1:
             torch.cuda.synchronize()
             hsa.timing_collect()               # drop anything recorded before
+            gpu_backlog(torch)                 # the step's launches then run back to back
             hsa.timing_enable(True)
         step()
     torch.cuda.synchronize()
@@ -313,18 +336,30 @@ def bench_decode(steps, warmup, torch, hsa):
         if i == warmup // 2:
             torch.cuda.synchronize()
             hsa.timing_collect()
+            gpu_backlog(torch, 0.1 * warmup + 1.0)
             hsa.timing_enable(True)
         hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
     torch.cuda.synchronize()
     hsa.timing_enable(False)
     kern = hsa.timing_collect()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(steps):
-        hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
-    e1.record()
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) / steps * 1e3
+
+    def timed(backlog):
+        # backlog: the steps queued behind a spin kernel, so that the events time the
+        # device's work alone (back to back, as a captured graph would run it); without it,
+        # the host's calls pace the steps
+        torch.cuda.synchronize()
+        if backlog:
+            gpu_backlog(torch, 0.1 * steps + 1.0)
+        e0.record()
+        for _ in range(steps):
+            hsa.hsa_decode(q, Kc, Vc, kbar, sh.S, sh.k, out=(o, idx, w), workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps * 1e3
+
+    us = timed(True)
+    us_host = timed(False)
     planted_ok = all(int(inp["planted"][b, g]) in idx[b, g].tolist()
                      for b in range(sh.B) for g in range(sh.G))
     C = sh.L // sh.S
@@ -334,6 +369,10 @@ def bench_decode(steps, warmup, torch, hsa):
     out = {"workload": "decode 1M ctx: B8, 1 token/seq, cache 2^20 tokens (16384 chunks of 64),"
                        " H16/G2 d128 k8, bf16 landmark cache",
            "us_per_step": round(us, 3), "us_per_sequence_token": round(us / sh.B, 3),
+           "us_per_step_host_paced": round(us_host, 3),
+           "timing": ("us_per_step: the steps' device time, queued back to back behind a spin "
+                      "kernel; us_per_step_host_paced: the same steps launched as the host "
+                      "makes the calls"),
            "tokens_per_s": round(sh.B / (us * 1e-6), 1), "planted_chunk_selected": planted_ok,
            "kernels_avg_us": {n: round(t / c * 1e3, 3) for n, (c, t) in kern.items()},
            "kernels_timed_in": "second half of the warm-up (event pairs around each launch)"}
@@ -371,6 +410,7 @@ def bench_decode(steps, warmup, torch, hsa):
         if i == warmup // 2:
             torch.cuda.synchronize()
             hsa.timing_collect()
+            gpu_backlog(torch, 0.1 * warmup + 1.0)
             hsa.timing_enable(True)
         hsa.hsa_decode_host(q, Kh, Vh, kbar, sh.S, sh.k, out=(oh, idxh, wh), workspace=wsh)
     torch.cuda.synchronize()

@@ -55,9 +55,10 @@ constexpr int FNST = 3;             // LDS stages of the group ring
 constexpr int BPW = 8 / NW;         // 1 KB row blocks of Q (and of dO) copied per wave and group
 constexpr int kStoresPerStep = 3;   // global stores per lane of one dq step (2 partial, 1 dw)
 
-// target of the stores of padding rows (a group's missing tokens), so that every wave issues
-// the same number of stores per group: 8 rows of partial dQ, then 64 float pairs
-constexpr size_t kTrashBytes = HG * D * 2 + 64 * 8;
+// target of the dw stores of padding rows (a group's missing tokens), so that every wave
+// issues the same number of stores per group: 64 float pairs (their partial dQ rows go to the
+// spare block after the partials)
+constexpr size_t kTrashBytes = 64 * 8;
 
 struct FusedWs {
     size_t bitmap, cnt, gstart, plan, pairsel, part, dkraw, dw, ds, qsum, pk, pv, pkb, dkbar, kmean,
@@ -77,7 +78,7 @@ __host__ __device__ inline FusedWs fused_ws(const Dims& dm) {
     // 4 per group, at most one group per 4 selections plus one partial group per row
     l.pairsel = l.plan + 256;
     l.part = l.pairsel + align256((nsel + 4 * R) * 4);
-    l.dkraw = l.part + align256(nsel * HG * D * 2);
+    l.dkraw = l.part + align256((nsel + 1) * HG * D * 2);     // + the spare block
     l.dw = l.dkraw + align256(nrow * D * 4);
     // dw per (token, slot); off by one, per (token, slot, head) the pair {dw, sum_keys dZ}
     l.ds = l.dw + align256(nsel * 4 * (dm.off1 ? 2 * HG : 1));
@@ -155,8 +156,11 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
-    uint16_t* const tpart = reinterpret_cast<uint16_t*>(trash);
-    float* const tdw = reinterpret_cast<float*>(trash + HG * D * 2);
+    // a lane's partial-store address is pbase + 2 KB * block, block = the (token, slot) or,
+    // for rows of missing tokens, tblk: the spare block after the partials
+    char* const pbase = reinterpret_cast<char*>(part) + 2 * ((row & 7) * D + 32 * wave + 8 * grp);
+    const uint32_t tblk = (uint32_t)((size_t)dm.B * dm.L * dm.G * dm.k);
+    float* const tdw = reinterpret_cast<float*>(trash);
 
     for (int r = find_row(gstart, R, g0); r < R; ++r) {
         const int rs = gstart[r], re = gstart[r + 1];
@@ -197,8 +201,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
 #pragma unroll
         for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
 
-        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
-            FStage& st = sm.st[gi % FNST];
+        auto issue = [&](int gi, int nl, FStage& st) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < BPW; ++i) {
                 const int blk = wave * BPW + i;
@@ -216,7 +219,7 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
         // slot, head): rows 16 rt + (lane & 15), d = 32 wave + 8 grp + (0..7); then
         // the group's dw (wave 0, carried from its combine step), off by one with the row's
         // sum of dZ over the keys (sig, times W here).  Exactly kStoresPerStep stores per
-        // lane: rows of missing tokens go to the trash area.
+        // lane: rows of missing tokens go to the spare block and the trash area.
         auto dq_step = [&](int gj, int nl, float dtok, float sig) __attribute__((always_inline)) {
             f32x4_t qa[2][2];
 #pragma unroll
@@ -237,9 +240,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
-                uint16_t* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                                (row & 7) * D + 32 * wave + 8 * grp;
-                *reinterpret_cast<u32x4_t*>(dst) = bfp_pack8(qa[0][rt], qa[1][rt]);
+                const uint32_t blk = so >= 0 ? (uint32_t)so : tblk;
+                *reinterpret_cast<u32x4_t*>(pbase + ((size_t)blk << 11)) =
+                    bfp_pack8(qa[0][rt], qa[1][rt]);
             }
             if (off1) {
                 // lane (token, head) of wave 0: {dw, W sum_keys dZ} of that head's row
@@ -301,9 +304,12 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
             const int ngroups = (nl + 3) / 4;
 #pragma unroll
             for (int u = 0; u < FNST - 1; ++u)
-                if (u < ngroups) issue(u, nl);
+                if (u < ngroups) issue(u, nl, sm.st[u]);
             float dtok_pend = 0.f, sig_pend = 0.f;
-            for (int gi = 0; gi < ngroups; ++gi) {
+            // one group's step; its stage index SI = gi % FNST is a constant (the loop below
+            // is unrolled by FNST), so the stage's LDS addresses are lane bases plus immediates
+            auto group = [&](int gi, auto si) __attribute__((always_inline)) {
+                constexpr int SI = decltype(si)::value;
                 // Group gi has landed once only the memory operations issued after its copies
                 // remain: the previous iteration's dq stores (when it ran one) and the next
                 // group's copies (when there is a next group).  Loads and stores complete in
@@ -316,8 +322,8 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                 lds_wait();
                 barrier_keep_copies();   // stage gi landed, dZ^T of gi - 1 complete, stage gi - 1 free
                 if (gi > 0) dq_step(gi - 1, nl, dtok_pend, sig_pend);
-                if (gi + FNST - 1 < ngroups) issue(gi + FNST - 1, nl);
-                const FStage& st = sm.st[gi % FNST];
+                if (gi + FNST - 1 < ngroups) issue(gi + FNST - 1, nl, sm.st[(SI + FNST - 1) % FNST]);
+                const FStage& st = sm.st[SI];
 
                 // ---- Z, dP for the wave's 16 keys (rows 16 rb + 4 grp + i, key 16 wave + row) --
                 f32x4_t z[2], dp[2];
@@ -450,6 +456,12 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                     aK[db] = mfma16(dzh, qb, aK[db]);
                     aK[db] = mfma16(dzl, qb, aK[db]);
                 }
+            };
+            static_assert(FNST == 3, "the group loop is unrolled by the ring depth");
+            for (int gb = 0; gb < ngroups; gb += FNST) {
+                group(gb, IntC<0>{});
+                if (gb + 1 < ngroups) group(gb + 1, IntC<1>{});
+                if (gb + 2 < ngroups) group(gb + 2, IntC<2>{});
             }
             lds_wait();
             barrier_keep_copies();   // dZ^T of the batch's last group complete
@@ -561,54 +573,56 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = lmk[i] = 0.f;
     const size_t kbbase = (size_t)b * dm.C * dm.G + g;
+    // Kbar_c serves the landmark term, and off by one the mean-key term of the partials
+    // (given the attention alone, the launcher passes the layer's key means)
+    const bool need_kb = ncand > 0 && (!attn_only || dm.off1);
+    // slot values are wave-uniform (lane reads), so the branches below are scalar
     for (int s0 = 0; s0 < k; s0 += 4) {
         u32x4_t pv[4][2];
         float4 kv[4][4];
-        float coef[4], sg[4];
-        int use[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
-            const bool in = s < k;
-            const int cs = in ? __builtin_amdgcn_readlane(cl, s) : -1;
-            use[j] = in ? __builtin_amdgcn_readlane(own, s) : 0;
-            coef[j] = in ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s)) : 0.f;
-            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+            if (s < k && __builtin_amdgcn_readlane(own, s)) {
+                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
+            }
+            if (s < k && need_kb) {
+                const int cs = __builtin_amdgcn_readlane(cl, s);
+                const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
+                const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
 #pragma unroll
-            for (int v = 0; v < 2; ++v)
-                pv[j][v] = use[j] ? *reinterpret_cast<const u32x4_t*>(pp + 8 * v)
-                                  : u32x4_t{0u, 0u, 0u, 0u};
-            // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
-            sg[j] = (use[j] && dm.off1) ? dwc[((so + s) * HG + head) * 2 + 1] : 0.f;
-            // Kbar_c: the landmark term, and off by one the mean-key term of the partials
-            // (given the attention alone, the launcher passes the layer's key means)
-            const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
-            const bool need_kb = ncand > 0 && (!attn_only || dm.off1);
-            const float* kb = need_kb ? Kbar + (kbbase + (size_t)cc * dm.G) * D + c0 : nullptr;
-#pragma unroll
-            for (int v = 0; v < 4; ++v)
-                kv[j][v] = need_kb ? *reinterpret_cast<const float4*>(kb + 4 * v)
-                                   : float4{0.f, 0.f, 0.f, 0.f};
+                for (int v = 0; v < 4; ++v) kv[j][v] = *reinterpret_cast<const float4*>(kb + 4 * v);
+            }
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                float x[8];
-                bfp_unpack8(pv[j][v], x);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) acc[8 * v + i] += x[i];
+            const int s = s0 + j;
+            if (s >= k) break;
+            if (__builtin_amdgcn_readlane(own, s)) {
+                bfp_accum8(pv[j][0], acc);
+                bfp_accum8(pv[j][1], acc + 8);
             }
+            if (!need_kb) continue;
+            const float coef = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s));
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                lmk[4 * v + 0] = fmaf(coef[j], kv[j][v].x, lmk[4 * v + 0]);
-                lmk[4 * v + 1] = fmaf(coef[j], kv[j][v].y, lmk[4 * v + 1]);
-                lmk[4 * v + 2] = fmaf(coef[j], kv[j][v].z, lmk[4 * v + 2]);
-                lmk[4 * v + 3] = fmaf(coef[j], kv[j][v].w, lmk[4 * v + 3]);
-                acc[4 * v + 0] = fmaf(sg[j], kv[j][v].x, acc[4 * v + 0]);
-                acc[4 * v + 1] = fmaf(sg[j], kv[j][v].y, acc[4 * v + 1]);
-                acc[4 * v + 2] = fmaf(sg[j], kv[j][v].z, acc[4 * v + 2]);
-                acc[4 * v + 3] = fmaf(sg[j], kv[j][v].w, acc[4 * v + 3]);
+                lmk[4 * v + 0] = fmaf(coef, kv[j][v].x, lmk[4 * v + 0]);
+                lmk[4 * v + 1] = fmaf(coef, kv[j][v].y, lmk[4 * v + 1]);
+                lmk[4 * v + 2] = fmaf(coef, kv[j][v].z, lmk[4 * v + 2]);
+                lmk[4 * v + 3] = fmaf(coef, kv[j][v].w, lmk[4 * v + 3]);
+            }
+            if (dm.off1 && __builtin_amdgcn_readlane(own, s)) {
+                // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
+                const float sg = dwc[((so + s) * HG + head) * 2 + 1];
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    acc[4 * v + 0] = fmaf(sg, kv[j][v].x, acc[4 * v + 0]);
+                    acc[4 * v + 1] = fmaf(sg, kv[j][v].y, acc[4 * v + 1]);
+                    acc[4 * v + 2] = fmaf(sg, kv[j][v].z, acc[4 * v + 2]);
+                    acc[4 * v + 3] = fmaf(sg, kv[j][v].w, acc[4 * v + 3]);
+                }
             }
         }
     }

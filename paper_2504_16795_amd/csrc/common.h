@@ -73,7 +73,8 @@ constexpr int kDppMirror = 0x140;       // lane i <- lane 15 - i within each 16 
 
 template <int CTRL>
 __device__ __forceinline__ int dpp_mov(int v) {
-    return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+    // every control used here reads a lane of the same row, so no lane is out of bounds
+    return __builtin_amdgcn_mov_dpp(v, CTRL, 0xF, 0xF, true);
 }
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {

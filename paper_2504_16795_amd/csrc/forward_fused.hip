@@ -35,11 +35,10 @@ constexpr int KMAX = 32;
 constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
 constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
 constexpr int kOStores = 2;         // global stores per lane of one output step (16 B each)
-constexpr size_t kOTrashBytes = HG * D * 2;
 constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
 
 struct FwdWs {
-    size_t bitmap, cnt, gstart, plan, part, trash, end;
+    size_t bitmap, cnt, gstart, plan, part, end;
 };
 __host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
     FwdWs l;
@@ -51,8 +50,7 @@ __host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
     l.gstart = l.cnt + align256(R * 4);
     l.plan = l.gstart + align256((R + 1) * 4);
     l.part = l.plan + 256;
-    l.trash = l.part + align256(nsel * HG * D * 2);
-    l.end = l.trash + kOTrashBytes;
+    l.end = l.part + align256((nsel + 1) * HG * D * 2);       // + the spare block
     return l;
 }
 
@@ -73,8 +71,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     Dims dm, const __bf16* __restrict__ Q, const __bf16* __restrict__ K,
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const uint32_t* __restrict__ bm, int nwords, const int* __restrict__ gstart,
-    const int* __restrict__ cntr, const int* __restrict__ plan, uint16_t* __restrict__ part,
-    char* __restrict__ trash) {
+    const int* __restrict__ cntr, const int* __restrict__ plan, uint16_t* __restrict__ part) {
     __shared__ SmemO sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
@@ -98,7 +95,10 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
     int zb[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) zb[rt] = zpos(4 * grp + (row >> 2), 4 * rt + (row & 3));
-    uint16_t* const tpart = reinterpret_cast<uint16_t*>(trash);
+    // a lane's partial-store address is pbase + 2 KB * block, block = the (token, slot) or,
+    // for rows of missing tokens, tblk: the spare block after the partials
+    char* const pbase = reinterpret_cast<char*>(part) + 2 * ((row & 7) * D + 32 * wave + 8 * grp);
+    const uint32_t tblk = (uint32_t)((size_t)dm.B * dm.L * dm.G * dm.k);
 
     for (int r = find_row(gstart, R, g0); r < R; ++r) {
         const int rs = gstart[r], re = gstart[r + 1];
@@ -148,7 +148,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
 
         // output partial of group gj from the staged (W P)^T (all waves' keys): rows
         // 16 rt + (lane & 15), d = 32 wave + 8 grp + (0..7) (tile dt holds 4 dt + (0..3));
-        // exactly kOStores stores per lane (rows of missing tokens go to the trash area)
+        // exactly kOStores stores per lane (rows of missing tokens go to the spare block)
         auto o_step = [&](int gj, int nl) __attribute__((always_inline)) {
             f32x4_t oa[2][2];
 #pragma unroll
@@ -166,9 +166,9 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
                 const int so = li < nl ? sm.lsel[li] : -1;
-                uint16_t* dst = (so >= 0 ? part + ((size_t)(uint32_t)so << 10) : tpart) +
-                                (row & 7) * D + 32 * wave + 8 * grp;
-                *reinterpret_cast<u32x4_t*>(dst) = bfp_pack8(oa[0][rt], oa[1][rt]);
+                const uint32_t blk = so >= 0 ? (uint32_t)so : tblk;
+                *reinterpret_cast<u32x4_t*>(pbase + ((size_t)blk << 11)) =
+                    bfp_pack8(oa[0][rt], oa[1][rt]);
             }
         };
 
@@ -326,26 +326,26 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
     float acc[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+    // slot values are wave-uniform (lane reads), so the branches below are scalar
     for (int s0 = 0; s0 < k; s0 += 4) {
         u32x4_t pv[4][2];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
-            const int use = s < k ? __builtin_amdgcn_readlane(own, s) : 0;
-            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
-#pragma unroll
-            for (int v = 0; v < 2; ++v)
-                pv[j][v] = use ? *reinterpret_cast<const u32x4_t*>(pp + 8 * v) : u32x4_t{0u, 0u, 0u, 0u};
+            if (s < k && __builtin_amdgcn_readlane(own, s)) {
+                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
+            }
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                float x[8];
-                bfp_unpack8(pv[j][v], x);
-#pragma unroll
-                for (int i = 0; i < 8; ++i) acc[8 * v + i] += x[i];
+        for (int j = 0; j < 4; ++j) {
+            const int s = s0 + j;
+            if (s < k && __builtin_amdgcn_readlane(own, s)) {
+                bfp_accum8(pv[j][0], acc);
+                bfp_accum8(pv[j][1], acc + 8);
             }
+        }
     }
     bf16x8_t o0, o1;
 #pragma unroll
@@ -404,7 +404,7 @@ hipError_t launch_forward_chunk(const Dims& dm, const void* Q, const void* K, co
         hipLaunchKernelGGL(fwd_chunk_mfma, dim3(kFwdWGs), dim3(NT), 0, st, dm,
                            (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
                            (const uint32_t*)bmp, nwords, (const int*)gstart, (const int*)cnt,
-                           (const int*)plan, part, wsb + l.trash);
+                           (const int*)plan, part);
     }
     e = hipGetLastError();
     if (e != hipSuccess) return e;

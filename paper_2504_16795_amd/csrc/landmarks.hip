@@ -11,6 +11,7 @@ namespace hsa {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kLoads = 8;         // row loads a thread keeps in flight
 
 template <typename T> struct Vec;
 template <> struct Vec<float> { static constexpr int n = 4; using raw = float4; };
@@ -50,13 +51,26 @@ __global__ __launch_bounds__(kThreads) void landmarks_kernel(Dims dm, const Tin*
 #pragma unroll
         for (int i = 0; i < VN; ++i) acc[i] = 0.f;
         if (r < R && v < nvec) {
-            for (int s = r; s < dm.S; s += R) {
-                const auto raw = *reinterpret_cast<const typename Vec<Tin>::raw*>(
-                    base + (size_t)s * row + (size_t)v * VN);
-                float x[VN];
-                unpack(raw, x);
+            // rows r, r + R, ... in order; the loads of up to kLoads rows are issued before
+            // any is added, so a thread has them in flight together
+            for (int s0 = r; s0 < dm.S; s0 += kLoads * R) {
+                typename Vec<Tin>::raw raw[kLoads];
 #pragma unroll
-                for (int i = 0; i < VN; ++i) acc[i] += x[i];
+                for (int u = 0; u < kLoads; ++u) {
+                    const int s = s0 + u * R;
+                    if (s < dm.S)
+                        raw[u] = *reinterpret_cast<const typename Vec<Tin>::raw*>(
+                            base + (size_t)s * row + (size_t)v * VN);
+                }
+#pragma unroll
+                for (int u = 0; u < kLoads; ++u) {
+                    if (s0 + u * R < dm.S) {
+                        float x[VN];
+                        unpack(raw[u], x);
+#pragma unroll
+                        for (int i = 0; i < VN; ++i) acc[i] += x[i];
+                    }
+                }
             }
         }
 #pragma unroll

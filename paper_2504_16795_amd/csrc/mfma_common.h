@@ -78,47 +78,64 @@ __device__ __forceinline__ int tpos(int d, int s, int n) { return (s + 8 * (d >>
 // mantissa bits, for products whose fp32 result cancels or accumulates many terms.
 __device__ __forceinline__ void split8(const f32x4_t& a, const f32x4_t& b, bf16x8_t& hi,
                                        bf16x8_t& lo) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const float v = (i < 4) ? a[i] : b[i - 4];
-        hi[i] = f2bf(v);
-        lo[i] = f2bf(v - (float)hi[i]);
+    for (int j = 0; j < 4; ++j) {
+        const float x0 = j < 2 ? a[2 * j] : b[2 * j - 4];
+        const float x1 = j < 2 ? a[2 * j + 1] : b[2 * j - 3];
+        // one conversion of the pair; its two halves read back as floats
+        const bf16x2_t hp = bf16x2_t{f2bf(x0), f2bf(x1)};
+        uint32_t u;
+        __builtin_memcpy(&u, &hp, 4);
+        hi[2 * j] = hp[0];
+        hi[2 * j + 1] = hp[1];
+        lo[2 * j] = f2bf(x0 - __uint_as_float(u << 16));
+        lo[2 * j + 1] = f2bf(x1 - __uint_as_float(u & 0xFFFF0000u));
     }
 }
 
 // Per-(token, slot) partial outputs are stored as blocks of 8 values in 16 bytes (block
-// floating point): one power-of-two scale per block and a 13-bit signed integer per value.
-// With E the biased exponent of the block's largest magnitude (at least 14), the value x
-// is stored as q = round(x 2^(139 - E)), |q| < 2^13, in the 16-bit field (q << 1) | bit i of
-// E (field i carries bit i of E).  The error is at most 2^-13 of the block's largest
-// magnitude (bf16 storage: up to 2^-8 of each value's own), in the bytes of bf16.
+// floating point): one power-of-two scale per block and a 16-bit signed integer per value.
+// With E the biased exponent of the block's largest magnitude (at least 14), every value is
+// below 2^(E - 126) in magnitude; x 2^(126 - E) is converted to a normalised 16-bit integer
+// (q = x 2^(126 - E) 32767, rounded, by v_cvt_pknorm_i16_f32), and the low bit of field i is
+// replaced by bit i of E.  The decoded value is field 2^(E - 126) / 32767: the conversion
+// and the replaced bit are off by at most 2 units of 2^(E - 126) / 32767, i.e. at most 2^-13
+// of the block's largest magnitude (bf16 storage: up to 2^-8 of each value's own), in the
+// bytes of bf16.
 __device__ __forceinline__ u32x4_t bfp_pack8(const f32x4_t& a, const f32x4_t& b) {
-    const float m = fmaxf(fmaxf(fmaxf(fabsf(a[0]), fabsf(a[1])), fmaxf(fabsf(a[2]), fabsf(a[3]))),
-                          fmaxf(fmaxf(fabsf(b[0]), fabsf(b[1])), fmaxf(fabsf(b[2]), fabsf(b[3]))));
+    float m = fmaxf(fmaxf(fabsf(a[0]), fabsf(a[1])), fabsf(a[2]));
+    m = fmaxf(fmaxf(m, fabsf(a[3])), fabsf(b[0]));
+    m = fmaxf(fmaxf(m, fabsf(b[1])), fabsf(b[2]));
+    m = fmaxf(m, fabsf(b[3]));
     const uint32_t e = max((__float_as_uint(m) >> 23) & 0xFFu, 14u);
-    const float sc = __uint_as_float((266u - e) << 23);        // 2^(139 - e)
-    uint32_t f[8];
+    const float s = __uint_as_float((253u - e) << 23);          // 2^(126 - e)
+    const auto p0 = __builtin_amdgcn_cvt_pknorm_i16(a[0] * s, a[1] * s);
+    const auto p1 = __builtin_amdgcn_cvt_pknorm_i16(a[2] * s, a[3] * s);
+    const auto p2 = __builtin_amdgcn_cvt_pknorm_i16(b[0] * s, b[1] * s);
+    const auto p3 = __builtin_amdgcn_cvt_pknorm_i16(b[2] * s, b[3] * s);
+    uint32_t w[4];
+    __builtin_memcpy(&w[0], &p0, 4);
+    __builtin_memcpy(&w[1], &p1, 4);
+    __builtin_memcpy(&w[2], &p2, 4);
+    __builtin_memcpy(&w[3], &p3, 4);
+    // bit 2j of E to field 2j (bit 0 of word j), bit 2j + 1 to field 2j + 1 (bit 16)
+    const uint32_t t = e | (e << 15);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const float x = i < 4 ? a[i] : b[i - 4];
-        // round to the nearest integer: |x sc| < 2^13, so x sc + 1.5 2^23 keeps it in the
-        // low mantissa bits
-        const int q = __float_as_int(fmaf(x, sc, 12582912.f)) - 0x4B400000;
-        f[i] = (((uint32_t)q << 1) | ((e >> i) & 1u)) & 0xFFFFu;
-    }
-    return u32x4_t{f[0] | (f[1] << 16), f[2] | (f[3] << 16), f[4] | (f[5] << 16),
-                   f[6] | (f[7] << 16)};
+    for (int j = 0; j < 4; ++j) w[j] = (w[j] & 0xFFFEFFFEu) | ((t >> (2 * j)) & 0x00010001u);
+    return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
-__device__ __forceinline__ void bfp_unpack8(const u32x4_t& v, float x[8]) {
-    uint32_t e = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) e |= ((v[j] & 1u) << (2 * j)) | (((v[j] >> 16) & 1u) << (2 * j + 1));
-    const float inv = __uint_as_float((e - 12u) << 23);         // 2^(e - 139)
+// Adds the 8 values of a block to acc[0..7] (field i to acc[i]).
+__device__ __forceinline__ void bfp_accum8(const u32x4_t& v, float acc[8]) {
+    const uint32_t x = (v[0] & 0x00010001u) | ((v[1] & 0x00010001u) << 2) |
+                       ((v[2] & 0x00010001u) << 4) | ((v[3] & 0x00010001u) << 6);
+    const uint32_t e = (x | (x >> 15)) & 0xFFu;
+    const float sc = __uint_as_float((e + 1u) << 23) * (1.0f / 32767.0f);   // 2^(e - 126) / 32767
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        x[2 * j] = (float)(((int32_t)(v[j] << 16)) >> 17) * inv;
-        x[2 * j + 1] = (float)(((int32_t)v[j]) >> 17) * inv;
+        acc[2 * j] = fmaf((float)(int16_t)(v[j] & 0xFFFFu), sc, acc[2 * j]);
+        acc[2 * j + 1] = fmaf((float)((int32_t)v[j] >> 16), sc, acc[2 * j + 1]);
     }
 }
 
@@ -128,6 +145,12 @@ __device__ __forceinline__ void bfp_unpack8(const u32x4_t& v, float x[8]) {
 // MFMAs wait for the in-order load counter to drain, i.e. for the next chunk's prefetch.
 // (s_waitcnt immediate: vmcnt 0, expcnt and lgkmcnt at their no-wait maxima.)
 __device__ __forceinline__ void wait_global_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// A compile-time integer as a value (selects a constant stage of a ring in unrolled loops).
+template <int N>
+struct IntC {
+    static constexpr int value = N;
+};
 
 // Logical workgroup id with an XCD-aware order: hardware dispatches consecutive ids to the
 // 8 XCDs round-robin, so consecutive logical ids (same (b, g), neighbouring tiles, sharing
