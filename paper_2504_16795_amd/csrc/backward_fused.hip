@@ -337,16 +337,18 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                     }
                 // ---- the wave's row statistics over its 16 keys, to LDS ------------------------
                 f32x4_t e[2];
+                float zl8[8], e8[8], m8[8];
+    #pragma unroll
+                for (int i = 0; i < 8; ++i) zl8[i] = z[i >> 2][i & 3] * sl2;
+                rows16_exp(zl8, e8, m8);
     #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) {
                     f32x4_t sm_m, sm_l, sm_n;
     #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const float zl = z[rb][i] * sl2;
-                        const float m = row16_max(zl);
-                        const float ev = fast_exp2(zl - m);
+                        const float ev = e8[4 * rb + i];
                         e[rb][i] = ev;
-                        sm_m[i] = m;
+                        sm_m[i] = m8[4 * rb + i];
                         sm_l[i] = group_sum<16>(ev);
                         sm_n[i] = group_sum<16>(ev * dp[rb][i]);
                     }

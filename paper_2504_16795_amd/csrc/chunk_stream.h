@@ -54,6 +54,31 @@ __device__ __forceinline__ void rows16_max(float (&x)[N]) {
 #pragma unroll
     for (int i = 0; i < N; ++i) x[i] = __int_as_float(v[i] ^ ((v[i] >> 31) & 0x7fffffff));
 }
+// Softmax exponentials of N row values per lane (rows of 16 lanes, the wave's keys along the
+// row): e = 2^(x - m) with m a reference per row, and m.  Any finite reference gives the same
+// softmax once the combine rescales by 2^(m - max); the reference is the row's value at its
+// first lane (one DPP broadcast) unless some exponential of the wave would exceed 2^64, in
+// which case (a logit spread of more than 64 in log2 units around that key) the rows take
+// their maxima.  Either way no exponential overflows and the row's largest is at least 1.
+template <int N>
+__device__ __forceinline__ void rows16_exp(const float (&x)[N], float (&e)[N], float (&m)[N]) {
+    float emax = 0.f;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        // row_newbcast:0: lane 16 r of each row of 16 lanes to the whole row
+        m[i] = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x[i]), 0x150, 0xF, 0xF, true));
+        e[i] = fast_exp2(x[i] - m[i]);
+        emax = fmaxf(emax, e[i]);
+    }
+    if (__builtin_amdgcn_ballot_w64(!(emax <= 0x1p64f))) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) m[i] = x[i];
+        rows16_max(m);
+#pragma unroll
+        for (int i = 0; i < N; ++i) e[i] = fast_exp2(x[i] - m[i]);
+    }
+}
+
 template <int N>
 __device__ __forceinline__ void rows16_sum(float (&x)[N]) {
 #pragma unroll

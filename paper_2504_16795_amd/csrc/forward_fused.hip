@@ -132,8 +132,7 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                 vT[dt][ks2] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
             }
 
-        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
-            __bf16* st = sm.st[gi % ONST];
+        auto issue = [&](int gi, int nl, __bf16* st) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < OBPW; ++i) {
                 const int blk = wave * OBPW + i;
@@ -212,8 +211,11 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
             const int ngroups = (nl + 3) / 4;
 #pragma unroll
             for (int u = 0; u < ONST - 1; ++u)
-                if (u < ngroups) issue(u, nl);
-            for (int gi = 0; gi < ngroups; ++gi) {
+                if (u < ngroups) issue(u, nl, sm.st[u]);
+            // one group's step; its stage index SI = gi % ONST is a constant (the loop below
+            // is unrolled by ONST), so the stage's LDS addresses are lane bases plus immediates
+            auto group = [&](int gi, auto si) __attribute__((always_inline)) {
+                constexpr int SI = decltype(si)::value;
                 // Group gi has landed once only the memory operations issued after its copies
                 // remain: the previous iteration's output stores (when it ran one) and the
                 // next group's copies (when there is a next group).  Loads and stores complete
@@ -226,8 +228,8 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                 lds_wait();
                 barrier_keep_copies();   // stage gi landed, (W P)^T of gi - 1 complete
                 if (gi > 0) o_step(gi - 1, nl);
-                if (gi + ONST - 1 < ngroups) issue(gi + ONST - 1, nl);
-                const __bf16* st = sm.st[gi % ONST];
+                if (gi + ONST - 1 < ngroups) issue(gi + ONST - 1, nl, sm.st[(SI + ONST - 1) % ONST]);
+                const __bf16* st = sm.st[SI];
 
                 // ---- Z for the wave's 16 keys (rows 16 rb + 4 grp + i, key 16 wave + row) --
                 f32x4_t z[2];
@@ -241,10 +243,10 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                 // (rows 16 rb + 4 grp + i at index 4 rb + i)
                 float zl[8], mx[8], ls[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) mx[i] = zl[i] = z[i >> 2][i & 3] * sl2;
-                rows16_max(mx);
+                for (int i = 0; i < 8; ++i) zl[i] = z[i >> 2][i & 3] * sl2;
+                rows16_exp(zl, ls, mx);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) ls[i] = zl[i] = fast_exp2(zl[i] - mx[i]);
+                for (int i = 0; i < 8; ++i) zl[i] = ls[i];
                 rows16_sum(ls);
                 f32x4_t e[2];
 #pragma unroll
@@ -291,6 +293,12 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                         bf16x4_t{f2bf(wt * e[rb][0] * fv[0]), f2bf(wt * e[rb][1] * fv[1]),
                                  f2bf(wt * e[rb][2] * fv[2]), f2bf(wt * e[rb][3] * fv[3])};
                 }
+            };
+            static_assert(ONST == 3, "the group loop is unrolled by the ring depth");
+            for (int gb = 0; gb < ngroups; gb += ONST) {
+                group(gb, IntC<0>{});
+                if (gb + 1 < ngroups) group(gb + 1, IntC<1>{});
+                if (gb + 2 < ngroups) group(gb + 2, IntC<2>{});
             }
             lds_wait();
             barrier_keep_copies();   // (W P)^T of the batch's last group complete
