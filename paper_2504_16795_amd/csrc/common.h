@@ -170,6 +170,34 @@ __device__ __forceinline__ float key_score(uint64_t key) {
 }
 __device__ __forceinline__ uint64_t max_u64(uint64_t a, uint64_t b) { return b > a ? b : a; }
 
+// Wave-wide maximum of an unsigned 32-bit value (DPP inside rows, then the lane swaps).
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+    x = max(x, (uint32_t)dpp_mov<kDppXor1>((int)x));
+    x = max(x, (uint32_t)dpp_mov<kDppXor2>((int)x));
+    x = max(x, (uint32_t)dpp_mov<kDppHalfMirror>((int)x));
+    x = max(x, (uint32_t)dpp_mov<kDppMirror>((int)x));
+    int a, b;
+    lane_swap<false>(a, b, (int)x);
+    x = max((uint32_t)a, (uint32_t)b);
+    lane_swap<true>(a, b, (int)x);
+    return max((uint32_t)a, (uint32_t)b);
+}
+
+// The maximum of wave_max_key, found on the upper word first (one 32-bit wave maximum) and
+// on the lower word only when several lanes share that upper word.  Every lane of the wave
+// must be active.
+__device__ __forceinline__ uint64_t wave_max_key_hi(uint64_t x) {
+    const uint32_t hi = (uint32_t)(x >> 32);
+    const uint32_t bh = wave_max_u32(hi);
+    const uint64_t tied = __builtin_amdgcn_ballot_w64(hi == bh);
+    uint32_t bl;
+    if (__builtin_popcountll(tied) == 1)
+        bl = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)x, __builtin_ctzll(tied));
+    else
+        bl = wave_max_u32(hi == bh ? (uint32_t)x : 0u);
+    return ((uint64_t)bh << 32) | bl;
+}
+
 // Wave-wide maximum of a 64-bit key, branch-free (DPP moves inside rows, then the lane
 // swaps across rows); every lane ends with the maximum.
 __device__ __forceinline__ uint64_t wave_max_key(uint64_t x) {

@@ -216,28 +216,41 @@ __global__ __launch_bounds__(kScanThreads, 2) void decode_scan(
         scan_scores_valu<Tq, Tk, D>(dm, q, Kbar, b, c0, nch, qs, sc);
     }
     __syncthreads();
-    // top-k of the slice for each group: k rounds of a wave-wide maximum of order keys
+    // top-k of the slice for each group: each lane sorts its SL / 64 order keys (descending);
+    // round i takes the wave-wide maximum of the lanes' first keys and the lane holding it
+    // drops its first key.
+    static_assert(SL == 256, "four keys per lane");
     for (int g = wave; g < G; g += kScanThreads / 64) {
-        uint64_t key[SL / 64];
+        uint64_t key[4];
 #pragma unroll
-        for (int m = 0; m < SL / 64; ++m) {
+        for (int m = 0; m < 4; ++m) {
             const int cl = lane + 64 * m;
             key[m] = (cl < nch) ? order_key(sc[cl * G + g], c0 + cl) : 0;
         }
+        auto cx = [](uint64_t& x, uint64_t& y) __attribute__((always_inline)) {
+            const uint64_t hi = max_u64(x, y), lo = x ^ y ^ hi;
+            x = hi;
+            y = lo;
+        };
+        cx(key[0], key[1]);
+        cx(key[2], key[3]);
+        cx(key[0], key[2]);
+        cx(key[1], key[3]);
+        cx(key[1], key[2]);
         float* os = cand_s + (((size_t)b * G + g) * nslices + slice) * k;
         int32_t* oc = cand_c + (((size_t)b * G + g) * nslices + slice) * k;
         for (int i = 0; i < k; ++i) {
-            uint64_t best = 0;
-#pragma unroll
-            for (int m = 0; m < SL / 64; ++m) best = max_u64(best, key[m]);
-            best = wave_max_key(best);
+            const uint64_t best = wave_max_key_hi(key[0]);
             if (lane == 0) {
                 os[i] = best ? key_score(best) : -INFINITY;
                 oc[i] = best ? key_chunk(best) : -1;
             }
-#pragma unroll
-            for (int m = 0; m < SL / 64; ++m)
-                if (key[m] == best) key[m] = 0;
+            if (key[0] == best && best != 0) {
+                key[0] = key[1];
+                key[1] = key[2];
+                key[2] = key[3];
+                key[3] = 0;
+            }
         }
     }
 }
@@ -406,7 +419,7 @@ __device__ __forceinline__ void merge_lists(const float* __restrict__ cs,
     for (int i = 0; i < KC; ++i) key[i] = c[i] >= 0 ? order_key(s[i], c[i]) : 0;
     uint64_t mine = 0;                   // lane r receives the r-th best
     for (int r = 0; r < n; ++r) {
-        const uint64_t best = wave_max_key(key[0]);
+        const uint64_t best = wave_max_key_hi(key[0]);
         if (lane == r) mine = best;
         if (best != 0 && key[0] == best) {
 #pragma unroll
