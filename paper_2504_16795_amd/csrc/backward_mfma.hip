@@ -18,7 +18,7 @@
 // and D, plus ds per (token, slot).
 //
 // Key pass: chunk-major, reading those statistics (see bwd_kv_mfma below).
-#include "chunk_lds.h"
+#include "chunk_stream.h"
 #include "tile_sel.h"
 
 namespace hsa {
@@ -34,21 +34,30 @@ constexpr int HG = 8;
 constexpr int KMAX = 32;
 constexpr int UWORDS = 1024;     // union bitmap words: up to 32768 candidate chunks
 
-__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // workspace layout shared by both passes (ds and the bitmap first, as in the generic path)
+// (the key pass's even split: tokens per (b, g, chunk) row, the group prefix, the plan, and
+// two fp32 partial dK / dV tiles per workgroup for the rows it shares)
+constexpr int kKvWGs = 512;      // workgroups of the key pass: two per CU
+
 struct WsLayout {
-    size_t ds, bitmap, lse, dd, end;
+    size_t ds, bitmap, lse, dd, cnt, gstart, plan, pk, pv, end;
 };
 __host__ __device__ inline WsLayout ws_layout(const Dims& dm) {
     WsLayout l;
     const size_t nsel = (size_t)dm.B * dm.L * dm.G * dm.k;
     const size_t nwords = (size_t)((dm.L + 31) / 32);
+    const size_t R = (size_t)dm.B * dm.G * dm.C;
     l.ds = 0;
     l.bitmap = align256(nsel * 4);
-    l.lse = l.bitmap + align256((size_t)dm.B * dm.G * dm.C * nwords * 4);
+    l.lse = l.bitmap + align256(R * nwords * 4);
     l.dd = l.lse + align256(nsel * dm.h * 4);
-    l.end = l.dd + align256(nsel * dm.h * 4);
+    l.cnt = l.dd + align256(nsel * dm.h * 4);
+    l.gstart = l.cnt + align256(R * 4);
+    l.plan = l.gstart + align256((R + 1) * 4);
+    l.pk = l.plan + 256;
+    l.pv = l.pk + (size_t)kKvWGs * 2 * dm.S * D * 4;
+    l.end = l.pv + (size_t)kKvWGs * 2 * dm.S * D * 4;
     return l;
 }
 
@@ -304,10 +313,13 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
 }
 
 // ----------------------------------------------------------------------------------------
-// Key pass (bwd_kv_mfma): workgroup = (b, g, chunk c); wave w owns keys 16w..16w+15 and
-// keeps K_sub, V_sub as B operands in registers and dK_sub, dV_sub [16 x 128] as fp32
-// accumulators.  The tokens that selected c are read from the selection bitmap in
-// increasing order, four at a time (32 rows = 4 tokens x 8 heads):
+// Key pass (bwd_kv_mfma): chunk-major over an even split of the work.  The selecting tokens
+// of each (b, g, chunk) row come from the selection bitmap in increasing order, in groups of
+// four (32 rows = 4 tokens x 8 heads); the groups of all rows are laid end to end and split
+// into kKvWGs equal ranges (stream_rowcount / stream_plan), so a chunk selected by thousands
+// of tokens is shared by several workgroups instead of setting the kernel time.  Wave w owns
+// keys 16w..16w+15 of the current chunk and keeps K_sub, V_sub as B operands in registers
+// and dK_sub, dV_sub [16 x 128] as fp32 accumulators.  Per group:
 //     Z  [32 x 16] = Q_rows K_sub^T,   dP = dO_rows V_sub^T          (MFMA)
 //     P  = exp(beta Z - lse_row),  dZ = w P (dP - D_row)            (stored by the query pass)
 //     dV_sub += (w P)^T dO_rows,  dK_sub += dZ^T Q_rows              (MFMA, K = 32 rows;
@@ -316,8 +328,10 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
 // (chunk_lds.h), two groups in flight while one is computed.  Z and dP read the rows; the
 // last two products read them transposed, in the row order of the C layout of Z, which
 // then serves as their A operand directly.  The landmark term dKbar_c / S =
-// (alpha / S) sum ds q~ is folded into dZ.  No atomics; fixed token order.
-constexpr int LISTCAP = 64 * 32 + 4;
+// (alpha / S) sum ds q~ is folded into dZ.  A workgroup that covers a row whole writes its
+// dK, dV; for a shared row (the first or last of its range) it writes fp32 partials, which
+// bwd_kv_finish adds in workgroup order.  No atomics; fixed token order.
+constexpr int LISTCAP = 2048;    // tokens listed at once (a multiple of 4)
 constexpr int KV_NST = 3;
 
 struct KvStage {
@@ -331,7 +345,7 @@ struct SmemKV {
     int list[LISTCAP];
     float lw[LISTCAP], lds[LISTCAP];
     uint8_t lslot[LISTCAP];
-    int nlist;
+    int wtot[16];
 };
 
 template <int S>
@@ -340,50 +354,25 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
     const __bf16* __restrict__ V, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const __bf16* __restrict__ dO, const float* __restrict__ ds, const float* __restrict__ lse,
     const float* __restrict__ dd, const uint32_t* __restrict__ bm, int nwords,
-    __bf16* __restrict__ dK, __bf16* __restrict__ dV) {
-    constexpr int NW = S / 16;              // waves
-    constexpr int NT = NW * 64;
-    constexpr int BPW = 8 / NW;             // 1 KB row blocks of Q (and of dO) per wave
+    const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
+    float* __restrict__ pk, float* __restrict__ pv, __bf16* __restrict__ dK,
+    __bf16* __restrict__ dV) {
+    constexpr int NWK = S / 16;             // waves
+    constexpr int NTK = NWK * 64;
+    constexpr int BPW = 8 / NWK;            // 1 KB row blocks of Q (and of dO) per wave
     __shared__ SmemKV sm;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
-    // With at least 8 (b, g) slices, the chunks of one slice run together on one XCD, so
-    // the Q / dO rows of a token, read once per chunk it selected, are shared through that
-    // XCD's L2.  With fewer slices, whole-slice ranges would leave the XCDs unevenly loaded
-    // (early chunks have more candidate tokens), so chunks stay interleaved over the XCDs.
-    const int nlog = dm.Call * dm.B * dm.G;
-    const int lid = (dm.B * dm.G >= 8) ? xcd_logical_id(nlog)
-                                        : ((int)blockIdx.x < nlog ? (int)blockIdx.x : -1);
+    // consecutive ranges (the chunks of one slice) run on one XCD, so a token's Q / dO rows,
+    // read once per chunk it selected, are shared through that XCD's L2
+    const int lid = xcd_logical_id(kKvWGs);
     if (lid < 0) return;
-    const int c = lid % dm.Call;
-    const int bg = lid / dm.Call, b = bg / dm.G, g = bg % dm.G;
+    const int R = dm.B * dm.G * dm.C;
+    const int total = plan[0], T = plan[1];
+    const int g0 = lid * T, g1 = min(g0 + T, total);
+    if (g0 >= g1) return;
     const int k = dm.k;
     const size_t rowstride = (size_t)dm.G * D;
-    const size_t cbase = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
-
-    if (c >= dm.C) {   // trailing partial chunk: never selected
-        const int rows = dm.L - c * S;
-        for (int i = tid; i < rows * D; i += NT) {
-            const size_t o = cbase + (size_t)(i / D) * rowstride + i % D;
-            dK[o] = __bf16(0.f);
-            dV[o] = __bf16(0.f);
-        }
-        return;
-    }
-
-    // B operands of the wave's 16 keys: K_sub^T[d][key], V_sub^T[d][key]
-    bf16x8_t kB[4], vB[4];
-    const int key = 16 * wave + row;
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-        kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
-        vB[ks] = ld_bf16x8(V + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
-    }
-    wait_global_loads();
-    f32x4_t aK[8], aV[8];
-#pragma unroll
-    for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
-    if (tid == 0) sm.nlist = 0;
     const float beta = dm.beta;
     const float l2e = 1.44269504088896341f;
     const float lmk = dm.alpha / (beta * (float)S);
@@ -391,161 +380,212 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
     row_read_offsets(lane, koff);
     tr_read_offsets(lane, toff);
 
-    // copies of group gi (tokens 4 gi .. 4 gi + 3 of the list; a missing token repeats the
-    // group's first one, with weight and ds 0): wave w copies the Q and dO row blocks
-    // w BPW .. w BPW + BPW - 1 (4 rows = half a token each); the last wave also copies the
-    // lse and D of the 32 rows
-    auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
-        KvStage& st = sm.st[gi % KV_NST];
-#pragma unroll
-        for (int i = 0; i < BPW; ++i) {
-            const int blk = wave * BPW + i;
-            const int r = blk * 4 + (lane >> 4);
-            int li = gi * 4 + (r >> 3);
-            if (li >= nl) li = gi * 4;
-            const size_t o = (((size_t)b * dm.L + sm.list[li]) * dm.H + (size_t)g * HG + (r & 7)) * D +
-                             unit_pos(r, lane & 15) * 8;
-            lds_copy16(Q + o, __builtin_amdgcn_readfirstlane(lds_address(st.q + blk * 512)));
-            lds_copy16(dO + o, __builtin_amdgcn_readfirstlane(lds_address(st.g + blk * 512)));
-        }
-        if (wave == NW - 1) {
-            // lanes 16 m + 2 j + h (j < 4 tokens, h halves of the 8 heads): m = 0 lse, m = 1 D,
-            // m >= 2 repeat (scratch)
-            int li = gi * 4 + ((lane & 7) >> 1);
-            if (li >= nl) li = gi * 4;
-            const size_t so =
-                ((((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li]) * HG +
-                4 * (lane & 1);
-            lds_copy16(((lane >> 3) & 1 ? dd : lse) + so,
-                       __builtin_amdgcn_readfirstlane(lds_address(st.meta)));
-        }
-    };
+    for (int r = find_row(gstart, R, g0); r < R; ++r) {
+        const int rs = gstart[r], re = gstart[r + 1];
+        if (rs >= g1) break;
+        if (re == rs) continue;
+        const Segment sg = segment_of(rs, re, g0, g1);
+        const int c = r % dm.C;
+        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
+        const size_t cbase = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
+        const int ntok = cntr[r];
 
-    const uint32_t* bmrow = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
-    const int wbeg = ((c + 1) * S) >> 5;
-    bool last_round = wbeg >= nwords;
-    for (int wb = wbeg; ; wb += 64) {
-        __syncthreads();
-        if (!last_round && wave == 0) {
-            const int wi = wb + lane;
-            const uint32_t word = wi < nwords ? bmrow[wi] : 0u;
-            const int cnt = __popc(word);
-            int incl = cnt;
+        __syncthreads();                  // the previous row's stages and lists are read
+        // B operands of the wave's 16 keys: K_sub^T[d][key], V_sub^T[d][key]
+        bf16x8_t kB[4], vB[4];
+        const int key = 16 * wave + row;
 #pragma unroll
-            for (int o = 1; o < 64; o <<= 1) {
-                const int v = __shfl_up(incl, o, 64);
-                if (lane >= o) incl += v;
-            }
-            const int n0 = sm.nlist;
-            int pos = n0 + incl - cnt;
-            uint32_t x = word;
-            while (x) {
-                sm.lslot[pos] = 0;
-                sm.list[pos++] = wi * 32 + (__ffs(x) - 1);
-                x &= x - 1;
-            }
-            const int tot = __shfl(incl, 63, 64);
-            if (lane == 0) sm.nlist = n0 + tot;
+        for (int ks = 0; ks < 4; ++ks) {
+            kB[ks] = ld_bf16x8(K + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
+            vB[ks] = ld_bf16x8(V + cbase + (size_t)key * rowstride + 32 * ks + 8 * grp);
         }
-        if (!last_round) last_round = wb + 64 >= nwords;
-        __syncthreads();
-        const int nl = sm.nlist;
-        // per-token slot, weight and ds of the batch.  Threads take consecutive (token,
-        // slot) entries, so every idx load is independent of the others and coalesced; the
-        // slot holding c (a token's valid entries are distinct, so one matches) is noted,
-        // then each token's w and ds are loaded.
-        for (int e = tid; e < nl * k; e += NT) {
-            const int li = e / k, s2 = e - li * k;
-            const size_t so = (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k;
-            if (idx[so + s2] == c) sm.lslot[li] = (uint8_t)s2;
-        }
-        __syncthreads();
-        for (int li = tid; li < nl; li += NT) {
-            const size_t so = (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li];
-            sm.lw[li] = w[so];
-            sm.lds[li] = ds[so];
-        }
-        __syncthreads();
-        const int ngroups = last_round ? (nl + 3) / 4 : nl / 4;
+        wait_global_loads();
+        f32x4_t aK[8], aV[8];
 #pragma unroll
-        for (int u = 0; u < KV_NST - 1; ++u)
-            if (u < ngroups) issue(u, nl);
-        for (int gi = 0; gi < ngroups; ++gi) {
-            // group gi has landed once at most the next group's copies remain
-            if (gi + 1 < ngroups) {
-                if (wave == NW - 1) wait_loads_le<2 * BPW + 1>();
-                else wait_loads_le<2 * BPW>();
-            } else {
-                wait_loads_le<0>();
-            }
-            barrier_keep_copies();            // ... for every wave; stage (gi - 1) % NST free
-            if (gi + KV_NST - 1 < ngroups) issue(gi + KV_NST - 1, nl);
-            const KvStage& st = sm.st[gi % KV_NST];
+        for (int db = 0; db < 8; ++db) aK[db] = aV[db] = zero4();
 
-            // ---- Z, dP for the wave's 16 keys ---------------------------------------------
-            f32x4_t z[2], dp[2];
-            z[0] = z[1] = dp[0] = dp[1] = zero4();
+        // copies of group gi (tokens 4 gi .. 4 gi + 3 of the list; a missing token repeats
+        // the group's first one, with weight and ds 0): wave w copies the Q and dO row blocks
+        // w BPW .. w BPW + BPW - 1 (4 rows = half a token each); the last wave also copies
+        // the lse and D of the 32 rows
+        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
+            KvStage& st = sm.st[gi % KV_NST];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
+            for (int i = 0; i < BPW; ++i) {
+                const int blk = wave * BPW + i;
+                const int rr = blk * 4 + (lane >> 4);
+                int li = gi * 4 + (rr >> 3);
+                if (li >= nl) li = gi * 4;
+                const size_t o = (((size_t)b * dm.L + sm.list[li]) * dm.H + (size_t)g * HG + (rr & 7)) * D +
+                                 unit_pos(rr, lane & 15) * 8;
+                lds_copy16(Q + o, __builtin_amdgcn_readfirstlane(lds_address(st.q + blk * 512)));
+                lds_copy16(dO + o, __builtin_amdgcn_readfirstlane(lds_address(st.g + blk * 512)));
+            }
+            if (wave == NWK - 1) {
+                // lanes 16 m + 2 j + h (j < 4 tokens, h halves of the 8 heads): m = 0 lse,
+                // m = 1 D, m >= 2 repeat (scratch)
+                int li = gi * 4 + ((lane & 7) >> 1);
+                if (li >= nl) li = gi * 4;
+                const size_t so =
+                    ((((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li]) * HG +
+                    4 * (lane & 1);
+                lds_copy16(((lane >> 3) & 1 ? dd : lse) + so,
+                           __builtin_amdgcn_readfirstlane(lds_address(st.meta)));
+            }
+        };
+
+        const uint32_t* bmrow = bm + (size_t)r * nwords;
+        const int wbeg = ((c + 1) * S) >> 5;
+        const int tend = min(4 * sg.j1, ntok);
+        for (int p0 = 4 * sg.j0; p0 < tend; p0 += LISTCAP) {
+            const int p1 = min(p0 + LISTCAP, tend);
+            const int nl = p1 - p0;
+            __syncthreads();              // the list of the previous batch is read
+            collect_tokens<NTK>(bmrow, wbeg, nwords, p0, p1, sm.list, sm.wtot, tid);
+            // per listed token: the slot holding c (a token's valid entries are distinct, so
+            // one matches; consecutive (token, slot) entries per thread keep the idx loads
+            // independent and coalesced), then its weight and ds there
+            for (int e = tid; e < nl * k; e += NTK) {
+                const int li = e / k, s2 = e - li * k;
+                const size_t so = (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k;
+                if (idx[so + s2] == c) sm.lslot[li] = (uint8_t)s2;
+            }
+            __syncthreads();
+            for (int li = tid; li < nl; li += NTK) {
+                const size_t so =
+                    (((size_t)b * dm.L + sm.list[li]) * dm.G + g) * k + sm.lslot[li];
+                sm.lw[li] = w[so];
+                sm.lds[li] = ds[so];
+            }
+            __syncthreads();
+            const int ngroups = (nl + 3) / 4;
+#pragma unroll
+            for (int u = 0; u < KV_NST - 1; ++u)
+                if (u < ngroups) issue(u, nl);
+            for (int gi = 0; gi < ngroups; ++gi) {
+                // group gi has landed once at most the next group's copies remain
+                if (gi + 1 < ngroups) {
+                    if (wave == NWK - 1) wait_loads_le<2 * BPW + 1>();
+                    else wait_loads_le<2 * BPW>();
+                } else {
+                    wait_loads_le<0>();
+                }
+                barrier_keep_copies();        // ... for every wave; stage (gi - 1) % NST free
+                if (gi + KV_NST - 1 < ngroups) issue(gi + KV_NST - 1, nl);
+                const KvStage& st = sm.st[gi % KV_NST];
+
+                // ---- Z, dP for the wave's 16 keys ---------------------------------------
+                f32x4_t z[2], dp[2];
+                z[0] = z[1] = dp[0] = dp[1] = zero4();
+#pragma unroll
+                for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+                    for (int rb = 0; rb < 2; ++rb) {
+                        z[rb] = mfma16(ld_bf16x8(st.q + koff[ks] + rb * 2048), kB[ks], z[rb]);
+                        dp[rb] = mfma16(ld_bf16x8(st.g + koff[ks] + rb * 2048), vB[ks], dp[rb]);
+                    }
+                // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2).  The landmark
+                // term dKbar_c / S = (alpha / S) sum_rows ds_tok q_row reaches every key of the
+                // chunk, so it is folded into dZ as alpha ds_tok / (beta S) before the dZ^T Q
+                // product.
+                f32x4_t pw[2], dz[2];
 #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) {
-                    z[rb] = mfma16(ld_bf16x8(st.q + koff[ks] + rb * 2048), kB[ks], z[rb]);
-                    dp[rb] = mfma16(ld_bf16x8(st.g + koff[ks] + rb * 2048), vB[ks], dp[rb]);
+                    const int li = gi * 4 + 2 * rb + (grp >> 1);
+                    const float wt = li < nl ? sm.lw[li] : 0.f;
+                    const float lm = li < nl ? sm.lds[li] * lmk : 0.f;
+                    const f32x4_t lv = *reinterpret_cast<const f32x4_t*>(&st.meta[16 * rb + 4 * grp]);
+                    const f32x4_t dv =
+                        *reinterpret_cast<const f32x4_t*>(&st.meta[32 + 16 * rb + 4 * grp]);
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float p = fast_exp2((beta * z[rb][i] - lv[i]) * l2e);
+                        pw[rb][i] = wt * p;
+                        dz[rb][i] = wt * p * (dp[rb][i] - dv[i]) + lm;
+                    }
                 }
-            // rows of this lane: 16 rb + 4 grp + i (token 2 rb + grp / 2).  The landmark term
-            // dKbar_c / S = (alpha / S) sum_rows ds_tok q_row reaches every key of the chunk, so
-            // it is folded into dZ as alpha ds_tok / (beta S) before the dZ^T Q product.
-            f32x4_t pw[2], dz[2];
+                // both products accumulate over every row that selected the chunk (thousands
+                // for a popular chunk): w P and dZ enter as bf16 hi/lo pairs
+                bf16x8_t pvh, pvl, dzh, dzl;
+                split8(pw[0], pw[1], pvh, pvl);
+                split8(dz[0], dz[1], dzh, dzl);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
-                const int li = gi * 4 + 2 * rb + (grp >> 1);
-                const float wt = li < nl ? sm.lw[li] : 0.f;
-                const float lm = li < nl ? sm.lds[li] * lmk : 0.f;
-                const f32x4_t lv = *reinterpret_cast<const f32x4_t*>(&st.meta[16 * rb + 4 * grp]);
-                const f32x4_t dv =
-                    *reinterpret_cast<const f32x4_t*>(&st.meta[32 + 16 * rb + 4 * grp]);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float p = fast_exp2((beta * z[rb][i] - lv[i]) * l2e);
-                    pw[rb][i] = wt * p;
-                    dz[rb][i] = wt * p * (dp[rb][i] - dv[i]) + lm;
+                for (int db = 0; db < 8; ++db) {
+                    const bf16x8_t gb =
+                        cat(ld_tr16(st.g + toff[db]), ld_tr16(st.g + toff[db] + 16 * D));
+                    aV[db] = mfma16(pvh, gb, aV[db]);
+                    aV[db] = mfma16(pvl, gb, aV[db]);
+                    const bf16x8_t qb =
+                        cat(ld_tr16(st.q + toff[db]), ld_tr16(st.q + toff[db] + 16 * D));
+                    aK[db] = mfma16(dzh, qb, aK[db]);
+                    aK[db] = mfma16(dzl, qb, aK[db]);
                 }
-            }
-            // both products accumulate over every row that selected the chunk (thousands for
-            // a popular chunk): w P and dZ enter as bf16 hi/lo pairs
-            bf16x8_t pvh, pvl, dzh, dzl;
-            split8(pw[0], pw[1], pvh, pvl);
-            split8(dz[0], dz[1], dzh, dzl);
-#pragma unroll
-            for (int db = 0; db < 8; ++db) {
-                const bf16x8_t gb = cat(ld_tr16(st.g + toff[db]), ld_tr16(st.g + toff[db] + 16 * D));
-                aV[db] = mfma16(pvh, gb, aV[db]);
-                aV[db] = mfma16(pvl, gb, aV[db]);
-                const bf16x8_t qb = cat(ld_tr16(st.q + toff[db]), ld_tr16(st.q + toff[db] + 16 * D));
-                aK[db] = mfma16(dzh, qb, aK[db]);
-                aK[db] = mfma16(dzl, qb, aK[db]);
             }
         }
-        // keep the tokens of an incomplete group for the next batch
-        if (!last_round) {
-            const int rem = nl - ngroups * 4;
-            __syncthreads();
-            if (tid < rem) sm.list[tid] = sm.list[ngroups * 4 + tid];
-            __syncthreads();
-            if (tid == 0) sm.nlist = rem;
-        } else {
-            break;
+        // the chunk's sums: final when this workgroup covered all its groups
+        float* ok = pk + ((size_t)lid * 2 + sg.pslot) * S * D;
+        float* ov = pv + ((size_t)lid * 2 + sg.pslot) * S * D;
+#pragma unroll
+        for (int db = 0; db < 8; ++db) {
+            const int d = 16 * db + row;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int kr = 16 * wave + 4 * grp + i;
+                if (sg.whole) {
+                    const size_t o = cbase + (size_t)kr * rowstride + d;
+                    dK[o] = f2bf(beta * aK[db][i]);
+                    dV[o] = f2bf(aV[db][i]);
+                } else {
+                    ok[kr * D + d] = beta * aK[db][i];
+                    ov[kr * D + d] = aV[db][i];
+                }
+            }
         }
     }
-#pragma unroll
-    for (int db = 0; db < 8; ++db) {
-        const int d = 16 * db + row;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const size_t o = cbase + (size_t)(16 * wave + 4 * grp + i) * rowstride + d;
-            dK[o] = f2bf(beta * aK[db][i]);
-            dV[o] = f2bf(aV[db][i]);
+}
+
+// Per chunk (b, g, c): the sum of the partials of the workgroups that shared it, in
+// workgroup order; zeros for chunks nobody selected and for the trailing partial chunk.  A
+// chunk one workgroup covered is final already.
+template <int S>
+__global__ __launch_bounds__(256) void bwd_kv_finish(
+    Dims dm, const int* __restrict__ gstart, const int* __restrict__ cntr,
+    const int* __restrict__ plan, const float* __restrict__ pk, const float* __restrict__ pv,
+    __bf16* __restrict__ dK, __bf16* __restrict__ dV) {
+    const int tid = threadIdx.x;
+    const int c = blockIdx.x % dm.Call;
+    const int bg = blockIdx.x / dm.Call, b = bg / dm.G, g = bg % dm.G;
+    const size_t rowstride = (size_t)dm.G * D;
+    const size_t cbase = ((size_t)b * dm.L + (size_t)c * S) * rowstride + (size_t)g * D;
+    const int r = bg * dm.C + c;
+    if (c >= dm.C || cntr[r] == 0) {            // trailing partial chunk, or never selected
+        const int rows = min(S, dm.L - c * S);
+        const bf16x4_t z4{__bf16(0.f), __bf16(0.f), __bf16(0.f), __bf16(0.f)};
+        for (int e = tid; e < rows * 32; e += 256) {
+            const size_t o = cbase + (size_t)(e >> 5) * rowstride + 4 * (e & 31);
+            *reinterpret_cast<bf16x4_t*>(dK + o) = z4;
+            *reinterpret_cast<bf16x4_t*>(dV + o) = z4;
         }
+        return;
+    }
+    const int T = plan[1];
+    const int rs = gstart[r], re = gstart[r + 1];
+    const int wf = rs / T, wl = (re - 1) / T;
+    if (wf == wl) return;                       // written by its workgroup
+    for (int e = tid; e < S * 32; e += 256) {
+        float4 sk{0.f, 0.f, 0.f, 0.f}, sv{0.f, 0.f, 0.f, 0.f};
+        for (int wg = wf; wg <= wl; ++wg) {
+            // the row is the first of the ranges after wf's, and of wf's when it starts there
+            const int sl = (wg > wf || rs == wf * T) ? 0 : 1;
+            const size_t po = ((size_t)wg * 2 + sl) * S * D + 4 * (size_t)e;
+            const float4 a = *reinterpret_cast<const float4*>(pk + po);
+            const float4 v = *reinterpret_cast<const float4*>(pv + po);
+            sk.x += a.x; sk.y += a.y; sk.z += a.z; sk.w += a.w;
+            sv.x += v.x; sv.y += v.y; sv.z += v.z; sv.w += v.w;
+        }
+        const size_t o = cbase + (size_t)(e >> 5) * rowstride + 4 * (e & 31);
+        *reinterpret_cast<bf16x4_t*>(dK + o) = bf16x4_t{f2bf(sk.x), f2bf(sk.y), f2bf(sk.z), f2bf(sk.w)};
+        *reinterpret_cast<bf16x4_t*>(dV + o) = bf16x4_t{f2bf(sv.x), f2bf(sv.y), f2bf(sv.z), f2bf(sv.w)};
     }
 }
 
@@ -593,20 +633,49 @@ hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, co
     e = launch_selection_bitmap(dm, idx, (uint32_t*)(wsb + l.bitmap), st);
     if (e != hipSuccess) return e;
     const int nwords = cdiv(dm.L, 32);
-    const dim3 g2(8 * cdiv(dm.Call * dm.B * dm.G, 8));
+    const int R = dm.B * dm.G * dm.C;
+    int* cnt = (int*)(wsb + l.cnt);
+    int* gstart = (int*)(wsb + l.gstart);
+    int* plan = (int*)(wsb + l.plan);
+    float* pk = (float*)(wsb + l.pk);
+    float* pv = (float*)(wsb + l.pv);
+    {
+        HSA_TIMED("bwd_plan", st);
+        if (R > 0)                       // no complete chunk: the plan is empty
+            hipLaunchKernelGGL(stream_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st,
+                               (const uint32_t*)(wsb + l.bitmap), R, nwords, dm.C, dm.S, cnt);
+        hipLaunchKernelGGL(stream_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R, kKvWGs,
+                           gstart, plan);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     if (dm.S == 64) {
         HSA_TIMED("bwd_kv_mfma", st);
-        hipLaunchKernelGGL((bwd_kv_mfma<64>), g2, dim3(256), 0, st, dm, (const __bf16*)Q,
-                           (const __bf16*)K, (const __bf16*)V, idx, w, (const __bf16*)dO, ds,
-                           lse, dd, (const uint32_t*)(wsb + l.bitmap), nwords, (__bf16*)dK,
-                           (__bf16*)dV);
+        hipLaunchKernelGGL((bwd_kv_mfma<64>), dim3(kKvWGs), dim3(256), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
+                           (const __bf16*)dO, ds, lse, dd, (const uint32_t*)(wsb + l.bitmap),
+                           nwords, (const int*)gstart, (const int*)cnt, (const int*)plan, pk, pv,
+                           (__bf16*)dK, (__bf16*)dV);
     } else {
         HSA_TIMED("bwd_kv_mfma", st);
-        hipLaunchKernelGGL((bwd_kv_mfma<128>), g2, dim3(512), 0, st, dm, (const __bf16*)Q,
-                           (const __bf16*)K, (const __bf16*)V, idx, w, (const __bf16*)dO, ds,
-                           lse, dd, (const uint32_t*)(wsb + l.bitmap), nwords, (__bf16*)dK,
-                           (__bf16*)dV);
+        hipLaunchKernelGGL((bwd_kv_mfma<128>), dim3(kKvWGs), dim3(512), 0, st, dm,
+                           (const __bf16*)Q, (const __bf16*)K, (const __bf16*)V, idx, w,
+                           (const __bf16*)dO, ds, lse, dd, (const uint32_t*)(wsb + l.bitmap),
+                           nwords, (const int*)gstart, (const int*)cnt, (const int*)plan, pk, pv,
+                           (__bf16*)dK, (__bf16*)dV);
     }
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 gf(dm.Call * dm.B * dm.G);
+    HSA_TIMED("bwd_kv_finish", st);
+    if (dm.S == 64)
+        hipLaunchKernelGGL((bwd_kv_finish<64>), gf, dim3(256), 0, st, dm, (const int*)gstart,
+                           (const int*)cnt, (const int*)plan, (const float*)pk, (const float*)pv,
+                           (__bf16*)dK, (__bf16*)dV);
+    else
+        hipLaunchKernelGGL((bwd_kv_finish<128>), gf, dim3(256), 0, st, dm, (const int*)gstart,
+                           (const int*)cnt, (const int*)plan, (const float*)pk, (const float*)pv,
+                           (__bf16*)dK, (__bf16*)dV);
     return hipGetLastError();
 }
 

@@ -109,14 +109,16 @@ __device__ __forceinline__ void lds_wait() {
 }
 
 // Tokens at positions [p0, p1) of a chunk's ascending token list (the set bits of bitmap
-// words wbeg .. nwords - 1 of its row) into list[0 .. p1 - p0).  Whole workgroup; the words
-// are counted 256 at a time with a workgroup prefix sum, stopping once p1 is reached.
+// words wbeg .. nwords - 1 of its row) into list[0 .. p1 - p0).  Whole workgroup (NTT
+// threads); the words are counted NTT at a time with a workgroup prefix sum, stopping once
+// p1 is reached.
+template <int NTT = NT>
 __device__ __forceinline__ void collect_tokens(const uint32_t* __restrict__ bmrow, int wbeg,
                                                int nwords, int p0, int p1, int* list,
                                                int* wtot, int tid) {
     const int lane = tid & 63, wave = tid >> 6;
     int base = 0;
-    for (int wb = wbeg; wb < nwords; wb += NT) {
+    for (int wb = wbeg; wb < nwords; wb += NTT) {
         const int wi = wb + tid;
         const uint32_t word = wi < nwords ? bmrow[wi] : 0u;
         const int cnt = __popc(word);
@@ -130,7 +132,7 @@ __device__ __forceinline__ void collect_tokens(const uint32_t* __restrict__ bmro
         __syncthreads();
         int before = 0, tot = 0;
 #pragma unroll
-        for (int w2 = 0; w2 < NW; ++w2) {
+        for (int w2 = 0; w2 < NTT / 64; ++w2) {
             const int v = wtot[w2];
             before += (w2 < wave) ? v : 0;
             tot += v;
