@@ -408,8 +408,7 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
         // the group's first one, with weight and ds 0): wave w copies the Q and dO row blocks
         // w BPW .. w BPW + BPW - 1 (4 rows = half a token each); the last wave also copies
         // the lse and D of the 32 rows
-        auto issue = [&](int gi, int nl) __attribute__((always_inline)) {
-            KvStage& st = sm.st[gi % KV_NST];
+        auto issue = [&](int gi, int nl, KvStage& st) __attribute__((always_inline)) {
 #pragma unroll
             for (int i = 0; i < BPW; ++i) {
                 const int blk = wave * BPW + i;
@@ -461,8 +460,11 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
             const int ngroups = (nl + 3) / 4;
 #pragma unroll
             for (int u = 0; u < KV_NST - 1; ++u)
-                if (u < ngroups) issue(u, nl);
-            for (int gi = 0; gi < ngroups; ++gi) {
+                if (u < ngroups) issue(u, nl, sm.st[u]);
+            // one group's step; its stage index SI = gi % KV_NST is a constant (the loop
+            // below is unrolled by KV_NST), so stage addresses are lane bases plus immediates
+            auto group = [&](int gi, auto si) __attribute__((always_inline)) {
+                constexpr int SI = decltype(si)::value;
                 // group gi has landed once at most the next group's copies remain
                 if (gi + 1 < ngroups) {
                     if (wave == NWK - 1) wait_loads_le<2 * BPW + 1>();
@@ -471,8 +473,8 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
                     wait_loads_le<0>();
                 }
                 barrier_keep_copies();        // ... for every wave; stage (gi - 1) % NST free
-                if (gi + KV_NST - 1 < ngroups) issue(gi + KV_NST - 1, nl);
-                const KvStage& st = sm.st[gi % KV_NST];
+                if (gi + KV_NST - 1 < ngroups) issue(gi + KV_NST - 1, nl, sm.st[(SI + KV_NST - 1) % KV_NST]);
+                const KvStage& st = sm.st[SI];
 
                 // ---- Z, dP for the wave's 16 keys ---------------------------------------
                 f32x4_t z[2], dp[2];
@@ -520,6 +522,12 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
                     aK[db] = mfma16(dzh, qb, aK[db]);
                     aK[db] = mfma16(dzl, qb, aK[db]);
                 }
+            };
+            static_assert(KV_NST == 3, "the group loop is unrolled by the ring depth");
+            for (int gb = 0; gb < ngroups; gb += KV_NST) {
+                group(gb, IntC<0>{});
+                if (gb + 1 < ngroups) group(gb + 1, IntC<1>{});
+                if (gb + 2 < ngroups) group(gb + 2, IntC<2>{});
             }
         }
         // the chunk's sums: final when this workgroup covered all its groups
