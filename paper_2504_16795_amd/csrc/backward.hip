@@ -222,7 +222,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     Dims dm, const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const T* __restrict__ dO,
     const float* __restrict__ ds, const uint32_t* __restrict__ bm, int nwords,
-    T* __restrict__ dK, T* __restrict__ dV) {
+    T* __restrict__ dK, T* __restrict__ dV, float* __restrict__ part) {
     constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
     constexpr int NE = CS * D / kThreads;
     __shared__ T Ks[CS * KP];
@@ -239,7 +239,11 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     const int h = dm.h, k = dm.k;
     const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;   // row cS
 
+    // split z of nsplit takes the chunk's tokens z, z + nsplit, ... (in increasing order) and,
+    // with more than one split, writes fp32 partials that kv_generic_finish adds in split order
+    const int z = blockIdx.z, nsplit = gridDim.z;
     if (c >= dm.C) {   // trailing partial chunk: never selected, zero gradient
+        if (z != 0) return;
         const int rows = dm.L - c * CS;
         for (int i = tid; i < rows * D; i += kThreads) {
             const size_t gi = (rowbase + (size_t)(i / D) * dm.G) * D + i % D;
@@ -260,11 +264,13 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     float dkbar = 0.f;   // thread tid < D owns element tid of dKbar
 
     const uint32_t* row = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
+    int ord = 0;                         // the token's place in the chunk's token list
     for (int wi = ((c + 1) * CS) >> 5; wi < nwords; ++wi) {
         uint32_t word = row[wi];
         while (word) {
             const int t = wi * 32 + (__ffs(word) - 1);
             word &= word - 1;
+            if (ord++ % nsplit != z) continue;
             const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
             int slot = 0;
             for (int i = 0; i < k; ++i)
@@ -335,42 +341,87 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     if (tid < D) dkb[tid] = dkbar;
     __syncthreads();
     const float invS = 1.f / (float)CS;
+    float* pk = nsplit > 1 ? part + (((size_t)z * dm.B * dm.G + bg) * dm.C + c) * (2 * CS * D)
+                           : nullptr;
 #pragma unroll
     for (int r = 0; r < NE; ++r) {
         const int i = tid + r * kThreads;
         const int s = i / D, e = i % D;
-        const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
-        dK[gi] = from_f32<T>(aK[r] + dkb[e] * invS);
-        dV[gi] = from_f32<T>(aV[r]);
+        if (nsplit > 1) {
+            pk[i] = aK[r] + dkb[e] * invS;
+            pk[CS * D + i] = aV[r];
+        } else {
+            const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
+            dK[gi] = from_f32<T>(aK[r] + dkb[e] * invS);
+            dV[gi] = from_f32<T>(aV[r]);
+        }
     }
+}
+
+// dK, dV of a complete chunk from the key pass's per-split partials, added in split order
+// (the chunk's elements spread over gridDim.z workgroups)
+template <typename T, int D, int CS>
+__global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nsplit,
+                                                              const float* __restrict__ part,
+                                                              T* __restrict__ dK,
+                                                              T* __restrict__ dV) {
+    const int c = blockIdx.x, bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
+    const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;
+    for (int i = blockIdx.z * kThreads + threadIdx.x; i < CS * D; i += gridDim.z * kThreads) {
+        float sk = 0.f, sv = 0.f;
+        for (int z = 0; z < nsplit; ++z) {
+            const float* pk = part + (((size_t)z * dm.B * dm.G + bg) * dm.C + c) * (2 * CS * D);
+            sk += pk[i];
+            sv += pk[CS * D + i];
+        }
+        const size_t gi = (rowbase + (size_t)(i / D) * dm.G) * D + i % D;
+        dK[gi] = from_f32<T>(sk);
+        dV[gi] = from_f32<T>(sv);
+    }
+}
+
+// Splits of the generic key pass: enough workgroups to fill the chip when the chunks are
+// few (each chunk's tokens are otherwise walked by one workgroup, one after another), at
+// most 16.
+inline int kv_splits(const Dims& dm) {
+    const long rows = (long)dm.B * dm.G * dm.Call;
+    long n = rows > 0 ? (1024 + rows - 1) / rows : 1;
+    return (int)(n < 1 ? 1 : (n > 16 ? 16 : n));
 }
 
 template <typename T, int D, int CS>
 void launch_kv(const Dims& dm, const void* Q, const void* K, const void* V, const int32_t* idx,
                const float* w, const void* dO, const float* ds, const uint32_t* bm, int nwords,
-               void* dK, void* dV, hipStream_t st) {
-    dim3 grid(dm.Call, dm.B * dm.G);
+               void* dK, void* dV, float* part, hipStream_t st) {
+    const int nsplit = kv_splits(dm);
+    dim3 grid(dm.Call, dm.B * dm.G, nsplit);
     {
         HSA_TIMED("bwd_kv_generic", st);
         hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), grid, dim3(kThreads), 0, st, dm, (const T*)Q,
                            (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm, nwords, (T*)dK,
-                           (T*)dV);
+                           (T*)dV, part);
+    }
+    if (nsplit > 1 && dm.C > 0) {
+        HSA_TIMED("bwd_kv_finish", st);
+        hipLaunchKernelGGL((kv_generic_finish<T, D, CS>), dim3(dm.C, dm.B * dm.G, 8), dim3(kThreads),
+                           0, st, dm, nsplit, (const float*)part, (T*)dK, (T*)dV);
     }
 }
 
 template <typename T, int D>
 void launch_kv_s(const Dims& dm, const void* Q, const void* K, const void* V,
                  const int32_t* idx, const float* w, const void* dO, const float* ds,
-                 const uint32_t* bm, int nwords, void* dK, void* dV, hipStream_t st) {
+                 const uint32_t* bm, int nwords, void* dK, void* dV, float* part,
+                 hipStream_t st) {
     switch (dm.S) {
-        case 16: launch_kv<T, D, 16>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
-        case 32: launch_kv<T, D, 32>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
-        case 64: launch_kv<T, D, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st); break;
+        case 16: launch_kv<T, D, 16>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
+        case 32: launch_kv<T, D, 32>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
+        case 64: launch_kv<T, D, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
         default:
             // fp32 with S = 128 and d = 128 exceeds the LDS of one workgroup; rejected by the
             // argument checks, so it is not instantiated.
             if constexpr (!(sizeof(T) == 4 && D == 128))
-                launch_kv<T, D, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+                launch_kv<T, D, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
             break;
     }
 }
@@ -397,10 +448,12 @@ void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
                                dm, idx, bm, nwords);
         }
     }
+    // the key pass's per-split partials follow the bitmap
+    float* part = (float*)((char*)bm + align256(nbm * 4));
     if (dm.d == 128)
-        launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+        launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
     else
-        launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, st);
+        launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
 }
 
 template <typename T>
@@ -445,8 +498,10 @@ hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t*
 
 size_t backward_generic_workspace(const Dims& dm) {
     const size_t nwords = (size_t)cdiv(dm.L, 32);
+    const int nsplit = kv_splits(dm);
+    const size_t part = nsplit > 1 ? (size_t)nsplit * dm.B * dm.G * dm.C * 2 * dm.S * dm.d * 4 : 0;
     return align256((size_t)dm.B * dm.L * dm.G * dm.k * 4) +
-           align256((size_t)dm.B * dm.G * dm.C * nwords * 4);
+           align256((size_t)dm.B * dm.G * dm.C * nwords * 4) + align256(part);
 }
 
 size_t backward_workspace(const Dims& dm) {
