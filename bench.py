@@ -607,7 +607,8 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
              "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic",
              "decode_scan": "decode_scan", "decode_attend_mfma": "decode_attend_mfma",
              "decode_gather": "decode_gather", "decode_finish": "decode_finish",
-             "decode_combine": "decode_combine"}
+             "decode_combine": "decode_combine", "decode_attend_slot": "decode_attend_mfma",
+             "bwd_kv_finish": "bwd_kv_finish", "kv_generic_finish": "bwd_kv_finish"}
     # per timing name: the bytes of every kernel that maps to it (the two plan kernels, say,
     # each launched once per step) summed, per launch of the stage (the largest dispatch
     # count among them); per full kernel name as well
