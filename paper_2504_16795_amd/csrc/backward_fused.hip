@@ -579,35 +579,45 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     // (given the attention alone, the launcher passes the layer's key means)
     const bool need_kb = ncand > 0 && (!attn_only || dm.off1);
     // slot values are wave-uniform (lane reads), so the branches below are scalar
+    // All loads of 4 slots are issued before their first use, with no branch between them
+    // (a slot past k reads slot k - 1's data, a slot that does not own its chunk reads its
+    // own stale partial); what is not used is dropped by a select on the partial's scale.
     for (int s0 = 0; s0 < k; s0 += 4) {
         u32x4_t pv[4][2];
         float4 kv[4][4];
+        float sgv[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int s = s0 + j;
-            if (s < k && __builtin_amdgcn_readlane(own, s)) {
-                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
-                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
-                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
-            }
-            if (s < k && need_kb) {
-                const int cs = __builtin_amdgcn_readlane(cl, s);
+            const int s = min(s0 + j, k - 1);
+            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+            pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+            pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
+        }
+        if (need_kb) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int cs = __builtin_amdgcn_readlane(cl, min(s0 + j, k - 1));
                 const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
                 const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) kv[j][v] = *reinterpret_cast<const float4*>(kb + 4 * v);
             }
         }
+        if (dm.off1) {
+            // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                sgv[j] = dwc[((so + min(s0 + j, k - 1)) * HG + head) * 2 + 1];
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
-            if (s >= k) break;
-            if (__builtin_amdgcn_readlane(own, s)) {
-                bfp_accum8(pv[j][0], acc);
-                bfp_accum8(pv[j][1], acc + 8);
-            }
+            const bool use = s < k && __builtin_amdgcn_readlane(own, min(s, k - 1)) != 0;
+            bfp_accum8(pv[j][0], acc, use);
+            bfp_accum8(pv[j][1], acc + 8, use);
             if (!need_kb) continue;
-            const float coef = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s));
+            const float coef =
+                s < k ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s)) : 0.f;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 lmk[4 * v + 0] = fmaf(coef, kv[j][v].x, lmk[4 * v + 0]);
@@ -615,9 +625,8 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
                 lmk[4 * v + 2] = fmaf(coef, kv[j][v].z, lmk[4 * v + 2]);
                 lmk[4 * v + 3] = fmaf(coef, kv[j][v].w, lmk[4 * v + 3]);
             }
-            if (dm.off1 && __builtin_amdgcn_readlane(own, s)) {
-                // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
-                const float sg = dwc[((so + s) * HG + head) * 2 + 1];
+            if (dm.off1) {
+                const float sg = use ? sgv[j] : 0.f;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     acc[4 * v + 0] = fmaf(sg, kv[j][v].x, acc[4 * v + 0]);

@@ -334,25 +334,23 @@ __global__ __launch_bounds__(256) void fwd_reduce(Dims dm, const int32_t* __rest
     float acc[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-    // slot values are wave-uniform (lane reads), so the branches below are scalar
+    // All loads of 4 slots are issued before their first use, with no branch between them
+    // (a slot past k reads slot k - 1's data, a slot that does not own its chunk reads its
+    // own stale partial); what is not used is dropped by a select on the partial's scale.
     for (int s0 = 0; s0 < k; s0 += 4) {
         u32x4_t pv[4][2];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int s = s0 + j;
-            if (s < k && __builtin_amdgcn_readlane(own, s)) {
-                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
-                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
-                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
-            }
+            const uint16_t* pp = part + ((so + min(s0 + j, k - 1)) * HG + head) * D + c0;
+            pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+            pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int s = s0 + j;
-            if (s < k && __builtin_amdgcn_readlane(own, s)) {
-                bfp_accum8(pv[j][0], acc);
-                bfp_accum8(pv[j][1], acc + 8);
-            }
+            const bool use = s < k && __builtin_amdgcn_readlane(own, min(s, k - 1)) != 0;
+            bfp_accum8(pv[j][0], acc, use);
+            bfp_accum8(pv[j][1], acc + 8, use);
         }
     }
     bf16x8_t o0, o1;

@@ -126,12 +126,14 @@ __device__ __forceinline__ u32x4_t bfp_pack8(const f32x4_t& a, const f32x4_t& b)
     return u32x4_t{w[0], w[1], w[2], w[3]};
 }
 
-// Adds the 8 values of a block to acc[0..7] (field i to acc[i]).
-__device__ __forceinline__ void bfp_accum8(const u32x4_t& v, float acc[8]) {
+// Adds the 8 values of a block to acc[0..7] (field i to acc[i]); with use false, adds zeros
+// whatever the 16 bytes hold (the scale is selected away, never multiplied by zero).
+__device__ __forceinline__ void bfp_accum8(const u32x4_t& v, float acc[8], bool use = true) {
     const uint32_t x = (v[0] & 0x00010001u) | ((v[1] & 0x00010001u) << 2) |
                        ((v[2] & 0x00010001u) << 4) | ((v[3] & 0x00010001u) << 6);
     const uint32_t e = (x | (x >> 15)) & 0xFFu;
-    const float sc = __uint_as_float((e + 1u) << 23) * (1.0f / 32767.0f);   // 2^(e - 126) / 32767
+    const float sc1 = __uint_as_float((e + 1u) << 23) * (1.0f / 32767.0f);  // 2^(e - 126) / 32767
+    const float sc = use ? sc1 : 0.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
         acc[2 * j] = fmaf((float)(int16_t)(v[j] & 0xFFFFu), sc, acc[2 * j]);
