@@ -351,6 +351,9 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
                         sm_m[i] = m8[4 * rb + i];
                         sm_l[i] = group_sum<16>(ev);
                         sm_n[i] = group_sum<16>(ev * dp[rb][i]);
+                        // complete in every lane before the branch below (otherwise the last
+                        // DPP step is sunk into it and can no longer fuse with its add)
+                        asm volatile("" : "+v"(sm_l[i]), "+v"(sm_n[i]));
                     }
                     if (row == 0) {
                         *reinterpret_cast<f32x4_t*>(&sm.stat[wave][0][16 * rb + 4 * grp]) = sm_m;

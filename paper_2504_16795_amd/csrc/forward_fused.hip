@@ -248,6 +248,10 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
 #pragma unroll
                 for (int i = 0; i < 8; ++i) zl[i] = ls[i];
                 rows16_sum(ls);
+                // complete in every lane before the branch below (otherwise the last DPP step
+                // is sunk into it and can no longer fuse with its add)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) asm volatile("" : "+v"(ls[i]));
                 f32x4_t e[2];
 #pragma unroll
                 for (int rb = 0; rb < 2; ++rb) {
