@@ -603,7 +603,7 @@ def pmc_summarize(workload, fetch_csv, write_csv, out_path):
              "bwd_rowcount": "bwd_plan", "bwd_plan": "bwd_plan",
              "fwd_chunk_mfma": "fwd_chunk_mfma", "fwd_reduce": "fwd_reduce",
              "stream_rowcount": "plan", "stream_plan": "plan",
-             "fill_zero_u32": "fill_zero_u32", "forward_generic": "forward_generic",
+             "forward_generic": "forward_generic",
              "bwd_q_generic": "bwd_q_generic", "bwd_kv_generic": "bwd_kv_generic",
              "decode_scan": "decode_scan", "decode_attend_mfma": "decode_attend_mfma",
              "decode_gather": "decode_gather", "decode_finish": "decode_finish",

@@ -178,42 +178,47 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
     }
 }
 
-__global__ void fill_zero_u32(uint32_t* __restrict__ p, size_t n) {
-    const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < n) p[i] = 0u;
-}
-
 // The selection bitmap (the M matrix of the key-side program as bits): bit t of word
-// (b, g, c, t / 32) is set when a slot of token t holds chunk c, 0 <= c < floor(t / S).  One
-// wave per (b, g, slot, 64 consecutive tokens): the lanes holding the same chunk are gathered
-// with a ballot, and one atomic OR per (chunk, word) sets their bits, so tokens that chose the
-// same chunk do not contend for its word one by one (order-independent, exact).
+// (b, g, c, t / 32) is set when a slot of token t holds chunk c, 0 <= c < floor(t / S), and
+// every other bit is clear.  One workgroup per (256-token block, b g, range of kBmRange
+// chunks) builds its 8-word slice of every row of the range in LDS (one LDS atomic OR per
+// valid (token, slot), order-independent and exact) and writes the whole slice, zeros
+// included, so no separate clearing pass and no global atomics are needed.  Chunks at or
+// past floor((t0 + 255) / S) cannot hold a bit of the block and are written as zeros
+// without touching LDS.
+constexpr int kBmRange = 1024;
+
 __global__ __launch_bounds__(256) void bitmap_build(Dims dm, const int32_t* __restrict__ idx,
                                                     uint32_t* __restrict__ bm, int nwords) {
-    const int lane = threadIdx.x & 63;
-    const size_t wv = (size_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int nblk = (dm.L + 63) / 64;
-    if (wv >= (size_t)dm.B * dm.G * dm.k * nblk) return;
-    const int blk = (int)(wv % nblk);
-    size_t r = wv / nblk;
-    const int s = (int)(r % dm.k);
-    r /= dm.k;
-    const int g = (int)(r % dm.G);
-    const int b = (int)(r / dm.G);
-    const int t = blk * 64 + lane;
-    const int c = t < dm.L ? idx[(((size_t)b * dm.L + t) * dm.G + g) * dm.k + s] : -1;
-    const bool valid = c >= 0 && c < t / dm.S;   // only valid entries; others are ignored
-    uint64_t active = __ballot(valid);
-    uint32_t* row = bm + ((size_t)b * dm.G + g) * dm.C * nwords + 2 * blk;
-    while (active) {
-        const int c0 = __builtin_amdgcn_readlane(c, __ffsll((unsigned long long)active) - 1);
-        const uint64_t m = __ballot(valid && c == c0);
-        if (lane == 0) {
-            const uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
-            if (lo) atomicOr(row + (size_t)c0 * nwords, lo);
-            if (hi) atomicOr(row + (size_t)c0 * nwords + 1, hi);
+    __shared__ uint32_t sl[kBmRange * 8];
+    const int tid = threadIdx.x;
+    const int t0 = blockIdx.x * 256;
+    const int bg = blockIdx.y;
+    const int b = bg / dm.G, g = bg % dm.G;
+    const int c0 = blockIdx.z * kBmRange;
+    const int c1 = min(dm.C, c0 + kBmRange);
+    const int tend = min(dm.L, t0 + 256);
+    const int nact = max(0, min(c1, (tend - 1) / dm.S) - c0);   // rows that can hold bits
+    for (int i = tid; i < nact * 8; i += 256) sl[i] = 0u;
+    __syncthreads();
+    const int t = t0 + tid;
+    if (t < dm.L) {
+        const int32_t* row = idx + (((size_t)b * dm.L + t) * dm.G + g) * dm.k;
+        const int lim = min(t / dm.S, c1);
+        const uint32_t bit = 1u << (tid & 31);
+#pragma unroll 8
+        for (int s = 0; s < dm.k; ++s) {
+            const int c = row[s];
+            if (c >= c0 && c < lim) atomicOr(&sl[(c - c0) * 8 + (tid >> 5)], bit);
         }
-        active &= ~m;
+    }
+    __syncthreads();
+    const int w0 = t0 >> 5;
+    const int nw = min(8, nwords - w0);
+    uint32_t* out = bm + (size_t)bg * dm.C * nwords + w0;
+    for (int i = tid; i < (c1 - c0) * 8; i += 256) {
+        const int cr = i >> 3, j = i & 7;
+        if (j < nw) out[(size_t)(c0 + cr) * nwords + j] = cr < nact ? sl[i] : 0u;
     }
 }
 
@@ -426,6 +431,15 @@ void launch_kv_s(const Dims& dm, const void* Q, const void* K, const void* V,
     }
 }
 
+void launch_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm, hipStream_t st) {
+    if ((size_t)dm.B * dm.G * dm.C * dm.L == 0) return;
+    HSA_TIMED("bitmap_build", st);
+    hipLaunchKernelGGL(bitmap_build,
+                       dim3((unsigned)cdiv(dm.L, 256), (unsigned)(dm.B * dm.G),
+                            (unsigned)cdiv(dm.C, kBmRange)),
+                       dim3(256), 0, st, dm, idx, bm, cdiv(dm.L, 32));
+}
+
 // selection bitmap, then the chunk-major key/value pass (ds already in the workspace)
 template <typename T>
 void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
@@ -435,19 +449,7 @@ void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
     const float* ds = (const float*)ws;
     uint32_t* bm = (uint32_t*)((char*)ws + align256((size_t)dm.B * dm.L * dm.G * dm.k * 4));
     const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
-    if (nbm) {
-        {
-            HSA_TIMED("fill_zero_u32", st);
-            hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0,
-                               st, bm, nbm);
-        }
-        const size_t nwv = (size_t)dm.B * dm.G * dm.k * cdiv(dm.L, 64);
-        {
-            HSA_TIMED("bitmap_build", st);
-            hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((nwv + 3) / 4)), dim3(256), 0, st,
-                               dm, idx, bm, nwords);
-        }
-    }
+    launch_bitmap(dm, idx, bm, st);
     // the key pass's per-split partials follow the bitmap
     float* part = (float*)((char*)bm + align256(nbm * 4));
     if (dm.d == 128)
@@ -479,20 +481,7 @@ hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
 
 hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t* bm,
                                    hipStream_t st) {
-    const int nwords = cdiv(dm.L, 32);
-    const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
-    if (!nbm) return hipSuccess;
-    {
-        HSA_TIMED("fill_zero_u32", st);
-        hipLaunchKernelGGL(fill_zero_u32, dim3((unsigned)((nbm + 255) / 256)), dim3(256), 0, st,
-                           bm, nbm);
-    }
-    const size_t nwv = (size_t)dm.B * dm.G * dm.k * cdiv(dm.L, 64);
-    {
-        HSA_TIMED("bitmap_build", st);
-        hipLaunchKernelGGL(bitmap_build, dim3((unsigned)((nwv + 3) / 4)), dim3(256), 0, st, dm,
-                           idx, bm, nwords);
-    }
+    launch_bitmap(dm, idx, bm, st);
     return hipGetLastError();
 }
 
