@@ -497,7 +497,10 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
 // Token-major completion of dQ (one wave per (b, t, g); lane: head lane >> 3, columns
 // 16 (lane & 7) .. +15).  A slot counts when 0 <= c < floor(t / S); a slot repeating an
 // earlier slot's chunk shares that slot's partial (already weighted by the sum of their
-// weights) and its dw.
+// weights) and its dw.  OFF1: the softmax off by one (the partials leave out a per-head
+// Kbar_c term, added here); a separate instantiation, so that the plain softmax's kernel
+// holds no per-slot key means in registers.
+template <bool OFF1>
 __global__ __launch_bounds__(256) void bwd_dq_reduce(
     Dims dm, const __bf16* __restrict__ Q, const float* __restrict__ Kbar,
     const int32_t* __restrict__ idx, const float* __restrict__ w,
@@ -524,7 +527,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
     if (lane < k) {
         cl = idx[so + lane];
         wl = w[so + lane];
-        dwl = dm.off1 ? dwc[(so + lane) * (2 * HG)] : dwc[so + lane];
+        dwl = OFF1 ? dwc[(so + lane) * (2 * HG)] : dwc[so + lane];
     }
     const bool valid = lane < k && cl >= 0 && cl < ncand;
     int canon = lane;                       // first slot holding the same chunk
@@ -578,57 +581,105 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[i] = lmk[i] = 0.f;
     const size_t kbbase = (size_t)b * dm.C * dm.G + g;
-    // Kbar_c serves the landmark term, and off by one the mean-key term of the partials
-    // (given the attention alone, the launcher passes the layer's key means)
-    const bool need_kb = ncand > 0 && (!attn_only || dm.off1);
-    // slot values are wave-uniform (lane reads), so the branches below are scalar
-    // All loads of 4 slots are issued before their first use, with no branch between them
+    // All loads of J slots are issued before their first use, with no branch between them
     // (a slot past k reads slot k - 1's data, a slot that does not own its chunk reads its
     // own stale partial); what is not used is dropped by a select on the partial's scale.
-    for (int s0 = 0; s0 < k; s0 += 4) {
-        u32x4_t pv[4][2];
-        float4 kv[4][4];
-        float sgv[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int s = min(s0 + j, k - 1);
-            const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
-            pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
-            pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
-        }
-        if (need_kb) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int cs = __builtin_amdgcn_readlane(cl, min(s0 + j, k - 1));
+    // Slot values are wave-uniform (lane reads), so the remaining branches are scalar.
+    if constexpr (!OFF1) {
+        // the landmark term sum_i ds_i Kbar_{c_i} is the same for every head: lane (head j)
+        // takes the slots j, j + 8, ..., and the 8 lanes of a column block sum their parts
+        // (its loads follow the first partial loads)
+        const bool need_kb = ncand > 0 && !attn_only;
+        auto landmark = [&]() __attribute__((always_inline)) {
+            for (int m = 0; m * HG < k; ++m) {
+                const int s = head + HG * m;
+                const int cs = __shfl(cl, min(s, k - 1), 64);
+                const float coef = s < k ? __shfl(dsl, min(s, k - 1), 64) : 0.f;
                 const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
                 const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
 #pragma unroll
-                for (int v = 0; v < 4; ++v) kv[j][v] = *reinterpret_cast<const float4*>(kb + 4 * v);
+                for (int v = 0; v < 4; ++v) {
+                    const float4 x = *reinterpret_cast<const float4*>(kb + 4 * v);
+                    lmk[4 * v + 0] = fmaf(coef, x.x, lmk[4 * v + 0]);
+                    lmk[4 * v + 1] = fmaf(coef, x.y, lmk[4 * v + 1]);
+                    lmk[4 * v + 2] = fmaf(coef, x.z, lmk[4 * v + 2]);
+                    lmk[4 * v + 3] = fmaf(coef, x.w, lmk[4 * v + 3]);
+                }
+            }
+        };
+        constexpr int J = 4;
+        for (int s0 = 0; s0 < k; s0 += J) {
+            u32x4_t pv[J][2];
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int s = min(s0 + j, k - 1);
+                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
+            }
+            if (s0 == 0 && need_kb) landmark();
+#pragma unroll
+            for (int j = 0; j < J; ++j) {
+                const int s = s0 + j;
+                const bool use = s < k && __builtin_amdgcn_readlane(own, min(s, k - 1)) != 0;
+                bfp_accum8(pv[j][0], acc, use);
+                bfp_accum8(pv[j][1], acc + 8, use);
             }
         }
-        if (dm.off1) {
-            // off by one: the head's W sum_keys dZ, whose Kbar_c part the partial left out
+        if (need_kb) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const float v = lmk[i] + dpp_mov<0x128>(lmk[i]);   // row_ror:8 = lane ^ 8
+                lmk[i] = pair32_sum(pair16_sum(v));
+            }
+        }
+    } else {
+        // off by one: per slot the key mean serves the landmark term and the head's
+        // W sum_keys dZ term, whose Kbar_c part the partial left out (given the attention
+        // alone, the launcher passes the layer's key means)
+        const bool need_kb = ncand > 0;
+        for (int s0 = 0; s0 < k; s0 += 4) {
+            u32x4_t pv[4][2];
+            float4 kv[4][4];
+            float sgv[4];
 #pragma unroll
             for (int j = 0; j < 4; ++j)
                 sgv[j] = dwc[((so + min(s0 + j, k - 1)) * HG + head) * 2 + 1];
-        }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int s = s0 + j;
-            const bool use = s < k && __builtin_amdgcn_readlane(own, min(s, k - 1)) != 0;
-            bfp_accum8(pv[j][0], acc, use);
-            bfp_accum8(pv[j][1], acc + 8, use);
-            if (!need_kb) continue;
-            const float coef =
-                s < k ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s)) : 0.f;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                lmk[4 * v + 0] = fmaf(coef, kv[j][v].x, lmk[4 * v + 0]);
-                lmk[4 * v + 1] = fmaf(coef, kv[j][v].y, lmk[4 * v + 1]);
-                lmk[4 * v + 2] = fmaf(coef, kv[j][v].z, lmk[4 * v + 2]);
-                lmk[4 * v + 3] = fmaf(coef, kv[j][v].w, lmk[4 * v + 3]);
+            for (int j = 0; j < 4; ++j) {
+                const int s = min(s0 + j, k - 1);
+                const uint16_t* pp = part + ((so + s) * HG + head) * D + c0;
+                pv[j][0] = *reinterpret_cast<const u32x4_t*>(pp);
+                pv[j][1] = *reinterpret_cast<const u32x4_t*>(pp + 8);
             }
-            if (dm.off1) {
+            if (need_kb) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int cs = __builtin_amdgcn_readlane(cl, min(s0 + j, k - 1));
+                    const int cc = (cs >= 0 && cs < ncand) ? cs : 0;
+                    const float* kb = Kbar + (kbbase + (size_t)cc * dm.G) * D + c0;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        kv[j][v] = *reinterpret_cast<const float4*>(kb + 4 * v);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int s = s0 + j;
+                const bool use = s < k && __builtin_amdgcn_readlane(own, min(s, k - 1)) != 0;
+                bfp_accum8(pv[j][0], acc, use);
+                bfp_accum8(pv[j][1], acc + 8, use);
+                if (!need_kb) continue;
+                const float coef =
+                    s < k ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(dsl), s))
+                          : 0.f;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    lmk[4 * v + 0] = fmaf(coef, kv[j][v].x, lmk[4 * v + 0]);
+                    lmk[4 * v + 1] = fmaf(coef, kv[j][v].y, lmk[4 * v + 1]);
+                    lmk[4 * v + 2] = fmaf(coef, kv[j][v].z, lmk[4 * v + 2]);
+                    lmk[4 * v + 3] = fmaf(coef, kv[j][v].w, lmk[4 * v + 3]);
+                }
                 const float sg = use ? sgv[j] : 0.f;
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -925,7 +976,8 @@ hipError_t launch_backward_fused(const Dims& dm, const void* Q, const void* K, c
     {
         const size_t items = (size_t)dm.B * dm.L * dm.G;
         HSA_TIMED("bwd_dq_reduce", st);
-        hipLaunchKernelGGL(bwd_dq_reduce, dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
+        hipLaunchKernelGGL(dm.off1 ? bwd_dq_reduce<true> : bwd_dq_reduce<false>,
+                           dim3((unsigned)((items + 3) / 4)), dim3(256), 0, st, dm,
                            (const __bf16*)Q, Kbar, idx, w, (const uint16_t*)part, (const float*)dwc,
                            (__bf16*)dQ, dsb, qs);
     }
