@@ -268,7 +268,7 @@ hsa_attn_status_t hsa_decode_host(const hsa_attn_params_t* p, const void* q,
 /* hsa_decode for callers that cannot allocate device memory (code under HIP graph capture,
  * serving loops that may not call hipMalloc, harnesses that forbid it): the same arguments
  * and results as hsa_decode, without the workspace arguments.  Its scratch memory (slice
- * candidates and, off the bf16 h = 8 path, per-slot partial outputs) is a file-scope device
+ * candidates and per-slot partial outputs) is a file-scope device
  * array of HSA_DECODE_NOALLOC_SCRATCH_BYTES per GPU, held until the process ends; the call
  * allocates and frees nothing.  Shapes whose hsa_attn_workspace_size(p, HSA_OP_DECODE)
  * exceeds that size return HSA_ATTN_ERR_UNSUPPORTED before any launch (the 1M-token cache of
