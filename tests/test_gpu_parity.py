@@ -37,6 +37,10 @@ CASES = {
     # keys dominated by their chunk's offset (about 23 times the per-key spread): dQ is a
     # strongly cancelling sum over each chunk's keys
     "key_offset_bf16": (Shape(1, 1024, 16, 2, 128, 64, 8, "bf16"), 21, "iid", 2.0),
+    # more than 1024 chunks: the selection bitmap is built over two chunk ranges (generic
+    # key pass, and the chunk-major forward and fused backward)
+    "C1062_S16_f32": (Shape(1, 17000, 2, 1, 64, 16, 4, "f32"), 23, "iid"),
+    "C1040_bf16": (Shape(1, 66560, 8, 1, 128, 64, 2, "bf16"), 24, "iid"),
 }
 
 _cache = {}
