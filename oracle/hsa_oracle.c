@@ -3,7 +3,7 @@
  *
  * Written from the paper's definitions (arXiv 2504.16795, Sec. 3.1 chunk-selection
  * equation, Sec. 3.1.1 chunk weights and hierarchical attention, Sec. 3.1.2 two-phase
- * backward) with the readings listed in the design doc:
+ * backward), with these readings where the paper is silent or ambiguous:
  *   - candidates are the chunks strictly before the token's own chunk;
  *   - the group score uses the concatenated group query against the tiled landmark,
  *     i.e. alpha * (sum_j q_j) . Kbar_c;
