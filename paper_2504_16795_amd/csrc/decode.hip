@@ -681,11 +681,21 @@ __global__ __launch_bounds__(kFinThreads) void decode_attend_slot(
             wait_loads_le<0>();
 #pragma unroll
             for (int ks2 = 0; ks2 < KS2; ++ks2) {
-                const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
+                // w P as a bf16 pair hi + lo (about 16 bits), as in the forward
+                f32x4_t pa, pc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pa[i] = z[2 * ks2][i] * scale;
+                    pc[i] = z[2 * ks2 + 1][i] * scale;
+                }
+                bf16x8_t ph, pl;
+                split8(pa, pc, ph, pl);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
                     const __bf16* pv = vst + toff[db] + 32 * ks2 * DD;
-                    acc[db] = mfma16(cat(ld_tr16(pv), ld_tr16(pv + 16 * DD)), pb, acc[db]);
+                    const bf16x8_t vt = cat(ld_tr16(pv), ld_tr16(pv + 16 * DD));
+                    acc[db] = mfma16(vt, ph, acc[db]);
+                    acc[db] = mfma16(vt, pl, acc[db]);
                 }
             }
         }

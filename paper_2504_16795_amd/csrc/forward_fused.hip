@@ -10,7 +10,8 @@
 //     each wave reduces its 16 keys per row (max m_w of the scaled logits, sum of
 //     exp(z - m_w)); the four waves' values are exchanged through LDS and combined into
 //     P = softmax over the chunk's 64 keys
-//     (W P)^T [64 keys x 32 rows] is staged in LDS (bf16), W the token's weight for c
+//     (W P)^T [64 keys x 32 rows] is staged in LDS as a bf16 pair hi + lo, W the token's
+//     weight for c
 //     (summed over slots repeating c); wave w forms
 //     O_c^T [d 32 w .. 32 w + 31 x 32 rows] = V_c^T (W P)^T                 (MFMA)
 //     and stores it (bf16) at the (token, slot, head) of the token's first slot holding c.
@@ -57,7 +58,8 @@ __host__ __device__ inline FwdWs fwd_ws(const Dims& dm) {
 struct SmemO {
     __bf16 st[ONST][32 * D];        // Q rows of a group, swizzled; stages 0, 1 hold the
                                     // chunk's V rows while V^T is read
-    __bf16 pt[CS * 32];             // (W P)^T of a group: [key][row], see zpos
+    __bf16 pt[2][CS * 32];          // (W P)^T of a group as a bf16 pair hi, lo: [key][row],
+                                    // see zpos
     float stat[NW][2][32];          // per wave and row: m_w, sum exp
     float fac[NW][32];              // per wave and row: P scale of the wave's keys
     int list[FLIST];                // token; then its first Q row, (b L + t) H + g h
@@ -155,12 +157,15 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-                for (int ks2 = 0; ks2 < 2; ++ks2) {
-                    const __bf16* zp = sm.pt + zb[rt] + 1024 * ks2;
-                    const bf16x8_t bp = cat(ld_tr16(zp), ld_tr16(zp + 512));
+                for (int ks2 = 0; ks2 < 2; ++ks2)
 #pragma unroll
-                    for (int dt = 0; dt < 2; ++dt) oa[dt][rt] = mfma16(vT[dt][ks2], bp, oa[dt][rt]);
-                }
+                    for (int hl = 0; hl < 2; ++hl) {
+                        const __bf16* zp = sm.pt[hl] + zb[rt] + 1024 * ks2;
+                        const bf16x8_t bp = cat(ld_tr16(zp), ld_tr16(zp + 512));
+#pragma unroll
+                        for (int dt = 0; dt < 2; ++dt)
+                            oa[dt][rt] = mfma16(vT[dt][ks2], bp, oa[dt][rt]);
+                    }
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
@@ -293,9 +298,20 @@ __global__ __launch_bounds__(NT, 3) void fwd_chunk_mfma(
                     const f32x4_t fv = *reinterpret_cast<const f32x4_t*>(&sm.fac[wave][16 * rb + 4 * grp]);
                     const int li = gi * 4 + 2 * rb + (grp >> 1);
                     const float wt = li < nl ? sm.lw[li] : 0.f;
-                    *reinterpret_cast<bf16x4_t*>(sm.pt + zpos(j, 4 * rb + grp)) =
-                        bf16x4_t{f2bf(wt * e[rb][0] * fv[0]), f2bf(wt * e[rb][1] * fv[1]),
-                                 f2bf(wt * e[rb][2] * fv[2]), f2bf(wt * e[rb][3] * fv[3])};
+                    // as a bf16 pair hi + lo (about 16 bits): one bf16 rounding of each
+                    // weighted probability would leave an error of up to 2^-9 of it in O
+                    f32x4_t x, x0;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        x[i] = wt * e[rb][i] * fv[i];
+                        x0[i] = 0.f;
+                    }
+                    bf16x8_t h8, l8;
+                    split8(x, x0, h8, l8);
+                    *reinterpret_cast<bf16x4_t*>(sm.pt[0] + zpos(j, 4 * rb + grp)) =
+                        bf16x4_t{h8[0], h8[1], h8[2], h8[3]};
+                    *reinterpret_cast<bf16x4_t*>(sm.pt[1] + zpos(j, 4 * rb + grp)) =
+                        bf16x4_t{l8[0], l8[1], l8[2], l8[3]};
                 }
             };
             static_assert(ONST == 3, "the group loop is unrolled by the ring depth");

@@ -12,8 +12,9 @@
 //  3. For each of its row blocks whose tokens selected the chunk (wave-uniform test), a wave
 //     runs
 //        Z^T [S x 16] = K_c [S x d] . Q^T [d x 16]        (S/16 * 4 MFMAs)
-//        P^T = softmax over keys, scaled by w_{t,c} (0 for the row block's other token)
-//        O^T [d x 16] += V_c^T [d x S] . P^T [S x 16]     (8 * S/32 MFMAs)
+//        P^T = softmax over keys, scaled by w_{t,c} (0 for the row block's other token),
+//              as a bf16 pair hi + lo
+//        O^T [d x 16] += V_c^T [d x S] . P^T [S x 16]     (2 * 8 * S/32 MFMAs)
 //     The C layout of Z^T feeds P^T straight into the B operand of the second product with
 //     a key permutation applied to the V^T fragments, which come from transposed LDS
 //     reads of the row-major V tile.  Q^T lives in registers for the whole kernel and O^T
@@ -198,11 +199,22 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
             // O^T += V^T P^T
 #pragma unroll
             for (int ks2 = 0; ks2 < KS2; ++ks2) {
-                const bf16x8_t pb = pack8(z[2 * ks2], z[2 * ks2 + 1], scale);
+                // w P as a bf16 pair hi + lo (about 16 bits): one bf16 rounding of each
+                // weighted probability would leave an error of up to 2^-9 of it in O
+                f32x4_t pa, pc;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pa[i] = z[2 * ks2][i] * scale;
+                    pc[i] = z[2 * ks2 + 1][i] * scale;
+                }
+                bf16x8_t ph, pl;
+                split8(pa, pc, ph, pl);
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
                     const __bf16* p = cs.v + toff[db] + 32 * ks2 * D;
-                    acc[r][db] = mfma16(cat(ld_tr16(p), ld_tr16(p + 16 * D)), pb, acc[r][db]);
+                    const bf16x8_t vt = cat(ld_tr16(p), ld_tr16(p + 16 * D));
+                    acc[r][db] = mfma16(vt, ph, acc[r][db]);
+                    acc[r][db] = mfma16(vt, pl, acc[r][db]);
                 }
             }
             if (mine) {

@@ -37,10 +37,6 @@ __device__ __forceinline__ bf16x4_t ld_bf16x4(const void* p) {
 __device__ __forceinline__ bf16x8_t cat(const bf16x4_t& a, const bf16x4_t& b) {
     return bf16x8_t{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
 }
-__device__ __forceinline__ bf16x8_t pack8(const f32x4_t& a, const f32x4_t& b, float s) {
-    return bf16x8_t{f2bf(a[0] * s), f2bf(a[1] * s), f2bf(a[2] * s), f2bf(a[3] * s),
-                    f2bf(b[0] * s), f2bf(b[1] * s), f2bf(b[2] * s), f2bf(b[3] * s)};
-}
 
 // Reductions over the four lanes l, l^16, l^32, l^48 that hold one column of a C layout,
 // with the gfx950 lane-swap instructions (no LDS traffic): a swap of v with itself returns

@@ -14,10 +14,11 @@ Tolerances (fixed in advance, independent of the measured error):
     tests that inject unnormalised weights of their own skip it (contract=False);
   - bf16 mode, in addition, element-wise bounds that follow the rounding steps:
       attention outputs O: |got - ref| <= 2^-8 (O_abs + |ref|), with
-      O_abs = sum_i |w_i| sum_s P_s |V_s| (the same operator applied to |V| and |w|): the
-      bf16 kernels round the weighted probabilities w P / sum to bf16 (relative error <=
-      2^-9) and the output once (<= 2^-9 |O|); every other step is fp32 on exact bf16
-      products, and the bound is that error sum with a factor-2 margin;
+      O_abs = sum_i |w_i| sum_s P_s |V_s| (the same operator applied to |V| and |w|): a
+      bf16 rounding of the weighted probabilities w P / sum (relative error <= 2^-9) and
+      one of the output (<= 2^-9 |O|), every other step fp32 on exact bf16 products, and a
+      factor-2 margin (the kernels carry w P as a bf16 pair hi + lo, so their error stays
+      well inside it);
       gradients: |got - ref| <= 2e-2 * RMS(ref) + 2^-8 * |ref|;
   - selected chunk indices: bit-exact for every token whose oracle top-k score gap is
     >= 1e-3; below that gap, a valid selection: the right count, distinct, descending,

@@ -31,6 +31,8 @@ CASES = {
     "ragged_mfma_bf16": (Shape(1, 1000, 16, 2, 128, 64, 8, "bf16"), 16, "iid"),
     "wide_k16_bf16": (Shape(1, 2304, 32, 4, 128, 128, 16, "bf16"), 17, "lowrank"),
     "k24_bf16": (Shape(1, 2048, 16, 2, 128, 32, 24, "bf16"), 18, "iid"),
+    # the largest k (32 slots: the widest selection lists, slot tables and dQ completion)
+    "k32_bf16": (Shape(1, 2560, 16, 2, 128, 64, 32, "bf16"), 25, "iid"),
     "k20_d64_f32": (Shape(1, 1500, 4, 2, 64, 32, 20, "f32"), 19, "iid"),
     # float32 with d = 128 (the largest float32 chunk: S d = 8192), generic kernels
     "f32_d128": (Shape(1, 1024, 8, 2, 128, 64, 4, "f32"), 22, "iid"),
