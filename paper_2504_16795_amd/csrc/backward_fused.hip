@@ -739,7 +739,7 @@ __global__ __launch_bounds__(NT) void bwd_lmk_stream(
     Dims dm, const int* __restrict__ pairsel, const float* __restrict__ dsm,
     const __bf16* __restrict__ qsum, const int* __restrict__ gstart, const int* __restrict__ cntr,
     const int* __restrict__ plan, float* __restrict__ dkbar, float* __restrict__ pkb) {
-    constexpr int U = 16;                     // pairs per lane group in flight
+    constexpr int U = 4;                      // pairs per lane group in flight
     constexpr int SEG = 2048;                 // pair records staged in LDS at once
     __shared__ float4 red[8][32];
     __shared__ int sels[SEG];
@@ -772,20 +772,27 @@ __global__ __launch_bounds__(NT) void bwd_lmk_stream(
             for (int p = j8; p < qn; p += 8 * U) {
                 float cf[U];
                 float4 q[U];
+                // positions past the segment's end load the segment's last record (a real
+                // row, so no address is shared by every workgroup) and add 0
+                bool live[U];
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    const int sel = (p + 8 * u < qn) ? sels[p + 8 * u] : -1;
-                    const int qr = max(sel, 0) >> 5;             // the token's q~ row
-                    cf[u] = sel >= 0 ? dsm[(size_t)qr * k + (sel & 31)] : 0.f;
+                    const int pu = p + 8 * u;
+                    const int sel = sels[min(pu, qn - 1)];
+                    live[u] = pu < qn && sel >= 0;
+                    const int su = max(sel, 0);
+                    const int qr = su >> 5;                      // the token's q~ row
+                    cf[u] = dsm[(size_t)qr * k + (su & 31)];
                     const bf16x4_t qv = ld_bf16x4(qsum + (size_t)qr * D + 4 * c4);
                     q[u] = float4{(float)qv[0], (float)qv[1], (float)qv[2], (float)qv[3]};
                 }
 #pragma unroll
                 for (int u = 0; u < U; ++u) {
-                    acc.x = fmaf(cf[u], q[u].x, acc.x);
-                    acc.y = fmaf(cf[u], q[u].y, acc.y);
-                    acc.z = fmaf(cf[u], q[u].z, acc.z);
-                    acc.w = fmaf(cf[u], q[u].w, acc.w);
+                    const float c = live[u] ? cf[u] : 0.f;
+                    acc.x = fmaf(c, q[u].x, acc.x);
+                    acc.y = fmaf(c, q[u].y, acc.y);
+                    acc.z = fmaf(c, q[u].z, acc.z);
+                    acc.w = fmaf(c, q[u].w, acc.w);
                 }
             }
         }
