@@ -36,7 +36,7 @@ constexpr int KMAX = 32;
 constexpr int ONST = 3;             // LDS stages of the group ring (Q rows only)
 constexpr int OBPW = 8 / NW;        // 1 KB row blocks of Q copied per wave and group
 constexpr int kOStores = 2;         // global stores per lane of one output step (16 B each)
-constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (42 KB of LDS each)
+constexpr int kFwdWGs = 768;        // workgroups of the split: three per CU (46 KB of LDS each)
 
 struct FwdWs {
     size_t bitmap, cnt, gstart, plan, part, end;
