@@ -209,12 +209,20 @@ __global__ __launch_bounds__(FCfg<S>::NW * 64, FCfg<S>::WPE) void forward_mfma(
                 }
                 bf16x8_t ph, pl;
                 split8(pa, pc, ph, pl);
+                // in halves of 4 column blocks: the hi products, then the lo ones, so that no
+                // product waits for the one just before it
 #pragma unroll
-                for (int db = 0; db < 8; ++db) {
-                    const __bf16* p = cs.v + toff[db] + 32 * ks2 * D;
-                    const bf16x8_t vt = cat(ld_tr16(p), ld_tr16(p + 16 * D));
-                    acc[r][db] = mfma16(vt, ph, acc[r][db]);
-                    acc[r][db] = mfma16(vt, pl, acc[r][db]);
+                for (int d0 = 0; d0 < 8; d0 += 4) {
+                    bf16x8_t vt[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const __bf16* p = cs.v + toff[d0 + j] + 32 * ks2 * D;
+                        vt[j] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[r][d0 + j] = mfma16(vt[j], ph, acc[r][d0 + j]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[r][d0 + j] = mfma16(vt[j], pl, acc[r][d0 + j]);
                 }
             }
             if (mine) {
