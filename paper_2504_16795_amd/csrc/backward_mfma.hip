@@ -223,12 +223,20 @@ __global__ __launch_bounds__(QCfg<S>::NW * 64, 2) void bwd_q_mfma(
             for (int ks2 = 0; ks2 < KS2; ++ks2) {
                 bf16x8_t zh, zl;
                 split8(z[2 * ks2], z[2 * ks2 + 1], zh, zl);
+                // in halves of 4 column blocks: the hi products, then the lo ones, so that no
+                // product waits for the one just before it
 #pragma unroll
-                for (int db = 0; db < 8; ++db) {
-                    const __bf16* p = cs.k + toff[db] + 32 * ks2 * D;
-                    const bf16x8_t a = cat(ld_tr16(p), ld_tr16(p + 16 * D));
-                    acc[db] = mfma16(a, zh, acc[db]);
-                    acc[db] = mfma16(a, zl, acc[db]);
+                for (int d0 = 0; d0 < 8; d0 += 4) {
+                    bf16x8_t a[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const __bf16* p = cs.k + toff[d0 + j] + 32 * ks2 * D;
+                        a[j] = cat(ld_tr16(p), ld_tr16(p + 16 * D));
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[d0 + j] = mfma16(a[j], zh, acc[d0 + j]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[d0 + j] = mfma16(a[j], zl, acc[d0 + j]);
                 }
             }
             // statistics of this (token, slot, head) and dw of the token
@@ -511,15 +519,17 @@ __global__ __launch_bounds__(S * 4, 2) void bwd_kv_mfma(
                 bf16x8_t pvh, pvl, dzh, dzl;
                 split8(pw[0], pw[1], pvh, pvl);
                 split8(dz[0], dz[1], dzh, dzl);
+                // per column block the hi products of dV and dK, then their lo ones, so that
+                // no product waits for the one just before it
 #pragma unroll
                 for (int db = 0; db < 8; ++db) {
                     const bf16x8_t gb =
                         cat(ld_tr16(st.g + toff[db]), ld_tr16(st.g + toff[db] + 16 * D));
-                    aV[db] = mfma16(pvh, gb, aV[db]);
-                    aV[db] = mfma16(pvl, gb, aV[db]);
                     const bf16x8_t qb =
                         cat(ld_tr16(st.q + toff[db]), ld_tr16(st.q + toff[db] + 16 * D));
+                    aV[db] = mfma16(pvh, gb, aV[db]);
                     aK[db] = mfma16(dzh, qb, aK[db]);
+                    aV[db] = mfma16(pvl, gb, aV[db]);
                     aK[db] = mfma16(dzl, qb, aK[db]);
                 }
             };
