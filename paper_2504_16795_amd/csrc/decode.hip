@@ -690,12 +690,19 @@ __global__ __launch_bounds__(kFinThreads) void decode_attend_slot(
                 }
                 bf16x8_t ph, pl;
                 split8(pa, pc, ph, pl);
+                // in halves of 4 column blocks: the hi products, then the lo ones
 #pragma unroll
-                for (int db = 0; db < 8; ++db) {
-                    const __bf16* pv = vst + toff[db] + 32 * ks2 * DD;
-                    const bf16x8_t vt = cat(ld_tr16(pv), ld_tr16(pv + 16 * DD));
-                    acc[db] = mfma16(vt, ph, acc[db]);
-                    acc[db] = mfma16(vt, pl, acc[db]);
+                for (int d0 = 0; d0 < 8; d0 += 4) {
+                    bf16x8_t vt[4];
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const __bf16* pv = vst + toff[d0 + j] + 32 * ks2 * DD;
+                        vt[j] = cat(ld_tr16(pv), ld_tr16(pv + 16 * DD));
+                    }
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[d0 + j] = mfma16(vt[j], ph, acc[d0 + j]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[d0 + j] = mfma16(vt[j], pl, acc[d0 + j]);
                 }
             }
         }
