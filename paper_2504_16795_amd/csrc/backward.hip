@@ -296,10 +296,17 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
                     const int s = lane + 64 * u;
                     float a = 0.f, bb = 0.f;
                     if (s < CS) {
-                        for (int e = 0; e < D; ++e) {
-                            a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
-                            bb = fmaf(gf[j * D + e], to_f32(Vs[s * KP + e]), bb);
+                        // four partial sums each, so the products do not wait on one another
+                        float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
+                        for (int e = 0; e < D; e += 4) {
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
+                                b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
+                            }
                         }
+                        a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                        bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
                         z[u] = dm.beta * a;
                     } else {
                         z[u] = -INFINITY;
@@ -328,17 +335,40 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
                 dkbar = fmaf(dm.alpha * dst, qs, dkbar);
             }
             __syncthreads();
+            // a thread's elements share their column when kThreads is a multiple of D: the
+            // token's q and dO values of that column are read once per head
+            if constexpr (kThreads % D == 0) {
+                const int e = tid % D;
+                float av[NE], ak[NE];
 #pragma unroll
-            for (int r = 0; r < NE; ++r) {
-                const int i = tid + r * kThreads;
-                const int s = i / D, e = i % D;
-                float av = 0.f, ak = 0.f;
+                for (int r = 0; r < NE; ++r) av[r] = ak[r] = 0.f;
                 for (int j = 0; j < h; ++j) {
-                    av = fmaf(pw[j * CS + s], gf[j * D + e], av);
-                    ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
+                    const float gv = gf[j * D + e], qv = qf[j * D + e];
+#pragma unroll
+                    for (int r = 0; r < NE; ++r) {
+                        const int s = (tid + r * kThreads) / D;
+                        av[r] = fmaf(pw[j * CS + s], gv, av[r]);
+                        ak[r] = fmaf(dz[j * CS + s], qv, ak[r]);
+                    }
                 }
-                aV[r] += av;
-                aK[r] = fmaf(dm.beta, ak, aK[r]);
+#pragma unroll
+                for (int r = 0; r < NE; ++r) {
+                    aV[r] += av[r];
+                    aK[r] = fmaf(dm.beta, ak[r], aK[r]);
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < NE; ++r) {
+                    const int i = tid + r * kThreads;
+                    const int s = i / D, e = i % D;
+                    float av = 0.f, ak = 0.f;
+                    for (int j = 0; j < h; ++j) {
+                        av = fmaf(pw[j * CS + s], gf[j * D + e], av);
+                        ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
+                    }
+                    aV[r] += av;
+                    aK[r] = fmaf(dm.beta, ak, aK[r]);
+                }
             }
         }
     }
