@@ -92,10 +92,17 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
                 const int s = lane + 64 * u;
                 float a = 0.f, bb = 0.f;
                 if (s < S) {
-                    for (int e = 0; e < D; ++e) {
-                        a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
-                        bb = fmaf(gf[j * D + e], to_f32(Vs[s * KP + e]), bb);
+                    // four partial sums each, so the products do not wait on one another
+                    float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
+                    for (int e = 0; e < D; e += 4) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) {
+                            a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
+                            b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
+                        }
                     }
+                    a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                    bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
                     z[u] = dm.beta * a;
                 } else {
                     z[u] = -INFINITY;
@@ -124,9 +131,13 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
             const int i = tid + r * kThreads;
             if (i < h * D) {
                 const int j = i / D, e = i % D;
-                float a = 0.f;
-                for (int s = 0; s < S; ++s) a = fmaf(dz[j * SMAX + s], to_f32(Ks[s * KP + e]), a);
-                acc[r] = fmaf(dm.beta, a, acc[r]);
+                float a4[4] = {0.f, 0.f, 0.f, 0.f};   // S is a multiple of 4
+                for (int s = 0; s < S; s += 4) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        a4[q] = fmaf(dz[j * SMAX + s + q], to_f32(Ks[(s + q) * KP + e]), a4[q]);
+                }
+                acc[r] = fmaf(dm.beta, (a4[0] + a4[1]) + (a4[2] + a4[3]), acc[r]);
             }
         }
     }

@@ -72,10 +72,15 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
 #pragma unroll
             for (int u = 0; u < 2; ++u) {
                 const int s = lane + 64 * u;
-                float a = 0.f;
                 if (s < S) {
-                    for (int e = 0; e < D; ++e) a = fmaf(qf[j * D + e], to_f32(Ks[s * KP + e]), a);
-                    z[u] = dm.beta * a;
+                    // four partial sums, so the products do not wait on one another
+                    float a4[4] = {0.f, 0.f, 0.f, 0.f};
+                    for (int e = 0; e < D; e += 4) {
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
+                    }
+                    z[u] = dm.beta * ((a4[0] + a4[1]) + (a4[2] + a4[3]));
                 } else {
                     z[u] = -INFINITY;
                 }
@@ -93,9 +98,13 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
             const int i = tid + r * kThreads;
             if (i < h * D) {
                 const int j = i / D, e = i % D;
-                float a = 0.f;
-                for (int s = 0; s < S; ++s) a = fmaf(p[j * SMAX + s], to_f32(Vs[s * D + e]), a);
-                acc[r] += a;
+                float a4[4] = {0.f, 0.f, 0.f, 0.f};   // S is a multiple of 4
+                for (int s = 0; s < S; s += 4) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        a4[q] = fmaf(p[j * SMAX + s + q], to_f32(Vs[(s + q) * D + e]), a4[q]);
+                }
+                acc[r] += (a4[0] + a4[1]) + (a4[2] + a4[3]);
             }
         }
     }
