@@ -428,11 +428,12 @@ __global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nspli
 
 // Splits of the generic key pass: enough workgroups to fill the chip when the chunks are
 // few (each chunk's tokens are otherwise walked by one workgroup, one after another), at
-// most 16.
+// most 32 (tiny fp32 workload: 32 splits 135 us with the finish, 16 splits 176, 64 splits
+// 185, the finish then summing too many partials).
 inline int kv_splits(const Dims& dm) {
     const long rows = (long)dm.B * dm.G * dm.Call;
     long n = rows > 0 ? (1024 + rows - 1) / rows : 1;
-    return (int)(n < 1 ? 1 : (n > 16 ? 16 : n));
+    return (int)(n < 1 ? 1 : (n > 32 ? 32 : n));
 }
 
 template <typename T, int D, int CS>
