@@ -15,6 +15,8 @@
 // workgroup and summed in a fixed order, so results are bitwise reproducible.
 //
 // The MFMA path for the main bf16 shapes lives in backward_mfma.hip.
+#include <type_traits>
+
 #include "common.h"
 
 namespace hsa {
@@ -35,24 +37,23 @@ hipError_t launch_backward_mfma(const Dims& dm, const void* Q, const void* K, co
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int SMAX = 128;
 constexpr int HMAX = 16;
 constexpr int KMAX = 32;
 
 __host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-template <typename T, int D>
+template <typename T, int D, int CS>
 __global__ __launch_bounds__(kThreads) void bwd_q_generic(
     Dims dm, const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const float* __restrict__ Kbar, const int32_t* __restrict__ idx, const float* __restrict__ w,
     const T* __restrict__ dO, T* __restrict__ dQ, float* __restrict__ ds_out) {
     constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
     constexpr int NACC = HMAX * D / kThreads;
-    __shared__ T Ks[SMAX * KP];
-    __shared__ T Vs[SMAX * KP];
+    __shared__ T Ks[CS * KP];
+    __shared__ T Vs[CS * KP];
     __shared__ float qf[HMAX * D];
     __shared__ float gf[HMAX * D];
-    __shared__ float dz[HMAX * SMAX];
+    __shared__ float dz[HMAX * CS];
     __shared__ float Dl[HMAX];
     __shared__ float dwl[KMAX];
 
@@ -116,8 +117,8 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
             p0 *= inv;
             p1 *= inv;
             const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
-            if (lane < S) dz[j * SMAX + lane] = wi * p0 * (dp[0] - Dj);
-            if (lane + 64 < S) dz[j * SMAX + lane + 64] = wi * p1 * (dp[1] - Dj);
+            if (lane < S) dz[j * CS + lane] = wi * p0 * (dp[0] - Dj);
+            if (lane + 64 < S) dz[j * CS + lane + 64] = wi * p1 * (dp[1] - Dj);
             if (lane == 0) Dl[j] = Dj;
         }
         __syncthreads();
@@ -135,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
                 for (int s = 0; s < S; s += 4) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        a4[q] = fmaf(dz[j * SMAX + s + q], to_f32(Ks[(s + q) * KP + e]), a4[q]);
+                        a4[q] = fmaf(dz[j * CS + s + q], to_f32(Ks[(s + q) * KP + e]), a4[q]);
                 }
                 acc[r] = fmaf(dm.beta, (a4[0] + a4[1]) + (a4[2] + a4[3]), acc[r]);
             }
@@ -506,15 +507,23 @@ hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
                     void* dQ, void* dK, void* dV, void* ws, hipStream_t st) {
     float* ds = (float*)ws;
     dim3 g1(dm.L, dm.B * dm.G);
-    if (dm.d == 128) {
+    // LDS sized for the chunk (so short chunks leave room for more workgroups per CU)
+    auto q_pass = [&](auto dc, auto sc) {
+        constexpr int DD = decltype(dc)::value, SS = decltype(sc)::value;
         HSA_TIMED("bwd_q_generic", st);
-        hipLaunchKernelGGL((bwd_q_generic<T, 128>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
+        hipLaunchKernelGGL((bwd_q_generic<T, DD, SS>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
                            (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
-    } else {
-        HSA_TIMED("bwd_q_generic", st);
-        hipLaunchKernelGGL((bwd_q_generic<T, 64>), g1, dim3(kThreads), 0, st, dm, (const T*)Q,
-                           (const T*)K, (const T*)V, Kbar, idx, w, (const T*)dO, (T*)dQ, ds);
-    }
+    };
+    auto q_pass_s = [&](auto dc) {
+        switch (dm.S) {
+            case 16: q_pass(dc, std::integral_constant<int, 16>{}); break;
+            case 32: q_pass(dc, std::integral_constant<int, 32>{}); break;
+            case 64: q_pass(dc, std::integral_constant<int, 64>{}); break;
+            default: q_pass(dc, std::integral_constant<int, 128>{}); break;
+        }
+    };
+    if (dm.d == 128) q_pass_s(std::integral_constant<int, 128>{});
+    else q_pass_s(std::integral_constant<int, 64>{});
     launch_kv_pass<T>(dm, Q, K, V, idx, w, dO, dK, dV, ws, st);
     return hipGetLastError();
 }

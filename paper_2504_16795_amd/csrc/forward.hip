@@ -9,6 +9,8 @@
 // The bf16 MFMA paths for the main shapes live in forward_mfma.hip (tile-major) and
 // forward_fused.hip (chunk-major, for sequences with many chunks); launch_forward selects
 // them when they apply.
+#include <type_traits>
+
 #include "common.h"
 
 namespace hsa {
@@ -26,10 +28,9 @@ hipError_t launch_forward_mfma(const Dims& dm, const void* Q, const void* K, con
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int SMAX = 128;
 constexpr int HMAX = 16;
 
-template <typename T, int D>
+template <typename T, int D, int CS>
 __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __restrict__ Q,
                                                             const T* __restrict__ K,
                                                             const T* __restrict__ V,
@@ -38,10 +39,10 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
                                                             T* __restrict__ O) {
     constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
     constexpr int NACC = HMAX * D / kThreads;
-    __shared__ T Ks[SMAX * KP];
-    __shared__ T Vs[SMAX * D];
+    __shared__ T Ks[CS * KP];
+    __shared__ T Vs[CS * D];
     __shared__ float qf[HMAX * D];
-    __shared__ float p[HMAX * SMAX];
+    __shared__ float p[HMAX * CS];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int t = blockIdx.x;
@@ -89,8 +90,8 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
             if (dm.off1) m = fmaxf(m, 0.f);
             const float e0 = expf(z[0] - m), e1 = expf(z[1] - m);
             const float scale = wi / (wave_sum(e0 + e1) + (dm.off1 ? expf(-m) : 0.f));
-            if (lane < S) p[j * SMAX + lane] = e0 * scale;
-            if (lane + 64 < S) p[j * SMAX + lane + 64] = e1 * scale;
+            if (lane < S) p[j * CS + lane] = e0 * scale;
+            if (lane + 64 < S) p[j * CS + lane + 64] = e1 * scale;
         }
         __syncthreads();
 #pragma unroll
@@ -102,7 +103,7 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
                 for (int s = 0; s < S; s += 4) {
 #pragma unroll
                     for (int q = 0; q < 4; ++q)
-                        a4[q] = fmaf(p[j * SMAX + s + q], to_f32(Vs[(s + q) * D + e]), a4[q]);
+                        a4[q] = fmaf(p[j * CS + s + q], to_f32(Vs[(s + q) * D + e]), a4[q]);
                 }
                 acc[r] += (a4[0] + a4[1]) + (a4[2] + a4[3]);
             }
@@ -119,15 +120,23 @@ template <typename T>
 hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
                     const int32_t* idx, const float* w, void* O, hipStream_t st) {
     dim3 grid(dm.L, dm.B * dm.G);
-    if (dm.d == 128) {
+    // LDS sized for the chunk (so short chunks leave room for more workgroups per CU)
+    auto fwd = [&](auto dc, auto sc) {
+        constexpr int DD = decltype(dc)::value, SS = decltype(sc)::value;
         HSA_TIMED("forward_generic", st);
-        hipLaunchKernelGGL((forward_generic<T, 128>), grid, dim3(kThreads), 0, st, dm,
+        hipLaunchKernelGGL((forward_generic<T, DD, SS>), grid, dim3(kThreads), 0, st, dm,
                            (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
-    } else {
-        HSA_TIMED("forward_generic", st);
-        hipLaunchKernelGGL((forward_generic<T, 64>), grid, dim3(kThreads), 0, st, dm,
-                           (const T*)Q, (const T*)K, (const T*)V, idx, w, (T*)O);
-    }
+    };
+    auto fwd_s = [&](auto dc) {
+        switch (dm.S) {
+            case 16: fwd(dc, std::integral_constant<int, 16>{}); break;
+            case 32: fwd(dc, std::integral_constant<int, 32>{}); break;
+            case 64: fwd(dc, std::integral_constant<int, 64>{}); break;
+            default: fwd(dc, std::integral_constant<int, 128>{}); break;
+        }
+    };
+    if (dm.d == 128) fwd_s(std::integral_constant<int, 128>{});
+    else fwd_s(std::integral_constant<int, 64>{});
     return hipGetLastError();
 }
 
