@@ -46,15 +46,19 @@ __device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
 }
 
 // ND: slices of 128 columns (d = 128 ND); QLO: the query is a sum over h > 1 heads (fp32,
-// so it enters as a bf16 hi / lo pair); otherwise it is one bf16 row, exact.
-template <int KC, int ND, bool QLO>
-__global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __restrict__ Q,
+// so it enters as a bf16 hi / lo pair); otherwise it is one bf16 row, exact.  NSTG: LDS
+// stages; with a single stage (every tile's candidates fit one block of 64 chunks and one
+// column slice) a workgroup takes 32 KB of LDS and at most 128 VGPRs, so four workgroups
+// share a CU and their load and compute phases overlap.
+template <int KC, int ND, bool QLO, int NSTG>
+__global__ __launch_bounds__(kNT, NSTG == 1 ? 4 : 2) void select_mfma(Dims dm, const __bf16* __restrict__ Q,
                                                       const float* __restrict__ Kbar,
                                                       int32_t* __restrict__ idx,
                                                       float* __restrict__ w, int ntiles) {
     static_assert(ND == 1 || !QLO, "a head sum needs d = 128");
     constexpr int DD = D * ND;         // the query / landmark row length
-    __shared__ SelStage st[2];
+    static_assert(NSTG == 1 || NSTG == 2, "one stage or a double buffer");
+    __shared__ SelStage st[NSTG];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
     const int nbg = dm.B * dm.G;
@@ -102,8 +106,9 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     const int nblk = cdiv(nwg, kCB);
     const int nst = nblk * ND;         // stages: (candidate block, column slice)
     // the first block's landmark loads go out before the query loads (independent of
-    // them), so both latencies overlap
-    if (nblk > 0) load_block(0);
+    // them), so both latencies overlap; with a single stage they follow the query sum
+    // (the registers they need are then free)
+    if (NSTG == 2 && nblk > 0) load_block(0);
 
     // B operand: q~ of the wave's 16 tokens as bf16 hi / lo; the lane holds d = 128 db +
     // 32 ks + 8 grp + i of token `row` (a token past the end reads the last one; unused)
@@ -122,19 +127,20 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
             for (int i = 0; i < 8; ++i) qs[ks][i] = 0.f;
         const __bf16* qp = Q + (((size_t)b * dm.L + min(t, dm.L - 1)) * dm.H + (size_t)g * dm.h) * D +
                            8 * grp;
-        // 8 heads at a time: all 32 loads are issued (head index clamped, branch-free)
-        // before the first sum, so the wave waits for one round trip per 8 heads rather
-        // than one per head
-        for (int j0 = 0; j0 < dm.h; j0 += 8) {
-            bf16x8_t v[8][4];
+        // HB heads at a time: all their loads are issued (head index clamped, branch-free)
+        // before the first sum, so the wave waits for one round trip per HB heads rather
+        // than one per head (HB = 4 within the single-stage register budget)
+        constexpr int HB = NSTG == 1 ? 4 : 8;
+        for (int j0 = 0; j0 < dm.h; j0 += HB) {
+            bf16x8_t v[HB][4];
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj)
+            for (int jj = 0; jj < HB; ++jj)
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks)
                     v[jj][ks] = ld_bf16x8(qp + (size_t)min(j0 + jj, dm.h - 1) * D + 32 * ks);
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int jj = 0; jj < 8; ++jj) {
+            for (int jj = 0; jj < HB; ++jj) {
                 const bool use = j0 + jj < dm.h;     // a select, so no load is sunk
 #pragma unroll
                 for (int ks = 0; ks < 4; ++ks)
@@ -162,6 +168,7 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
     int koff[4];
     row_read_offsets(lane, koff);
     const float alpha = dm.alpha;
+    if (NSTG == 1 && nblk > 0) load_block(0);
     if (nblk > 0) store_block(0);
     constexpr int MB = kCB / 16;
     for (int blk = 0; blk < nblk; ++blk) {
@@ -174,8 +181,8 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
         for (int db = 0; db < ND; ++db) {
             const int si = blk * ND + db;
             __syncthreads();           // stage si staged; the other stage's readers are done
-            if (si + 1 < nst) load_block(si + 1);
-            const SelStage& sb = st[si & 1];
+            if (NSTG == 2 && si + 1 < nst) load_block(si + 1);
+            const SelStage& sb = st[si & (NSTG - 1)];
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks) {
                 bf16x8_t ah[MB], al[MB];
@@ -193,7 +200,7 @@ __global__ __launch_bounds__(kNT, 2) void select_mfma(Dims dm, const __bf16* __r
 #pragma unroll
                 for (int mb = 0; mb < MB; ++mb) acc[mb] = mfma16(al[mb], qh[db][ks], acc[mb]);
             }
-            if (si + 1 < nst) store_block((si + 1) & 1);
+            if (NSTG == 2 && si + 1 < nst) store_block((si + 1) & (NSTG - 1));
         }
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb) {
@@ -269,8 +276,17 @@ template <int KC, int ND, bool QLO>
 void launch_nd(const Dims& dm, const void* Q, const float* Kbar, int32_t* idx, float* w,
                hipStream_t st) {
     const int ntiles = cdiv(dm.L, kMT);
-    hipLaunchKernelGGL((select_mfma<KC, ND, QLO>), dim3(ntiles * dm.B * dm.G), dim3(kNT), 0, st,
-                       dm, (const __bf16*)Q, Kbar, idx, w, ntiles);
+    const dim3 grid(ntiles * dm.B * dm.G);
+    // one stage when the last token's candidates fit one block (and one column slice)
+    if constexpr (ND == 1 && KC == 8) {
+        if (dm.L > 0 && (dm.L - 1) / dm.S <= kCB) {
+            hipLaunchKernelGGL((select_mfma<KC, ND, QLO, 1>), grid, dim3(kNT), 0, st, dm,
+                               (const __bf16*)Q, Kbar, idx, w, ntiles);
+            return;
+        }
+    }
+    hipLaunchKernelGGL((select_mfma<KC, ND, QLO, 2>), grid, dim3(kNT), 0, st, dm,
+                       (const __bf16*)Q, Kbar, idx, w, ntiles);
 }
 
 template <int KC>
