@@ -43,6 +43,9 @@ CASES = {
     # key pass, and the chunk-major forward and fused backward)
     "C1062_S16_f32": (Shape(1, 17000, 2, 1, 64, 16, 4, "f32"), 23, "iid"),
     "C1040_bf16": (Shape(1, 66560, 8, 1, 128, 64, 2, "bf16"), 24, "iid"),
+    # the most query heads per KV head (16; generic kernels, the selection's head sum in
+    # several load rounds), ragged length
+    "h16_bf16": (Shape(1, 1100, 16, 1, 128, 64, 8, "bf16"), 26, "iid"),
 }
 
 _cache = {}
@@ -408,6 +411,26 @@ def test_select_many_candidates(hsa_gpu, shape):
     sure, loose = assert_indices(idx, idx_ref, gap, shape.S)
     assert loose == 0
     assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= W_ATOL
+
+
+@pytest.mark.parametrize("L", [4160, 4161], ids=["64_candidates", "65_candidates"])
+def test_select_block_boundary(hsa_gpu, L):
+    """The last tokens see exactly 64 candidate chunks (one full block: the selection's
+    single-stage form) or 65 (a second block of one chunk: the double-buffered form)."""
+    shape = Shape(1, L, 16, 2, 128, 64, 8, "bf16")
+    banner("select_L%d" % L, "hsa_select_topk, candidate block boundary")
+    inp, _ = make_case(shape, 43, kind="iid")
+    Kbar_ref = oracle.landmarks(inp["K"], shape.S)
+    idx_ref, w_ref, gap, _ = oracle.select(inp["Q"], Kbar_ref, shape.G, shape.S, shape.k)
+    Q = to_dev(inp["Q"], shape)
+    Kbar = torch.from_numpy(Kbar_ref.astype(np.float32)).cuda()
+    idx, w = hsa_gpu.hsa_select_topk(Q, Kbar, shape.G, shape.S, shape.k)
+    torch.cuda.synchronize()
+    sure, loose = assert_indices(idx, idx_ref, gap, shape.S)
+    assert loose == 0
+    assert np.max(np.abs(w.cpu().numpy() - w_ref)) <= W_ATOL
+    # no index beyond the last candidate: 63 (L = 4160) or 64 (L = 4161)
+    assert int(idx.max()) <= (L - 1) // 64 - 1
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
