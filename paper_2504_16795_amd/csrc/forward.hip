@@ -132,7 +132,11 @@ hipError_t launch_t(const Dims& dm, const void* Q, const void* K, const void* V,
             case 16: fwd(dc, std::integral_constant<int, 16>{}); break;
             case 32: fwd(dc, std::integral_constant<int, 32>{}); break;
             case 64: fwd(dc, std::integral_constant<int, 64>{}); break;
-            default: fwd(dc, std::integral_constant<int, 128>{}); break;
+            default:
+                // float32 with S = 128 and d = 128 is rejected by the argument checks
+                if constexpr (!(sizeof(T) == 4 && decltype(dc)::value == 128))
+                    fwd(dc, std::integral_constant<int, 128>{});
+                break;
         }
     };
     if (dm.d == 128) fwd_s(std::integral_constant<int, 128>{});
