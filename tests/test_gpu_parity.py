@@ -46,6 +46,8 @@ CASES = {
     # the most query heads per KV head (16; generic kernels, the selection's head sum in
     # several load rounds), ragged length
     "h16_bf16": (Shape(1, 1100, 16, 1, 128, 64, 8, "bf16"), 26, "iid"),
+    # one slot: every weight is 1 and the score gradient vanishes (ds = w (dw - w dw) = 0)
+    "k1_bf16": (Shape(1, 1024, 16, 2, 128, 64, 1, "bf16"), 27, "iid"),
 }
 
 _cache = {}
