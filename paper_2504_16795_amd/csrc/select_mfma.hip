@@ -13,8 +13,9 @@
 // as hi.hi + hi.lo + lo.hi, so the scores carry about 16 bits (the dropped lo.lo term is
 // below 2^-16 of each product).  The fp32 landmark rows of a block are loaded with
 // coalesced 16-byte loads (the next block in flight during the current block's products),
-// split into bf16 hi / lo once per workgroup and staged in LDS (double buffer, the row
-// swizzle of chunk_lds.h, conflict-free row reads).
+// split into bf16 hi / lo once per workgroup and staged in LDS (double buffer, or one stage
+// when every tile's candidates fit one block; the row swizzle of chunk_lds.h, conflict-free
+// row reads).
 //
 // In the C layout each lane holds 4 candidates of one token per 16-chunk block and keeps a
 // running top-KC list of its candidates (registers, descending; a candidate moves up past
