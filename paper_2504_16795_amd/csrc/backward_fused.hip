@@ -224,18 +224,24 @@ __global__ __launch_bounds__(NT, 2) void bwd_fused_mfma(
             f32x4_t qa[2][2];
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt) qa[dt][0] = qa[dt][1] = zero4();
+            // both row tiles' operands of a step loaded first: four independent accumulators
+            // between two products on one
 #pragma unroll
-            for (int rt = 0; rt < 2; ++rt)
+            for (int ks2 = 0; ks2 < 2; ++ks2)
 #pragma unroll
-                for (int ks2 = 0; ks2 < 2; ++ks2)
+                for (int hl = 0; hl < 2; ++hl) {
+                    bf16x8_t bz[2];
 #pragma unroll
-                    for (int hl = 0; hl < 2; ++hl) {
+                    for (int rt = 0; rt < 2; ++rt) {
                         const __bf16* zp = sm.dzt[hl] + zb[rt] + 1024 * ks2;
-                        const bf16x8_t bz = cat(ld_tr16(zp), ld_tr16(zp + 512));
+                        bz[rt] = cat(ld_tr16(zp), ld_tr16(zp + 512));
+                    }
+#pragma unroll
+                    for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
                         for (int dt = 0; dt < 2; ++dt)
-                            qa[dt][rt] = mfma16(kT[dt][ks2], bz, qa[dt][rt]);
-                    }
+                            qa[dt][rt] = mfma16(kT[dt][ks2], bz[rt], qa[dt][rt]);
+                }
 #pragma unroll
             for (int rt = 0; rt < 2; ++rt) {
                 const int li = gj * 4 + 2 * rt + (row >> 3);
