@@ -249,6 +249,9 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     __shared__ float pw[HMAX * CS];
     __shared__ float dz[HMAX * CS];
     __shared__ float dkb[D];
+    __shared__ uint32_t wlist[kThreads];
+    __shared__ int tlist[HMAX];          // the tokens of a batch
+    __shared__ float twt[HMAX], tds[HMAX];   // their weights and ds for this chunk
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c = blockIdx.x;
@@ -280,110 +283,140 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     for (int r = 0; r < NE; ++r) aK[r] = aV[r] = 0.f;
     float dkbar = 0.f;   // thread tid < D owns element tid of dKbar
 
-    const uint32_t* row = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
-    int ord = 0;                         // the token's place in the chunk's token list
-    for (int wi = ((c + 1) * CS) >> 5; wi < nwords; ++wi) {
-        uint32_t word = row[wi];
-        while (word) {
-            const int t = wi * 32 + (__ffs(word) - 1);
-            word &= word - 1;
-            if (ord++ % nsplit != z) continue;
-            const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
+    // Tokens are taken TB = floor(HMAX / h) at a time: the batch's (token, head) rows fill
+    // the HMAX-row LDS arrays, so a batch costs the barriers and memory round trips of one
+    // token.
+    const int TB = HMAX / h;
+    auto batch = [&](int n) __attribute__((always_inline)) {
+        const int nrows = n * h;
+        __syncthreads();                  // the previous batch's rows are read
+        for (int i = tid; i < nrows * D; i += kThreads) {
+            const int tk = i / (h * D), r = i - tk * (h * D);
+            const size_t qoff = (((size_t)b * dm.L + tlist[tk]) * dm.H + (size_t)g * h) * D;
+            qf[i] = to_f32(Q[qoff + r]);
+            gf[i] = to_f32(dO[qoff + r]);
+        }
+        if (tid < n) {                    // the token's slot holding c: its w and ds
+            const size_t sel = (((size_t)b * dm.L + tlist[tid]) * dm.G + g) * k;
             int slot = 0;
             for (int i = 0; i < k; ++i)
                 if (idx[sel + i] == c) slot = i;
-            const float wt = w[sel + slot];
-            const float dst = ds[sel + slot];
-            const size_t qoff = (((size_t)b * dm.L + t) * dm.H + (size_t)g * h) * D;
-            __syncthreads();
-            for (int i = tid; i < h * D; i += kThreads) {
-                qf[i] = to_f32(Q[qoff + i]);
-                gf[i] = to_f32(dO[qoff + i]);
-            }
-            __syncthreads();
-            for (int j = wave; j < h; j += kThreads / 64) {
-                float z[2], dp[2];
+            twt[tid] = w[sel + slot];
+            tds[tid] = ds[sel + slot];
+        }
+        __syncthreads();
+        for (int j = wave; j < nrows; j += kThreads / 64) {
+            const float wt = twt[j / h];
+            float z[2], dp[2];
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int s = lane + 64 * u;
-                    float a = 0.f, bb = 0.f;
-                    if (s < CS) {
-                        // four partial sums each, so the products do not wait on one another
-                        float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
-                        for (int e = 0; e < D; e += 4) {
+            for (int u = 0; u < 2; ++u) {
+                const int s = lane + 64 * u;
+                float a = 0.f, bb = 0.f;
+                if (s < CS) {
+                    // four partial sums each, so the products do not wait on one another
+                    float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
+                    for (int e = 0; e < D; e += 4) {
 #pragma unroll
-                            for (int q = 0; q < 4; ++q) {
-                                a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
-                                b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
-                            }
+                        for (int q = 0; q < 4; ++q) {
+                            a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
+                            b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
                         }
-                        a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
-                        bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
-                        z[u] = dm.beta * a;
-                    } else {
-                        z[u] = -INFINITY;
                     }
-                    dp[u] = bb;
+                    a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                    bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
+                    z[u] = dm.beta * a;
+                } else {
+                    z[u] = -INFINITY;
                 }
-                float m = wave_max(fmaxf(z[0], z[1]));
-                if (dm.off1) m = fmaxf(m, 0.f);
-                float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
-                const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
-                p0 *= inv;
-                p1 *= inv;
-                const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
-                if (lane < CS) {
-                    pw[j * CS + lane] = wt * p0;
-                    dz[j * CS + lane] = wt * p0 * (dp[0] - Dj);
-                }
-                if (lane + 64 < CS) {
-                    pw[j * CS + lane + 64] = wt * p1;
-                    dz[j * CS + lane + 64] = wt * p1 * (dp[1] - Dj);
-                }
+                dp[u] = bb;
             }
-            if (tid < D) {
+            float m = wave_max(fmaxf(z[0], z[1]));
+            if (dm.off1) m = fmaxf(m, 0.f);
+            float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
+            const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
+            p0 *= inv;
+            p1 *= inv;
+            const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
+            if (lane < CS) {
+                pw[j * CS + lane] = wt * p0;
+                dz[j * CS + lane] = wt * p0 * (dp[0] - Dj);
+            }
+            if (lane + 64 < CS) {
+                pw[j * CS + lane + 64] = wt * p1;
+                dz[j * CS + lane + 64] = wt * p1 * (dp[1] - Dj);
+            }
+        }
+        if (tid < D) {
+            for (int tk = 0; tk < n; ++tk) {
                 float qs = 0.f;
-                for (int j = 0; j < h; ++j) qs += qf[j * D + tid];
-                dkbar = fmaf(dm.alpha * dst, qs, dkbar);
+                for (int j = 0; j < h; ++j) qs += qf[(tk * h + j) * D + tid];
+                dkbar = fmaf(dm.alpha * tds[tk], qs, dkbar);
             }
-            __syncthreads();
-            // a thread's elements share their column when kThreads is a multiple of D: the
-            // token's q and dO values of that column are read once per head
-            if constexpr (kThreads % D == 0) {
-                const int e = tid % D;
-                float av[NE], ak[NE];
+        }
+        __syncthreads();
+        // a thread's elements share their column when kThreads is a multiple of D: the
+        // batch's q and dO values of that column are read once per row
+        if constexpr (kThreads % D == 0) {
+            const int e = tid % D;
+            float av[NE], ak[NE];
 #pragma unroll
-                for (int r = 0; r < NE; ++r) av[r] = ak[r] = 0.f;
-                for (int j = 0; j < h; ++j) {
-                    const float gv = gf[j * D + e], qv = qf[j * D + e];
-#pragma unroll
-                    for (int r = 0; r < NE; ++r) {
-                        const int s = (tid + r * kThreads) / D;
-                        av[r] = fmaf(pw[j * CS + s], gv, av[r]);
-                        ak[r] = fmaf(dz[j * CS + s], qv, ak[r]);
-                    }
-                }
+            for (int r = 0; r < NE; ++r) av[r] = ak[r] = 0.f;
+            for (int j = 0; j < nrows; ++j) {
+                const float gv = gf[j * D + e], qv = qf[j * D + e];
 #pragma unroll
                 for (int r = 0; r < NE; ++r) {
-                    aV[r] += av[r];
-                    aK[r] = fmaf(dm.beta, ak[r], aK[r]);
+                    const int s = (tid + r * kThreads) / D;
+                    av[r] = fmaf(pw[j * CS + s], gv, av[r]);
+                    ak[r] = fmaf(dz[j * CS + s], qv, ak[r]);
                 }
-            } else {
+            }
 #pragma unroll
-                for (int r = 0; r < NE; ++r) {
-                    const int i = tid + r * kThreads;
-                    const int s = i / D, e = i % D;
-                    float av = 0.f, ak = 0.f;
-                    for (int j = 0; j < h; ++j) {
-                        av = fmaf(pw[j * CS + s], gf[j * D + e], av);
-                        ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
-                    }
-                    aV[r] += av;
-                    aK[r] = fmaf(dm.beta, ak, aK[r]);
+            for (int r = 0; r < NE; ++r) {
+                aV[r] += av[r];
+                aK[r] = fmaf(dm.beta, ak[r], aK[r]);
+            }
+        } else {
+#pragma unroll
+            for (int r = 0; r < NE; ++r) {
+                const int i = tid + r * kThreads;
+                const int s = i / D, e = i % D;
+                float av = 0.f, ak = 0.f;
+                for (int j = 0; j < nrows; ++j) {
+                    av = fmaf(pw[j * CS + s], gf[j * D + e], av);
+                    ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
+                }
+                aV[r] += av;
+                aK[r] = fmaf(dm.beta, ak, aK[r]);
+            }
+        }
+    };
+
+    const uint32_t* row = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
+    int ord = 0;                         // the token's place in the chunk's token list
+    int nb = 0;                          // tokens of the current batch
+    // the bitmap row is read kThreads words at a time into LDS (one load per thread), so
+    // the walk over the words waits for no memory access of its own
+    for (int wb = ((c + 1) * CS) >> 5; wb < nwords; wb += kThreads) {
+        __syncthreads();                 // the previous batch of words is read
+        if (wb + tid < nwords) wlist[tid] = row[wb + tid];
+        __syncthreads();
+        const int wend = min(nwords, wb + kThreads);
+        for (int wi = wb; wi < wend; ++wi) {
+            uint32_t word = wlist[wi - wb];
+            while (word) {
+                const int t = wi * 32 + (__ffs(word) - 1);
+                word &= word - 1;
+                if (ord++ % nsplit != z) continue;
+                // the list is read by the batch only after its first barrier
+                if (tid == 0) tlist[nb] = t;
+                if (++nb == TB) {
+                    batch(nb);
+                    nb = 0;
                 }
             }
         }
     }
+    if (nb > 0) batch(nb);
     __syncthreads();
     if (tid < D) dkb[tid] = dkbar;
     __syncthreads();
@@ -429,8 +462,9 @@ __global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nspli
 
 // Splits of the generic key pass: enough workgroups to fill the chip when the chunks are
 // few (each chunk's tokens are otherwise walked by one workgroup, one after another), at
-// most 32 (tiny fp32 workload: 32 splits 135 us with the finish, 16 splits 176, 64 splits
-// 185, the finish then summing too many partials).
+// most 32 (tiny fp32 workload, key pass and finish: 32 splits 118 us, 24 splits 132, 16
+// splits 150, 48 splits 170, 64 splits 181: past two workgroups per CU the splits run in
+// two rounds and the finish sums more partials).
 inline int kv_splits(const Dims& dm) {
     const long rows = (long)dm.B * dm.G * dm.Call;
     long n = rows > 0 ? (1024 + rows - 1) / rows : 1;
