@@ -447,12 +447,25 @@ __global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nspli
                                                               T* __restrict__ dV) {
     const int c = blockIdx.x, bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
     const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;
+    const size_t zstride = (size_t)dm.B * dm.G * dm.C * (2 * CS * D);
+    const float* p0 = part + ((size_t)bg * dm.C + c) * (2 * CS * D);
     for (int i = blockIdx.z * kThreads + threadIdx.x; i < CS * D; i += gridDim.z * kThreads) {
         float sk = 0.f, sv = 0.f;
-        for (int z = 0; z < nsplit; ++z) {
-            const float* pk = part + (((size_t)z * dm.B * dm.G + bg) * dm.C + c) * (2 * CS * D);
-            sk += pk[i];
-            sv += pk[CS * D + i];
+        // the loads of 8 splits in flight together, the sums still in split order
+        for (int z0 = 0; z0 < nsplit; z0 += 8) {
+            float vk[8], vv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float* pk = p0 + (size_t)min(z0 + j, nsplit - 1) * zstride;
+                vk[j] = pk[i];
+                vv[j] = pk[CS * D + i];
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (z0 + j < nsplit) {
+                    sk += vk[j];
+                    sv += vv[j];
+                }
         }
         const size_t gi = (rowbase + (size_t)(i / D) * dm.G) * D + i % D;
         dK[gi] = from_f32<T>(sk);
@@ -462,7 +475,7 @@ __global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nspli
 
 // Splits of the generic key pass: enough workgroups to fill the chip when the chunks are
 // few (each chunk's tokens are otherwise walked by one workgroup, one after another), at
-// most 32 (tiny fp32 workload, key pass and finish: 32 splits 118 us, 24 splits 132, 16
+// most 32 (tiny fp32 workload, key pass and finish: 32 splits 109 us, 24 splits 132, 16
 // splits 150, 48 splits 170, 64 splits 181: past two workgroups per CU the splits run in
 // two rounds and the finish sums more partials).
 inline int kv_splits(const Dims& dm) {
@@ -485,8 +498,9 @@ void launch_kv(const Dims& dm, const void* Q, const void* K, const void* V, cons
     }
     if (nsplit > 1 && dm.C > 0) {
         HSA_TIMED("bwd_kv_finish", st);
-        hipLaunchKernelGGL((kv_generic_finish<T, D, CS>), dim3(dm.C, dm.B * dm.G, 8), dim3(kThreads),
-                           0, st, dm, nsplit, (const float*)part, (T*)dK, (T*)dV);
+        hipLaunchKernelGGL((kv_generic_finish<T, D, CS>), dim3(dm.C, dm.B * dm.G, 16),
+                           dim3(kThreads), 0, st, dm, nsplit, (const float*)part, (T*)dK,
+                           (T*)dV);
     }
 }
 
