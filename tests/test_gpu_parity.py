@@ -157,9 +157,13 @@ def test_end_to_end_pipeline(hsa_gpu, name):
         assert_close(n, shape, t, ref[n])
 
 
-def test_backward_is_bitwise_deterministic(hsa_gpu):
-    shape, inp, ref, dev = case("L4K_like_bf16")
-    banner("L4K_like_bf16", "backward determinism")
+@pytest.mark.parametrize("name", ["L4K_like_bf16", "wide_like_bf16", "tiny_f32", "C1062_S16_f32"])
+def test_backward_is_bitwise_deterministic(hsa_gpu, name):
+    """Two calls give the same bits: the fused pass (L4K_like), the two-pass backward with
+    its key pass split over workgroups (wide_like, S = 128) and the generic kernels with
+    their per-split partials (tiny, and more than 1024 chunks)."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "backward determinism")
     Kbar = hsa_gpu.hsa_landmarks(dev["K"], shape.S)
     idx, w = hsa_gpu.hsa_select_topk(dev["Q"], Kbar, shape.G, shape.S, shape.k)
     r1 = hsa_gpu.hsa_backward(dev["Q"], dev["K"], dev["V"], Kbar, idx, w, dev["dO"], shape.S)
