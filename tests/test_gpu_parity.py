@@ -173,6 +173,21 @@ def test_backward_is_bitwise_deterministic(hsa_gpu, name):
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("name", ["L4K_like_bf16", "C1040_bf16", "tiny_f32"])
+def test_forward_is_bitwise_deterministic(hsa_gpu, name):
+    """Two calls give the same bits: the tile-major forward (L4K_like), the chunk-major one
+    with its per-(token, slot) partials summed in slot order (more than 256 chunks) and the
+    generic kernel."""
+    shape, inp, ref, dev = case(name)
+    banner(name, "forward determinism")
+    idx = torch.from_numpy(ref["idx"]).cuda()
+    w = torch.from_numpy(ref["w"].astype(np.float32)).cuda()
+    o1 = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    o2 = hsa_gpu.hsa_forward(dev["Q"], dev["K"], dev["V"], idx, w, shape.S)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2)
+
+
 def test_outputs_fully_overwritten(hsa_gpu):
     shape, inp, ref, dev = case("ragged_bf16")
     banner("ragged_bf16", "overwrite semantics")
