@@ -198,3 +198,14 @@ def test_decode_noalloc_checks(lib):
     # the 1M-token decode workload fits
     p1 = B.make_params(8, 1 << 20, 16, 2, 128, 64, 8, 1)
     assert lib.hsa_attn_workspace_size(ctypes.byref(p1), B.HSA_OP_DECODE) <= (8 << 20)
+
+
+def test_no_cpu_fallback():
+    """The product path has no CPU route: a missing library raises, and CPU tensors are
+    refused before any call into the library."""
+    import torch
+    with pytest.raises(RuntimeError, match="not built"):
+        binding.load(os.path.join(ROOT, "no_such_library.so"))
+    K = torch.zeros((1, 128, 2, 128), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU tensor"):
+        hsa.hsa_landmarks(K, 64)
