@@ -18,6 +18,7 @@
 #include <type_traits>
 
 #include "common.h"
+#include "chunk_stream.h"
 
 namespace hsa {
 
@@ -39,8 +40,11 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int HMAX = 16;
 constexpr int KMAX = 32;
+// the generic key pass: workgroups of the even split of (chunk, 4-token group) work, and the
+// tokens of a chunk listed at once
+constexpr int kGenWGs = 512;
+constexpr int kGenList = 256;
 
-__host__ __device__ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 template <typename T, int D, int CS>
 __global__ __launch_bounds__(kThreads) void bwd_q_generic(
@@ -239,6 +243,7 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     Dims dm, const T* __restrict__ Q, const T* __restrict__ K, const T* __restrict__ V,
     const int32_t* __restrict__ idx, const float* __restrict__ w, const T* __restrict__ dO,
     const float* __restrict__ ds, const uint32_t* __restrict__ bm, int nwords,
+    const int* __restrict__ gstart, const int* __restrict__ cntr, const int* __restrict__ plan,
     T* __restrict__ dK, T* __restrict__ dV, float* __restrict__ part) {
     constexpr int KP = D + (sizeof(T) == 4 ? 1 : 2);
     constexpr int NE = CS * D / kThreads;
@@ -249,220 +254,219 @@ __global__ __launch_bounds__(kThreads) void bwd_kv_generic(
     __shared__ float pw[HMAX * CS];
     __shared__ float dz[HMAX * CS];
     __shared__ float dkb[D];
-    __shared__ uint32_t wlist[kThreads];
-    __shared__ int tlist[HMAX];          // the tokens of a batch
-    __shared__ float twt[HMAX], tds[HMAX];   // their weights and ds for this chunk
+    __shared__ int tlist[kGenList];          // a run of the chunk's tokens
+    __shared__ int wtot[kThreads / 64];
+    __shared__ float twt[HMAX], tds[HMAX];   // a batch's weights and ds for this chunk
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int c = blockIdx.x;
-    const int bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
     const int h = dm.h, k = dm.k;
-    const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;   // row cS
+    const int R = dm.B * dm.G * dm.C;
+    const int lid = blockIdx.x;
+    const int total = plan[0], Tg = plan[1];
+    const int g0 = lid * Tg, g1 = min(g0 + Tg, total);
+    if (g0 >= g1) return;
+    const float invS = 1.f / (float)CS;
 
-    // split z of nsplit takes the chunk's tokens z, z + nsplit, ... (in increasing order) and,
-    // with more than one split, writes fp32 partials that kv_generic_finish adds in split order
-    const int z = blockIdx.z, nsplit = gridDim.z;
-    if (c >= dm.C) {   // trailing partial chunk: never selected, zero gradient
-        if (z != 0) return;
-        const int rows = dm.L - c * CS;
-        for (int i = tid; i < rows * D; i += kThreads) {
+    // the rows (b, g, chunk) that this workgroup's range of 4-token groups touches
+    for (int r = find_row(gstart, R, g0); r < R; ++r) {
+        const int rs = gstart[r], re = gstart[r + 1];
+        if (rs >= g1) break;
+        if (re == rs) continue;
+        const Segment sg = segment_of(rs, re, g0, g1);
+        const int c = r % dm.C;
+        const int bg = r / dm.C, b = bg / dm.G, g = bg % dm.G;
+        const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;   // row cS
+
+        __syncthreads();                     // the previous row's tiles and sums are read
+        for (int i = tid; i < CS * D; i += kThreads) {
+            const int s = i / D, e = i % D;
+            const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
+            Ks[s * KP + e] = K[gi];
+            Vs[s * KP + e] = V[gi];
+        }
+        float aK[NE], aV[NE];
+#pragma unroll
+        for (int r2 = 0; r2 < NE; ++r2) aK[r2] = aV[r2] = 0.f;
+        float dkbar = 0.f;   // thread tid < D owns element tid of dKbar
+
+        // Tokens are taken TB = floor(HMAX / h) at a time: the batch's (token, head) rows fill
+        // the HMAX-row LDS arrays, so a batch costs the barriers and memory round trips of one
+        // token.
+        const int TB = HMAX / h;
+        auto batch = [&](const int* tl, int n) __attribute__((always_inline)) {
+            const int nrows = n * h;
+            __syncthreads();                  // the previous batch's rows are read
+            for (int i = tid; i < nrows * D; i += kThreads) {
+                const int tk = i / (h * D), r = i - tk * (h * D);
+                const size_t qoff = (((size_t)b * dm.L + tl[tk]) * dm.H + (size_t)g * h) * D;
+                qf[i] = to_f32(Q[qoff + r]);
+                gf[i] = to_f32(dO[qoff + r]);
+            }
+            if (tid < n) {                    // the token's slot holding c: its w and ds
+                const size_t sel = (((size_t)b * dm.L + tl[tid]) * dm.G + g) * k;
+                int slot = 0;
+                for (int i = 0; i < k; ++i)
+                    if (idx[sel + i] == c) slot = i;
+                twt[tid] = w[sel + slot];
+                tds[tid] = ds[sel + slot];
+            }
+            __syncthreads();
+            for (int j = wave; j < nrows; j += kThreads / 64) {
+                const float wt = twt[j / h];
+                float z[2], dp[2];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    const int s = lane + 64 * u;
+                    float a = 0.f, bb = 0.f;
+                    if (s < CS) {
+                        // four partial sums each, so the products do not wait on one another
+                        float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
+                        #pragma unroll 4
+                        for (int e = 0; e < D; e += 4) {
+#pragma unroll
+                            for (int q = 0; q < 4; ++q) {
+                                a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
+                                b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
+                            }
+                        }
+                        a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                        bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
+                        z[u] = dm.beta * a;
+                    } else {
+                        z[u] = -INFINITY;
+                    }
+                    dp[u] = bb;
+                }
+                float m = wave_max(fmaxf(z[0], z[1]));
+                if (dm.off1) m = fmaxf(m, 0.f);
+                float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
+                const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
+                p0 *= inv;
+                p1 *= inv;
+                const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
+                // dZ carries beta, so the sums below go straight into the chunk's accumulators
+                const float bwt = dm.beta * wt;
+                if (lane < CS) {
+                    pw[j * CS + lane] = wt * p0;
+                    dz[j * CS + lane] = bwt * p0 * (dp[0] - Dj);
+                }
+                if (lane + 64 < CS) {
+                    pw[j * CS + lane + 64] = wt * p1;
+                    dz[j * CS + lane + 64] = bwt * p1 * (dp[1] - Dj);
+                }
+            }
+            if (tid < D) {
+                for (int tk = 0; tk < n; ++tk) {
+                    float qs = 0.f;
+                    for (int j = 0; j < h; ++j) qs += qf[(tk * h + j) * D + tid];
+                    dkbar = fmaf(dm.alpha * tds[tk], qs, dkbar);
+                }
+            }
+            __syncthreads();
+            // a thread's elements share their column when kThreads is a multiple of D: the
+            // batch's q and dO values of that column are read once per row
+            if constexpr (kThreads % D == 0) {
+                const int e = tid % D;
+                for (int j = 0; j < nrows; ++j) {
+                    const float gv = gf[j * D + e], qv = qf[j * D + e];
+#pragma unroll
+                    for (int r = 0; r < NE; ++r) {
+                        const int s = (tid + r * kThreads) / D;
+                        aV[r] = fmaf(pw[j * CS + s], gv, aV[r]);
+                        aK[r] = fmaf(dz[j * CS + s], qv, aK[r]);
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int r = 0; r < NE; ++r) {
+                    const int i = tid + r * kThreads;
+                    const int s = i / D, e = i % D;
+                    for (int j = 0; j < nrows; ++j) {
+                        aV[r] = fmaf(pw[j * CS + s], gf[j * D + e], aV[r]);
+                        aK[r] = fmaf(dz[j * CS + s], qf[j * D + e], aK[r]);
+                    }
+                }
+            }
+        };
+
+        // the segment's tokens [4 j0, min(4 j1, count)) of the chunk's ascending token list, a
+        // run of kGenList at a time, in batches of TB
+        const uint32_t* bmrow = bm + (size_t)r * nwords;
+        const int p0 = 4 * sg.j0, p1 = min(4 * sg.j1, cntr[r]);
+        for (int q0 = p0; q0 < p1; q0 += kGenList) {
+            const int q1 = min(q0 + kGenList, p1);
+            __syncthreads();                 // the previous run's list is read
+            collect_tokens<kThreads>(bmrow, ((c + 1) * CS) >> 5, nwords, q0, q1, tlist, wtot, tid);
+            __syncthreads();
+            for (int i0 = 0; i0 < q1 - q0; i0 += TB) batch(tlist + i0, min(TB, q1 - q0 - i0));
+        }
+        __syncthreads();
+        if (tid < D) dkb[tid] = dkbar;
+        __syncthreads();
+        // a row covered whole is final; a shared one leaves fp32 partials in the workgroup's
+        // slot (first row of its range 0, last 1), added in workgroup order by kv_generic_finish
+        float* pk = part + ((size_t)lid * 2 + sg.pslot) * (2 * CS * D);
+#pragma unroll
+        for (int r2 = 0; r2 < NE; ++r2) {
+            const int i = tid + r2 * kThreads;
+            const int s = i / D, e = i % D;
+            if (sg.whole) {
+                const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
+                dK[gi] = from_f32<T>(aK[r2] + dkb[e] * invS);
+                dV[gi] = from_f32<T>(aV[r2]);
+            } else {
+                pk[i] = aK[r2] + dkb[e] * invS;
+                pk[CS * D + i] = aV[r2];
+            }
+        }
+    }
+}
+
+// dK, dV of every chunk row the key pass did not write: zeros for a trailing partial chunk or
+// one no token selected, and for a chunk shared by several workgroups the sum of their
+// partials in workgroup order (a chunk selected by most tokens is shared by a hundred and
+// more: its elements are spread over gridDim.y workgroups, and the loads of 16 partials are
+// in flight together)
+template <typename T, int D, int CS>
+__global__ __launch_bounds__(kThreads) void kv_generic_finish(
+    Dims dm, const int* __restrict__ gstart, const int* __restrict__ cntr,
+    const int* __restrict__ plan, const float* __restrict__ part, T* __restrict__ dK,
+    T* __restrict__ dV) {
+    const int c = blockIdx.x % dm.Call;
+    const int bg = blockIdx.x / dm.Call, b = bg / dm.G, g = bg % dm.G;
+    const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;
+    const int r = bg * dm.C + c;
+    const int i0 = blockIdx.y * kThreads + threadIdx.x, istep = gridDim.y * kThreads;
+    if (c >= dm.C || cntr[r] == 0) {
+        const int rows = min(CS, dm.L - c * CS);
+        for (int i = i0; i < rows * D; i += istep) {
             const size_t gi = (rowbase + (size_t)(i / D) * dm.G) * D + i % D;
             dK[gi] = from_f32<T>(0.f);
             dV[gi] = from_f32<T>(0.f);
         }
         return;
     }
-    for (int i = tid; i < CS * D; i += kThreads) {
-        const int s = i / D, e = i % D;
-        const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
-        Ks[s * KP + e] = K[gi];
-        Vs[s * KP + e] = V[gi];
-    }
-    float aK[NE], aV[NE];
-#pragma unroll
-    for (int r = 0; r < NE; ++r) aK[r] = aV[r] = 0.f;
-    float dkbar = 0.f;   // thread tid < D owns element tid of dKbar
-
-    // Tokens are taken TB = floor(HMAX / h) at a time: the batch's (token, head) rows fill
-    // the HMAX-row LDS arrays, so a batch costs the barriers and memory round trips of one
-    // token.
-    const int TB = HMAX / h;
-    auto batch = [&](int n) __attribute__((always_inline)) {
-        const int nrows = n * h;
-        __syncthreads();                  // the previous batch's rows are read
-        for (int i = tid; i < nrows * D; i += kThreads) {
-            const int tk = i / (h * D), r = i - tk * (h * D);
-            const size_t qoff = (((size_t)b * dm.L + tlist[tk]) * dm.H + (size_t)g * h) * D;
-            qf[i] = to_f32(Q[qoff + r]);
-            gf[i] = to_f32(dO[qoff + r]);
-        }
-        if (tid < n) {                    // the token's slot holding c: its w and ds
-            const size_t sel = (((size_t)b * dm.L + tlist[tid]) * dm.G + g) * k;
-            int slot = 0;
-            for (int i = 0; i < k; ++i)
-                if (idx[sel + i] == c) slot = i;
-            twt[tid] = w[sel + slot];
-            tds[tid] = ds[sel + slot];
-        }
-        __syncthreads();
-        for (int j = wave; j < nrows; j += kThreads / 64) {
-            const float wt = twt[j / h];
-            float z[2], dp[2];
-#pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int s = lane + 64 * u;
-                float a = 0.f, bb = 0.f;
-                if (s < CS) {
-                    // four partial sums each, so the products do not wait on one another
-                    float a4[4] = {0.f, 0.f, 0.f, 0.f}, b4[4] = {0.f, 0.f, 0.f, 0.f};
-                    for (int e = 0; e < D; e += 4) {
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) {
-                            a4[q] = fmaf(qf[j * D + e + q], to_f32(Ks[s * KP + e + q]), a4[q]);
-                            b4[q] = fmaf(gf[j * D + e + q], to_f32(Vs[s * KP + e + q]), b4[q]);
-                        }
-                    }
-                    a = (a4[0] + a4[1]) + (a4[2] + a4[3]);
-                    bb = (b4[0] + b4[1]) + (b4[2] + b4[3]);
-                    z[u] = dm.beta * a;
-                } else {
-                    z[u] = -INFINITY;
-                }
-                dp[u] = bb;
-            }
-            float m = wave_max(fmaxf(z[0], z[1]));
-            if (dm.off1) m = fmaxf(m, 0.f);
-            float p0 = expf(z[0] - m), p1 = expf(z[1] - m);
-            const float inv = 1.f / (wave_sum(p0 + p1) + (dm.off1 ? expf(-m) : 0.f));
-            p0 *= inv;
-            p1 *= inv;
-            const float Dj = wave_sum(p0 * dp[0] + p1 * dp[1]);
-            if (lane < CS) {
-                pw[j * CS + lane] = wt * p0;
-                dz[j * CS + lane] = wt * p0 * (dp[0] - Dj);
-            }
-            if (lane + 64 < CS) {
-                pw[j * CS + lane + 64] = wt * p1;
-                dz[j * CS + lane + 64] = wt * p1 * (dp[1] - Dj);
-            }
-        }
-        if (tid < D) {
-            for (int tk = 0; tk < n; ++tk) {
-                float qs = 0.f;
-                for (int j = 0; j < h; ++j) qs += qf[(tk * h + j) * D + tid];
-                dkbar = fmaf(dm.alpha * tds[tk], qs, dkbar);
-            }
-        }
-        __syncthreads();
-        // a thread's elements share their column when kThreads is a multiple of D: the
-        // batch's q and dO values of that column are read once per row
-        if constexpr (kThreads % D == 0) {
-            const int e = tid % D;
-            float av[NE], ak[NE];
-#pragma unroll
-            for (int r = 0; r < NE; ++r) av[r] = ak[r] = 0.f;
-            for (int j = 0; j < nrows; ++j) {
-                const float gv = gf[j * D + e], qv = qf[j * D + e];
-#pragma unroll
-                for (int r = 0; r < NE; ++r) {
-                    const int s = (tid + r * kThreads) / D;
-                    av[r] = fmaf(pw[j * CS + s], gv, av[r]);
-                    ak[r] = fmaf(dz[j * CS + s], qv, ak[r]);
-                }
-            }
-#pragma unroll
-            for (int r = 0; r < NE; ++r) {
-                aV[r] += av[r];
-                aK[r] = fmaf(dm.beta, ak[r], aK[r]);
-            }
-        } else {
-#pragma unroll
-            for (int r = 0; r < NE; ++r) {
-                const int i = tid + r * kThreads;
-                const int s = i / D, e = i % D;
-                float av = 0.f, ak = 0.f;
-                for (int j = 0; j < nrows; ++j) {
-                    av = fmaf(pw[j * CS + s], gf[j * D + e], av);
-                    ak = fmaf(dz[j * CS + s], qf[j * D + e], ak);
-                }
-                aV[r] += av;
-                aK[r] = fmaf(dm.beta, ak, aK[r]);
-            }
-        }
-    };
-
-    const uint32_t* row = bm + (((size_t)b * dm.G + g) * dm.C + c) * nwords;
-    int ord = 0;                         // the token's place in the chunk's token list
-    int nb = 0;                          // tokens of the current batch
-    // the bitmap row is read kThreads words at a time into LDS (one load per thread), so
-    // the walk over the words waits for no memory access of its own
-    for (int wb = ((c + 1) * CS) >> 5; wb < nwords; wb += kThreads) {
-        __syncthreads();                 // the previous batch of words is read
-        if (wb + tid < nwords) wlist[tid] = row[wb + tid];
-        __syncthreads();
-        const int wend = min(nwords, wb + kThreads);
-        for (int wi = wb; wi < wend; ++wi) {
-            uint32_t word = wlist[wi - wb];
-            while (word) {
-                const int t = wi * 32 + (__ffs(word) - 1);
-                word &= word - 1;
-                if (ord++ % nsplit != z) continue;
-                // the list is read by the batch only after its first barrier
-                if (tid == 0) tlist[nb] = t;
-                if (++nb == TB) {
-                    batch(nb);
-                    nb = 0;
-                }
-            }
-        }
-    }
-    if (nb > 0) batch(nb);
-    __syncthreads();
-    if (tid < D) dkb[tid] = dkbar;
-    __syncthreads();
-    const float invS = 1.f / (float)CS;
-    float* pk = nsplit > 1 ? part + (((size_t)z * dm.B * dm.G + bg) * dm.C + c) * (2 * CS * D)
-                           : nullptr;
-#pragma unroll
-    for (int r = 0; r < NE; ++r) {
-        const int i = tid + r * kThreads;
-        const int s = i / D, e = i % D;
-        if (nsplit > 1) {
-            pk[i] = aK[r] + dkb[e] * invS;
-            pk[CS * D + i] = aV[r];
-        } else {
-            const size_t gi = (rowbase + (size_t)s * dm.G) * D + e;
-            dK[gi] = from_f32<T>(aK[r] + dkb[e] * invS);
-            dV[gi] = from_f32<T>(aV[r]);
-        }
-    }
-}
-
-// dK, dV of a complete chunk from the key pass's per-split partials, added in split order
-// (the chunk's elements spread over gridDim.z workgroups)
-template <typename T, int D, int CS>
-__global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nsplit,
-                                                              const float* __restrict__ part,
-                                                              T* __restrict__ dK,
-                                                              T* __restrict__ dV) {
-    const int c = blockIdx.x, bg = blockIdx.y, b = bg / dm.G, g = bg % dm.G;
-    const size_t rowbase = ((size_t)b * dm.L + (size_t)c * CS) * dm.G + g;
-    const size_t zstride = (size_t)dm.B * dm.G * dm.C * (2 * CS * D);
-    const float* p0 = part + ((size_t)bg * dm.C + c) * (2 * CS * D);
-    for (int i = blockIdx.z * kThreads + threadIdx.x; i < CS * D; i += gridDim.z * kThreads) {
+    const int Tg = plan[1];
+    const int rs = gstart[r], re = gstart[r + 1];
+    const int wf = rs / Tg, wl = (re - 1) / Tg;
+    if (wf == wl) return;                // written by its workgroup
+    for (int i = i0; i < CS * D; i += istep) {
         float sk = 0.f, sv = 0.f;
-        // the loads of 8 splits in flight together, the sums still in split order
-        for (int z0 = 0; z0 < nsplit; z0 += 8) {
-            float vk[8], vv[8];
+        for (int w0 = wf; w0 <= wl; w0 += 16) {
+            float vk[16], vv[16];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float* pk = p0 + (size_t)min(z0 + j, nsplit - 1) * zstride;
+            for (int j = 0; j < 16; ++j) {
+                const int wg = min(w0 + j, wl);
+                // the row is the first of each later workgroup's range, and of wf's when
+                // wf's range starts there
+                const int sl = (wg > wf || rs == wf * Tg) ? 0 : 1;
+                const float* pk = part + ((size_t)wg * 2 + sl) * (2 * CS * D);
                 vk[j] = pk[i];
                 vv[j] = pk[CS * D + i];
             }
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                if (z0 + j < nsplit) {
+            for (int j = 0; j < 16; ++j)
+                if (w0 + j <= wl) {
                     sk += vk[j];
                     sv += vv[j];
                 }
@@ -473,51 +477,62 @@ __global__ __launch_bounds__(kThreads) void kv_generic_finish(Dims dm, int nspli
     }
 }
 
-// Splits of the generic key pass: enough workgroups to fill the chip when the chunks are
-// few (each chunk's tokens are otherwise walked by one workgroup, one after another), at
-// most 32 (tiny fp32 workload, key pass and finish: 32 splits 109 us, 24 splits 132, 16
-// splits 150, 48 splits 170, 64 splits 181: past two workgroups per CU the splits run in
-// two rounds and the finish sums more partials).
-inline int kv_splits(const Dims& dm) {
-    const long rows = (long)dm.B * dm.G * dm.Call;
-    long n = rows > 0 ? (1024 + rows - 1) / rows : 1;
-    return (int)(n < 1 ? 1 : (n > 32 ? 32 : n));
-}
-
+// The generic key pass runs on the even split of (chunk, 4-token group) work over kGenWGs
+// workgroups (stream_rowcount, stream_plan), so a chunk selected by most tokens is shared
+// by several workgroups instead of setting the kernel time (tiny fp32 workload: key pass and
+// finish 110 -> 69 us with the plan, against 32 fixed splits per chunk).
 template <typename T, int D, int CS>
 void launch_kv(const Dims& dm, const void* Q, const void* K, const void* V, const int32_t* idx,
                const float* w, const void* dO, const float* ds, const uint32_t* bm, int nwords,
-               void* dK, void* dV, float* part, hipStream_t st) {
-    const int nsplit = kv_splits(dm);
-    dim3 grid(dm.Call, dm.B * dm.G, nsplit);
-    {
+               void* dK, void* dV, int* plan_ws, float* part, hipStream_t st) {
+    const int R = dm.B * dm.G * dm.C;
+    int* cnt = plan_ws;
+    int* gstart = cnt + R;
+    int* plan = gstart + R + 1;
+    if (R > 0) {
+        {
+            HSA_TIMED("bwd_plan", st);
+            hipLaunchKernelGGL(stream_rowcount, dim3(cdiv(R, 4)), dim3(256), 0, st, bm, R,
+                               nwords, dm.C, dm.S, cnt);
+            hipLaunchKernelGGL(stream_plan, dim3(1), dim3(1024), 0, st, (const int*)cnt, R,
+                               kGenWGs, gstart, plan);
+        }
         HSA_TIMED("bwd_kv_generic", st);
-        hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), grid, dim3(kThreads), 0, st, dm, (const T*)Q,
-                           (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm, nwords, (T*)dK,
-                           (T*)dV, part);
+        hipLaunchKernelGGL((bwd_kv_generic<T, D, CS>), dim3(kGenWGs), dim3(kThreads), 0, st, dm,
+                           (const T*)Q, (const T*)K, (const T*)V, idx, w, (const T*)dO, ds, bm,
+                           nwords, (const int*)gstart, (const int*)cnt, (const int*)plan,
+                           (T*)dK, (T*)dV, part);
     }
-    if (nsplit > 1 && dm.C > 0) {
-        HSA_TIMED("bwd_kv_finish", st);
-        hipLaunchKernelGGL((kv_generic_finish<T, D, CS>), dim3(dm.C, dm.B * dm.G, 16),
-                           dim3(kThreads), 0, st, dm, nsplit, (const float*)part, (T*)dK,
-                           (T*)dV);
-    }
+    HSA_TIMED("bwd_kv_finish", st);
+    hipLaunchKernelGGL((kv_generic_finish<T, D, CS>), dim3(dm.Call * dm.B * dm.G, 16),
+                       dim3(kThreads), 0, st, dm, (const int*)gstart, (const int*)cnt,
+                       (const int*)plan, (const float*)part, (T*)dK, (T*)dV);
 }
 
 template <typename T, int D>
 void launch_kv_s(const Dims& dm, const void* Q, const void* K, const void* V,
                  const int32_t* idx, const float* w, const void* dO, const float* ds,
-                 const uint32_t* bm, int nwords, void* dK, void* dV, float* part,
-                 hipStream_t st) {
+                 const uint32_t* bm, int nwords, void* dK, void* dV, int* plan_ws,
+                 float* part, hipStream_t st) {
     switch (dm.S) {
-        case 16: launch_kv<T, D, 16>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
-        case 32: launch_kv<T, D, 32>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
-        case 64: launch_kv<T, D, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st); break;
+        case 16:
+            launch_kv<T, D, 16>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws, part,
+                              st);
+            break;
+        case 32:
+            launch_kv<T, D, 32>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws, part,
+                              st);
+            break;
+        case 64:
+            launch_kv<T, D, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws, part,
+                              st);
+            break;
         default:
             // fp32 with S = 128 and d = 128 exceeds the LDS of one workgroup; rejected by the
             // argument checks, so it is not instantiated.
             if constexpr (!(sizeof(T) == 4 && D == 128))
-                launch_kv<T, D, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
+                launch_kv<T, D, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws,
+                                     part, st);
             break;
     }
 }
@@ -541,12 +556,14 @@ void launch_kv_pass(const Dims& dm, const void* Q, const void* K, const void* V,
     uint32_t* bm = (uint32_t*)((char*)ws + align256((size_t)dm.B * dm.L * dm.G * dm.k * 4));
     const size_t nbm = (size_t)dm.B * dm.G * dm.C * nwords;
     launch_bitmap(dm, idx, bm, st);
-    // the key pass's per-split partials follow the bitmap
-    float* part = (float*)((char*)bm + align256(nbm * 4));
+    // the split's row counts, group prefix and plan, then the per-workgroup partials
+    const size_t R = (size_t)dm.B * dm.G * dm.C;
+    int* plan_ws = (int*)((char*)bm + align256(nbm * 4));
+    float* part = (float*)((char*)plan_ws + align256((2 * R + 3) * 4));
     if (dm.d == 128)
-        launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
+        launch_kv_s<T, 128>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws, part, st);
     else
-        launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, part, st);
+        launch_kv_s<T, 64>(dm, Q, K, V, idx, w, dO, ds, bm, nwords, dK, dV, plan_ws, part, st);
 }
 
 template <typename T>
@@ -590,10 +607,10 @@ hipError_t launch_selection_bitmap(const Dims& dm, const int32_t* idx, uint32_t*
 
 size_t backward_generic_workspace(const Dims& dm) {
     const size_t nwords = (size_t)cdiv(dm.L, 32);
-    const int nsplit = kv_splits(dm);
-    const size_t part = nsplit > 1 ? (size_t)nsplit * dm.B * dm.G * dm.C * 2 * dm.S * dm.d * 4 : 0;
-    return align256((size_t)dm.B * dm.L * dm.G * dm.k * 4) +
-           align256((size_t)dm.B * dm.G * dm.C * nwords * 4) + align256(part);
+    const size_t R = (size_t)dm.B * dm.G * dm.C;
+    const size_t part = (size_t)kGenWGs * 2 * 2 * dm.S * dm.d * 4;
+    return align256((size_t)dm.B * dm.L * dm.G * dm.k * 4) + align256(R * nwords * 4) +
+           align256((2 * R + 3) * 4) + align256(part);
 }
 
 size_t backward_workspace(const Dims& dm) {

@@ -1,8 +1,8 @@
 // The even split of chunk-major work used by the fused forward and backward passes (bf16,
-// h = 8, d = 128, S = 64), and helpers they share.
+// h = 8, d = 128, S = 64) and by the generic key pass, and helpers they share.
 //
-// Work is counted in groups of 4 consecutive tokens of a chunk's selecting tokens (32 rows =
-// 4 tokens x 8 heads of a KV group).  A chunk's tokens come from the selection bitmap (bit t
+// Work is counted in groups of 4 consecutive tokens of a chunk's selecting tokens (in the
+// fused passes 32 rows = 4 tokens x 8 heads of a KV group).  A chunk's tokens come from the selection bitmap (bit t
 // of row (b, g, c) set when token t selected chunk c) in increasing order.  The groups of all
 // rows are laid end to end (slices, then chunks) and split into kStreamWGs equal ranges, one
 // per workgroup: stream_rowcount counts each row's tokens, stream_plan lays out the group
