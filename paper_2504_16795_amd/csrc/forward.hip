@@ -29,6 +29,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int HMAX = 16;
+constexpr int KMAX = 32;
 
 template <typename T, int D, int CS>
 __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __restrict__ Q,
@@ -43,6 +44,8 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
     __shared__ T Vs[CS * D];
     __shared__ float qf[HMAX * D];
     __shared__ float p[HMAX * CS];
+    __shared__ int sc[KMAX];
+    __shared__ float sw[KMAX];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int t = blockIdx.x;
@@ -50,23 +53,66 @@ __global__ __launch_bounds__(kThreads) void forward_generic(Dims dm, const T* __
     const int h = dm.h, S = dm.S, k = dm.k;
     const size_t qoff = (((size_t)b * dm.L + t) * dm.H + (size_t)g * h) * D;
 
+    // the token's slots (an empty or out-of-range one as -1), its query rows
+    const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
+    if (tid < k) {
+        const int c = idx[sel + tid];
+        sc[tid] = (c < 0 || c >= t / S) ? -1 : c;
+        sw[tid] = w[sel + tid];
+    }
     for (int i = tid; i < h * D; i += kThreads) qf[i] = to_f32(Q[qoff + i]);
     float acc[NACC];
 #pragma unroll
     for (int r = 0; r < NACC; ++r) acc[r] = 0.f;
+    __syncthreads();
 
-    const size_t sel = (((size_t)b * dm.L + t) * dm.G + g) * k;
-    for (int slot = 0; slot < k; ++slot) {
-        const int c = idx[sel + slot];
-        if (c < 0 || c >= t / S) continue;   // empty (or out-of-range) slot
-        const float wi = w[sel + slot];
-        __syncthreads();
-        for (int i = tid; i < S * D; i += kThreads) {
-            const int s = i / D, e = i % D;
+    // each slot's K / V rows are loaded into registers while the slot before is computed
+    // (for chunks of up to 4096 elements; larger ones would cost the workgroups per CU)
+    constexpr int NS = CS * D / kThreads;
+    constexpr bool PREF = CS * D <= 4096;
+    T kr[NS], vr[NS];
+    auto load_chunk = [&](int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int r = 0; r < NS; ++r) {
+            const int i = tid + r * kThreads, s = i / D, e = i % D;
             const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
-            Ks[s * KP + e] = K[gi];
-            Vs[s * D + e] = V[gi];
+            kr[r] = K[gi];
+            vr[r] = V[gi];
         }
+    };
+    auto next_slot = [&](int from) __attribute__((always_inline)) {
+        int s2 = from;
+        while (s2 < k && sc[s2] < 0) ++s2;
+        return s2;
+    };
+    int slot = next_slot(0);
+    if constexpr (PREF) {
+        if (slot < k) load_chunk(sc[slot]);
+    }
+    while (slot < k) {
+        const float wi = sw[slot];
+        __syncthreads();                  // the previous slot's tiles and weights are read
+        if constexpr (PREF) {
+#pragma unroll
+            for (int r = 0; r < NS; ++r) {
+                const int i = tid + r * kThreads, s = i / D, e = i % D;
+                Ks[s * KP + e] = kr[r];
+                Vs[s * D + e] = vr[r];
+            }
+        } else {
+            const int c = sc[slot];
+            for (int i = tid; i < S * D; i += kThreads) {
+                const int s = i / D, e = i % D;
+                const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+                Ks[s * KP + e] = K[gi];
+                Vs[s * D + e] = V[gi];
+            }
+        }
+        const int nslot = next_slot(slot + 1);
+        if constexpr (PREF) {
+            if (nslot < k) load_chunk(sc[nslot]);
+        }
+        slot = nslot;
         __syncthreads();
         for (int j = wave; j < h; j += kThreads / 64) {
             float z[2];
