@@ -60,6 +60,8 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
     __shared__ float dz[HMAX * CS];
     __shared__ float Dl[HMAX];
     __shared__ float dwl[KMAX];
+    __shared__ int sc[KMAX];
+    __shared__ float sw[KMAX];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int t = blockIdx.x;
@@ -74,20 +76,63 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
         gf[i] = to_f32(dO[qoff + i]);
     }
     if (tid < KMAX) dwl[tid] = 0.f;
+    // the token's slots (an empty or out-of-range one as -1)
+    if (tid < k) {
+        const int c = idx[sel + tid];
+        sc[tid] = (c < 0 || c >= ncand) ? -1 : c;
+        sw[tid] = w[sel + tid];
+    }
     float acc[NACC];
 #pragma unroll
     for (int r = 0; r < NACC; ++r) acc[r] = 0.f;
+    __syncthreads();
 
-    for (int slot = 0; slot < k; ++slot) {
-        const int c = idx[sel + slot];
-        if (c < 0 || c >= ncand) continue;
-        const float wi = w[sel + slot];
-        __syncthreads();
-        for (int i = tid; i < S * D; i += kThreads) {
-            const int s = i / D, e = i % D;
+    // each slot's K / V rows are loaded into registers while the slot before is computed
+    // (for chunks of up to 4096 elements; larger ones would cost the workgroups per CU)
+    constexpr int NS = CS * D / kThreads;
+    constexpr bool PREF = CS * D <= 4096;
+    T kr[PREF ? NS : 1], vr[PREF ? NS : 1];
+    auto load_chunk = [&](int c) __attribute__((always_inline)) {
+#pragma unroll
+        for (int r = 0; r < NS; ++r) {
+            const int i = tid + r * kThreads, s = i / D, e = i % D;
             const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
-            Ks[s * KP + e] = K[gi];
-            Vs[s * KP + e] = V[gi];
+            kr[r] = K[gi];
+            vr[r] = V[gi];
+        }
+    };
+    auto next_slot = [&](int from) __attribute__((always_inline)) {
+        int s2 = from;
+        while (s2 < k && sc[s2] < 0) ++s2;
+        return s2;
+    };
+    int slot = next_slot(0);
+    if constexpr (PREF) {
+        if (slot < k) load_chunk(sc[slot]);
+    }
+    while (slot < k) {
+        const int cur = slot;
+        const float wi = sw[cur];
+        __syncthreads();                  // the previous slot's tiles and sums are read
+        if constexpr (PREF) {
+#pragma unroll
+            for (int r = 0; r < NS; ++r) {
+                const int i = tid + r * kThreads, s = i / D, e = i % D;
+                Ks[s * KP + e] = kr[r];
+                Vs[s * KP + e] = vr[r];
+            }
+        } else {
+            const int c = sc[cur];
+            for (int i = tid; i < S * D; i += kThreads) {
+                const int s = i / D, e = i % D;
+                const size_t gi = (((size_t)b * dm.L + (size_t)c * S + s) * dm.G + g) * D + e;
+                Ks[s * KP + e] = K[gi];
+                Vs[s * KP + e] = V[gi];
+            }
+        }
+        slot = next_slot(cur + 1);
+        if constexpr (PREF) {
+            if (slot < k) load_chunk(sc[slot]);
         }
         __syncthreads();
         for (int j = wave; j < h; j += kThreads / 64) {
@@ -129,7 +174,7 @@ __global__ __launch_bounds__(kThreads) void bwd_q_generic(
         if (tid == 0) {
             float s = 0.f;
             for (int j = 0; j < h; ++j) s += Dl[j];
-            dwl[slot] = s;
+            dwl[cur] = s;
         }
 #pragma unroll
         for (int r = 0; r < NACC; ++r) {
